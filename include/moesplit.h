@@ -1,0 +1,271 @@
+/*
+ * moesplit.h -- C ABI of libmoesplit, the per-layer MoE forward over split
+ * experts for one AMD Instinct MI355X (gfx950).
+ *
+ * Method: arXiv 2509.08342 ("MoEpic").  Each expert's SwiGLU FFN is cut into
+ * a top and a bottom segment (Sec. 2.3, split ratio theta = share of the top
+ * segment).  Top segments of some experts are cached in a budgeted VRAM pool
+ * (Sec. 3.1, 3.4.1: per-layer budget V_i, cache size C_i = V_i / theta_i);
+ * bottom segments and uncached experts stay in host RAM and are copied into a
+ * VRAM buffer on demand or by speculative prefetch (Sec. 3.2).  After routing,
+ * resident segments are computed while missing ones are copied (Sec. 3.2,
+ * Eq. (5)-(6)).
+ *
+ * The cut runs along the FFN intermediate axis: the top segment holds units
+ * [0, F_top) of W_gate/W_up columns and W_down rows, the bottom [F_top, F).
+ * Each segment's contribution is a partial down-projection and the partials
+ * sum to the unsplit expert, so the layer output does not depend on r, on
+ * residency or on prediction.
+ *
+ * Conventions for every entry point:
+ *  - Return value: ms_status.  No exceptions cross the ABI.  On MS_E_INVALID,
+ *    MS_E_BUDGET, MS_E_STATE and MS_E_UNSUPPORTED the context state is
+ *    unchanged.  MS_E_HIP means a HIP runtime call failed; the context is then
+ *    poisoned and every later call except ms_last_error/ms_destroy returns
+ *    MS_E_HIP.  ms_last_error() gives a human-readable message.
+ *  - A context is used by one host thread at a time.
+ *  - Streams are passed as void* (a hipStream_t); NULL means the null stream.
+ *    The library creates two more streams of its own (default priority): a
+ *    copy stream for host-to-device segment transfers and a side stream for
+ *    computing streamed segments.
+ *  - "h_dev", "y_dev", ... are device pointers owned by the caller.
+ *    Host arrays passed to ms_set_* are copied before the call returns.
+ *  - Element type of weights and activations is the model's dtype (MS_F32 or
+ *    MS_BF16, bf16 passed as raw 16-bit patterns); accumulation is fp32.
+ */
+#ifndef MOESPLIT_H
+#define MOESPLIT_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  MS_OK = 0,
+  MS_E_INVALID = 1,     /* bad argument (pointer, index, size, range)        */
+  MS_E_BUDGET = 2,      /* device pool or top-segment cache too small         */
+  MS_E_STATE = 3,       /* call not valid in the current state                */
+  MS_E_HIP = 4,         /* HIP runtime error; context poisoned                */
+  MS_E_NOMEM = 5,       /* host allocation (pinned store) failed              */
+  MS_E_UNSUPPORTED = 6  /* shape outside what the kernels support             */
+} ms_status;
+
+typedef enum { MS_F32 = 0, MS_BF16 = 1 } ms_dtype;
+
+/* Model shape.  Sec. 2.1: L layers, N (= n_experts) experts per layer, K
+ * (= top_k) activated per token, hidden width d.  d_ff is each expert's
+ * intermediate width F.  n_shared always-active experts of width d_ff_shared
+ * (weight 1) extend the paper's module for models that have them; they are
+ * always VRAM-resident and count as non-expert parameters U_n (Sec. 3.4.1).
+ * renormalize = 1 divides the selected scores by their sum as in Eq. (2).
+ * max_tokens bounds T of every forward; n_buffer_slots is the number of
+ * full-expert slots of the VRAM staging buffer U_b (0 -> 2*top_k: one set for
+ * the running layer, one for the next layer's prefetch). */
+typedef struct {
+  int32_t n_layers;
+  int32_t d_model;
+  int32_t d_ff;
+  int32_t n_experts;
+  int32_t top_k;
+  int32_t n_shared;
+  int32_t d_ff_shared;
+  int32_t dtype;
+  int32_t renormalize;
+  int32_t max_tokens;
+  int32_t n_buffer_slots;
+} ms_model_desc;
+
+/* Sizes the library derives from a model shape (pure host arithmetic). */
+typedef struct {
+  uint64_t chunk_bytes;       /* bytes of one 64-unit chunk: 3 * 64 * d * elem */
+  int32_t n_chunks;           /* ceil(F / 64)                                  */
+  uint64_t expert_bytes;      /* n_chunks * chunk_bytes (U_e, zero-padded)     */
+  uint64_t fixed_pool_bytes;  /* device pool bytes needed besides top caches:
+                                 routers, shared experts, work buffers and the
+                                 staging buffer                                */
+  uint64_t buffer_bytes;      /* of which: staging buffer (U_b)                */
+} ms_sizes;
+
+/* Per-layer statistics (counts since the last ms_reset_stats). */
+typedef struct {
+  uint64_t forwards;
+  uint64_t tokens;
+  uint64_t selected;          /* (token, expert) selections                   */
+  uint64_t experts_active;    /* distinct experts summed over forwards         */
+  uint64_t alpha;             /* active experts fully in VRAM at routing time  */
+  uint64_t beta;              /* active experts with only the top cached       */
+  uint64_t gamma;             /* active experts with nothing in VRAM           */
+  uint64_t buffer_hits;       /* active experts whose missing part had already
+                                 been (at least partly) prefetched             */
+  uint64_t bytes_miss;        /* H2D bytes issued after routing                */
+  uint64_t bytes_prefetch;    /* H2D bytes issued by prefetch                  */
+  uint64_t bytes_prefetch_used;  /* prefetched bytes a forward then consumed  */
+  uint64_t bytes_prefetch_dropped; /* prefetch bytes dropped before issue     */
+  uint64_t predicted_hits;    /* selected experts among the top-K predicted    */
+  uint64_t predictions;       /* forwards that had a prediction to check       */
+} ms_layer_stats;
+
+/* Timeline record (see ms_timeline_begin). */
+typedef enum {
+  MS_IV_ROUTER = 0,        /* router + top-K (+ prediction) kernel              */
+  MS_IV_GROUP = 1,         /* token grouping kernel                              */
+  MS_IV_FFN_RESIDENT = 2,  /* SwiGLU over resident chunks (compute stream)       */
+  MS_IV_FFN_STREAMED = 3,  /* SwiGLU over streamed chunks (side stream)          */
+  MS_IV_COMBINE = 4,       /* weighted combine kernel                            */
+  MS_IV_COPY_MISS = 5,     /* H2D copy issued after routing                      */
+  MS_IV_COPY_PREFETCH = 6, /* H2D copy issued by prefetch                        */
+  MS_IV_COPY_TOP = 7,      /* H2D copy of a top segment (ms_load_top)            */
+  MS_IV_PREDICT = 8        /* prediction ranking kernel                          */
+} ms_interval_kind;
+
+typedef struct {
+  int32_t kind;       /* ms_interval_kind                                        */
+  int32_t layer;
+  double t0_ms;       /* start, ms since the timeline origin event               */
+  double t1_ms;       /* end                                                     */
+  uint64_t bytes;     /* kernels: weight bytes read (algorithmic);
+                         copies: bytes transferred                               */
+} ms_interval;
+
+typedef struct ms_ctx ms_ctx;
+
+/* ---- sizing (no GPU needed) ------------------------------------------------ */
+
+/* Derived sizes of a model shape.  MS_E_INVALID / MS_E_UNSUPPORTED if the
+ * shape is not accepted (d must be a multiple of 64 and at most 8192; see the
+ * DESIGN notes for the other limits). */
+ms_status ms_query_sizes(const ms_model_desc* desc, ms_sizes* out);
+
+/* The split point and cache size of Sec. 3.4 for one layer, without a
+ * context: F_top = 64 * floor(r * F / 64 + 1/2) clamped to [0, F] (whole
+ * chunks), top_bytes = chunks(F_top) * chunk_bytes, and C_i =
+ * floor(budget_bytes / top_bytes) capped at n_experts (0 if top_bytes = 0).
+ * r must lie in [0, 1]. */
+ms_status ms_split_plan(const ms_model_desc* desc, uint64_t budget_bytes, float r,
+                        int32_t* top_units_out, uint64_t* top_bytes_out,
+                        int32_t* top_slots_out);
+
+/* ---- context --------------------------------------------------------------- */
+
+/* Create a context on the current HIP device.  dev_pool/pool_bytes is a
+ * caller-owned device allocation that emulates the VRAM budget V of Eq. (8):
+ * every device byte the library uses (routers, shared experts, work buffers,
+ * the staging buffer U_b and the top-segment caches sum_i V_i) is carved from
+ * it.  pool_bytes must cover ms_sizes.fixed_pool_bytes (else MS_E_BUDGET).
+ * The pinned host expert store (hipHostMalloc) is allocated here:
+ * n_layers * n_experts * expert_bytes (MS_E_NOMEM on failure), unless
+ * host_store_experts > 0 limits it to that many distinct expert blobs, in
+ * which case experts must be provided with ms_alias_expert beyond that. */
+ms_status ms_create(const ms_model_desc* desc, void* dev_pool, uint64_t pool_bytes,
+                    int32_t host_store_experts, ms_ctx** out);
+void ms_destroy(ms_ctx* ctx);
+const char* ms_last_error(const ms_ctx* ctx);
+
+/* Router R^i of layer i (Sec. 2.1): w_r host [d][E] in the model dtype
+ * (logits = h . w_r); bias host [E] fp32 or NULL, added to the logits. */
+ms_status ms_set_router(ms_ctx* ctx, int32_t layer, const void* w_r, const float* bias);
+
+/* Expert e of layer i: host w_gate [d][F], w_up [d][F], w_down [F][d] in the
+ * model dtype, E(h) = (silu(h.w_gate) * (h.w_up)) . w_down.  Copied into the
+ * pinned host store in chunk-packed order: per 64-unit chunk, the 64 gate
+ * columns, the 64 up columns and the 64 down rows, each as d-contiguous rows,
+ * so that a top segment is a contiguous prefix of the blob and a bottom
+ * segment a contiguous suffix. */
+ms_status ms_set_expert(ms_ctx* ctx, int32_t layer, int32_t e, const void* w_gate,
+                        const void* w_up, const void* w_down);
+
+/* Make expert (layer, e) use the host blob of (src_layer, src_e), which must
+ * already be set.  Lets a deep stack reuse a few distinct weight sets. */
+ms_status ms_alias_expert(ms_ctx* ctx, int32_t layer, int32_t e, int32_t src_layer,
+                          int32_t src_e);
+
+/* Shared expert s of layer i (same layout, width d_ff_shared), copied to the
+ * device pool and always resident. */
+ms_status ms_set_shared_expert(ms_ctx* ctx, int32_t layer, int32_t s, const void* w_gate,
+                               const void* w_up, const void* w_down);
+
+/* Cache configuration of Sec. 3.4 (the output of Algorithm 1, or any other
+ * plan): per-layer budget V_i in bytes and split ratio theta_i = r[i] in
+ * [0, 1].  Derives F_top, top_bytes and C_i per layer as in ms_split_plan,
+ * carves sum_i C_i * top_bytes_i from the pool (MS_E_BUDGET if it does not
+ * fit), writes C_i to top_slots_out[i] (nullable), and resets residency: no
+ * top cached, staging buffer empty.  Synchronises the library's streams. */
+ms_status ms_configure(ms_ctx* ctx, const uint64_t* budget_bytes, const float* r,
+                       int32_t* top_slots_out);
+
+/* Cache the top segment of expert e in layer i: asynchronous H2D copy of the
+ * blob prefix into a free cache slot on the copy stream; later forwards wait
+ * for it.  MS_E_BUDGET if all C_i slots are taken, MS_E_STATE if already
+ * cached or if the layer's split has no top (F_top = 0). */
+ms_status ms_load_top(ms_ctx* ctx, int32_t layer, int32_t e);
+
+/* Drop expert e's top segment from layer i's cache (MS_E_STATE if not
+ * cached).  The slot is reused only after forwards that read it finished. */
+ms_status ms_evict_top(ms_ctx* ctx, int32_t layer, int32_t e);
+
+/* Residency of layer i's experts: state_out[E] = 0 nothing, 1 top segment
+ * cached, 2 whole expert in VRAM (top cached with F_top = F). */
+ms_status ms_residency(ms_ctx* ctx, int32_t layer, uint8_t* state_out);
+
+/* Speculative prediction of Eq. (3): apply layer i's router to h (usually the
+ * previous layer's activation h^{i-1}) and rank layer i's experts by the
+ * token-summed softmax score, descending, lower index first on equal scores.
+ * h_dev [T][d] (model dtype) on `stream`.  Blocks until the result is on the
+ * host: order_out[E] (int32), score_out[E] (fp32, nullable). */
+ms_status ms_predict(ms_ctx* ctx, int32_t layer, const void* h_dev, int32_t T,
+                     void* stream, int32_t* order_out, float* score_out);
+
+/* Prefetch of Sec. 3.2: copy the missing part of experts[0..n) of layer i
+ * into the staging buffer, one expert after the other in the given order --
+ * the bottom segment if the top is cached, the whole expert otherwise --
+ * while free buffer slots last.  Copies are issued a few chunks ahead;
+ * whatever is not yet issued when layer i's routing result is known
+ * (ms_forward of layer i) is dropped. */
+ms_status ms_prefetch(ms_ctx* ctx, int32_t layer, const int32_t* experts, int32_t n);
+
+/* Flags of ms_forward. */
+#define MS_FWD_PREDICT_NEXT 1  /* after issuing the misses, predict the next
+                                  layer (layer+1, or layer 0 of the next token
+                                  after the last layer) from this layer's h and
+                                  prefetch its experts (Sec. 3.2)            */
+
+/* MoE module of layer i (Eq. (2) without residual and Norm) on T tokens,
+ * 0 <= T <= max_tokens:
+ *   idx_dev[T][K] (int32): experts with the K largest router logits, in
+ *     descending order, lower index first on equal logits;
+ *   w_dev[T][K] (fp32): softmax scores of the selected experts, divided by
+ *     their sum if renormalize;
+ *   y_dev[T][d] (fp32): sum_k w[t][k] * E_{idx[t][k]}(h_t) + shared experts.
+ * Enqueued on `stream`; returns after the missing segments have been
+ * issued (the host waits for the routing result).  Outputs are valid once
+ * `stream` has completed.  h_dev, y_dev, idx_dev, w_dev must not be reused
+ * by the caller before that. */
+ms_status ms_forward(ms_ctx* ctx, int32_t layer, const void* h_dev, int32_t T,
+                     float* y_dev, int32_t* idx_dev, float* w_dev, int32_t flags,
+                     void* stream);
+
+/* Wait until every copy and kernel the library issued has finished. */
+ms_status ms_sync(ms_ctx* ctx);
+
+/* Drop the staging buffer's contents (prefetched or streamed segments). */
+ms_status ms_drop_buffer(ms_ctx* ctx);
+
+ms_status ms_stats(ms_ctx* ctx, int32_t layer, ms_layer_stats* out);
+ms_status ms_reset_stats(ms_ctx* ctx);
+
+/* Timeline instrumentation.  ms_timeline_begin records an origin event on
+ * `stream` and from then on brackets every kernel and copy the library
+ * issues with HIP events on the stream it runs on (at most `capacity`
+ * records).  ms_timeline_end synchronises, writes up to `cap` records to
+ * out[] (in issue order) and their count to n_out, and stops recording. */
+ms_status ms_timeline_begin(ms_ctx* ctx, void* stream, int32_t capacity);
+ms_status ms_timeline_end(ms_ctx* ctx, ms_interval* out, int32_t cap, int32_t* n_out);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* MOESPLIT_H */

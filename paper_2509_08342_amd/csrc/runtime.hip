@@ -1,0 +1,1257 @@
+// runtime.hip -- host runtime of libmoesplit: context, device-pool carve-up,
+// pinned chunk-packed expert store, per-layer top-segment caches, staging
+// buffer with chunk-group copies, prefetch queue, and the per-layer forward
+// that overlaps resident-segment compute with the transfer of missing
+// segments (arXiv 2509.08342, Sec. 3.1-3.2, Eq. (5)-(6)).
+//
+// Streams: the caller's compute stream runs routing, grouping, the resident
+// FFN launch and the combine; the library's copy stream carries every H2D
+// segment transfer; the library's side stream computes streamed chunk groups
+// as their copy events fire.  All streams have the default priority.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cstdio>
+#include <cstring>
+#include <deque>
+#include <string>
+#include <thread>
+#include <vector>
+
+#include "kernels.h"
+#include "moesplit.h"
+
+namespace {
+
+constexpr int kUnits = msk::kChunkUnits;
+constexpr uint64_t kAlign = 256;
+constexpr uint64_t kGroupTargetBytes = 16ull << 20;  // H2D copy granularity
+constexpr int kPrefetchWindow = 2;                   // prefetch groups in flight
+constexpr int kMaxD = 8192;
+
+uint64_t align_up(uint64_t x, uint64_t a) { return (x + a - 1) / a * a; }
+
+struct Shape {
+  int L, d, F, E, K, n_sh, F_sh, dtype, renorm, max_T, n_buf;
+  int elem;
+  uint64_t chunk_bytes;
+  int n_chunks, n_chunks_sh;
+  uint64_t expert_bytes, shared_bytes;
+  int group_chunks;  // chunks per H2D copy group
+  // fixed pool layout (byte offsets)
+  uint64_t off_router, off_bias, off_shared, off_ppred, off_offsets, off_perm, off_pos;
+  uint64_t off_part, off_part_sh, off_score, off_order, off_buffer, fixed_bytes;
+  uint64_t router_stride, bias_stride, part_bytes, part_sh_bytes;
+  int64_t sh_plane;
+};
+
+ms_status derive_shape(const ms_model_desc* d, Shape* s, std::string* err) {
+  if (!d) {
+    *err = "desc is NULL";
+    return MS_E_INVALID;
+  }
+  if (d->n_layers <= 0 || d->d_model <= 0 || d->d_ff <= 0 || d->n_experts <= 0 || d->top_k <= 0 ||
+      d->top_k > d->n_experts || d->n_shared < 0 || d->max_tokens <= 0 || d->n_buffer_slots < 0 ||
+      (d->dtype != MS_F32 && d->dtype != MS_BF16) || (d->n_shared > 0 && d->d_ff_shared <= 0)) {
+    *err = "invalid model description";
+    return MS_E_INVALID;
+  }
+  if (d->d_model % 64 != 0 || d->d_model > kMaxD) {
+    *err = "d_model must be a multiple of 64 and at most 8192";
+    return MS_E_UNSUPPORTED;
+  }
+  if (d->n_experts > msk::kMaxExperts || d->top_k > msk::kMaxTopK) {
+    *err = "n_experts <= 512 and top_k <= 64 are supported";
+    return MS_E_UNSUPPORTED;
+  }
+  if (static_cast<int64_t>(d->max_tokens) * d->top_k > (1 << 24)) {
+    *err = "max_tokens * top_k too large";
+    return MS_E_UNSUPPORTED;
+  }
+  s->L = d->n_layers;
+  s->d = d->d_model;
+  s->F = d->d_ff;
+  s->E = d->n_experts;
+  s->K = d->top_k;
+  s->n_sh = d->n_shared;
+  s->F_sh = d->n_shared > 0 ? d->d_ff_shared : 0;
+  s->dtype = d->dtype;
+  s->renorm = d->renormalize ? 1 : 0;
+  s->max_T = d->max_tokens;
+  s->n_buf = d->n_buffer_slots > 0 ? d->n_buffer_slots : 2 * d->top_k;
+  s->elem = d->dtype == MS_BF16 ? 2 : 4;
+  s->chunk_bytes = 3ull * kUnits * s->d * s->elem;
+  s->n_chunks = (s->F + kUnits - 1) / kUnits;
+  s->n_chunks_sh = (s->F_sh + kUnits - 1) / kUnits;
+  s->expert_bytes = s->chunk_bytes * s->n_chunks;
+  s->shared_bytes = s->chunk_bytes * s->n_chunks_sh;
+  s->group_chunks = static_cast<int>(std::max<uint64_t>(1, kGroupTargetBytes / s->chunk_bytes));
+
+  const uint64_t TK = static_cast<uint64_t>(s->max_T) * s->K;
+  uint64_t off = 0;
+  s->router_stride = align_up(static_cast<uint64_t>(s->d) * s->E * s->elem, kAlign);
+  s->off_router = off;
+  off += s->router_stride * s->L;
+  s->bias_stride = align_up(static_cast<uint64_t>(s->E) * 4, kAlign);
+  s->off_bias = off;
+  off += s->bias_stride * s->L;
+  s->off_shared = off;
+  off += align_up(s->shared_bytes, kAlign) * s->n_sh * s->L;
+  s->off_ppred = off;
+  off += align_up(static_cast<uint64_t>(s->max_T) * s->E * 4, kAlign);
+  s->off_offsets = off;
+  off += align_up(static_cast<uint64_t>(s->E + 1) * 4, kAlign);
+  s->off_perm = off;
+  off += align_up(TK * 4, kAlign);
+  s->off_pos = off;
+  off += align_up(TK * 4, kAlign);
+  s->part_bytes = static_cast<uint64_t>(s->n_chunks) * TK * s->d * 4;
+  s->off_part = off;
+  off += align_up(s->part_bytes, kAlign);
+  s->sh_plane = static_cast<int64_t>(s->n_chunks_sh) * s->max_T * s->d;
+  s->part_sh_bytes = static_cast<uint64_t>(s->sh_plane) * 4 * s->n_sh;
+  s->off_part_sh = off;
+  off += align_up(s->part_sh_bytes, kAlign);
+  s->off_score = off;
+  off += align_up(static_cast<uint64_t>(s->E) * 4, kAlign);
+  s->off_order = off;
+  off += align_up(static_cast<uint64_t>(s->E) * 4, kAlign);
+  s->off_buffer = off;
+  off += s->expert_bytes * s->n_buf;  // expert_bytes is a multiple of 256
+  s->fixed_bytes = off;
+  return MS_OK;
+}
+
+int top_units_for(float r, int F) {
+  double x = static_cast<double>(r) * F / kUnits + 0.5;
+  int units = static_cast<int>(x) * kUnits;
+  return std::max(0, std::min(units, F));
+}
+
+// Pack one SwiGLU FFN (w_gate, w_up [d][F], w_down [F][d]) into chunk order:
+// per 64-unit chunk, 64 gate columns, 64 up columns and 64 down rows, each a
+// d-contiguous row; units past F are zero.
+template <typename T>
+void pack_expert_t(const T* wg, const T* wu, const T* wd, int d, int F, int n_chunks, T* dst) {
+  auto work = [&](int c0, int c1) {
+    for (int c = c0; c < c1; ++c) {
+      T* G = dst + static_cast<size_t>(c) * 3 * kUnits * d;
+      T* U = G + static_cast<size_t>(kUnits) * d;
+      T* D = U + static_cast<size_t>(kUnits) * d;
+      const int f0 = c * kUnits;
+      const int nu = std::min(kUnits, F - f0);
+      if (nu < kUnits) std::memset(G, 0, sizeof(T) * 3 * kUnits * d);
+      for (int j = 0; j < d; ++j) {
+        const T* gr = wg + static_cast<size_t>(j) * F + f0;
+        const T* ur = wu + static_cast<size_t>(j) * F + f0;
+        for (int u = 0; u < nu; ++u) {
+          G[static_cast<size_t>(u) * d + j] = gr[u];
+          U[static_cast<size_t>(u) * d + j] = ur[u];
+        }
+      }
+      for (int u = 0; u < nu; ++u)
+        std::memcpy(D + static_cast<size_t>(u) * d, wd + static_cast<size_t>(f0 + u) * d, sizeof(T) * d);
+    }
+  };
+  const int n_threads = std::max(1, std::min<int>(16, static_cast<int>(std::thread::hardware_concurrency())));
+  if (n_chunks < 4 || n_threads == 1) {
+    work(0, n_chunks);
+    return;
+  }
+  std::vector<std::thread> th;
+  const int per = (n_chunks + n_threads - 1) / n_threads;
+  for (int i = 0; i < n_threads; ++i) {
+    const int c0 = i * per, c1 = std::min(n_chunks, c0 + per);
+    if (c0 < c1) th.emplace_back(work, c0, c1);
+  }
+  for (auto& t : th) t.join();
+}
+
+void pack_expert(const void* wg, const void* wu, const void* wd, int d, int F, int n_chunks, int elem,
+                 void* dst) {
+  if (elem == 2)
+    pack_expert_t(static_cast<const uint16_t*>(wg), static_cast<const uint16_t*>(wu),
+                  static_cast<const uint16_t*>(wd), d, F, n_chunks, static_cast<uint16_t*>(dst));
+  else
+    pack_expert_t(static_cast<const float*>(wg), static_cast<const float*>(wu),
+                  static_cast<const float*>(wd), d, F, n_chunks, static_cast<float*>(dst));
+}
+
+struct Group {
+  int c_lo = 0, c_hi = 0;
+  bool issued = false;
+  bool prefetch = false;  // issued by prefetch
+  bool used = false;      // consumed by a forward
+};
+
+struct BufSlot {
+  unsigned char* base = nullptr;  // device, expert_bytes
+  int layer = -1, expert = -1;
+  int first_chunk = 0;            // content covers chunks [first_chunk, n_chunks)
+  std::vector<Group> groups;
+  std::vector<hipEvent_t> gev;    // per group copy-done event
+  hipEvent_t last_read = nullptr; // side-stream event after the last reader
+  bool has_last_read = false;
+  uint64_t tick = 0;              // last use
+  int use_order = -1;             // order of use in the running forward (-1: not used)
+};
+
+struct LayerState {
+  bool router_set = false, bias_set = false;
+  std::vector<int> blob_of;        // [E] -> index into ctx blobs, -1 unset
+  std::vector<bool> shared_set;
+  // cache configuration (Sec. 3.4)
+  bool configured = false;
+  uint64_t budget = 0;
+  float r = 0.f;
+  int top_units = 0, top_chunks = 0;
+  uint64_t top_bytes = 0;
+  int slots = 0;                   // C_i
+  unsigned char* cache_base = nullptr;
+  std::vector<int> slot_of;        // [E] -> cache slot or -1
+  std::vector<int> slot_owner;     // [C_i] -> expert or -1
+  std::vector<hipEvent_t> pending_loads;
+  hipEvent_t last_fwd = nullptr;
+  bool has_last_fwd = false;
+  // prediction made for this layer (Eq. (3)), checked at its next routing
+  std::vector<int> pred_order;
+  bool has_pred = false;
+  ms_layer_stats st{};
+};
+
+struct TlRec {
+  int kind, layer;
+  uint64_t bytes;
+  hipEvent_t e0, e1;
+};
+
+struct PendingGroup {
+  int slot, group;
+};
+
+}  // namespace
+
+struct ms_ctx {
+  Shape s{};
+  std::string err;
+  bool poisoned = false;
+  int device = 0;
+  unsigned char* pool = nullptr;
+  uint64_t pool_bytes = 0;
+  hipStream_t copy = nullptr, side = nullptr;
+  // pinned host store
+  std::vector<unsigned char*> blobs;
+  int blob_cap = 0;  // 0: unlimited
+  // host-visible small buffers written by kernels
+  int32_t* h_offsets = nullptr;
+  int32_t* h_order = nullptr;
+  float* h_score = nullptr;
+  int32_t* d_offsets_map = nullptr;  // device views of the three buffers above
+  int32_t* d_order_map = nullptr;
+  float* d_score_map = nullptr;
+  std::vector<LayerState> layers;
+  std::vector<BufSlot> buf;
+  uint64_t tick = 0;
+  std::deque<PendingGroup> pf_queue;
+  std::vector<PendingGroup> pf_inflight;
+  hipEvent_t ev_route = nullptr, ev_side_done = nullptr, ev_last = nullptr;
+  bool has_last = false;
+  hipStream_t last_stream = nullptr;
+  std::vector<hipEvent_t> free_events;
+  // timeline
+  bool tl_on = false;
+  int tl_cap = 0;
+  hipEvent_t tl_origin = nullptr;
+  std::vector<TlRec> tl;
+  std::vector<hipEvent_t> tl_pool;
+
+  unsigned char* dev(uint64_t off) { return pool + off; }
+};
+
+namespace {
+
+#define MS_HIP(call)                                                                  \
+  do {                                                                                \
+    hipError_t e_ = (call);                                                           \
+    if (e_ != hipSuccess) return poison(ctx, #call, e_);                              \
+  } while (0)
+
+ms_status poison(ms_ctx* ctx, const char* what, hipError_t e) {
+  ctx->poisoned = true;
+  ctx->err = std::string("HIP error in ") + what + ": " + hipGetErrorString(e);
+  return MS_E_HIP;
+}
+
+ms_status fail(ms_ctx* ctx, ms_status st, const std::string& msg) {
+  ctx->err = msg;
+  return st;
+}
+
+#define MS_CHECK_CTX(ctx)                                   \
+  do {                                                      \
+    if (!(ctx)) return MS_E_INVALID;                        \
+    if ((ctx)->poisoned) return MS_E_HIP;                   \
+  } while (0)
+
+hipError_t new_event(ms_ctx* ctx, hipEvent_t* ev) {
+  if (!ctx->free_events.empty()) {
+    *ev = ctx->free_events.back();
+    ctx->free_events.pop_back();
+    return hipSuccess;
+  }
+  return hipEventCreateWithFlags(ev, hipEventDisableTiming);
+}
+
+// ---- timeline
+
+int tl_begin(ms_ctx* ctx, hipStream_t st, int kind, int layer, uint64_t bytes) {
+  if (!ctx->tl_on || static_cast<int>(ctx->tl.size()) >= ctx->tl_cap) return -1;
+  TlRec r{kind, layer, bytes, nullptr, nullptr};
+  for (hipEvent_t* e : {&r.e0, &r.e1}) {
+    if (!ctx->tl_pool.empty()) {
+      *e = ctx->tl_pool.back();
+      ctx->tl_pool.pop_back();
+    } else if (hipEventCreate(e) != hipSuccess) {
+      return -1;
+    }
+  }
+  if (hipEventRecord(r.e0, st) != hipSuccess) return -1;
+  ctx->tl.push_back(r);
+  return static_cast<int>(ctx->tl.size()) - 1;
+}
+
+void tl_end(ms_ctx* ctx, int idx, hipStream_t st) {
+  if (idx < 0) return;
+  (void)hipEventRecord(ctx->tl[idx].e1, st);
+}
+
+// ---- copies
+
+ms_status issue_copy(ms_ctx* ctx, void* dst, const void* src, uint64_t bytes, int kind, int layer) {
+  const int ti = tl_begin(ctx, ctx->copy, kind, layer, bytes);
+  MS_HIP(hipMemcpyAsync(dst, src, bytes, hipMemcpyHostToDevice, ctx->copy));
+  tl_end(ctx, ti, ctx->copy);
+  return MS_OK;
+}
+
+// Issue one group of a staging slot on the copy stream and record its event.
+ms_status issue_group(ms_ctx* ctx, int si, int gi, bool prefetch) {
+  BufSlot& b = ctx->buf[si];
+  Group& g = b.groups[gi];
+  const uint64_t cb = ctx->s.chunk_bytes;
+  const unsigned char* src = ctx->blobs[ctx->layers[b.layer].blob_of[b.expert]];
+  const uint64_t off = cb * g.c_lo, bytes = cb * (g.c_hi - g.c_lo);
+  ms_status st = issue_copy(ctx, b.base + off, src + off, bytes,
+                            prefetch ? MS_IV_COPY_PREFETCH : MS_IV_COPY_MISS, b.layer);
+  if (st != MS_OK) return st;
+  MS_HIP(hipEventRecord(b.gev[gi], ctx->copy));
+  g.issued = true;
+  g.prefetch = prefetch;
+  LayerState& L = ctx->layers[b.layer];
+  if (prefetch)
+    L.st.bytes_prefetch += bytes;
+  else
+    L.st.bytes_miss += bytes;
+  return MS_OK;
+}
+
+// Point a staging slot at (layer, e) covering chunks [first, n_chunks).  The
+// copy stream first waits for the slot's previous readers.
+ms_status assign_slot(ms_ctx* ctx, int si, int layer, int e, int first) {
+  BufSlot& b = ctx->buf[si];
+  if (b.has_last_read) MS_HIP(hipStreamWaitEvent(ctx->copy, b.last_read, 0));
+  b.layer = layer;
+  b.expert = e;
+  b.first_chunk = first;
+  b.groups.clear();
+  const int n = ctx->s.n_chunks, G = ctx->s.group_chunks;
+  for (int c = first; c < n; c += G) {
+    Group g;
+    g.c_lo = c;
+    g.c_hi = std::min(n, c + G);
+    b.groups.push_back(g);
+  }
+  while (b.gev.size() < b.groups.size()) {
+    hipEvent_t ev;
+    MS_HIP(hipEventCreateWithFlags(&ev, hipEventDisableTiming));
+    b.gev.push_back(ev);
+  }
+  return MS_OK;
+}
+
+void clear_slot(BufSlot& b) {
+  b.layer = -1;
+  b.expert = -1;
+  b.groups.clear();
+}
+
+int find_slot(ms_ctx* ctx, int layer, int e) {
+  for (int i = 0; i < static_cast<int>(ctx->buf.size()); ++i)
+    if (ctx->buf[i].layer == layer && ctx->buf[i].expert == e) return i;
+  return -1;
+}
+
+// Pick a staging slot for new content.  Prefers empty slots, then the least
+// recently used slot not used by the running forward; if allow_busy, falls
+// back to the slot the running forward used first (its readers were already
+// enqueued, and the copy stream will wait for them).
+int pick_victim(ms_ctx* ctx, bool allow_busy) {
+  int best = -1;
+  for (int i = 0; i < static_cast<int>(ctx->buf.size()); ++i) {
+    const BufSlot& b = ctx->buf[i];
+    if (b.use_order >= 0) continue;
+    if (b.layer < 0) return i;
+    if (best < 0 || b.tick < ctx->buf[best].tick) best = i;
+  }
+  if (best >= 0 || !allow_busy) return best;
+  for (int i = 0; i < static_cast<int>(ctx->buf.size()); ++i)
+    if (best < 0 || ctx->buf[i].use_order < ctx->buf[best].use_order) best = i;
+  return best;
+}
+
+// Keep up to kPrefetchWindow prefetch groups in flight.
+ms_status pump_prefetch(ms_ctx* ctx) {
+  for (size_t i = 0; i < ctx->pf_inflight.size();) {
+    const PendingGroup pg = ctx->pf_inflight[i];
+    const hipError_t q = hipEventQuery(ctx->buf[pg.slot].gev[pg.group]);
+    if (q == hipSuccess) {
+      ctx->pf_inflight.erase(ctx->pf_inflight.begin() + i);
+    } else if (q == hipErrorNotReady) {
+      ++i;
+    } else {
+      return poison(ctx, "hipEventQuery(prefetch)", q);
+    }
+  }
+  while (static_cast<int>(ctx->pf_inflight.size()) < kPrefetchWindow && !ctx->pf_queue.empty()) {
+    const PendingGroup pg = ctx->pf_queue.front();
+    ctx->pf_queue.pop_front();
+    ms_status st = issue_group(ctx, pg.slot, pg.group, true);
+    if (st != MS_OK) return st;
+    ctx->pf_inflight.push_back(pg);
+  }
+  return MS_OK;
+}
+
+// Drop every prefetch group not yet issued (Sec. 3.2: the prefetch stops when
+// a layer's routing result arrives).  Slots left with nothing issued become
+// empty.
+void terminate_prefetch(ms_ctx* ctx) {
+  for (const PendingGroup& pg : ctx->pf_queue) {
+    BufSlot& b = ctx->buf[pg.slot];
+    const Group& g = b.groups[pg.group];
+    if (b.layer >= 0)
+      ctx->layers[b.layer].st.bytes_prefetch_dropped += ctx->s.chunk_bytes * (g.c_hi - g.c_lo);
+  }
+  ctx->pf_queue.clear();
+  for (BufSlot& b : ctx->buf) {
+    if (b.layer < 0) continue;
+    bool any = false;
+    for (const Group& g : b.groups) any = any || g.issued;
+    if (!any) clear_slot(b);
+  }
+}
+
+// Resident chunks of expert e in layer L: [0, top_chunks) if its top is
+// cached, none otherwise.
+int resident_chunks(const LayerState& L, int e) { return L.slot_of[e] >= 0 ? L.top_chunks : 0; }
+
+// Enqueue the prefetch of experts[0..n) of `layer` (in order) into free
+// staging slots: the bottom if the top is cached, else the whole expert.
+ms_status enqueue_prefetch(ms_ctx* ctx, int layer, const int32_t* experts, int n) {
+  LayerState& L = ctx->layers[layer];
+  const int nch = ctx->s.n_chunks;
+  for (int i = 0; i < n; ++i) {
+    const int e = experts[i];
+    const int res = resident_chunks(L, e);
+    if (res >= nch) continue;                       // already whole in VRAM
+    if (L.blob_of[e] < 0) continue;                 // weights not set
+    const int have = find_slot(ctx, layer, e);
+    if (have >= 0 && ctx->buf[have].first_chunk <= res) {
+      // already (partly) buffered: queue what has not been issued
+      BufSlot& hb = ctx->buf[have];
+      bool queued = false;
+      for (const PendingGroup& pg : ctx->pf_queue) queued = queued || pg.slot == have;
+      if (queued) continue;
+      for (int gi = 0; gi < static_cast<int>(hb.groups.size()); ++gi)
+        if (!hb.groups[gi].issued && hb.groups[gi].c_hi > res) ctx->pf_queue.push_back({have, gi});
+      hb.tick = ++ctx->tick;
+      continue;
+    }
+    int si = have >= 0 ? have : pick_victim(ctx, false);
+    if (si < 0) break;                              // no free slot left
+    if (ctx->buf[si].use_order >= 0) break;
+    // a slot already queued for prefetch must not be taken over
+    bool queued = false;
+    for (const PendingGroup& pg : ctx->pf_queue) queued = queued || pg.slot == si;
+    for (const PendingGroup& pg : ctx->pf_inflight) queued = queued || pg.slot == si;
+    if (queued) break;
+    ms_status st = assign_slot(ctx, si, layer, e, res);
+    if (st != MS_OK) return st;
+    ctx->buf[si].tick = ++ctx->tick;
+    for (int gi = 0; gi < static_cast<int>(ctx->buf[si].groups.size()); ++gi)
+      ctx->pf_queue.push_back({si, gi});
+  }
+  return pump_prefetch(ctx);
+}
+
+ms_status check_layer(ms_ctx* ctx, int layer) {
+  if (layer < 0 || layer >= ctx->s.L) return fail(ctx, MS_E_INVALID, "layer out of range");
+  return MS_OK;
+}
+
+// Order work on `stream` after the previous forward/prediction of this
+// context (they share the work buffers).
+ms_status order_after_last(ms_ctx* ctx, hipStream_t stream) {
+  if (ctx->has_last && ctx->last_stream != stream) MS_HIP(hipStreamWaitEvent(stream, ctx->ev_last, 0));
+  return MS_OK;
+}
+
+}  // namespace
+
+// ============================================================== C ABI ====
+
+extern "C" {
+
+ms_status ms_query_sizes(const ms_model_desc* desc, ms_sizes* out) {
+  if (!out) return MS_E_INVALID;
+  Shape s;
+  std::string err;
+  ms_status st = derive_shape(desc, &s, &err);
+  if (st != MS_OK) return st;
+  out->chunk_bytes = s.chunk_bytes;
+  out->n_chunks = s.n_chunks;
+  out->expert_bytes = s.expert_bytes;
+  out->fixed_pool_bytes = s.fixed_bytes;
+  out->buffer_bytes = s.expert_bytes * s.n_buf;
+  return MS_OK;
+}
+
+ms_status ms_split_plan(const ms_model_desc* desc, uint64_t budget_bytes, float r, int32_t* top_units_out,
+                        uint64_t* top_bytes_out, int32_t* top_slots_out) {
+  Shape s;
+  std::string err;
+  ms_status st = derive_shape(desc, &s, &err);
+  if (st != MS_OK) return st;
+  if (!(r >= 0.0f && r <= 1.0f)) return MS_E_INVALID;
+  const int units = top_units_for(r, s.F);
+  const int chunks = (units + kUnits - 1) / kUnits;
+  const uint64_t tb = s.chunk_bytes * chunks;
+  int32_t slots = 0;
+  if (tb > 0) slots = static_cast<int32_t>(std::min<uint64_t>(budget_bytes / tb, s.E));
+  if (top_units_out) *top_units_out = units;
+  if (top_bytes_out) *top_bytes_out = tb;
+  if (top_slots_out) *top_slots_out = slots;
+  return MS_OK;
+}
+
+const char* ms_last_error(const ms_ctx* ctx) { return ctx ? ctx->err.c_str() : "NULL context"; }
+
+ms_status ms_create(const ms_model_desc* desc, void* dev_pool, uint64_t pool_bytes, int32_t host_store_experts,
+                    ms_ctx** out) {
+  if (!out) return MS_E_INVALID;
+  *out = nullptr;
+  ms_ctx* ctx = new ms_ctx();
+  std::string err;
+  ms_status st = derive_shape(desc, &ctx->s, &err);
+  if (st != MS_OK) {
+    delete ctx;
+    return st;
+  }
+  if (!dev_pool || (reinterpret_cast<uintptr_t>(dev_pool) % kAlign) != 0) {
+    delete ctx;
+    return MS_E_INVALID;
+  }
+  if (pool_bytes < ctx->s.fixed_bytes) {
+    delete ctx;
+    return MS_E_BUDGET;
+  }
+  if (host_store_experts < 0) {
+    delete ctx;
+    return MS_E_INVALID;
+  }
+  ctx->pool = static_cast<unsigned char*>(dev_pool);
+  ctx->pool_bytes = pool_bytes;
+  ctx->blob_cap = host_store_experts;
+  const Shape& s = ctx->s;
+  auto cleanup_fail = [&](hipError_t e, const char* what) {
+    ms_status rs = poison(ctx, what, e);
+    (void)rs;
+    ms_destroy(ctx);
+    return MS_E_HIP;
+  };
+  hipError_t e;
+  if ((e = hipGetDevice(&ctx->device)) != hipSuccess) return cleanup_fail(e, "hipGetDevice");
+  if ((e = hipStreamCreateWithFlags(&ctx->copy, hipStreamNonBlocking)) != hipSuccess)
+    return cleanup_fail(e, "hipStreamCreate(copy)");
+  if ((e = hipStreamCreateWithFlags(&ctx->side, hipStreamNonBlocking)) != hipSuccess)
+    return cleanup_fail(e, "hipStreamCreate(side)");
+  for (hipEvent_t* ev : {&ctx->ev_route, &ctx->ev_side_done, &ctx->ev_last})
+    if ((e = hipEventCreateWithFlags(ev, hipEventDisableTiming)) != hipSuccess)
+      return cleanup_fail(e, "hipEventCreate");
+  // small host buffers that kernels write directly (mapped, coherent)
+  const unsigned mflags = hipHostMallocMapped | hipHostMallocCoherent;
+  if ((e = hipHostMalloc(reinterpret_cast<void**>(&ctx->h_offsets), sizeof(int32_t) * (s.E + 1), mflags)) != hipSuccess)
+    return cleanup_fail(e, "hipHostMalloc(offsets)");
+  if ((e = hipHostMalloc(reinterpret_cast<void**>(&ctx->h_order), sizeof(int32_t) * s.E, mflags)) != hipSuccess)
+    return cleanup_fail(e, "hipHostMalloc(order)");
+  if ((e = hipHostMalloc(reinterpret_cast<void**>(&ctx->h_score), sizeof(float) * s.E, mflags)) != hipSuccess)
+    return cleanup_fail(e, "hipHostMalloc(score)");
+  if ((e = hipHostGetDevicePointer(reinterpret_cast<void**>(&ctx->d_offsets_map), ctx->h_offsets, 0)) != hipSuccess)
+    return cleanup_fail(e, "hipHostGetDevicePointer(offsets)");
+  if ((e = hipHostGetDevicePointer(reinterpret_cast<void**>(&ctx->d_order_map), ctx->h_order, 0)) != hipSuccess)
+    return cleanup_fail(e, "hipHostGetDevicePointer(order)");
+  if ((e = hipHostGetDevicePointer(reinterpret_cast<void**>(&ctx->d_score_map), ctx->h_score, 0)) != hipSuccess)
+    return cleanup_fail(e, "hipHostGetDevicePointer(score)");
+  ctx->layers.resize(s.L);
+  for (LayerState& L : ctx->layers) {
+    L.blob_of.assign(s.E, -1);
+    L.shared_set.assign(s.n_sh, false);
+    L.slot_of.assign(s.E, -1);
+    if ((e = hipEventCreateWithFlags(&L.last_fwd, hipEventDisableTiming)) != hipSuccess)
+      return cleanup_fail(e, "hipEventCreate(layer)");
+  }
+  ctx->buf.resize(s.n_buf);
+  for (int i = 0; i < s.n_buf; ++i) {
+    ctx->buf[i].base = ctx->dev(s.off_buffer + s.expert_bytes * i);
+    if ((e = hipEventCreateWithFlags(&ctx->buf[i].last_read, hipEventDisableTiming)) != hipSuccess)
+      return cleanup_fail(e, "hipEventCreate(slot)");
+  }
+  *out = ctx;
+  return MS_OK;
+}
+
+void ms_destroy(ms_ctx* ctx) {
+  if (!ctx) return;
+  if (ctx->copy) (void)hipStreamSynchronize(ctx->copy);
+  if (ctx->side) (void)hipStreamSynchronize(ctx->side);
+  if (ctx->has_last) (void)hipEventSynchronize(ctx->ev_last);
+  for (LayerState& L : ctx->layers) {
+    for (hipEvent_t ev : L.pending_loads) (void)hipEventDestroy(ev);
+    if (L.last_fwd) (void)hipEventDestroy(L.last_fwd);
+  }
+  for (BufSlot& b : ctx->buf) {
+    for (hipEvent_t ev : b.gev) (void)hipEventDestroy(ev);
+    if (b.last_read) (void)hipEventDestroy(b.last_read);
+  }
+  for (hipEvent_t ev : ctx->free_events) (void)hipEventDestroy(ev);
+  for (TlRec& r : ctx->tl) {
+    (void)hipEventDestroy(r.e0);
+    (void)hipEventDestroy(r.e1);
+  }
+  for (hipEvent_t ev : ctx->tl_pool) (void)hipEventDestroy(ev);
+  if (ctx->tl_origin) (void)hipEventDestroy(ctx->tl_origin);
+  for (hipEvent_t ev : {ctx->ev_route, ctx->ev_side_done, ctx->ev_last})
+    if (ev) (void)hipEventDestroy(ev);
+  for (unsigned char* p : ctx->blobs) (void)hipHostFree(p);
+  if (ctx->h_offsets) (void)hipHostFree(ctx->h_offsets);
+  if (ctx->h_order) (void)hipHostFree(ctx->h_order);
+  if (ctx->h_score) (void)hipHostFree(ctx->h_score);
+  if (ctx->copy) (void)hipStreamDestroy(ctx->copy);
+  if (ctx->side) (void)hipStreamDestroy(ctx->side);
+  delete ctx;
+}
+
+ms_status ms_set_router(ms_ctx* ctx, int32_t layer, const void* w_r, const float* bias) {
+  MS_CHECK_CTX(ctx);
+  ms_status st = check_layer(ctx, layer);
+  if (st != MS_OK) return st;
+  if (!w_r) return fail(ctx, MS_E_INVALID, "w_r is NULL");
+  const Shape& s = ctx->s;
+  MS_HIP(hipMemcpy(ctx->dev(s.off_router + s.router_stride * layer), w_r,
+                   static_cast<size_t>(s.d) * s.E * s.elem, hipMemcpyHostToDevice));
+  LayerState& L = ctx->layers[layer];
+  if (bias) MS_HIP(hipMemcpy(ctx->dev(s.off_bias + s.bias_stride * layer), bias, sizeof(float) * s.E,
+                             hipMemcpyHostToDevice));
+  L.router_set = true;
+  L.bias_set = bias != nullptr;
+  return MS_OK;
+}
+
+ms_status ms_set_expert(ms_ctx* ctx, int32_t layer, int32_t e, const void* w_gate, const void* w_up,
+                        const void* w_down) {
+  MS_CHECK_CTX(ctx);
+  ms_status st = check_layer(ctx, layer);
+  if (st != MS_OK) return st;
+  const Shape& s = ctx->s;
+  if (e < 0 || e >= s.E) return fail(ctx, MS_E_INVALID, "expert out of range");
+  if (!w_gate || !w_up || !w_down) return fail(ctx, MS_E_INVALID, "weight pointer is NULL");
+  LayerState& L = ctx->layers[layer];
+  int bi = L.blob_of[e];
+  // reuse the blob only if no other (layer, expert) aliases it
+  if (bi >= 0) {
+    int users = 0;
+    for (const LayerState& L2 : ctx->layers)
+      for (int b : L2.blob_of) users += (b == bi);
+    if (users > 1) bi = -1;
+  }
+  if (bi < 0) {
+    if (ctx->blob_cap > 0 && static_cast<int>(ctx->blobs.size()) >= ctx->blob_cap)
+      return fail(ctx, MS_E_NOMEM, "host expert store is full (host_store_experts)");
+    void* p = nullptr;
+    hipError_t he = hipHostMalloc(&p, s.expert_bytes);
+    if (he != hipSuccess || !p) {
+      (void)hipGetLastError();
+      return fail(ctx, MS_E_NOMEM, "hipHostMalloc of an expert blob failed");
+    }
+    ctx->blobs.push_back(static_cast<unsigned char*>(p));
+    bi = static_cast<int>(ctx->blobs.size()) - 1;
+  }
+  // the blob may be read by in-flight copies: wait for them before rewriting
+  MS_HIP(hipStreamSynchronize(ctx->copy));
+  pack_expert(w_gate, w_up, w_down, s.d, s.F, s.n_chunks, s.elem, ctx->blobs[bi]);
+  L.blob_of[e] = bi;
+  return MS_OK;
+}
+
+ms_status ms_alias_expert(ms_ctx* ctx, int32_t layer, int32_t e, int32_t src_layer, int32_t src_e) {
+  MS_CHECK_CTX(ctx);
+  if (check_layer(ctx, layer) != MS_OK || check_layer(ctx, src_layer) != MS_OK)
+    return fail(ctx, MS_E_INVALID, "layer out of range");
+  const Shape& s = ctx->s;
+  if (e < 0 || e >= s.E || src_e < 0 || src_e >= s.E) return fail(ctx, MS_E_INVALID, "expert out of range");
+  const int bi = ctx->layers[src_layer].blob_of[src_e];
+  if (bi < 0) return fail(ctx, MS_E_STATE, "source expert not set");
+  ctx->layers[layer].blob_of[e] = bi;
+  return MS_OK;
+}
+
+ms_status ms_set_shared_expert(ms_ctx* ctx, int32_t layer, int32_t sidx, const void* w_gate, const void* w_up,
+                               const void* w_down) {
+  MS_CHECK_CTX(ctx);
+  ms_status st = check_layer(ctx, layer);
+  if (st != MS_OK) return st;
+  const Shape& s = ctx->s;
+  if (sidx < 0 || sidx >= s.n_sh) return fail(ctx, MS_E_INVALID, "shared expert out of range");
+  if (!w_gate || !w_up || !w_down) return fail(ctx, MS_E_INVALID, "weight pointer is NULL");
+  std::vector<unsigned char> tmp(s.shared_bytes);
+  pack_expert(w_gate, w_up, w_down, s.d, s.F_sh, s.n_chunks_sh, s.elem, tmp.data());
+  const uint64_t off = s.off_shared + align_up(s.shared_bytes, kAlign) * (static_cast<uint64_t>(layer) * s.n_sh + sidx);
+  if (ctx->has_last) MS_HIP(hipEventSynchronize(ctx->ev_last));
+  MS_HIP(hipMemcpy(ctx->dev(off), tmp.data(), s.shared_bytes, hipMemcpyHostToDevice));
+  ctx->layers[layer].shared_set[sidx] = true;
+  return MS_OK;
+}
+
+ms_status ms_sync(ms_ctx* ctx) {
+  MS_CHECK_CTX(ctx);
+  MS_HIP(hipStreamSynchronize(ctx->copy));
+  MS_HIP(hipStreamSynchronize(ctx->side));
+  if (ctx->has_last) MS_HIP(hipEventSynchronize(ctx->ev_last));
+  return MS_OK;
+}
+
+ms_status ms_configure(ms_ctx* ctx, const uint64_t* budget_bytes, const float* r, int32_t* top_slots_out) {
+  MS_CHECK_CTX(ctx);
+  if (!budget_bytes || !r) return fail(ctx, MS_E_INVALID, "NULL budget or ratio array");
+  const Shape& s = ctx->s;
+  uint64_t total = 0;
+  for (int i = 0; i < s.L; ++i) {
+    if (!(r[i] >= 0.0f && r[i] <= 1.0f)) return fail(ctx, MS_E_INVALID, "split ratio outside [0, 1]");
+    total += budget_bytes[i];
+  }
+  if (total > ctx->pool_bytes - s.fixed_bytes)
+    return fail(ctx, MS_E_BUDGET, "sum of layer budgets exceeds the device pool");
+  ms_status st = ms_sync(ctx);
+  if (st != MS_OK) return st;
+  ctx->pf_queue.clear();
+  ctx->pf_inflight.clear();
+  for (BufSlot& b : ctx->buf) {
+    clear_slot(b);
+    b.has_last_read = false;
+    b.use_order = -1;
+  }
+  uint64_t off = s.fixed_bytes;
+  for (int i = 0; i < s.L; ++i) {
+    LayerState& L = ctx->layers[i];
+    L.budget = budget_bytes[i];
+    L.r = r[i];
+    L.top_units = top_units_for(r[i], s.F);
+    L.top_chunks = (L.top_units + kUnits - 1) / kUnits;
+    L.top_bytes = s.chunk_bytes * L.top_chunks;
+    L.slots = L.top_bytes > 0 ? static_cast<int>(std::min<uint64_t>(budget_bytes[i] / L.top_bytes, s.E)) : 0;
+    L.cache_base = ctx->dev(off);
+    off += align_up(L.top_bytes * L.slots, kAlign);
+    L.slot_of.assign(s.E, -1);
+    L.slot_owner.assign(L.slots, -1);
+    for (hipEvent_t ev : L.pending_loads) ctx->free_events.push_back(ev);
+    L.pending_loads.clear();
+    L.has_pred = false;
+    L.configured = true;
+    if (top_slots_out) top_slots_out[i] = L.slots;
+  }
+  return MS_OK;
+}
+
+ms_status ms_load_top(ms_ctx* ctx, int32_t layer, int32_t e) {
+  MS_CHECK_CTX(ctx);
+  ms_status st = check_layer(ctx, layer);
+  if (st != MS_OK) return st;
+  LayerState& L = ctx->layers[layer];
+  if (e < 0 || e >= ctx->s.E) return fail(ctx, MS_E_INVALID, "expert out of range");
+  if (!L.configured) return fail(ctx, MS_E_STATE, "layer not configured");
+  if (L.top_chunks == 0) return fail(ctx, MS_E_STATE, "layer split has no top segment");
+  if (L.blob_of[e] < 0) return fail(ctx, MS_E_STATE, "expert weights not set");
+  if (L.slot_of[e] >= 0) return fail(ctx, MS_E_STATE, "top segment already cached");
+  int slot = -1;
+  for (int i = 0; i < L.slots; ++i)
+    if (L.slot_owner[i] < 0) {
+      slot = i;
+      break;
+    }
+  if (slot < 0) return fail(ctx, MS_E_BUDGET, "no free top-segment slot in this layer");
+  if (L.has_last_fwd) MS_HIP(hipStreamWaitEvent(ctx->copy, L.last_fwd, 0));
+  st = issue_copy(ctx, L.cache_base + L.top_bytes * slot, ctx->blobs[L.blob_of[e]], L.top_bytes, MS_IV_COPY_TOP,
+                  layer);
+  if (st != MS_OK) return st;
+  hipEvent_t ev;
+  MS_HIP(new_event(ctx, &ev));
+  MS_HIP(hipEventRecord(ev, ctx->copy));
+  L.pending_loads.push_back(ev);
+  L.slot_of[e] = slot;
+  L.slot_owner[slot] = e;
+  return MS_OK;
+}
+
+ms_status ms_evict_top(ms_ctx* ctx, int32_t layer, int32_t e) {
+  MS_CHECK_CTX(ctx);
+  ms_status st = check_layer(ctx, layer);
+  if (st != MS_OK) return st;
+  LayerState& L = ctx->layers[layer];
+  if (e < 0 || e >= ctx->s.E) return fail(ctx, MS_E_INVALID, "expert out of range");
+  if (!L.configured || L.slot_of[e] < 0) return fail(ctx, MS_E_STATE, "top segment not cached");
+  L.slot_owner[L.slot_of[e]] = -1;
+  L.slot_of[e] = -1;
+  return MS_OK;
+}
+
+ms_status ms_residency(ms_ctx* ctx, int32_t layer, uint8_t* state_out) {
+  MS_CHECK_CTX(ctx);
+  ms_status st = check_layer(ctx, layer);
+  if (st != MS_OK) return st;
+  if (!state_out) return fail(ctx, MS_E_INVALID, "state_out is NULL");
+  const LayerState& L = ctx->layers[layer];
+  for (int e = 0; e < ctx->s.E; ++e) {
+    uint8_t v = 0;
+    if (L.configured && L.slot_of[e] >= 0) v = (L.top_chunks >= ctx->s.n_chunks) ? 2 : 1;
+    state_out[e] = v;
+  }
+  return MS_OK;
+}
+
+ms_status ms_drop_buffer(ms_ctx* ctx) {
+  MS_CHECK_CTX(ctx);
+  ctx->pf_queue.clear();
+  for (BufSlot& b : ctx->buf) clear_slot(b);
+  return MS_OK;
+}
+
+ms_status ms_prefetch(ms_ctx* ctx, int32_t layer, const int32_t* experts, int32_t n) {
+  MS_CHECK_CTX(ctx);
+  ms_status st = check_layer(ctx, layer);
+  if (st != MS_OK) return st;
+  if (n < 0 || (n > 0 && !experts)) return fail(ctx, MS_E_INVALID, "bad expert list");
+  for (int i = 0; i < n; ++i)
+    if (experts[i] < 0 || experts[i] >= ctx->s.E) return fail(ctx, MS_E_INVALID, "expert out of range");
+  if (!ctx->layers[layer].configured) return fail(ctx, MS_E_STATE, "layer not configured");
+  return enqueue_prefetch(ctx, layer, experts, n);
+}
+
+ms_status ms_predict(ms_ctx* ctx, int32_t layer, const void* h_dev, int32_t T, void* stream, int32_t* order_out,
+                     float* score_out) {
+  MS_CHECK_CTX(ctx);
+  ms_status st = check_layer(ctx, layer);
+  if (st != MS_OK) return st;
+  const Shape& s = ctx->s;
+  if (T < 1 || T > s.max_T || !h_dev || !order_out) return fail(ctx, MS_E_INVALID, "bad prediction arguments");
+  if ((reinterpret_cast<uintptr_t>(h_dev) % 16) != 0) return fail(ctx, MS_E_INVALID, "h_dev not 16-byte aligned");
+  LayerState& L = ctx->layers[layer];
+  if (!L.router_set) return fail(ctx, MS_E_STATE, "router not set");
+  hipStream_t sm = static_cast<hipStream_t>(stream);
+  st = order_after_last(ctx, sm);
+  if (st != MS_OK) return st;
+  msk::RouterArgs ra{};
+  ra.h = h_dev;
+  ra.T = T;
+  ra.d = s.d;
+  ra.E = s.E;
+  ra.K = s.K;
+  ra.dtype = s.dtype;
+  ra.renormalize = s.renorm;
+  ra.wr_next = ctx->dev(s.off_router + s.router_stride * layer);
+  ra.bias_next = L.bias_set ? reinterpret_cast<const float*>(ctx->dev(s.off_bias + s.bias_stride * layer)) : nullptr;
+  ra.p_pred = reinterpret_cast<float*>(ctx->dev(s.off_ppred));
+  int ti = tl_begin(ctx, sm, MS_IV_ROUTER, layer, static_cast<uint64_t>(s.d) * s.E * s.elem);
+  MS_HIP(msk::launch_router(ra, sm));
+  tl_end(ctx, ti, sm);
+  msk::RankArgs rk{};
+  rk.p_pred = ra.p_pred;
+  rk.T = T;
+  rk.E = s.E;
+  rk.score = reinterpret_cast<float*>(ctx->dev(s.off_score));
+  rk.order = reinterpret_cast<int32_t*>(ctx->dev(s.off_order));
+  rk.host_score = ctx->d_score_map;
+  rk.host_order = ctx->d_order_map;
+  ti = tl_begin(ctx, sm, MS_IV_PREDICT, layer, 0);
+  MS_HIP(msk::launch_rank(rk, sm));
+  tl_end(ctx, ti, sm);
+  MS_HIP(hipEventRecord(ctx->ev_last, sm));
+  ctx->has_last = true;
+  ctx->last_stream = sm;
+  MS_HIP(hipEventSynchronize(ctx->ev_last));
+  std::memcpy(order_out, const_cast<const int32_t*>(ctx->h_order), sizeof(int32_t) * s.E);
+  if (score_out) std::memcpy(score_out, const_cast<const float*>(ctx->h_score), sizeof(float) * s.E);
+  L.pred_order.assign(order_out, order_out + s.E);
+  L.has_pred = true;
+  return MS_OK;
+}
+
+ms_status ms_forward(ms_ctx* ctx, int32_t layer, const void* h_dev, int32_t T, float* y_dev, int32_t* idx_dev,
+                     float* w_dev, int32_t flags, void* stream) {
+  MS_CHECK_CTX(ctx);
+  ms_status st = check_layer(ctx, layer);
+  if (st != MS_OK) return st;
+  const Shape& s = ctx->s;
+  if (T < 0 || T > s.max_T) return fail(ctx, MS_E_INVALID, "T outside [0, max_tokens]");
+  if (T == 0) return MS_OK;
+  if (!h_dev || !y_dev || !idx_dev || !w_dev) return fail(ctx, MS_E_INVALID, "NULL device buffer");
+  if ((reinterpret_cast<uintptr_t>(h_dev) % 16) != 0 || (reinterpret_cast<uintptr_t>(y_dev) % 16) != 0)
+    return fail(ctx, MS_E_INVALID, "h_dev and y_dev must be 16-byte aligned");
+  LayerState& L = ctx->layers[layer];
+  if (!L.configured) return fail(ctx, MS_E_STATE, "layer not configured (ms_configure)");
+  if (!L.router_set) return fail(ctx, MS_E_STATE, "router not set");
+  for (int e = 0; e < s.E; ++e)
+    if (L.blob_of[e] < 0) return fail(ctx, MS_E_STATE, "expert weights not set");
+  for (int i = 0; i < s.n_sh; ++i)
+    if (!L.shared_set[i]) return fail(ctx, MS_E_STATE, "shared expert weights not set");
+  const bool predict_next = (flags & MS_FWD_PREDICT_NEXT) != 0;
+  const int next_layer = (layer + 1) % s.L;
+  if (predict_next && !ctx->layers[next_layer].router_set)
+    return fail(ctx, MS_E_STATE, "next layer's router not set");
+
+  hipStream_t sm = static_cast<hipStream_t>(stream);
+  st = order_after_last(ctx, sm);
+  if (st != MS_OK) return st;
+  for (hipEvent_t ev : L.pending_loads) {
+    MS_HIP(hipStreamWaitEvent(sm, ev, 0));
+    ctx->free_events.push_back(ev);
+  }
+  L.pending_loads.clear();
+
+  const int TK = T * s.K;
+  int32_t* d_offsets = reinterpret_cast<int32_t*>(ctx->dev(s.off_offsets));
+  int32_t* d_perm = reinterpret_cast<int32_t*>(ctx->dev(s.off_perm));
+  int32_t* d_pos = reinterpret_cast<int32_t*>(ctx->dev(s.off_pos));
+  float* d_part = reinterpret_cast<float*>(ctx->dev(s.off_part));
+  float* d_part_sh = reinterpret_cast<float*>(ctx->dev(s.off_part_sh));
+  const int rows_routed = s.max_T * s.K;
+
+  // 1. routing (+ next-layer prediction), grouping
+  msk::RouterArgs ra{};
+  ra.h = h_dev;
+  ra.T = T;
+  ra.d = s.d;
+  ra.E = s.E;
+  ra.K = s.K;
+  ra.dtype = s.dtype;
+  ra.renormalize = s.renorm;
+  ra.wr = ctx->dev(s.off_router + s.router_stride * layer);
+  ra.bias = L.bias_set ? reinterpret_cast<const float*>(ctx->dev(s.off_bias + s.bias_stride * layer)) : nullptr;
+  ra.idx = idx_dev;
+  ra.w = w_dev;
+  if (predict_next) {
+    const LayerState& N = ctx->layers[next_layer];
+    ra.wr_next = ctx->dev(s.off_router + s.router_stride * next_layer);
+    ra.bias_next = N.bias_set ? reinterpret_cast<const float*>(ctx->dev(s.off_bias + s.bias_stride * next_layer)) : nullptr;
+    ra.p_pred = reinterpret_cast<float*>(ctx->dev(s.off_ppred));
+  }
+  const uint64_t router_bytes = static_cast<uint64_t>(s.d) * s.E * s.elem * (predict_next ? 2 : 1);
+  int ti = tl_begin(ctx, sm, MS_IV_ROUTER, layer, router_bytes);
+  MS_HIP(msk::launch_router(ra, sm));
+  tl_end(ctx, ti, sm);
+
+  msk::GroupArgs ga{};
+  ga.idx = idx_dev;
+  ga.TK = TK;
+  ga.E = s.E;
+  ga.offsets = d_offsets;
+  ga.perm = d_perm;
+  ga.pos = d_pos;
+  ga.host_offsets = ctx->d_offsets_map;
+  ti = tl_begin(ctx, sm, MS_IV_GROUP, layer, 0);
+  MS_HIP(msk::launch_group(ga, sm));
+  tl_end(ctx, ti, sm);
+  if (predict_next) {
+    msk::RankArgs rk{};
+    rk.p_pred = ra.p_pred;
+    rk.T = T;
+    rk.E = s.E;
+    rk.score = reinterpret_cast<float*>(ctx->dev(s.off_score));
+    rk.order = reinterpret_cast<int32_t*>(ctx->dev(s.off_order));
+    rk.host_score = ctx->d_score_map;
+    rk.host_order = ctx->d_order_map;
+    ti = tl_begin(ctx, sm, MS_IV_PREDICT, layer, 0);
+    MS_HIP(msk::launch_rank(rk, sm));
+    tl_end(ctx, ti, sm);
+  }
+  MS_HIP(hipEventRecord(ctx->ev_route, sm));
+
+  // 2. resident segments (Eq. (5): processed while missing ones load)
+  msk::FfnArgs fa{};
+  fa.h = h_dev;
+  fa.offsets = d_offsets;
+  fa.perm = d_perm;
+  fa.part = d_part;
+  fa.part_sh = d_part_sh;
+  fa.chunk_bytes = s.chunk_bytes;
+  fa.sh_plane = s.sh_plane;
+  fa.rows_routed = rows_routed;
+  fa.rows_shared = s.max_T;
+  fa.d = s.d;
+  fa.K = s.K;
+  fa.T = T;
+  fa.dtype = s.dtype;
+  std::vector<msk::FfnTask> res_tasks;
+  std::vector<int> res_task_expert;
+  for (int e = 0; e < s.E; ++e) {
+    const int rc = resident_chunks(L, e);
+    if (rc <= 0) continue;
+    msk::FfnTask t{};
+    t.base = L.cache_base + L.top_bytes * L.slot_of[e];
+    t.expert = e;
+    t.chunk_lo = 0;
+    t.n_chunks = rc;
+    res_tasks.push_back(t);
+  }
+  for (int i = 0; i < s.n_sh; ++i) {
+    msk::FfnTask t{};
+    t.base = ctx->dev(s.off_shared + align_up(s.shared_bytes, kAlign) * (static_cast<uint64_t>(layer) * s.n_sh + i));
+    t.expert = -1 - i;
+    t.chunk_lo = 0;
+    t.n_chunks = s.n_chunks_sh;
+    res_tasks.push_back(t);
+  }
+  std::vector<int> res_tl;  // timeline records of resident launches (bytes fixed after routing)
+  std::vector<std::vector<msk::FfnTask>> res_batches;
+  for (size_t i0 = 0; i0 < res_tasks.size(); i0 += msk::kMaxTasks) {
+    const size_t i1 = std::min(res_tasks.size(), i0 + msk::kMaxTasks);
+    fa.n_tasks = static_cast<int>(i1 - i0);
+    int wg = 0;
+    for (size_t i = i0; i < i1; ++i) {
+      fa.tasks[i - i0] = res_tasks[i];
+      fa.tasks[i - i0].wg_begin = wg;
+      wg += res_tasks[i].n_chunks;
+    }
+    fa.n_wg = wg;
+    ti = tl_begin(ctx, sm, MS_IV_FFN_RESIDENT, layer, 0);
+    MS_HIP(msk::launch_ffn(fa, T, sm));
+    tl_end(ctx, ti, sm);
+    res_tl.push_back(ti);
+    res_batches.emplace_back(res_tasks.begin() + i0, res_tasks.begin() + i1);
+  }
+
+  // 3. wait for the routing result on the host, keeping prefetch copies fed
+  for (;;) {
+    const hipError_t q = hipEventQuery(ctx->ev_route);
+    if (q == hipSuccess) break;
+    if (q != hipErrorNotReady) return poison(ctx, "hipEventQuery(route)", q);
+    st = pump_prefetch(ctx);
+    if (st != MS_OK) return st;
+  }
+  std::vector<int32_t> offs(s.E + 1);
+  for (int e = 0; e <= s.E; ++e) offs[e] = reinterpret_cast<volatile int32_t*>(ctx->h_offsets)[e];
+  std::vector<int> pred;
+  if (predict_next) {
+    pred.resize(s.E);
+    for (int e = 0; e < s.E; ++e) pred[e] = reinterpret_cast<volatile int32_t*>(ctx->h_order)[e];
+  }
+  terminate_prefetch(ctx);
+  for (auto& pg : ctx->pf_inflight) (void)pg;  // in-flight groups complete on their own
+  ctx->pf_inflight.clear();
+
+  // bytes of the resident launches now that the active experts are known
+  const uint64_t shb = s.shared_bytes;
+  for (size_t bi = 0; bi < res_tl.size(); ++bi) {
+    if (res_tl[bi] < 0) continue;
+    uint64_t bytes = 0;
+    for (const msk::FfnTask& t : res_batches[bi]) {
+      if (t.expert >= 0 && offs[t.expert + 1] == offs[t.expert]) continue;
+      bytes += (t.expert >= 0 ? s.chunk_bytes * t.n_chunks : shb);
+    }
+    ctx->tl[res_tl[bi]].bytes = bytes;
+  }
+
+  // 4. statistics of this routing (Sec. 3.4.1: alpha / beta / gamma)
+  L.st.forwards += 1;
+  L.st.tokens += T;
+  L.st.selected += TK;
+  if (L.has_pred) {
+    for (int k = 0; k < std::min<int>(s.K, static_cast<int>(L.pred_order.size())); ++k) {
+      const int e = L.pred_order[k];
+      if (offs[e + 1] > offs[e]) L.st.predicted_hits += 1;
+    }
+    L.st.predictions += 1;
+    L.has_pred = false;
+  }
+
+  // 5. missing segments: copy stream issues, side stream computes per group
+  MS_HIP(hipStreamWaitEvent(ctx->side, ctx->ev_route, 0));
+  // slots already holding an active expert's missing part are reserved so
+  // that no other miss of this forward evicts them first
+  constexpr int kReserved = 1 << 30;
+  for (int e = 0; e < s.E; ++e) {
+    if (offs[e + 1] == offs[e]) continue;
+    const int si = find_slot(ctx, layer, e);
+    if (si >= 0 && ctx->buf[si].first_chunk <= resident_chunks(L, e)) ctx->buf[si].use_order = kReserved;
+  }
+  int use_counter = 0;
+  for (int e = 0; e < s.E; ++e) {
+    if (offs[e + 1] == offs[e]) continue;
+    L.st.experts_active += 1;
+    const int res = resident_chunks(L, e);
+    if (res >= s.n_chunks) {
+      L.st.alpha += 1;
+      continue;
+    }
+    if (res > 0)
+      L.st.beta += 1;
+    else
+      L.st.gamma += 1;
+    int si = find_slot(ctx, layer, e);
+    bool hit = false;
+    if (si >= 0 && ctx->buf[si].first_chunk <= res) {
+      for (const Group& g : ctx->buf[si].groups) hit = hit || g.issued;
+    } else {
+      if (si < 0) si = pick_victim(ctx, true);
+      st = assign_slot(ctx, si, layer, e, res);
+      if (st != MS_OK) return st;
+    }
+    if (hit) L.st.buffer_hits += 1;
+    BufSlot& b = ctx->buf[si];
+    b.use_order = use_counter++;
+    b.tick = ++ctx->tick;
+    for (int gi = 0; gi < static_cast<int>(b.groups.size()); ++gi) {
+      Group& g = b.groups[gi];
+      const int lo = std::max(g.c_lo, res);
+      if (lo >= g.c_hi) continue;
+      if (!g.issued) {
+        st = issue_group(ctx, si, gi, false);
+        if (st != MS_OK) return st;
+      } else if (g.prefetch && !g.used) {
+        L.st.bytes_prefetch_used += s.chunk_bytes * (g.c_hi - g.c_lo);
+      }
+      g.used = true;
+      MS_HIP(hipStreamWaitEvent(ctx->side, b.gev[gi], 0));
+      fa.n_tasks = 1;
+      fa.tasks[0].base = b.base;
+      fa.tasks[0].expert = e;
+      fa.tasks[0].chunk_lo = lo;
+      fa.tasks[0].n_chunks = g.c_hi - lo;
+      fa.tasks[0].wg_begin = 0;
+      fa.n_wg = g.c_hi - lo;
+      ti = tl_begin(ctx, ctx->side, MS_IV_FFN_STREAMED, layer, s.chunk_bytes * (g.c_hi - lo));
+      MS_HIP(msk::launch_ffn(fa, offs[e + 1] - offs[e], ctx->side));
+      tl_end(ctx, ti, ctx->side);
+    }
+    MS_HIP(hipEventRecord(b.last_read, ctx->side));
+    b.has_last_read = true;
+  }
+  MS_HIP(hipEventRecord(ctx->ev_side_done, ctx->side));
+  MS_HIP(hipStreamWaitEvent(sm, ctx->ev_side_done, 0));
+
+  // 6. combine (Eq. (2) weighted sum, fixed order)
+  msk::CombineArgs ca{};
+  ca.part = d_part;
+  ca.part_sh = d_part_sh;
+  ca.pos = d_pos;
+  ca.w = w_dev;
+  ca.y = y_dev;
+  ca.sh_plane = s.sh_plane;
+  ca.rows_routed = rows_routed;
+  ca.rows_shared = s.max_T;
+  ca.n_chunks = s.n_chunks;
+  ca.n_chunks_sh = s.n_chunks_sh;
+  ca.n_shared = s.n_sh;
+  ca.T = T;
+  ca.K = s.K;
+  ca.d = s.d;
+  ti = tl_begin(ctx, sm, MS_IV_COMBINE, layer, 0);
+  MS_HIP(msk::launch_combine(ca, sm));
+  tl_end(ctx, ti, sm);
+  MS_HIP(hipEventRecord(L.last_fwd, sm));
+  L.has_last_fwd = true;
+  MS_HIP(hipEventRecord(ctx->ev_last, sm));
+  ctx->has_last = true;
+  ctx->last_stream = sm;
+
+  // 7. speculative prefetch of the next layer, predicted order (Sec. 3.2)
+  if (predict_next) {
+    LayerState& N = ctx->layers[next_layer];
+    N.pred_order = pred;
+    N.has_pred = true;
+    if (N.configured) {
+      st = enqueue_prefetch(ctx, next_layer, pred.data(), static_cast<int>(pred.size()));
+      if (st != MS_OK) return st;
+    }
+  }
+  for (BufSlot& b : ctx->buf) b.use_order = -1;
+  return MS_OK;
+}
+
+ms_status ms_stats(ms_ctx* ctx, int32_t layer, ms_layer_stats* out) {
+  MS_CHECK_CTX(ctx);
+  ms_status st = check_layer(ctx, layer);
+  if (st != MS_OK) return st;
+  if (!out) return fail(ctx, MS_E_INVALID, "out is NULL");
+  *out = ctx->layers[layer].st;
+  return MS_OK;
+}
+
+ms_status ms_reset_stats(ms_ctx* ctx) {
+  MS_CHECK_CTX(ctx);
+  for (LayerState& L : ctx->layers) L.st = ms_layer_stats{};
+  return MS_OK;
+}
+
+ms_status ms_timeline_begin(ms_ctx* ctx, void* stream, int32_t capacity) {
+  MS_CHECK_CTX(ctx);
+  if (capacity <= 0) return fail(ctx, MS_E_INVALID, "capacity must be positive");
+  if (ctx->tl_on) return fail(ctx, MS_E_STATE, "timeline already running");
+  for (TlRec& r : ctx->tl) {
+    ctx->tl_pool.push_back(r.e0);
+    ctx->tl_pool.push_back(r.e1);
+  }
+  ctx->tl.clear();
+  if (!ctx->tl_origin) MS_HIP(hipEventCreate(&ctx->tl_origin));
+  MS_HIP(hipEventRecord(ctx->tl_origin, static_cast<hipStream_t>(stream)));
+  ctx->tl_on = true;
+  ctx->tl_cap = capacity;
+  return MS_OK;
+}
+
+ms_status ms_timeline_end(ms_ctx* ctx, ms_interval* out, int32_t cap, int32_t* n_out) {
+  MS_CHECK_CTX(ctx);
+  if (!ctx->tl_on) return fail(ctx, MS_E_STATE, "timeline not running");
+  ms_status st = ms_sync(ctx);
+  if (st != MS_OK) return st;
+  MS_HIP(hipEventSynchronize(ctx->tl_origin));
+  int n = 0;
+  for (const TlRec& r : ctx->tl) {
+    MS_HIP(hipEventSynchronize(r.e1));
+    if (out && n < cap) {
+      float a = 0.f, b = 0.f;
+      MS_HIP(hipEventElapsedTime(&a, ctx->tl_origin, r.e0));
+      MS_HIP(hipEventElapsedTime(&b, ctx->tl_origin, r.e1));
+      out[n].kind = r.kind;
+      out[n].layer = r.layer;
+      out[n].t0_ms = a;
+      out[n].t1_ms = b;
+      out[n].bytes = r.bytes;
+      ++n;
+    }
+  }
+  if (n_out) *n_out = n;
+  ctx->tl_on = false;
+  return MS_OK;
+}
+
+}  // extern "C"
