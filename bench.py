@@ -1,0 +1,282 @@
+"""Benchmark of the split-expert MoE layer on one MI355X.
+
+Workload: the Mixtral-8x7B-shaped MoE layer (d=4096, F=14336, E=8, top-2,
+bf16 weights, fp32 accumulation), decode batch 1, split ratio r=0.5 with the
+top segments of experts 0-3 cached in the VRAM pool and every other segment
+in pinned host RAM.  One step = one decode token through the whole hot path:
+routing + next-layer prediction, grouping, residency resolution and miss
+transfers, resident-segment FFN, streamed-segment FFN, combine, and the
+speculative prefetch for the next token (a one-layer model predicts its own
+next pass).  Inputs are a seeded correlated sequence of N(0,1) tokens, all
+resident in HBM before timing starts.
+
+Prints one JSON line: value = MoE-layer latency in us per layer (lower is
+better); plus the dominant kernel's roofline from HIP events over the timed
+region, H2D bandwidth and overlap figures from the same events, an
+all-resident (r=1) variant that isolates the HBM-bound expert read, and the
+CPU oracle timed on a bounded sample.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBPS = 8000.0
+METRIC = "MoE-layer decode µs/layer + achieved HBM GB/s; H2D overlap % at fixed VRAM budget"
+KERNEL_KINDS = ("router", "group", "predict", "ffn_resident", "ffn_streamed", "combine")
+COPY_KINDS = ("copy_miss", "copy_prefetch")
+
+
+# ------------------------------------------------------------ interval math
+
+def _union(iv):
+    iv = sorted((a, b) for a, b in iv if b > a)
+    out = []
+    for a, b in iv:
+        if out and a <= out[-1][1]:
+            out[-1][1] = max(out[-1][1], b)
+        else:
+            out.append([a, b])
+    return out
+
+
+def _length(u):
+    return sum(b - a for a, b in u)
+
+
+def _intersect(u, v):
+    i = j = 0
+    tot = 0.0
+    while i < len(u) and j < len(v):
+        a, b = max(u[i][0], v[j][0]), min(u[i][1], v[j][1])
+        if b > a:
+            tot += b - a
+        if u[i][1] < v[j][1]:
+            i += 1
+        else:
+            j += 1
+    return tot
+
+
+def analyse(tl, steps, ms_per_step):
+    by = {}
+    for r in tl:
+        by.setdefault(r["kind"], []).append(r)
+    kern = {}
+    for k in KERNEL_KINDS:
+        rs = by.get(k, [])
+        dur = sum(r["t1_ms"] - r["t0_ms"] for r in rs)
+        kern[k] = dict(launches=len(rs), total_ms=dur, bytes=sum(r["bytes"] for r in rs))
+    copies = [r for k in COPY_KINDS for r in by.get(k, [])]
+    copy_u = _union([(r["t0_ms"], r["t1_ms"]) for r in copies])
+    kern_u = _union([(r["t0_ms"], r["t1_ms"]) for k in KERNEL_KINDS for r in by.get(k, [])])
+    copy_t, kern_t = _length(copy_u), _length(kern_u)
+    both = _intersect(copy_u, kern_u)
+    copy_bytes = sum(r["bytes"] for r in copies)
+    t_layer = ms_per_step * steps
+    eta = None
+    if copy_t > 0 and kern_t > 0:
+        eta = (kern_t + copy_t - t_layer) / min(kern_t, copy_t)
+    return dict(
+        kernels=kern,
+        copy_ms=copy_t, kernel_ms=kern_t, copy_bytes=copy_bytes,
+        h2d_gbps=(copy_bytes / (copy_t * 1e-3) / 1e9) if copy_t > 0 else None,
+        hidden_frac=(both / copy_t) if copy_t > 0 else None,
+        compute_hidden_frac=(both / kern_t) if kern_t > 0 else None,
+        overlap_eta=eta,
+        miss_bytes=sum(r["bytes"] for r in by.get("copy_miss", [])),
+        prefetch_bytes=sum(r["bytes"] for r in by.get("copy_prefetch", [])),
+    )
+
+
+def ffn_roofline(an):
+    """SwiGLU chunk kernel (resident and streamed launches are the same
+    kernel): weight bytes read per launch / average launch duration."""
+    ks = [an["kernels"]["ffn_resident"], an["kernels"]["ffn_streamed"]]
+    n = sum(k["launches"] for k in ks)
+    ms_tot = sum(k["total_ms"] for k in ks)
+    b = sum(k["bytes"] for k in ks)
+    if n == 0 or ms_tot <= 0:
+        return None
+    gbps = b / (ms_tot * 1e-3) / 1e9
+    return dict(bound="hbm", achieved=round(gbps, 1), peak=HBM_PEAK_GBPS, unit="GB/s",
+                frac=round(gbps / HBM_PEAK_GBPS, 4), traffic=None,
+                launches=n, avg_launch_us=round(ms_tot / n * 1e3, 2),
+                bytes_per_launch=int(b / n))
+
+
+# ------------------------------------------------------------------ timing
+
+def run_steps(rig, hs, steps, warmup, flags, timeline=True):
+    import torch
+    from paper_2509_08342_amd import moesplit as ms
+    stream = torch.cuda.current_stream()
+    y, idx, w = rig.outputs(1)
+    for i in range(warmup):
+        rig.forward(0, hs[i % len(hs)], 1, y, idx, w, flags, stream)
+    ms.ms_sync(rig.ctx)
+    torch.cuda.synchronize()
+    ms.ms_reset_stats(rig.ctx)
+    if timeline:
+        ms.ms_timeline_begin(rig.ctx, stream, 1 << 16)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(steps):
+        rig.forward(0, hs[(warmup + i) % len(hs)], 1, y, idx, w, flags, stream)
+    ms.ms_sync(rig.ctx)
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    tl = ms.ms_timeline_end(rig.ctx) if timeline else []
+    st = ms.ms_stats(rig.ctx, 0)
+    return (t1 - t0) * 1e3 / steps, tl, st
+
+
+def h2d_link_peak_gbps():
+    import torch
+    n = 1 << 30
+    hbuf = torch.empty(n, dtype=torch.uint8, pin_memory=True)
+    dbuf = torch.empty(n, dtype=torch.uint8, device="cuda")
+    s = torch.cuda.Stream()
+    with torch.cuda.stream(s):
+        dbuf.copy_(hbuf, non_blocking=True)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(s)
+        for _ in range(3):
+            dbuf.copy_(hbuf, non_blocking=True)
+        e1.record(s)
+    torch.cuda.synchronize()
+    ms_ = e0.elapsed_time(e1) / 3
+    del hbuf, dbuf
+    return n / (ms_ * 1e-3) / 1e9
+
+
+def cpu_baseline(rig, hf_list, budget_s):
+    """The oracle as it stands, one thread, on as many decode tokens of the
+    same layer as fit in about budget_s seconds."""
+    import oracle
+    s = rig.shape
+    t0 = time.perf_counter()
+    n = 0
+    for hf in hf_list:
+        oracle.moe_layer(hf, rig.routers[0], rig.layer_experts(0), s.top_k,
+                         renormalize=s.renormalize, bias=rig.biases[0], shared=rig.shared[0])
+        n += 1
+        if time.perf_counter() - t0 > budget_s:
+            break
+    dt = time.perf_counter() - t0
+    return dict(value=round(dt / n * 1e6, 1), unit="us/layer", cores=1, kind="oracle",
+                sample="%d decode tokens of the Mixtral-shaped layer (router + 2 experts, fp64)" % n)
+
+
+def log(msg):
+    print("[bench] " + msg, file=sys.stderr, flush=True)
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=32)
+    ap.add_argument("--warmup", type=int, default=4)
+    ap.add_argument("--cpu-seconds", type=float, default=12.0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-all-resident", action="store_true")
+    ap.add_argument("--timeline-out", default=None)
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print("bench.py measures one GPU: this build of the split-expert layer has no "
+              "multi-GPU path; run with --gpus 1", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import synth
+    from paper_2509_08342_amd import moesplit as ms
+    from workload import SplitRig, to_device, top_bytes
+
+    torch.cuda.set_device(0)
+    shape = synth.MIXTRAL
+    t_setup = time.perf_counter()
+    log("generating %s weights and filling the pinned store" % shape.name)
+    rig = SplitRig(shape, seed=0, max_tokens=1, budget_bytes=shape.n_experts * shape.expert_bytes,
+                   keep_f32=not args.no_cpu_baseline, threads=16)
+    n_tok = args.warmup + args.steps
+    seq = synth.walk(shape, 0, n_tok, T=1)
+    hs = [to_device(raw, shape.dtype) for raw, _ in seq]
+    torch.cuda.synchronize()
+    setup_s = time.perf_counter() - t_setup
+
+    log("setup done in %.1f s; timing the split layer" % setup_s)
+    # headline: r = 0.5, tops of experts 0-3 cached (C = 4), rest in host RAM
+    slots = rig.configure([4 * top_bytes(rig, 0.5)], [0.5])
+    rig.load_tops(0, [0, 1, 2, 3])
+    ms.ms_sync(rig.ctx)
+    ms_step, tl, st = run_steps(rig, hs, args.steps, args.warmup, ms.MS_FWD_PREDICT_NEXT)
+    an = analyse(tl, args.steps, ms_step)
+    roof = ffn_roofline(an)
+    if args.timeline_out:
+        with open(args.timeline_out, "w") as f:
+            json.dump(dict(split=tl), f)
+
+    out = {
+        "metric": METRIC,
+        "value": round(ms_step * 1e3, 1),
+        "unit": "us/layer",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 4),
+        "higher_is_better": False,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": "mixtral-8x7b-shaped MoE layer, decode T=1, r=0.5, tops of experts "
+                               "0-3 cached (C=%d), other segments in pinned host RAM, prediction + "
+                               "prefetch on" % int(slots[0]),
+                   "d_model": shape.d_model, "d_ff": shape.d_ff, "n_experts": shape.n_experts,
+                   "top_k": shape.top_k, "r": 0.5, "tokens_per_step": 1},
+        "roofline": roof,
+        "tokens_per_s": round(1e3 / ms_step, 2),
+        "h2d_gbps": None if an["h2d_gbps"] is None else round(an["h2d_gbps"], 2),
+        "overlap": {"h2d_hidden_frac": an["hidden_frac"], "compute_hidden_frac": an["compute_hidden_frac"],
+                    "eta": an["overlap_eta"], "copy_ms_per_step": an["copy_ms"] / args.steps,
+                    "kernel_ms_per_step": an["kernel_ms"] / args.steps},
+        "h2d_bytes_per_step": {"miss": an["miss_bytes"] // args.steps,
+                               "prefetch": an["prefetch_bytes"] // args.steps},
+        "stats": st,
+        "kernels": {k: {"launches": v["launches"], "avg_us": round(v["total_ms"] / v["launches"] * 1e3, 2)
+                        if v["launches"] else None} for k, v in an["kernels"].items()},
+        "setup_s": round(setup_s, 1),
+    }
+    out["h2d_link_peak_gbps"] = round(h2d_link_peak_gbps(), 2)
+
+    log("split layer: %.3f ms/step" % ms_step)
+    if not args.no_all_resident:
+        # all eight experts whole in VRAM (r = 1): the expert read is HBM-bound
+        rig.configure([shape.n_experts * shape.expert_bytes], [1.0])
+        rig.load_tops(0, range(shape.n_experts))
+        ms.ms_sync(rig.ctx)
+        ms_ar, tl_ar, _ = run_steps(rig, hs, args.steps, args.warmup, ms.MS_FWD_PREDICT_NEXT)
+        an_ar = analyse(tl_ar, args.steps, ms_ar)
+        out["all_resident"] = {"us_per_layer": round(ms_ar * 1e3, 1), "roofline": ffn_roofline(an_ar),
+                               "kernels": {k: {"launches": v["launches"],
+                                               "avg_us": round(v["total_ms"] / v["launches"] * 1e3, 2)
+                                               if v["launches"] else None}
+                                           for k, v in an_ar["kernels"].items()}}
+    log("all-resident variant done")
+    if not args.no_cpu_baseline:
+        log("timing the CPU oracle")
+        out["cpu_baseline"] = cpu_baseline(rig, [f for _, f in seq], args.cpu_seconds)
+    rig.close()
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -133,39 +133,58 @@ void orc_gate_weights(const float *logits, const int32_t *idx, int T, int E,
 
 static double silu(double x) { return x / (1.0 + exp(-x)); }
 
+/* Gate and up dot products of one token for units f in [lo,hi):
+ * g[f-lo] = sum_j h[j] w_gate[j][f], u[f-lo] = sum_j h[j] w_up[j][f], each
+ * summed over j in ascending order (rows of the weights are walked in
+ * storage order, which does not change any sum). */
+static void gate_up(const float *h, const float *w_gate, const float *w_up,
+                    int d, int F, int lo, int hi, double *g, double *u) {
+  int n = hi - lo;
+  for (int i = 0; i < n; ++i) g[i] = u[i] = 0.0;
+  for (int j = 0; j < d; ++j) {
+    double hj = (double)h[j];
+    const float *gr = w_gate + (size_t)j * F + lo;
+    const float *ur = w_up + (size_t)j * F + lo;
+    for (int i = 0; i < n; ++i) {
+      g[i] += hj * (double)gr[i];
+      u[i] += hj * (double)ur[i];
+    }
+  }
+}
+
 /* Range form of one expert for one token: acc[c] += sum_{f in [lo,hi)}
- * silu(h.G_f) * (h.U_f) * w_down[f][c], units f in ascending order, every dot
- * product summed sequentially over j.  Calling it on [0,F) gives E(h); calling
- * it on [0,F_top) and then on [F_top,F) with the same accumulator reproduces
- * E(h) exactly (the top segment's result continued by the bottom's), which is
- * how the split of Sec. 3.1 leaves the output unchanged. */
+ * silu(h.G_f) * (h.U_f) * w_down[f][c], units f in ascending order.  Calling
+ * it on [0,F) gives E(h); calling it on [0,F_top) and then on [F_top,F) with
+ * the same accumulator reproduces E(h) exactly (the top segment's result
+ * continued by the bottom's), which is how the split of Sec. 3.1 leaves the
+ * output unchanged. */
 void orc_expert_range(const float *h, const float *w_gate, const float *w_up,
                       const float *w_down, int d, int F, int lo, int hi,
                       double *acc) {
+  if (hi <= lo) return;
+  double *g = (double *)malloc(sizeof(double) * (size_t)(hi - lo));
+  double *u = (double *)malloc(sizeof(double) * (size_t)(hi - lo));
+  gate_up(h, w_gate, w_up, d, F, lo, hi, g, u);
   for (int f = lo; f < hi; ++f) {
-    double g = 0.0, u = 0.0;
-    for (int j = 0; j < d; ++j) {
-      g += (double)h[j] * (double)w_gate[(size_t)j * F + f];
-      u += (double)h[j] * (double)w_up[(size_t)j * F + f];
-    }
-    double a = silu(g) * u;
+    double a = silu(g[f - lo]) * u[f - lo];
     const float *dr = w_down + (size_t)f * d;
     for (int c = 0; c < d; ++c) acc[c] += a * (double)dr[c];
   }
+  free(g);
+  free(u);
 }
 
 /* The SwiGLU intermediate activations a_f = silu(h.G_f) * (h.U_f) of one
  * token for f in [lo,hi), written to a[f-lo]. */
 void orc_expert_act(const float *h, const float *w_gate, const float *w_up,
                     int d, int F, int lo, int hi, double *a) {
-  for (int f = lo; f < hi; ++f) {
-    double g = 0.0, u = 0.0;
-    for (int j = 0; j < d; ++j) {
-      g += (double)h[j] * (double)w_gate[(size_t)j * F + f];
-      u += (double)h[j] * (double)w_up[(size_t)j * F + f];
-    }
-    a[f - lo] = silu(g) * u;
-  }
+  if (hi <= lo) return;
+  double *g = (double *)malloc(sizeof(double) * (size_t)(hi - lo));
+  double *u = (double *)malloc(sizeof(double) * (size_t)(hi - lo));
+  gate_up(h, w_gate, w_up, d, F, lo, hi, g, u);
+  for (int f = lo; f < hi; ++f) a[f - lo] = silu(g[f - lo]) * u[f - lo];
+  free(g);
+  free(u);
 }
 
 /* ----------------------------------------------------------------- layer -- */
