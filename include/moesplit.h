@@ -63,7 +63,10 @@ typedef enum { MS_F32 = 0, MS_BF16 = 1 } ms_dtype;
  * renormalize = 1 divides the selected scores by their sum as in Eq. (2).
  * max_tokens bounds T of every forward; n_buffer_slots is the number of
  * full-expert slots of the VRAM staging buffer U_b (0 -> 2*top_k: one set for
- * the running layer, one for the next layer's prefetch). */
+ * the running layer, one for the next layer's prefetch).  ffn_splits is the
+ * number of work-groups that share one 64-unit chunk of the FFN kernel (1, 2
+ * or 4; 0 -> chosen from the shape so that a decode step fills the GPU).  It
+ * changes the summation grouping, not what is computed. */
 typedef struct {
   int32_t n_layers;
   int32_t d_model;
@@ -76,6 +79,7 @@ typedef struct {
   int32_t renormalize;
   int32_t max_tokens;
   int32_t n_buffer_slots;
+  int32_t ffn_splits;
 } ms_model_desc;
 
 /* Sizes the library derives from a model shape (pure host arithmetic). */

@@ -54,77 +54,210 @@ __device__ __forceinline__ void load16(const uint16_t* p, float (&o)[8]) {
   o[7] = __uint_as_float(v.w & 0xffff0000u);
 }
 
+__device__ __forceinline__ uint4 ld16(const void* p) { return *reinterpret_cast<const uint4*>(p); }
+
+#ifndef MSK_NT_LOADS
+#define MSK_NT_LOADS 0
+#endif
+typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
+// 16-byte load of expert weights, which are streamed once per forward.
+__device__ __forceinline__ uint4 ldw16(const void* p) {
+#if MSK_NT_LOADS
+  const u32x4_t v = __builtin_nontemporal_load(reinterpret_cast<const u32x4_t*>(p));
+  return make_uint4(v.x, v.y, v.z, v.w);
+#else
+  return *reinterpret_cast<const uint4*>(p);
+#endif
+}
+
+__device__ __forceinline__ void unpack(const uint4 v, float (&o)[4]) {
+  o[0] = __uint_as_float(v.x);
+  o[1] = __uint_as_float(v.y);
+  o[2] = __uint_as_float(v.z);
+  o[3] = __uint_as_float(v.w);
+}
+__device__ __forceinline__ void unpack(const uint4 v, float (&o)[8]) {
+  o[0] = __uint_as_float(v.x << 16);
+  o[1] = __uint_as_float(v.x & 0xffff0000u);
+  o[2] = __uint_as_float(v.y << 16);
+  o[3] = __uint_as_float(v.y & 0xffff0000u);
+  o[4] = __uint_as_float(v.z << 16);
+  o[5] = __uint_as_float(v.z & 0xffff0000u);
+  o[6] = __uint_as_float(v.w << 16);
+  o[7] = __uint_as_float(v.w & 0xffff0000u);
+}
+
 __device__ __forceinline__ float silu(float x) { return x / (1.0f + expf(-x)); }
 
-// ------------------------------------------------------------------- router
+// ------------------------------------------------------------------- logits
 //
-// One wave per token.  A logit is computed in the fixed fp32 order that makes
-// the selection reproducible: lane l accumulates h[j] * w[j][e] with fma over
+// A logit is computed in the fixed fp32 order that makes the selection
+// reproducible: lane l accumulates h[j] * w[j][e] with fma over
 // j = l, l+64, ... ascending, then lane partials are added in a halving tree
 // that pairs lane l with lane l+s for s = 32, 16, ..., 1 (lane 0 ends with
 // the result); a bias is added once afterwards.
+//
+// Work-group = 4 waves = 4 tokens x one block of 8 experts of one router.
+// The block's weight columns are staged in LDS tile by tile (all 256 threads
+// load), then each wave runs its token's fma chains from LDS.
 
-constexpr int kRouterWaves = 4;
-constexpr int kLogitBlock = 16;  // experts accumulated per pass over h
+constexpr int kLgWaves = 4;
+constexpr int kLgBlock = 8;           // experts per work-group
+constexpr int kLgTileBytes = 32768;   // LDS tile of router rows
 
 template <typename W>
-__device__ void wave_logits(const W* __restrict__ hrow, const W* __restrict__ wr,
-                            const float* __restrict__ bias, int d, int E,
-                            float* __restrict__ out /* LDS [E] */) {
-  const int lane = threadIdx.x & 63;
-  for (int e0 = 0; e0 < E; e0 += kLogitBlock) {
-    const int ne = min(kLogitBlock, E - e0);
-    float acc[kLogitBlock];
+__global__ __launch_bounds__(64 * kLgWaves) void logits_kernel(LogitsArgs a) {
+  __shared__ __align__(16) W tile[kLgTileBytes / sizeof(W)];
+  constexpr int RT = kLgTileBytes / (kLgBlock * sizeof(W));  // rows per tile (multiple of 64)
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int nb = (a.E + kLgBlock - 1) / kLgBlock;
+  const int mat = blockIdx.y / nb, eb = blockIdx.y - mat * nb;
+  const W* wr = static_cast<const W*>(mat == 0 ? a.wr : a.wr2);
+  const float* bias = mat == 0 ? a.bias : a.bias2;
+  float* out = mat == 0 ? a.logits : a.logits2;
+  const int e0 = eb * kLgBlock, ne = min(kLgBlock, a.E - e0);
+  const bool vec = (ne == kLgBlock) && ((a.E * static_cast<int>(sizeof(W))) % 16 == 0);
+  const int t = blockIdx.x * kLgWaves + wave;
+  const bool active = t < a.T;
+  const W* hrow = static_cast<const W*>(a.h) + static_cast<size_t>(active ? t : 0) * a.d;
+  float acc[kLgBlock];
 #pragma unroll
-    for (int q = 0; q < kLogitBlock; ++q) acc[q] = 0.0f;
-    for (int j = lane; j < d; j += 64) {
-      const float hj = to_f32(hrow[j]);
-      const W* row = wr + static_cast<size_t>(j) * E + e0;
+  for (int q = 0; q < kLgBlock; ++q) acc[q] = 0.0f;
+
+  constexpr int NV = static_cast<int>(kLgBlock * sizeof(W)) / 16;  // 16-byte pieces per tile row
+  constexpr int RB = RT / (64 * kLgWaves);                           // tile rows per thread
+  for (int j0 = 0; j0 < a.d; j0 += RT) {
+    const int rows = min(RT, a.d - j0);
+    if (vec) {
+      // all of this thread's row loads first, then the LDS stores
+      uint4 buf[RB][NV];
 #pragma unroll
-      for (int q = 0; q < kLogitBlock; ++q)
-        if (q < ne) acc[q] = fmaf(hj, to_f32(row[q]), acc[q]);
+      for (int u = 0; u < RB; ++u) {
+        const int r = min(tid + 64 * kLgWaves * u, rows - 1);
+        const uint4* src = reinterpret_cast<const uint4*>(wr + static_cast<size_t>(j0 + r) * a.E + e0);
+#pragma unroll
+        for (int b = 0; b < NV; ++b) buf[u][b] = src[b];
+      }
+#pragma unroll
+      for (int u = 0; u < RB; ++u) {
+        const int r = tid + 64 * kLgWaves * u;
+        if (r < rows) {
+#pragma unroll
+          for (int b = 0; b < NV; ++b) reinterpret_cast<uint4*>(tile + r * kLgBlock)[b] = buf[u][b];
+        }
+      }
+    } else {
+      for (int r = tid; r < rows; r += 64 * kLgWaves) {
+        const W* src = wr + static_cast<size_t>(j0 + r) * a.E + e0;
+#pragma unroll
+        for (int q = 0; q < kLgBlock; ++q) tile[r * kLgBlock + q] = q < ne ? src[q] : W(0);
+      }
     }
+    __syncthreads();
+    if (active) {
+      for (int jb = lane; jb < rows; jb += 64 * 8) {
+        float hv[8];
 #pragma unroll
-    for (int q = 0; q < kLogitBlock; ++q) {
+        for (int u = 0; u < 8; ++u) {
+          const int j = jb + 64 * u;
+          hv[u] = j < rows ? to_f32(hrow[j0 + j]) : 0.0f;
+        }
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+          const int j = jb + 64 * u;
+          if (j < rows) {
+            float wv[kLgBlock];
+#pragma unroll
+            for (int q = 0; q < kLgBlock; ++q) wv[q] = to_f32(tile[j * kLgBlock + q]);
+#pragma unroll
+            for (int q = 0; q < kLgBlock; ++q) acc[q] = fmaf(hv[u], wv[q], acc[q]);
+          }
+        }
+      }
+    }
+    __syncthreads();
+  }
+  if (active) {
+#pragma unroll
+    for (int q = 0; q < kLgBlock; ++q) {
       float v = acc[q];
 #pragma unroll
       for (int s = 32; s >= 1; s >>= 1) v = v + __shfl_down(v, s, 64);
       if (lane == 0 && q < ne) {
         if (bias != nullptr) v = v + bias[e0 + q];
-        out[e0 + q] = v;
+        out[static_cast<size_t>(t) * a.E + e0 + q] = v;
       }
     }
   }
 }
 
-template <typename W>
-__global__ __launch_bounds__(64 * kRouterWaves) void router_kernel(RouterArgs a) {
-  extern __shared__ __align__(16) float rl_smem[];
-  const int wave = threadIdx.x >> 6;
-  const int lane = threadIdx.x & 63;
-  const int t = blockIdx.x * kRouterWaves + wave;
-  const bool active = t < a.T;  // no early return: the block syncs below
-  float* logits = rl_smem + wave * a.E;
-  const W* hrow = static_cast<const W*>(a.h) + static_cast<size_t>(active ? t : 0) * a.d;
+hipError_t launch_logits(const LogitsArgs& a, hipStream_t s) {
+  if (a.T <= 0) return hipSuccess;
+  const int nb = (a.E + kLgBlock - 1) / kLgBlock;
+  const int mats = (a.wr != nullptr ? 1 : 0) + (a.wr2 != nullptr ? 1 : 0);
+  if (mats == 0) return hipSuccess;
+  LogitsArgs b = a;
+  if (a.wr == nullptr) {  // only the second router: move it to slot 0
+    b.wr = a.wr2;
+    b.bias = a.bias2;
+    b.logits = a.logits2;
+    b.wr2 = nullptr;
+  }
+  const dim3 grid((a.T + kLgWaves - 1) / kLgWaves, nb * mats);
+  if (a.dtype == kBF16)
+    hipLaunchKernelGGL(logits_kernel<uint16_t>, grid, dim3(64 * kLgWaves), 0, s, b);
+  else
+    hipLaunchKernelGGL(logits_kernel<float>, grid, dim3(64 * kLgWaves), 0, s, b);
+  return hipGetLastError();
+}
 
-  if (a.wr != nullptr) {
-    if (active) wave_logits<W>(hrow, static_cast<const W*>(a.wr), a.bias, a.d, a.E, logits);
-    __syncthreads();
-    if (active) {
-      // K rounds of wave argmax over the untaken experts: the larger logit
-      // wins, the lower index on equal logits.
-      uint64_t taken = 0;  // bit q: expert lane + 64 q taken (E <= 4096)
+// -------------------------------------------------------------------- route
+//
+// One work-group of 16 waves:
+//  1. selection, one wave per token: K rounds of wave argmax over the
+//     untaken experts (larger logit wins, the lower index on equal logits,
+//     NaN ranks last), then the Eq. (2) weights from exp(logit - max);
+//  2. grouping: stable counting sort of the T*K slots by expert --
+//     histogram, exclusive scan, then blocks of 1024 slots placed in slot
+//     order (within a wave by ballot rank, across waves by per-wave counts);
+//  3. ranking of the prediction: per-token softmax of the second logits,
+//     summed over tokens (per wave, then over waves in order), experts
+//     ordered by descending score, lower index first on equal scores.
+
+constexpr int kRouteThreads = 1024;
+constexpr int kRouteWaves = kRouteThreads / 64;
+constexpr int kLanesQ = kMaxExperts / 64;  // expert values held per lane
+
+__global__ __launch_bounds__(kRouteThreads) void route_kernel(RouteArgs a) {
+  __shared__ int base[kMaxExperts];
+  __shared__ float score_s[kMaxExperts];
+  __shared__ int wbuf[kRouteWaves][kMaxExperts];  // per-wave counts / scores
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int E = a.E, K = a.K;
+
+  if (a.logits != nullptr) {
+    // 1. selection
+    for (int t = wave; t < a.T; t += kRouteWaves) {
+      const float* lg = a.logits + static_cast<size_t>(t) * E;
+      float lv[kLanesQ];
+#pragma unroll
+      for (int q = 0; q < kLanesQ; ++q) {
+        const int e = lane + 64 * q;
+        float v = e < E ? lg[e] : -INFINITY;
+        if (v != v) v = -INFINITY;  // NaN ranks last, so an index is always found
+        lv[q] = v;
+      }
+      uint32_t taken = 0;
       float m = 0.0f, zsel = 0.0f, my_ex = 0.0f;
       int my_idx = 0;
-      for (int k = 0; k < a.K; ++k) {
+      for (int k = 0; k < K; ++k) {
         float bv = -INFINITY;
         int bi = 0x7fffffff;
-        for (int q = 0, e = lane; e < a.E; ++q, e += 64) {
-          if ((taken >> q) & 1ull) continue;
-          float v = logits[e];
-          if (v != v) v = -INFINITY;  // NaN ranks last, so an index is always found
-          if (v > bv || (v == bv && e < bi)) {
-            bv = v;
+#pragma unroll
+        for (int q = 0; q < kLanesQ; ++q) {
+          const int e = lane + 64 * q;
+          if (e < E && !((taken >> q) & 1u) && (lv[q] > bv || (lv[q] == bv && e < bi))) {
+            bv = lv[q];
             bi = e;
           }
         }
@@ -137,7 +270,7 @@ __global__ __launch_bounds__(64 * kRouterWaves) void router_kernel(RouterArgs a)
             bi = oi;
           }
         }
-        if ((bi & 63) == lane) taken |= 1ull << (bi >> 6);
+        if ((bi & 63) == lane) taken |= 1u << (bi >> 6);
         if (k == 0) m = bv;  // the first pick is the largest logit
         const float ex = expf(bv - m);
         zsel += ex;
@@ -149,176 +282,166 @@ __global__ __launch_bounds__(64 * kRouterWaves) void router_kernel(RouterArgs a)
       float z = zsel;
       if (!a.renormalize) {
         float part = 0.0f;
-        for (int e = lane; e < a.E; e += 64) part += expf(logits[e] - m);
+#pragma unroll
+        for (int q = 0; q < kLanesQ; ++q)
+          if (lane + 64 * q < E) part += expf(lv[q] - m);
 #pragma unroll
         for (int s = 32; s >= 1; s >>= 1) part += __shfl_xor(part, s, 64);
         z = part;
       }
-      if (lane < a.K) {
-        a.idx[static_cast<size_t>(t) * a.K + lane] = my_idx;
-        a.w[static_cast<size_t>(t) * a.K + lane] = my_ex / z;
+      if (lane < K) {
+        a.idx[static_cast<size_t>(t) * K + lane] = my_idx;
+        a.w[static_cast<size_t>(t) * K + lane] = my_ex / z;
       }
     }
+    __threadfence();
     __syncthreads();
+
+    // 2. grouping
+    const int TK = a.T * K;
+    int* cnt = &wbuf[0][0];
+    for (int e = tid; e < E; e += kRouteThreads) cnt[e] = 0;
+    __syncthreads();
+    // indices lie in [0, E) (selection above); the clamp only keeps LDS
+    // accesses in bounds whatever the input
+    for (int s = tid; s < TK; s += kRouteThreads) atomicAdd(&cnt[min(max(a.idx[s], 0), E - 1)], 1);
+    __syncthreads();
+    if (tid == 0) {
+      int run = 0;
+      for (int e = 0; e < E; ++e) {
+        base[e] = run;
+        a.offsets[e] = run;
+        if (a.host_offsets) a.host_offsets[e] = run;
+        run += cnt[e];
+      }
+      a.offsets[E] = run;
+      if (a.host_offsets) a.host_offsets[E] = run;
+    }
+    __syncthreads();
+    const uint64_t lt = (lane == 0) ? 0ull : ((~0ull) >> (64 - lane));
+    for (int b0 = 0; b0 < TK; b0 += kRouteThreads) {
+      for (int i = tid; i < kRouteWaves * E; i += kRouteThreads) wbuf[i / E][i % E] = 0;
+      __syncthreads();
+      const int s = b0 + tid;
+      const int e = (s < TK) ? min(max(a.idx[s], 0), E - 1) : -1;
+      int rank = 0;
+      uint64_t pending = __ballot(e >= 0);
+      while (pending) {
+        const int leader = __ffsll(static_cast<unsigned long long>(pending)) - 1;
+        const int le = __shfl(e, leader, 64);
+        const uint64_t same = __ballot(e == le);
+        if (e == le) rank = __popcll(same & lt);
+        if (lane == leader) wbuf[wave][le] = __popcll(same);
+        pending &= ~same;
+      }
+      __syncthreads();
+      if (e >= 0) {
+        int p = base[e] + rank;
+        for (int w2 = 0; w2 < wave; ++w2) p += wbuf[w2][e];
+        a.perm[p] = s;
+        a.pos[s] = p;
+      }
+      __syncthreads();
+      for (int e2 = tid; e2 < E; e2 += kRouteThreads) {
+        int add = 0;
+        for (int w2 = 0; w2 < kRouteWaves; ++w2) add += wbuf[w2][e2];
+        base[e2] += add;
+      }
+      __syncthreads();
+    }
   }
 
-  if (a.wr_next != nullptr) {
-    if (active) wave_logits<W>(hrow, static_cast<const W*>(a.wr_next), a.bias_next, a.d, a.E, logits);
-    __syncthreads();
-    if (active) {
+  if (a.logits_pred != nullptr) {
+    // 3. prediction ranking
+    float acc[kLanesQ];
+#pragma unroll
+    for (int q = 0; q < kLanesQ; ++q) acc[q] = 0.0f;
+    for (int t = wave; t < a.T; t += kRouteWaves) {
+      const float* lg = a.logits_pred + static_cast<size_t>(t) * E;
+      float lv[kLanesQ];
       float m = -INFINITY;
-      for (int e = lane; e < a.E; e += 64) m = fmaxf(m, logits[e]);
+#pragma unroll
+      for (int q = 0; q < kLanesQ; ++q) {
+        const int e = lane + 64 * q;
+        lv[q] = e < E ? lg[e] : -INFINITY;
+        m = fmaxf(m, lv[q]);
+      }
 #pragma unroll
       for (int s = 32; s >= 1; s >>= 1) m = fmaxf(m, __shfl_xor(m, s, 64));
       float z = 0.0f;
-      for (int e = lane; e < a.E; e += 64) z += expf(logits[e] - m);
+#pragma unroll
+      for (int q = 0; q < kLanesQ; ++q) {
+        lv[q] = (lane + 64 * q < E) ? expf(lv[q] - m) : 0.0f;
+        z += lv[q];
+      }
 #pragma unroll
       for (int s = 32; s >= 1; s >>= 1) z += __shfl_xor(z, s, 64);
-      for (int e = lane; e < a.E; e += 64)
-        a.p_pred[static_cast<size_t>(t) * a.E + e] = expf(logits[e] - m) / z;
+#pragma unroll
+      for (int q = 0; q < kLanesQ; ++q) acc[q] += lv[q] / z;
     }
-  }
-}
-
-hipError_t launch_router(const RouterArgs& a, hipStream_t s) {
-  if (a.T <= 0) return hipSuccess;
-  const dim3 grid((a.T + kRouterWaves - 1) / kRouterWaves);
-  const size_t lds = sizeof(float) * kRouterWaves * a.E;
-  if (a.dtype == kBF16)
-    hipLaunchKernelGGL(router_kernel<uint16_t>, grid, dim3(64 * kRouterWaves), lds, s, a);
-  else
-    hipLaunchKernelGGL(router_kernel<float>, grid, dim3(64 * kRouterWaves), lds, s, a);
-  return hipGetLastError();
-}
-
-// ----------------------------------------------------------------- grouping
-//
-// Stable counting sort of the T*K slots by expert in one work-group:
-// histogram, exclusive scan, then blocks of 1024 slots placed in slot order
-// (within a wave by ballot rank, across waves by per-wave counts).
-
-constexpr int kGroupThreads = 1024;
-constexpr int kGroupWaves = kGroupThreads / 64;
-
-__global__ __launch_bounds__(kGroupThreads) void group_kernel(GroupArgs a) {
-  __shared__ int cnt[kMaxExperts];
-  __shared__ int base[kMaxExperts];
-  __shared__ int wcnt[kGroupWaves][kMaxExperts];
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  for (int e = tid; e < a.E; e += kGroupThreads) cnt[e] = 0;
-  __syncthreads();
-  // indices come from the router kernel and lie in [0, E); the clamp only
-  // keeps LDS accesses in bounds whatever the input
-  for (int s = tid; s < a.TK; s += kGroupThreads) atomicAdd(&cnt[min(max(a.idx[s], 0), a.E - 1)], 1);
-  __syncthreads();
-  if (tid == 0) {
-    int run = 0;
-    for (int e = 0; e < a.E; ++e) {
-      base[e] = run;
-      a.offsets[e] = run;
-      if (a.host_offsets) a.host_offsets[e] = run;
-      run += cnt[e];
-    }
-    a.offsets[a.E] = run;
-    if (a.host_offsets) a.host_offsets[a.E] = run;
-  }
-  __syncthreads();
-  const uint64_t lt = (lane == 0) ? 0ull : ((~0ull) >> (64 - lane));
-  for (int b0 = 0; b0 < a.TK; b0 += kGroupThreads) {
-    for (int i = tid; i < kGroupWaves * a.E; i += kGroupThreads) (&wcnt[0][0])[(i / a.E) * kMaxExperts + i % a.E] = 0;
+    float* ws = reinterpret_cast<float*>(&wbuf[0][0]);
     __syncthreads();
-    const int s = b0 + tid;
-    const int e = (s < a.TK) ? min(max(a.idx[s], 0), a.E - 1) : -1;
-    int rank = 0;
-    uint64_t pending = __ballot(e >= 0);
-    while (pending) {
-      const int leader = __ffsll(static_cast<unsigned long long>(pending)) - 1;
-      const int le = __shfl(e, leader, 64);
-      const uint64_t same = __ballot(e == le);
-      if (e == le) rank = __popcll(same & lt);
-      if (lane == leader) wcnt[wave][le] = __popcll(same);
-      pending &= ~same;
+#pragma unroll
+    for (int q = 0; q < kLanesQ; ++q)
+      if (lane + 64 * q < E) ws[wave * kMaxExperts + lane + 64 * q] = acc[q];
+    __syncthreads();
+    for (int e = tid; e < E; e += kRouteThreads) {
+      float sc = 0.0f;
+      for (int w2 = 0; w2 < kRouteWaves && w2 < a.T; ++w2) sc += ws[w2 * kMaxExperts + e];
+      score_s[e] = sc;
     }
     __syncthreads();
-    if (e >= 0) {
-      int p = base[e] + rank;
-      for (int w2 = 0; w2 < wave; ++w2) p += wcnt[w2][e];
-      a.perm[p] = s;
-      a.pos[s] = p;
+    for (int e = tid; e < E; e += kRouteThreads) {
+      const float v = score_s[e];
+      int r = 0;
+      for (int o = 0; o < E; ++o) {
+        const float u = score_s[o];
+        r += (u > v) || (u == v && o < e);
+      }
+      a.order[r] = e;
+      a.score[e] = v;
+      if (a.host_order) a.host_order[r] = e;
+      if (a.host_score) a.host_score[e] = v;
     }
-    __syncthreads();
-    for (int e2 = tid; e2 < a.E; e2 += kGroupThreads) {
-      int add = 0;
-      for (int w2 = 0; w2 < kGroupWaves; ++w2) add += wcnt[w2][e2];
-      base[e2] += add;
-    }
-    __syncthreads();
   }
-  if (a.host_offsets) __threadfence_system();
+  if (a.host_offsets || a.host_order) __threadfence_system();
 }
 
-hipError_t launch_group(const GroupArgs& a, hipStream_t s) {
-  hipLaunchKernelGGL(group_kernel, dim3(1), dim3(kGroupThreads), 0, s, a);
-  return hipGetLastError();
-}
-
-// ------------------------------------------------------ prediction ranking
-
-constexpr int kRankThreads = 1024;
-
-__global__ __launch_bounds__(kRankThreads) void rank_kernel(RankArgs a) {
-  __shared__ float part[kRankThreads];
-  __shared__ float score[kMaxExperts];
-  const int tid = threadIdx.x;
-  int epad = 1;
-  while (epad < a.E) epad <<= 1;
-  const int G = kRankThreads / epad;  // token groups (>= 2 for E <= 512)
-  const int e = tid % epad, g = tid / epad;
-  float acc = 0.0f;
-  if (e < a.E && g < G)
-    for (int t = g; t < a.T; t += G) acc += a.p_pred[static_cast<size_t>(t) * a.E + e];
-  part[tid] = acc;
-  __syncthreads();
-  if (tid < a.E) {
-    float s = 0.0f;
-    for (int g2 = 0; g2 < G; ++g2) s += part[g2 * epad + tid];
-    score[tid] = s;
-  }
-  __syncthreads();
-  if (tid < a.E) {
-    const float v = score[tid];
-    int r = 0;
-    for (int o = 0; o < a.E; ++o) {
-      const float u = score[o];
-      r += (u > v) || (u == v && o < tid);
-    }
-    a.order[r] = tid;
-    a.score[tid] = v;
-    if (a.host_order) a.host_order[r] = tid;
-    if (a.host_score) a.host_score[tid] = v;
-  }
-  if (a.host_order) __threadfence_system();
-}
-
-hipError_t launch_rank(const RankArgs& a, hipStream_t s) {
-  hipLaunchKernelGGL(rank_kernel, dim3(1), dim3(kRankThreads), 0, s, a);
+hipError_t launch_route(const RouteArgs& a, hipStream_t s) {
+  hipLaunchKernelGGL(route_kernel, dim3(1), dim3(kRouteThreads), 0, s, a);
   return hipGetLastError();
 }
 
 // --------------------------------------------------------------- SwiGLU FFN
 //
-// One work-group computes one 64-unit chunk c of one expert for all of the
-// expert's tokens, NT tokens at a time:
-//   phase 1: a[t][f] = silu(h_t . G_f) * (h_t . U_f) for the chunk's units f
-//            (8 waves x 8 units, 8 lanes per unit row, 16-byte loads);
-//   phase 2: y[t][:] = sum_f a[t][f] * D_f (each thread owns VEC columns);
-//   writes y as the chunk's fp32 partial row of that token.
-// Chunk layout (model dtype): [G: 64 x d][U: 64 x d][D: 64 x d], rows
-// d-contiguous.  The same code serves resident and streamed chunks.
+// A work-group computes UPW units (one sub-range of a 64-unit chunk c) of one
+// expert for all of the expert's tokens, NT tokens at a time:
+//   phase 1: a[t][f] = silu(h_t . G_f) * (h_t . U_f) for its units f
+//            (8 lanes per unit row, 16-byte loads, batches of kRowBatch
+//            loads per lane issued before use);
+//   phase 2: y[t][:] = sum_f a[t][f] * D_f over its units (each thread owns
+//            VEC columns per pass);
+//   writes y as the fp32 partial row of (token, plane c * subs + sub).
+// Chunk layout (model dtype): [G][U][D], 64 x d elements each.  G and U are
+// k-tiled: element (unit f, k) sits at ((k / 64) * 64 + f) * 64 + k % 64, so
+// the units' pieces of one 64-wide k slice are adjacent; D is row-major
+// (down row f at f * d).  The same code serves resident and streamed chunks,
+// and a given chunk is always split the same way, so its partials do not
+// depend on which launch computed it.
 
-template <typename W, int NT, int Q>
-__global__ __launch_bounds__(kFfnThreads) void ffn_chunk_kernel(FfnArgs a) {
+#ifndef MSK_ROW_BATCH
+#define MSK_ROW_BATCH 4
+#endif
+constexpr int kRowBatch = MSK_ROW_BATCH;  // 16-byte loads per lane and row stream
+constexpr int kLpu = kFfnLanesPerUnit;
+constexpr int kKTile = 64;                // k elements per gate/up piece
+
+template <typename W, int NT, int Q, int UPW>
+__global__ __launch_bounds__(UPW * kLpu) void ffn_chunk_kernel(FfnArgs a) {
   constexpr int VEC = Vec<W>::N;
+  constexpr int THREADS = UPW * kLpu;
+  constexpr int STEP = kLpu * VEC;  // k covered by the lanes of a unit per step
+  static_assert(STEP <= kKTile && kKTile % STEP == 0, "a unit's lanes must tile a k piece");
   extern __shared__ __align__(16) unsigned char ffn_smem[];
   const int d = a.d;
   const int wg = blockIdx.x;
@@ -326,7 +449,9 @@ __global__ __launch_bounds__(kFfnThreads) void ffn_chunk_kernel(FfnArgs a) {
   for (int i = 1; i < a.n_tasks; ++i)
     if (a.tasks[i].wg_begin <= wg) ti = i;
   const FfnTask tk = a.tasks[ti];
-  const int c = tk.chunk_lo + (wg - tk.wg_begin);
+  const int local = wg - tk.wg_begin;
+  const int c = tk.chunk_lo + local / a.subs;
+  const int sub = local % a.subs;
   const bool routed = tk.expert >= 0;
   int p0 = 0, n_tok = a.T;
   if (routed) {
@@ -341,69 +466,87 @@ __global__ __launch_bounds__(kFfnThreads) void ffn_chunk_kernel(FfnArgs a) {
   const W* D = U + cd;
   float* part = routed ? a.part : a.part_sh + static_cast<size_t>(-1 - tk.expert) * a.sh_plane;
   const int rows = routed ? a.rows_routed : a.rows_shared;
+  const int plane = c * a.subs + sub;
 
   W* hs = reinterpret_cast<W*>(ffn_smem);                                  // [NT][d]
-  float* as = reinterpret_cast<float*>(ffn_smem + sizeof(W) * NT * d);     // [NT][64]
+  float* as = reinterpret_cast<float*>(ffn_smem + sizeof(W) * NT * d);     // [NT][UPW]
   const W* hsrc = static_cast<const W*>(a.h);
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int sub = lane & 7, grp = lane >> 3;
-  const int unit = wave * 8 + grp;  // 8 waves x 8 units = 64
+  const int tid = threadIdx.x;
+  const int lane_u = tid % kLpu;           // lane within the unit's lane group
+  const int lu = tid / kLpu;               // unit within this work-group
+  const int unit = sub * UPW + lu;         // unit within the chunk
+  const int f_first = sub * UPW;           // first down row of this work-group
 
   for (int tile = 0; tile < n_tok; tile += NT) {
     const int nt = min(NT, n_tok - tile);
     // stage the tile's activations in LDS (zero rows past nt)
     const int vec_per_row = d / VEC;
-    for (int i = tid; i < NT * vec_per_row; i += kFfnThreads) {
+    for (int i = tid; i < NT * vec_per_row; i += THREADS) {
       const int t = i / vec_per_row, k = (i - t * vec_per_row) * VEC;
       uint4 v = make_uint4(0, 0, 0, 0);
       if (t < nt) {
         const int tok = routed ? a.perm[p0 + tile + t] / a.K : tile + t;
-        v = *reinterpret_cast<const uint4*>(hsrc + static_cast<size_t>(tok) * d + k);
+        v = ld16(hsrc + static_cast<size_t>(tok) * d + k);
       }
       *reinterpret_cast<uint4*>(hs + static_cast<size_t>(t) * d + k) = v;
     }
     __syncthreads();
 
-    // phase 1: gate/up dot products of this wave's 8 units
+    // phase 1: gate/up dot products of this lane group's unit
     {
       float ag[NT], au[NT];
 #pragma unroll
       for (int t = 0; t < NT; ++t) ag[t] = au[t] = 0.0f;
-      const W* grow = G + static_cast<size_t>(unit) * d;
-      const W* urow = U + static_cast<size_t>(unit) * d;
-#pragma unroll 4
-      for (int k0 = sub * VEC; k0 < d; k0 += 8 * VEC) {
-        float gv[VEC], uv[VEC];
-        load16(grow + k0, gv);
-        load16(urow + k0, uv);
+      const int n_steps = d / STEP;
+      for (int s0 = 0; s0 < n_steps; s0 += kRowBatch) {
+        uint4 gr[kRowBatch], ur[kRowBatch];
 #pragma unroll
-        for (int t = 0; t < NT; ++t) {
-          float hv[VEC];
-          load16(hs + static_cast<size_t>(t) * d + k0, hv);
+        for (int u = 0; u < kRowBatch; ++u) {
+          const int sk = (s0 + u) * STEP;  // first k of the step
+          if (s0 + u < n_steps) {
+            const size_t off =
+                (static_cast<size_t>(sk / kKTile) * kChunkUnits + unit) * kKTile + (sk % kKTile) + lane_u * VEC;
+            gr[u] = ldw16(G + off);
+            ur[u] = ldw16(U + off);
+          }
+        }
 #pragma unroll
-          for (int i = 0; i < VEC; ++i) {
-            ag[t] = fmaf(gv[i], hv[i], ag[t]);
-            au[t] = fmaf(uv[i], hv[i], au[t]);
+        for (int u = 0; u < kRowBatch; ++u) {
+          if (s0 + u < n_steps) {
+            const int k = (s0 + u) * STEP + lane_u * VEC;
+            float gv[VEC], uv[VEC];
+            unpack(gr[u], gv);
+            unpack(ur[u], uv);
+#pragma unroll
+            for (int t = 0; t < NT; ++t) {
+              float hv[VEC];
+              unpack(ld16(hs + static_cast<size_t>(t) * d + k), hv);
+#pragma unroll
+              for (int i = 0; i < VEC; ++i) {
+                ag[t] = fmaf(gv[i], hv[i], ag[t]);
+                au[t] = fmaf(uv[i], hv[i], au[t]);
+              }
+            }
           }
         }
       }
 #pragma unroll
       for (int t = 0; t < NT; ++t) {
 #pragma unroll
-        for (int s = 1; s <= 4; s <<= 1) {
+        for (int s = 1; s < kLpu; s <<= 1) {
           ag[t] += __shfl_xor(ag[t], s, 64);
           au[t] += __shfl_xor(au[t], s, 64);
         }
       }
-      if (sub == 0) {
+      if (lane_u == 0) {
 #pragma unroll
-        for (int t = 0; t < NT; ++t) as[t * kChunkUnits + unit] = silu(ag[t]) * au[t];
+        for (int t = 0; t < NT; ++t) as[t * UPW + lu] = silu(ag[t]) * au[t];
       }
     }
     __syncthreads();
 
-    // phase 2: partial down-projection of the chunk
+    // phase 2: partial down-projection over this work-group's units
     {
       float y[NT][Q][VEC];
 #pragma unroll
@@ -412,22 +555,31 @@ __global__ __launch_bounds__(kFfnThreads) void ffn_chunk_kernel(FfnArgs a) {
         for (int q = 0; q < Q; ++q)
 #pragma unroll
           for (int i = 0; i < VEC; ++i) y[t][q][i] = 0.0f;
-#pragma unroll 4
-      for (int f = 0; f < kChunkUnits; ++f) {
-        const W* drow = D + static_cast<size_t>(f) * d;
-        float av[NT];
+      for (int f0 = 0; f0 < UPW; f0 += kRowBatch) {
+        uint4 dr[kRowBatch][Q];
 #pragma unroll
-        for (int t = 0; t < NT; ++t) av[t] = as[t * kChunkUnits + f];
+        for (int u = 0; u < kRowBatch; ++u)
 #pragma unroll
-        for (int q = 0; q < Q; ++q) {
-          const int col = (tid + kFfnThreads * q) * VEC;
-          if (col < d) {
-            float dv[VEC];
-            load16(drow + col, dv);
+          for (int q = 0; q < Q; ++q) {
+            const int col = (tid + THREADS * q) * VEC;
+            if (col < d) dr[u][q] = ldw16(D + static_cast<size_t>(f_first + f0 + u) * d + col);
+          }
 #pragma unroll
-            for (int t = 0; t < NT; ++t)
+        for (int u = 0; u < kRowBatch; ++u) {
+          float av[NT];
 #pragma unroll
-              for (int i = 0; i < VEC; ++i) y[t][q][i] = fmaf(av[t], dv[i], y[t][q][i]);
+          for (int t = 0; t < NT; ++t) av[t] = as[t * UPW + f0 + u];
+#pragma unroll
+          for (int q = 0; q < Q; ++q) {
+            const int col = (tid + THREADS * q) * VEC;
+            if (col < d) {
+              float dv[VEC];
+              unpack(dr[u][q], dv);
+#pragma unroll
+              for (int t = 0; t < NT; ++t)
+#pragma unroll
+                for (int i = 0; i < VEC; ++i) y[t][q][i] = fmaf(av[t], dv[i], y[t][q][i]);
+            }
           }
         }
       }
@@ -435,10 +587,10 @@ __global__ __launch_bounds__(kFfnThreads) void ffn_chunk_kernel(FfnArgs a) {
       for (int t = 0; t < NT; ++t) {
         if (t < nt) {
           const int row = routed ? (p0 + tile + t) : (tile + t);
-          float* dst = part + (static_cast<size_t>(c) * rows + row) * d;
+          float* dst = part + (static_cast<size_t>(plane) * rows + row) * d;
 #pragma unroll
           for (int q = 0; q < Q; ++q) {
-            const int col = (tid + kFfnThreads * q) * VEC;
+            const int col = (tid + THREADS * q) * VEC;
             if (col < d) {
 #pragma unroll
               for (int i = 0; i < VEC; i += 4)
@@ -453,49 +605,62 @@ __global__ __launch_bounds__(kFfnThreads) void ffn_chunk_kernel(FfnArgs a) {
   }
 }
 
-template <typename W, int NT, int Q>
+template <typename W, int NT, int Q, int UPW>
 static hipError_t launch_ffn_one(const FfnArgs& a, hipStream_t s) {
-  const size_t lds = sizeof(W) * NT * a.d + sizeof(float) * NT * kChunkUnits;
-  hipLaunchKernelGGL((ffn_chunk_kernel<W, NT, Q>), dim3(a.n_wg), dim3(kFfnThreads), lds, s, a);
+  const size_t lds = sizeof(W) * NT * a.d + sizeof(float) * NT * UPW;
+  hipLaunchKernelGGL((ffn_chunk_kernel<W, NT, Q, UPW>), dim3(a.n_wg), dim3(UPW * kLpu), lds, s, a);
   return hipGetLastError();
 }
 
 // Only the (NT, Q) pairs whose accumulators fit (NT * Q * VEC <= 64) exist.
-template <typename W>
+template <typename W, int UPW>
 static hipError_t dispatch_ffn(const FfnArgs& a, int nt, int q, hipStream_t s) {
   constexpr int V = Vec<W>::N;
-#define MSK_FFN_CASE(NT_, Q_)                                          \
-  if (nt == NT_ && q == Q_) {                                          \
-    if constexpr (NT_ * Q_ * V <= 64) return launch_ffn_one<W, NT_, Q_>(a, s); \
+#define MSK_FFN_CASE(NT_, Q_)                                                        \
+  if (nt == NT_ && q == Q_) {                                                        \
+    if constexpr (NT_ * Q_ * V <= 64) return launch_ffn_one<W, NT_, Q_, UPW>(a, s);  \
   }
   MSK_FFN_CASE(1, 1) MSK_FFN_CASE(2, 1) MSK_FFN_CASE(4, 1) MSK_FFN_CASE(8, 1)
   MSK_FFN_CASE(1, 2) MSK_FFN_CASE(2, 2) MSK_FFN_CASE(4, 2) MSK_FFN_CASE(8, 2)
   MSK_FFN_CASE(1, 4) MSK_FFN_CASE(2, 4) MSK_FFN_CASE(4, 4) MSK_FFN_CASE(8, 4)
+  MSK_FFN_CASE(1, 8) MSK_FFN_CASE(2, 8) MSK_FFN_CASE(4, 8) MSK_FFN_CASE(8, 8)
 #undef MSK_FFN_CASE
   return hipErrorInvalidValue;
 }
 
 // Tokens per tile: the smallest of {1, 2, 4, 8} covering max_tok, limited so
 // that the LDS tile stays within 64 KiB and the accumulators NT*Q*VEC <= 64.
-static int pick_nt(int max_tok, int d, int elem, int q, int vec) {
+static int pick_nt(int max_tok, int d, int elem, int q, int vec, int upw) {
   int nt = 1;
   while (nt < max_tok && nt < 8) nt <<= 1;
   while (nt > 1 &&
-         (static_cast<size_t>(nt) * (static_cast<size_t>(d) * elem + sizeof(float) * kChunkUnits) > 65536 ||
+         (static_cast<size_t>(nt) * (static_cast<size_t>(d) * elem + sizeof(float) * upw) > 65536 ||
           nt * q * vec > 64))
     nt >>= 1;
   return nt;
 }
 
+template <typename W>
+static hipError_t launch_ffn_w(const FfnArgs& a, int max_tok, hipStream_t s) {
+  constexpr int vec = Vec<W>::N;
+  const int upw = kChunkUnits / a.subs;
+  const int threads = upw * kLpu;
+  const int q = (a.d + threads * vec - 1) / (threads * vec);
+  int qq = 1;
+  while (qq < q) qq <<= 1;
+  if (qq > 8) return hipErrorInvalidValue;
+  const int nt = pick_nt(max_tok, a.d, static_cast<int>(sizeof(W)), qq, vec, upw);
+  switch (a.subs) {
+    case 1: return dispatch_ffn<W, 64>(a, nt, qq, s);
+    case 2: return dispatch_ffn<W, 32>(a, nt, qq, s);
+    case 4: return dispatch_ffn<W, 16>(a, nt, qq, s);
+    default: return hipErrorInvalidValue;
+  }
+}
+
 hipError_t launch_ffn(const FfnArgs& a, int max_tok, hipStream_t s) {
   if (a.n_wg <= 0 || a.n_tasks <= 0) return hipSuccess;
-  const int vec = (a.dtype == kBF16) ? 8 : 4;
-  const int elem = (a.dtype == kBF16) ? 2 : 4;
-  const int q = (a.d + kFfnThreads * vec - 1) / (kFfnThreads * vec);
-  const int qq = q <= 1 ? 1 : (q <= 2 ? 2 : 4);
-  if (q > 4) return hipErrorInvalidValue;
-  const int nt = pick_nt(max_tok, a.d, elem, qq, vec);
-  return (a.dtype == kBF16) ? dispatch_ffn<uint16_t>(a, nt, qq, s) : dispatch_ffn<float>(a, nt, qq, s);
+  return (a.dtype == kBF16) ? launch_ffn_w<uint16_t>(a, max_tok, s) : launch_ffn_w<float>(a, max_tok, s);
 }
 
 // ------------------------------------------------------------------ combine
@@ -528,12 +693,12 @@ __global__ __launch_bounds__(64 * kCombineWaves) void combine_kernel(CombineArgs
       base = a.part;
       row = a.pos[t * a.K + term];
       rows = a.rows_routed;
-      nch = a.n_chunks;
+      nch = a.n_planes;
     } else {
       base = a.part_sh + static_cast<size_t>(term - a.K) * a.sh_plane;
       row = t;
       rows = a.rows_shared;
-      nch = a.n_chunks_sh;
+      nch = a.n_planes_sh;
     }
     float4 s = make_float4(0.f, 0.f, 0.f, 0.f);
     if (live)

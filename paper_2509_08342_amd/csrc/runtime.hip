@@ -32,14 +32,14 @@ constexpr int kMaxD = 8192;
 uint64_t align_up(uint64_t x, uint64_t a) { return (x + a - 1) / a * a; }
 
 struct Shape {
-  int L, d, F, E, K, n_sh, F_sh, dtype, renorm, max_T, n_buf;
+  int L, d, F, E, K, n_sh, F_sh, dtype, renorm, max_T, n_buf, subs;
   int elem;
   uint64_t chunk_bytes;
   int n_chunks, n_chunks_sh;
   uint64_t expert_bytes, shared_bytes;
   int group_chunks;  // chunks per H2D copy group
   // fixed pool layout (byte offsets)
-  uint64_t off_router, off_bias, off_shared, off_ppred, off_offsets, off_perm, off_pos;
+  uint64_t off_router, off_bias, off_shared, off_logits, off_logits2, off_offsets, off_perm, off_pos;
   uint64_t off_part, off_part_sh, off_score, off_order, off_buffer, fixed_bytes;
   uint64_t router_stride, bias_stride, part_bytes, part_sh_bytes;
   int64_t sh_plane;
@@ -52,7 +52,8 @@ ms_status derive_shape(const ms_model_desc* d, Shape* s, std::string* err) {
   }
   if (d->n_layers <= 0 || d->d_model <= 0 || d->d_ff <= 0 || d->n_experts <= 0 || d->top_k <= 0 ||
       d->top_k > d->n_experts || d->n_shared < 0 || d->max_tokens <= 0 || d->n_buffer_slots < 0 ||
-      (d->dtype != MS_F32 && d->dtype != MS_BF16) || (d->n_shared > 0 && d->d_ff_shared <= 0)) {
+      (d->dtype != MS_F32 && d->dtype != MS_BF16) || (d->n_shared > 0 && d->d_ff_shared <= 0) ||
+      (d->ffn_splits != 0 && d->ffn_splits != 1 && d->ffn_splits != 2 && d->ffn_splits != 4)) {
     *err = "invalid model description";
     return MS_E_INVALID;
   }
@@ -86,6 +87,16 @@ ms_status derive_shape(const ms_model_desc* d, Shape* s, std::string* err) {
   s->expert_bytes = s->chunk_bytes * s->n_chunks;
   s->shared_bytes = s->chunk_bytes * s->n_chunks_sh;
   s->group_chunks = static_cast<int>(std::max<uint64_t>(1, kGroupTargetBytes / s->chunk_bytes));
+  // work-groups per chunk: enough that a decode step over the experts a
+  // forward can activate gives the FFN kernel >= 768 work-groups
+  if (d->ffn_splits > 0) {
+    s->subs = d->ffn_splits;
+  } else {
+    const int64_t active = std::min<int64_t>(s->E, static_cast<int64_t>(s->max_T) * s->K) + s->n_sh;
+    const int64_t work = active * s->n_chunks;
+    s->subs = 1;
+    while (s->subs < 4 && work * s->subs < 768) s->subs *= 2;
+  }
 
   const uint64_t TK = static_cast<uint64_t>(s->max_T) * s->K;
   uint64_t off = 0;
@@ -97,7 +108,9 @@ ms_status derive_shape(const ms_model_desc* d, Shape* s, std::string* err) {
   off += s->bias_stride * s->L;
   s->off_shared = off;
   off += align_up(s->shared_bytes, kAlign) * s->n_sh * s->L;
-  s->off_ppred = off;
+  s->off_logits = off;
+  off += align_up(static_cast<uint64_t>(s->max_T) * s->E * 4, kAlign);
+  s->off_logits2 = off;
   off += align_up(static_cast<uint64_t>(s->max_T) * s->E * 4, kAlign);
   s->off_offsets = off;
   off += align_up(static_cast<uint64_t>(s->E + 1) * 4, kAlign);
@@ -105,10 +118,10 @@ ms_status derive_shape(const ms_model_desc* d, Shape* s, std::string* err) {
   off += align_up(TK * 4, kAlign);
   s->off_pos = off;
   off += align_up(TK * 4, kAlign);
-  s->part_bytes = static_cast<uint64_t>(s->n_chunks) * TK * s->d * 4;
+  s->part_bytes = static_cast<uint64_t>(s->n_chunks) * s->subs * TK * s->d * 4;
   s->off_part = off;
   off += align_up(s->part_bytes, kAlign);
-  s->sh_plane = static_cast<int64_t>(s->n_chunks_sh) * s->max_T * s->d;
+  s->sh_plane = static_cast<int64_t>(s->n_chunks_sh) * s->subs * s->max_T * s->d;
   s->part_sh_bytes = static_cast<uint64_t>(s->sh_plane) * 4 * s->n_sh;
   s->off_part_sh = off;
   off += align_up(s->part_sh_bytes, kAlign);
@@ -129,10 +142,13 @@ int top_units_for(float r, int F) {
 }
 
 // Pack one SwiGLU FFN (w_gate, w_up [d][F], w_down [F][d]) into chunk order:
-// per 64-unit chunk, 64 gate columns, 64 up columns and 64 down rows, each a
-// d-contiguous row; units past F are zero.
+// per 64-unit chunk, the gate block, the up block and the down block.  Gate
+// and up blocks are k-tiled -- unit u's weights for k in [64 kb, 64 kb + 64)
+// form one 64-element piece at ((kb * 64) + u) * 64 -- and the down block
+// holds the 64 down rows, each d-contiguous.  Units past F are zero.
 template <typename T>
 void pack_expert_t(const T* wg, const T* wu, const T* wd, int d, int F, int n_chunks, T* dst) {
+  constexpr int KT = 64;
   auto work = [&](int c0, int c1) {
     for (int c = c0; c < c1; ++c) {
       T* G = dst + static_cast<size_t>(c) * 3 * kUnits * d;
@@ -144,9 +160,10 @@ void pack_expert_t(const T* wg, const T* wu, const T* wd, int d, int F, int n_ch
       for (int j = 0; j < d; ++j) {
         const T* gr = wg + static_cast<size_t>(j) * F + f0;
         const T* ur = wu + static_cast<size_t>(j) * F + f0;
+        const size_t base = static_cast<size_t>(j / KT) * kUnits * KT + (j % KT);
         for (int u = 0; u < nu; ++u) {
-          G[static_cast<size_t>(u) * d + j] = gr[u];
-          U[static_cast<size_t>(u) * d + j] = ur[u];
+          G[base + static_cast<size_t>(u) * KT] = gr[u];
+          U[base + static_cast<size_t>(u) * KT] = ur[u];
         }
       }
       for (int u = 0; u < nu; ++u)
@@ -182,6 +199,7 @@ struct Group {
   bool issued = false;
   bool prefetch = false;  // issued by prefetch
   bool used = false;      // consumed by a forward
+  bool pre = false;       // computed by the running forward's resident launch
 };
 
 struct BufSlot {
@@ -254,7 +272,7 @@ struct ms_ctx {
   uint64_t tick = 0;
   std::deque<PendingGroup> pf_queue;
   std::vector<PendingGroup> pf_inflight;
-  hipEvent_t ev_route = nullptr, ev_side_done = nullptr, ev_last = nullptr;
+  hipEvent_t ev_route = nullptr, ev_res = nullptr, ev_side_done = nullptr, ev_last = nullptr;
   bool has_last = false;
   hipStream_t last_stream = nullptr;
   std::vector<hipEvent_t> free_events;
@@ -585,7 +603,7 @@ ms_status ms_create(const ms_model_desc* desc, void* dev_pool, uint64_t pool_byt
     return cleanup_fail(e, "hipStreamCreate(copy)");
   if ((e = hipStreamCreateWithFlags(&ctx->side, hipStreamNonBlocking)) != hipSuccess)
     return cleanup_fail(e, "hipStreamCreate(side)");
-  for (hipEvent_t* ev : {&ctx->ev_route, &ctx->ev_side_done, &ctx->ev_last})
+  for (hipEvent_t* ev : {&ctx->ev_route, &ctx->ev_res, &ctx->ev_side_done, &ctx->ev_last})
     if ((e = hipEventCreateWithFlags(ev, hipEventDisableTiming)) != hipSuccess)
       return cleanup_fail(e, "hipEventCreate");
   // small host buffers that kernels write directly (mapped, coherent)
@@ -640,7 +658,7 @@ void ms_destroy(ms_ctx* ctx) {
   }
   for (hipEvent_t ev : ctx->tl_pool) (void)hipEventDestroy(ev);
   if (ctx->tl_origin) (void)hipEventDestroy(ctx->tl_origin);
-  for (hipEvent_t ev : {ctx->ev_route, ctx->ev_side_done, ctx->ev_last})
+  for (hipEvent_t ev : {ctx->ev_route, ctx->ev_res, ctx->ev_side_done, ctx->ev_last})
     if (ev) (void)hipEventDestroy(ev);
   for (unsigned char* p : ctx->blobs) (void)hipHostFree(p);
   if (ctx->h_offsets) (void)hipHostFree(ctx->h_offsets);
@@ -869,30 +887,30 @@ ms_status ms_predict(ms_ctx* ctx, int32_t layer, const void* h_dev, int32_t T, v
   hipStream_t sm = static_cast<hipStream_t>(stream);
   st = order_after_last(ctx, sm);
   if (st != MS_OK) return st;
-  msk::RouterArgs ra{};
-  ra.h = h_dev;
-  ra.T = T;
-  ra.d = s.d;
-  ra.E = s.E;
-  ra.K = s.K;
-  ra.dtype = s.dtype;
-  ra.renormalize = s.renorm;
-  ra.wr_next = ctx->dev(s.off_router + s.router_stride * layer);
-  ra.bias_next = L.bias_set ? reinterpret_cast<const float*>(ctx->dev(s.off_bias + s.bias_stride * layer)) : nullptr;
-  ra.p_pred = reinterpret_cast<float*>(ctx->dev(s.off_ppred));
+  msk::LogitsArgs la{};
+  la.h = h_dev;
+  la.T = T;
+  la.d = s.d;
+  la.E = s.E;
+  la.dtype = s.dtype;
+  la.wr2 = ctx->dev(s.off_router + s.router_stride * layer);
+  la.bias2 = L.bias_set ? reinterpret_cast<const float*>(ctx->dev(s.off_bias + s.bias_stride * layer)) : nullptr;
+  la.logits2 = reinterpret_cast<float*>(ctx->dev(s.off_logits2));
   int ti = tl_begin(ctx, sm, MS_IV_ROUTER, layer, static_cast<uint64_t>(s.d) * s.E * s.elem);
-  MS_HIP(msk::launch_router(ra, sm));
+  MS_HIP(msk::launch_logits(la, sm));
   tl_end(ctx, ti, sm);
-  msk::RankArgs rk{};
-  rk.p_pred = ra.p_pred;
+  msk::RouteArgs rk{};
   rk.T = T;
   rk.E = s.E;
+  rk.K = s.K;
+  rk.renormalize = s.renorm;
+  rk.logits_pred = la.logits2;
   rk.score = reinterpret_cast<float*>(ctx->dev(s.off_score));
   rk.order = reinterpret_cast<int32_t*>(ctx->dev(s.off_order));
   rk.host_score = ctx->d_score_map;
   rk.host_order = ctx->d_order_map;
   ti = tl_begin(ctx, sm, MS_IV_PREDICT, layer, 0);
-  MS_HIP(msk::launch_rank(rk, sm));
+  MS_HIP(msk::launch_route(rk, sm));
   tl_end(ctx, ti, sm);
   MS_HIP(hipEventRecord(ctx->ev_last, sm));
   ctx->has_last = true;
@@ -946,56 +964,54 @@ ms_status ms_forward(ms_ctx* ctx, int32_t layer, const void* h_dev, int32_t T, f
   const int rows_routed = s.max_T * s.K;
 
   // 1. routing (+ next-layer prediction), grouping
-  msk::RouterArgs ra{};
-  ra.h = h_dev;
-  ra.T = T;
-  ra.d = s.d;
-  ra.E = s.E;
-  ra.K = s.K;
-  ra.dtype = s.dtype;
-  ra.renormalize = s.renorm;
-  ra.wr = ctx->dev(s.off_router + s.router_stride * layer);
-  ra.bias = L.bias_set ? reinterpret_cast<const float*>(ctx->dev(s.off_bias + s.bias_stride * layer)) : nullptr;
-  ra.idx = idx_dev;
-  ra.w = w_dev;
+  msk::LogitsArgs la{};
+  la.h = h_dev;
+  la.T = T;
+  la.d = s.d;
+  la.E = s.E;
+  la.dtype = s.dtype;
+  la.wr = ctx->dev(s.off_router + s.router_stride * layer);
+  la.bias = L.bias_set ? reinterpret_cast<const float*>(ctx->dev(s.off_bias + s.bias_stride * layer)) : nullptr;
+  la.logits = reinterpret_cast<float*>(ctx->dev(s.off_logits));
   if (predict_next) {
     const LayerState& N = ctx->layers[next_layer];
-    ra.wr_next = ctx->dev(s.off_router + s.router_stride * next_layer);
-    ra.bias_next = N.bias_set ? reinterpret_cast<const float*>(ctx->dev(s.off_bias + s.bias_stride * next_layer)) : nullptr;
-    ra.p_pred = reinterpret_cast<float*>(ctx->dev(s.off_ppred));
+    la.wr2 = ctx->dev(s.off_router + s.router_stride * next_layer);
+    la.bias2 = N.bias_set ? reinterpret_cast<const float*>(ctx->dev(s.off_bias + s.bias_stride * next_layer)) : nullptr;
+    la.logits2 = reinterpret_cast<float*>(ctx->dev(s.off_logits2));
   }
   const uint64_t router_bytes = static_cast<uint64_t>(s.d) * s.E * s.elem * (predict_next ? 2 : 1);
   int ti = tl_begin(ctx, sm, MS_IV_ROUTER, layer, router_bytes);
-  MS_HIP(msk::launch_router(ra, sm));
+  MS_HIP(msk::launch_logits(la, sm));
   tl_end(ctx, ti, sm);
 
-  msk::GroupArgs ga{};
-  ga.idx = idx_dev;
-  ga.TK = TK;
+  msk::RouteArgs ga{};
+  ga.T = T;
   ga.E = s.E;
+  ga.K = s.K;
+  ga.renormalize = s.renorm;
+  ga.logits = la.logits;
+  ga.idx = idx_dev;
+  ga.w = w_dev;
   ga.offsets = d_offsets;
   ga.perm = d_perm;
   ga.pos = d_pos;
   ga.host_offsets = ctx->d_offsets_map;
-  ti = tl_begin(ctx, sm, MS_IV_GROUP, layer, 0);
-  MS_HIP(msk::launch_group(ga, sm));
-  tl_end(ctx, ti, sm);
   if (predict_next) {
-    msk::RankArgs rk{};
-    rk.p_pred = ra.p_pred;
-    rk.T = T;
-    rk.E = s.E;
-    rk.score = reinterpret_cast<float*>(ctx->dev(s.off_score));
-    rk.order = reinterpret_cast<int32_t*>(ctx->dev(s.off_order));
-    rk.host_score = ctx->d_score_map;
-    rk.host_order = ctx->d_order_map;
-    ti = tl_begin(ctx, sm, MS_IV_PREDICT, layer, 0);
-    MS_HIP(msk::launch_rank(rk, sm));
-    tl_end(ctx, ti, sm);
+    ga.logits_pred = la.logits2;
+    ga.score = reinterpret_cast<float*>(ctx->dev(s.off_score));
+    ga.order = reinterpret_cast<int32_t*>(ctx->dev(s.off_order));
+    ga.host_score = ctx->d_score_map;
+    ga.host_order = ctx->d_order_map;
   }
+  ti = tl_begin(ctx, sm, MS_IV_GROUP, layer, 0);
+  MS_HIP(msk::launch_route(ga, sm));
+  tl_end(ctx, ti, sm);
   MS_HIP(hipEventRecord(ctx->ev_route, sm));
 
-  // 2. resident segments (Eq. (5): processed while missing ones load)
+  // 2. segments already in VRAM (Eq. (5): processed while missing ones
+  //    load): cached tops, staging-buffer groups of this layer whose copies
+  //    have completed, and the shared experts.  Experts that turn out not to
+  //    be selected exit at once.
   msk::FfnArgs fa{};
   fa.h = h_dev;
   fa.offsets = d_offsets;
@@ -1010,8 +1026,8 @@ ms_status ms_forward(ms_ctx* ctx, int32_t layer, const void* h_dev, int32_t T, f
   fa.K = s.K;
   fa.T = T;
   fa.dtype = s.dtype;
+  fa.subs = s.subs;
   std::vector<msk::FfnTask> res_tasks;
-  std::vector<int> res_task_expert;
   for (int e = 0; e < s.E; ++e) {
     const int rc = resident_chunks(L, e);
     if (rc <= 0) continue;
@@ -1021,6 +1037,31 @@ ms_status ms_forward(ms_ctx* ctx, int32_t layer, const void* h_dev, int32_t T, f
     t.chunk_lo = 0;
     t.n_chunks = rc;
     res_tasks.push_back(t);
+  }
+  bool any_pre = false;
+  for (BufSlot& b : ctx->buf) {
+    if (b.layer != layer) continue;
+    const int res = resident_chunks(L, b.expert);
+    for (int gi = 0; gi < static_cast<int>(b.groups.size()); ++gi) {
+      Group& g = b.groups[gi];
+      const int lo = std::max(g.c_lo, res);
+      if (!g.issued || lo >= g.c_hi) continue;
+      const hipError_t q = hipEventQuery(b.gev[gi]);
+      if (q == hipErrorNotReady) continue;
+      if (q != hipSuccess) return poison(ctx, "hipEventQuery(group)", q);
+      msk::FfnTask t{};
+      t.base = b.base;
+      t.expert = b.expert;
+      t.chunk_lo = lo;
+      t.n_chunks = g.c_hi - lo;
+      if (!res_tasks.empty() && res_tasks.back().base == t.base && res_tasks.back().expert == t.expert &&
+          res_tasks.back().chunk_lo + res_tasks.back().n_chunks == lo)
+        res_tasks.back().n_chunks += t.n_chunks;  // contiguous with the previous group
+      else
+        res_tasks.push_back(t);
+      g.pre = true;
+      any_pre = true;
+    }
   }
   for (int i = 0; i < s.n_sh; ++i) {
     msk::FfnTask t{};
@@ -1032,22 +1073,31 @@ ms_status ms_forward(ms_ctx* ctx, int32_t layer, const void* h_dev, int32_t T, f
   }
   std::vector<int> res_tl;  // timeline records of resident launches (bytes fixed after routing)
   std::vector<std::vector<msk::FfnTask>> res_batches;
-  for (size_t i0 = 0; i0 < res_tasks.size(); i0 += msk::kMaxTasks) {
-    const size_t i1 = std::min(res_tasks.size(), i0 + msk::kMaxTasks);
-    fa.n_tasks = static_cast<int>(i1 - i0);
-    int wg = 0;
-    for (size_t i = i0; i < i1; ++i) {
-      fa.tasks[i - i0] = res_tasks[i];
-      fa.tasks[i - i0].wg_begin = wg;
-      wg += res_tasks[i].n_chunks;
+  auto launch_tasks = [&](const std::vector<msk::FfnTask>& tasks, hipStream_t st, int kind, int max_tok,
+                          std::vector<int>* tl_ids, std::vector<std::vector<msk::FfnTask>>* batches) -> ms_status {
+    for (size_t i0 = 0; i0 < tasks.size(); i0 += msk::kMaxTasks) {
+      const size_t i1 = std::min(tasks.size(), i0 + msk::kMaxTasks);
+      fa.n_tasks = static_cast<int>(i1 - i0);
+      int wg = 0;
+      uint64_t bytes = 0;
+      for (size_t i = i0; i < i1; ++i) {
+        fa.tasks[i - i0] = tasks[i];
+        fa.tasks[i - i0].wg_begin = wg;
+        wg += tasks[i].n_chunks * s.subs;
+        bytes += s.chunk_bytes * tasks[i].n_chunks;
+      }
+      fa.n_wg = wg;
+      const int id = tl_begin(ctx, st, kind, layer, bytes);
+      MS_HIP(msk::launch_ffn(fa, max_tok, st));
+      tl_end(ctx, id, st);
+      if (tl_ids) tl_ids->push_back(id);
+      if (batches) batches->emplace_back(tasks.begin() + i0, tasks.begin() + i1);
     }
-    fa.n_wg = wg;
-    ti = tl_begin(ctx, sm, MS_IV_FFN_RESIDENT, layer, 0);
-    MS_HIP(msk::launch_ffn(fa, T, sm));
-    tl_end(ctx, ti, sm);
-    res_tl.push_back(ti);
-    res_batches.emplace_back(res_tasks.begin() + i0, res_tasks.begin() + i1);
-  }
+    return MS_OK;
+  };
+  st = launch_tasks(res_tasks, sm, MS_IV_FFN_RESIDENT, T, &res_tl, &res_batches);
+  if (st != MS_OK) return st;
+  if (any_pre) MS_HIP(hipEventRecord(ctx->ev_res, sm));
 
   // 3. wait for the routing result on the host, keeping prefetch copies fed
   for (;;) {
@@ -1065,17 +1115,15 @@ ms_status ms_forward(ms_ctx* ctx, int32_t layer, const void* h_dev, int32_t T, f
     for (int e = 0; e < s.E; ++e) pred[e] = reinterpret_cast<volatile int32_t*>(ctx->h_order)[e];
   }
   terminate_prefetch(ctx);
-  for (auto& pg : ctx->pf_inflight) (void)pg;  // in-flight groups complete on their own
-  ctx->pf_inflight.clear();
+  ctx->pf_inflight.clear();  // in-flight groups complete on their own
 
   // bytes of the resident launches now that the active experts are known
-  const uint64_t shb = s.shared_bytes;
   for (size_t bi = 0; bi < res_tl.size(); ++bi) {
     if (res_tl[bi] < 0) continue;
     uint64_t bytes = 0;
     for (const msk::FfnTask& t : res_batches[bi]) {
       if (t.expert >= 0 && offs[t.expert + 1] == offs[t.expert]) continue;
-      bytes += (t.expert >= 0 ? s.chunk_bytes * t.n_chunks : shb);
+      bytes += s.chunk_bytes * t.n_chunks;
     }
     ctx->tl[res_tl[bi]].bytes = bytes;
   }
@@ -1093,8 +1141,11 @@ ms_status ms_forward(ms_ctx* ctx, int32_t layer, const void* h_dev, int32_t T, f
     L.has_pred = false;
   }
 
-  // 5. missing segments: copy stream issues, side stream computes per group
-  MS_HIP(hipStreamWaitEvent(ctx->side, ctx->ev_route, 0));
+  // 5. missing segments.  Side stream: first one wide launch over buffer
+  //    groups that landed by now, then one launch per group still to land,
+  //    each after its copy event.  Slots read by the resident launch are
+  //    released only after it (the side stream waits for it).
+  MS_HIP(hipStreamWaitEvent(ctx->side, any_pre ? ctx->ev_res : ctx->ev_route, 0));
   // slots already holding an active expert's missing part are reserved so
   // that no other miss of this forward evicts them first
   constexpr int kReserved = 1 << 30;
@@ -1104,6 +1155,60 @@ ms_status ms_forward(ms_ctx* ctx, int32_t layer, const void* h_dev, int32_t T, f
     if (si >= 0 && ctx->buf[si].first_chunk <= resident_chunks(L, e)) ctx->buf[si].use_order = kReserved;
   }
   int use_counter = 0;
+  auto count_used = [&](Group& g) {
+    if (g.prefetch && !g.used) L.st.bytes_prefetch_used += s.chunk_bytes * (g.c_hi - g.c_lo);
+    g.used = true;
+  };
+  // 5a. landed groups of covering slots
+  std::vector<msk::FfnTask> landed;
+  std::vector<int> landed_slots;
+  for (int e = 0; e < s.E; ++e) {
+    if (offs[e + 1] == offs[e]) continue;
+    const int res = resident_chunks(L, e);
+    if (res >= s.n_chunks) continue;
+    const int si = find_slot(ctx, layer, e);
+    if (si < 0 || ctx->buf[si].first_chunk > res) continue;
+    BufSlot& b = ctx->buf[si];
+    bool any = false;
+    for (int gi = 0; gi < static_cast<int>(b.groups.size()); ++gi) {
+      Group& g = b.groups[gi];
+      const int lo = std::max(g.c_lo, res);
+      if (lo >= g.c_hi || !g.issued) continue;
+      if (g.pre) {
+        count_used(g);
+        continue;
+      }
+      const hipError_t q = hipEventQuery(b.gev[gi]);
+      if (q == hipErrorNotReady) continue;
+      if (q != hipSuccess) return poison(ctx, "hipEventQuery(group)", q);
+      msk::FfnTask t{};
+      t.base = b.base;
+      t.expert = e;
+      t.chunk_lo = lo;
+      t.n_chunks = g.c_hi - lo;
+      if (!landed.empty() && landed.back().base == t.base && landed.back().chunk_lo + landed.back().n_chunks == lo)
+        landed.back().n_chunks += t.n_chunks;
+      else
+        landed.push_back(t);
+      g.pre = true;  // computed now; the per-group pass skips it
+      count_used(g);
+      any = true;
+    }
+    if (any) landed_slots.push_back(si);
+  }
+  if (!landed.empty()) {
+    st = launch_tasks(landed, ctx->side, MS_IV_FFN_STREAMED, T, nullptr, nullptr);
+    if (st != MS_OK) return st;
+  }
+  for (BufSlot& b : ctx->buf) {
+    bool read = false;
+    for (const Group& g : b.groups) read = read || g.pre;
+    if (read) {
+      MS_HIP(hipEventRecord(b.last_read, ctx->side));
+      b.has_last_read = true;
+    }
+  }
+  // 5b. the rest: issue what is missing, compute each group as it lands
   for (int e = 0; e < s.E; ++e) {
     if (offs[e + 1] == offs[e]) continue;
     L.st.experts_active += 1;
@@ -1129,17 +1234,16 @@ ms_status ms_forward(ms_ctx* ctx, int32_t layer, const void* h_dev, int32_t T, f
     BufSlot& b = ctx->buf[si];
     b.use_order = use_counter++;
     b.tick = ++ctx->tick;
+    bool launched = false;
     for (int gi = 0; gi < static_cast<int>(b.groups.size()); ++gi) {
       Group& g = b.groups[gi];
       const int lo = std::max(g.c_lo, res);
-      if (lo >= g.c_hi) continue;
+      if (lo >= g.c_hi || g.pre) continue;
       if (!g.issued) {
         st = issue_group(ctx, si, gi, false);
         if (st != MS_OK) return st;
-      } else if (g.prefetch && !g.used) {
-        L.st.bytes_prefetch_used += s.chunk_bytes * (g.c_hi - g.c_lo);
       }
-      g.used = true;
+      count_used(g);
       MS_HIP(hipStreamWaitEvent(ctx->side, b.gev[gi], 0));
       fa.n_tasks = 1;
       fa.tasks[0].base = b.base;
@@ -1147,14 +1251,19 @@ ms_status ms_forward(ms_ctx* ctx, int32_t layer, const void* h_dev, int32_t T, f
       fa.tasks[0].chunk_lo = lo;
       fa.tasks[0].n_chunks = g.c_hi - lo;
       fa.tasks[0].wg_begin = 0;
-      fa.n_wg = g.c_hi - lo;
+      fa.n_wg = (g.c_hi - lo) * s.subs;
       ti = tl_begin(ctx, ctx->side, MS_IV_FFN_STREAMED, layer, s.chunk_bytes * (g.c_hi - lo));
       MS_HIP(msk::launch_ffn(fa, offs[e + 1] - offs[e], ctx->side));
       tl_end(ctx, ti, ctx->side);
+      launched = true;
     }
-    MS_HIP(hipEventRecord(b.last_read, ctx->side));
-    b.has_last_read = true;
+    if (launched) {
+      MS_HIP(hipEventRecord(b.last_read, ctx->side));
+      b.has_last_read = true;
+    }
   }
+  for (BufSlot& b : ctx->buf)
+    for (Group& g : b.groups) g.pre = false;
   MS_HIP(hipEventRecord(ctx->ev_side_done, ctx->side));
   MS_HIP(hipStreamWaitEvent(sm, ctx->ev_side_done, 0));
 
@@ -1168,8 +1277,8 @@ ms_status ms_forward(ms_ctx* ctx, int32_t layer, const void* h_dev, int32_t T, f
   ca.sh_plane = s.sh_plane;
   ca.rows_routed = rows_routed;
   ca.rows_shared = s.max_T;
-  ca.n_chunks = s.n_chunks;
-  ca.n_chunks_sh = s.n_chunks_sh;
+  ca.n_planes = s.n_chunks * s.subs;
+  ca.n_planes_sh = s.n_chunks_sh * s.subs;
   ca.n_shared = s.n_sh;
   ca.T = T;
   ca.K = s.K;
@@ -1189,7 +1298,9 @@ ms_status ms_forward(ms_ctx* ctx, int32_t layer, const void* h_dev, int32_t T, f
     N.pred_order = pred;
     N.has_pred = true;
     if (N.configured) {
-      st = enqueue_prefetch(ctx, next_layer, pred.data(), static_cast<int>(pred.size()));
+      // the paper's buffer holds K whole experts: prefetch candidates are the
+      // K highest-ranked predictions, in rank order
+      st = enqueue_prefetch(ctx, next_layer, pred.data(), std::min<int>(s.K, static_cast<int>(pred.size())));
       if (st != MS_OK) return st;
     }
   }

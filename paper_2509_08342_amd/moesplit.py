@@ -29,7 +29,7 @@ INTERVAL_NAMES = ["router", "group", "ffn_resident", "ffn_streamed", "combine",
 class ms_model_desc(ctypes.Structure):
     _fields_ = [(n, ctypes.c_int32) for n in (
         "n_layers", "d_model", "d_ff", "n_experts", "top_k", "n_shared", "d_ff_shared",
-        "dtype", "renormalize", "max_tokens", "n_buffer_slots")]
+        "dtype", "renormalize", "max_tokens", "n_buffer_slots", "ffn_splits")]
 
 
 class ms_sizes(ctypes.Structure):
@@ -126,12 +126,12 @@ def _stream(s):
     return s.cuda_stream
 
 
-def model_desc(shape, max_tokens, n_buffer_slots=0):
+def model_desc(shape, max_tokens, n_buffer_slots=0, ffn_splits=0):
     """ms_model_desc from a synth.ModelShape-like object."""
     return ms_model_desc(shape.n_layers, shape.d_model, shape.d_ff, shape.n_experts, shape.top_k,
                          shape.n_shared, shape.d_ff_shared,
                          MS_BF16 if shape.dtype == "bf16" else MS_F32, shape.renormalize,
-                         max_tokens, n_buffer_slots)
+                         max_tokens, n_buffer_slots, ffn_splits)
 
 
 def _check(st, ctx=None, what=""):

@@ -218,3 +218,24 @@ def test_router_follows_fixed_logit_order(which):
         rig.forward(0, torch.from_numpy(h).cuda(), 1, y, idx, w)
         torch.cuda.synchronize()
         assert int(idx[0, 0]) == expect
+
+
+@pytest.mark.parametrize("splits", [1, 2, 4])
+def test_tiny_every_chunk_split_matches_oracle(splits):
+    """The FFN kernel's work-group split of a chunk changes only the
+    summation grouping: each split passes parity and is residency-invariant."""
+    from workload import SplitRig, top_bytes
+    with SplitRig(synth.TINY, seed=0, max_tokens=16, budget_bytes=8 * synth.TINY.expert_bytes,
+                  ffn_splits=splits) as r:
+        h, hf = r.hidden(16, tag=31)
+        outs = []
+        for ratio, tops in ((0.5, [0, 1, 2, 3]), (1.0, list(range(8))), (0.0, [])):
+            tb = top_bytes(r, ratio)
+            r.configure([8 * tb], [ratio])
+            r.load_tops(0, tops)
+            y, idx, w = r.outputs(16)
+            r.forward(0, h, 16, y, idx, w)
+            torch.cuda.synchronize()
+            check_layer(r, 0, hf, y, idx, w)
+            outs.append(y.cpu().numpy())
+        assert np.array_equal(outs[0], outs[1]) and np.array_equal(outs[0], outs[2])

@@ -37,13 +37,13 @@ class SplitRig:
     oracle."""
 
     def __init__(self, shape: synth.ModelShape, *, seed=0, max_tokens=1, n_sets=None,
-                 n_buffer_slots=0, budget_bytes=0, keep_f32=True, threads=8):
+                 n_buffer_slots=0, budget_bytes=0, keep_f32=True, threads=8, ffn_splits=0):
         self.shape = shape
         self.seed = seed
         self.max_tokens = max_tokens
         L = shape.n_layers
         self.n_sets = L if n_sets is None else max(1, min(n_sets, L))
-        self.desc = ms.model_desc(shape, max_tokens, n_buffer_slots)
+        self.desc = ms.model_desc(shape, max_tokens, n_buffer_slots, ffn_splits)
         self.sizes = ms.ms_query_sizes(self.desc)
         self.pool_bytes = int(self.sizes.fixed_pool_bytes) + int(budget_bytes)
         self.pool = torch.empty(self.pool_bytes, dtype=torch.uint8, device="cuda")
