@@ -30,7 +30,7 @@ struct LogitsArgs {
   const float* bias2;
   float* logits2;
 };
-hipError_t launch_logits(const LogitsArgs& a, hipStream_t s);
+
 
 // One work-group: top-K selection with lowest-index ties and Eq. (2) gate
 // weights, the stable token-to-expert grouping, and the ranking of the
@@ -51,7 +51,8 @@ struct RouteArgs {
   float* host_score;        // host-visible or NULL
   int32_t* host_order;      // host-visible or NULL
 };
-hipError_t launch_route(const RouteArgs& a, hipStream_t s);
+// Logits launch, then the route launch on them.
+hipError_t launch_logits_route(const LogitsArgs& a, const RouteArgs& ra, hipStream_t s);
 
 // One FFN task: chunks [chunk_lo, chunk_lo + n_chunks) of one expert whose
 // chunk c lives at base + c * chunk_bytes.  expert >= 0: routed expert (its
@@ -71,8 +72,8 @@ struct FfnArgs {
   const void* h;              // [T][d] model dtype
   const int32_t* offsets;     // [E+1] grouping
   const int32_t* perm;        // [TK]
-  float* part;                // routed partials [n_chunks * subs][rows_routed][d]
-  float* part_sh;             // shared partials [n_shared][n_chunks_sh * subs][rows_shared][d]
+  float* part;                // routed partials [rows_routed][n_planes][d]
+  float* part_sh;             // shared partials [n_shared][rows_shared][n_planes_sh][d]
   uint64_t chunk_bytes;       // bytes of one chunk (3 * 64 * d * elem)
   int64_t sh_plane;           // floats per shared expert in part_sh
   int32_t rows_routed;        // row stride of one routed chunk plane (max T*K)
@@ -82,24 +83,31 @@ struct FfnArgs {
   int32_t n_tasks;
   int32_t n_wg;               // total work-groups: sum of task chunks * subs
   int32_t subs;               // work-groups per chunk: 1, 2 or 4
+  int32_t n_planes;           // routed partial planes: n_chunks * subs
+  int32_t n_planes_sh;        // shared partial planes: n_chunks_sh * subs
   FfnTask tasks[kMaxTasks];
 };
 // Launches n_wg work-groups; max_tok bounds the tokens of any task.
 hipError_t launch_ffn(const FfnArgs& a, int max_tok, hipStream_t s);
 
 // y[t] = sum_k w[t][k] * sum_c part[c][pos[t*K+k]] + sum_s sum_c part_sh[s][c][t],
-// c over the partial planes (chunks * subs).
+// c over the partial planes (chunks * subs), in two launches: a first pass
+// over plane groups into `red`, then the weighted sum per token.
 struct CombineArgs {
   const float* part;
   const float* part_sh;
   const int32_t* pos;         // [T*K]
   const float* w;             // [T*K]
   float* y;                   // [T][d]
+  float* red;                 // [pg][T*(K+n_shared)][d] first-pass sums
   int64_t sh_plane;
   int32_t rows_routed, rows_shared;
   int32_t n_planes, n_planes_sh, n_shared;
   int32_t T, K, d;
+  int32_t pg;                 // plane groups of the first pass (combine_groups)
 };
+// Plane groups for the first pass at this shape (a power of two <= 16).
+int combine_groups(int T, int K, int n_shared, int d, int n_planes);
 hipError_t launch_combine(const CombineArgs& a, hipStream_t s);
 
 }  // namespace msk

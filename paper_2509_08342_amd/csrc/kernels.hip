@@ -89,155 +89,33 @@ __device__ __forceinline__ void unpack(const uint4 v, float (&o)[8]) {
 
 __device__ __forceinline__ float silu(float x) { return x / (1.0f + expf(-x)); }
 
-// ------------------------------------------------------------------- logits
-//
-// A logit is computed in the fixed fp32 order that makes the selection
-// reproducible: lane l accumulates h[j] * w[j][e] with fma over
-// j = l, l+64, ... ascending, then lane partials are added in a halving tree
-// that pairs lane l with lane l+s for s = 32, 16, ..., 1 (lane 0 ends with
-// the result); a bias is added once afterwards.
-//
-// Work-group = 4 waves = 4 tokens x one block of 8 experts of one router.
-// The block's weight columns are staged in LDS tile by tile (all 256 threads
-// load), then each wave runs its token's fma chains from LDS.
-
-constexpr int kLgWaves = 4;
-constexpr int kLgBlock = 8;           // experts per work-group
-constexpr int kLgTileBytes = 32768;   // LDS tile of router rows
-
-template <typename W>
-__global__ __launch_bounds__(64 * kLgWaves) void logits_kernel(LogitsArgs a) {
-  __shared__ __align__(16) W tile[kLgTileBytes / sizeof(W)];
-  constexpr int RT = kLgTileBytes / (kLgBlock * sizeof(W));  // rows per tile (multiple of 64)
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int nb = (a.E + kLgBlock - 1) / kLgBlock;
-  const int mat = blockIdx.y / nb, eb = blockIdx.y - mat * nb;
-  const W* wr = static_cast<const W*>(mat == 0 ? a.wr : a.wr2);
-  const float* bias = mat == 0 ? a.bias : a.bias2;
-  float* out = mat == 0 ? a.logits : a.logits2;
-  const int e0 = eb * kLgBlock, ne = min(kLgBlock, a.E - e0);
-  const bool vec = (ne == kLgBlock) && ((a.E * static_cast<int>(sizeof(W))) % 16 == 0);
-  const int t = blockIdx.x * kLgWaves + wave;
-  const bool active = t < a.T;
-  const W* hrow = static_cast<const W*>(a.h) + static_cast<size_t>(active ? t : 0) * a.d;
-  float acc[kLgBlock];
-#pragma unroll
-  for (int q = 0; q < kLgBlock; ++q) acc[q] = 0.0f;
-
-  constexpr int NV = static_cast<int>(kLgBlock * sizeof(W)) / 16;  // 16-byte pieces per tile row
-  constexpr int RB = RT / (64 * kLgWaves);                           // tile rows per thread
-  for (int j0 = 0; j0 < a.d; j0 += RT) {
-    const int rows = min(RT, a.d - j0);
-    if (vec) {
-      // all of this thread's row loads first, then the LDS stores
-      uint4 buf[RB][NV];
-#pragma unroll
-      for (int u = 0; u < RB; ++u) {
-        const int r = min(tid + 64 * kLgWaves * u, rows - 1);
-        const uint4* src = reinterpret_cast<const uint4*>(wr + static_cast<size_t>(j0 + r) * a.E + e0);
-#pragma unroll
-        for (int b = 0; b < NV; ++b) buf[u][b] = src[b];
-      }
-#pragma unroll
-      for (int u = 0; u < RB; ++u) {
-        const int r = tid + 64 * kLgWaves * u;
-        if (r < rows) {
-#pragma unroll
-          for (int b = 0; b < NV; ++b) reinterpret_cast<uint4*>(tile + r * kLgBlock)[b] = buf[u][b];
-        }
-      }
-    } else {
-      for (int r = tid; r < rows; r += 64 * kLgWaves) {
-        const W* src = wr + static_cast<size_t>(j0 + r) * a.E + e0;
-#pragma unroll
-        for (int q = 0; q < kLgBlock; ++q) tile[r * kLgBlock + q] = q < ne ? src[q] : W(0);
-      }
-    }
-    __syncthreads();
-    if (active) {
-      for (int jb = lane; jb < rows; jb += 64 * 8) {
-        float hv[8];
-#pragma unroll
-        for (int u = 0; u < 8; ++u) {
-          const int j = jb + 64 * u;
-          hv[u] = j < rows ? to_f32(hrow[j0 + j]) : 0.0f;
-        }
-#pragma unroll
-        for (int u = 0; u < 8; ++u) {
-          const int j = jb + 64 * u;
-          if (j < rows) {
-            float wv[kLgBlock];
-#pragma unroll
-            for (int q = 0; q < kLgBlock; ++q) wv[q] = to_f32(tile[j * kLgBlock + q]);
-#pragma unroll
-            for (int q = 0; q < kLgBlock; ++q) acc[q] = fmaf(hv[u], wv[q], acc[q]);
-          }
-        }
-      }
-    }
-    __syncthreads();
-  }
-  if (active) {
-#pragma unroll
-    for (int q = 0; q < kLgBlock; ++q) {
-      float v = acc[q];
-#pragma unroll
-      for (int s = 32; s >= 1; s >>= 1) v = v + __shfl_down(v, s, 64);
-      if (lane == 0 && q < ne) {
-        if (bias != nullptr) v = v + bias[e0 + q];
-        out[static_cast<size_t>(t) * a.E + e0 + q] = v;
-      }
-    }
-  }
-}
-
-hipError_t launch_logits(const LogitsArgs& a, hipStream_t s) {
-  if (a.T <= 0) return hipSuccess;
-  const int nb = (a.E + kLgBlock - 1) / kLgBlock;
-  const int mats = (a.wr != nullptr ? 1 : 0) + (a.wr2 != nullptr ? 1 : 0);
-  if (mats == 0) return hipSuccess;
-  LogitsArgs b = a;
-  if (a.wr == nullptr) {  // only the second router: move it to slot 0
-    b.wr = a.wr2;
-    b.bias = a.bias2;
-    b.logits = a.logits2;
-    b.wr2 = nullptr;
-  }
-  const dim3 grid((a.T + kLgWaves - 1) / kLgWaves, nb * mats);
-  if (a.dtype == kBF16)
-    hipLaunchKernelGGL(logits_kernel<uint16_t>, grid, dim3(64 * kLgWaves), 0, s, b);
-  else
-    hipLaunchKernelGGL(logits_kernel<float>, grid, dim3(64 * kLgWaves), 0, s, b);
-  return hipGetLastError();
-}
-
 // -------------------------------------------------------------------- route
 //
-// One work-group of 16 waves:
+// Route body, run by one work-group of NW waves:
 //  1. selection, one wave per token: K rounds of wave argmax over the
 //     untaken experts (larger logit wins, the lower index on equal logits,
 //     NaN ranks last), then the Eq. (2) weights from exp(logit - max);
 //  2. grouping: stable counting sort of the T*K slots by expert --
-//     histogram, exclusive scan, then blocks of 1024 slots placed in slot
+//     histogram, exclusive scan, then blocks of 64*NW slots placed in slot
 //     order (within a wave by ballot rank, across waves by per-wave counts);
 //  3. ranking of the prediction: per-token softmax of the second logits,
 //     summed over tokens (per wave, then over waves in order), experts
 //     ordered by descending score, lower index first on equal scores.
 
-constexpr int kRouteThreads = 1024;
-constexpr int kRouteWaves = kRouteThreads / 64;
 constexpr int kLanesQ = kMaxExperts / 64;  // expert values held per lane
 
-__global__ __launch_bounds__(kRouteThreads) void route_kernel(RouteArgs a) {
+template <int NW>
+__device__ void route_body(const RouteArgs& a) {
   __shared__ int base[kMaxExperts];
   __shared__ float score_s[kMaxExperts];
-  __shared__ int wbuf[kRouteWaves][kMaxExperts];  // per-wave counts / scores
+  __shared__ int wbuf[NW][kMaxExperts];  // per-wave counts / scores
+  constexpr int NT = 64 * NW;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int E = a.E, K = a.K;
 
   if (a.logits != nullptr) {
     // 1. selection
-    for (int t = wave; t < a.T; t += kRouteWaves) {
+    for (int t = wave; t < a.T; t += NW) {
       const float* lg = a.logits + static_cast<size_t>(t) * E;
       float lv[kLanesQ];
 #pragma unroll
@@ -294,33 +172,48 @@ __global__ __launch_bounds__(kRouteThreads) void route_kernel(RouteArgs a) {
         a.w[static_cast<size_t>(t) * K + lane] = my_ex / z;
       }
     }
-    __threadfence();
+    __threadfence_block();  // idx written above is read back by other waves of this work-group
     __syncthreads();
 
     // 2. grouping
     const int TK = a.T * K;
     int* cnt = &wbuf[0][0];
-    for (int e = tid; e < E; e += kRouteThreads) cnt[e] = 0;
+    for (int e = tid; e < E; e += NT) cnt[e] = 0;
     __syncthreads();
     // indices lie in [0, E) (selection above); the clamp only keeps LDS
     // accesses in bounds whatever the input
-    for (int s = tid; s < TK; s += kRouteThreads) atomicAdd(&cnt[min(max(a.idx[s], 0), E - 1)], 1);
+    for (int s = tid; s < TK; s += NT) atomicAdd(&cnt[min(max(a.idx[s], 0), E - 1)], 1);
     __syncthreads();
-    if (tid == 0) {
+    if (wave == 0) {
+      // exclusive scan over experts, 64 at a time with a wave prefix sum
       int run = 0;
-      for (int e = 0; e < E; ++e) {
-        base[e] = run;
-        a.offsets[e] = run;
-        if (a.host_offsets) a.host_offsets[e] = run;
-        run += cnt[e];
+      for (int e0 = 0; e0 < E; e0 += 64) {
+        const int e = e0 + lane;
+        const int c = e < E ? cnt[e] : 0;
+        int incl = c;
+#pragma unroll
+        for (int s = 1; s < 64; s <<= 1) {
+          const int o = __shfl_up(incl, s, 64);
+          if (lane >= s) incl += o;
+        }
+        if (e < E) {
+          base[e] = run + incl - c;
+          a.offsets[e] = run + incl - c;
+          if (a.host_offsets) a.host_offsets[e] = run + incl - c;
+        }
+        run += __shfl(incl, 63, 64);
       }
-      a.offsets[E] = run;
-      if (a.host_offsets) a.host_offsets[E] = run;
+      if (lane == 0) {
+        a.offsets[E] = run;
+        if (a.host_offsets) a.host_offsets[E] = run;
+      }
+      // the host reads the offsets once this launch completes
+      if (a.host_offsets) __threadfence_system();
     }
     __syncthreads();
     const uint64_t lt = (lane == 0) ? 0ull : ((~0ull) >> (64 - lane));
-    for (int b0 = 0; b0 < TK; b0 += kRouteThreads) {
-      for (int i = tid; i < kRouteWaves * E; i += kRouteThreads) wbuf[i / E][i % E] = 0;
+    for (int b0 = 0; b0 < TK; b0 += NT) {
+      for (int i = tid; i < NW * E; i += NT) wbuf[i / E][i % E] = 0;
       __syncthreads();
       const int s = b0 + tid;
       const int e = (s < TK) ? min(max(a.idx[s], 0), E - 1) : -1;
@@ -342,9 +235,9 @@ __global__ __launch_bounds__(kRouteThreads) void route_kernel(RouteArgs a) {
         a.pos[s] = p;
       }
       __syncthreads();
-      for (int e2 = tid; e2 < E; e2 += kRouteThreads) {
+      for (int e2 = tid; e2 < E; e2 += NT) {
         int add = 0;
-        for (int w2 = 0; w2 < kRouteWaves; ++w2) add += wbuf[w2][e2];
+        for (int w2 = 0; w2 < NW; ++w2) add += wbuf[w2][e2];
         base[e2] += add;
       }
       __syncthreads();
@@ -356,7 +249,7 @@ __global__ __launch_bounds__(kRouteThreads) void route_kernel(RouteArgs a) {
     float acc[kLanesQ];
 #pragma unroll
     for (int q = 0; q < kLanesQ; ++q) acc[q] = 0.0f;
-    for (int t = wave; t < a.T; t += kRouteWaves) {
+    for (int t = wave; t < a.T; t += NW) {
       const float* lg = a.logits_pred + static_cast<size_t>(t) * E;
       float lv[kLanesQ];
       float m = -INFINITY;
@@ -385,13 +278,13 @@ __global__ __launch_bounds__(kRouteThreads) void route_kernel(RouteArgs a) {
     for (int q = 0; q < kLanesQ; ++q)
       if (lane + 64 * q < E) ws[wave * kMaxExperts + lane + 64 * q] = acc[q];
     __syncthreads();
-    for (int e = tid; e < E; e += kRouteThreads) {
+    for (int e = tid; e < E; e += NT) {
       float sc = 0.0f;
-      for (int w2 = 0; w2 < kRouteWaves && w2 < a.T; ++w2) sc += ws[w2 * kMaxExperts + e];
+      for (int w2 = 0; w2 < NW; ++w2) sc += ws[w2 * kMaxExperts + e];
       score_s[e] = sc;
     }
     __syncthreads();
-    for (int e = tid; e < E; e += kRouteThreads) {
+    for (int e = tid; e < E; e += NT) {
       const float v = score_s[e];
       int r = 0;
       for (int o = 0; o < E; ++o) {
@@ -403,12 +296,140 @@ __global__ __launch_bounds__(kRouteThreads) void route_kernel(RouteArgs a) {
       if (a.host_order) a.host_order[r] = e;
       if (a.host_score) a.host_score[e] = v;
     }
+    if (a.host_order && tid < E) __threadfence_system();
   }
-  if (a.host_offsets || a.host_order) __threadfence_system();
 }
 
-hipError_t launch_route(const RouteArgs& a, hipStream_t s) {
-  hipLaunchKernelGGL(route_kernel, dim3(1), dim3(kRouteThreads), 0, s, a);
+constexpr int kRouteWaves = 16;
+
+__global__ __launch_bounds__(64 * kRouteWaves) void route_kernel(RouteArgs a) { route_body<kRouteWaves>(a); }
+
+// ------------------------------------------------------------------- logits
+//
+// A logit is computed in the fixed fp32 order that makes the selection
+// reproducible: lane l accumulates h[j] * w[j][e] with fma over
+// j = l, l+64, ... ascending, then lane partials are added in a halving tree
+// that pairs lane l with lane l+s for s = 32, 16, ..., 1 (lane 0 ends with
+// the result); a bias is added once afterwards.
+//
+// Work-group = 4 waves = 4 tokens x one block of 8 experts of one router.
+// The block's weight columns are staged in LDS tile by tile (all 256 threads
+// load), then each wave runs its token's fma chains from LDS.
+
+constexpr int kLgWaves = 4;
+constexpr int kLgBlock = 8;           // experts per work-group
+constexpr int kLgTileBytes = 32768;   // LDS tile of router rows
+
+template <typename W>
+__global__ __launch_bounds__(64 * kLgWaves) void logits_kernel(LogitsArgs a) {
+  __shared__ __align__(16) W tile[kLgTileBytes / sizeof(W)];
+  constexpr int RT = kLgTileBytes / (kLgBlock * sizeof(W));  // rows per tile (multiple of 64)
+  constexpr int NV = static_cast<int>(kLgBlock * sizeof(W)) / 16;  // 16-byte pieces per tile row
+  constexpr int RB = RT / (64 * kLgWaves);                           // tile rows per thread
+  constexpr int HR = RT / 64;                                        // tile rows per lane
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int nb = (a.E + kLgBlock - 1) / kLgBlock;
+  const int mat = blockIdx.y / nb, eb = blockIdx.y - mat * nb;
+  const W* wr = static_cast<const W*>(mat == 0 ? a.wr : a.wr2);
+  const float* bias = mat == 0 ? a.bias : a.bias2;
+  float* out = mat == 0 ? a.logits : a.logits2;
+  const int e0 = eb * kLgBlock, ne = min(kLgBlock, a.E - e0);
+  const bool vec = (ne == kLgBlock) && ((a.E * static_cast<int>(sizeof(W))) % 16 == 0);
+  const int t = blockIdx.x * kLgWaves + wave;
+  const bool active = t < a.T;
+  const W* hrow = static_cast<const W*>(a.h) + static_cast<size_t>(active ? t : 0) * a.d;
+  float acc[kLgBlock];
+#pragma unroll
+  for (int q = 0; q < kLgBlock; ++q) acc[q] = 0.0f;
+
+  for (int j0 = 0; j0 < a.d; j0 += RT) {
+    const int rows = min(RT, a.d - j0);
+    // this lane's activations for the tile (rows j0 + lane + 64 m); every
+    // load is issued (clamped into the row), unused values are zeroed
+    float hv[HR];
+#pragma unroll
+    for (int m = 0; m < HR; ++m) hv[m] = to_f32(hrow[j0 + min(lane + 64 * m, rows - 1)]);
+#pragma unroll
+    for (int m = 0; m < HR; ++m)
+      if (lane + 64 * m >= rows) hv[m] = 0.0f;
+    if (vec) {
+      // all of this thread's row loads first, then the LDS stores
+      uint4 buf[RB][NV];
+#pragma unroll
+      for (int u = 0; u < RB; ++u) {
+        const int r = min(tid + 64 * kLgWaves * u, rows - 1);
+        const uint4* src = reinterpret_cast<const uint4*>(wr + static_cast<size_t>(j0 + r) * a.E + e0);
+#pragma unroll
+        for (int b = 0; b < NV; ++b) buf[u][b] = src[b];
+      }
+#pragma unroll
+      for (int u = 0; u < RB; ++u) {
+        const int r = tid + 64 * kLgWaves * u;
+        if (r < rows) {
+#pragma unroll
+          for (int b = 0; b < NV; ++b) reinterpret_cast<uint4*>(tile + r * kLgBlock)[b] = buf[u][b];
+        }
+      }
+    } else {
+      for (int r = tid; r < rows; r += 64 * kLgWaves) {
+        const W* src = wr + static_cast<size_t>(j0 + r) * a.E + e0;
+#pragma unroll
+        for (int q = 0; q < kLgBlock; ++q) tile[r * kLgBlock + q] = q < ne ? src[q] : W(0);
+      }
+    }
+    __syncthreads();
+    if (active) {
+#pragma unroll
+      for (int m = 0; m < HR; ++m) {
+        const int j = min(lane + 64 * m, rows - 1);
+        if (lane + 64 * m < rows) {
+          float wv[kLgBlock];
+#pragma unroll
+          for (int q = 0; q < kLgBlock; ++q) wv[q] = to_f32(tile[j * kLgBlock + q]);
+#pragma unroll
+          for (int q = 0; q < kLgBlock; ++q) acc[q] = fmaf(hv[m], wv[q], acc[q]);
+        }
+      }
+    }
+    __syncthreads();
+  }
+  if (active) {
+#pragma unroll
+    for (int q = 0; q < kLgBlock; ++q) {
+      float v = acc[q];
+#pragma unroll
+      for (int s = 32; s >= 1; s >>= 1) v = v + __shfl_down(v, s, 64);
+      if (lane == 0 && q < ne) {
+        if (bias != nullptr) v = v + bias[e0 + q];
+        out[static_cast<size_t>(t) * a.E + e0 + q] = v;
+      }
+    }
+  }
+}
+
+// Logits launch, then the route launch (a kernel boundary, not a device-
+// scope fence, hands the logits over: with one L2 per XCD such fences write
+// back and invalidate L2 and cost far more than a launch).
+hipError_t launch_logits_route(const LogitsArgs& a, const RouteArgs& ra, hipStream_t s) {
+  if (a.T <= 0) return hipSuccess;
+  const int nb = (a.E + kLgBlock - 1) / kLgBlock;
+  const int mats = (a.wr != nullptr ? 1 : 0) + (a.wr2 != nullptr ? 1 : 0);
+  if (mats == 0) return hipErrorInvalidValue;
+  LogitsArgs b = a;
+  if (a.wr == nullptr) {  // only the second router: move it to slot 0
+    b.wr = a.wr2;
+    b.bias = a.bias2;
+    b.logits = a.logits2;
+    b.wr2 = nullptr;
+  }
+  const dim3 grid((a.T + kLgWaves - 1) / kLgWaves, nb * mats);
+  if (a.dtype == kBF16)
+    hipLaunchKernelGGL(logits_kernel<uint16_t>, grid, dim3(64 * kLgWaves), 0, s, b);
+  else
+    hipLaunchKernelGGL(logits_kernel<float>, grid, dim3(64 * kLgWaves), 0, s, b);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(route_kernel, dim3(1), dim3(64 * kRouteWaves), 0, s, ra);
   return hipGetLastError();
 }
 
@@ -465,7 +486,8 @@ __global__ __launch_bounds__(UPW * kLpu) void ffn_chunk_kernel(FfnArgs a) {
   const W* U = G + cd;
   const W* D = U + cd;
   float* part = routed ? a.part : a.part_sh + static_cast<size_t>(-1 - tk.expert) * a.sh_plane;
-  const int rows = routed ? a.rows_routed : a.rows_shared;
+  // partial layout [row][plane][d]: one slot's planes are contiguous
+  const int a_planes = routed ? a.n_planes : a.n_planes_sh;
   const int plane = c * a.subs + sub;
 
   W* hs = reinterpret_cast<W*>(ffn_smem);                                  // [NT][d]
@@ -587,7 +609,7 @@ __global__ __launch_bounds__(UPW * kLpu) void ffn_chunk_kernel(FfnArgs a) {
       for (int t = 0; t < NT; ++t) {
         if (t < nt) {
           const int row = routed ? (p0 + tile + t) : (tile + t);
-          float* dst = part + (static_cast<size_t>(plane) * rows + row) * d;
+          float* dst = part + (static_cast<size_t>(row) * a_planes + plane) * d;
 #pragma unroll
           for (int q = 0; q < Q; ++q) {
             const int col = (tid + THREADS * q) * VEC;
@@ -665,66 +687,113 @@ hipError_t launch_ffn(const FfnArgs& a, int max_tok, hipStream_t s) {
 
 // ------------------------------------------------------------------ combine
 //
-// One work-group of 16 waves per (token, 256 columns).  Wave w sums chunks
-// c = w, w+16, ... of one (token, k) partial; the 16 wave sums are added in
-// wave order; the k terms are added in selection order with their gate
-// weights, then the shared experts in index order.  The order is fixed, so
-// the output is the same whichever stream or launch produced each chunk.
+// Two launches with a fixed summation order (so the output is the same
+// whichever stream or launch produced each partial plane):
+//  1. work-group (term slot, 256 columns, plane group g): wave w sums planes
+//     p = 4 g + w + 4 G j (j ascending, four interleaved accumulators added
+//     in order); the four wave sums are added in wave order -> red[g][slot];
+//  2. per (token, 256 columns): S_term = sum_g red[g][slot] (g ascending),
+//     y[t] = sum_k w[t][k] * S_k in selection order, then + the shared
+//     experts' S_s in index order.
 
-constexpr int kCombineWaves = 16;
+constexpr int kCombWaves = 4;
+constexpr int kCombMaxGroups = 16;
 
 __device__ __forceinline__ float4 f4add(float4 x, float4 y) {
   return make_float4(x.x + y.x, x.y + y.y, x.z + y.z, x.w + y.w);
 }
 
-__global__ __launch_bounds__(64 * kCombineWaves) void combine_kernel(CombineArgs a) {
-  __shared__ float4 red[kCombineWaves][64];
-  const int t = blockIdx.x;
+__global__ __launch_bounds__(64 * kCombWaves) void combine_planes_kernel(CombineArgs a) {
+  __shared__ float4 red4[kCombWaves][64];
+  const int ts = blockIdx.x, cb = blockIdx.y, pg = blockIdx.z;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int col = blockIdx.y * 256 + lane * 4;
+  const int col = cb * 256 + lane * 4;
   const bool live = col < a.d;
-  float4 y = make_float4(0.f, 0.f, 0.f, 0.f);
-  const int n_terms = a.K + a.n_shared;
-  for (int term = 0; term < n_terms; ++term) {
-    const bool routed = term < a.K;
-    const float* base;
-    int row, rows, nch;
-    if (routed) {
-      base = a.part;
-      row = a.pos[t * a.K + term];
-      rows = a.rows_routed;
-      nch = a.n_planes;
-    } else {
-      base = a.part_sh + static_cast<size_t>(term - a.K) * a.sh_plane;
-      row = t;
-      rows = a.rows_shared;
-      nch = a.n_planes_sh;
-    }
-    float4 s = make_float4(0.f, 0.f, 0.f, 0.f);
-    if (live)
-      for (int c = wave; c < nch; c += kCombineWaves)
-        s = f4add(s, *reinterpret_cast<const float4*>(base + (static_cast<size_t>(c) * rows + row) * a.d + col));
-    red[wave][lane] = s;
-    __syncthreads();
-    if (wave == 0) {
-      float4 tot = red[0][lane];
-      for (int w2 = 1; w2 < kCombineWaves; ++w2) tot = f4add(tot, red[w2][lane]);
-      if (routed) {
-        const float wk = a.w[t * a.K + term];
-        y = make_float4(fmaf(wk, tot.x, y.x), fmaf(wk, tot.y, y.y), fmaf(wk, tot.z, y.z), fmaf(wk, tot.w, y.w));
-      } else {
-        y = f4add(y, tot);
-      }
-    }
-    __syncthreads();
+  const int TK = a.T * a.K;
+  const int n_slots = TK + a.T * a.n_shared;
+  const float* base;
+  int row, np;
+  if (ts < TK) {
+    base = a.part;
+    row = a.pos[ts];
+    np = a.n_planes;
+  } else {
+    const int si = ts - TK;
+    const int t = si / a.n_shared;
+    const int sh = si - t * a.n_shared;
+    base = a.part_sh + static_cast<size_t>(sh) * a.sh_plane;
+    row = t;
+    np = a.n_planes_sh;
   }
-  if (wave == 0 && live) *reinterpret_cast<float4*>(a.y + static_cast<size_t>(t) * a.d + col) = y;
+  float4 acc[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) acc[i] = make_float4(0.f, 0.f, 0.f, 0.f);
+  if (live) {
+    const float* rbase = base + static_cast<size_t>(row) * np * a.d + col;  // this slot's contiguous planes
+    const int stride = kCombWaves * a.pg;
+    for (int p0 = pg * kCombWaves + wave; p0 < np; p0 += 4 * stride) {
+      float4 v[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i)  // clamped loads, unused ones dropped below
+        v[i] = *reinterpret_cast<const float4*>(rbase + static_cast<size_t>(min(p0 + i * stride, np - 1)) * a.d);
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+        if (p0 + i * stride < np) acc[i] = f4add(acc[i], v[i]);
+    }
+  }
+  red4[wave][lane] = f4add(f4add(acc[0], acc[1]), f4add(acc[2], acc[3]));
+  __syncthreads();
+  if (wave == 0 && live) {
+    float4 tot = red4[0][lane];
+    for (int w2 = 1; w2 < kCombWaves; ++w2) tot = f4add(tot, red4[w2][lane]);
+    *reinterpret_cast<float4*>(a.red + (static_cast<size_t>(pg) * n_slots + ts) * a.d + col) = tot;
+  }
+}
+
+__global__ __launch_bounds__(64) void combine_final_kernel(CombineArgs a) {
+  const int t = blockIdx.x;
+  const int col = blockIdx.y * 256 + threadIdx.x * 4;
+  if (col >= a.d) return;
+  const int TK = a.T * a.K;
+  const int n_slots = TK + a.T * a.n_shared;
+  float4 y = make_float4(0.f, 0.f, 0.f, 0.f);
+  for (int term = 0; term < a.K + a.n_shared; ++term) {
+    const int slot = term < a.K ? t * a.K + term : TK + t * a.n_shared + (term - a.K);
+    float4 v[kCombMaxGroups];
+#pragma unroll
+    for (int g = 0; g < kCombMaxGroups; ++g)  // clamped loads, unused ones dropped below
+      v[g] = *reinterpret_cast<const float4*>(a.red + (static_cast<size_t>(min(g, a.pg - 1)) * n_slots + slot) * a.d + col);
+    float4 sum = v[0];
+#pragma unroll
+    for (int g = 1; g < kCombMaxGroups; ++g)
+      if (g < a.pg) sum = f4add(sum, v[g]);
+    if (term < a.K) {
+      const float wk = a.w[t * a.K + term];
+      y = make_float4(fmaf(wk, sum.x, y.x), fmaf(wk, sum.y, y.y), fmaf(wk, sum.z, y.z), fmaf(wk, sum.w, y.w));
+    } else {
+      y = f4add(y, sum);
+    }
+  }
+  *reinterpret_cast<float4*>(a.y + static_cast<size_t>(t) * a.d + col) = y;
+}
+
+int combine_groups(int T, int K, int n_shared, int d, int n_planes) {
+  const int slots = T * (K + n_shared);
+  const int ncb = (d + 255) / 256;
+  int g = 1;
+  while (g < kCombMaxGroups && static_cast<int64_t>(slots) * ncb * g * 2 <= 512 && g * 2 * kCombWaves <= n_planes)
+    g *= 2;
+  return g;
 }
 
 hipError_t launch_combine(const CombineArgs& a, hipStream_t s) {
   if (a.T <= 0) return hipSuccess;
-  const dim3 grid(a.T, (a.d + 255) / 256);
-  hipLaunchKernelGGL(combine_kernel, grid, dim3(64 * kCombineWaves), 0, s, a);
+  const int ncb = (a.d + 255) / 256;
+  const int slots = a.T * (a.K + a.n_shared);
+  hipLaunchKernelGGL(combine_planes_kernel, dim3(slots, ncb, a.pg), dim3(64 * kCombWaves), 0, s, a);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(combine_final_kernel, dim3(a.T, ncb), dim3(64), 0, s, a);
   return hipGetLastError();
 }
 

@@ -40,7 +40,7 @@ struct Shape {
   int group_chunks;  // chunks per H2D copy group
   // fixed pool layout (byte offsets)
   uint64_t off_router, off_bias, off_shared, off_logits, off_logits2, off_offsets, off_perm, off_pos;
-  uint64_t off_part, off_part_sh, off_score, off_order, off_buffer, fixed_bytes;
+  uint64_t off_part, off_part_sh, off_red, off_score, off_order, off_buffer, fixed_bytes;
   uint64_t router_stride, bias_stride, part_bytes, part_sh_bytes;
   int64_t sh_plane;
 };
@@ -125,6 +125,14 @@ ms_status derive_shape(const ms_model_desc* d, Shape* s, std::string* err) {
   s->part_sh_bytes = static_cast<uint64_t>(s->sh_plane) * 4 * s->n_sh;
   s->off_part_sh = off;
   off += align_up(s->part_sh_bytes, kAlign);
+  // first-pass combine sums [pg][T*(K+n_shared)][d]: with one plane group
+  // that is the slots of max_T tokens; with more, pg * slots * ceil(d/256)
+  // stays <= 1024 (combine_groups)
+  const uint64_t red_bytes = std::max<uint64_t>(static_cast<uint64_t>(s->max_T) * (s->K + s->n_sh),
+                                                512 / ((s->d + 255) / 256)) * s->d * 4;
+  s->off_red = off;
+  off += align_up(red_bytes, kAlign);
+
   s->off_score = off;
   off += align_up(static_cast<uint64_t>(s->E) * 4, kAlign);
   s->off_order = off;
@@ -896,9 +904,6 @@ ms_status ms_predict(ms_ctx* ctx, int32_t layer, const void* h_dev, int32_t T, v
   la.wr2 = ctx->dev(s.off_router + s.router_stride * layer);
   la.bias2 = L.bias_set ? reinterpret_cast<const float*>(ctx->dev(s.off_bias + s.bias_stride * layer)) : nullptr;
   la.logits2 = reinterpret_cast<float*>(ctx->dev(s.off_logits2));
-  int ti = tl_begin(ctx, sm, MS_IV_ROUTER, layer, static_cast<uint64_t>(s.d) * s.E * s.elem);
-  MS_HIP(msk::launch_logits(la, sm));
-  tl_end(ctx, ti, sm);
   msk::RouteArgs rk{};
   rk.T = T;
   rk.E = s.E;
@@ -909,8 +914,8 @@ ms_status ms_predict(ms_ctx* ctx, int32_t layer, const void* h_dev, int32_t T, v
   rk.order = reinterpret_cast<int32_t*>(ctx->dev(s.off_order));
   rk.host_score = ctx->d_score_map;
   rk.host_order = ctx->d_order_map;
-  ti = tl_begin(ctx, sm, MS_IV_PREDICT, layer, 0);
-  MS_HIP(msk::launch_route(rk, sm));
+  int ti = tl_begin(ctx, sm, MS_IV_PREDICT, layer, static_cast<uint64_t>(s.d) * s.E * s.elem);
+  MS_HIP(msk::launch_logits_route(la, rk, sm));
   tl_end(ctx, ti, sm);
   MS_HIP(hipEventRecord(ctx->ev_last, sm));
   ctx->has_last = true;
@@ -980,9 +985,6 @@ ms_status ms_forward(ms_ctx* ctx, int32_t layer, const void* h_dev, int32_t T, f
     la.logits2 = reinterpret_cast<float*>(ctx->dev(s.off_logits2));
   }
   const uint64_t router_bytes = static_cast<uint64_t>(s.d) * s.E * s.elem * (predict_next ? 2 : 1);
-  int ti = tl_begin(ctx, sm, MS_IV_ROUTER, layer, router_bytes);
-  MS_HIP(msk::launch_logits(la, sm));
-  tl_end(ctx, ti, sm);
 
   msk::RouteArgs ga{};
   ga.T = T;
@@ -1003,8 +1005,8 @@ ms_status ms_forward(ms_ctx* ctx, int32_t layer, const void* h_dev, int32_t T, f
     ga.host_score = ctx->d_score_map;
     ga.host_order = ctx->d_order_map;
   }
-  ti = tl_begin(ctx, sm, MS_IV_GROUP, layer, 0);
-  MS_HIP(msk::launch_route(ga, sm));
+  int ti = tl_begin(ctx, sm, MS_IV_ROUTER, layer, router_bytes);
+  MS_HIP(msk::launch_logits_route(la, ga, sm));
   tl_end(ctx, ti, sm);
   MS_HIP(hipEventRecord(ctx->ev_route, sm));
 
@@ -1027,6 +1029,8 @@ ms_status ms_forward(ms_ctx* ctx, int32_t layer, const void* h_dev, int32_t T, f
   fa.T = T;
   fa.dtype = s.dtype;
   fa.subs = s.subs;
+  fa.n_planes = s.n_chunks * s.subs;
+  fa.n_planes_sh = s.n_chunks_sh * s.subs;
   std::vector<msk::FfnTask> res_tasks;
   for (int e = 0; e < s.E; ++e) {
     const int rc = resident_chunks(L, e);
@@ -1279,6 +1283,8 @@ ms_status ms_forward(ms_ctx* ctx, int32_t layer, const void* h_dev, int32_t T, f
   ca.rows_shared = s.max_T;
   ca.n_planes = s.n_chunks * s.subs;
   ca.n_planes_sh = s.n_chunks_sh * s.subs;
+  ca.red = reinterpret_cast<float*>(ctx->dev(s.off_red));
+  ca.pg = msk::combine_groups(T, s.K, s.n_sh, s.d, s.n_chunks * s.subs);
   ca.n_shared = s.n_sh;
   ca.T = T;
   ca.K = s.K;
