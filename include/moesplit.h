@@ -122,7 +122,8 @@ typedef enum {
   MS_IV_COPY_MISS = 5,     /* H2D copy issued after routing                      */
   MS_IV_COPY_PREFETCH = 6, /* H2D copy issued by prefetch                        */
   MS_IV_COPY_TOP = 7,      /* H2D copy of a top segment (ms_load_top)            */
-  MS_IV_PREDICT = 8        /* prediction ranking kernel                          */
+  MS_IV_PREDICT = 8,       /* prediction ranking kernel                          */
+  MS_IV_FFN_DOWN = 9       /* matrix-core down-projection (prefill path)         */
 } ms_interval_kind;
 
 typedef struct {
@@ -237,6 +238,11 @@ ms_status ms_prefetch(ms_ctx* ctx, int32_t layer, const int32_t* experts, int32_
                                   layer (layer+1, or layer 0 of the next token
                                   after the last layer) from this layer's h and
                                   prefetch its experts (Sec. 3.2)            */
+#define MS_FWD_MATRIX_CORES 2  /* force the prefill path: gate/up and down
+                                  projections on the matrix cores (bf16 only) */
+#define MS_FWD_NO_MATRIX_CORES 4 /* force the decode path (chunk kernel)    */
+/* Without either flag a bf16 forward takes the prefill path when
+ * T * top_k >= 8 * n_experts (on average >= 8 tokens per expert). */
 
 /* MoE module of layer i (Eq. (2) without residual and Norm) on T tokens,
  * 0 <= T <= max_tokens:

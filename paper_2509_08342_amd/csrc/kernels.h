@@ -90,6 +90,48 @@ struct FfnArgs {
 // Launches n_wg work-groups; max_tok bounds the tokens of any task.
 hipError_t launch_ffn(const FfnArgs& a, int max_tok, hipStream_t s);
 
+// Prefill (many tokens per expert) runs on the matrix cores in two steps:
+//  gate/up (mma_gateup): act[row][f] = bf16(silu(h_row . G_f) * (h_row . U_f))
+//    for a task's chunk range, 64 rows x 64 units per work-group; runs per
+//    segment as data lands (disjoint columns of act);
+//  down (mma_down): out[row][:] = sum_f act[row][f] * D_f over all of the
+//    expert's chunks (chunks < split at base, the rest at base2), 64 rows x
+//    128 columns per work-group, written as the single partial plane.
+constexpr int kMaxMmaTasks = 80;
+constexpr int kMmaRows = 64;     // rows (token slots) per work-group
+constexpr int kMmaCols = 128;    // output columns per down work-group
+
+struct MmaTask {
+  const unsigned char* base;   // chunk c at base + c * chunk_bytes
+  const unsigned char* base2;  // down: chunks >= split at base2 + c * chunk_bytes
+  int32_t expert;              // >= 0 routed expert; -1 - s shared expert s
+  int32_t chunk_lo;            // gate/up: first chunk
+  int32_t n_chunks;            // gate/up: chunks in the task; down: all chunks
+  int32_t split;               // down: first chunk read from base2
+  int32_t wg_begin;
+  int32_t m_tiles;             // row tiles of this task
+};
+
+struct MmaArgs {
+  const void* h;               // [T][d] bf16
+  const int32_t* offsets;      // [E+1]
+  const int32_t* perm;         // [TK]
+  uint16_t* act;               // routed [rows_routed][f_pad] bf16
+  uint16_t* act_sh;            // shared [n_shared][rows_shared][f_pad_sh] bf16
+  float* part;                 // down output, routed [rows_routed][d] (one plane)
+  float* part_sh;              // shared [n_shared] planes of sh_plane floats
+  uint64_t chunk_bytes;
+  int64_t sh_plane;
+  int32_t d, K, T;
+  int32_t f_pad, f_pad_sh;     // act row strides (chunks * 64)
+  int32_t rows_shared;         // shared rows per expert (max T)
+  int32_t n_tasks, n_wg;
+  int32_t ncb;                 // down: column blocks (ceil(d / kMmaCols))
+  MmaTask tasks[kMaxMmaTasks];
+};
+hipError_t launch_mma_gateup(const MmaArgs& a, hipStream_t s);
+hipError_t launch_mma_down(const MmaArgs& a, hipStream_t s);
+
 // y[t] = sum_k w[t][k] * sum_c part[c][pos[t*K+k]] + sum_s sum_c part_sh[s][c][t],
 // c over the partial planes (chunks * subs), in two launches: a first pass
 // over plane groups into `red`, then the weighted sum per token.

@@ -685,6 +685,201 @@ hipError_t launch_ffn(const FfnArgs& a, int max_tok, hipStream_t s) {
   return (a.dtype == kBF16) ? launch_ffn_w<uint16_t>(a, max_tok, s) : launch_ffn_w<float>(a, max_tok, s);
 }
 
+// ------------------------------------------------------------ prefill MFMA
+//
+// v_mfma_f32_16x16x32_bf16: lane l holds A[row l%16][8 k from 8*(l/16)],
+// B[8 k from 8*(l/16)][column l%16] and the result C[rows 4*(l/16)+r][column
+// l%16].  The k order inside a step is the same for A and B, which is all
+// the contraction needs.
+
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ bf16x8_t as_bf16x8(uint4 v) { return __builtin_bit_cast(bf16x8_t, v); }
+
+__device__ __forceinline__ f32x4_t mfma16(bf16x8_t a, bf16x8_t b, f32x4_t c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+}
+
+// fp32 -> bf16, round to nearest even (finite values)
+__device__ __forceinline__ uint16_t f2bf(float f) {
+  const uint32_t u = __float_as_uint(f);
+  return static_cast<uint16_t>((u + 0x7fffu + ((u >> 16) & 1u)) >> 16);
+}
+
+__device__ __forceinline__ int find_task(const MmaTask* tasks, int n, int wg) {
+  int ti = 0;
+  for (int i = 1; i < n; ++i)
+    if (tasks[i].wg_begin <= wg) ti = i;
+  return ti;
+}
+
+// Rows of a task's row tile: routed experts take grouped positions
+// [offsets[e] + 64 mt, ...), shared experts take tokens [64 mt, ...).
+struct TileRows {
+  int p0, n;
+};
+__device__ __forceinline__ TileRows tile_rows(const MmaArgs& a, const MmaTask& tk, int mt) {
+  TileRows r;
+  if (tk.expert >= 0) {
+    const int b = a.offsets[tk.expert], e = a.offsets[tk.expert + 1];
+    r.p0 = b + mt * kMmaRows;
+    r.n = min(kMmaRows, e - r.p0);
+  } else {
+    r.p0 = mt * kMmaRows;
+    r.n = min(kMmaRows, a.T - r.p0);
+  }
+  return r;
+}
+
+__global__ __launch_bounds__(256) void mma_gateup_kernel(MmaArgs a) {
+  const int wg = blockIdx.x;
+  const MmaTask tk = a.tasks[find_task(a.tasks, a.n_tasks, wg)];
+  const int local = wg - tk.wg_begin;
+  const int mt = local % tk.m_tiles;
+  const int c = tk.chunk_lo + local / tk.m_tiles;
+  const TileRows tr = tile_rows(a, tk, mt);
+  if (tr.n <= 0) return;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int d = a.d;
+  const bool routed = tk.expert >= 0;
+  // this lane's A row: tile row 16 wave + lane % 16 (clamped; masked at the end)
+  const int ar = min(16 * wave + (lane & 15), tr.n - 1);
+  const int tok = routed ? a.perm[tr.p0 + ar] / a.K : tr.p0 + ar;
+  const uint16_t* hrow = static_cast<const uint16_t*>(a.h) + static_cast<size_t>(tok) * d;
+  const uint16_t* G = reinterpret_cast<const uint16_t*>(tk.base + static_cast<size_t>(c) * a.chunk_bytes);
+  const uint16_t* U = G + static_cast<size_t>(kChunkUnits) * d;
+  const int kq = 8 * (lane >> 4);  // this lane's k offset inside a 32-wide step
+  f32x4_t ag[4], au[4];
+#pragma unroll
+  for (int nf = 0; nf < 4; ++nf) ag[nf] = au[nf] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  constexpr int KB = 2;  // k steps loaded per batch
+  for (int k0 = 0; k0 < d; k0 += 32 * KB) {
+    uint4 av[KB], gv[KB][4], uv[KB][4];
+#pragma unroll
+    for (int s = 0; s < KB; ++s) {
+      const int k = min(k0 + 32 * s, d - 32);
+      av[s] = ld16(hrow + k + kq);
+#pragma unroll
+      for (int nf = 0; nf < 4; ++nf) {
+        const int unit = 16 * nf + (lane & 15);
+        const size_t off = (static_cast<size_t>(k / kKTile) * kChunkUnits + unit) * kKTile + (k % kKTile) + kq;
+        gv[s][nf] = ldw16(G + off);
+        uv[s][nf] = ldw16(U + off);
+      }
+    }
+#pragma unroll
+    for (int s = 0; s < KB; ++s) {
+      if (k0 + 32 * s < d) {
+        const bf16x8_t A = as_bf16x8(av[s]);
+#pragma unroll
+        for (int nf = 0; nf < 4; ++nf) {
+          ag[nf] = mfma16(A, as_bf16x8(gv[s][nf]), ag[nf]);
+          au[nf] = mfma16(A, as_bf16x8(uv[s][nf]), au[nf]);
+        }
+      }
+    }
+  }
+  // epilogue: act = silu(g) * u as bf16, rows 4*(lane/16)+r of this wave's 16
+  uint16_t* act = routed ? a.act : a.act_sh + static_cast<size_t>(-1 - tk.expert) * a.rows_shared * a.f_pad_sh;
+  const int f_pad = routed ? a.f_pad : a.f_pad_sh;
+#pragma unroll
+  for (int nf = 0; nf < 4; ++nf) {
+    const int f = c * kChunkUnits + 16 * nf + (lane & 15);
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int row = 16 * wave + 4 * (lane >> 4) + r;
+      if (row < tr.n) {
+        const float g = ag[nf][r], u = au[nf][r];
+        act[static_cast<size_t>(tr.p0 + row) * f_pad + f] = f2bf(silu(g) * u);
+      }
+    }
+  }
+}
+
+__global__ __launch_bounds__(256) void mma_down_kernel(MmaArgs a) {
+  constexpr int PITCH = kChunkUnits + 8;  // transposed D tile row: 64 units + pad
+  __shared__ __align__(16) uint16_t dt[kMmaCols * PITCH];
+  const int wg = blockIdx.x;
+  const MmaTask tk = a.tasks[find_task(a.tasks, a.n_tasks, wg)];
+  const int local = wg - tk.wg_begin;
+  const int mt = local / a.ncb, cb = local % a.ncb;
+  const TileRows tr = tile_rows(a, tk, mt);
+  if (tr.n <= 0) return;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int d = a.d;
+  const bool routed = tk.expert >= 0;
+  const uint16_t* act = routed ? a.act : a.act_sh + static_cast<size_t>(-1 - tk.expert) * a.rows_shared * a.f_pad_sh;
+  const int f_pad = routed ? a.f_pad : a.f_pad_sh;
+  const int ar = min(16 * wave + (lane & 15), tr.n - 1);
+  const uint16_t* arow = act + static_cast<size_t>(tr.p0 + ar) * f_pad;
+  const int kq = 8 * (lane >> 4);
+  const int col0 = cb * kMmaCols;
+  f32x4_t acc[8];
+#pragma unroll
+  for (int nf = 0; nf < 8; ++nf) acc[nf] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  for (int c = 0; c < tk.n_chunks; ++c) {
+    const unsigned char* cbase = (c < tk.split ? tk.base : tk.base2) + static_cast<size_t>(c) * a.chunk_bytes;
+    const uint16_t* D = reinterpret_cast<const uint16_t*>(cbase) + 2 * static_cast<size_t>(kChunkUnits) * d;
+    // stage D[64 units][128 columns] transposed: dt[column][unit]
+    uint4 dv[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int piece = tid + 256 * i;           // 64 units x 16 pieces of 8 columns
+      const int f = piece >> 4, q = piece & 15;
+      const int col = min(col0 + 8 * q, d - 8);  // clamped; columns past d are never stored
+      dv[i] = ld16(D + static_cast<size_t>(f) * d + col);
+    }
+    __syncthreads();  // previous chunk's readers are done with dt
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int piece = tid + 256 * i;
+      const int f = piece >> 4, q = piece & 15;
+      const uint32_t w4[4] = {dv[i].x, dv[i].y, dv[i].z, dv[i].w};
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        dt[(8 * q + 2 * j) * PITCH + f] = static_cast<uint16_t>(w4[j] & 0xffffu);
+        dt[(8 * q + 2 * j + 1) * PITCH + f] = static_cast<uint16_t>(w4[j] >> 16);
+      }
+    }
+    __syncthreads();
+#pragma unroll
+    for (int ks = 0; ks < 2; ++ks) {
+      const bf16x8_t A = as_bf16x8(ld16(arow + c * kChunkUnits + 32 * ks + kq));
+#pragma unroll
+      for (int nf = 0; nf < 8; ++nf) {
+        const uint4 bv = *reinterpret_cast<const uint4*>(&dt[(16 * nf + (lane & 15)) * PITCH + 32 * ks + kq]);
+        acc[nf] = mfma16(A, as_bf16x8(bv), acc[nf]);
+      }
+    }
+  }
+  // epilogue: fp32 rows of the single partial plane
+  float* out = routed ? a.part : a.part_sh + static_cast<size_t>(-1 - tk.expert) * a.sh_plane;
+#pragma unroll
+  for (int nf = 0; nf < 8; ++nf) {
+    const int col = col0 + 16 * nf + (lane & 15);
+    if (col < d) {
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int row = 16 * wave + 4 * (lane >> 4) + r;
+        if (row < tr.n) out[static_cast<size_t>(tr.p0 + row) * d + col] = acc[nf][r];
+      }
+    }
+  }
+}
+
+hipError_t launch_mma_gateup(const MmaArgs& a, hipStream_t s) {
+  if (a.n_wg <= 0 || a.n_tasks <= 0) return hipSuccess;
+  hipLaunchKernelGGL(mma_gateup_kernel, dim3(a.n_wg), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_mma_down(const MmaArgs& a, hipStream_t s) {
+  if (a.n_wg <= 0 || a.n_tasks <= 0) return hipSuccess;
+  hipLaunchKernelGGL(mma_down_kernel, dim3(a.n_wg), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
 // ------------------------------------------------------------------ combine
 //
 // Two launches with a fixed summation order (so the output is the same

@@ -40,7 +40,7 @@ struct Shape {
   int group_chunks;  // chunks per H2D copy group
   // fixed pool layout (byte offsets)
   uint64_t off_router, off_bias, off_shared, off_logits, off_logits2, off_offsets, off_perm, off_pos;
-  uint64_t off_part, off_part_sh, off_red, off_score, off_order, off_buffer, fixed_bytes;
+  uint64_t off_part, off_part_sh, off_red, off_act, off_act_sh, off_score, off_order, off_buffer, fixed_bytes;
   uint64_t router_stride, bias_stride, part_bytes, part_sh_bytes;
   int64_t sh_plane;
 };
@@ -132,6 +132,15 @@ ms_status derive_shape(const ms_model_desc* d, Shape* s, std::string* err) {
                                                 512 / ((s->d + 255) / 256)) * s->d * 4;
   s->off_red = off;
   off += align_up(red_bytes, kAlign);
+  // prefill path (bf16): SwiGLU activations [rows][chunks * 64] per routed
+  // slot and per shared expert and token
+  s->off_act = off;
+  s->off_act_sh = off;
+  if (s->dtype == MS_BF16) {
+    off += align_up(TK * s->n_chunks * kUnits * 2, kAlign);
+    s->off_act_sh = off;
+    off += align_up(static_cast<uint64_t>(s->n_sh) * s->max_T * s->n_chunks_sh * kUnits * 2, kAlign);
+  }
 
   s->off_score = off;
   off += align_up(static_cast<uint64_t>(s->E) * 4, kAlign);
@@ -529,6 +538,189 @@ ms_status check_layer(ms_ctx* ctx, int layer) {
 // context (they share the work buffers).
 ms_status order_after_last(ms_ctx* ctx, hipStream_t stream) {
   if (ctx->has_last && ctx->last_stream != stream) MS_HIP(hipStreamWaitEvent(stream, ctx->ev_last, 0));
+  return MS_OK;
+}
+
+// Prefill path of one forward, after the host has the routing (offsets).
+// Matrix-core gate/up writes bf16 activations per routed slot (and per token
+// for shared experts); the down projection runs once all of an expert's
+// chunks are in VRAM and writes the slot's single partial plane.
+//   compute stream: gate/up over cached tops, staging groups that already
+//     landed and shared experts; then the down projection of every expert
+//     now complete in VRAM and of the shared experts;
+//   side stream (after that gate/up): per expert with missing chunks, issue
+//     the copies, gate/up per group as it lands, then its down projection,
+//     then release its staging slot.
+ms_status prefill_experts(ms_ctx* ctx, int layer, const void* h_dev, int T, const std::vector<int32_t>& offs,
+                          hipStream_t sm) {
+  const Shape& s = ctx->s;
+  LayerState& L = ctx->layers[layer];
+  const uint64_t gu_bytes = 2ull * kUnits * s.d * s.elem;  // gate + up bytes of one chunk
+  const uint64_t dn_bytes = 1ull * kUnits * s.d * s.elem;  // down bytes of one chunk
+  msk::MmaArgs ma{};
+  ma.h = h_dev;
+  ma.offsets = reinterpret_cast<const int32_t*>(ctx->dev(s.off_offsets));
+  ma.perm = reinterpret_cast<const int32_t*>(ctx->dev(s.off_perm));
+  ma.act = reinterpret_cast<uint16_t*>(ctx->dev(s.off_act));
+  ma.act_sh = reinterpret_cast<uint16_t*>(ctx->dev(s.off_act_sh));
+  ma.part = reinterpret_cast<float*>(ctx->dev(s.off_part));
+  ma.part_sh = reinterpret_cast<float*>(ctx->dev(s.off_part_sh));
+  ma.chunk_bytes = s.chunk_bytes;
+  ma.sh_plane = s.sh_plane;
+  ma.d = s.d;
+  ma.K = s.K;
+  ma.T = T;
+  ma.f_pad = s.n_chunks * kUnits;
+  ma.f_pad_sh = s.n_chunks_sh * kUnits;
+  ma.rows_shared = s.max_T;
+  ma.ncb = (s.d + msk::kMmaCols - 1) / msk::kMmaCols;
+  auto m_tiles = [&](int e) {
+    const int n = e >= 0 ? offs[e + 1] - offs[e] : T;
+    return (n + msk::kMmaRows - 1) / msk::kMmaRows;
+  };
+  auto shared_base = [&](int i) {
+    return ctx->dev(s.off_shared + align_up(s.shared_bytes, kAlign) * (static_cast<uint64_t>(layer) * s.n_sh + i));
+  };
+  auto launch = [&](const std::vector<msk::MmaTask>& tasks, hipStream_t st, bool down) -> ms_status {
+    for (size_t i0 = 0; i0 < tasks.size(); i0 += msk::kMaxMmaTasks) {
+      const size_t i1 = std::min(tasks.size(), i0 + msk::kMaxMmaTasks);
+      ma.n_tasks = static_cast<int>(i1 - i0);
+      int wg = 0;
+      uint64_t bytes = 0;
+      for (size_t i = i0; i < i1; ++i) {
+        ma.tasks[i - i0] = tasks[i];
+        ma.tasks[i - i0].wg_begin = wg;
+        wg += tasks[i].m_tiles * (down ? ma.ncb : tasks[i].n_chunks);
+        bytes += (down ? dn_bytes : gu_bytes) * tasks[i].n_chunks;
+      }
+      ma.n_wg = wg;
+      const int id = tl_begin(ctx, st, down ? MS_IV_FFN_DOWN : (st == sm ? MS_IV_FFN_RESIDENT : MS_IV_FFN_STREAMED),
+                              layer, bytes);
+      MS_HIP(down ? msk::launch_mma_down(ma, st) : msk::launch_mma_gateup(ma, st));
+      tl_end(ctx, id, st);
+    }
+    return MS_OK;
+  };
+  auto task = [](const unsigned char* base, const unsigned char* base2, int e, int lo, int n, int split, int mt) {
+    msk::MmaTask t{};
+    t.base = base;
+    t.base2 = base2;
+    t.expert = e;
+    t.chunk_lo = lo;
+    t.n_chunks = n;
+    t.split = split;
+    t.m_tiles = mt;
+    return t;
+  };
+
+  // statistics and, per active expert, whether all its chunks are in VRAM now
+  std::vector<int> covering(s.E, -1);
+  std::vector<char> complete(s.E, 0);
+  std::vector<msk::MmaTask> gu, dn;
+  for (int e = 0; e < s.E; ++e) {
+    if (offs[e + 1] == offs[e]) continue;
+    L.st.experts_active += 1;
+    const int res = resident_chunks(L, e);
+    const unsigned char* top = res > 0 ? L.cache_base + L.top_bytes * L.slot_of[e] : nullptr;
+    if (res > 0) gu.push_back(task(top, nullptr, e, 0, res, 0, m_tiles(e)));
+    if (res >= s.n_chunks) {
+      L.st.alpha += 1;
+      complete[e] = 1;
+      dn.push_back(task(top, top, e, 0, s.n_chunks, s.n_chunks, m_tiles(e)));
+      continue;
+    }
+    if (res > 0)
+      L.st.beta += 1;
+    else
+      L.st.gamma += 1;
+    const int si = find_slot(ctx, layer, e);
+    if (si < 0 || ctx->buf[si].first_chunk > res) continue;
+    covering[e] = si;
+    BufSlot& b = ctx->buf[si];
+    bool any_issued = false, all_landed = true;
+    for (int gi = 0; gi < static_cast<int>(b.groups.size()); ++gi) {
+      Group& g = b.groups[gi];
+      any_issued = any_issued || g.issued;
+      const int lo = std::max(g.c_lo, res);
+      if (lo >= g.c_hi) continue;
+      hipError_t q = hipErrorNotReady;
+      if (g.issued) q = hipEventQuery(b.gev[gi]);
+      if (q != hipSuccess && q != hipErrorNotReady) return poison(ctx, "hipEventQuery(group)", q);
+      if (q == hipSuccess) {
+        gu.push_back(task(b.base, nullptr, e, lo, g.c_hi - lo, 0, m_tiles(e)));
+        g.pre = true;
+        if (g.prefetch && !g.used) L.st.bytes_prefetch_used += s.chunk_bytes * (g.c_hi - g.c_lo);
+        g.used = true;
+      } else {
+        all_landed = false;
+      }
+    }
+    if (any_issued) L.st.buffer_hits += 1;
+    if (all_landed) {
+      complete[e] = 1;
+      dn.push_back(task(top ? top : b.base, b.base, e, 0, s.n_chunks, res, m_tiles(e)));
+      b.use_order = 1 << 30;  // read by this forward; not a victim
+    }
+  }
+  for (int i = 0; i < s.n_sh; ++i) {
+    gu.push_back(task(shared_base(i), nullptr, -1 - i, 0, s.n_chunks_sh, 0, m_tiles(-1)));
+    dn.push_back(task(shared_base(i), shared_base(i), -1 - i, 0, s.n_chunks_sh, s.n_chunks_sh, m_tiles(-1)));
+  }
+  ms_status st = launch(gu, sm, false);
+  if (st != MS_OK) return st;
+  MS_HIP(hipEventRecord(ctx->ev_res, sm));
+  st = launch(dn, sm, true);
+  if (st != MS_OK) return st;
+  for (int e = 0; e < s.E; ++e) {
+    if (covering[e] >= 0 && complete[e]) {
+      BufSlot& b = ctx->buf[covering[e]];
+      MS_HIP(hipEventRecord(b.last_read, sm));
+      b.has_last_read = true;
+    }
+  }
+
+  // experts still missing chunks: side stream.  Slots that already hold a
+  // pending expert's part are reserved so that no earlier miss evicts them.
+  MS_HIP(hipStreamWaitEvent(ctx->side, ctx->ev_res, 0));
+  for (int e = 0; e < s.E; ++e)
+    if (covering[e] >= 0 && !complete[e]) ctx->buf[covering[e]].use_order = 1 << 30;
+  int use_counter = 0;
+  for (int e = 0; e < s.E; ++e) {
+    if (offs[e + 1] == offs[e] || complete[e]) continue;
+    const int res = resident_chunks(L, e);
+    int si = covering[e];
+    if (si >= 0 && !(ctx->buf[si].layer == layer && ctx->buf[si].expert == e && ctx->buf[si].first_chunk <= res))
+      si = -1;  // taken over by an earlier miss of this forward
+    if (si < 0) {
+      si = find_slot(ctx, layer, e);
+      if (si < 0 || ctx->buf[si].first_chunk > res) si = pick_victim(ctx, true);
+      st = assign_slot(ctx, si, layer, e, res);
+      if (st != MS_OK) return st;
+    }
+    BufSlot& b = ctx->buf[si];
+    b.use_order = use_counter++;
+    b.tick = ++ctx->tick;
+    for (int gi = 0; gi < static_cast<int>(b.groups.size()); ++gi) {
+      Group& g = b.groups[gi];
+      const int lo = std::max(g.c_lo, res);
+      if (lo >= g.c_hi || g.pre) continue;
+      if (!g.issued) {
+        st = issue_group(ctx, si, gi, false);
+        if (st != MS_OK) return st;
+      } else if (g.prefetch && !g.used) {
+        L.st.bytes_prefetch_used += s.chunk_bytes * (g.c_hi - g.c_lo);
+      }
+      g.used = true;
+      MS_HIP(hipStreamWaitEvent(ctx->side, b.gev[gi], 0));
+      st = launch({task(b.base, nullptr, e, lo, g.c_hi - lo, 0, m_tiles(e))}, ctx->side, false);
+      if (st != MS_OK) return st;
+    }
+    const unsigned char* top = res > 0 ? L.cache_base + L.top_bytes * L.slot_of[e] : b.base;
+    st = launch({task(top, b.base, e, 0, s.n_chunks, res, m_tiles(e))}, ctx->side, true);
+    if (st != MS_OK) return st;
+    MS_HIP(hipEventRecord(b.last_read, ctx->side));
+    b.has_last_read = true;
+  }
   return MS_OK;
 }
 
@@ -1010,10 +1202,16 @@ ms_status ms_forward(ms_ctx* ctx, int32_t layer, const void* h_dev, int32_t T, f
   tl_end(ctx, ti, sm);
   MS_HIP(hipEventRecord(ctx->ev_route, sm));
 
+  // decode path (chunk kernel, launched before the host sees the routing)
+  // or prefill path (matrix cores, launched once the token counts are known)
+  bool prefill = s.dtype == MS_BF16 && static_cast<int64_t>(T) * s.K >= 8ll * s.E;
+  if (flags & MS_FWD_MATRIX_CORES) prefill = s.dtype == MS_BF16;
+  if (flags & MS_FWD_NO_MATRIX_CORES) prefill = false;
+
   // 2. segments already in VRAM (Eq. (5): processed while missing ones
   //    load): cached tops, staging-buffer groups of this layer whose copies
   //    have completed, and the shared experts.  Experts that turn out not to
-  //    be selected exit at once.
+  //    be selected exit at once.  (Decode path only.)
   msk::FfnArgs fa{};
   fa.h = h_dev;
   fa.offsets = d_offsets;
@@ -1032,7 +1230,7 @@ ms_status ms_forward(ms_ctx* ctx, int32_t layer, const void* h_dev, int32_t T, f
   fa.n_planes = s.n_chunks * s.subs;
   fa.n_planes_sh = s.n_chunks_sh * s.subs;
   std::vector<msk::FfnTask> res_tasks;
-  for (int e = 0; e < s.E; ++e) {
+  for (int e = 0; e < s.E && !prefill; ++e) {
     const int rc = resident_chunks(L, e);
     if (rc <= 0) continue;
     msk::FfnTask t{};
@@ -1044,7 +1242,7 @@ ms_status ms_forward(ms_ctx* ctx, int32_t layer, const void* h_dev, int32_t T, f
   }
   bool any_pre = false;
   for (BufSlot& b : ctx->buf) {
-    if (b.layer != layer) continue;
+    if (b.layer != layer || prefill) continue;
     const int res = resident_chunks(L, b.expert);
     for (int gi = 0; gi < static_cast<int>(b.groups.size()); ++gi) {
       Group& g = b.groups[gi];
@@ -1067,9 +1265,12 @@ ms_status ms_forward(ms_ctx* ctx, int32_t layer, const void* h_dev, int32_t T, f
       any_pre = true;
     }
   }
-  for (int i = 0; i < s.n_sh; ++i) {
+  auto shared_base = [&](int i) {
+    return ctx->dev(s.off_shared + align_up(s.shared_bytes, kAlign) * (static_cast<uint64_t>(layer) * s.n_sh + i));
+  };
+  for (int i = 0; i < s.n_sh && !prefill; ++i) {
     msk::FfnTask t{};
-    t.base = ctx->dev(s.off_shared + align_up(s.shared_bytes, kAlign) * (static_cast<uint64_t>(layer) * s.n_sh + i));
+    t.base = shared_base(i);
     t.expert = -1 - i;
     t.chunk_lo = 0;
     t.n_chunks = s.n_chunks_sh;
@@ -1145,6 +1346,7 @@ ms_status ms_forward(ms_ctx* ctx, int32_t layer, const void* h_dev, int32_t T, f
     L.has_pred = false;
   }
 
+  if (!prefill) {
   // 5. missing segments.  Side stream: first one wide launch over buffer
   //    groups that landed by now, then one launch per group still to land,
   //    each after its copy event.  Slots read by the resident launch are
@@ -1266,6 +1468,10 @@ ms_status ms_forward(ms_ctx* ctx, int32_t layer, const void* h_dev, int32_t T, f
       b.has_last_read = true;
     }
   }
+  } else {
+    st = prefill_experts(ctx, layer, h_dev, T, offs, sm);
+    if (st != MS_OK) return st;
+  }
   for (BufSlot& b : ctx->buf)
     for (Group& g : b.groups) g.pre = false;
   MS_HIP(hipEventRecord(ctx->ev_side_done, ctx->side));
@@ -1281,10 +1487,10 @@ ms_status ms_forward(ms_ctx* ctx, int32_t layer, const void* h_dev, int32_t T, f
   ca.sh_plane = s.sh_plane;
   ca.rows_routed = rows_routed;
   ca.rows_shared = s.max_T;
-  ca.n_planes = s.n_chunks * s.subs;
-  ca.n_planes_sh = s.n_chunks_sh * s.subs;
+  ca.n_planes = prefill ? 1 : s.n_chunks * s.subs;
+  ca.n_planes_sh = prefill ? 1 : s.n_chunks_sh * s.subs;
   ca.red = reinterpret_cast<float*>(ctx->dev(s.off_red));
-  ca.pg = msk::combine_groups(T, s.K, s.n_sh, s.d, s.n_chunks * s.subs);
+  ca.pg = msk::combine_groups(T, s.K, s.n_sh, s.d, ca.n_planes);
   ca.n_shared = s.n_sh;
   ca.T = T;
   ca.K = s.K;

@@ -20,10 +20,12 @@ STATUS_NAMES = {0: "MS_OK", 1: "MS_E_INVALID", 2: "MS_E_BUDGET", 3: "MS_E_STATE"
                 5: "MS_E_NOMEM", 6: "MS_E_UNSUPPORTED"}
 MS_F32, MS_BF16 = 0, 1
 MS_FWD_PREDICT_NEXT = 1
+MS_FWD_MATRIX_CORES = 2
+MS_FWD_NO_MATRIX_CORES = 4
 (MS_IV_ROUTER, MS_IV_GROUP, MS_IV_FFN_RESIDENT, MS_IV_FFN_STREAMED, MS_IV_COMBINE,
- MS_IV_COPY_MISS, MS_IV_COPY_PREFETCH, MS_IV_COPY_TOP, MS_IV_PREDICT) = range(9)
+ MS_IV_COPY_MISS, MS_IV_COPY_PREFETCH, MS_IV_COPY_TOP, MS_IV_PREDICT, MS_IV_FFN_DOWN) = range(10)
 INTERVAL_NAMES = ["router", "group", "ffn_resident", "ffn_streamed", "combine",
-                  "copy_miss", "copy_prefetch", "copy_top", "predict"]
+                  "copy_miss", "copy_prefetch", "copy_top", "predict", "ffn_down"]
 
 
 class ms_model_desc(ctypes.Structure):
