@@ -30,8 +30,34 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBPS = 8000.0
+GIB = 1 << 30
+
+# name -> (shape, tokens per step, split ratio, per-layer budget in top
+# segments (None: whole budget of the reference config), which tops to cache)
+def _workloads():
+    import dataclasses
+    import synth
+    ds1 = dataclasses.replace(synth.DEEPSEEK, n_layers=1)
+    qw1 = dataclasses.replace(synth.QWEN3, n_layers=1)
+    return {
+        # Mixtral-8x7B-shaped layer, decode batch 1, r = .5, tops of experts 0-3
+        "mixtral-decode": dict(shape=synth.MIXTRAL, T=1, r=0.5, budget=lambda tb: 4 * tb,
+                               tops=lambda rig: [0, 1, 2, 3]),
+        # DeepSeek-V2-Lite-shaped layer: 4 GiB over 26 layers at r = .5 (19 tops)
+        "deepseek-decode": dict(shape=ds1, T=1, r=0.5, budget=lambda tb: (4 * GIB) // 26,
+                                tops=lambda rig: list(range(19))),
+        "deepseek-prefill": dict(shape=ds1, T=512, r=0.5, budget=lambda tb: (4 * GIB) // 26,
+                                 tops=lambda rig: list(range(19))),
+        # Qwen3-30B-A3B-shaped layer: 8 GiB over 48 layers at r = .5 (37 tops),
+        # the Zipf-hot experts cached
+        "qwen-decode16": dict(shape=qw1, T=16, r=0.5, budget=lambda tb: (8 * GIB) // 48,
+                              tops=lambda rig: list(np.argsort(-rig.biases[0], kind="stable")[:37])),
+        "qwen-prefill": dict(shape=qw1, T=2048, r=0.5, budget=lambda tb: (8 * GIB) // 48,
+                             tops=lambda rig: list(np.argsort(-rig.biases[0], kind="stable")[:37])),
+    }
+
 METRIC = "MoE-layer decode µs/layer + achieved HBM GB/s; H2D overlap % at fixed VRAM budget"
-KERNEL_KINDS = ("router", "group", "predict", "ffn_resident", "ffn_streamed", "combine")
+KERNEL_KINDS = ("router", "group", "predict", "ffn_resident", "ffn_streamed", "ffn_down", "combine")
 COPY_KINDS = ("copy_miss", "copy_prefetch")
 
 
@@ -98,9 +124,10 @@ def analyse(tl, steps, ms_per_step):
 
 
 def ffn_roofline(an):
-    """SwiGLU chunk kernel (resident and streamed launches are the same
-    kernel): weight bytes read per launch / average launch duration."""
-    ks = [an["kernels"]["ffn_resident"], an["kernels"]["ffn_streamed"]]
+    """Expert FFN kernels (resident and streamed launches are the same
+    kernel; the prefill path adds the down projection): weight bytes read per
+    launch / average launch duration."""
+    ks = [an["kernels"]["ffn_resident"], an["kernels"]["ffn_streamed"], an["kernels"]["ffn_down"]]
     n = sum(k["launches"] for k in ks)
     ms_tot = sum(k["total_ms"] for k in ks)
     b = sum(k["bytes"] for k in ks)
@@ -115,22 +142,33 @@ def ffn_roofline(an):
 
 # ------------------------------------------------------------------ timing
 
-def run_steps(rig, hs, steps, warmup, flags, timeline=True):
+def run_steps(rig, hs, steps, warmup, flags, timeline=True, cold=False, T=1):
+    """Time `steps` batches of T tokens through layer 0.  cold=True drops the
+    staging buffer before every batch, so each pays all of its misses."""
     import torch
     from paper_2509_08342_amd import moesplit as ms
     stream = torch.cuda.current_stream()
-    y, idx, w = rig.outputs(1)
+    y, idx, w = rig.outputs(T)
+    # every pass starts from an empty staging buffer, so passes over the same
+    # tokens start from the same state
+    ms.ms_drop_buffer(rig.ctx)
     for i in range(warmup):
-        rig.forward(0, hs[i % len(hs)], 1, y, idx, w, flags, stream)
+        if cold:
+            ms.ms_drop_buffer(rig.ctx)
+        rig.forward(0, hs[i % len(hs)], T, y, idx, w, flags, stream)
     ms.ms_sync(rig.ctx)
     torch.cuda.synchronize()
     ms.ms_reset_stats(rig.ctx)
     if timeline:
-        ms.ms_timeline_begin(rig.ctx, stream, 1 << 16)
+        # room for every record of the timed steps (events are created up front)
+        cap = min(1 << 16, max(1024, steps * (4 * rig.shape.n_experts + 64)))
+        ms.ms_timeline_begin(rig.ctx, stream, cap)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for i in range(steps):
-        rig.forward(0, hs[(warmup + i) % len(hs)], 1, y, idx, w, flags, stream)
+        if cold:
+            ms.ms_drop_buffer(rig.ctx)
+        rig.forward(0, hs[(warmup + i) % len(hs)], T, y, idx, w, flags, stream)
     ms.ms_sync(rig.ctx)
     torch.cuda.synchronize()
     t1 = time.perf_counter()
@@ -159,21 +197,28 @@ def h2d_link_peak_gbps():
 
 
 def cpu_baseline(rig, hf_list, budget_s):
-    """The oracle as it stands, one thread, on as many decode tokens of the
-    same layer as fit in about budget_s seconds."""
+    """The oracle as it stands, one thread, on as many batches of the same
+    layer as fit in about budget_s seconds.  For batches of more than 16
+    tokens the experts are evaluated on 16 of the rows (routing on all) and
+    the time is scaled to the whole batch."""
     import oracle
     s = rig.shape
+    T = hf_list[0].shape[0]
+    rows = list(range(min(T, 16)))
     t0 = time.perf_counter()
     n = 0
     for hf in hf_list:
         oracle.moe_layer(hf, rig.routers[0], rig.layer_experts(0), s.top_k,
-                         renormalize=s.renormalize, bias=rig.biases[0], shared=rig.shared[0])
+                         renormalize=s.renormalize, bias=rig.biases[0], shared=rig.shared[0],
+                         tokens=rows)
         n += 1
         if time.perf_counter() - t0 > budget_s:
             break
     dt = time.perf_counter() - t0
-    return dict(value=round(dt / n * 1e6, 1), unit="us/layer", cores=1, kind="oracle",
-                sample="%d decode tokens of the Mixtral-shaped layer (router + 2 experts, fp64)" % n)
+    scale = T / len(rows)
+    return dict(value=round(dt / n * scale * 1e6, 1), unit="us/layer", cores=1, kind="oracle",
+                sample="%d batches of %d token(s) of the %s layer (router on all rows, %d experts per "
+                "row on %d rows, fp64, scaled to the batch)" % (n, T, s.name, s.top_k, len(rows)))
 
 
 def log(msg):
@@ -189,6 +234,9 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-all-resident", action="store_true")
     ap.add_argument("--timeline-out", default=None)
+    ap.add_argument("--workload", default="mixtral-decode",
+                    help="mixtral-decode (default), deepseek-decode, deepseek-prefill, "
+                         "qwen-decode16, qwen-prefill")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one GPU: this build of the split-expert layer has no "
@@ -201,23 +249,27 @@ def main():
     from workload import SplitRig, to_device, top_bytes
 
     torch.cuda.set_device(0)
-    shape = synth.MIXTRAL
+    wl = _workloads()[args.workload]
+    shape, T = wl["shape"], wl["T"]
     t_setup = time.perf_counter()
     log("generating %s weights and filling the pinned store" % shape.name)
-    rig = SplitRig(shape, seed=0, max_tokens=1, budget_bytes=shape.n_experts * shape.expert_bytes,
+    rig = SplitRig(shape, seed=0, max_tokens=T, budget_bytes=shape.n_experts * shape.expert_bytes,
                    keep_f32=not args.no_cpu_baseline, threads=16)
     n_tok = args.warmup + args.steps
-    seq = synth.walk(shape, 0, n_tok, T=1)
+    seq = synth.walk(shape, 0, n_tok, T=T)
     hs = [to_device(raw, shape.dtype) for raw, _ in seq]
     torch.cuda.synchronize()
     setup_s = time.perf_counter() - t_setup
-
     log("setup done in %.1f s; timing the split layer" % setup_s)
-    # headline: r = 0.5, tops of experts 0-3 cached (C = 4), rest in host RAM
-    slots = rig.configure([4 * top_bytes(rig, 0.5)], [0.5])
-    rig.load_tops(0, [0, 1, 2, 3])
+    # the split configuration: per-layer budget, split ratio, cached tops
+    r = wl["r"]
+    tops = [int(e) for e in wl["tops"](rig)]
+    slots = rig.configure([wl["budget"](top_bytes(rig, r))], [r])
+    rig.load_tops(0, tops[:int(slots[0])])
     ms.ms_sync(rig.ctx)
-    ms_step, tl, st = run_steps(rig, hs, args.steps, args.warmup, ms.MS_FWD_PREDICT_NEXT)
+    ms_step, tl, st = run_steps(rig, hs, args.steps, args.warmup, ms.MS_FWD_PREDICT_NEXT, T=T)
+    # the same steps without the timeline's events: the cost of instrumenting
+    ms_plain, _, _ = run_steps(rig, hs, args.steps, args.warmup, ms.MS_FWD_PREDICT_NEXT, timeline=False, T=T)
     an = analyse(tl, args.steps, ms_step)
     roof = ffn_roofline(an)
     if args.timeline_out:
@@ -232,18 +284,20 @@ def main():
         "steps": args.steps,
         "warmup": args.warmup,
         "ms_per_step": round(ms_step, 4),
+        "ms_per_step_uninstrumented": round(ms_plain, 4),
         "higher_is_better": False,
         "scaling": "weak",
         "vs_baseline": None,
         "dtype": "bf16",
         "data": "synthetic",
-        "config": {"workload": "mixtral-8x7b-shaped MoE layer, decode T=1, r=0.5, tops of experts "
-                               "0-3 cached (C=%d), other segments in pinned host RAM, prediction + "
-                               "prefetch on" % int(slots[0]),
+        "config": {"workload": "%s: %s-shaped MoE layer, %s T=%d, r=%.2f, %d top segments cached, other "
+                               "segments in pinned host RAM, prediction + prefetch on"
+                               % (args.workload, shape.name, "prefill" if T > 16 else "decode", T, r,
+                                  int(slots[0])),
                    "d_model": shape.d_model, "d_ff": shape.d_ff, "n_experts": shape.n_experts,
-                   "top_k": shape.top_k, "r": 0.5, "tokens_per_step": 1},
+                   "top_k": shape.top_k, "n_shared": shape.n_shared, "r": r, "tokens_per_step": T},
         "roofline": roof,
-        "tokens_per_s": round(1e3 / ms_step, 2),
+        "tokens_per_s": round(T * 1e3 / ms_step, 2),
         "h2d_gbps": None if an["h2d_gbps"] is None else round(an["h2d_gbps"], 2),
         "overlap": {"h2d_hidden_frac": an["hidden_frac"], "compute_hidden_frac": an["compute_hidden_frac"],
                     "eta": an["overlap_eta"], "copy_ms_per_step": an["copy_ms"] / args.steps,
@@ -257,13 +311,28 @@ def main():
     }
     out["h2d_link_peak_gbps"] = round(h2d_link_peak_gbps(), 2)
 
+    # the miss path alone: same tokens and residency, buffer emptied before
+    # every token and no prefetch, so every selected expert's missing
+    # segment is copied after routing
+    ms_cold, tl_cold, st_cold = run_steps(rig, hs, args.steps, args.warmup, 0, cold=True, T=T)
+    an_c = analyse(tl_cold, args.steps, ms_cold)
+    out["cold_miss_path"] = {
+        "us_per_layer": round(ms_cold * 1e3, 1),
+        "h2d_gbps": None if an_c["h2d_gbps"] is None else round(an_c["h2d_gbps"], 2),
+        "h2d_bytes_per_step": an_c["miss_bytes"] // args.steps,
+        "overlap": {"h2d_hidden_frac": an_c["hidden_frac"], "compute_hidden_frac": an_c["compute_hidden_frac"],
+                    "eta": an_c["overlap_eta"]},
+        "roofline": ffn_roofline(an_c),
+        "alpha_beta_gamma": [st_cold["alpha"], st_cold["beta"], st_cold["gamma"]]}
+    log("cold miss path: %.3f ms/step" % ms_cold)
+
     log("split layer: %.3f ms/step" % ms_step)
     if not args.no_all_resident:
         # all eight experts whole in VRAM (r = 1): the expert read is HBM-bound
         rig.configure([shape.n_experts * shape.expert_bytes], [1.0])
         rig.load_tops(0, range(shape.n_experts))
         ms.ms_sync(rig.ctx)
-        ms_ar, tl_ar, _ = run_steps(rig, hs, args.steps, args.warmup, ms.MS_FWD_PREDICT_NEXT)
+        ms_ar, tl_ar, _ = run_steps(rig, hs, args.steps, args.warmup, ms.MS_FWD_PREDICT_NEXT, T=T)
         an_ar = analyse(tl_ar, args.steps, ms_ar)
         out["all_resident"] = {"us_per_layer": round(ms_ar * 1e3, 1), "roofline": ffn_roofline(an_ar),
                                "kernels": {k: {"launches": v["launches"],

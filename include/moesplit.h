@@ -180,7 +180,12 @@ ms_status ms_set_router(ms_ctx* ctx, int32_t layer, const void* w_r, const float
  * pinned host store in chunk-packed order: per 64-unit chunk, the 64 gate
  * columns, the 64 up columns and the 64 down rows, each as d-contiguous rows,
  * so that a top segment is a contiguous prefix of the blob and a bottom
- * segment a contiguous suffix. */
+ * segment a contiguous suffix (gate and up rows k-tiled: 64 consecutive
+ * elements of one row, then the next row's).  The store is pinned, coherent
+ * host memory, read by the device over PCIe.  Setting an expert again waits
+ * for work in flight, rewrites its blob in place (also for every expert
+ * aliasing it), drops staged copies of it and re-copies its cached top
+ * segments, so later forwards use only the new weights. */
 ms_status ms_set_expert(ms_ctx* ctx, int32_t layer, int32_t e, const void* w_gate,
                         const void* w_up, const void* w_down);
 
@@ -271,7 +276,8 @@ ms_status ms_reset_stats(ms_ctx* ctx);
 /* Timeline instrumentation.  ms_timeline_begin records an origin event on
  * `stream` and from then on brackets every kernel and copy the library
  * issues with HIP events on the stream it runs on (at most `capacity`
- * records).  ms_timeline_end synchronises, writes up to `cap` records to
+ * records; their events are created here, up front).  ms_timeline_end
+ * synchronises, writes up to `cap` records to
  * out[] (in issue order) and their count to n_out, and stops recording. */
 ms_status ms_timeline_begin(ms_ctx* ctx, void* stream, int32_t capacity);
 ms_status ms_timeline_end(ms_ctx* ctx, ms_interval* out, int32_t cap, int32_t* n_out);

@@ -24,12 +24,23 @@ struct LogitsArgs {
   int T, d, E;
   int dtype;
   const void* wr;         // [d][E] model dtype
+  const void* wt;         // the same router transposed, [E][d] (many-token path)
   const float* bias;      // [E] or NULL
   float* logits;          // [T][E]
   const void* wr2;        // second router or NULL
+  const void* wt2;
   const float* bias2;
   float* logits2;
 };
+
+// Routing of T >= kManyTokens tokens runs over many work-groups: logits in
+// tiles of 8 tokens x 16 experts per wave, selection and per-block expert
+// counts for blocks of route_block_tokens(K) tokens, one work-group for the
+// scans over blocks (and the prediction ranking), then the scatter of the
+// grouping.  Fewer tokens take one work-group for everything after the
+// logits.
+constexpr int kManyTokens = 64;
+inline int route_block_tokens(int K) { return K <= 16 ? 16 : 4; }
 
 
 // One work-group: top-K selection with lowest-index ties and Eq. (2) gate
@@ -50,6 +61,11 @@ struct RouteArgs {
   int32_t* order;           // [E]
   float* host_score;        // host-visible or NULL
   int32_t* host_order;      // host-visible or NULL
+  // many-token workspace (ignored below kManyTokens tokens)
+  int32_t* lrank;           // [T*K] rank of a slot among its block's slots of the same expert
+  int32_t* blk;             // [E][nblk_cap] per-block expert counts, then their prefix sums
+  float* psc;               // [nblk_cap][E] per-block prediction score sums
+  int32_t nblk_cap;
 };
 // Logits launch, then the route launch on them.
 hipError_t launch_logits_route(const LogitsArgs& a, const RouteArgs& ra, hipStream_t s);
@@ -131,6 +147,14 @@ struct MmaArgs {
 };
 hipError_t launch_mma_gateup(const MmaArgs& a, hipStream_t s);
 hipError_t launch_mma_down(const MmaArgs& a, hipStream_t s);
+
+// Host-to-device copy of `bytes` (a multiple of 16; both addresses 16-byte
+// aligned) from pinned host memory that the device can address (src is its
+// device-side address) into device memory, by a streaming kernel of
+// kH2dWorkGroups work-groups.  Unlike a DMA-engine copy, it orders after
+// other streams' work through ordinary kernel-to-kernel dependencies.
+constexpr int kH2dWorkGroups = 32;
+hipError_t launch_h2d(void* dst, const void* src, uint64_t bytes, hipStream_t s);
 
 // y[t] = sum_k w[t][k] * sum_c part[c][pos[t*K+k]] + sum_s sum_c part_sh[s][c][t],
 // c over the partial planes (chunks * subs), in two launches: a first pass

@@ -9,6 +9,8 @@
 // bottom-segment chunks (Sec. 3.1: segments are combined at compute time).
 #include <hip/hip_runtime.h>
 #include <math.h>
+
+#include <algorithm>
 #include <stdint.h>
 
 #include "kernels.h"
@@ -91,19 +93,151 @@ __device__ __forceinline__ float silu(float x) { return x / (1.0f + expf(-x)); }
 
 // -------------------------------------------------------------------- route
 //
-// Route body, run by one work-group of NW waves:
-//  1. selection, one wave per token: K rounds of wave argmax over the
-//     untaken experts (larger logit wins, the lower index on equal logits,
-//     NaN ranks last), then the Eq. (2) weights from exp(logit - max);
-//  2. grouping: stable counting sort of the T*K slots by expert --
-//     histogram, exclusive scan, then blocks of 64*NW slots placed in slot
-//     order (within a wave by ballot rank, across waves by per-wave counts);
-//  3. ranking of the prediction: per-token softmax of the second logits,
-//     summed over tokens (per wave, then over waves in order), experts
-//     ordered by descending score, lower index first on equal scores.
+// Per token (one wave): K rounds of wave argmax over the untaken experts
+// (larger logit wins, the lower index on equal logits, NaN ranks last), then
+// the Eq. (2) weights from exp(logit - max).  Per token for the prediction
+// (Sec. 3.2, Eq. (3)): the softmax of its second logits, added to the
+// lane's running expert sums.  The grouping is a stable counting sort of
+// the T*K slots by expert.  The prediction ranking orders experts by
+// descending summed score, the lower index first on equal scores.
 
 constexpr int kLanesQ = kMaxExperts / 64;  // expert values held per lane
 
+// Selection of one token by one wave; lanes k < K return the k-th pick and
+// its weight.
+__device__ __forceinline__ void select_token(const float* lg, int E, int K, int renormalize, int lane,
+                                             int& my_idx, float& my_w) {
+  float lv[kLanesQ];
+#pragma unroll
+  for (int q = 0; q < kLanesQ; ++q) {
+    const int e = lane + 64 * q;
+    float v = e < E ? lg[e] : -INFINITY;
+    if (v != v) v = -INFINITY;  // NaN ranks last, so an index is always found
+    lv[q] = v;
+  }
+  uint32_t taken = 0;
+  float m = 0.0f, zsel = 0.0f, my_ex = 0.0f;
+  my_idx = 0;
+  for (int k = 0; k < K; ++k) {
+    float bv = -INFINITY;
+    int bi = 0x7fffffff;
+#pragma unroll
+    for (int q = 0; q < kLanesQ; ++q) {
+      const int e = lane + 64 * q;
+      if (e < E && !((taken >> q) & 1u) && (lv[q] > bv || (lv[q] == bv && e < bi))) {
+        bv = lv[q];
+        bi = e;
+      }
+    }
+#pragma unroll
+    for (int s = 32; s >= 1; s >>= 1) {
+      const float ov = __shfl_xor(bv, s, 64);
+      const int oi = __shfl_xor(bi, s, 64);
+      if (ov > bv || (ov == bv && oi < bi)) {
+        bv = ov;
+        bi = oi;
+      }
+    }
+    if ((bi & 63) == lane) taken |= 1u << (bi >> 6);
+    if (k == 0) m = bv;  // the first pick is the largest logit
+    const float ex = expf(bv - m);
+    zsel += ex;
+    if (lane == k) {
+      my_ex = ex;
+      my_idx = bi;
+    }
+  }
+  float z = zsel;
+  if (!renormalize) {
+    float part = 0.0f;
+#pragma unroll
+    for (int q = 0; q < kLanesQ; ++q)
+      if (lane + 64 * q < E) part += expf(lv[q] - m);
+#pragma unroll
+    for (int s = 32; s >= 1; s >>= 1) part += __shfl_xor(part, s, 64);
+    z = part;
+  }
+  my_w = my_ex / z;
+}
+
+// acc[q] (expert lane + 64 q) += softmax(lg)[expert], one token, one wave.
+__device__ __forceinline__ void pred_add(const float* lg, int E, int lane, float (&acc)[kLanesQ]) {
+  float lv[kLanesQ];
+  float m = -INFINITY;
+#pragma unroll
+  for (int q = 0; q < kLanesQ; ++q) {
+    const int e = lane + 64 * q;
+    lv[q] = e < E ? lg[e] : -INFINITY;
+    m = fmaxf(m, lv[q]);
+  }
+#pragma unroll
+  for (int s = 32; s >= 1; s >>= 1) m = fmaxf(m, __shfl_xor(m, s, 64));
+  float z = 0.0f;
+#pragma unroll
+  for (int q = 0; q < kLanesQ; ++q) {
+    lv[q] = (lane + 64 * q < E) ? expf(lv[q] - m) : 0.0f;
+    z += lv[q];
+  }
+#pragma unroll
+  for (int s = 32; s >= 1; s >>= 1) z += __shfl_xor(z, s, 64);
+#pragma unroll
+  for (int q = 0; q < kLanesQ; ++q) acc[q] += lv[q] / z;
+}
+
+// Ranks score_s (LDS, E values) and stores order / score (and their host-
+// visible copies); threads tid < E of a work-group of NT threads.
+__device__ __forceinline__ void rank_scores(const float* score_s, const RouteArgs& a, int tid, int NT) {
+  const int E = a.E;
+  for (int e = tid; e < E; e += NT) {
+    const float v = score_s[e];
+    int r = 0;
+    for (int o = 0; o < E; ++o) {
+      const float u = score_s[o];
+      r += (u > v) || (u == v && o < e);
+    }
+    a.order[r] = e;
+    a.score[e] = v;
+    if (a.host_order) a.host_order[r] = e;
+    if (a.host_score) a.host_score[e] = v;
+  }
+  // the host reads these once the launch completes
+  if (a.host_order && tid < E) __threadfence_system();
+}
+
+// Exclusive scan of cnt[0..E) by wave 0 into offsets (and the host-visible
+// copy, fenced for the host); base (LDS, optional) receives the same values.
+__device__ __forceinline__ void scan_offsets(const int* cnt, int* base, const RouteArgs& a, int lane) {
+  const int E = a.E;
+  int run = 0;
+  for (int e0 = 0; e0 < E; e0 += 64) {
+    const int e = e0 + lane;
+    const int c = e < E ? cnt[e] : 0;
+    int incl = c;
+#pragma unroll
+    for (int s = 1; s < 64; s <<= 1) {
+      const int o = __shfl_up(incl, s, 64);
+      if (lane >= s) incl += o;
+    }
+    if (e < E) {
+      if (base) base[e] = run + incl - c;
+      a.offsets[e] = run + incl - c;
+      if (a.host_offsets) a.host_offsets[e] = run + incl - c;
+    }
+    run += __shfl(incl, 63, 64);
+  }
+  if (lane == 0) {
+    a.offsets[E] = run;
+    if (a.host_offsets) a.host_offsets[E] = run;
+  }
+  // the host reads the offsets once this launch completes
+  if (a.host_offsets) __threadfence_system();
+}
+
+// Few tokens: everything after the logits in one work-group of NW waves --
+// selection one wave per token; grouping as histogram, exclusive scan, then
+// blocks of 64*NW slots placed in slot order (within a wave by ballot rank,
+// across waves by per-wave counts); prediction sums per wave, then over
+// waves in order.
 template <int NW>
 __device__ void route_body(const RouteArgs& a) {
   __shared__ int base[kMaxExperts];
@@ -116,60 +250,12 @@ __device__ void route_body(const RouteArgs& a) {
   if (a.logits != nullptr) {
     // 1. selection
     for (int t = wave; t < a.T; t += NW) {
-      const float* lg = a.logits + static_cast<size_t>(t) * E;
-      float lv[kLanesQ];
-#pragma unroll
-      for (int q = 0; q < kLanesQ; ++q) {
-        const int e = lane + 64 * q;
-        float v = e < E ? lg[e] : -INFINITY;
-        if (v != v) v = -INFINITY;  // NaN ranks last, so an index is always found
-        lv[q] = v;
-      }
-      uint32_t taken = 0;
-      float m = 0.0f, zsel = 0.0f, my_ex = 0.0f;
-      int my_idx = 0;
-      for (int k = 0; k < K; ++k) {
-        float bv = -INFINITY;
-        int bi = 0x7fffffff;
-#pragma unroll
-        for (int q = 0; q < kLanesQ; ++q) {
-          const int e = lane + 64 * q;
-          if (e < E && !((taken >> q) & 1u) && (lv[q] > bv || (lv[q] == bv && e < bi))) {
-            bv = lv[q];
-            bi = e;
-          }
-        }
-#pragma unroll
-        for (int s = 32; s >= 1; s >>= 1) {
-          const float ov = __shfl_xor(bv, s, 64);
-          const int oi = __shfl_xor(bi, s, 64);
-          if (ov > bv || (ov == bv && oi < bi)) {
-            bv = ov;
-            bi = oi;
-          }
-        }
-        if ((bi & 63) == lane) taken |= 1u << (bi >> 6);
-        if (k == 0) m = bv;  // the first pick is the largest logit
-        const float ex = expf(bv - m);
-        zsel += ex;
-        if (lane == k) {
-          my_ex = ex;
-          my_idx = bi;
-        }
-      }
-      float z = zsel;
-      if (!a.renormalize) {
-        float part = 0.0f;
-#pragma unroll
-        for (int q = 0; q < kLanesQ; ++q)
-          if (lane + 64 * q < E) part += expf(lv[q] - m);
-#pragma unroll
-        for (int s = 32; s >= 1; s >>= 1) part += __shfl_xor(part, s, 64);
-        z = part;
-      }
+      int my_idx;
+      float my_w;
+      select_token(a.logits + static_cast<size_t>(t) * E, E, K, a.renormalize, lane, my_idx, my_w);
       if (lane < K) {
         a.idx[static_cast<size_t>(t) * K + lane] = my_idx;
-        a.w[static_cast<size_t>(t) * K + lane] = my_ex / z;
+        a.w[static_cast<size_t>(t) * K + lane] = my_w;
       }
     }
     __threadfence_block();  // idx written above is read back by other waves of this work-group
@@ -184,32 +270,7 @@ __device__ void route_body(const RouteArgs& a) {
     // accesses in bounds whatever the input
     for (int s = tid; s < TK; s += NT) atomicAdd(&cnt[min(max(a.idx[s], 0), E - 1)], 1);
     __syncthreads();
-    if (wave == 0) {
-      // exclusive scan over experts, 64 at a time with a wave prefix sum
-      int run = 0;
-      for (int e0 = 0; e0 < E; e0 += 64) {
-        const int e = e0 + lane;
-        const int c = e < E ? cnt[e] : 0;
-        int incl = c;
-#pragma unroll
-        for (int s = 1; s < 64; s <<= 1) {
-          const int o = __shfl_up(incl, s, 64);
-          if (lane >= s) incl += o;
-        }
-        if (e < E) {
-          base[e] = run + incl - c;
-          a.offsets[e] = run + incl - c;
-          if (a.host_offsets) a.host_offsets[e] = run + incl - c;
-        }
-        run += __shfl(incl, 63, 64);
-      }
-      if (lane == 0) {
-        a.offsets[E] = run;
-        if (a.host_offsets) a.host_offsets[E] = run;
-      }
-      // the host reads the offsets once this launch completes
-      if (a.host_offsets) __threadfence_system();
-    }
+    if (wave == 0) scan_offsets(cnt, base, a, lane);
     __syncthreads();
     const uint64_t lt = (lane == 0) ? 0ull : ((~0ull) >> (64 - lane));
     for (int b0 = 0; b0 < TK; b0 += NT) {
@@ -249,29 +310,7 @@ __device__ void route_body(const RouteArgs& a) {
     float acc[kLanesQ];
 #pragma unroll
     for (int q = 0; q < kLanesQ; ++q) acc[q] = 0.0f;
-    for (int t = wave; t < a.T; t += NW) {
-      const float* lg = a.logits_pred + static_cast<size_t>(t) * E;
-      float lv[kLanesQ];
-      float m = -INFINITY;
-#pragma unroll
-      for (int q = 0; q < kLanesQ; ++q) {
-        const int e = lane + 64 * q;
-        lv[q] = e < E ? lg[e] : -INFINITY;
-        m = fmaxf(m, lv[q]);
-      }
-#pragma unroll
-      for (int s = 32; s >= 1; s >>= 1) m = fmaxf(m, __shfl_xor(m, s, 64));
-      float z = 0.0f;
-#pragma unroll
-      for (int q = 0; q < kLanesQ; ++q) {
-        lv[q] = (lane + 64 * q < E) ? expf(lv[q] - m) : 0.0f;
-        z += lv[q];
-      }
-#pragma unroll
-      for (int s = 32; s >= 1; s >>= 1) z += __shfl_xor(z, s, 64);
-#pragma unroll
-      for (int q = 0; q < kLanesQ; ++q) acc[q] += lv[q] / z;
-    }
+    for (int t = wave; t < a.T; t += NW) pred_add(a.logits_pred + static_cast<size_t>(t) * E, E, lane, acc);
     float* ws = reinterpret_cast<float*>(&wbuf[0][0]);
     __syncthreads();
 #pragma unroll
@@ -284,25 +323,123 @@ __device__ void route_body(const RouteArgs& a) {
       score_s[e] = sc;
     }
     __syncthreads();
-    for (int e = tid; e < E; e += NT) {
-      const float v = score_s[e];
-      int r = 0;
-      for (int o = 0; o < E; ++o) {
-        const float u = score_s[o];
-        r += (u > v) || (u == v && o < e);
-      }
-      a.order[r] = e;
-      a.score[e] = v;
-      if (a.host_order) a.host_order[r] = e;
-      if (a.host_score) a.host_score[e] = v;
-    }
-    if (a.host_order && tid < E) __threadfence_system();
+    rank_scores(score_s, a, tid, NT);
   }
 }
 
 constexpr int kRouteWaves = 16;
 
 __global__ __launch_bounds__(64 * kRouteWaves) void route_kernel(RouteArgs a) { route_body<kRouteWaves>(a); }
+
+// Many tokens, step 1 (work-group b: tokens [b TB, (b+1) TB), one wave per
+// token): selection, then each slot's rank among the block's earlier slots
+// of the same expert and the block's expert counts blk[e][b]; the block's
+// prediction score sums (waves in order) into psc[b][e].
+constexpr int kSelWaves = 4;
+
+__global__ __launch_bounds__(64 * kSelWaves) void select_many_kernel(RouteArgs a, int TB) {
+  __shared__ int sidx[64 * kSelWaves];
+  __shared__ int cnt[kMaxExperts];
+  __shared__ float wsc[kSelWaves][kMaxExperts];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int E = a.E, K = a.K;
+  const int b = blockIdx.x, t0 = b * TB, t1 = min(a.T, t0 + TB);
+  if (a.logits != nullptr) {
+    for (int e = tid; e < E; e += 64 * kSelWaves) cnt[e] = 0;
+    for (int t = t0 + wave; t < t1; t += kSelWaves) {
+      int my_idx;
+      float my_w;
+      select_token(a.logits + static_cast<size_t>(t) * E, E, K, a.renormalize, lane, my_idx, my_w);
+      if (lane < K) {
+        a.idx[static_cast<size_t>(t) * K + lane] = my_idx;
+        a.w[static_cast<size_t>(t) * K + lane] = my_w;
+        sidx[(t - t0) * K + lane] = my_idx;
+      }
+    }
+    __syncthreads();
+    const int n = (t1 - t0) * K;  // <= TB * K <= 64 * kSelWaves
+    if (tid < n) {
+      const int e = min(max(sidx[tid], 0), E - 1);
+      int r = 0;
+      for (int j = 0; j < tid; ++j) r += (sidx[j] == e);
+      a.lrank[static_cast<size_t>(t0) * K + tid] = r;
+      atomicAdd(&cnt[e], 1);
+    }
+    __syncthreads();
+    for (int e = tid; e < E; e += 64 * kSelWaves) a.blk[static_cast<size_t>(e) * a.nblk_cap + b] = cnt[e];
+  }
+  if (a.logits_pred != nullptr) {
+    float acc[kLanesQ];
+#pragma unroll
+    for (int q = 0; q < kLanesQ; ++q) acc[q] = 0.0f;
+    for (int t = t0 + wave; t < t1; t += kSelWaves) pred_add(a.logits_pred + static_cast<size_t>(t) * E, E, lane, acc);
+#pragma unroll
+    for (int q = 0; q < kLanesQ; ++q)
+      if (lane + 64 * q < E) wsc[wave][lane + 64 * q] = acc[q];
+    __syncthreads();
+    for (int e = tid; e < E; e += 64 * kSelWaves) {
+      float sc = wsc[0][e];
+#pragma unroll
+      for (int w2 = 1; w2 < kSelWaves; ++w2) sc += wsc[w2][e];
+      a.psc[static_cast<size_t>(b) * E + e] = sc;
+    }
+  }
+}
+
+// Many tokens, step 2 (one work-group): per expert the exclusive prefix of
+// its block counts (in place in blk) and its total; the exclusive scan over
+// experts into offsets; the prediction scores summed over blocks in order,
+// and their ranking.
+constexpr int kScanWaves = 16;
+
+__global__ __launch_bounds__(64 * kScanWaves) void scan_many_kernel(RouteArgs a, int nblk) {
+  __shared__ int tot[kMaxExperts];
+  __shared__ float score_s[kMaxExperts];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int E = a.E;
+  if (a.logits != nullptr) {
+    for (int e = wave; e < E; e += kScanWaves) {
+      int* row = a.blk + static_cast<size_t>(e) * a.nblk_cap;
+      int run = 0;
+      for (int b0 = 0; b0 < nblk; b0 += 64) {
+        const int b = b0 + lane;
+        const int c = b < nblk ? row[b] : 0;
+        int incl = c;
+#pragma unroll
+        for (int s = 1; s < 64; s <<= 1) {
+          const int o = __shfl_up(incl, s, 64);
+          if (lane >= s) incl += o;
+        }
+        if (b < nblk) row[b] = run + incl - c;
+        run += __shfl(incl, 63, 64);
+      }
+      if (lane == 0) tot[e] = run;
+    }
+    __syncthreads();
+    if (wave == 0) scan_offsets(tot, nullptr, a, lane);
+  }
+  if (a.logits_pred != nullptr) {
+    for (int e = tid; e < E; e += 64 * kScanWaves) {
+      float sc = 0.0f;
+      for (int b = 0; b < nblk; ++b) sc += a.psc[static_cast<size_t>(b) * E + e];
+      score_s[e] = sc;
+    }
+    __syncthreads();
+    rank_scores(score_s, a, tid, 64 * kScanWaves);
+  }
+}
+
+// Many tokens, step 3: slot s of token t (block t / TB) goes to grouped
+// position offsets[e] + (earlier blocks' slots of e) + (its rank in block).
+__global__ __launch_bounds__(256) void scatter_many_kernel(RouteArgs a, int TB) {
+  const int s = blockIdx.x * 256 + threadIdx.x;
+  if (s >= a.T * a.K) return;
+  const int b = (s / a.K) / TB;
+  const int e = min(max(a.idx[s], 0), a.E - 1);
+  const int p = a.offsets[e] + a.blk[static_cast<size_t>(e) * a.nblk_cap + b] + a.lrank[s];
+  a.perm[p] = s;
+  a.pos[s] = p;
+}
 
 // ------------------------------------------------------------------- logits
 //
@@ -312,9 +449,10 @@ __global__ __launch_bounds__(64 * kRouteWaves) void route_kernel(RouteArgs a) { 
 // that pairs lane l with lane l+s for s = 32, 16, ..., 1 (lane 0 ends with
 // the result); a bias is added once afterwards.
 //
-// Work-group = 4 waves = 4 tokens x one block of 8 experts of one router.
-// The block's weight columns are staged in LDS tile by tile (all 256 threads
-// load), then each wave runs its token's fma chains from LDS.
+// Few tokens: work-group = 4 waves = 4 tokens x one block of 8 experts of
+// one router.  The block's weight columns are staged in LDS tile by tile
+// (all 256 threads load), then each wave runs its token's fma chains from
+// LDS.
 
 constexpr int kLgWaves = 4;
 constexpr int kLgBlock = 8;           // experts per work-group
@@ -407,30 +545,207 @@ __global__ __launch_bounds__(64 * kLgWaves) void logits_kernel(LogitsArgs a) {
   }
 }
 
-// Logits launch, then the route launch (a kernel boundary, not a device-
-// scope fence, hands the logits over: with one L2 per XCD such fences write
-// back and invalidate L2 and cost far more than a launch).
+// Many tokens: the same order, with each lane running the fma chains of 8
+// consecutive residues (l = 8 m + k, k < 8, m = lane % 8) for a 4-token x
+// 4-expert output tile (o = lane / 8 picks the tile), reading 16 bytes per
+// row and step from h and from the transposed router [E][d].  A wave covers
+// 8 tokens x 16 experts, a work-group 32 tokens x 16 experts of one router.
+// The halving tree pairs residues l and l + 32, l + 16, l + 8 across lanes
+// m ^ 4, m ^ 2, m ^ 1 -- each level a butterfly in which the two lanes keep
+// opposite halves of the outputs -- and l + 4, + 2, + 1 inside the lane.
+constexpr int kLmTokens = 32;   // tokens per work-group (8 per wave)
+constexpr int kLmExperts = 16;  // experts per work-group
+
+template <typename W>
+__global__ __launch_bounds__(256) void logits_many_kernel(LogitsArgs a) {
+  constexpr int VPR = static_cast<int>(8 * sizeof(W)) / 16;  // 16-byte loads per row and step
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int m = lane & 7, o = lane >> 3;
+  const int nb = (a.E + kLmExperts - 1) / kLmExperts;
+  const int mat = blockIdx.y / nb, eb = blockIdx.y - mat * nb;
+  const W* wt = static_cast<const W*>(mat == 0 ? a.wt : a.wt2);
+  const float* bias = mat == 0 ? a.bias : a.bias2;
+  float* out = mat == 0 ? a.logits : a.logits2;
+  const int tq0 = blockIdx.x * kLmTokens + 8 * wave + 4 * (o >> 2);  // this lane's first token
+  const int eq0 = eb * kLmExperts + 4 * (o & 3);                      // this lane's first expert
+  const W* hp[4];
+  const W* wp[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    hp[i] = static_cast<const W*>(a.h) + static_cast<size_t>(min(tq0 + i, a.T - 1)) * a.d + 8 * m;
+    wp[i] = wt + static_cast<size_t>(min(eq0 + i, a.E - 1)) * a.d + 8 * m;
+  }
+  float acc[16][8];
+#pragma unroll
+  for (int q = 0; q < 16; ++q)
+#pragma unroll
+    for (int k = 0; k < 8; ++k) acc[q][k] = 0.0f;
+  const int steps = a.d / 64;
+  uint4 hn[4][VPR], wn[4][VPR];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int v = 0; v < VPR; ++v) {
+      hn[i][v] = ld16(hp[i] + 8 / VPR * v);
+      wn[i][v] = ld16(wp[i] + 8 / VPR * v);
+    }
+  for (int st = 0; st < steps; ++st) {
+    uint4 hc[4][VPR], wc[4][VPR];
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int v = 0; v < VPR; ++v) {
+        hc[i][v] = hn[i][v];
+        wc[i][v] = wn[i][v];
+      }
+    // next step's loads (the last step reloads itself: always in bounds)
+    const size_t nx = static_cast<size_t>(64) * min(st + 1, steps - 1);
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int v = 0; v < VPR; ++v) {
+        hn[i][v] = ld16(hp[i] + nx + 8 / VPR * v);
+        wn[i][v] = ld16(wp[i] + nx + 8 / VPR * v);
+      }
+    float wf[4][8];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      if constexpr (VPR == 1) {
+        unpack(wc[i][0], wf[i]);
+      } else {
+        float lo[4], hi[4];
+        unpack(wc[i][0], lo);
+        unpack(wc[i][1], hi);
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+          wf[i][k] = lo[k];
+          wf[i][4 + k] = hi[k];
+        }
+      }
+    }
+#pragma unroll
+    for (int ti = 0; ti < 4; ++ti) {
+      float hf[8];
+      if constexpr (VPR == 1) {
+        unpack(hc[ti][0], hf);
+      } else {
+        float lo[4], hi[4];
+        unpack(hc[ti][0], lo);
+        unpack(hc[ti][1], hi);
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+          hf[k] = lo[k];
+          hf[4 + k] = hi[k];
+        }
+      }
+#pragma unroll
+      for (int ei = 0; ei < 4; ++ei)
+#pragma unroll
+        for (int k = 0; k < 8; ++k) acc[4 * ti + ei][k] = fmaf(hf[k], wf[ei][k], acc[4 * ti + ei][k]);
+    }
+  }
+  // residues l, l + 32 (lanes m, m ^ 4): keep outputs [8 b2, 8 b2 + 8)
+  float r1[8][8];
+  {
+    const bool up = (m & 4) != 0;
+#pragma unroll
+    for (int j = 0; j < 8; ++j)
+#pragma unroll
+      for (int k = 0; k < 8; ++k) {
+        const float send = up ? acc[j][k] : acc[j + 8][k];
+        const float keep = up ? acc[j + 8][k] : acc[j][k];
+        r1[j][k] = keep + __shfl_xor(send, 4, 64);
+      }
+  }
+  float r2[4][8];
+  {
+    const bool up = (m & 2) != 0;
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+#pragma unroll
+      for (int k = 0; k < 8; ++k) {
+        const float send = up ? r1[j][k] : r1[j + 4][k];
+        const float keep = up ? r1[j + 4][k] : r1[j][k];
+        r2[j][k] = keep + __shfl_xor(send, 2, 64);
+      }
+  }
+  float r3[2][8];
+  {
+    const bool up = (m & 1) != 0;
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+      for (int k = 0; k < 8; ++k) {
+        const float send = up ? r2[j][k] : r2[j + 2][k];
+        const float keep = up ? r2[j + 2][k] : r2[j][k];
+        r3[j][k] = keep + __shfl_xor(send, 1, 64);
+      }
+  }
+  // this lane now holds outputs q = 2 m + j (token q / 4, expert q % 4)
+#pragma unroll
+  for (int j = 0; j < 2; ++j) {
+    const float* r = r3[j];
+    float v = ((r[0] + r[4]) + (r[2] + r[6])) + ((r[1] + r[5]) + (r[3] + r[7]));
+    const int q = 2 * m + j;
+    const int t = tq0 + (q >> 2), e = eq0 + (q & 3);
+    if (t < a.T && e < a.E) {
+      if (bias != nullptr) v = v + bias[e];
+      out[static_cast<size_t>(t) * a.E + e] = v;
+    }
+  }
+}
+
+// Logits launch, then the route launches (a kernel boundary, not a device-
+// scope fence, hands data between the steps: with one L2 per XCD such
+// fences write back and invalidate L2 and cost far more than a launch).
 hipError_t launch_logits_route(const LogitsArgs& a, const RouteArgs& ra, hipStream_t s) {
   if (a.T <= 0) return hipSuccess;
-  const int nb = (a.E + kLgBlock - 1) / kLgBlock;
   const int mats = (a.wr != nullptr ? 1 : 0) + (a.wr2 != nullptr ? 1 : 0);
   if (mats == 0) return hipErrorInvalidValue;
   LogitsArgs b = a;
   if (a.wr == nullptr) {  // only the second router: move it to slot 0
     b.wr = a.wr2;
+    b.wt = a.wt2;
     b.bias = a.bias2;
     b.logits = a.logits2;
     b.wr2 = nullptr;
+    b.wt2 = nullptr;
   }
-  const dim3 grid((a.T + kLgWaves - 1) / kLgWaves, nb * mats);
-  if (a.dtype == kBF16)
-    hipLaunchKernelGGL(logits_kernel<uint16_t>, grid, dim3(64 * kLgWaves), 0, s, b);
-  else
-    hipLaunchKernelGGL(logits_kernel<float>, grid, dim3(64 * kLgWaves), 0, s, b);
+  const int TB = route_block_tokens(ra.K);
+  const int nblk = (a.T + TB - 1) / TB;
+  const bool many = a.T >= kManyTokens && b.wt != nullptr && (mats == 1 || b.wt2 != nullptr) &&
+                    ra.lrank != nullptr && ra.blk != nullptr && ra.psc != nullptr && nblk <= ra.nblk_cap &&
+                    TB * ra.K <= 64 * kSelWaves;
+  if (many) {
+    const int nb = (a.E + kLmExperts - 1) / kLmExperts;
+    const dim3 grid((a.T + kLmTokens - 1) / kLmTokens, nb * mats);
+    if (a.dtype == kBF16)
+      hipLaunchKernelGGL(logits_many_kernel<uint16_t>, grid, dim3(256), 0, s, b);
+    else
+      hipLaunchKernelGGL(logits_many_kernel<float>, grid, dim3(256), 0, s, b);
+  } else {
+    const int nb = (a.E + kLgBlock - 1) / kLgBlock;
+    const dim3 grid((a.T + kLgWaves - 1) / kLgWaves, nb * mats);
+    if (a.dtype == kBF16)
+      hipLaunchKernelGGL(logits_kernel<uint16_t>, grid, dim3(64 * kLgWaves), 0, s, b);
+    else
+      hipLaunchKernelGGL(logits_kernel<float>, grid, dim3(64 * kLgWaves), 0, s, b);
+  }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(route_kernel, dim3(1), dim3(64 * kRouteWaves), 0, s, ra);
-  return hipGetLastError();
+  if (!many) {
+    hipLaunchKernelGGL(route_kernel, dim3(1), dim3(64 * kRouteWaves), 0, s, ra);
+    return hipGetLastError();
+  }
+  hipLaunchKernelGGL(select_many_kernel, dim3(nblk), dim3(64 * kSelWaves), 0, s, ra, TB);
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  hipLaunchKernelGGL(scan_many_kernel, dim3(1), dim3(64 * kScanWaves), 0, s, ra, nblk);
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  if (ra.logits != nullptr) {
+    hipLaunchKernelGGL(scatter_many_kernel, dim3((a.T * ra.K + 255) / 256), dim3(256), 0, s, ra, TB);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+  }
+  return hipSuccess;
 }
 
 // --------------------------------------------------------------- SwiGLU FFN
@@ -877,6 +1192,45 @@ hipError_t launch_mma_gateup(const MmaArgs& a, hipStream_t s) {
 hipError_t launch_mma_down(const MmaArgs& a, hipStream_t s) {
   if (a.n_wg <= 0 || a.n_tasks <= 0) return hipSuccess;
   hipLaunchKernelGGL(mma_down_kernel, dim3(a.n_wg), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+// --------------------------------------------------------------- H2D copy
+//
+// Each work-group moves 256 x kH2dUnroll 16-byte pieces per round (all loads
+// of a round issued before its stores), rounds strided over the grid.  32
+// work-groups keep enough PCIe reads in flight to reach the link rate.
+
+constexpr int kH2dUnroll = 4;
+
+__global__ __launch_bounds__(256) void h2d_kernel(uint4* __restrict__ dst, const uint4* __restrict__ src,
+                                                  uint64_t n) {
+  const uint64_t stride = static_cast<uint64_t>(gridDim.x) * 256 * kH2dUnroll;
+  for (uint64_t base = static_cast<uint64_t>(blockIdx.x) * 256 * kH2dUnroll + threadIdx.x; base < n;
+       base += stride) {
+    uint4 v[kH2dUnroll];
+#pragma unroll
+    for (int u = 0; u < kH2dUnroll; ++u) {
+      const uint64_t i = base + static_cast<uint64_t>(u) * 256;
+      v[u] = src[i < n ? i : n - 1];  // clamped: every load is issued and in bounds
+    }
+#pragma unroll
+    for (int u = 0; u < kH2dUnroll; ++u) {
+      const uint64_t i = base + static_cast<uint64_t>(u) * 256;
+      if (i < n) dst[i] = v[u];
+    }
+  }
+}
+
+hipError_t launch_h2d(void* dst, const void* src, uint64_t bytes, hipStream_t s) {
+  if (bytes == 0) return hipSuccess;
+  if ((bytes % 16) != 0 || (reinterpret_cast<uintptr_t>(dst) % 16) != 0 || (reinterpret_cast<uintptr_t>(src) % 16) != 0)
+    return hipErrorInvalidValue;
+  const uint64_t n = bytes / 16;
+  const uint64_t per_wg = 256ull * kH2dUnroll;
+  const int wgs = static_cast<int>(std::min<uint64_t>(kH2dWorkGroups, (n + per_wg - 1) / per_wg));
+  hipLaunchKernelGGL(h2d_kernel, dim3(wgs), dim3(256), 0, s, static_cast<uint4*>(dst),
+                     static_cast<const uint4*>(src), n);
   return hipGetLastError();
 }
 

@@ -28,6 +28,7 @@ constexpr uint64_t kAlign = 256;
 constexpr uint64_t kGroupTargetBytes = 16ull << 20;  // H2D copy granularity
 constexpr int kPrefetchWindow = 2;                   // prefetch groups in flight
 constexpr int kMaxD = 8192;
+constexpr int kReserved = 1 << 30;                   // BufSlot::use_order of a reserved slot
 
 uint64_t align_up(uint64_t x, uint64_t a) { return (x + a - 1) / a * a; }
 
@@ -41,6 +42,8 @@ struct Shape {
   // fixed pool layout (byte offsets)
   uint64_t off_router, off_bias, off_shared, off_logits, off_logits2, off_offsets, off_perm, off_pos;
   uint64_t off_part, off_part_sh, off_red, off_act, off_act_sh, off_score, off_order, off_buffer, fixed_bytes;
+  uint64_t off_router_t, off_lrank, off_blk, off_psc;
+  int nblk_cap;  // token blocks of the many-token routing
   uint64_t router_stride, bias_stride, part_bytes, part_sh_bytes;
   int64_t sh_plane;
 };
@@ -103,6 +106,8 @@ ms_status derive_shape(const ms_model_desc* d, Shape* s, std::string* err) {
   s->router_stride = align_up(static_cast<uint64_t>(s->d) * s->E * s->elem, kAlign);
   s->off_router = off;
   off += s->router_stride * s->L;
+  s->off_router_t = off;  // the same routers transposed, [E][d]
+  off += s->router_stride * s->L;
   s->bias_stride = align_up(static_cast<uint64_t>(s->E) * 4, kAlign);
   s->off_bias = off;
   off += s->bias_stride * s->L;
@@ -141,6 +146,16 @@ ms_status derive_shape(const ms_model_desc* d, Shape* s, std::string* err) {
     s->off_act_sh = off;
     off += align_up(static_cast<uint64_t>(s->n_sh) * s->max_T * s->n_chunks_sh * kUnits * 2, kAlign);
   }
+
+  // many-token routing workspace
+  const int tb = msk::route_block_tokens(s->K);
+  s->nblk_cap = (s->max_T + tb - 1) / tb;
+  s->off_lrank = off;
+  off += align_up(TK * 4, kAlign);
+  s->off_blk = off;
+  off += align_up(static_cast<uint64_t>(s->E) * s->nblk_cap * 4, kAlign);
+  s->off_psc = off;
+  off += align_up(static_cast<uint64_t>(s->E) * s->nblk_cap * 4, kAlign);
 
   s->off_score = off;
   off += align_up(static_cast<uint64_t>(s->E) * 4, kAlign);
@@ -228,7 +243,8 @@ struct BufSlot {
   hipEvent_t last_read = nullptr; // side-stream event after the last reader
   bool has_last_read = false;
   uint64_t tick = 0;              // last use
-  int use_order = -1;             // order of use in the running forward (-1: not used)
+  int use_order = -1;             // order of use in the running forward (-1: not used,
+                                  // kReserved: holds an expert not yet processed)
 };
 
 struct LayerState {
@@ -275,7 +291,8 @@ struct ms_ctx {
   uint64_t pool_bytes = 0;
   hipStream_t copy = nullptr, side = nullptr;
   // pinned host store
-  std::vector<unsigned char*> blobs;
+  std::vector<unsigned char*> blobs;      // pinned, coherent host memory (never cached by the GPU)
+  std::vector<unsigned char*> blobs_dev;  // the same memory's device-side addresses
   int blob_cap = 0;  // 0: unlimited
   // host-visible small buffers written by kernels
   int32_t* h_offsets = nullptr;
@@ -362,9 +379,11 @@ void tl_end(ms_ctx* ctx, int idx, hipStream_t st) {
 
 // ---- copies
 
-ms_status issue_copy(ms_ctx* ctx, void* dst, const void* src, uint64_t bytes, int kind, int layer) {
+// H2D copy on the copy stream from a host blob (src_dev: its device-side
+// address), by the streaming copy kernel.
+ms_status issue_copy(ms_ctx* ctx, void* dst, const void* src_dev, uint64_t bytes, int kind, int layer) {
   const int ti = tl_begin(ctx, ctx->copy, kind, layer, bytes);
-  MS_HIP(hipMemcpyAsync(dst, src, bytes, hipMemcpyHostToDevice, ctx->copy));
+  MS_HIP(msk::launch_h2d(dst, src_dev, bytes, ctx->copy));
   tl_end(ctx, ti, ctx->copy);
   return MS_OK;
 }
@@ -374,7 +393,7 @@ ms_status issue_group(ms_ctx* ctx, int si, int gi, bool prefetch) {
   BufSlot& b = ctx->buf[si];
   Group& g = b.groups[gi];
   const uint64_t cb = ctx->s.chunk_bytes;
-  const unsigned char* src = ctx->blobs[ctx->layers[b.layer].blob_of[b.expert]];
+  const unsigned char* src = ctx->blobs_dev[ctx->layers[b.layer].blob_of[b.expert]];
   const uint64_t off = cb * g.c_lo, bytes = cb * (g.c_hi - g.c_lo);
   ms_status st = issue_copy(ctx, b.base + off, src + off, bytes,
                             prefetch ? MS_IV_COPY_PREFETCH : MS_IV_COPY_MISS, b.layer);
@@ -399,11 +418,15 @@ ms_status assign_slot(ms_ctx* ctx, int si, int layer, int e, int first) {
   b.expert = e;
   b.first_chunk = first;
   b.groups.clear();
+  // at most group_chunks per copy, in groups of near-equal size (a small
+  // tail copy runs far below the link rate)
   const int n = ctx->s.n_chunks, G = ctx->s.group_chunks;
-  for (int c = first; c < n; c += G) {
+  const int ng = (n - first + G - 1) / G;
+  const int per = ng > 0 ? (n - first + ng - 1) / ng : 1;
+  for (int c = first; c < n; c += per) {
     Group g;
     g.c_lo = c;
-    g.c_hi = std::min(n, c + G);
+    g.c_hi = std::min(n, c + per);
     b.groups.push_back(g);
   }
   while (b.gev.size() < b.groups.size()) {
@@ -413,6 +436,10 @@ ms_status assign_slot(ms_ctx* ctx, int si, int layer, int e, int first) {
   }
   return MS_OK;
 }
+
+// Resident chunks of expert e in layer L: [0, top_chunks) if its top is
+// cached, none otherwise.
+int resident_chunks(const LayerState& L, int e) { return L.slot_of[e] >= 0 ? L.top_chunks : 0; }
 
 void clear_slot(BufSlot& b) {
   b.layer = -1;
@@ -428,8 +455,9 @@ int find_slot(ms_ctx* ctx, int layer, int e) {
 
 // Pick a staging slot for new content.  Prefers empty slots, then the least
 // recently used slot not used by the running forward; if allow_busy, falls
-// back to the slot the running forward used first (its readers were already
-// enqueued, and the copy stream will wait for them).
+// back to the slot whose readers in the running forward were enqueued first
+// (the copy stream will wait for them).  Reserved slots are never taken;
+// returns -1 if nothing can be taken.
 int pick_victim(ms_ctx* ctx, bool allow_busy) {
   int best = -1;
   for (int i = 0; i < static_cast<int>(ctx->buf.size()); ++i) {
@@ -439,9 +467,32 @@ int pick_victim(ms_ctx* ctx, bool allow_busy) {
     if (best < 0 || b.tick < ctx->buf[best].tick) best = i;
   }
   if (best >= 0 || !allow_busy) return best;
-  for (int i = 0; i < static_cast<int>(ctx->buf.size()); ++i)
-    if (best < 0 || ctx->buf[i].use_order < ctx->buf[best].use_order) best = i;
+  for (int i = 0; i < static_cast<int>(ctx->buf.size()); ++i) {
+    const int u = ctx->buf[i].use_order;
+    if (u >= kReserved) continue;
+    if (best < 0 || u < ctx->buf[best].use_order) best = i;
+  }
   return best;
+}
+
+// Active experts of a forward that miss chunks, in processing order: those
+// whose missing part a staging slot already holds come first, so that their
+// reserved slots are released before any other miss needs a victim.
+std::vector<int> miss_order(ms_ctx* ctx, int layer, const std::vector<int32_t>& offs,
+                            const std::vector<char>* skip) {
+  const LayerState& L = ctx->layers[layer];
+  std::vector<int> first, rest;
+  for (int e = 0; e < ctx->s.E; ++e) {
+    if (offs[e + 1] == offs[e] || resident_chunks(L, e) >= ctx->s.n_chunks) continue;
+    if (skip && (*skip)[e]) continue;
+    const int si = find_slot(ctx, layer, e);
+    if (si >= 0 && ctx->buf[si].first_chunk <= resident_chunks(L, e))
+      first.push_back(e);
+    else
+      rest.push_back(e);
+  }
+  first.insert(first.end(), rest.begin(), rest.end());
+  return first;
 }
 
 // Keep up to kPrefetchWindow prefetch groups in flight.
@@ -486,9 +537,6 @@ void terminate_prefetch(ms_ctx* ctx) {
   }
 }
 
-// Resident chunks of expert e in layer L: [0, top_chunks) if its top is
-// cached, none otherwise.
-int resident_chunks(const LayerState& L, int e) { return L.slot_of[e] >= 0 ? L.top_chunks : 0; }
 
 // Enqueue the prefetch of experts[0..n) of `layer` (in order) into free
 // staging slots: the bottom if the top is cached, else the whole expert.
@@ -532,6 +580,14 @@ ms_status enqueue_prefetch(ms_ctx* ctx, int layer, const int32_t* experts, int n
 ms_status check_layer(ms_ctx* ctx, int layer) {
   if (layer < 0 || layer >= ctx->s.L) return fail(ctx, MS_E_INVALID, "layer out of range");
   return MS_OK;
+}
+
+void set_route_workspace(ms_ctx* ctx, msk::RouteArgs* r) {
+  const Shape& s = ctx->s;
+  r->lrank = reinterpret_cast<int32_t*>(ctx->dev(s.off_lrank));
+  r->blk = reinterpret_cast<int32_t*>(ctx->dev(s.off_blk));
+  r->psc = reinterpret_cast<float*>(ctx->dev(s.off_psc));
+  r->nblk_cap = s.nblk_cap;
 }
 
 // Order work on `stream` after the previous forward/prediction of this
@@ -616,6 +672,7 @@ ms_status prefill_experts(ms_ctx* ctx, int layer, const void* h_dev, int T, cons
   // statistics and, per active expert, whether all its chunks are in VRAM now
   std::vector<int> covering(s.E, -1);
   std::vector<char> complete(s.E, 0);
+  int use_counter = 0;
   std::vector<msk::MmaTask> gu, dn;
   for (int e = 0; e < s.E; ++e) {
     if (offs[e + 1] == offs[e]) continue;
@@ -659,7 +716,7 @@ ms_status prefill_experts(ms_ctx* ctx, int layer, const void* h_dev, int T, cons
     if (all_landed) {
       complete[e] = 1;
       dn.push_back(task(top ? top : b.base, b.base, e, 0, s.n_chunks, res, m_tiles(e)));
-      b.use_order = 1 << 30;  // read by this forward; not a victim
+      b.use_order = use_counter++;  // read first, by the compute stream
     }
   }
   for (int i = 0; i < s.n_sh; ++i) {
@@ -679,21 +736,19 @@ ms_status prefill_experts(ms_ctx* ctx, int layer, const void* h_dev, int T, cons
     }
   }
 
-  // experts still missing chunks: side stream.  Slots that already hold a
-  // pending expert's part are reserved so that no earlier miss evicts them.
+  // experts still missing chunks: side stream, those a staging slot already
+  // covers first.  Their slots stay reserved until then, so that no other
+  // miss evicts them.
   MS_HIP(hipStreamWaitEvent(ctx->side, ctx->ev_res, 0));
   for (int e = 0; e < s.E; ++e)
-    if (covering[e] >= 0 && !complete[e]) ctx->buf[covering[e]].use_order = 1 << 30;
-  int use_counter = 0;
-  for (int e = 0; e < s.E; ++e) {
-    if (offs[e + 1] == offs[e] || complete[e]) continue;
+    if (covering[e] >= 0 && !complete[e]) ctx->buf[covering[e]].use_order = kReserved;
+  for (const int e : miss_order(ctx, layer, offs, &complete)) {
     const int res = resident_chunks(L, e);
     int si = covering[e];
-    if (si >= 0 && !(ctx->buf[si].layer == layer && ctx->buf[si].expert == e && ctx->buf[si].first_chunk <= res))
-      si = -1;  // taken over by an earlier miss of this forward
     if (si < 0) {
       si = find_slot(ctx, layer, e);
       if (si < 0 || ctx->buf[si].first_chunk > res) si = pick_victim(ctx, true);
+      if (si < 0) return fail(ctx, MS_E_STATE, "no staging slot can be taken");
       st = assign_slot(ctx, si, layer, e, res);
       if (st != MS_OK) return st;
     }
@@ -877,6 +932,16 @@ ms_status ms_set_router(ms_ctx* ctx, int32_t layer, const void* w_r, const float
   const Shape& s = ctx->s;
   MS_HIP(hipMemcpy(ctx->dev(s.off_router + s.router_stride * layer), w_r,
                    static_cast<size_t>(s.d) * s.E * s.elem, hipMemcpyHostToDevice));
+  {
+    // transposed copy [E][d] for the many-token logits kernel
+    std::vector<unsigned char> wt(static_cast<size_t>(s.d) * s.E * s.elem);
+    const unsigned char* src = static_cast<const unsigned char*>(w_r);
+    for (int j = 0; j < s.d; ++j)
+      for (int e = 0; e < s.E; ++e)
+        std::memcpy(&wt[(static_cast<size_t>(e) * s.d + j) * s.elem], src + (static_cast<size_t>(j) * s.E + e) * s.elem,
+                    s.elem);
+    MS_HIP(hipMemcpy(ctx->dev(s.off_router_t + s.router_stride * layer), wt.data(), wt.size(), hipMemcpyHostToDevice));
+  }
   LayerState& L = ctx->layers[layer];
   if (bias) MS_HIP(hipMemcpy(ctx->dev(s.off_bias + s.bias_stride * layer), bias, sizeof(float) * s.E,
                              hipMemcpyHostToDevice));
@@ -905,19 +970,49 @@ ms_status ms_set_expert(ms_ctx* ctx, int32_t layer, int32_t e, const void* w_gat
   if (bi < 0) {
     if (ctx->blob_cap > 0 && static_cast<int>(ctx->blobs.size()) >= ctx->blob_cap)
       return fail(ctx, MS_E_NOMEM, "host expert store is full (host_store_experts)");
+    // coherent: the copy kernel reads it over PCIe uncached, so a blob
+    // rewritten (or freed and reallocated) later is never read stale
     void* p = nullptr;
-    hipError_t he = hipHostMalloc(&p, s.expert_bytes);
+    hipError_t he = hipHostMalloc(&p, s.expert_bytes, hipHostMallocCoherent);
     if (he != hipSuccess || !p) {
       (void)hipGetLastError();
       return fail(ctx, MS_E_NOMEM, "hipHostMalloc of an expert blob failed");
     }
+    void* pd = nullptr;
+    he = hipHostGetDevicePointer(&pd, p, 0);
+    if (he != hipSuccess || !pd) {
+      (void)hipGetLastError();
+      (void)hipHostFree(p);
+      return fail(ctx, MS_E_NOMEM, "expert blob has no device address");
+    }
     ctx->blobs.push_back(static_cast<unsigned char*>(p));
+    ctx->blobs_dev.push_back(static_cast<unsigned char*>(pd));
     bi = static_cast<int>(ctx->blobs.size()) - 1;
   }
-  // the blob may be read by in-flight copies: wait for them before rewriting
-  MS_HIP(hipStreamSynchronize(ctx->copy));
+  // the blob may be read by work in flight: drain it before rewriting
+  st = ms_sync(ctx);
+  if (st != MS_OK) return st;
   pack_expert(w_gate, w_up, w_down, s.d, s.F, s.n_chunks, s.elem, ctx->blobs[bi]);
   L.blob_of[e] = bi;
+  // copies of the old weights: staging slots are dropped (with any queued
+  // prefetch), cached top segments are copied again
+  ctx->pf_queue.clear();
+  ctx->pf_inflight.clear();
+  for (BufSlot& b : ctx->buf)
+    if (b.layer >= 0 && ctx->layers[b.layer].blob_of[b.expert] == bi) clear_slot(b);
+  for (int l = 0; l < s.L; ++l) {
+    LayerState& L2 = ctx->layers[l];
+    for (int e2 = 0; e2 < s.E; ++e2) {
+      if (L2.blob_of[e2] != bi || L2.slot_of[e2] < 0) continue;
+      st = issue_copy(ctx, L2.cache_base + L2.top_bytes * L2.slot_of[e2], ctx->blobs_dev[bi], L2.top_bytes,
+                      MS_IV_COPY_TOP, l);
+      if (st != MS_OK) return st;
+      hipEvent_t ev;
+      MS_HIP(new_event(ctx, &ev));
+      MS_HIP(hipEventRecord(ev, ctx->copy));
+      L2.pending_loads.push_back(ev);
+    }
+  }
   return MS_OK;
 }
 
@@ -1018,7 +1113,7 @@ ms_status ms_load_top(ms_ctx* ctx, int32_t layer, int32_t e) {
     }
   if (slot < 0) return fail(ctx, MS_E_BUDGET, "no free top-segment slot in this layer");
   if (L.has_last_fwd) MS_HIP(hipStreamWaitEvent(ctx->copy, L.last_fwd, 0));
-  st = issue_copy(ctx, L.cache_base + L.top_bytes * slot, ctx->blobs[L.blob_of[e]], L.top_bytes, MS_IV_COPY_TOP,
+  st = issue_copy(ctx, L.cache_base + L.top_bytes * slot, ctx->blobs_dev[L.blob_of[e]], L.top_bytes, MS_IV_COPY_TOP,
                   layer);
   if (st != MS_OK) return st;
   hipEvent_t ev;
@@ -1094,6 +1189,7 @@ ms_status ms_predict(ms_ctx* ctx, int32_t layer, const void* h_dev, int32_t T, v
   la.E = s.E;
   la.dtype = s.dtype;
   la.wr2 = ctx->dev(s.off_router + s.router_stride * layer);
+  la.wt2 = ctx->dev(s.off_router_t + s.router_stride * layer);
   la.bias2 = L.bias_set ? reinterpret_cast<const float*>(ctx->dev(s.off_bias + s.bias_stride * layer)) : nullptr;
   la.logits2 = reinterpret_cast<float*>(ctx->dev(s.off_logits2));
   msk::RouteArgs rk{};
@@ -1102,6 +1198,7 @@ ms_status ms_predict(ms_ctx* ctx, int32_t layer, const void* h_dev, int32_t T, v
   rk.K = s.K;
   rk.renormalize = s.renorm;
   rk.logits_pred = la.logits2;
+  set_route_workspace(ctx, &rk);
   rk.score = reinterpret_cast<float*>(ctx->dev(s.off_score));
   rk.order = reinterpret_cast<int32_t*>(ctx->dev(s.off_order));
   rk.host_score = ctx->d_score_map;
@@ -1168,11 +1265,13 @@ ms_status ms_forward(ms_ctx* ctx, int32_t layer, const void* h_dev, int32_t T, f
   la.E = s.E;
   la.dtype = s.dtype;
   la.wr = ctx->dev(s.off_router + s.router_stride * layer);
+  la.wt = ctx->dev(s.off_router_t + s.router_stride * layer);
   la.bias = L.bias_set ? reinterpret_cast<const float*>(ctx->dev(s.off_bias + s.bias_stride * layer)) : nullptr;
   la.logits = reinterpret_cast<float*>(ctx->dev(s.off_logits));
   if (predict_next) {
     const LayerState& N = ctx->layers[next_layer];
     la.wr2 = ctx->dev(s.off_router + s.router_stride * next_layer);
+    la.wt2 = ctx->dev(s.off_router_t + s.router_stride * next_layer);
     la.bias2 = N.bias_set ? reinterpret_cast<const float*>(ctx->dev(s.off_bias + s.bias_stride * next_layer)) : nullptr;
     la.logits2 = reinterpret_cast<float*>(ctx->dev(s.off_logits2));
   }
@@ -1190,6 +1289,7 @@ ms_status ms_forward(ms_ctx* ctx, int32_t layer, const void* h_dev, int32_t T, f
   ga.perm = d_perm;
   ga.pos = d_pos;
   ga.host_offsets = ctx->d_offsets_map;
+  set_route_workspace(ctx, &ga);
   if (predict_next) {
     ga.logits_pred = la.logits2;
     ga.score = reinterpret_cast<float*>(ctx->dev(s.off_score));
@@ -1354,7 +1454,6 @@ ms_status ms_forward(ms_ctx* ctx, int32_t layer, const void* h_dev, int32_t T, f
   MS_HIP(hipStreamWaitEvent(ctx->side, any_pre ? ctx->ev_res : ctx->ev_route, 0));
   // slots already holding an active expert's missing part are reserved so
   // that no other miss of this forward evicts them first
-  constexpr int kReserved = 1 << 30;
   for (int e = 0; e < s.E; ++e) {
     if (offs[e + 1] == offs[e]) continue;
     const int si = find_slot(ctx, layer, e);
@@ -1419,20 +1518,22 @@ ms_status ms_forward(ms_ctx* ctx, int32_t layer, const void* h_dev, int32_t T, f
     if (offs[e + 1] == offs[e]) continue;
     L.st.experts_active += 1;
     const int res = resident_chunks(L, e);
-    if (res >= s.n_chunks) {
+    if (res >= s.n_chunks)
       L.st.alpha += 1;
-      continue;
-    }
-    if (res > 0)
+    else if (res > 0)
       L.st.beta += 1;
     else
       L.st.gamma += 1;
+  }
+  for (const int e : miss_order(ctx, layer, offs, nullptr)) {
+    const int res = resident_chunks(L, e);
     int si = find_slot(ctx, layer, e);
     bool hit = false;
     if (si >= 0 && ctx->buf[si].first_chunk <= res) {
       for (const Group& g : ctx->buf[si].groups) hit = hit || g.issued;
     } else {
       if (si < 0) si = pick_victim(ctx, true);
+      if (si < 0) return fail(ctx, MS_E_STATE, "no staging slot can be taken");
       st = assign_slot(ctx, si, layer, e, res);
       if (st != MS_OK) return st;
     }
@@ -1544,6 +1645,13 @@ ms_status ms_timeline_begin(ms_ctx* ctx, void* stream, int32_t capacity) {
     ctx->tl_pool.push_back(r.e1);
   }
   ctx->tl.clear();
+  // every record's two events exist before recording starts: creating
+  // events while work is in flight would perturb what is measured
+  while (static_cast<int64_t>(ctx->tl_pool.size()) < 2ll * capacity) {
+    hipEvent_t ev;
+    MS_HIP(hipEventCreate(&ev));
+    ctx->tl_pool.push_back(ev);
+  }
   if (!ctx->tl_origin) MS_HIP(hipEventCreate(&ctx->tl_origin));
   MS_HIP(hipEventRecord(ctx->tl_origin, static_cast<hipStream_t>(stream)));
   ctx->tl_on = true;

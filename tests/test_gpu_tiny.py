@@ -239,3 +239,29 @@ def test_tiny_every_chunk_split_matches_oracle(splits):
             check_layer(r, 0, hf, y, idx, w)
             outs.append(y.cpu().numpy())
         assert np.array_equal(outs[0], outs[1]) and np.array_equal(outs[0], outs[2])
+
+
+def test_tiny_rewritten_expert_is_streamed_fresh():
+    """Expert weights set again after forwards have streamed (and cached)
+    the old ones -- the same host blob, rewritten in place: the next forward
+    uses only the new weights, streamed and cached."""
+    from paper_2509_08342_amd import moesplit as ms
+    from workload import SplitRig, top_bytes
+    with SplitRig(synth.TINY, seed=0, max_tokens=8, budget_bytes=8 * synth.TINY.expert_bytes) as r:
+        r.configure([4 * top_bytes(r, 0.5)], [0.5])
+        r.load_tops(0, [0, 1, 2, 3])
+        h, hf = r.hidden(8, tag=61)
+        for _ in range(2):
+            y, idx, w = r.outputs(8)
+            r.forward(0, h, 8, y, idx, w)
+            torch.cuda.synchronize()
+        check_layer(r, 0, hf, y, idx, w)
+        for e in range(8):
+            ex = synth.expert(synth.TINY, 17, 0, e)
+            ms.ms_set_expert(r.ctx, 0, e, *ex.raw)
+            r.experts[0][e] = ex.f32
+        assert ms.ms_residency(r.ctx, 0, 8).tolist() == [1, 1, 1, 1, 0, 0, 0, 0]
+        y, idx, w = r.outputs(8)
+        r.forward(0, h, 8, y, idx, w)
+        torch.cuda.synchronize()
+        check_layer(r, 0, hf, y, idx, w)
