@@ -31,6 +31,43 @@ sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBPS = 8000.0
 GIB = 1 << 30
+PROFILES = os.path.join(ROOT, "profiles")
+CALIB_BYTES = 256 << 20   # device-to-device copy that calibrates the PMC byte counters
+FFN_KERNELS = ("ffn_chunk_kernel", "mma_gateup_kernel", "mma_down_kernel")
+
+
+def kernel_sources_sha():
+    """Hash of the kernel sources: PMC traffic figures hold only for them."""
+    import hashlib
+    h = hashlib.sha256()
+    for f in ("kernels.hip", "kernels.h"):
+        with open(os.path.join(ROOT, "paper_2509_08342_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
+
+
+def pmc_profile_path(workload):
+    return os.path.join(PROFILES, "ffn_%s_pmc.md" % workload)
+
+
+def traffic_from_profile(workload):
+    """HBM bytes per FFN launch from the committed PMC summary of this
+    workload, or None when there is none or the kernels changed since."""
+    path = pmc_profile_path(workload)
+    if not os.path.exists(path):
+        return None
+    vals = {}
+    with open(path) as f:
+        for line in f:
+            if ":" in line and line.startswith("- ") and "`" in line:
+                k, v = line[2:].split(":", 1)
+                vals[k.strip().strip("`")] = v.strip().strip("`")
+    if vals.get("kernels_sha256") != kernel_sources_sha():
+        return None
+    try:
+        return int(vals["ffn_traffic_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
 
 # name -> (shape, tokens per step, split ratio, per-layer budget in top
 # segments (None: whole budget of the reference config), which tops to cache)
@@ -101,6 +138,13 @@ def analyse(tl, steps, ms_per_step):
         rs = by.get(k, [])
         dur = sum(r["t1_ms"] - r["t0_ms"] for r in rs)
         kern[k] = dict(launches=len(rs), total_ms=dur, bytes=sum(r["bytes"] for r in rs))
+    # per-step latency: from a step's routing launch to its last record
+    starts = sorted(r["t0_ms"] for r in by.get("router", []))
+    step_ms = []
+    for i, t0 in enumerate(starts):
+        t1 = starts[i + 1] if i + 1 < len(starts) else float("inf")
+        ends = [r["t1_ms"] for r in tl if t0 <= r["t0_ms"] < t1]
+        step_ms.append(max(ends) - t0)
     copies = [r for k in COPY_KINDS for r in by.get(k, [])]
     copy_u = _union([(r["t0_ms"], r["t1_ms"]) for r in copies])
     kern_u = _union([(r["t0_ms"], r["t1_ms"]) for k in KERNEL_KINDS for r in by.get(k, [])])
@@ -118,6 +162,8 @@ def analyse(tl, steps, ms_per_step):
         hidden_frac=(both / copy_t) if copy_t > 0 else None,
         compute_hidden_frac=(both / kern_t) if kern_t > 0 else None,
         overlap_eta=eta,
+        step_us=({q: round(float(np.percentile(step_ms, p)) * 1e3, 1) for q, p in (("p10", 10), ("p50", 50), ("p90", 90))}
+                 if step_ms else None),
         miss_bytes=sum(r["bytes"] for r in by.get("copy_miss", [])),
         prefetch_bytes=sum(r["bytes"] for r in by.get("copy_prefetch", [])),
     )
@@ -142,7 +188,7 @@ def ffn_roofline(an):
 
 # ------------------------------------------------------------------ timing
 
-def run_steps(rig, hs, steps, warmup, flags, timeline=True, cold=False, T=1):
+def run_steps(rig, hs, steps, warmup, flags, timeline=True, cold=False, T=1, before_timed=None):
     """Time `steps` batches of T tokens through layer 0.  cold=True drops the
     staging buffer before every batch, so each pays all of its misses."""
     import torch
@@ -159,6 +205,8 @@ def run_steps(rig, hs, steps, warmup, flags, timeline=True, cold=False, T=1):
     ms.ms_sync(rig.ctx)
     torch.cuda.synchronize()
     ms.ms_reset_stats(rig.ctx)
+    if before_timed is not None:
+        before_timed()
     if timeline:
         # room for every record of the timed steps (events are created up front)
         cap = min(1 << 16, max(1024, steps * (4 * rig.shape.n_experts + 64)))
@@ -225,6 +273,103 @@ def log(msg):
     print("[bench] " + msg, file=sys.stderr, flush=True)
 
 
+# ------------------------------------------------------- rocprofv3 summaries
+
+def _read_rows(d, suffix):
+    import csv
+    import glob
+    rows = []
+    for f in sorted(glob.glob(os.path.join(d, "**", "*" + suffix), recursive=True)):
+        with open(f, newline="") as fh:
+            rows.extend(csv.DictReader(fh))
+    if not rows:
+        raise SystemExit("no *%s under %s" % (suffix, d))
+    return rows
+
+
+def _counter_by_dispatch(d):
+    """{dispatch id: (kernel name, counter value)} from a --pmc run of one counter."""
+    out = {}
+    for r in _read_rows(d, "counter_collection.csv"):
+        did = int(r["Dispatch_Id"])
+        name, val = r["Kernel_Name"], float(r["Counter_Value"])
+        prev = out.get(did)
+        out[did] = (name, val + (prev[1] if prev else 0.0))
+    return out
+
+
+def pmc_summary(fetch_dir, write_dir, workload, out, cmd_fetch, cmd_write):
+    """FETCH_SIZE and WRITE_SIZE (KiB per dispatch) of the FFN kernels in the
+    timed steps of a --pmc-pass run, each scaled by the same counter on the
+    calibration copy of CALIB_BYTES (the largest __amd_rocclr_copyBuffer
+    dispatch, issued just before the timed steps)."""
+    res = {}
+    for label, d in (("FETCH_SIZE", fetch_dir), ("WRITE_SIZE", write_dir)):
+        by = _counter_by_dispatch(d)
+        copies = [(v[1], did) for did, v in by.items() if "copyBuffer" in v[0]]
+        cal_kib, cal_id = max(copies)
+        factor = cal_kib * 1024.0 / CALIB_BYTES
+        kern = {}
+        for did, (name, val) in by.items():
+            if did <= cal_id:
+                continue
+            short = name.split("(")[0].replace("void ", "")
+            k = kern.setdefault(short, [0, 0.0])
+            k[0] += 1
+            k[1] += val
+        res[label] = dict(cal_kib=cal_kib, factor=factor, kern=kern)
+    f_fac, w_fac = res["FETCH_SIZE"]["factor"], res["WRITE_SIZE"]["factor"]
+    names = sorted(set(res["FETCH_SIZE"]["kern"]) | set(res["WRITE_SIZE"]["kern"]))
+    ffn_n, ffn_bytes = 0, 0.0
+    lines = ["# FFN kernels, %s workload: HBM traffic from rocprofv3 counters" % workload, "",
+             "Commands (from the repository root, on one MI355X):", "",
+             "    " + cmd_fetch, "    " + cmd_write, "",
+             "Calibration: a device-to-device copy of %d bytes (torch copy_, the runtime's "
+             "copyBuffer kernel) issued right before the timed steps; each counter is divided "
+             "by what it reads for that copy per byte moved." % CALIB_BYTES, "",
+             "| counter | calibration copy reads (KiB) | factor (counter bytes per byte moved) |",
+             "|---|---|---|",
+             "| FETCH_SIZE | %.0f | %.4f |" % (res["FETCH_SIZE"]["cal_kib"], f_fac),
+             "| WRITE_SIZE | %.0f | %.4f |" % (res["WRITE_SIZE"]["cal_kib"], w_fac), "",
+             "Dispatches after the calibration copy (warm-up excluded), scaled bytes per dispatch:", "",
+             "| kernel | dispatches | fetch MB/dispatch | write MB/dispatch |", "|---|---|---|---|"]
+    for n in names:
+        fk = res["FETCH_SIZE"]["kern"].get(n, [0, 0.0])
+        wk = res["WRITE_SIZE"]["kern"].get(n, [0, 0.0])
+        cnt = max(fk[0], wk[0])
+        fb = fk[1] * 1024.0 / f_fac / max(fk[0], 1)
+        wb = wk[1] * 1024.0 / w_fac / max(wk[0], 1)
+        lines.append("| `%s` | %d | %.3f | %.3f |" % (n, cnt, fb / 1e6, wb / 1e6))
+        if any(k in n for k in FFN_KERNELS):
+            ffn_n += cnt
+            ffn_bytes += (fb + wb) * cnt
+    per = int(ffn_bytes / max(ffn_n, 1))
+    lines += ["", "Figures bench.py reads (valid while the kernel sources hash the same):", "",
+              "- `workload`: `%s`" % workload,
+              "- `ffn_dispatches`: `%d`" % ffn_n,
+              "- `ffn_traffic_bytes_per_launch`: `%d`" % per,
+              "- `kernels_sha256`: `%s`" % kernel_sources_sha(), ""]
+    with open(out, "w") as f:
+        f.write("\n".join(lines))
+    print("wrote %s: %d FFN dispatches, %.3f MB per launch" % (out, ffn_n, per / 1e6))
+
+
+def trace_summary(d, out, cmd):
+    """Kernel statistics of a rocprofv3 --kernel-trace --stats run."""
+    rows = _read_rows(d, "kernel_stats.csv")
+    rows.sort(key=lambda r: -float(r["TotalDurationNs"]))
+    lines = ["# Kernel time, rocprofv3 --kernel-trace --stats", "", "Command (from the repository root, on one MI355X):",
+             "", "    " + cmd, "", "| kernel | calls | total ms | average us | min us | max us | share |",
+             "|---|---|---|---|---|---|---|"]
+    for r in rows:
+        lines.append("| `%s` | %s | %.3f | %.2f | %.2f | %.2f | %.1f%% |" % (
+            r["Name"].split("(")[0].replace("void ", ""), r["Calls"], float(r["TotalDurationNs"]) / 1e6,
+            float(r["AverageNs"]) / 1e3, float(r["MinNs"]) / 1e3, float(r["MaxNs"]) / 1e3, float(r["Percentage"])))
+    with open(out, "w") as f:
+        f.write("\n".join(lines) + "\n")
+    print("wrote %s (%d kernels)" % (out, len(rows)))
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -237,7 +382,22 @@ def main():
     ap.add_argument("--workload", default="mixtral-decode",
                     help="mixtral-decode (default), deepseek-decode, deepseek-prefill, "
                          "qwen-decode16, qwen-prefill")
+    ap.add_argument("--pmc-pass", action="store_true",
+                    help="only the split pass, with the counter calibration copy before its timed steps "
+                         "(run under rocprofv3 --pmc)")
+    ap.add_argument("--pmc-summary", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
+                    help="summarise two --pmc-pass runs (FETCH_SIZE, WRITE_SIZE) into --out")
+    ap.add_argument("--trace-summary", metavar="DIR", help="summarise a --kernel-trace --stats run into --out")
+    ap.add_argument("--out", default=None)
+    ap.add_argument("--cmd", nargs="*", default=[], help="the profiling command(s), recorded in the summary")
     args = ap.parse_args()
+    if args.pmc_summary:
+        pmc_summary(args.pmc_summary[0], args.pmc_summary[1], args.workload,
+                    args.out or pmc_profile_path(args.workload), *(args.cmd + ["", ""])[:2])
+        return
+    if args.trace_summary:
+        trace_summary(args.trace_summary, args.out, " ".join(args.cmd))
+        return
     if args.gpus != 1:
         print("bench.py measures one GPU: this build of the split-expert layer has no "
               "multi-GPU path; run with --gpus 1", file=sys.stderr)
@@ -267,11 +427,25 @@ def main():
     slots = rig.configure([wl["budget"](top_bytes(rig, r))], [r])
     rig.load_tops(0, tops[:int(slots[0])])
     ms.ms_sync(rig.ctx)
+    if args.pmc_pass:
+        def calibrate():
+            a = torch.empty(CALIB_BYTES, dtype=torch.uint8, device="cuda")
+            b = torch.empty_like(a)
+            b.copy_(a)
+            torch.cuda.synchronize()
+        ms_p, _, _ = run_steps(rig, hs, args.steps, args.warmup, ms.MS_FWD_PREDICT_NEXT, timeline=False, T=T,
+                               before_timed=calibrate)
+        rig.close()
+        print(json.dumps({"pmc_pass": args.workload, "ms_per_step": round(ms_p, 4), "steps": args.steps,
+                          "calib_bytes": CALIB_BYTES}), flush=True)
+        return
     ms_step, tl, st = run_steps(rig, hs, args.steps, args.warmup, ms.MS_FWD_PREDICT_NEXT, T=T)
     # the same steps without the timeline's events: the cost of instrumenting
     ms_plain, _, _ = run_steps(rig, hs, args.steps, args.warmup, ms.MS_FWD_PREDICT_NEXT, timeline=False, T=T)
     an = analyse(tl, args.steps, ms_step)
     roof = ffn_roofline(an)
+    if roof is not None:
+        roof["traffic"] = traffic_from_profile(args.workload)
     if args.timeline_out:
         with open(args.timeline_out, "w") as f:
             json.dump(dict(split=tl), f)
@@ -285,6 +459,7 @@ def main():
         "warmup": args.warmup,
         "ms_per_step": round(ms_step, 4),
         "ms_per_step_uninstrumented": round(ms_plain, 4),
+        "step_us": an["step_us"],
         "higher_is_better": False,
         "scaling": "weak",
         "vs_baseline": None,
