@@ -273,6 +273,17 @@ ms_status ms_drop_buffer(ms_ctx* ctx);
 ms_status ms_stats(ms_ctx* ctx, int32_t layer, ms_layer_stats* out);
 ms_status ms_reset_stats(ms_ctx* ctx);
 
+/* Glue between stacked MoE layers (outside the layer; the residual stream
+ * of a stack whose layers are MoE only, with a weightless RMSNorm):
+ * out[t] = x / sqrt(mean(x^2) + 1e-6) with x = h[t] + y[t] in fp32.
+ * h_dev [T][d] in the model dtype, y_dev [T][d] fp32 (an ms_forward output),
+ * out_dev [T][d] in the model dtype (bf16 rounded to nearest even); out_dev
+ * may equal h_dev.  Device pointers, 16-byte aligned; enqueued on `stream`
+ * after the context's previous work there.  MS_E_INVALID for T outside
+ * [0, max_tokens] or a NULL/misaligned pointer. */
+ms_status ms_residual_norm(ms_ctx* ctx, const void* h_dev, const float* y_dev, int32_t T, void* out_dev,
+                           void* stream);
+
 /* Timeline instrumentation.  ms_timeline_begin records an origin event on
  * `stream` and from then on brackets every kernel and copy the library
  * issues with HIP events on the stream it runs on (at most `capacity`

@@ -13,6 +13,14 @@ constexpr int kMaxTasks = 120;     // tasks passed by value in one FFN launch
 constexpr int kFfnLanesPerUnit = 8;  // lanes sharing one unit row in phase 1
 constexpr int kMaxExperts = 512;   // grouping / ranking kernels' LDS bound
 constexpr int kMaxTopK = 64;
+constexpr int kMaxModelDim = 8192;  // d_model limit of every kernel
+// Work-groups per chunk the FFN kernel supports at this width and element
+// size (16-byte loads; at most 8 column passes in the down projection).
+inline int max_ffn_splits(int d, int elem) {
+  int subs = 4;
+  while (subs > 1 && d > (64 / subs) * kFfnLanesPerUnit * (16 / elem) * 8) subs >>= 1;
+  return subs;
+}
 
 enum Dtype { kF32 = 0, kBF16 = 1 };
 
@@ -155,6 +163,12 @@ hipError_t launch_mma_down(const MmaArgs& a, hipStream_t s);
 // other streams' work through ordinary kernel-to-kernel dependencies.
 constexpr int kH2dWorkGroups = 32;
 hipError_t launch_h2d(void* dst, const void* src, uint64_t bytes, hipStream_t s);
+
+// Glue between stacked layers: out[t] = x / sqrt(mean(x^2) + eps) with
+// x = h[t] + y[t], in fp32, stored in the model dtype (bf16: round to
+// nearest even).  One work-group per token.
+hipError_t launch_residual_norm(const void* h, const float* y, void* out, int T, int d, int dtype, float eps,
+                                hipStream_t s);
 
 // y[t] = sum_k w[t][k] * sum_c part[c][pos[t*K+k]] + sum_s sum_c part_sh[s][c][t],
 // c over the partial planes (chunks * subs), in two launches: a first pass

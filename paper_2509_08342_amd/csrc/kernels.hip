@@ -753,8 +753,8 @@ hipError_t launch_logits_route(const LogitsArgs& a, const RouteArgs& ra, hipStre
 // A work-group computes UPW units (one sub-range of a 64-unit chunk c) of one
 // expert for all of the expert's tokens, NT tokens at a time:
 //   phase 1: a[t][f] = silu(h_t . G_f) * (h_t . U_f) for its units f
-//            (8 lanes per unit row, 16-byte loads, batches of kRowBatch
-//            loads per lane issued before use);
+//            (8 lanes per unit row, 16-byte loads, batches of RB loads per
+//            lane and row stream issued before use);
 //   phase 2: y[t][:] = sum_f a[t][f] * D_f over its units (each thread owns
 //            VEC columns per pass);
 //   writes y as the fp32 partial row of (token, plane c * subs + sub).
@@ -763,21 +763,32 @@ hipError_t launch_logits_route(const LogitsArgs& a, const RouteArgs& ra, hipStre
 // the units' pieces of one 64-wide k slice are adjacent; D is row-major
 // (down row f at f * d).  The same code serves resident and streamed chunks,
 // and a given chunk is always split the same way, so its partials do not
-// depend on which launch computed it.
+// depend on which launch computed it.  Loads run one batch ahead of use;
+// the batch depth RB only changes how many are in flight, not the order of
+// any sum: launches of many work-groups use RB = 4 (more work-groups per
+// CU), launches of fewer than one work-group per CU use RB = 8 (each
+// work-group alone must keep enough bytes in flight to cover the latency).
 
 #ifndef MSK_ROW_BATCH
 #define MSK_ROW_BATCH 4
 #endif
-constexpr int kRowBatch = MSK_ROW_BATCH;  // 16-byte loads per lane and row stream
+constexpr int kRowBatch = MSK_ROW_BATCH;  // RB of launches that fill the GPU
+constexpr int kRowBatchDeep = 8;    // RB of launches with fewer work-groups than CUs
+#ifndef MSK_DEEP_BELOW
+#define MSK_DEEP_BELOW 256
+#endif
+constexpr int kDeepBelowWgs = MSK_DEEP_BELOW;
 constexpr int kLpu = kFfnLanesPerUnit;
 constexpr int kKTile = 64;                // k elements per gate/up piece
 
-template <typename W, int NT, int Q, int UPW>
+template <typename W, int NT, int Q, int UPW, int RB>
 __global__ __launch_bounds__(UPW * kLpu) void ffn_chunk_kernel(FfnArgs a) {
   constexpr int VEC = Vec<W>::N;
   constexpr int THREADS = UPW * kLpu;
   constexpr int STEP = kLpu * VEC;  // k covered by the lanes of a unit per step
+  constexpr int PB = (RB < 16 / Q) ? RB : 16 / Q;  // phase-2 rows per batch (<= 2 x 16 loads in flight)
   static_assert(STEP <= kKTile && kKTile % STEP == 0, "a unit's lanes must tile a k piece");
+  static_assert(UPW % PB == 0, "phase-2 batches must tile the work-group's units");
   extern __shared__ __align__(16) unsigned char ffn_smem[];
   const int d = a.d;
   const int wg = blockIdx.x;
@@ -836,20 +847,29 @@ __global__ __launch_bounds__(UPW * kLpu) void ffn_chunk_kernel(FfnArgs a) {
 #pragma unroll
       for (int t = 0; t < NT; ++t) ag[t] = au[t] = 0.0f;
       const int n_steps = d / STEP;
-      for (int s0 = 0; s0 < n_steps; s0 += kRowBatch) {
-        uint4 gr[kRowBatch], ur[kRowBatch];
+      // software pipeline: batch s0 + RB is loaded while batch s0 is used;
+      // every load is issued (clamped to the last step), used only in range
+      uint4 gr[RB], ur[RB], gn[RB], un[RB];
+      auto load_batch = [&](int s0, uint4(&g)[RB], uint4(&uu)[RB]) {
 #pragma unroll
-        for (int u = 0; u < kRowBatch; ++u) {
-          const int sk = (s0 + u) * STEP;  // first k of the step
-          if (s0 + u < n_steps) {
-            const size_t off =
-                (static_cast<size_t>(sk / kKTile) * kChunkUnits + unit) * kKTile + (sk % kKTile) + lane_u * VEC;
-            gr[u] = ldw16(G + off);
-            ur[u] = ldw16(U + off);
-          }
+        for (int u = 0; u < RB; ++u) {
+          const int sk = min(s0 + u, n_steps - 1) * STEP;  // first k of the step
+          const size_t off =
+              (static_cast<size_t>(sk / kKTile) * kChunkUnits + unit) * kKTile + (sk % kKTile) + lane_u * VEC;
+          g[u] = ldw16(G + off);
+          uu[u] = ldw16(U + off);
         }
+      };
+      load_batch(0, gn, un);
+      for (int s0 = 0; s0 < n_steps; s0 += RB) {
 #pragma unroll
-        for (int u = 0; u < kRowBatch; ++u) {
+        for (int u = 0; u < RB; ++u) {
+          gr[u] = gn[u];
+          ur[u] = un[u];
+        }
+        load_batch(s0 + RB, gn, un);
+#pragma unroll
+        for (int u = 0; u < RB; ++u) {
           if (s0 + u < n_steps) {
             const int k = (s0 + u) * STEP + lane_u * VEC;
             float gv[VEC], uv[VEC];
@@ -892,17 +912,26 @@ __global__ __launch_bounds__(UPW * kLpu) void ffn_chunk_kernel(FfnArgs a) {
         for (int q = 0; q < Q; ++q)
 #pragma unroll
           for (int i = 0; i < VEC; ++i) y[t][q][i] = 0.0f;
-      for (int f0 = 0; f0 < UPW; f0 += kRowBatch) {
-        uint4 dr[kRowBatch][Q];
+      // software pipeline as in phase 1 (rows clamped to the work-group's last)
+      uint4 dr[PB][Q], dn[PB][Q];
+      auto load_rows = [&](int f0, uint4(&dd)[PB][Q]) {
 #pragma unroll
-        for (int u = 0; u < kRowBatch; ++u)
+        for (int u = 0; u < PB; ++u)
 #pragma unroll
           for (int q = 0; q < Q; ++q) {
-            const int col = (tid + THREADS * q) * VEC;
-            if (col < d) dr[u][q] = ldw16(D + static_cast<size_t>(f_first + f0 + u) * d + col);
+            const int col = min((tid + THREADS * q) * VEC, d - VEC);  // clamped; used only if in range
+            dd[u][q] = ldw16(D + static_cast<size_t>(f_first + min(f0 + u, UPW - 1)) * d + col);
           }
+      };
+      load_rows(0, dn);
+      for (int f0 = 0; f0 < UPW; f0 += PB) {
 #pragma unroll
-        for (int u = 0; u < kRowBatch; ++u) {
+        for (int u = 0; u < PB; ++u)
+#pragma unroll
+          for (int q = 0; q < Q; ++q) dr[u][q] = dn[u][q];
+        load_rows(f0 + PB, dn);
+#pragma unroll
+        for (int u = 0; u < PB; ++u) {
           float av[NT];
 #pragma unroll
           for (int t = 0; t < NT; ++t) av[t] = as[t * UPW + f0 + u];
@@ -945,17 +974,31 @@ __global__ __launch_bounds__(UPW * kLpu) void ffn_chunk_kernel(FfnArgs a) {
 template <typename W, int NT, int Q, int UPW>
 static hipError_t launch_ffn_one(const FfnArgs& a, hipStream_t s) {
   const size_t lds = sizeof(W) * NT * a.d + sizeof(float) * NT * UPW;
-  hipLaunchKernelGGL((ffn_chunk_kernel<W, NT, Q, UPW>), dim3(a.n_wg), dim3(UPW * kLpu), lds, s, a);
+  // deep batches (bf16 weights) only where few tokens and columns keep the
+  // accumulators small enough to leave room for the loads in flight
+  if constexpr (NT <= 2 && Q <= 4 && sizeof(W) == 2) {
+    if (a.n_wg < kDeepBelowWgs) {
+      hipLaunchKernelGGL((ffn_chunk_kernel<W, NT, Q, UPW, kRowBatchDeep>), dim3(a.n_wg), dim3(UPW * kLpu), lds, s,
+                         a);
+      return hipGetLastError();
+    }
+  }
+  hipLaunchKernelGGL((ffn_chunk_kernel<W, NT, Q, UPW, kRowBatch>), dim3(a.n_wg), dim3(UPW * kLpu), lds, s, a);
   return hipGetLastError();
 }
 
-// Only the (NT, Q) pairs whose accumulators fit (NT * Q * VEC <= 64) exist.
+// Accumulators the kernel can hold beside its pipelined loads.
+constexpr bool ffn_fits(int nt, int q, int vec) { return nt * q * vec <= (q >= 4 ? 32 : 64); }
+
+// Only the (NT, Q) pairs whose accumulators fit exist.
 template <typename W, int UPW>
 static hipError_t dispatch_ffn(const FfnArgs& a, int nt, int q, hipStream_t s) {
   constexpr int V = Vec<W>::N;
-#define MSK_FFN_CASE(NT_, Q_)                                                        \
-  if (nt == NT_ && q == Q_) {                                                        \
-    if constexpr (NT_ * Q_ * V <= 64) return launch_ffn_one<W, NT_, Q_, UPW>(a, s);  \
+  // Q_ > 1 exists only where some d <= kMaxModelDim needs it
+#define MSK_FFN_CASE(NT_, Q_)                                                                     \
+  if (nt == NT_ && q == Q_) {                                                                     \
+    if constexpr (ffn_fits(NT_, Q_, V) && (Q_ == 1 || UPW * kLpu * V * (Q_ / 2) < kMaxModelDim))  \
+      return launch_ffn_one<W, NT_, Q_, UPW>(a, s);                                               \
   }
   MSK_FFN_CASE(1, 1) MSK_FFN_CASE(2, 1) MSK_FFN_CASE(4, 1) MSK_FFN_CASE(8, 1)
   MSK_FFN_CASE(1, 2) MSK_FFN_CASE(2, 2) MSK_FFN_CASE(4, 2) MSK_FFN_CASE(8, 2)
@@ -966,13 +1009,13 @@ static hipError_t dispatch_ffn(const FfnArgs& a, int nt, int q, hipStream_t s) {
 }
 
 // Tokens per tile: the smallest of {1, 2, 4, 8} covering max_tok, limited so
-// that the LDS tile stays within 64 KiB and the accumulators NT*Q*VEC <= 64.
+// that the LDS tile stays within 64 KiB and the accumulators fit.
 static int pick_nt(int max_tok, int d, int elem, int q, int vec, int upw) {
   int nt = 1;
   while (nt < max_tok && nt < 8) nt <<= 1;
   while (nt > 1 &&
          (static_cast<size_t>(nt) * (static_cast<size_t>(d) * elem + sizeof(float) * upw) > 65536 ||
-          nt * q * vec > 64))
+          !ffn_fits(nt, q, vec)))
     nt >>= 1;
   return nt;
 }
@@ -1192,6 +1235,80 @@ hipError_t launch_mma_gateup(const MmaArgs& a, hipStream_t s) {
 hipError_t launch_mma_down(const MmaArgs& a, hipStream_t s) {
   if (a.n_wg <= 0 || a.n_tasks <= 0) return hipSuccess;
   hipLaunchKernelGGL(mma_down_kernel, dim3(a.n_wg), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+// ------------------------------------------------------ residual + RMSNorm
+//
+// 256 threads per token; each holds up to kRnPer 16-byte pieces of the row
+// (d <= 8192).  Squares are summed per thread, then over the wave with a
+// butterfly and over the four waves in order.
+
+constexpr int kRnThreads = 256;
+
+template <typename W>
+__global__ __launch_bounds__(kRnThreads) void residual_norm_kernel(const W* __restrict__ h,
+                                                                   const float* __restrict__ y,
+                                                                   W* __restrict__ out, int d, float eps) {
+  constexpr int VEC = Vec<W>::N;
+  constexpr int PER = kMaxModelDim / (kRnThreads * VEC);  // 16-byte pieces per thread at most
+  __shared__ float wsum[kRnThreads / 64];
+  const int t = blockIdx.x, tid = threadIdx.x;
+  const W* hr = h + static_cast<size_t>(t) * d;
+  const float* yr = y + static_cast<size_t>(t) * d;
+  W* orow = out + static_cast<size_t>(t) * d;
+  const int n = d / VEC;  // 16-byte pieces of the row
+  float x[PER][VEC];
+  float ss = 0.0f;
+#pragma unroll
+  for (int m = 0; m < PER; ++m) {
+    const int i = tid + m * kRnThreads;
+    if (i < n) {
+      float hv[VEC];
+      unpack(ld16(hr + static_cast<size_t>(i) * VEC), hv);
+#pragma unroll
+      for (int j = 0; j < VEC; ++j) {
+        x[m][j] = hv[j] + yr[static_cast<size_t>(i) * VEC + j];
+        ss = fmaf(x[m][j], x[m][j], ss);
+      }
+    }
+  }
+#pragma unroll
+  for (int s = 32; s >= 1; s >>= 1) ss += __shfl_xor(ss, s, 64);
+  if ((tid & 63) == 0) wsum[tid >> 6] = ss;
+  __syncthreads();
+  float tot = 0.0f;
+#pragma unroll
+  for (int w = 0; w < kRnThreads / 64; ++w) tot += wsum[w];
+  const float inv = 1.0f / sqrtf(tot / static_cast<float>(d) + eps);
+#pragma unroll
+  for (int m = 0; m < PER; ++m) {
+    const int i = tid + m * kRnThreads;
+    if (i < n) {
+      if constexpr (sizeof(W) == 2) {
+        uint32_t wv[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+          wv[j] = static_cast<uint32_t>(f2bf(x[m][2 * j] * inv)) | (static_cast<uint32_t>(f2bf(x[m][2 * j + 1] * inv)) << 16);
+        *reinterpret_cast<uint4*>(orow + static_cast<size_t>(i) * VEC) = make_uint4(wv[0], wv[1], wv[2], wv[3]);
+      } else {
+        *reinterpret_cast<float4*>(orow + static_cast<size_t>(i) * VEC) =
+            make_float4(x[m][0] * inv, x[m][1] * inv, x[m][2] * inv, x[m][3] * inv);
+      }
+    }
+  }
+}
+
+hipError_t launch_residual_norm(const void* h, const float* y, void* out, int T, int d, int dtype, float eps,
+                                hipStream_t s) {
+  if (T <= 0) return hipSuccess;
+  if (d <= 0 || d > kMaxModelDim || d % 64 != 0) return hipErrorInvalidValue;
+  if (dtype == kBF16)
+    hipLaunchKernelGGL(residual_norm_kernel<uint16_t>, dim3(T), dim3(kRnThreads), 0, s,
+                       static_cast<const uint16_t*>(h), y, static_cast<uint16_t*>(out), d, eps);
+  else
+    hipLaunchKernelGGL(residual_norm_kernel<float>, dim3(T), dim3(kRnThreads), 0, s, static_cast<const float*>(h), y,
+                       static_cast<float*>(out), d, eps);
   return hipGetLastError();
 }
 

@@ -27,7 +27,7 @@ constexpr int kUnits = msk::kChunkUnits;
 constexpr uint64_t kAlign = 256;
 constexpr uint64_t kGroupTargetBytes = 16ull << 20;  // H2D copy granularity
 constexpr int kPrefetchWindow = 2;                   // prefetch groups in flight
-constexpr int kMaxD = 8192;
+constexpr int kMaxD = msk::kMaxModelDim;
 constexpr int kReserved = 1 << 30;                   // BufSlot::use_order of a reserved slot
 
 uint64_t align_up(uint64_t x, uint64_t a) { return (x + a - 1) / a * a; }
@@ -92,13 +92,18 @@ ms_status derive_shape(const ms_model_desc* d, Shape* s, std::string* err) {
   s->group_chunks = static_cast<int>(std::max<uint64_t>(1, kGroupTargetBytes / s->chunk_bytes));
   // work-groups per chunk: enough that a decode step over the experts a
   // forward can activate gives the FFN kernel >= 768 work-groups
+  const int max_subs = msk::max_ffn_splits(d->d_model, d->dtype == MS_BF16 ? 2 : 4);
+  if (d->ffn_splits > max_subs) {
+    *err = "ffn_splits too large for this d_model and dtype";
+    return MS_E_UNSUPPORTED;
+  }
   if (d->ffn_splits > 0) {
     s->subs = d->ffn_splits;
   } else {
     const int64_t active = std::min<int64_t>(s->E, static_cast<int64_t>(s->max_T) * s->K) + s->n_sh;
     const int64_t work = active * s->n_chunks;
     s->subs = 1;
-    while (s->subs < 4 && work * s->subs < 768) s->subs *= 2;
+    while (s->subs < max_subs && work * s->subs < 768) s->subs *= 2;
   }
 
   const uint64_t TK = static_cast<uint64_t>(s->max_T) * s->K;
@@ -1618,6 +1623,23 @@ ms_status ms_forward(ms_ctx* ctx, int32_t layer, const void* h_dev, int32_t T, f
     }
   }
   for (BufSlot& b : ctx->buf) b.use_order = -1;
+  return MS_OK;
+}
+
+ms_status ms_residual_norm(ms_ctx* ctx, const void* h_dev, const float* y_dev, int32_t T, void* out_dev,
+                           void* stream) {
+  MS_CHECK_CTX(ctx);
+  const Shape& s = ctx->s;
+  if (T < 0 || T > s.max_T) return fail(ctx, MS_E_INVALID, "T outside [0, max_tokens]");
+  if (T == 0) return MS_OK;
+  if (!h_dev || !y_dev || !out_dev) return fail(ctx, MS_E_INVALID, "NULL device buffer");
+  if ((reinterpret_cast<uintptr_t>(h_dev) | reinterpret_cast<uintptr_t>(y_dev) | reinterpret_cast<uintptr_t>(out_dev)) %
+          16 != 0)
+    return fail(ctx, MS_E_INVALID, "buffers must be 16-byte aligned");
+  hipStream_t sm = static_cast<hipStream_t>(stream);
+  ms_status st = order_after_last(ctx, sm);
+  if (st != MS_OK) return st;
+  MS_HIP(msk::launch_residual_norm(h_dev, y_dev, out_dev, T, s.d, s.dtype, 1e-6f, sm));
   return MS_OK;
 }
 

@@ -82,6 +82,7 @@ def _load():
         "ms_drop_buffer": [P],
         "ms_stats": [P, I32, ctypes.POINTER(ms_layer_stats)],
         "ms_reset_stats": [P],
+        "ms_residual_norm": [P, P, P, I32, P, P],
         "ms_timeline_begin": [P, P, I32],
         "ms_timeline_end": [P, ctypes.POINTER(ms_interval), I32, ctypes.POINTER(I32)],
     }
@@ -237,6 +238,10 @@ def ms_sync(ctx):
 
 def ms_drop_buffer(ctx):
     _check(lib.ms_drop_buffer(ctx), ctx)
+
+
+def ms_residual_norm(ctx, h_dev, y_dev, T, out_dev, stream=None):
+    _check(lib.ms_residual_norm(ctx, _ptr(h_dev), _ptr(y_dev), T, _ptr(out_dev), _stream(stream)), ctx)
 
 
 def ms_stats(ctx, layer):
