@@ -93,6 +93,19 @@ def _workloads():
                              tops=lambda rig: list(np.argsort(-rig.biases[0], kind="stable")[:37])),
     }
 
+# stacked workloads: shape, total budget V_e, uniform r (or "mixed": r by layer
+# index mod 3 over {.25, .5, .75}), prefill tokens (0: none), decode batch
+def _stacks():
+    import synth
+    return {
+        "mixtral-stack": dict(shape=synth.MIXTRAL_STACK, budget=12 * GIB, r=0.5, prefill=0, T=1, n_sets=4),
+        "mixtral-stack-mixed": dict(shape=synth.MIXTRAL_STACK, budget=12 * GIB, r="mixed", prefill=0, T=1,
+                                    n_sets=4),
+        "deepseek-stack": dict(shape=synth.DEEPSEEK, budget=4 * GIB, r=0.5, prefill=512, T=1, n_sets=4),
+        "qwen-stack": dict(shape=synth.QWEN3, budget=8 * GIB, r=0.5, prefill=2048, T=16, n_sets=4),
+    }
+
+
 METRIC = "MoE-layer decode µs/layer + achieved HBM GB/s; H2D overlap % at fixed VRAM budget"
 KERNEL_KINDS = ("router", "group", "predict", "ffn_resident", "ffn_streamed", "ffn_down", "combine")
 COPY_KINDS = ("copy_miss", "copy_prefetch")
@@ -370,6 +383,80 @@ def trace_summary(d, out, cmd):
     print("wrote %s (%d kernels)" % (out, len(rows)))
 
 
+def run_stack(args):
+    """A whole stack: warm-up statistics pick each layer's cached tops, an
+    optional prefill pass, then decode steps through every layer with
+    cross-layer prediction and prefetch."""
+    import torch
+    from paper_2509_08342_amd import moesplit as ms
+    from stack import Stack, decode_inputs, stack_top_bytes
+    cfg = _stacks()[args.workload]
+    shape, T, P = cfg["shape"], cfg["T"], cfg["prefill"]
+    L = shape.n_layers
+    t_setup = time.perf_counter()
+    log("generating %s weights (%d distinct sets over %d layers)" % (shape.name, cfg["n_sets"], L))
+    st = Stack(shape, seed=0, n_sets=cfg["n_sets"], max_tokens=max(T, P), budget_total=cfg["budget"],
+               keep_f32=False)
+    r = cfg["r"]
+    rs = [(0.25, 0.5, 0.75)[l % 3] for l in range(L)] if r == "mixed" else [r] * L
+    slots = st.configure(rs, cfg["budget"])
+    n_warm, n_steps = 16, args.steps
+    xs = decode_inputs(shape, 0, n_warm + args.warmup + n_steps, T)
+    log("setup %.1f s; %d-step warm-up for the cache contents" % (time.perf_counter() - t_setup, n_warm))
+    counts = st.warmup_counts([x for x, _ in xs[:n_warm]], T)
+    st.load_most_selected(counts)
+    stream = torch.cuda.current_stream()
+    out = {"metric": "MoE-stack decode µs/layer", "unit": "us/layer", "higher_is_better": False,
+           "data": "synthetic", "dtype": "bf16", "n_gpus": 1,
+           "config": {"workload": "%s: %s, %d layers, V_e %.0f GiB, r %s, C_i %s, %s decode batch %d" % (
+               args.workload, shape.name, L, cfg["budget"] / GIB, r, sorted(set(int(c) for c in slots)),
+               ("prefill %d then" % P) if P else "", T)}}
+    if P:
+        h, _ = st.rig.hidden(P, tag=11)
+        ms.ms_reset_stats(st.ctx)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        st.step(h, P)
+        ms.ms_sync(st.ctx)
+        torch.cuda.synchronize()
+        out["prefill_ms"] = round((time.perf_counter() - t0) * 1e3, 2)
+        out["prefill_tokens_per_s"] = round(P / (time.perf_counter() - t0), 1)
+        log("prefill %d tokens: %.1f ms" % (P, out["prefill_ms"]))
+    for x, _ in xs[n_warm:n_warm + args.warmup]:
+        st.step(x, T)
+    ms.ms_sync(st.ctx)
+    torch.cuda.synchronize()
+    ms.ms_reset_stats(st.ctx)
+    step_ms = []
+    t0 = time.perf_counter()
+    for x, _ in xs[n_warm + args.warmup:]:
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        st.step(x, T)
+        e1.record(stream)
+        step_ms.append((e0, e1))
+    ms.ms_sync(st.ctx)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    per = [a.elapsed_time(b) for a, b in step_ms]
+    stats = st.stats()
+    tot = {k: sum(s[k] for s in stats) for k in stats[0]}
+    out.update({
+        "value": round(wall / n_steps / L * 1e6, 1), "steps": n_steps, "warmup": args.warmup,
+        "ms_per_step": round(wall / n_steps * 1e3, 3),
+        "step_ms": {q: round(float(np.percentile(per, p)), 3) for q, p in (("p10", 10), ("p50", 50), ("p90", 90))},
+        "tokens_per_s": round(T * n_steps / wall, 2),
+        "selected": tot["selected"], "alpha_beta_gamma": [tot["alpha"], tot["beta"], tot["gamma"]],
+        "buffer_hits": tot["buffer_hits"], "predicted_hits_per_layer_step": round(
+            tot["predicted_hits"] / max(tot["predictions"], 1), 3),
+        "h2d_bytes_per_step": {"miss": tot["bytes_miss"] // n_steps, "prefetch": tot["bytes_prefetch"] // n_steps,
+                               "prefetch_used": tot["bytes_prefetch_used"] // n_steps},
+        "h2d_gbps_over_step": round((tot["bytes_miss"] + tot["bytes_prefetch"]) / wall / 1e9, 2),
+    })
+    st.close()
+    print(json.dumps(out), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -381,7 +468,8 @@ def main():
     ap.add_argument("--timeline-out", default=None)
     ap.add_argument("--workload", default="mixtral-decode",
                     help="mixtral-decode (default), deepseek-decode, deepseek-prefill, "
-                         "qwen-decode16, qwen-prefill")
+                         "qwen-decode16, qwen-prefill; stacks: mixtral-stack, mixtral-stack-mixed, "
+                         "deepseek-stack, qwen-stack")
     ap.add_argument("--pmc-pass", action="store_true",
                     help="only the split pass, with the counter calibration copy before its timed steps "
                          "(run under rocprofv3 --pmc)")
@@ -409,6 +497,9 @@ def main():
     from workload import SplitRig, to_device, top_bytes
 
     torch.cuda.set_device(0)
+    if args.workload in _stacks():
+        run_stack(args)
+        return
     wl = _workloads()[args.workload]
     shape, T = wl["shape"], wl["T"]
     t_setup = time.perf_counter()
