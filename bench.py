@@ -476,6 +476,10 @@ def main():
     ap.add_argument("--pmc-summary", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
                     help="summarise two --pmc-pass runs (FETCH_SIZE, WRITE_SIZE) into --out")
     ap.add_argument("--trace-summary", metavar="DIR", help="summarise a --kernel-trace --stats run into --out")
+    ap.add_argument("--r", type=float, default=None,
+                    help="split ratio instead of the workload's (the cache keeps the same number of tops)")
+    ap.add_argument("--all-tops", action="store_true",
+                    help="cache the top segment of every expert (the budget grows with it)")
     ap.add_argument("--out", default=None)
     ap.add_argument("--cmd", nargs="*", default=[], help="the profiling command(s), recorded in the summary")
     args = ap.parse_args()
@@ -513,9 +517,13 @@ def main():
     setup_s = time.perf_counter() - t_setup
     log("setup done in %.1f s; timing the split layer" % setup_s)
     # the split configuration: per-layer budget, split ratio, cached tops
-    r = wl["r"]
+    r = wl["r"] if args.r is None else args.r
     tops = [int(e) for e in wl["tops"](rig)]
-    slots = rig.configure([wl["budget"](top_bytes(rig, r))], [r])
+    budget = wl["budget"](top_bytes(rig, r))
+    if args.all_tops:
+        tops = list(range(shape.n_experts))
+        budget = shape.n_experts * top_bytes(rig, r)
+    slots = rig.configure([budget], [r])
     rig.load_tops(0, tops[:int(slots[0])])
     ms.ms_sync(rig.ctx)
     if args.pmc_pass:
