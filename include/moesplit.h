@@ -110,6 +110,7 @@ typedef struct {
   uint64_t bytes_prefetch_dropped; /* prefetch bytes dropped before issue     */
   uint64_t predicted_hits;    /* selected experts among the top-K predicted    */
   uint64_t predictions;       /* forwards that had a prediction to check       */
+  uint64_t cache_inserts;     /* top segments cached by the online policy      */
 } ms_layer_stats;
 
 /* Timeline record (see ms_timeline_begin). */
@@ -272,6 +273,81 @@ ms_status ms_drop_buffer(ms_ctx* ctx);
 
 ms_status ms_stats(ms_ctx* ctx, int32_t layer, ms_layer_stats* out);
 ms_status ms_reset_stats(ms_ctx* ctx);
+
+/* ---- Cache configurator (Sec. 3.3-3.4, Eq. (4)-(11), Algorithm 1) ---- */
+
+/* Statistics of layer i gathered by ms_forward since ms_create or
+ * ms_reset_plan_stats (Sec. 3.4.2), normalised: hit[C] = H_i(C), the share of
+ * activations whose expert was among the C highest cache priorities (Eq. (4))
+ * at that forward, C = 0..N; pred[y-1] = P_i(y), the tokens per token that
+ * activated the expert the prediction ranked y-th; pred_hit[(y-1)*(N+1)+C] =
+ * PH_i(y, C), the share of tokens for which that expert was among the C
+ * highest priorities.  P and PH count the forwards that had a prediction for
+ * layer i (MS_FWD_PREDICT_NEXT of the previous layer or ms_predict); a batch
+ * of T tokens shares its prediction.  Host arrays of N+1, N and N*(N+1)
+ * doubles (any may be NULL).  tokens_out (may be NULL): [q, q_pred]. */
+ms_status ms_plan_stats(ms_ctx* ctx, int32_t layer, double* hit, double* pred, double* pred_hit,
+                        uint64_t* tokens_out);
+ms_status ms_reset_plan_stats(ms_ctx* ctx);
+
+/* Cache priority of every expert of layer i (Eq. (4)): mu * rho^(nu/omega),
+ * mu = activations so far, nu = forwards since the last activation (a batch
+ * counts as one forward).  rho, omega from ms_set_cache_policy (default
+ * 0.25, 128).  prio_out: host [N] doubles. */
+ms_status ms_lcp_priority(ms_ctx* ctx, int32_t layer, double* prio_out);
+
+/* Inputs of the configurator: model shape, profiled latencies in
+ * microseconds (Sec. 3.4.1: attention, MoE layer, head, one whole expert's
+ * load), and per-layer statistics laid out as ms_plan_stats returns them
+ * ([L] consecutive blocks). */
+typedef struct {
+  int32_t n_layers, n_experts, top_k;
+  uint64_t expert_bytes;
+  double t_att_us, t_moe_us, t_head_us, t_load_us;
+  const double* hit;       /* [L][N+1]   */
+  const double* pred;      /* [L][N]     */
+  const double* pred_hit;  /* [L][N][N+1] */
+} ms_plan_problem;
+
+/* Algorithm 1's VramAllocation over a total expert budget v_e_bytes (V_e):
+ * starting from start_budgets ([L] bytes, each > 0; NULL: V_e / L each),
+ * repeatedly move floor(zeta * V_e) bytes from the layer whose exposed
+ * loading latency grows least to the one whose latency falls most, while the
+ * summed exposed latency decreases (at most max_iter moves).  Each layer's
+ * split ratio solves the sub-problem of Eq. (11) under the window its
+ * predecessor leaves (Eq. (7)).  Outputs (host arrays of L; any but
+ * budgets_out may be NULL): budgets, split ratios theta_i, cache sizes C_i
+ * (the planner's count of experts), exposed latencies (us) and the moves
+ * taken.  Pure host arithmetic; needs no context.  MS_E_INVALID for bad
+ * sizes, zeta outside (0, 1), or a start budget <= 0. */
+ms_status ms_plan_solve(const ms_plan_problem* p, uint64_t v_e_bytes, double zeta, const uint64_t* start_budgets,
+                        int32_t max_iter, uint64_t* budgets_out, double* theta_out, int32_t* cache_out,
+                        double* exposed_us_out, int32_t* iters_out);
+
+/* Apply a plan (Algorithm 1, "update the expert cache"): ms_configure with
+ * these budgets and ratios, then per layer cache the top segments of the C_i
+ * experts of highest priority (Eq. (4); ties to the lower index).  Waits for
+ * work in flight; clears the staging buffer. */
+ms_status ms_cache_update(ms_ctx* ctx, const uint64_t* budgets, const float* r);
+
+/* Online replacement (Sec. 3.3): after a forward in which a selected expert
+ * had no cached top, cache its top segment (copied from the staging slot
+ * that holds the whole expert) in place of the cached expert the policy
+ * ranks lowest: MS_CACHE_LCP by Eq. (4), MS_CACHE_LRU by last activation,
+ * MS_CACHE_LFU by activation count, MS_CACHE_RND uniformly (seeded), each
+ * with ties to the lower index.  Missed experts are taken in descending
+ * order of the policy's rank, at most one per cache slot and forward, and an
+ * expert cached in this forward is not evicted in it.  MS_CACHE_STATIC (the
+ * default) never changes the cache on its own.  rho in (0, 1) and omega > 0
+ * parameterise Eq. (4) for the statistics and LCP. */
+typedef enum {
+  MS_CACHE_STATIC = 0,
+  MS_CACHE_LCP = 1,
+  MS_CACHE_LRU = 2,
+  MS_CACHE_LFU = 3,
+  MS_CACHE_RND = 4
+} ms_cache_policy;
+ms_status ms_set_cache_policy(ms_ctx* ctx, int32_t policy, double rho, double omega, uint64_t seed);
 
 /* Glue between stacked MoE layers (outside the layer; the residual stream
  * of a stack whose layers are MoE only, with a weightless RMSNorm):

@@ -11,6 +11,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <cmath>
 #include <cstdio>
 #include <cstring>
 #include <deque>
@@ -20,6 +21,7 @@
 
 #include "kernels.h"
 #include "moesplit.h"
+#include "planner.h"
 
 namespace {
 
@@ -273,6 +275,14 @@ struct LayerState {
   std::vector<int> pred_order;
   bool has_pred = false;
   ms_layer_stats st{};
+  // cache priority state (Eq. (4)) and the configurator's statistics
+  // (Sec. 3.4.2): activations by priority rank, by prediction rank, and the
+  // priority rank of each prediction rank
+  std::vector<double> mu, nu;        // [E]
+  std::vector<uint64_t> last_use;    // [E] forward count at the last activation (0: never)
+  uint64_t clock = 0;                // forwards of this layer
+  uint64_t q = 0, q_pred = 0;        // tokens; tokens of forwards with a prediction
+  std::vector<uint64_t> hit_hist, pred_act, pred_rank;  // [E], [E], [E][E]
 };
 
 struct TlRec {
@@ -291,6 +301,10 @@ struct ms_ctx {
   Shape s{};
   std::string err;
   bool poisoned = false;
+  // online cache replacement (Sec. 3.3) and the priority's parameters
+  int policy = MS_CACHE_STATIC;
+  double rho = 0.25, omega = 128.0;
+  uint64_t rng = 0x9e3779b97f4a7c15ull;
   int device = 0;
   unsigned char* pool = nullptr;
   uint64_t pool_bytes = 0;
@@ -585,6 +599,75 @@ ms_status enqueue_prefetch(ms_ctx* ctx, int layer, const int32_t* experts, int n
 ms_status check_layer(ms_ctx* ctx, int layer) {
   if (layer < 0 || layer >= ctx->s.L) return fail(ctx, MS_E_INVALID, "layer out of range");
   return MS_OK;
+}
+
+// ---- cache priority (Eq. (4)) and configurator statistics (Sec. 3.4.2)
+
+double lcp_priority(const ms_ctx* ctx, const LayerState& L, int e) {
+  return L.mu[e] * std::pow(ctx->rho, L.nu[e] / ctx->omega);
+}
+
+// Experts in descending order of `key`, ties to the lower index.
+std::vector<int> order_by(const std::vector<double>& key) {
+  std::vector<int> o(key.size());
+  for (size_t i = 0; i < o.size(); ++i) o[i] = static_cast<int>(i);
+  std::stable_sort(o.begin(), o.end(), [&](int a, int b) { return key[a] > key[b]; });
+  return o;
+}
+
+std::vector<int> priority_order(const ms_ctx* ctx, const LayerState& L) {
+  std::vector<double> p(ctx->s.E);
+  for (int e = 0; e < ctx->s.E; ++e) p[e] = lcp_priority(ctx, L, e);
+  return order_by(p);
+}
+
+// One forward's routing (tokens per expert from the grouping offsets) into
+// the statistics, ranked by the priorities before this forward, then the
+// priority state.  A batch is one step of the activation interval.
+void update_plan_stats(ms_ctx* ctx, LayerState& L, const std::vector<int32_t>& offs, int T) {
+  const int E = ctx->s.E;
+  const std::vector<int> order = priority_order(ctx, L);
+  std::vector<int> rank(E);
+  for (int r = 0; r < E; ++r) rank[order[r]] = r;
+  for (int e = 0; e < E; ++e) L.hit_hist[rank[e]] += static_cast<uint64_t>(offs[e + 1] - offs[e]);
+  if (L.has_pred && static_cast<int>(L.pred_order.size()) == E) {
+    for (int y = 0; y < E; ++y) {
+      const int e = L.pred_order[y];
+      L.pred_act[y] += static_cast<uint64_t>(offs[e + 1] - offs[e]);
+      L.pred_rank[static_cast<size_t>(y) * E + rank[e]] += static_cast<uint64_t>(T);
+    }
+    L.q_pred += static_cast<uint64_t>(T);
+  }
+  L.q += static_cast<uint64_t>(T);
+  L.clock += 1;
+  for (int e = 0; e < E; ++e) {
+    const int n = offs[e + 1] - offs[e];
+    L.mu[e] += n;
+    L.nu[e] = n > 0 ? 0.0 : L.nu[e] + 1.0;
+    if (n > 0) L.last_use[e] = L.clock;
+  }
+}
+
+uint64_t next_random(ms_ctx* ctx) {  // splitmix64
+  uint64_t z = (ctx->rng += 0x9e3779b97f4a7c15ull);
+  z = (z ^ (z >> 30)) * 0xbf58476d1ce4e5b9ull;
+  z = (z ^ (z >> 27)) * 0x94d049bb133111ebull;
+  return z ^ (z >> 31);
+}
+
+// The replacement policy's ranking key of each expert (larger = keep).
+std::vector<double> policy_key(ms_ctx* ctx, const LayerState& L) {
+  const int E = ctx->s.E;
+  std::vector<double> k(E);
+  for (int e = 0; e < E; ++e) {
+    switch (ctx->policy) {
+      case MS_CACHE_LCP: k[e] = lcp_priority(ctx, L, e); break;
+      case MS_CACHE_LRU: k[e] = static_cast<double>(L.last_use[e]); break;
+      case MS_CACHE_LFU: k[e] = L.mu[e]; break;
+      default: k[e] = static_cast<double>(next_random(ctx) >> 11); break;
+    }
+  }
+  return k;
 }
 
 void set_route_workspace(ms_ctx* ctx, msk::RouteArgs* r) {
@@ -885,6 +968,12 @@ ms_status ms_create(const ms_model_desc* desc, void* dev_pool, uint64_t pool_byt
     L.blob_of.assign(s.E, -1);
     L.shared_set.assign(s.n_sh, false);
     L.slot_of.assign(s.E, -1);
+    L.mu.assign(s.E, 0.0);
+    L.nu.assign(s.E, 0.0);
+    L.last_use.assign(s.E, 0);
+    L.hit_hist.assign(s.E, 0);
+    L.pred_act.assign(s.E, 0);
+    L.pred_rank.assign(static_cast<size_t>(s.E) * s.E, 0);
     if ((e = hipEventCreateWithFlags(&L.last_fwd, hipEventDisableTiming)) != hipSuccess)
       return cleanup_fail(e, "hipEventCreate(layer)");
   }
@@ -1438,7 +1527,9 @@ ms_status ms_forward(ms_ctx* ctx, int32_t layer, const void* h_dev, int32_t T, f
     ctx->tl[res_tl[bi]].bytes = bytes;
   }
 
-  // 4. statistics of this routing (Sec. 3.4.1: alpha / beta / gamma)
+  // 4. statistics of this routing (Sec. 3.4.1: alpha / beta / gamma; the
+  //    configurator's H, P, PH and the cache priorities, Sec. 3.4.2)
+  update_plan_stats(ctx, L, offs, T);
   L.st.forwards += 1;
   L.st.tokens += T;
   L.st.selected += TK;
@@ -1604,6 +1695,51 @@ ms_status ms_forward(ms_ctx* ctx, int32_t layer, const void* h_dev, int32_t T, f
   ti = tl_begin(ctx, sm, MS_IV_COMBINE, layer, 0);
   MS_HIP(msk::launch_combine(ca, sm));
   tl_end(ctx, ti, sm);
+
+  // 6b. online replacement (Sec. 3.3): experts with no cached top that are
+  //     now whole in a staging slot take the place of the lowest-ranked
+  //     cached experts; the copies follow this forward's reads on `sm`
+  if (ctx->policy != MS_CACHE_STATIC && L.slots > 0 && L.top_chunks > 0 && L.top_chunks <= s.n_chunks) {
+    const std::vector<double> key = policy_key(ctx, L);
+    std::vector<int> missed;
+    for (int e = 0; e < s.E; ++e) {
+      if (offs[e + 1] == offs[e] || L.slot_of[e] >= 0) continue;
+      const int si = find_slot(ctx, layer, e);
+      if (si >= 0 && ctx->buf[si].first_chunk == 0) missed.push_back(e);
+    }
+    std::stable_sort(missed.begin(), missed.end(), [&](int a, int b) { return key[a] > key[b]; });
+    std::vector<char> fresh(s.E, 0);
+    int inserted = 0;
+    for (const int e : missed) {
+      if (inserted >= L.slots) break;
+      int slot = -1;
+      for (int i = 0; i < L.slots && slot < 0; ++i)
+        if (L.slot_owner[i] < 0) slot = i;
+      if (slot < 0) {  // evict the lowest-ranked cached expert not cached just now
+        int victim = -1;
+        for (int i = 0; i < L.slots; ++i) {
+          const int v = L.slot_owner[i];
+          if (fresh[v]) continue;
+          if (victim < 0 || key[v] < key[victim] || (key[v] == key[victim] && v < victim)) victim = v;
+        }
+        if (victim < 0) break;
+        slot = L.slot_of[victim];
+        L.slot_of[victim] = -1;
+        L.slot_owner[slot] = -1;
+      }
+      BufSlot& b = ctx->buf[find_slot(ctx, layer, e)];
+      const int cti = tl_begin(ctx, sm, MS_IV_COPY_TOP, layer, L.top_bytes);
+      MS_HIP(msk::launch_h2d(L.cache_base + L.top_bytes * slot, b.base, L.top_bytes, sm));
+      tl_end(ctx, cti, sm);
+      MS_HIP(hipEventRecord(b.last_read, sm));
+      b.has_last_read = true;
+      L.slot_of[e] = slot;
+      L.slot_owner[slot] = e;
+      fresh[e] = 1;
+      ++inserted;
+      L.st.cache_inserts += 1;
+    }
+  }
   MS_HIP(hipEventRecord(L.last_fwd, sm));
   L.has_last_fwd = true;
   MS_HIP(hipEventRecord(ctx->ev_last, sm));
@@ -1655,6 +1791,120 @@ ms_status ms_stats(ms_ctx* ctx, int32_t layer, ms_layer_stats* out) {
 ms_status ms_reset_stats(ms_ctx* ctx) {
   MS_CHECK_CTX(ctx);
   for (LayerState& L : ctx->layers) L.st = ms_layer_stats{};
+  return MS_OK;
+}
+
+ms_status ms_plan_stats(ms_ctx* ctx, int32_t layer, double* hit, double* pred, double* pred_hit,
+                        uint64_t* tokens_out) {
+  MS_CHECK_CTX(ctx);
+  ms_status st = check_layer(ctx, layer);
+  if (st != MS_OK) return st;
+  const LayerState& L = ctx->layers[layer];
+  const int E = ctx->s.E;
+  const uint64_t tot = L.q * static_cast<uint64_t>(ctx->s.K);
+  if (hit) {
+    uint64_t run = 0;
+    hit[0] = 0.0;
+    for (int c = 0; c < E; ++c) {
+      run += L.hit_hist[c];
+      hit[c + 1] = tot ? static_cast<double>(run) / static_cast<double>(tot) : 0.0;
+    }
+  }
+  if (pred)
+    for (int y = 0; y < E; ++y)
+      pred[y] = L.q_pred ? static_cast<double>(L.pred_act[y]) / static_cast<double>(L.q_pred) : 0.0;
+  if (pred_hit) {
+    for (int y = 0; y < E; ++y) {
+      double* row = pred_hit + static_cast<size_t>(y) * (E + 1);
+      uint64_t run = 0;
+      row[0] = 0.0;
+      for (int c = 0; c < E; ++c) {
+        run += L.pred_rank[static_cast<size_t>(y) * E + c];
+        row[c + 1] = L.q_pred ? static_cast<double>(run) / static_cast<double>(L.q_pred) : 0.0;
+      }
+    }
+  }
+  if (tokens_out) {
+    tokens_out[0] = L.q;
+    tokens_out[1] = L.q_pred;
+  }
+  return MS_OK;
+}
+
+ms_status ms_reset_plan_stats(ms_ctx* ctx) {
+  MS_CHECK_CTX(ctx);
+  for (LayerState& L : ctx->layers) {
+    std::fill(L.mu.begin(), L.mu.end(), 0.0);
+    std::fill(L.nu.begin(), L.nu.end(), 0.0);
+    std::fill(L.last_use.begin(), L.last_use.end(), 0);
+    std::fill(L.hit_hist.begin(), L.hit_hist.end(), 0);
+    std::fill(L.pred_act.begin(), L.pred_act.end(), 0);
+    std::fill(L.pred_rank.begin(), L.pred_rank.end(), 0);
+    L.clock = L.q = L.q_pred = 0;
+  }
+  return MS_OK;
+}
+
+ms_status ms_lcp_priority(ms_ctx* ctx, int32_t layer, double* prio_out) {
+  MS_CHECK_CTX(ctx);
+  ms_status st = check_layer(ctx, layer);
+  if (st != MS_OK) return st;
+  if (!prio_out) return fail(ctx, MS_E_INVALID, "prio_out is NULL");
+  for (int e = 0; e < ctx->s.E; ++e) prio_out[e] = lcp_priority(ctx, ctx->layers[layer], e);
+  return MS_OK;
+}
+
+ms_status ms_plan_solve(const ms_plan_problem* p, uint64_t v_e_bytes, double zeta, const uint64_t* start_budgets,
+                        int32_t max_iter, uint64_t* budgets_out, double* theta_out, int32_t* cache_out,
+                        double* exposed_us_out, int32_t* iters_out) {
+  if (!p || !budgets_out || !p->hit || !p->pred || !p->pred_hit) return MS_E_INVALID;
+  if (p->n_layers <= 0 || p->n_experts <= 0 || p->top_k <= 0 || p->top_k > p->n_experts || p->expert_bytes == 0 ||
+      !(zeta > 0.0 && zeta < 1.0) || max_iter < 0 || v_e_bytes >= (1ull << 53) ||
+      !(p->t_load_us >= 0.0) || !(p->t_moe_us >= 0.0) || !(p->t_att_us >= 0.0) || !(p->t_head_us >= 0.0))
+    return MS_E_INVALID;
+  msp::Problem pr{p->n_layers, p->n_experts, p->top_k, static_cast<double>(p->expert_bytes), p->t_att_us,
+                  p->t_moe_us, p->t_head_us, p->t_load_us, p->hit, p->pred, p->pred_hit};
+  std::vector<int64_t> V(p->n_layers);
+  for (int i = 0; i < p->n_layers; ++i) {
+    V[i] = start_budgets ? static_cast<int64_t>(start_budgets[i]) : static_cast<int64_t>(v_e_bytes / p->n_layers);
+    if (V[i] <= 0) return MS_E_INVALID;
+  }
+  msp::Split out;
+  const int it = msp::vram_allocation(pr, v_e_bytes, zeta, V, max_iter, &out);
+  for (int i = 0; i < p->n_layers; ++i) {
+    budgets_out[i] = static_cast<uint64_t>(V[i]);
+    if (theta_out) theta_out[i] = out.theta[i];
+    if (cache_out) cache_out[i] = out.C[i];
+    if (exposed_us_out) exposed_us_out[i] = out.exposed[i];
+  }
+  if (iters_out) *iters_out = it;
+  return MS_OK;
+}
+
+ms_status ms_cache_update(ms_ctx* ctx, const uint64_t* budgets, const float* r) {
+  MS_CHECK_CTX(ctx);
+  std::vector<int32_t> slots(ctx->s.L);
+  ms_status st = ms_configure(ctx, budgets, r, slots.data());
+  if (st != MS_OK) return st;
+  for (int l = 0; l < ctx->s.L; ++l) {
+    const std::vector<int> order = priority_order(ctx, ctx->layers[l]);
+    for (int c = 0; c < slots[l]; ++c) {
+      if (ctx->layers[l].blob_of[order[c]] < 0) continue;
+      st = ms_load_top(ctx, l, order[c]);
+      if (st != MS_OK) return st;
+    }
+  }
+  return MS_OK;
+}
+
+ms_status ms_set_cache_policy(ms_ctx* ctx, int32_t policy, double rho, double omega, uint64_t seed) {
+  MS_CHECK_CTX(ctx);
+  if (policy < MS_CACHE_STATIC || policy > MS_CACHE_RND) return fail(ctx, MS_E_INVALID, "unknown cache policy");
+  if (!(rho > 0.0 && rho < 1.0) || !(omega > 0.0)) return fail(ctx, MS_E_INVALID, "rho must be in (0, 1), omega > 0");
+  ctx->policy = policy;
+  ctx->rho = rho;
+  ctx->omega = omega;
+  ctx->rng = seed ^ 0x9e3779b97f4a7c15ull;
   return MS_OK;
 }
 

@@ -44,10 +44,20 @@ class ms_layer_stats(ctypes.Structure):
     _fields_ = [(n, ctypes.c_uint64) for n in (
         "forwards", "tokens", "selected", "experts_active", "alpha", "beta", "gamma",
         "buffer_hits", "bytes_miss", "bytes_prefetch", "bytes_prefetch_used",
-        "bytes_prefetch_dropped", "predicted_hits", "predictions")]
+        "bytes_prefetch_dropped", "predicted_hits", "predictions", "cache_inserts")]
 
     def as_dict(self):
         return {n: int(getattr(self, n)) for n, _ in self._fields_}
+
+
+class ms_plan_problem(ctypes.Structure):
+    _fields_ = [("n_layers", ctypes.c_int32), ("n_experts", ctypes.c_int32), ("top_k", ctypes.c_int32),
+                ("expert_bytes", ctypes.c_uint64), ("t_att_us", ctypes.c_double), ("t_moe_us", ctypes.c_double),
+                ("t_head_us", ctypes.c_double), ("t_load_us", ctypes.c_double),
+                ("hit", ctypes.c_void_p), ("pred", ctypes.c_void_p), ("pred_hit", ctypes.c_void_p)]
+
+
+MS_CACHE_STATIC, MS_CACHE_LCP, MS_CACHE_LRU, MS_CACHE_LFU, MS_CACHE_RND = range(5)
 
 
 class ms_interval(ctypes.Structure):
@@ -83,6 +93,12 @@ def _load():
         "ms_stats": [P, I32, ctypes.POINTER(ms_layer_stats)],
         "ms_reset_stats": [P],
         "ms_residual_norm": [P, P, P, I32, P, P],
+        "ms_plan_stats": [P, I32, P, P, P, P],
+        "ms_reset_plan_stats": [P],
+        "ms_lcp_priority": [P, I32, P],
+        "ms_plan_solve": [ctypes.POINTER(ms_plan_problem), U64, ctypes.c_double, P, I32, P, P, P, P, P],
+        "ms_cache_update": [P, P, P],
+        "ms_set_cache_policy": [P, I32, ctypes.c_double, ctypes.c_double, U64],
         "ms_timeline_begin": [P, P, I32],
         "ms_timeline_end": [P, ctypes.POINTER(ms_interval), I32, ctypes.POINTER(I32)],
     }
@@ -242,6 +258,59 @@ def ms_drop_buffer(ctx):
 
 def ms_residual_norm(ctx, h_dev, y_dev, T, out_dev, stream=None):
     _check(lib.ms_residual_norm(ctx, _ptr(h_dev), _ptr(y_dev), T, _ptr(out_dev), _stream(stream)), ctx)
+
+
+def ms_plan_stats(ctx, layer, n_experts):
+    """(hit [N+1], pred [N], pred_hit [N][N+1], (q, q_pred)) of one layer."""
+    N = n_experts
+    hit = np.zeros(N + 1)
+    pred = np.zeros(N)
+    ph = np.zeros((N, N + 1))
+    tok = np.zeros(2, np.uint64)
+    _check(lib.ms_plan_stats(ctx, layer, _ptr(hit), _ptr(pred), _ptr(ph), _ptr(tok)), ctx)
+    return hit, pred, ph, (int(tok[0]), int(tok[1]))
+
+
+def ms_reset_plan_stats(ctx):
+    _check(lib.ms_reset_plan_stats(ctx), ctx)
+
+
+def ms_lcp_priority(ctx, layer, n_experts):
+    out = np.zeros(n_experts)
+    _check(lib.ms_lcp_priority(ctx, layer, _ptr(out)), ctx)
+    return out
+
+
+def ms_plan_solve(n_layers, n_experts, top_k, expert_bytes, t_att_us, t_moe_us, t_head_us, t_load_us,
+                  hit, pred, pred_hit, v_e_bytes, zeta=0.01, start_budgets=None, max_iter=100000):
+    """Algorithm 1 over per-layer statistics (arrays [L][N+1], [L][N],
+    [L][N][N+1]); returns dict(budgets, theta, cache, exposed_us, iters)."""
+    L, N = n_layers, n_experts
+    hit = np.ascontiguousarray(hit, np.float64).reshape(L, N + 1)
+    pred = np.ascontiguousarray(pred, np.float64).reshape(L, N)
+    pred_hit = np.ascontiguousarray(pred_hit, np.float64).reshape(L, N, N + 1)
+    prob = ms_plan_problem(L, N, top_k, int(expert_bytes), float(t_att_us), float(t_moe_us), float(t_head_us),
+                           float(t_load_us), hit.ctypes.data, pred.ctypes.data, pred_hit.ctypes.data)
+    start = None if start_budgets is None else np.ascontiguousarray(start_budgets, np.uint64)
+    budgets = np.zeros(L, np.uint64)
+    theta = np.zeros(L)
+    cache = np.zeros(L, np.int32)
+    exposed = np.zeros(L)
+    iters = ctypes.c_int32()
+    _check(lib.ms_plan_solve(ctypes.byref(prob), int(v_e_bytes), float(zeta), _ptr(start), int(max_iter),
+                             _ptr(budgets), _ptr(theta), _ptr(cache), _ptr(exposed), ctypes.byref(iters)),
+           what="ms_plan_solve")
+    return dict(budgets=budgets, theta=theta, cache=cache, exposed_us=exposed, iters=iters.value)
+
+
+def ms_cache_update(ctx, budgets, r):
+    b = np.ascontiguousarray(budgets, np.uint64)
+    rr = np.ascontiguousarray(r, np.float32)
+    _check(lib.ms_cache_update(ctx, _ptr(b), _ptr(rr)), ctx)
+
+
+def ms_set_cache_policy(ctx, policy, rho=0.25, omega=128.0, seed=0):
+    _check(lib.ms_set_cache_policy(ctx, int(policy), float(rho), float(omega), int(seed)), ctx)
 
 
 def ms_stats(ctx, layer):
