@@ -98,11 +98,16 @@ def _workloads():
 def _stacks():
     import synth
     return {
-        "mixtral-stack": dict(shape=synth.MIXTRAL_STACK, budget=12 * GIB, r=0.5, prefill=0, T=1, n_sets=4),
+        # t_moe_us: the layer with every expert resident at the decode batch
+        # (measured on this GPU), the configurator's T_comp^moe
+        "mixtral-stack": dict(shape=synth.MIXTRAL_STACK, budget=12 * GIB, r=0.5, prefill=0, T=1, n_sets=4,
+                              t_moe_us=208.0),
         "mixtral-stack-mixed": dict(shape=synth.MIXTRAL_STACK, budget=12 * GIB, r="mixed", prefill=0, T=1,
-                                    n_sets=4),
-        "deepseek-stack": dict(shape=synth.DEEPSEEK, budget=4 * GIB, r=0.5, prefill=512, T=1, n_sets=4),
-        "qwen-stack": dict(shape=synth.QWEN3, budget=8 * GIB, r=0.5, prefill=2048, T=16, n_sets=4),
+                                    n_sets=4, t_moe_us=208.0),
+        "deepseek-stack": dict(shape=synth.DEEPSEEK, budget=4 * GIB, r=0.5, prefill=512, T=1, n_sets=4,
+                               t_moe_us=117.0),
+        "qwen-stack": dict(shape=synth.QWEN3, budget=8 * GIB, r=0.5, prefill=2048, T=16, n_sets=4,
+                           t_moe_us=305.0),
     }
 
 
@@ -403,14 +408,42 @@ def run_stack(args):
     n_warm, n_steps = 16, args.steps
     xs = decode_inputs(shape, 0, n_warm + args.warmup + n_steps, T)
     log("setup %.1f s; %d-step warm-up for the cache contents" % (time.perf_counter() - t_setup, n_warm))
+    ms.ms_reset_plan_stats(st.ctx)
     counts = st.warmup_counts([x for x, _ in xs[:n_warm]], T)
     st.load_most_selected(counts)
+    plan = None
+    if args.configure:
+        # Algorithm 1 on the warm-up statistics, then its cache update
+        E = shape.n_experts
+        hs_, ps_, phs_ = [], [], []
+        for l in range(L):
+            h_, p_, ph_, _ = ms.ms_plan_stats(st.ctx, l, E)
+            hs_.append(h_)
+            ps_.append(p_)
+            phs_.append(ph_)
+        t_load = shape.expert_bytes / 55e3   # us per whole expert at the kernel copy's 55 GB/s
+        plan = ms.ms_plan_solve(L, E, shape.top_k, shape.expert_bytes, 0.0, cfg["t_moe_us"], 0.0, t_load,
+                                np.array(hs_), np.array(ps_), np.array(phs_), cfg["budget"], args.zeta)
+        ms.ms_cache_update(st.ctx, plan["budgets"], plan["theta"].astype(np.float32))
+        slots = [int(sum(ms.ms_residency(st.ctx, l, E) > 0)) for l in range(L)]
+        log("configurator: %d moves, theta %.3f..%.3f, C %d..%d" % (
+            plan["iters"], plan["theta"].min(), plan["theta"].max(), min(slots), max(slots)))
+    if args.policy != "static":
+        ms.ms_set_cache_policy(st.ctx, {"lcp": ms.MS_CACHE_LCP, "lru": ms.MS_CACHE_LRU, "lfu": ms.MS_CACHE_LFU,
+                                        "rnd": ms.MS_CACHE_RND}[args.policy])
     stream = torch.cuda.current_stream()
     out = {"metric": "MoE-stack decode µs/layer", "unit": "us/layer", "higher_is_better": False,
            "data": "synthetic", "dtype": "bf16", "n_gpus": 1,
-           "config": {"workload": "%s: %s, %d layers, V_e %.0f GiB, r %s, C_i %s, %s decode batch %d" % (
-               args.workload, shape.name, L, cfg["budget"] / GIB, r, sorted(set(int(c) for c in slots)),
-               ("prefill %d then" % P) if P else "", T)}}
+           "config": {"workload": "%s: %s, %d layers, V_e %.0f GiB, r %s, C_i %s, %s decode batch %d, "
+                                  "cache policy %s" % (
+               args.workload, shape.name, L, cfg["budget"] / GIB,
+               "from the configurator" if plan is not None else r, sorted(set(int(c) for c in slots)),
+               ("prefill %d then" % P) if P else "", T, args.policy)}}
+    if plan is not None:
+        out["plan"] = {"moves": plan["iters"], "theta": [round(float(t), 4) for t in plan["theta"]],
+                       "cache": [int(c) for c in plan["cache"]],
+                       "budget_mb": [round(int(b) / 1e6, 1) for b in plan["budgets"]],
+                       "exposed_us_model": round(float(plan["exposed_us"].sum()), 1)}
     if P:
         h, _ = st.rig.hidden(P, tag=11)
         ms.ms_reset_stats(st.ctx)
@@ -447,6 +480,8 @@ def run_stack(args):
         "step_ms": {q: round(float(np.percentile(per, p)), 3) for q, p in (("p10", 10), ("p50", 50), ("p90", 90))},
         "tokens_per_s": round(T * n_steps / wall, 2),
         "selected": tot["selected"], "alpha_beta_gamma": [tot["alpha"], tot["beta"], tot["gamma"]],
+        "hit_rate": round((tot["alpha"] + tot["beta"]) / max(tot["experts_active"], 1), 4),
+        "cache_inserts": tot["cache_inserts"],
         "buffer_hits": tot["buffer_hits"], "predicted_hits_per_layer_step": round(
             tot["predicted_hits"] / max(tot["predictions"], 1), 3),
         "h2d_bytes_per_step": {"miss": tot["bytes_miss"] // n_steps, "prefetch": tot["bytes_prefetch"] // n_steps,
@@ -480,6 +515,11 @@ def main():
                     help="split ratio instead of the workload's (the cache keeps the same number of tops)")
     ap.add_argument("--all-tops", action="store_true",
                     help="cache the top segment of every expert (the budget grows with it)")
+    ap.add_argument("--policy", default="static", choices=["static", "lcp", "lru", "lfu", "rnd"],
+                    help="stacks: online cache replacement on misses")
+    ap.add_argument("--configure", action="store_true",
+                    help="stacks: per-layer budgets and split ratios from the cache configurator")
+    ap.add_argument("--zeta", type=float, default=0.01)
     ap.add_argument("--out", default=None)
     ap.add_argument("--cmd", nargs="*", default=[], help="the profiling command(s), recorded in the summary")
     args = ap.parse_args()

@@ -163,6 +163,10 @@ hipError_t launch_mma_down(const MmaArgs& a, hipStream_t s);
 // other streams' work through ordinary kernel-to-kernel dependencies.
 constexpr int kH2dWorkGroups = 32;
 hipError_t launch_h2d(void* dst, const void* src, uint64_t bytes, hipStream_t s);
+// The same kernel for a device-to-device copy, over enough work-groups to
+// run at HBM rate.
+constexpr int kD2dWorkGroups = 1024;
+hipError_t launch_d2d(void* dst, const void* src, uint64_t bytes, hipStream_t s);
 
 // Glue between stacked layers: out[t] = x / sqrt(mean(x^2) + eps) with
 // x = h[t] + y[t], in fp32, stored in the model dtype (bf16: round to

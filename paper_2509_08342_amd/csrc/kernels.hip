@@ -1339,16 +1339,24 @@ __global__ __launch_bounds__(256) void h2d_kernel(uint4* __restrict__ dst, const
   }
 }
 
-hipError_t launch_h2d(void* dst, const void* src, uint64_t bytes, hipStream_t s) {
+static hipError_t launch_copy(void* dst, const void* src, uint64_t bytes, int max_wgs, hipStream_t s) {
   if (bytes == 0) return hipSuccess;
   if ((bytes % 16) != 0 || (reinterpret_cast<uintptr_t>(dst) % 16) != 0 || (reinterpret_cast<uintptr_t>(src) % 16) != 0)
     return hipErrorInvalidValue;
   const uint64_t n = bytes / 16;
   const uint64_t per_wg = 256ull * kH2dUnroll;
-  const int wgs = static_cast<int>(std::min<uint64_t>(kH2dWorkGroups, (n + per_wg - 1) / per_wg));
+  const int wgs = static_cast<int>(std::min<uint64_t>(max_wgs, (n + per_wg - 1) / per_wg));
   hipLaunchKernelGGL(h2d_kernel, dim3(wgs), dim3(256), 0, s, static_cast<uint4*>(dst),
                      static_cast<const uint4*>(src), n);
   return hipGetLastError();
+}
+
+hipError_t launch_h2d(void* dst, const void* src, uint64_t bytes, hipStream_t s) {
+  return launch_copy(dst, src, bytes, kH2dWorkGroups, s);
+}
+
+hipError_t launch_d2d(void* dst, const void* src, uint64_t bytes, hipStream_t s) {
+  return launch_copy(dst, src, bytes, kD2dWorkGroups, s);
 }
 
 // ------------------------------------------------------------------ combine

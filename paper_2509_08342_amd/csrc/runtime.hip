@@ -1729,7 +1729,7 @@ ms_status ms_forward(ms_ctx* ctx, int32_t layer, const void* h_dev, int32_t T, f
       }
       BufSlot& b = ctx->buf[find_slot(ctx, layer, e)];
       const int cti = tl_begin(ctx, sm, MS_IV_COPY_TOP, layer, L.top_bytes);
-      MS_HIP(msk::launch_h2d(L.cache_base + L.top_bytes * slot, b.base, L.top_bytes, sm));
+      MS_HIP(msk::launch_d2d(L.cache_base + L.top_bytes * slot, b.base, L.top_bytes, sm));
       tl_end(ctx, cti, sm);
       MS_HIP(hipEventRecord(b.last_read, sm));
       b.has_last_read = true;
