@@ -31,8 +31,8 @@ struct LogitsArgs {
   const void* h;          // [T][d] model dtype
   int T, d, E;
   int dtype;
-  const void* wr;         // [d][E] model dtype
-  const void* wt;         // the same router transposed, [E][d] (many-token path)
+  const void* wr;         // [d][E] model dtype (NULL: this router is absent)
+  const void* wt;         // the same router transposed, [E][d] (read by the kernels)
   const float* bias;      // [E] or NULL
   float* logits;          // [T][E]
   const void* wr2;        // second router or NULL
@@ -45,7 +45,8 @@ struct LogitsArgs {
 // tiles of 8 tokens x 16 experts per wave, selection and per-block expert
 // counts for blocks of route_block_tokens(K) tokens, one work-group for the
 // scans over blocks (and the prediction ranking), then the scatter of the
-// grouping.  Fewer tokens take one work-group for everything after the
+// grouping.  Fewer tokens: one wave per logit, then one work-group for
+// everything after the logits -- a single launch when there are at most 32
 // logits.
 constexpr int kManyTokens = 64;
 inline int route_block_tokens(int K) { return K <= 16 ? 16 : 4; }

@@ -449,100 +449,74 @@ __global__ __launch_bounds__(256) void scatter_many_kernel(RouteArgs a, int TB) 
 // that pairs lane l with lane l+s for s = 32, 16, ..., 1 (lane 0 ends with
 // the result); a bias is added once afterwards.
 //
-// Few tokens: work-group = 4 waves = 4 tokens x one block of 8 experts of
-// one router.  The block's weight columns are staged in LDS tile by tile
-// (all 256 threads load), then each wave runs its token's fma chains from
-// LDS.
+// Few tokens (T < kManyTokens): one wave per (router, token, expert) logit,
+// lane l running residue l's fma chain from h and the transposed router
+// (coalesced 128-byte rows), kWaveSteps steps of loads in flight per batch,
+// then the halving tree -- the order above with no LDS staging, so a logit
+// costs about one memory round trip per STEPS * 64 elements of d.
+// Logit o of the launch: router o / (T E), token and expert from the rest.
+constexpr int kWaveSteps = 64;
 
-constexpr int kLgWaves = 4;
-constexpr int kLgBlock = 8;           // experts per work-group
-constexpr int kLgTileBytes = 32768;   // LDS tile of router rows
+template <typename W, int STEPS>
+__device__ __forceinline__ float wave_logit(const LogitsArgs& a, int o, int lane) {
+  const int per = a.T * a.E;
+  const int mat = o / per, te = o - mat * per;
+  const int t = te / a.E, e = te - t * a.E;
+  const W* hrow = static_cast<const W*>(a.h) + static_cast<size_t>(t) * a.d + lane;
+  const W* wrow = static_cast<const W*>(mat == 0 ? a.wt : a.wt2) + static_cast<size_t>(e) * a.d + lane;
+  const float* bias = mat == 0 ? a.bias : a.bias2;
+  const int steps = a.d / 64;
+  float acc = 0.0f;
+  for (int s0 = 0; s0 < steps; s0 += STEPS) {
+    float hv[STEPS], wv[STEPS];
+#pragma unroll
+    for (int u = 0; u < STEPS; ++u) {
+      const int su = min(s0 + u, steps - 1);  // clamped: every load in bounds, used only in range
+      hv[u] = to_f32(hrow[static_cast<size_t>(su) * 64]);
+      wv[u] = to_f32(wrow[static_cast<size_t>(su) * 64]);
+    }
+#pragma unroll
+    for (int u = 0; u < STEPS; ++u)
+      if (s0 + u < steps) acc = fmaf(hv[u], wv[u], acc);
+  }
+#pragma unroll
+  for (int s = 32; s >= 1; s >>= 1) acc = acc + __shfl_down(acc, s, 64);
+  if (bias != nullptr) acc = acc + bias[e];
+  return acc;  // valid in lane 0
+}
 
 template <typename W>
-__global__ __launch_bounds__(64 * kLgWaves) void logits_kernel(LogitsArgs a) {
-  __shared__ __align__(16) W tile[kLgTileBytes / sizeof(W)];
-  constexpr int RT = kLgTileBytes / (kLgBlock * sizeof(W));  // rows per tile (multiple of 64)
-  constexpr int NV = static_cast<int>(kLgBlock * sizeof(W)) / 16;  // 16-byte pieces per tile row
-  constexpr int RB = RT / (64 * kLgWaves);                           // tile rows per thread
-  constexpr int HR = RT / 64;                                        // tile rows per lane
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int nb = (a.E + kLgBlock - 1) / kLgBlock;
-  const int mat = blockIdx.y / nb, eb = blockIdx.y - mat * nb;
-  const W* wr = static_cast<const W*>(mat == 0 ? a.wr : a.wr2);
-  const float* bias = mat == 0 ? a.bias : a.bias2;
-  float* out = mat == 0 ? a.logits : a.logits2;
-  const int e0 = eb * kLgBlock, ne = min(kLgBlock, a.E - e0);
-  const bool vec = (ne == kLgBlock) && ((a.E * static_cast<int>(sizeof(W))) % 16 == 0);
-  const int t = blockIdx.x * kLgWaves + wave;
-  const bool active = t < a.T;
-  const W* hrow = static_cast<const W*>(a.h) + static_cast<size_t>(active ? t : 0) * a.d;
-  float acc[kLgBlock];
-#pragma unroll
-  for (int q = 0; q < kLgBlock; ++q) acc[q] = 0.0f;
+__global__ __launch_bounds__(256) void logits_wave_kernel(LogitsArgs a) {
+  const int lane = threadIdx.x & 63;
+  const int o = blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int per = a.T * a.E;
+  if (o >= per * (a.wr2 != nullptr ? 2 : 1)) return;  // whole waves only: no barrier below
+  const float v = wave_logit<W, kWaveSteps>(a, o, lane);
+  if (lane == 0) {
+    const int mat = o / per, te = o - mat * per;
+    (mat == 0 ? a.logits : a.logits2)[te] = v;
+  }
+}
 
-  for (int j0 = 0; j0 < a.d; j0 += RT) {
-    const int rows = min(RT, a.d - j0);
-    // this lane's activations for the tile (rows j0 + lane + 64 m); every
-    // load is issued (clamped into the row), unused values are zeroed
-    float hv[HR];
-#pragma unroll
-    for (int m = 0; m < HR; ++m) hv[m] = to_f32(hrow[j0 + min(lane + 64 * m, rows - 1)]);
-#pragma unroll
-    for (int m = 0; m < HR; ++m)
-      if (lane + 64 * m >= rows) hv[m] = 0.0f;
-    if (vec) {
-      // all of this thread's row loads first, then the LDS stores
-      uint4 buf[RB][NV];
-#pragma unroll
-      for (int u = 0; u < RB; ++u) {
-        const int r = min(tid + 64 * kLgWaves * u, rows - 1);
-        const uint4* src = reinterpret_cast<const uint4*>(wr + static_cast<size_t>(j0 + r) * a.E + e0);
-#pragma unroll
-        for (int b = 0; b < NV; ++b) buf[u][b] = src[b];
-      }
-#pragma unroll
-      for (int u = 0; u < RB; ++u) {
-        const int r = tid + 64 * kLgWaves * u;
-        if (r < rows) {
-#pragma unroll
-          for (int b = 0; b < NV; ++b) reinterpret_cast<uint4*>(tile + r * kLgBlock)[b] = buf[u][b];
-        }
-      }
-    } else {
-      for (int r = tid; r < rows; r += 64 * kLgWaves) {
-        const W* src = wr + static_cast<size_t>(j0 + r) * a.E + e0;
-#pragma unroll
-        for (int q = 0; q < kLgBlock; ++q) tile[r * kLgBlock + q] = q < ne ? src[q] : W(0);
-      }
-    }
-    __syncthreads();
-    if (active) {
-#pragma unroll
-      for (int m = 0; m < HR; ++m) {
-        const int j = min(lane + 64 * m, rows - 1);
-        if (lane + 64 * m < rows) {
-          float wv[kLgBlock];
-#pragma unroll
-          for (int q = 0; q < kLgBlock; ++q) wv[q] = to_f32(tile[j * kLgBlock + q]);
-#pragma unroll
-          for (int q = 0; q < kLgBlock; ++q) acc[q] = fmaf(hv[m], wv[q], acc[q]);
-        }
-      }
-    }
-    __syncthreads();
+// At most kFusedLogits logits: the route work-group computes them itself
+// (one wave per logit, as above) into LDS and goes on with the route body.
+constexpr int kFusedLogits = 32;
+
+template <typename W>
+__global__ __launch_bounds__(64 * kRouteWaves) void route_fused_kernel(LogitsArgs la, RouteArgs ra) {
+  __shared__ float lg[kFusedLogits];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int per = la.T * la.E;
+  const int n_out = per * (la.wr2 != nullptr ? 2 : 1);
+  for (int o = wave; o < n_out; o += kRouteWaves) {
+    const float v = wave_logit<W, kWaveSteps / 2>(la, o, lane);  // 1024 threads: 128 registers a lane
+    if (lane == 0) lg[o] = v;
   }
-  if (active) {
-#pragma unroll
-    for (int q = 0; q < kLgBlock; ++q) {
-      float v = acc[q];
-#pragma unroll
-      for (int s = 32; s >= 1; s >>= 1) v = v + __shfl_down(v, s, 64);
-      if (lane == 0 && q < ne) {
-        if (bias != nullptr) v = v + bias[e0 + q];
-        out[static_cast<size_t>(t) * a.E + e0 + q] = v;
-      }
-    }
-  }
+  __syncthreads();
+  RouteArgs a = ra;
+  a.logits = ra.logits != nullptr ? lg : nullptr;
+  a.logits_pred = ra.logits_pred != nullptr ? (ra.logits != nullptr ? lg + per : lg) : nullptr;
+  route_body<kRouteWaves>(a);
 }
 
 // Many tokens: the same order, with each lane running the fma chains of 8
@@ -701,7 +675,8 @@ __global__ __launch_bounds__(256) void logits_many_kernel(LogitsArgs a) {
 hipError_t launch_logits_route(const LogitsArgs& a, const RouteArgs& ra, hipStream_t s) {
   if (a.T <= 0) return hipSuccess;
   const int mats = (a.wr != nullptr ? 1 : 0) + (a.wr2 != nullptr ? 1 : 0);
-  if (mats == 0) return hipErrorInvalidValue;
+  if (mats == 0 || (a.wr != nullptr && a.wt == nullptr) || (a.wr2 != nullptr && a.wt2 == nullptr))
+    return hipErrorInvalidValue;
   LogitsArgs b = a;
   if (a.wr == nullptr) {  // only the second router: move it to slot 0
     b.wr = a.wr2;
@@ -713,8 +688,7 @@ hipError_t launch_logits_route(const LogitsArgs& a, const RouteArgs& ra, hipStre
   }
   const int TB = route_block_tokens(ra.K);
   const int nblk = (a.T + TB - 1) / TB;
-  const bool many = a.T >= kManyTokens && b.wt != nullptr && (mats == 1 || b.wt2 != nullptr) &&
-                    ra.lrank != nullptr && ra.blk != nullptr && ra.psc != nullptr && nblk <= ra.nblk_cap &&
+  const bool many = a.T >= kManyTokens && ra.lrank != nullptr && ra.blk != nullptr && ra.psc != nullptr && nblk <= ra.nblk_cap &&
                     TB * ra.K <= 64 * kSelWaves;
   if (many) {
     const int nb = (a.E + kLmExperts - 1) / kLmExperts;
@@ -724,12 +698,19 @@ hipError_t launch_logits_route(const LogitsArgs& a, const RouteArgs& ra, hipStre
     else
       hipLaunchKernelGGL(logits_many_kernel<float>, grid, dim3(256), 0, s, b);
   } else {
-    const int nb = (a.E + kLgBlock - 1) / kLgBlock;
-    const dim3 grid((a.T + kLgWaves - 1) / kLgWaves, nb * mats);
+    const int n_out = a.T * a.E * mats;
+    if (n_out <= kFusedLogits) {  // one launch for logits and route
+      if (a.dtype == kBF16)
+        hipLaunchKernelGGL(route_fused_kernel<uint16_t>, dim3(1), dim3(64 * kRouteWaves), 0, s, b, ra);
+      else
+        hipLaunchKernelGGL(route_fused_kernel<float>, dim3(1), dim3(64 * kRouteWaves), 0, s, b, ra);
+      return hipGetLastError();
+    }
+    const dim3 grid((n_out + 3) / 4);
     if (a.dtype == kBF16)
-      hipLaunchKernelGGL(logits_kernel<uint16_t>, grid, dim3(64 * kLgWaves), 0, s, b);
+      hipLaunchKernelGGL(logits_wave_kernel<uint16_t>, grid, dim3(256), 0, s, b);
     else
-      hipLaunchKernelGGL(logits_kernel<float>, grid, dim3(64 * kLgWaves), 0, s, b);
+      hipLaunchKernelGGL(logits_wave_kernel<float>, grid, dim3(256), 0, s, b);
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;

@@ -239,6 +239,7 @@ struct Group {
   bool prefetch = false;  // issued by prefetch
   bool used = false;      // consumed by a forward
   bool pre = false;       // computed by the running forward's resident launch
+  bool landed = false;    // its copy was seen complete (not polled again)
 };
 
 struct BufSlot {
@@ -302,6 +303,8 @@ struct ms_ctx {
   std::string err;
   bool poisoned = false;
   // online cache replacement (Sec. 3.3) and the priority's parameters
+  bool side_work = false;  // the running forward enqueued kernels on the side stream
+  bool side2_work = false;  // ... on the second side stream
   int policy = MS_CACHE_STATIC;
   double rho = 0.25, omega = 128.0;
   uint64_t rng = 0x9e3779b97f4a7c15ull;
@@ -309,6 +312,7 @@ struct ms_ctx {
   unsigned char* pool = nullptr;
   uint64_t pool_bytes = 0;
   hipStream_t copy = nullptr, side = nullptr;
+  hipStream_t side2 = nullptr;  // prefill: every other missing expert's compute
   // pinned host store
   std::vector<unsigned char*> blobs;      // pinned, coherent host memory (never cached by the GPU)
   std::vector<unsigned char*> blobs_dev;  // the same memory's device-side addresses
@@ -326,6 +330,7 @@ struct ms_ctx {
   std::deque<PendingGroup> pf_queue;
   std::vector<PendingGroup> pf_inflight;
   hipEvent_t ev_route = nullptr, ev_res = nullptr, ev_side_done = nullptr, ev_last = nullptr;
+  hipEvent_t ev_side2_done = nullptr;
   bool has_last = false;
   hipStream_t last_stream = nullptr;
   std::vector<hipEvent_t> free_events;
@@ -428,6 +433,17 @@ ms_status issue_group(ms_ctx* ctx, int si, int gi, bool prefetch) {
   return MS_OK;
 }
 
+// Whether group gi of slot si has landed: its event is polled until it has
+// been seen complete once (each poll is a runtime call on the host).
+hipError_t group_landed(ms_ctx* ctx, int si, int gi) {
+  Group& g = ctx->buf[si].groups[gi];
+  if (g.landed) return hipSuccess;
+  if (!g.issued) return hipErrorNotReady;
+  const hipError_t q = hipEventQuery(ctx->buf[si].gev[gi]);
+  if (q == hipSuccess) g.landed = true;
+  return q;
+}
+
 // Point a staging slot at (layer, e) covering chunks [first, n_chunks).  The
 // copy stream first waits for the slot's previous readers.
 ms_status assign_slot(ms_ctx* ctx, int si, int layer, int e, int first) {
@@ -518,7 +534,7 @@ std::vector<int> miss_order(ms_ctx* ctx, int layer, const std::vector<int32_t>& 
 ms_status pump_prefetch(ms_ctx* ctx) {
   for (size_t i = 0; i < ctx->pf_inflight.size();) {
     const PendingGroup pg = ctx->pf_inflight[i];
-    const hipError_t q = hipEventQuery(ctx->buf[pg.slot].gev[pg.group]);
+    const hipError_t q = group_landed(ctx, pg.slot, pg.group);
     if (q == hipSuccess) {
       ctx->pf_inflight.erase(ctx->pf_inflight.begin() + i);
     } else if (q == hipErrorNotReady) {
@@ -788,8 +804,7 @@ ms_status prefill_experts(ms_ctx* ctx, int layer, const void* h_dev, int T, cons
       any_issued = any_issued || g.issued;
       const int lo = std::max(g.c_lo, res);
       if (lo >= g.c_hi) continue;
-      hipError_t q = hipErrorNotReady;
-      if (g.issued) q = hipEventQuery(b.gev[gi]);
+      const hipError_t q = group_landed(ctx, si, gi);
       if (q != hipSuccess && q != hipErrorNotReady) return poison(ctx, "hipEventQuery(group)", q);
       if (q == hipSuccess) {
         gu.push_back(task(b.base, nullptr, e, lo, g.c_hi - lo, 0, m_tiles(e)));
@@ -827,10 +842,15 @@ ms_status prefill_experts(ms_ctx* ctx, int layer, const void* h_dev, int T, cons
   // experts still missing chunks: side stream, those a staging slot already
   // covers first.  Their slots stay reserved until then, so that no other
   // miss evicts them.
+  // Missing experts alternate between two side streams: each expert's
+  // launches are small (a few row tiles), so two run side by side.
   MS_HIP(hipStreamWaitEvent(ctx->side, ctx->ev_res, 0));
+  MS_HIP(hipStreamWaitEvent(ctx->side2, ctx->ev_res, 0));
   for (int e = 0; e < s.E; ++e)
     if (covering[e] >= 0 && !complete[e]) ctx->buf[covering[e]].use_order = kReserved;
+  int n_missing = 0;
   for (const int e : miss_order(ctx, layer, offs, &complete)) {
+    hipStream_t ss = (n_missing++ % 2) ? ctx->side2 : ctx->side;
     const int res = resident_chunks(L, e);
     int si = covering[e];
     if (si < 0) {
@@ -854,14 +874,16 @@ ms_status prefill_experts(ms_ctx* ctx, int layer, const void* h_dev, int T, cons
         L.st.bytes_prefetch_used += s.chunk_bytes * (g.c_hi - g.c_lo);
       }
       g.used = true;
-      MS_HIP(hipStreamWaitEvent(ctx->side, b.gev[gi], 0));
-      st = launch({task(b.base, nullptr, e, lo, g.c_hi - lo, 0, m_tiles(e))}, ctx->side, false);
+      MS_HIP(hipStreamWaitEvent(ss, b.gev[gi], 0));
+      (ss == ctx->side ? ctx->side_work : ctx->side2_work) = true;
+      st = launch({task(b.base, nullptr, e, lo, g.c_hi - lo, 0, m_tiles(e))}, ss, false);
       if (st != MS_OK) return st;
     }
     const unsigned char* top = res > 0 ? L.cache_base + L.top_bytes * L.slot_of[e] : b.base;
-    st = launch({task(top, b.base, e, 0, s.n_chunks, res, m_tiles(e))}, ctx->side, true);
+    (ss == ctx->side ? ctx->side_work : ctx->side2_work) = true;
+    st = launch({task(top, b.base, e, 0, s.n_chunks, res, m_tiles(e))}, ss, true);
     if (st != MS_OK) return st;
-    MS_HIP(hipEventRecord(b.last_read, ctx->side));
+    MS_HIP(hipEventRecord(b.last_read, ss));
     b.has_last_read = true;
   }
   return MS_OK;
@@ -946,7 +968,9 @@ ms_status ms_create(const ms_model_desc* desc, void* dev_pool, uint64_t pool_byt
     return cleanup_fail(e, "hipStreamCreate(copy)");
   if ((e = hipStreamCreateWithFlags(&ctx->side, hipStreamNonBlocking)) != hipSuccess)
     return cleanup_fail(e, "hipStreamCreate(side)");
-  for (hipEvent_t* ev : {&ctx->ev_route, &ctx->ev_res, &ctx->ev_side_done, &ctx->ev_last})
+  if ((e = hipStreamCreateWithFlags(&ctx->side2, hipStreamNonBlocking)) != hipSuccess)
+    return cleanup_fail(e, "hipStreamCreate(side2)");
+  for (hipEvent_t* ev : {&ctx->ev_route, &ctx->ev_res, &ctx->ev_side_done, &ctx->ev_last, &ctx->ev_side2_done})
     if ((e = hipEventCreateWithFlags(ev, hipEventDisableTiming)) != hipSuccess)
       return cleanup_fail(e, "hipEventCreate");
   // small host buffers that kernels write directly (mapped, coherent)
@@ -991,6 +1015,7 @@ void ms_destroy(ms_ctx* ctx) {
   if (!ctx) return;
   if (ctx->copy) (void)hipStreamSynchronize(ctx->copy);
   if (ctx->side) (void)hipStreamSynchronize(ctx->side);
+  if (ctx->side2) (void)hipStreamSynchronize(ctx->side2);
   if (ctx->has_last) (void)hipEventSynchronize(ctx->ev_last);
   for (LayerState& L : ctx->layers) {
     for (hipEvent_t ev : L.pending_loads) (void)hipEventDestroy(ev);
@@ -1007,7 +1032,7 @@ void ms_destroy(ms_ctx* ctx) {
   }
   for (hipEvent_t ev : ctx->tl_pool) (void)hipEventDestroy(ev);
   if (ctx->tl_origin) (void)hipEventDestroy(ctx->tl_origin);
-  for (hipEvent_t ev : {ctx->ev_route, ctx->ev_res, ctx->ev_side_done, ctx->ev_last})
+  for (hipEvent_t ev : {ctx->ev_route, ctx->ev_res, ctx->ev_side_done, ctx->ev_last, ctx->ev_side2_done})
     if (ev) (void)hipEventDestroy(ev);
   for (unsigned char* p : ctx->blobs) (void)hipHostFree(p);
   if (ctx->h_offsets) (void)hipHostFree(ctx->h_offsets);
@@ -1015,6 +1040,7 @@ void ms_destroy(ms_ctx* ctx) {
   if (ctx->h_score) (void)hipHostFree(ctx->h_score);
   if (ctx->copy) (void)hipStreamDestroy(ctx->copy);
   if (ctx->side) (void)hipStreamDestroy(ctx->side);
+  if (ctx->side2) (void)hipStreamDestroy(ctx->side2);
   delete ctx;
 }
 
@@ -1143,6 +1169,7 @@ ms_status ms_sync(ms_ctx* ctx) {
   MS_CHECK_CTX(ctx);
   MS_HIP(hipStreamSynchronize(ctx->copy));
   MS_HIP(hipStreamSynchronize(ctx->side));
+  MS_HIP(hipStreamSynchronize(ctx->side2));
   if (ctx->has_last) MS_HIP(hipEventSynchronize(ctx->ev_last));
   return MS_OK;
 }
@@ -1343,6 +1370,7 @@ ms_status ms_forward(ms_ctx* ctx, int32_t layer, const void* h_dev, int32_t T, f
   }
   L.pending_loads.clear();
 
+  ctx->side_work = ctx->side2_work = false;
   const int TK = T * s.K;
   int32_t* d_offsets = reinterpret_cast<int32_t*>(ctx->dev(s.off_offsets));
   int32_t* d_perm = reinterpret_cast<int32_t*>(ctx->dev(s.off_perm));
@@ -1442,7 +1470,7 @@ ms_status ms_forward(ms_ctx* ctx, int32_t layer, const void* h_dev, int32_t T, f
       Group& g = b.groups[gi];
       const int lo = std::max(g.c_lo, res);
       if (!g.issued || lo >= g.c_hi) continue;
-      const hipError_t q = hipEventQuery(b.gev[gi]);
+      const hipError_t q = group_landed(ctx, static_cast<int>(&b - ctx->buf.data()), gi);
       if (q == hipErrorNotReady) continue;
       if (q != hipSuccess) return poison(ctx, "hipEventQuery(group)", q);
       msk::FfnTask t{};
@@ -1579,7 +1607,7 @@ ms_status ms_forward(ms_ctx* ctx, int32_t layer, const void* h_dev, int32_t T, f
         count_used(g);
         continue;
       }
-      const hipError_t q = hipEventQuery(b.gev[gi]);
+      const hipError_t q = group_landed(ctx, si, gi);
       if (q == hipErrorNotReady) continue;
       if (q != hipSuccess) return poison(ctx, "hipEventQuery(group)", q);
       msk::FfnTask t{};
@@ -1598,6 +1626,7 @@ ms_status ms_forward(ms_ctx* ctx, int32_t layer, const void* h_dev, int32_t T, f
     if (any) landed_slots.push_back(si);
   }
   if (!landed.empty()) {
+    ctx->side_work = true;
     st = launch_tasks(landed, ctx->side, MS_IV_FFN_STREAMED, T, nullptr, nullptr);
     if (st != MS_OK) return st;
   }
@@ -1655,6 +1684,7 @@ ms_status ms_forward(ms_ctx* ctx, int32_t layer, const void* h_dev, int32_t T, f
       fa.tasks[0].n_chunks = g.c_hi - lo;
       fa.tasks[0].wg_begin = 0;
       fa.n_wg = (g.c_hi - lo) * s.subs;
+      ctx->side_work = true;
       ti = tl_begin(ctx, ctx->side, MS_IV_FFN_STREAMED, layer, s.chunk_bytes * (g.c_hi - lo));
       MS_HIP(msk::launch_ffn(fa, offs[e + 1] - offs[e], ctx->side));
       tl_end(ctx, ti, ctx->side);
@@ -1671,8 +1701,16 @@ ms_status ms_forward(ms_ctx* ctx, int32_t layer, const void* h_dev, int32_t T, f
   }
   for (BufSlot& b : ctx->buf)
     for (Group& g : b.groups) g.pre = false;
-  MS_HIP(hipEventRecord(ctx->ev_side_done, ctx->side));
-  MS_HIP(hipStreamWaitEvent(sm, ctx->ev_side_done, 0));
+  // the combine needs the side stream only if this forward put kernels on
+  // it (a cross-stream hand-off costs tens of microseconds)
+  if (ctx->side_work) {
+    MS_HIP(hipEventRecord(ctx->ev_side_done, ctx->side));
+    MS_HIP(hipStreamWaitEvent(sm, ctx->ev_side_done, 0));
+  }
+  if (ctx->side2_work) {
+    MS_HIP(hipEventRecord(ctx->ev_side2_done, ctx->side2));
+    MS_HIP(hipStreamWaitEvent(sm, ctx->ev_side2_done, 0));
+  }
 
   // 6. combine (Eq. (2) weighted sum, fixed order)
   msk::CombineArgs ca{};
