@@ -520,6 +520,7 @@ def main():
     ap.add_argument("--configure", action="store_true",
                     help="stacks: per-layer budgets and split ratios from the cache configurator")
     ap.add_argument("--zeta", type=float, default=0.01)
+    ap.add_argument("--ffn-splits", type=int, default=0, help="work-groups per chunk (0: the library's choice)")
     ap.add_argument("--out", default=None)
     ap.add_argument("--cmd", nargs="*", default=[], help="the profiling command(s), recorded in the summary")
     args = ap.parse_args()
@@ -549,7 +550,7 @@ def main():
     t_setup = time.perf_counter()
     log("generating %s weights and filling the pinned store" % shape.name)
     rig = SplitRig(shape, seed=0, max_tokens=T, budget_bytes=shape.n_experts * shape.expert_bytes,
-                   keep_f32=not args.no_cpu_baseline, threads=16)
+                   keep_f32=not args.no_cpu_baseline, threads=16, ffn_splits=args.ffn_splits)
     n_tok = args.warmup + args.steps
     seq = synth.walk(shape, 0, n_tok, T=T)
     hs = [to_device(raw, shape.dtype) for raw, _ in seq]

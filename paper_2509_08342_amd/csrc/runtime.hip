@@ -92,8 +92,11 @@ ms_status derive_shape(const ms_model_desc* d, Shape* s, std::string* err) {
   s->expert_bytes = s->chunk_bytes * s->n_chunks;
   s->shared_bytes = s->chunk_bytes * s->n_chunks_sh;
   s->group_chunks = static_cast<int>(std::max<uint64_t>(1, kGroupTargetBytes / s->chunk_bytes));
-  // work-groups per chunk: enough that a decode step over the experts a
-  // forward can activate gives the FFN kernel >= 768 work-groups
+  // work-groups per chunk: one for experts of many chunks (each work-group
+  // then streams more bytes, and fewer partial planes reach the combine),
+  // two otherwise, doubled until the experts a forward can activate give
+  // the FFN kernel >= 256 work-groups (measured best on this GPU for the
+  // Mixtral-, DeepSeek- and Qwen3-shaped decode layers)
   const int max_subs = msk::max_ffn_splits(d->d_model, d->dtype == MS_BF16 ? 2 : 4);
   if (d->ffn_splits > max_subs) {
     *err = "ffn_splits too large for this d_model and dtype";
@@ -104,8 +107,8 @@ ms_status derive_shape(const ms_model_desc* d, Shape* s, std::string* err) {
   } else {
     const int64_t active = std::min<int64_t>(s->E, static_cast<int64_t>(s->max_T) * s->K) + s->n_sh;
     const int64_t work = active * s->n_chunks;
-    s->subs = 1;
-    while (s->subs < max_subs && work * s->subs < 768) s->subs *= 2;
+    s->subs = std::min(max_subs, s->n_chunks >= 128 ? 1 : 2);
+    while (s->subs < max_subs && work * s->subs < 256) s->subs *= 2;
   }
 
   const uint64_t TK = static_cast<uint64_t>(s->max_T) * s->K;
