@@ -49,7 +49,7 @@ struct LogitsArgs {
 // everything after the logits -- a single launch when there are at most 32
 // logits.
 constexpr int kManyTokens = 64;
-inline int route_block_tokens(int K) { return K <= 16 ? 16 : 4; }
+inline int route_block_tokens(int /*K*/) { return 4; }  // one token per wave of the selection
 
 
 // One work-group: top-K selection with lowest-index ties and Eq. (2) gate
@@ -117,12 +117,16 @@ hipError_t launch_ffn(const FfnArgs& a, int max_tok, hipStream_t s);
 
 // Prefill (many tokens per expert) runs on the matrix cores in two steps:
 //  gate/up (mma_gateup): act[row][f] = bf16(silu(h_row . G_f) * (h_row . U_f))
-//    for a task's chunk range, 64 rows x 64 units per work-group; runs per
-//    segment as data lands (disjoint columns of act);
+//    for a task's chunk range, 64 rows x 64 / gu_split units per work-group
+//    (m_tiles * n_chunks * gu_split work-groups per task); runs per segment
+//    as data lands (disjoint columns of act);
 //  down (mma_down): out[row][:] = sum_f act[row][f] * D_f over all of the
 //    expert's chunks (chunks < split at base, the rest at base2), 64 rows x
 //    128 columns per work-group, written as the single partial plane.
 constexpr int kMaxMmaTasks = 80;
+// gate/up work-groups per chunk and row tile: 4 (16 units each) for launches
+// of fewer than kGuSplitBelow row-tile chunks, else 1 (whole chunks)
+constexpr int kGuSplitBelow = 256;
 constexpr int kMmaRows = 64;     // rows (token slots) per work-group
 constexpr int kMmaCols = 128;    // output columns per down work-group
 
@@ -152,6 +156,7 @@ struct MmaArgs {
   int32_t rows_shared;         // shared rows per expert (max T)
   int32_t n_tasks, n_wg;
   int32_t ncb;                 // down: column blocks (ceil(d / kMmaCols))
+  int32_t gu_split;            // gate/up: work-groups per chunk and row tile (1 or 4)
   MmaTask tasks[kMaxMmaTasks];
 };
 hipError_t launch_mma_gateup(const MmaArgs& a, hipStream_t s);

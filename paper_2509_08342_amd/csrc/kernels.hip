@@ -398,20 +398,35 @@ __global__ __launch_bounds__(64 * kScanWaves) void scan_many_kernel(RouteArgs a,
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int E = a.E;
   if (a.logits != nullptr) {
+    // per expert (one wave): the counts of up to kScanPer x 64 blocks are
+    // loaded together, then scanned 64 at a time
+    constexpr int kScanPer = 8;
     for (int e = wave; e < E; e += kScanWaves) {
       int* row = a.blk + static_cast<size_t>(e) * a.nblk_cap;
       int run = 0;
-      for (int b0 = 0; b0 < nblk; b0 += 64) {
-        const int b = b0 + lane;
-        const int c = b < nblk ? row[b] : 0;
-        int incl = c;
+      for (int B0 = 0; B0 < nblk; B0 += 64 * kScanPer) {
+        int cv[kScanPer];
 #pragma unroll
-        for (int s = 1; s < 64; s <<= 1) {
-          const int o = __shfl_up(incl, s, 64);
-          if (lane >= s) incl += o;
+        for (int j = 0; j < kScanPer; ++j) {
+          const int b = B0 + 64 * j + lane;
+          cv[j] = row[min(b, nblk - 1)];  // every load issued, in bounds
         }
-        if (b < nblk) row[b] = run + incl - c;
-        run += __shfl(incl, 63, 64);
+#pragma unroll
+        for (int j = 0; j < kScanPer; ++j)
+          if (B0 + 64 * j + lane >= nblk) cv[j] = 0;
+#pragma unroll
+        for (int j = 0; j < kScanPer; ++j) {
+          const int b = B0 + 64 * j + lane;
+          const int c = cv[j];
+          int incl = c;
+#pragma unroll
+          for (int s = 1; s < 64; s <<= 1) {
+            const int o = __shfl_up(incl, s, 64);
+            if (lane >= s) incl += o;
+          }
+          if (b < nblk) row[b] = run + incl - c;
+          run += __shfl(incl, 63, 64);
+        }
       }
       if (lane == 0) tot[e] = run;
     }
@@ -419,10 +434,26 @@ __global__ __launch_bounds__(64 * kScanWaves) void scan_many_kernel(RouteArgs a,
     if (wave == 0) scan_offsets(tot, nullptr, a, lane);
   }
   if (a.logits_pred != nullptr) {
-    for (int e = tid; e < E; e += 64 * kScanWaves) {
+    // per expert (one wave): lanes sum blocks lane, lane + 64, ... in order,
+    // then a fixed halving tree over the lanes
+    for (int e = wave; e < E; e += kScanWaves) {
       float sc = 0.0f;
-      for (int b = 0; b < nblk; ++b) sc += a.psc[static_cast<size_t>(b) * E + e];
-      score_s[e] = sc;
+      for (int B0 = 0; B0 < nblk; B0 += 64 * 8) {
+        float pv[8];
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+          const int b = B0 + 64 * j + lane;
+          pv[j] = a.psc[static_cast<size_t>(min(b, nblk - 1)) * E + e];  // every load issued, in bounds
+        }
+#pragma unroll
+        for (int j = 0; j < 8; ++j)
+          if (B0 + 64 * j + lane >= nblk) pv[j] = 0.0f;
+#pragma unroll
+        for (int j = 0; j < 8; ++j) sc += pv[j];  // blocks lane, lane + 64, ... in order
+      }
+#pragma unroll
+      for (int s = 32; s >= 1; s >>= 1) sc = sc + __shfl_down(sc, s, 64);
+      if (lane == 0) score_s[e] = sc;
     }
     __syncthreads();
     rank_scores(score_s, a, tid, 64 * kScanWaves);
@@ -1071,15 +1102,27 @@ __device__ __forceinline__ TileRows tile_rows(const MmaArgs& a, const MmaTask& t
   return r;
 }
 
+// gate/up: a work-group takes 64 rows x 16 NF units (kChunkUnits / (16 NF)
+// = a.gu_split work-groups per chunk and row tile); wave w the rows 16 w ..
+// 16 w + 15.  Per 32-wide k step a lane loads one A fragment and NF G and NF
+// U fragments; loads run one batch ahead of the MFMAs.  Launches with few
+// row-tile chunks split each chunk four ways (NF = 1) for parallelism;
+// large ones keep whole chunks (NF = 4), so the activation rows are read
+// once per chunk.  Each activation is written once, so the split changes no
+// result.
+template <int NF>
 __global__ __launch_bounds__(256) void mma_gateup_kernel(MmaArgs a) {
+  constexpr int KB = NF == 1 ? 4 : 2;  // k steps per batch
   const int wg = blockIdx.x;
   const MmaTask tk = a.tasks[find_task(a.tasks, a.n_tasks, wg)];
   const int local = wg - tk.wg_begin;
   const int mt = local % tk.m_tiles;
-  const int c = tk.chunk_lo + local / tk.m_tiles;
+  const int cq = local / tk.m_tiles;          // chunk * split + part
+  const int split = kChunkUnits / (16 * NF);
+  const int c = tk.chunk_lo + cq / split, part = cq % split;
   const TileRows tr = tile_rows(a, tk, mt);
-  if (tr.n <= 0) return;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  if (16 * wave >= tr.n) return;  // no rows for this wave (no barrier in this kernel)
   const int d = a.d;
   const bool routed = tk.expert >= 0;
   // this lane's A row: tile row 16 wave + lane % 16 (clamped; masked at the end)
@@ -1088,50 +1131,61 @@ __global__ __launch_bounds__(256) void mma_gateup_kernel(MmaArgs a) {
   const uint16_t* hrow = static_cast<const uint16_t*>(a.h) + static_cast<size_t>(tok) * d;
   const uint16_t* G = reinterpret_cast<const uint16_t*>(tk.base + static_cast<size_t>(c) * a.chunk_bytes);
   const uint16_t* U = G + static_cast<size_t>(kChunkUnits) * d;
-  const int kq = 8 * (lane >> 4);  // this lane's k offset inside a 32-wide step
-  f32x4_t ag[4], au[4];
+  const int unit0 = 16 * NF * part + (lane & 15);  // this lane's first B column (unit within the chunk)
+  const int kq = 8 * (lane >> 4);                // this lane's k offset inside a 32-wide step
+  f32x4_t ag[NF], au[NF];
 #pragma unroll
-  for (int nf = 0; nf < 4; ++nf) ag[nf] = au[nf] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-  constexpr int KB = 2;  // k steps loaded per batch
-  for (int k0 = 0; k0 < d; k0 += 32 * KB) {
-    uint4 av[KB], gv[KB][4], uv[KB][4];
+  for (int n = 0; n < NF; ++n) ag[n] = au[n] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  uint4 an[KB], gn[KB][NF], un[KB][NF];
+  auto load = [&](int k0) {  // steps past d reload the last one (in bounds, not used)
 #pragma unroll
     for (int s = 0; s < KB; ++s) {
       const int k = min(k0 + 32 * s, d - 32);
-      av[s] = ld16(hrow + k + kq);
+      an[s] = ld16(hrow + k + kq);
 #pragma unroll
-      for (int nf = 0; nf < 4; ++nf) {
-        const int unit = 16 * nf + (lane & 15);
-        const size_t off = (static_cast<size_t>(k / kKTile) * kChunkUnits + unit) * kKTile + (k % kKTile) + kq;
-        gv[s][nf] = ldw16(G + off);
-        uv[s][nf] = ldw16(U + off);
+      for (int n = 0; n < NF; ++n) {
+        const size_t off =
+            (static_cast<size_t>(k / kKTile) * kChunkUnits + unit0 + 16 * n) * kKTile + (k % kKTile) + kq;
+        gn[s][n] = ldw16(G + off);
+        un[s][n] = ldw16(U + off);
       }
     }
+  };
+  load(0);
+  for (int k0 = 0; k0 < d; k0 += 32 * KB) {
+    uint4 ac[KB], gc[KB][NF], uc[KB][NF];
+#pragma unroll
+    for (int s = 0; s < KB; ++s) {
+      ac[s] = an[s];
+#pragma unroll
+      for (int n = 0; n < NF; ++n) {
+        gc[s][n] = gn[s][n];
+        uc[s][n] = un[s][n];
+      }
+    }
+    load(k0 + 32 * KB);
 #pragma unroll
     for (int s = 0; s < KB; ++s) {
       if (k0 + 32 * s < d) {
-        const bf16x8_t A = as_bf16x8(av[s]);
+        const bf16x8_t A = as_bf16x8(ac[s]);
 #pragma unroll
-        for (int nf = 0; nf < 4; ++nf) {
-          ag[nf] = mfma16(A, as_bf16x8(gv[s][nf]), ag[nf]);
-          au[nf] = mfma16(A, as_bf16x8(uv[s][nf]), au[nf]);
+        for (int n = 0; n < NF; ++n) {
+          ag[n] = mfma16(A, as_bf16x8(gc[s][n]), ag[n]);
+          au[n] = mfma16(A, as_bf16x8(uc[s][n]), au[n]);
         }
       }
     }
   }
-  // epilogue: act = silu(g) * u as bf16, rows 4*(lane/16)+r of this wave's 16
+  // epilogue: act = silu(g) * u as bf16, rows 16 wave + 4 (lane / 16) + r
   uint16_t* act = routed ? a.act : a.act_sh + static_cast<size_t>(-1 - tk.expert) * a.rows_shared * a.f_pad_sh;
   const int f_pad = routed ? a.f_pad : a.f_pad_sh;
 #pragma unroll
-  for (int nf = 0; nf < 4; ++nf) {
-    const int f = c * kChunkUnits + 16 * nf + (lane & 15);
+  for (int n = 0; n < NF; ++n) {
+    const int f = c * kChunkUnits + unit0 + 16 * n;
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
       const int row = 16 * wave + 4 * (lane >> 4) + r;
-      if (row < tr.n) {
-        const float g = ag[nf][r], u = au[nf][r];
-        act[static_cast<size_t>(tr.p0 + row) * f_pad + f] = f2bf(silu(g) * u);
-      }
+      if (row < tr.n) act[static_cast<size_t>(tr.p0 + row) * f_pad + f] = f2bf(silu(ag[n][r]) * au[n][r]);
     }
   }
 }
@@ -1157,18 +1211,31 @@ __global__ __launch_bounds__(256) void mma_down_kernel(MmaArgs a) {
   f32x4_t acc[8];
 #pragma unroll
   for (int nf = 0; nf < 8; ++nf) acc[nf] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-  for (int c = 0; c < tk.n_chunks; ++c) {
+  const bool active = 16 * wave < tr.n;  // waves without rows still stage D tiles
+  // the next chunk's D tile and A fragments load while this chunk computes
+  uint4 dn[4], an[2];
+  auto load_chunk = [&](int c) {
     const unsigned char* cbase = (c < tk.split ? tk.base : tk.base2) + static_cast<size_t>(c) * a.chunk_bytes;
     const uint16_t* D = reinterpret_cast<const uint16_t*>(cbase) + 2 * static_cast<size_t>(kChunkUnits) * d;
-    // stage D[64 units][128 columns] transposed: dt[column][unit]
-    uint4 dv[4];
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int piece = tid + 256 * i;           // 64 units x 16 pieces of 8 columns
       const int f = piece >> 4, q = piece & 15;
       const int col = min(col0 + 8 * q, d - 8);  // clamped; columns past d are never stored
-      dv[i] = ld16(D + static_cast<size_t>(f) * d + col);
+      dn[i] = ld16(D + static_cast<size_t>(f) * d + col);
     }
+#pragma unroll
+    for (int ks = 0; ks < 2; ++ks) an[ks] = ld16(arow + c * kChunkUnits + 32 * ks + kq);
+  };
+  load_chunk(0);
+  for (int c = 0; c < tk.n_chunks; ++c) {
+    uint4 dv[4], av[2];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) dv[i] = dn[i];
+    av[0] = an[0];
+    av[1] = an[1];
+    load_chunk(min(c + 1, tk.n_chunks - 1));  // the last chunk reloads itself (in bounds, unused)
+    // stage D[64 units][128 columns] transposed: dt[column][unit]
     __syncthreads();  // previous chunk's readers are done with dt
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
@@ -1182,13 +1249,15 @@ __global__ __launch_bounds__(256) void mma_down_kernel(MmaArgs a) {
       }
     }
     __syncthreads();
+    if (active) {
 #pragma unroll
-    for (int ks = 0; ks < 2; ++ks) {
-      const bf16x8_t A = as_bf16x8(ld16(arow + c * kChunkUnits + 32 * ks + kq));
+      for (int ks = 0; ks < 2; ++ks) {
+        const bf16x8_t A = as_bf16x8(av[ks]);
 #pragma unroll
-      for (int nf = 0; nf < 8; ++nf) {
-        const uint4 bv = *reinterpret_cast<const uint4*>(&dt[(16 * nf + (lane & 15)) * PITCH + 32 * ks + kq]);
-        acc[nf] = mfma16(A, as_bf16x8(bv), acc[nf]);
+        for (int nf = 0; nf < 8; ++nf) {
+          const uint4 bv = *reinterpret_cast<const uint4*>(&dt[(16 * nf + (lane & 15)) * PITCH + 32 * ks + kq]);
+          acc[nf] = mfma16(A, as_bf16x8(bv), acc[nf]);
+        }
       }
     }
   }
@@ -1209,7 +1278,12 @@ __global__ __launch_bounds__(256) void mma_down_kernel(MmaArgs a) {
 
 hipError_t launch_mma_gateup(const MmaArgs& a, hipStream_t s) {
   if (a.n_wg <= 0 || a.n_tasks <= 0) return hipSuccess;
-  hipLaunchKernelGGL(mma_gateup_kernel, dim3(a.n_wg), dim3(256), 0, s, a);
+  if (a.gu_split == 4)
+    hipLaunchKernelGGL(mma_gateup_kernel<1>, dim3(a.n_wg), dim3(256), 0, s, a);
+  else if (a.gu_split == 1)
+    hipLaunchKernelGGL(mma_gateup_kernel<4>, dim3(a.n_wg), dim3(256), 0, s, a);
+  else
+    return hipErrorInvalidValue;
   return hipGetLastError();
 }
 
@@ -1432,6 +1506,29 @@ __global__ __launch_bounds__(64) void combine_final_kernel(CombineArgs a) {
   *reinterpret_cast<float4*>(a.y + static_cast<size_t>(t) * a.d + col) = y;
 }
 
+// One partial plane per slot (prefill path): the same sums in one pass,
+// straight from the partials (a first pass would only copy them).
+__global__ __launch_bounds__(64) void combine_direct_kernel(CombineArgs a) {
+  const int t = blockIdx.x;
+  const int col = blockIdx.y * 256 + threadIdx.x * 4;
+  if (col >= a.d) return;
+  float4 y = make_float4(0.f, 0.f, 0.f, 0.f);
+  for (int term = 0; term < a.K + a.n_shared; ++term) {
+    float4 v;
+    if (term < a.K) {
+      const int row = a.pos[t * a.K + term];
+      v = *reinterpret_cast<const float4*>(a.part + static_cast<size_t>(row) * a.d + col);
+      const float wk = a.w[t * a.K + term];
+      y = make_float4(fmaf(wk, v.x, y.x), fmaf(wk, v.y, y.y), fmaf(wk, v.z, y.z), fmaf(wk, v.w, y.w));
+    } else {
+      v = *reinterpret_cast<const float4*>(a.part_sh + static_cast<size_t>(term - a.K) * a.sh_plane +
+                                           static_cast<size_t>(t) * a.d + col);
+      y = f4add(y, v);
+    }
+  }
+  *reinterpret_cast<float4*>(a.y + static_cast<size_t>(t) * a.d + col) = y;
+}
+
 int combine_groups(int T, int K, int n_shared, int d, int n_planes) {
   const int slots = T * (K + n_shared);
   const int ncb = (d + 255) / 256;
@@ -1444,6 +1541,10 @@ int combine_groups(int T, int K, int n_shared, int d, int n_planes) {
 hipError_t launch_combine(const CombineArgs& a, hipStream_t s) {
   if (a.T <= 0) return hipSuccess;
   const int ncb = (a.d + 255) / 256;
+  if (a.n_planes == 1 && (a.n_shared == 0 || a.n_planes_sh == 1)) {
+    hipLaunchKernelGGL(combine_direct_kernel, dim3(a.T, ncb), dim3(64), 0, s, a);
+    return hipGetLastError();
+  }
   const int slots = a.T * (a.K + a.n_shared);
   hipLaunchKernelGGL(combine_planes_kernel, dim3(slots, ncb, a.pg), dim3(64 * kCombWaves), 0, s, a);
   hipError_t e = hipGetLastError();

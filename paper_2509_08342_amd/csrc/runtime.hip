@@ -748,12 +748,15 @@ ms_status prefill_experts(ms_ctx* ctx, int layer, const void* h_dev, int T, cons
     for (size_t i0 = 0; i0 < tasks.size(); i0 += msk::kMaxMmaTasks) {
       const size_t i1 = std::min(tasks.size(), i0 + msk::kMaxMmaTasks);
       ma.n_tasks = static_cast<int>(i1 - i0);
+      int tiles = 0;
+      for (size_t i = i0; i < i1; ++i) tiles += tasks[i].m_tiles * tasks[i].n_chunks;
+      ma.gu_split = tiles < msk::kGuSplitBelow ? 4 : 1;
       int wg = 0;
       uint64_t bytes = 0;
       for (size_t i = i0; i < i1; ++i) {
         ma.tasks[i - i0] = tasks[i];
         ma.tasks[i - i0].wg_begin = wg;
-        wg += tasks[i].m_tiles * (down ? ma.ncb : tasks[i].n_chunks);
+        wg += tasks[i].m_tiles * (down ? ma.ncb : tasks[i].n_chunks * ma.gu_split);
         bytes += (down ? dn_bytes : gu_bytes) * tasks[i].n_chunks;
       }
       ma.n_wg = wg;
