@@ -402,6 +402,8 @@ def run_stack(args):
     log("generating %s weights (%d distinct sets over %d layers)" % (shape.name, cfg["n_sets"], L))
     st = Stack(shape, seed=0, n_sets=cfg["n_sets"], max_tokens=max(T, P), budget_total=cfg["budget"],
                keep_f32=False)
+    if args.copy_engine == "dma":
+        ms.ms_set_copy_engine(st.ctx, ms.MS_COPY_DMA)
     r = cfg["r"]
     rs = [(0.25, 0.5, 0.75)[l % 3] for l in range(L)] if r == "mixed" else [r] * L
     slots = st.configure(rs, cfg["budget"])
@@ -521,6 +523,8 @@ def main():
                     help="stacks: per-layer budgets and split ratios from the cache configurator")
     ap.add_argument("--zeta", type=float, default=0.01)
     ap.add_argument("--ffn-splits", type=int, default=0, help="work-groups per chunk (0: the library's choice)")
+    ap.add_argument("--copy-engine", default="kernel", choices=["kernel", "dma"],
+                    help="host-to-device copies: the copy kernel (default) or the DMA engines where possible")
     ap.add_argument("--out", default=None)
     ap.add_argument("--cmd", nargs="*", default=[], help="the profiling command(s), recorded in the summary")
     args = ap.parse_args()
@@ -551,6 +555,8 @@ def main():
     log("generating %s weights and filling the pinned store" % shape.name)
     rig = SplitRig(shape, seed=0, max_tokens=T, budget_bytes=shape.n_experts * shape.expert_bytes,
                    keep_f32=not args.no_cpu_baseline, threads=16, ffn_splits=args.ffn_splits)
+    if args.copy_engine == "dma":
+        ms.ms_set_copy_engine(rig.ctx, ms.MS_COPY_DMA)
     n_tok = args.warmup + args.steps
     seq = synth.walk(shape, 0, n_tok, T=T)
     hs = [to_device(raw, shape.dtype) for raw, _ in seq]
@@ -592,13 +598,14 @@ def main():
 
     out = {
         "metric": METRIC,
-        "value": round(ms_step * 1e3, 1),
+        # the pass without timeline events; the instrumented pass gives the breakdown
+        "value": round(ms_plain * 1e3, 1),
         "unit": "us/layer",
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
-        "ms_per_step": round(ms_step, 4),
-        "ms_per_step_uninstrumented": round(ms_plain, 4),
+        "ms_per_step": round(ms_plain, 4),
+        "ms_per_step_instrumented": round(ms_step, 4),
         "step_us": an["step_us"],
         "higher_is_better": False,
         "scaling": "weak",
@@ -612,7 +619,7 @@ def main():
                    "d_model": shape.d_model, "d_ff": shape.d_ff, "n_experts": shape.n_experts,
                    "top_k": shape.top_k, "n_shared": shape.n_shared, "r": r, "tokens_per_step": T},
         "roofline": roof,
-        "tokens_per_s": round(T * 1e3 / ms_step, 2),
+        "tokens_per_s": round(T * 1e3 / ms_plain, 2),
         "h2d_gbps": None if an["h2d_gbps"] is None else round(an["h2d_gbps"], 2),
         "overlap": {"h2d_hidden_frac": an["hidden_frac"], "compute_hidden_frac": an["compute_hidden_frac"],
                     "eta": an["overlap_eta"], "copy_ms_per_step": an["copy_ms"] / args.steps,
@@ -648,8 +655,10 @@ def main():
         rig.load_tops(0, range(shape.n_experts))
         ms.ms_sync(rig.ctx)
         ms_ar, tl_ar, _ = run_steps(rig, hs, args.steps, args.warmup, ms.MS_FWD_PREDICT_NEXT, T=T)
+        ms_ar_plain, _, _ = run_steps(rig, hs, args.steps, args.warmup, ms.MS_FWD_PREDICT_NEXT, timeline=False, T=T)
         an_ar = analyse(tl_ar, args.steps, ms_ar)
-        out["all_resident"] = {"us_per_layer": round(ms_ar * 1e3, 1), "roofline": ffn_roofline(an_ar),
+        out["all_resident"] = {"us_per_layer": round(ms_ar_plain * 1e3, 1),
+                               "us_per_layer_instrumented": round(ms_ar * 1e3, 1), "roofline": ffn_roofline(an_ar),
                                "kernels": {k: {"launches": v["launches"],
                                                "avg_us": round(v["total_ms"] / v["launches"] * 1e3, 2)
                                                if v["launches"] else None}

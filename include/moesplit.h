@@ -349,6 +349,21 @@ typedef enum {
 } ms_cache_policy;
 ms_status ms_set_cache_policy(ms_ctx* ctx, int32_t policy, double rho, double omega, uint64_t seed);
 
+/* Engine of the host-to-device segment copies on the copy stream.
+ * MS_COPY_KERNEL (the default): a streaming kernel of a few work-groups that
+ * reads the pinned store over PCIe.  MS_COPY_DMA: the DMA engines
+ * (hipMemcpyAsync), which leave the compute units and their caches to the
+ * kernels that run beside the copy, except while the copy stream waits for
+ * unfinished work of another stream (a staging slot's previous reader, a
+ * layer's last forward): those copies still run as the kernel, ordered on
+ * the GPU (a DMA transfer queued behind such a wait can hold the host in the
+ * runtime's copy call).  Results do not depend on the engine. */
+typedef enum {
+  MS_COPY_KERNEL = 0,
+  MS_COPY_DMA = 1
+} ms_copy_engine;
+ms_status ms_set_copy_engine(ms_ctx* ctx, int32_t engine);
+
 /* Glue between stacked MoE layers (outside the layer; the residual stream
  * of a stack whose layers are MoE only, with a weightless RMSNorm):
  * out[t] = x / sqrt(mean(x^2) + 1e-6) with x = h[t] + y[t] in fp32.

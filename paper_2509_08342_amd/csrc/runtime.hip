@@ -316,6 +316,11 @@ struct ms_ctx {
   uint64_t pool_bytes = 0;
   hipStream_t copy = nullptr, side = nullptr;
   hipStream_t side2 = nullptr;  // prefill: every other missing expert's compute
+  // host-to-device copies: the copy kernel, or (MS_COPY_DMA) the DMA
+  // engines except while the copy stream waits on unfinished work of
+  // another stream (copy_waits)
+  int copy_engine = MS_COPY_KERNEL;
+  std::vector<hipEvent_t> copy_waits;
   // pinned host store
   std::vector<unsigned char*> blobs;      // pinned, coherent host memory (never cached by the GPU)
   std::vector<unsigned char*> blobs_dev;  // the same memory's device-side addresses
@@ -406,11 +411,39 @@ void tl_end(ms_ctx* ctx, int idx, hipStream_t st) {
 
 // ---- copies
 
-// H2D copy on the copy stream from a host blob (src_dev: its device-side
-// address), by the streaming copy kernel.
-ms_status issue_copy(ms_ctx* ctx, void* dst, const void* src_dev, uint64_t bytes, int kind, int layer) {
+// Order the copy stream after `ev`, recorded on another stream.  Finished
+// work needs no wait.  Unfinished work gets a stream wait, and until it has
+// finished the copies use the copy kernel: a DMA transfer queued behind such
+// a wait can hold the host inside the runtime's copy call for the length of
+// the awaited work.
+ms_status copy_after(ms_ctx* ctx, hipEvent_t ev) {
+  const hipError_t q = hipEventQuery(ev);
+  if (q == hipSuccess) return MS_OK;
+  if (q != hipErrorNotReady) MS_HIP(q);
+  MS_HIP(hipStreamWaitEvent(ctx->copy, ev, 0));
+  ctx->copy_waits.push_back(ev);
+  return MS_OK;
+}
+
+// Whether some wait queued by copy_after is still unfinished (an event
+// recorded again since then only reports later work, so the answer errs
+// towards the copy kernel).
+bool copy_waits_pending(ms_ctx* ctx) {
+  auto& w = ctx->copy_waits;
+  w.erase(std::remove_if(w.begin(), w.end(), [](hipEvent_t e) { return hipEventQuery(e) == hipSuccess; }), w.end());
+  return !w.empty();
+}
+
+// H2D copy on the copy stream from a host blob (src: its host address,
+// src_dev: its device-side address), by the streaming copy kernel, or in
+// MS_COPY_DMA mode by the DMA engines when nothing unfinished is awaited.
+ms_status issue_copy(ms_ctx* ctx, void* dst, const void* src, const void* src_dev, uint64_t bytes, int kind,
+                     int layer) {
   const int ti = tl_begin(ctx, ctx->copy, kind, layer, bytes);
-  MS_HIP(msk::launch_h2d(dst, src_dev, bytes, ctx->copy));
+  if (ctx->copy_engine == MS_COPY_DMA && !copy_waits_pending(ctx))
+    MS_HIP(hipMemcpyAsync(dst, src, bytes, hipMemcpyHostToDevice, ctx->copy));
+  else
+    MS_HIP(msk::launch_h2d(dst, src_dev, bytes, ctx->copy));
   tl_end(ctx, ti, ctx->copy);
   return MS_OK;
 }
@@ -420,9 +453,9 @@ ms_status issue_group(ms_ctx* ctx, int si, int gi, bool prefetch) {
   BufSlot& b = ctx->buf[si];
   Group& g = b.groups[gi];
   const uint64_t cb = ctx->s.chunk_bytes;
-  const unsigned char* src = ctx->blobs_dev[ctx->layers[b.layer].blob_of[b.expert]];
+  const int bi = ctx->layers[b.layer].blob_of[b.expert];
   const uint64_t off = cb * g.c_lo, bytes = cb * (g.c_hi - g.c_lo);
-  ms_status st = issue_copy(ctx, b.base + off, src + off, bytes,
+  ms_status st = issue_copy(ctx, b.base + off, ctx->blobs[bi] + off, ctx->blobs_dev[bi] + off, bytes,
                             prefetch ? MS_IV_COPY_PREFETCH : MS_IV_COPY_MISS, b.layer);
   if (st != MS_OK) return st;
   MS_HIP(hipEventRecord(b.gev[gi], ctx->copy));
@@ -451,7 +484,10 @@ hipError_t group_landed(ms_ctx* ctx, int si, int gi) {
 // copy stream first waits for the slot's previous readers.
 ms_status assign_slot(ms_ctx* ctx, int si, int layer, int e, int first) {
   BufSlot& b = ctx->buf[si];
-  if (b.has_last_read) MS_HIP(hipStreamWaitEvent(ctx->copy, b.last_read, 0));
+  if (b.has_last_read) {
+    const ms_status st = copy_after(ctx, b.last_read);
+    if (st != MS_OK) return st;
+  }
   b.layer = layer;
   b.expert = e;
   b.first_chunk = first;
@@ -1130,8 +1166,8 @@ ms_status ms_set_expert(ms_ctx* ctx, int32_t layer, int32_t e, const void* w_gat
     LayerState& L2 = ctx->layers[l];
     for (int e2 = 0; e2 < s.E; ++e2) {
       if (L2.blob_of[e2] != bi || L2.slot_of[e2] < 0) continue;
-      st = issue_copy(ctx, L2.cache_base + L2.top_bytes * L2.slot_of[e2], ctx->blobs_dev[bi], L2.top_bytes,
-                      MS_IV_COPY_TOP, l);
+      st = issue_copy(ctx, L2.cache_base + L2.top_bytes * L2.slot_of[e2], ctx->blobs[bi], ctx->blobs_dev[bi],
+                      L2.top_bytes, MS_IV_COPY_TOP, l);
       if (st != MS_OK) return st;
       hipEvent_t ev;
       MS_HIP(new_event(ctx, &ev));
@@ -1239,9 +1275,12 @@ ms_status ms_load_top(ms_ctx* ctx, int32_t layer, int32_t e) {
       break;
     }
   if (slot < 0) return fail(ctx, MS_E_BUDGET, "no free top-segment slot in this layer");
-  if (L.has_last_fwd) MS_HIP(hipStreamWaitEvent(ctx->copy, L.last_fwd, 0));
-  st = issue_copy(ctx, L.cache_base + L.top_bytes * slot, ctx->blobs_dev[L.blob_of[e]], L.top_bytes, MS_IV_COPY_TOP,
-                  layer);
+  if (L.has_last_fwd) {
+    st = copy_after(ctx, L.last_fwd);
+    if (st != MS_OK) return st;
+  }
+  st = issue_copy(ctx, L.cache_base + L.top_bytes * slot, ctx->blobs[L.blob_of[e]], ctx->blobs_dev[L.blob_of[e]],
+                  L.top_bytes, MS_IV_COPY_TOP, layer);
   if (st != MS_OK) return st;
   hipEvent_t ev;
   MS_HIP(new_event(ctx, &ev));
@@ -1949,6 +1988,13 @@ ms_status ms_set_cache_policy(ms_ctx* ctx, int32_t policy, double rho, double om
   ctx->rho = rho;
   ctx->omega = omega;
   ctx->rng = seed ^ 0x9e3779b97f4a7c15ull;
+  return MS_OK;
+}
+
+ms_status ms_set_copy_engine(ms_ctx* ctx, int32_t engine) {
+  MS_CHECK_CTX(ctx);
+  if (engine != MS_COPY_KERNEL && engine != MS_COPY_DMA) return fail(ctx, MS_E_INVALID, "unknown copy engine");
+  ctx->copy_engine = engine;
   return MS_OK;
 }
 

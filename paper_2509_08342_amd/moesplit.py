@@ -58,6 +58,7 @@ class ms_plan_problem(ctypes.Structure):
 
 
 MS_CACHE_STATIC, MS_CACHE_LCP, MS_CACHE_LRU, MS_CACHE_LFU, MS_CACHE_RND = range(5)
+MS_COPY_KERNEL, MS_COPY_DMA = range(2)
 
 
 class ms_interval(ctypes.Structure):
@@ -99,6 +100,7 @@ def _load():
         "ms_plan_solve": [ctypes.POINTER(ms_plan_problem), U64, ctypes.c_double, P, I32, P, P, P, P, P],
         "ms_cache_update": [P, P, P],
         "ms_set_cache_policy": [P, I32, ctypes.c_double, ctypes.c_double, U64],
+        "ms_set_copy_engine": [P, I32],
         "ms_timeline_begin": [P, P, I32],
         "ms_timeline_end": [P, ctypes.POINTER(ms_interval), I32, ctypes.POINTER(I32)],
     }
@@ -311,6 +313,10 @@ def ms_cache_update(ctx, budgets, r):
 
 def ms_set_cache_policy(ctx, policy, rho=0.25, omega=128.0, seed=0):
     _check(lib.ms_set_cache_policy(ctx, int(policy), float(rho), float(omega), int(seed)), ctx)
+
+
+def ms_set_copy_engine(ctx, engine):
+    _check(lib.ms_set_copy_engine(ctx, int(engine)), ctx)
 
 
 def ms_stats(ctx, layer):

@@ -133,6 +133,35 @@ def test_tiny_predict_next_and_prefetch_keep_outputs(rig):
     assert np.array_equal(y.cpu().numpy(), ref[0])
 
 
+def test_tiny_copy_engines_give_equal_outputs(rig):
+    """Segment copies by the copy kernel (default) and by the DMA engines
+    move the same bytes: same outputs bitwise and the same copy statistics,
+    over forwards with misses, prediction and prefetch."""
+    from paper_2509_08342_amd import moesplit as ms
+    steps = synth.walk(synth.TINY, 4, 10, T=3)
+    runs = []
+    for engine in (ms.MS_COPY_DMA, ms.MS_COPY_KERNEL):
+        ms.ms_set_copy_engine(rig.ctx, engine)
+        _setup(rig, 0.5, [1, 3])
+        ms.ms_drop_buffer(rig.ctx)
+        ms.ms_reset_stats(rig.ctx)
+        ys = []
+        for i, (raw, f) in enumerate(steps):
+            h = torch.from_numpy(raw).cuda()
+            y, idx, w = _run(rig, h, 3, ms.MS_FWD_PREDICT_NEXT if i % 2 else 0)
+            ys.append(y.cpu().numpy().copy())
+            if i == 4:
+                check_layer(rig, 0, f, y, idx, w)
+                ms.ms_drop_buffer(rig.ctx)
+        st = ms.ms_stats(rig.ctx, 0)
+        runs.append((ys, st["bytes_miss"], st["bytes_prefetch"]))
+    with pytest.raises(RuntimeError):
+        ms.ms_set_copy_engine(rig.ctx, 7)
+    assert all(np.array_equal(a, b) for a, b in zip(runs[0][0], runs[1][0]))
+    assert runs[0][1:] == runs[1][1:]
+    assert runs[0][1] > 0
+
+
 def test_tiny_zero_tokens_is_a_no_op(rig):
     _setup(rig, 0.5, [0])
     h, _ = rig.hidden(1)
