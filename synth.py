@@ -42,6 +42,7 @@ class ModelShape:
     d_ff_shared: int = 0
     renormalize: int = 1
     zipf: float = 0.0            # router-bias skew exponent (0 = none)
+    expert_bits: int = 0         # 0: experts in `dtype`; 2 or 4: affine codes (see QuantExpert)
 
     @property
     def elem_bytes(self) -> int:
@@ -49,6 +50,9 @@ class ModelShape:
 
     @property
     def expert_bytes(self) -> int:
+        if self.expert_bits:
+            # codes of three matrices plus one 4-byte (scale, zero) per group of 64
+            return 3 * self.d_model * self.d_ff * self.expert_bits // 8 + 3 * (self.d_model * self.d_ff // 64) * 4
         return 3 * self.d_model * self.d_ff * self.elem_bytes
 
 
@@ -61,7 +65,11 @@ DEEPSEEK = ModelShape("deepseek-v2-lite", 26, 2048, 1408, 64, 6, n_shared=2,
                       d_ff_shared=1408)
 QWEN3 = ModelShape("qwen3-30b-a3b", 48, 2048, 768, 128, 8, zipf=1.1)
 
-SHAPES = {s.name: s for s in (TINY, MIXTRAL, MIXTRAL_STACK, DEEPSEEK, QWEN3)}
+# The paper's Mixtral setting stores the MoE weights as 2-bit HQQ codes.
+MIXTRAL_Q2 = dataclasses.replace(MIXTRAL, name="mixtral-8x7b-q2", expert_bits=2)
+MIXTRAL_Q2_STACK = dataclasses.replace(MIXTRAL_Q2, name="mixtral-8x7b-q2-stack", n_layers=32)
+
+SHAPES = {s.name: s for s in (TINY, MIXTRAL, MIXTRAL_STACK, DEEPSEEK, QWEN3, MIXTRAL_Q2, MIXTRAL_Q2_STACK)}
 
 
 def _rng(seed: int, kind: int, layer: int, index: int) -> np.random.Generator:
@@ -129,6 +137,68 @@ def expert(shape: ModelShape, seed: int, layer: int, e: int, shared: bool = Fals
         raw.append(r)
         f32.append(x)
     return Expert(tuple(raw), tuple(f32))
+
+
+# ------------------------------------------------------ quantized storage --
+#
+# Experts stored as affine b-bit codes in the format of HQQ (half-quadratic
+# quantization), which the paper uses for its 2-bit Mixtral: each matrix is
+# taken as [out][in] (gate and up: [F][d]; down: [d][F]) and every group of
+# QGROUP consecutive elements along `in` has one scale and one zero, both
+# fp16, with w = (q - zero) * scale.  The synthetic weights are the same
+# N(0, 0.02) draws as the bf16 experts, quantized by round-to-nearest over
+# each group's [min, max] (HQQ's starting point; its zero-point refinement
+# changes values, not the format or the bytes moved).
+
+QGROUP = 64
+
+
+@dataclasses.dataclass
+class QuantExpert:
+    """codes: (gate [F][d/P], up [F][d/P], down [d][F/P]) uint8 with P = 8 /
+    bits codes per byte, element i of a row at bits (i % P) * bits of byte
+    i // P; meta: (gate [F][d/64][2], up [F][d/64][2], down [d][F/64][2])
+    uint16 fp16 bit patterns (scale, zero)."""
+    bits: int
+    codes: tuple
+    meta: tuple
+
+
+def pack_codes(q: np.ndarray, bits: int) -> np.ndarray:
+    """[rows][n] codes (0 .. 2^bits - 1) -> [rows][n * bits / 8] bytes."""
+    P = 8 // bits
+    q = np.asarray(q, np.uint8)
+    out = np.zeros((q.shape[0], q.shape[1] // P), np.uint8)
+    for j in range(P):
+        out |= (q[:, j::P] << (j * bits)).astype(np.uint8)
+    return out
+
+
+def quantize_rows(w: np.ndarray, bits: int):
+    """Round-to-nearest affine codes of w [rows][n] (n a multiple of 64):
+    returns (packed codes, meta [rows][n/64][2] uint16)."""
+    rows, n = w.shape
+    g = np.asarray(w, np.float32).reshape(rows, n // QGROUP, QGROUP)
+    lo, hi = g.min(axis=2), g.max(axis=2)
+    qmax = np.float32(2 ** bits - 1)
+    scale = ((hi - lo) / qmax).astype(np.float32)
+    scale[scale == 0] = 1.0
+    s16 = scale.astype(np.float16)
+    z16 = (-lo / s16.astype(np.float32)).astype(np.float16)
+    q = np.rint(g / s16.astype(np.float32)[:, :, None] + z16.astype(np.float32)[:, :, None])
+    q = np.clip(q, 0, qmax).astype(np.uint8).reshape(rows, n)
+    meta = np.stack([s16.view(np.uint16), z16.view(np.uint16)], axis=2)
+    return pack_codes(q, bits), np.ascontiguousarray(meta)
+
+
+def quant_expert(shape: ModelShape, seed: int, layer: int, e: int, bits: int) -> QuantExpert:
+    """Expert e of `layer` as b-bit codes (same draws as expert())."""
+    d, F = shape.d_model, shape.d_ff
+    wg = _normal(seed, KIND_GATE, layer, e, (d, F), WEIGHT_STD)
+    wu = _normal(seed, KIND_UP, layer, e, (d, F), WEIGHT_STD)
+    wd = _normal(seed, KIND_DOWN, layer, e, (F, d), WEIGHT_STD)
+    parts = [quantize_rows(np.ascontiguousarray(m), bits) for m in (wg.T, wu.T, wd.T)]
+    return QuantExpert(bits, tuple(p[0] for p in parts), tuple(p[1] for p in parts))
 
 
 def router(shape: ModelShape, seed: int, layer: int):
