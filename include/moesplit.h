@@ -66,7 +66,13 @@ typedef enum { MS_F32 = 0, MS_BF16 = 1 } ms_dtype;
  * the running layer, one for the next layer's prefetch).  ffn_splits is the
  * number of work-groups that share one 64-unit chunk of the FFN kernel (1, 2
  * or 4; 0 -> chosen from the shape so that a decode step fills the GPU).  It
- * changes the summation grouping, not what is computed. */
+ * changes the summation grouping, not what is computed.  expert_bits = 2 or
+ * 4 stores the routed experts as affine b-bit codes (the HQQ format of the
+ * paper's 2-bit Mixtral setting, Sec. 5.1; see ms_set_expert_q); 0 keeps
+ * them in the model dtype.  b-bit experts need dtype MS_BF16, no shared
+ * experts, d_ff a multiple of 64, d_model a multiple of 64 in [256, 8192] and
+ * ffn_splits 0 or 1 (MS_E_UNSUPPORTED otherwise); every token count runs on
+ * the chunk kernel (no matrix-core path). */
 typedef struct {
   int32_t n_layers;
   int32_t d_model;
@@ -80,11 +86,13 @@ typedef struct {
   int32_t max_tokens;
   int32_t n_buffer_slots;
   int32_t ffn_splits;
+  int32_t expert_bits;
 } ms_model_desc;
 
 /* Sizes the library derives from a model shape (pure host arithmetic). */
 typedef struct {
-  uint64_t chunk_bytes;       /* bytes of one 64-unit chunk: 3 * 64 * d * elem */
+  uint64_t chunk_bytes;       /* bytes of one 64-unit chunk: 3 * 64 * d * elem,
+                                 b-bit experts 24 * b * d + 12 * d             */
   int32_t n_chunks;           /* ceil(F / 64)                                  */
   uint64_t expert_bytes;      /* n_chunks * chunk_bytes (U_e, zero-padded)     */
   uint64_t fixed_pool_bytes;  /* device pool bytes needed besides top caches:
@@ -189,6 +197,21 @@ ms_status ms_set_router(ms_ctx* ctx, int32_t layer, const void* w_r, const float
  * segments, so later forwards use only the new weights. */
 ms_status ms_set_expert(ms_ctx* ctx, int32_t layer, int32_t e, const void* w_gate,
                         const void* w_up, const void* w_down);
+
+/* Expert e of layer i of a b-bit model (expert_bits = b): affine codes with
+ * one fp16 scale s and zero z per group of 64 consecutive elements along each
+ * matrix's input axis, w = (q - z) * s.  Matrices are [out][in]: gate and up
+ * [F][d] (W_gate = gate^T), down [d][F] (W_down = down^T).  gate_q, up_q:
+ * host [F][d * b / 8] bytes, down_q: host [d][F * b / 8] bytes, codes packed
+ * 8 / b per byte, element i of a row at bits (i % (8 / b)) * b of byte
+ * i / (8 / b); gate_m, up_m: host [F][d / 64][2], down_m: host [d][F / 64][2]
+ * uint16 fp16 bit patterns (scale, zero).  Repacked into the chunk order of
+ * the b-bit kernel in the pinned store (a top segment is still a prefix of
+ * the blob); rewrite semantics as ms_set_expert.  MS_E_STATE on a model
+ * whose experts are not b-bit (and ms_set_expert returns MS_E_STATE on one
+ * whose experts are). */
+ms_status ms_set_expert_q(ms_ctx* ctx, int32_t layer, int32_t e, const void* gate_q, const void* gate_m,
+                          const void* up_q, const void* up_m, const void* down_q, const void* down_m);
 
 /* Make expert (layer, e) use the host blob of (src_layer, src_e), which must
  * already be set.  Lets a deep stack reuse a few distinct weight sets. */

@@ -110,10 +110,31 @@ struct FfnArgs {
   int32_t subs;               // work-groups per chunk: 1, 2 or 4
   int32_t n_planes;           // routed partial planes: n_chunks * subs
   int32_t n_planes_sh;        // shared partial planes: n_chunks_sh * subs
+  int32_t bits;               // 0: chunks in the model dtype; 2 or 4: b-bit codes
+                              // (bf16 activations, routed experts, subs = 1)
   FfnTask tasks[kMaxTasks];
 };
 // Launches n_wg work-groups; max_tok bounds the tokens of any task.
 hipError_t launch_ffn(const FfnArgs& a, int max_tok, hipStream_t s);
+
+// Chunks of b-bit experts (FfnArgs::bits = 2 or 4): affine codes with one
+// fp16 scale s and zero z per group of 64 elements along each matrix's input
+// axis, w = (q - z) * s.  Per 64-unit chunk:
+//   Gq, Uq [64 units][d / 64 groups][8 b bytes]; Dq [d columns][8 b bytes]
+//   (the chunk's 64 units of one down column form one group);
+//   Gm, Um [64 units][d / 64] and Dm [d] words: fp16 scale | fp16 zero << 16.
+// Inside a group, 32-bit word m holds the codes of elements 2p and 2p + 1,
+// p = m * 16 / b + j, at bits j * b and 16 + j * b (j < 16 / b).
+inline uint64_t q_chunk_bytes(int d, int bits) {
+  return 3ull * kChunkUnits * d * bits / 8 + 12ull * d;
+}
+inline uint64_t q_off_uq(int d, int bits) { return 1ull * kChunkUnits * d * bits / 8; }
+inline uint64_t q_off_dq(int d, int bits) { return 2ull * kChunkUnits * d * bits / 8; }
+inline uint64_t q_off_gm(int d, int bits) { return 3ull * kChunkUnits * d * bits / 8; }
+inline uint64_t q_off_um(int d, int bits) { return q_off_gm(d, bits) + 4ull * d; }
+inline uint64_t q_off_dm(int d, int bits) { return q_off_gm(d, bits) + 8ull * d; }
+// Quantized chunks need d a multiple of 64 in [256, 8192].
+inline bool q_supported(int d) { return d % 64 == 0 && d >= 256 && d <= kMaxModelDim; }
 
 // Prefill (many tokens per expert) runs on the matrix cores in two steps:
 //  gate/up (mma_gateup): act[row][f] = bf16(silu(h_row . G_f) * (h_row . U_f))

@@ -1050,8 +1050,344 @@ static hipError_t launch_ffn_w(const FfnArgs& a, int max_tok, hipStream_t s) {
   }
 }
 
+// ---------------------------------------------------- SwiGLU FFN, b-bit codes
+//
+// One work-group per (task, chunk), all of the expert's tokens, NT at a time.
+// The dot products run on v_dot2_f32_bf16: a code pair becomes the bf16 pair
+// (1 + q0 / C, 1 + q1 / C), C = 2^b (the code in the top b bits of the
+// mantissa of 1.0), so that over one group
+//   sum_k q_k x_k = C (acc - xsum),  acc = sum_k (1 + q_k / C) x_k,
+// and the group's contribution is s (C acc - (C + z) xsum) with xsum the
+// group's sum of x.  x is the bf16 activation row in phase 1 and the bf16
+// rounding of the SwiGLU intermediate in phase 2.
+//   phase 1: lanes of a segment (LPU lanes, GPL groups each) cover the d/64
+//            groups of one unit; every lane keeps its groups of the token
+//            tile in registers and walks the units, B at a time, whose sums
+//            a transposing butterfly over the segment completes;
+//   phase 2: one down column per thread and step, the 64 intermediate values
+//            of the tile in registers; writes the fp32 partial row of plane c.
+
+constexpr uint32_t kBf16OnePair = 0x3F803F80u;
+
+__device__ __forceinline__ float dot2bf(uint32_t a, uint32_t b, float c) {
+  typedef __bf16 bf2_t __attribute__((ext_vector_type(2)));
+  return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf2_t, a), __builtin_bit_cast(bf2_t, b), c, false);
+}
+
+// Pair j of a code word as two bf16 values 1 + q / 2^BITS.
+template <int BITS, int J>
+__device__ __forceinline__ uint32_t code_pair(uint32_t w) {
+  constexpr int SH = (7 - BITS) - J * BITS;
+  constexpr uint32_t M = ((1u << BITS) - 1u) << (7 - BITS);
+  const uint32_t x = SH >= 0 ? (w << (SH >= 0 ? SH : 0)) : (w >> (SH < 0 ? -SH : 0));
+  return (x & (M | (M << 16))) | kBf16OnePair;
+}
+
+// acc[t] = sum over one group's code words (WPG words) of pair . x[t], for
+// the NT rows x[t] (32 bf16 pairs each); each pair is formed once and used
+// by every row.
+template <int BITS, int WPG, int NT>
+__device__ __forceinline__ void group_dot(const uint32_t (&cw)[WPG], const uint32_t (*x)[32], float (&acc)[NT]) {
+  constexpr int PPW = 16 / BITS;  // pairs per word
+#pragma unroll
+  for (int t = 0; t < NT; ++t) acc[t] = 0.0f;
+#pragma unroll
+  for (int m = 0; m < WPG; ++m) {
+    const uint32_t w = cw[m];
+#define MSK_QP(J)                                                                 \
+  if constexpr (J < PPW) {                                                        \
+    const uint32_t pr = code_pair<BITS, J>(w);                                    \
+    _Pragma("unroll") for (int t = 0; t < NT; ++t) acc[t] = dot2bf(pr, x[t][m * PPW + J], acc[t]); \
+  }
+    MSK_QP(0) MSK_QP(1) MSK_QP(2) MSK_QP(3) MSK_QP(4) MSK_QP(5) MSK_QP(6) MSK_QP(7)
+#undef MSK_QP
+  }
+}
+
+__device__ __forceinline__ float fp16_lo(uint32_t m) {
+  return static_cast<float>(__builtin_bit_cast(_Float16, static_cast<uint16_t>(m & 0xffffu)));
+}
+__device__ __forceinline__ float fp16_hi(uint32_t m) {
+  return static_cast<float>(__builtin_bit_cast(_Float16, static_cast<uint16_t>(m >> 16)));
+}
+
+__device__ __forceinline__ uint16_t f32_to_bf16_rne(float f) {
+  const uint32_t u = __float_as_uint(f);
+  return static_cast<uint16_t>((u + 0x7fffu + ((u >> 16) & 1u)) >> 16);
+}
+
+// B unit sums per lane -> one complete unit sum per lane: log2(B) halving
+// exchanges over the segment's top lane bits, then plain butterflies.  The
+// lane's unit is (lane & m1 ? B/2 : 0) + (lane & m2 ? 1 : 0) (B = 4) or
+// (lane & m1 ? 1 : 0) (B = 2).
+template <int LPU, int B>
+__device__ __forceinline__ float seg_reduce(const float (&v)[B], int li) {
+  static_assert(B == 2 || B == 4, "two or four units per batch");
+  static_assert(LPU >= B, "a segment needs a lane per unit of the batch");
+  constexpr int m1 = LPU / 2;
+  const bool h1 = (li & m1) != 0;
+  float r;
+  if constexpr (B == 4) {
+    constexpr int m2 = LPU / 4;
+    const float a0 = (h1 ? v[2] : v[0]) + __shfl_xor(h1 ? v[0] : v[2], m1, 64);
+    const float a1 = (h1 ? v[3] : v[1]) + __shfl_xor(h1 ? v[1] : v[3], m1, 64);
+    const bool h2 = (li & m2) != 0;
+    r = (h2 ? a1 : a0) + __shfl_xor(h2 ? a0 : a1, m2, 64);
+#pragma unroll
+    for (int m = LPU / 8; m >= 1; m >>= 1) r += __shfl_xor(r, m, 64);
+  } else {
+    r = (h1 ? v[1] : v[0]) + __shfl_xor(h1 ? v[0] : v[1], m1, 64);
+#pragma unroll
+    for (int m = LPU / 4; m >= 1; m >>= 1) r += __shfl_xor(r, m, 64);
+  }
+  return r;
+}
+
+template <int BITS, int LPU, int GPL, int NT, int B>
+struct QCfg {
+  static constexpr int SEG = 64 / LPU;                       // segments per wave
+  static constexpr int WAVES = (64 / (SEG * B)) < 4 ? (64 / (SEG * B)) : 4;
+  static constexpr int THREADS = 64 * WAVES;
+  static constexpr int PASSES = 64 / (WAVES * SEG * B);     // unit batches per lane
+  static constexpr int WPG = 2 * BITS;                      // code words per group (64 codes)
+  static constexpr int C = 1 << BITS;
+  static_assert(PASSES * WAVES * SEG * B == 64, "passes must tile the chunk's units");
+};
+
+template <int BITS, int LPU, int GPL, int NT, int B>
+__global__ __launch_bounds__((QCfg<BITS, LPU, GPL, NT, B>::THREADS)) __attribute__((amdgpu_waves_per_eu(2))) void ffn_q_kernel(FfnArgs a) {
+  using Q = QCfg<BITS, LPU, GPL, NT, B>;
+  constexpr int WPG = Q::WPG;
+  constexpr float C = static_cast<float>(Q::C);
+  __shared__ __align__(16) uint16_t act[NT][kChunkUnits];  // bf16 SwiGLU intermediate of the tile
+  const int d = a.d;
+  const int ngr = d / 64;  // groups per gate/up row
+  const int wg = blockIdx.x;
+  int ti = 0;
+  for (int i = 1; i < a.n_tasks; ++i)
+    if (a.tasks[i].wg_begin <= wg) ti = i;
+  const FfnTask tk = a.tasks[ti];
+  const int c = tk.chunk_lo + (wg - tk.wg_begin);
+  const int p0 = a.offsets[tk.expert];
+  const int n_tok = a.offsets[tk.expert + 1] - p0;
+  if (n_tok <= 0) return;
+
+  const unsigned char* chunk = tk.base + static_cast<size_t>(c) * a.chunk_bytes;
+  const size_t qrow = static_cast<size_t>(d) * BITS / 8;  // code bytes of one gate/up row
+  const uint4* Gq = reinterpret_cast<const uint4*>(chunk);
+  const uint4* Uq = reinterpret_cast<const uint4*>(chunk + 64 * qrow);
+  const uint4* Dq = reinterpret_cast<const uint4*>(chunk + 128 * qrow);
+  const uint32_t* Gm = reinterpret_cast<const uint32_t*>(chunk + 192 * qrow);
+  const uint32_t* Um = Gm + 64 * ngr;
+  const uint32_t* Dm = Gm + 128 * ngr;
+  const uint32_t* hsrc = static_cast<const uint32_t*>(a.h);  // bf16 pairs
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63, wave = tid >> 6;
+  const int sg = lane / LPU, li = lane % LPU;
+  constexpr int V4 = WPG / 4;  // uint4 loads per group
+
+  for (int tile = 0; tile < n_tok; tile += NT) {
+    const int nt = min(NT, n_tok - tile);
+    // ---- phase 1
+    {
+      uint32_t xh[GPL][NT][32];
+      float xs[GPL][NT];
+#pragma unroll
+      for (int t = 0; t < NT; ++t) {
+        const int tok = a.perm[p0 + tile + min(t, nt - 1)] / a.K;  // clamped: rows past nt are not stored
+#pragma unroll
+        for (int i = 0; i < GPL; ++i) {
+          const uint4* hp = reinterpret_cast<const uint4*>(hsrc + (static_cast<size_t>(tok) * d + (li + LPU * i) * 64) / 2);
+#pragma unroll
+          for (int v = 0; v < 8; ++v) {
+            const uint4 q = hp[v];
+            xh[i][t][4 * v] = q.x;
+            xh[i][t][4 * v + 1] = q.y;
+            xh[i][t][4 * v + 2] = q.z;
+            xh[i][t][4 * v + 3] = q.w;
+          }
+          float sum = 0.0f;
+#pragma unroll
+          for (int p = 0; p < 32; ++p) sum = dot2bf(xh[i][t][p], kBf16OnePair, sum);
+          xs[i][t] = sum;
+        }
+      }
+      // code words and metadata of a batch of B units, loaded one batch ahead
+      uint4 gcur[B][GPL][V4], ucur[B][GPL][V4], gnx[B][GPL][V4], unx[B][GPL][V4];
+      uint32_t gmc[B][GPL], umc[B][GPL], gmn[B][GPL], umn[B][GPL];
+      auto load_batch = [&](int pass, uint4(&g)[B][GPL][V4], uint4(&u)[B][GPL][V4], uint32_t(&gm)[B][GPL],
+                            uint32_t(&um)[B][GPL]) {
+        const int pc = min(pass, Q::PASSES - 1);  // clamped: the batch past the last is loaded, not used
+        const int ub = ((pc * Q::WAVES + wave) * Q::SEG + sg) * B;
+#pragma unroll
+        for (int j = 0; j < B; ++j)
+#pragma unroll
+          for (int i = 0; i < GPL; ++i) {
+            const size_t grp = static_cast<size_t>(ub + j) * ngr + li + LPU * i;
+#pragma unroll
+            for (int v = 0; v < V4; ++v) {
+              g[j][i][v] = ldw16(Gq + grp * V4 + v);
+              u[j][i][v] = ldw16(Uq + grp * V4 + v);
+            }
+            gm[j][i] = Gm[grp];
+            um[j][i] = Um[grp];
+          }
+      };
+      load_batch(0, gnx, unx, gmn, umn);
+      for (int pass = 0; pass < Q::PASSES; ++pass) {
+#pragma unroll
+        for (int j = 0; j < B; ++j)
+#pragma unroll
+          for (int i = 0; i < GPL; ++i) {
+#pragma unroll
+            for (int v = 0; v < V4; ++v) {
+              gcur[j][i][v] = gnx[j][i][v];
+              ucur[j][i][v] = unx[j][i][v];
+            }
+            gmc[j][i] = gmn[j][i];
+            umc[j][i] = umn[j][i];
+          }
+        load_batch(pass + 1, gnx, unx, gmn, umn);
+        const int ub = ((pass * Q::WAVES + wave) * Q::SEG + sg) * B;
+        float gv[NT][B], uv[NT][B];
+#pragma unroll
+        for (int j = 0; j < B; ++j) {
+#pragma unroll
+          for (int t = 0; t < NT; ++t) gv[t][j] = uv[t][j] = 0.0f;
+#pragma unroll
+          for (int i = 0; i < GPL; ++i) {
+            uint32_t gw[WPG], uw[WPG];
+#pragma unroll
+            for (int v = 0; v < V4; ++v) {
+              gw[4 * v] = gcur[j][i][v].x;
+              gw[4 * v + 1] = gcur[j][i][v].y;
+              gw[4 * v + 2] = gcur[j][i][v].z;
+              gw[4 * v + 3] = gcur[j][i][v].w;
+              uw[4 * v] = ucur[j][i][v].x;
+              uw[4 * v + 1] = ucur[j][i][v].y;
+              uw[4 * v + 2] = ucur[j][i][v].z;
+              uw[4 * v + 3] = ucur[j][i][v].w;
+            }
+            float ga[NT], ua[NT];
+            group_dot<BITS, WPG, NT>(gw, xh[i], ga);
+            group_dot<BITS, WPG, NT>(uw, xh[i], ua);
+            const float gs = fp16_lo(gmc[j][i]), gz = C + fp16_hi(gmc[j][i]);
+            const float us = fp16_lo(umc[j][i]), uz = C + fp16_hi(umc[j][i]);
+#pragma unroll
+            for (int t = 0; t < NT; ++t) {
+              gv[t][j] += gs * (C * ga[t] - gz * xs[i][t]);
+              uv[t][j] += us * (C * ua[t] - uz * xs[i][t]);
+            }
+          }
+        }
+#pragma unroll
+        for (int t = 0; t < NT; ++t) {
+          const float g = seg_reduce<LPU, B>(gv[t], li);
+          const float u = seg_reduce<LPU, B>(uv[t], li);
+          constexpr int WR = LPU / B;  // lanes holding the same unit after the reduction
+          if ((li % WR) == 0) {
+            const int j = li / WR;
+            act[t][ub + j] = f32_to_bf16_rne(silu(g) * u);
+          }
+        }
+      }
+    }
+    __syncthreads();
+    // ---- phase 2
+    {
+      uint32_t xa[NT][32];
+      float as[NT];
+#pragma unroll
+      for (int t = 0; t < NT; ++t) {
+        const uint4* ap = reinterpret_cast<const uint4*>(&act[t][0]);
+#pragma unroll
+        for (int v = 0; v < 8; ++v) {
+          const uint4 q = ap[v];
+          xa[t][4 * v] = q.x;
+          xa[t][4 * v + 1] = q.y;
+          xa[t][4 * v + 2] = q.z;
+          xa[t][4 * v + 3] = q.w;
+        }
+        float sum = 0.0f;
+#pragma unroll
+        for (int p = 0; p < 32; ++p) sum = dot2bf(xa[t][p], kBf16OnePair, sum);
+        as[t] = sum;
+      }
+      const int ncol = d / Q::THREADS;
+      uint4 dc[V4], dn[V4];
+      uint32_t dmc, dmn;
+      auto load_col = [&](int k, uint4(&dd)[V4], uint32_t& dm) {
+        const int col = tid + Q::THREADS * min(k, ncol - 1);  // clamped past the last column
+#pragma unroll
+        for (int v = 0; v < V4; ++v) dd[v] = ldw16(Dq + static_cast<size_t>(col) * V4 + v);
+        dm = Dm[col];
+      };
+      load_col(0, dn, dmn);
+      for (int k = 0; k < ncol; ++k) {
+#pragma unroll
+        for (int v = 0; v < V4; ++v) dc[v] = dn[v];
+        dmc = dmn;
+        load_col(k + 1, dn, dmn);
+        const int col = tid + Q::THREADS * k;
+        uint32_t dw[WPG];
+#pragma unroll
+        for (int v = 0; v < V4; ++v) {
+          dw[4 * v] = dc[v].x;
+          dw[4 * v + 1] = dc[v].y;
+          dw[4 * v + 2] = dc[v].z;
+          dw[4 * v + 3] = dc[v].w;
+        }
+        const float sc = fp16_lo(dmc), zc = C + fp16_hi(dmc);
+        float acc[NT];
+        group_dot<BITS, WPG, NT>(dw, xa, acc);
+#pragma unroll
+        for (int t = 0; t < NT; ++t) {
+          if (t < nt) {
+            const int row = p0 + tile + t;
+            a.part[(static_cast<size_t>(row) * a.n_planes + c) * d + col] = sc * (C * acc[t] - zc * as[t]);
+          }
+        }
+      }
+    }
+    __syncthreads();
+  }
+}
+
+// One token per tile: the pairs of a second token's dot products would
+// need more registers than the work-group keeps (decode tiles hold one or
+// two tokens per expert; more tokens loop over the tile).
+template <int BITS, int LPU, int GPL, int B>
+static hipError_t launch_ffn_q_one(const FfnArgs& a, hipStream_t s) {
+  hipLaunchKernelGGL((ffn_q_kernel<BITS, LPU, GPL, 1, B>), dim3(a.n_wg), dim3(QCfg<BITS, LPU, GPL, 1, B>::THREADS), 0,
+                     s, a);
+  return hipGetLastError();
+}
+
+template <int BITS>
+static hipError_t launch_ffn_q_bits(const FfnArgs& a, hipStream_t s) {
+  constexpr int B = BITS == 2 ? 4 : 2;  // units per lane and batch: code registers in flight
+  switch (a.d / 64) {
+    case 4: return launch_ffn_q_one<BITS, 4, 1, B>(a, s);
+    case 8: return launch_ffn_q_one<BITS, 8, 1, B>(a, s);
+    case 16: return launch_ffn_q_one<BITS, 16, 1, B>(a, s);
+    case 32: return launch_ffn_q_one<BITS, 32, 1, B>(a, s);
+    case 64: return launch_ffn_q_one<BITS, 64, 1, B>(a, s);
+    case 128: return launch_ffn_q_one<BITS, 64, 2, B>(a, s);
+    default: return hipErrorInvalidValue;
+  }
+}
+
 hipError_t launch_ffn(const FfnArgs& a, int max_tok, hipStream_t s) {
   if (a.n_wg <= 0 || a.n_tasks <= 0) return hipSuccess;
+  if (a.bits != 0) {
+    if (a.dtype != kBF16 || a.subs != 1 || !q_supported(a.d)) return hipErrorInvalidValue;
+    for (int i = 0; i < a.n_tasks; ++i)
+      if (a.tasks[i].expert < 0) return hipErrorInvalidValue;  // shared experts stay in the model dtype
+    if (a.bits == 2) return launch_ffn_q_bits<2>(a, s);
+    if (a.bits == 4) return launch_ffn_q_bits<4>(a, s);
+    return hipErrorInvalidValue;
+  }
   return (a.dtype == kBF16) ? launch_ffn_w<uint16_t>(a, max_tok, s) : launch_ffn_w<float>(a, max_tok, s);
 }
 

@@ -11,6 +11,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <functional>
 #include <cmath>
 #include <cstdio>
 #include <cstring>
@@ -37,6 +38,7 @@ uint64_t align_up(uint64_t x, uint64_t a) { return (x + a - 1) / a * a; }
 struct Shape {
   int L, d, F, E, K, n_sh, F_sh, dtype, renorm, max_T, n_buf, subs;
   int elem;
+  int bits;  // 0: routed experts in the model dtype; 2 or 4: b-bit codes
   uint64_t chunk_bytes;
   int n_chunks, n_chunks_sh;
   uint64_t expert_bytes, shared_bytes;
@@ -86,7 +88,20 @@ ms_status derive_shape(const ms_model_desc* d, Shape* s, std::string* err) {
   s->max_T = d->max_tokens;
   s->n_buf = d->n_buffer_slots > 0 ? d->n_buffer_slots : 2 * d->top_k;
   s->elem = d->dtype == MS_BF16 ? 2 : 4;
-  s->chunk_bytes = 3ull * kUnits * s->d * s->elem;
+  s->bits = d->expert_bits;
+  if (s->bits != 0) {
+    if (s->bits != 2 && s->bits != 4) {
+      *err = "expert_bits must be 0, 2 or 4";
+      return MS_E_INVALID;
+    }
+    if (d->dtype != MS_BF16 || d->n_shared != 0 || d->d_ff % kUnits != 0 || !msk::q_supported(d->d_model) ||
+        d->ffn_splits > 1) {
+      *err = "b-bit experts need bf16 activations, no shared experts, d_ff a multiple of 64, "
+             "d_model a multiple of 64 in [256, 8192] and one work-group per chunk";
+      return MS_E_UNSUPPORTED;
+    }
+  }
+  s->chunk_bytes = s->bits ? msk::q_chunk_bytes(s->d, s->bits) : 3ull * kUnits * s->d * s->elem;
   s->n_chunks = (s->F + kUnits - 1) / kUnits;
   s->n_chunks_sh = (s->F_sh + kUnits - 1) / kUnits;
   s->expert_bytes = s->chunk_bytes * s->n_chunks;
@@ -102,7 +117,9 @@ ms_status derive_shape(const ms_model_desc* d, Shape* s, std::string* err) {
     *err = "ffn_splits too large for this d_model and dtype";
     return MS_E_UNSUPPORTED;
   }
-  if (d->ffn_splits > 0) {
+  if (s->bits != 0) {
+    s->subs = 1;  // the b-bit kernel takes a whole chunk per work-group
+  } else if (d->ffn_splits > 0) {
     s->subs = d->ffn_splits;
   } else {
     const int64_t active = std::min<int64_t>(s->E, static_cast<int64_t>(s->max_T) * s->K) + s->n_sh;
@@ -151,7 +168,7 @@ ms_status derive_shape(const ms_model_desc* d, Shape* s, std::string* err) {
   // slot and per shared expert and token
   s->off_act = off;
   s->off_act_sh = off;
-  if (s->dtype == MS_BF16) {
+  if (s->dtype == MS_BF16 && s->bits == 0) {
     off += align_up(TK * s->n_chunks * kUnits * 2, kAlign);
     s->off_act_sh = off;
     off += align_up(static_cast<uint64_t>(s->n_sh) * s->max_T * s->n_chunks_sh * kUnits * 2, kAlign);
@@ -234,6 +251,74 @@ void pack_expert(const void* wg, const void* wu, const void* wd, int d, int F, i
   else
     pack_expert_t(static_cast<const float*>(wg), static_cast<const float*>(wu),
                   static_cast<const float*>(wd), d, F, n_chunks, static_cast<float*>(dst));
+}
+
+// Pack one b-bit expert (gate_q, up_q [F][d b/8] and down_q [d][F b/8]
+// codes, element i of a row at bits (i % (8/b)) b of byte i / (8/b); meta
+// [rows][in/64][2] fp16 (scale, zero)) into the chunk order of the b-bit
+// kernel: per chunk Gq, Uq, Dq, Gm, Um, Dm (msk::q_chunk_bytes), each
+// group's 64 codes as 2b words of code pairs (elements 2p, 2p + 1 at bits
+// j b and 16 + j b of word p / (16 / b), j = p % (16 / b)).
+void pack_group_pairs(const uint8_t* row, int first, int bits, uint32_t* out) {
+  const int per = 8 / bits, ppw = 16 / bits, words = 2 * bits;
+  const unsigned mask = (1u << bits) - 1u;
+  auto code = [&](int i) { return (static_cast<unsigned>(row[(first + i) / per]) >> (((first + i) % per) * bits)) & mask; };
+  for (int m = 0; m < words; ++m) {
+    uint32_t w = 0;
+    for (int j = 0; j < ppw; ++j) {
+      const int p = m * ppw + j;
+      w |= code(2 * p) << (j * bits);
+      w |= code(2 * p + 1) << (16 + j * bits);
+    }
+    out[m] = w;
+  }
+}
+
+void pack_expert_q(const uint8_t* gq, const uint16_t* gm, const uint8_t* uq, const uint16_t* um, const uint8_t* dq,
+                   const uint16_t* dm, int d, int F, int bits, uint8_t* dst) {
+  const int n_chunks = F / kUnits, ngr = d / 64, ngr_f = F / 64;
+  const size_t qrow_in = static_cast<size_t>(d) * bits / 8;   // bytes of one gate/up code row
+  const size_t drow_in = static_cast<size_t>(F) * bits / 8;   // bytes of one down code row
+  const size_t gbytes = 8ull * bits;                          // bytes of one group's codes
+  const uint64_t cb = msk::q_chunk_bytes(d, bits);
+  auto work = [&](int c0, int c1) {
+    for (int c = c0; c < c1; ++c) {
+      uint8_t* base = dst + cb * c;
+      uint32_t* Gq = reinterpret_cast<uint32_t*>(base);
+      uint32_t* Uq = reinterpret_cast<uint32_t*>(base + msk::q_off_uq(d, bits));
+      uint32_t* Dq = reinterpret_cast<uint32_t*>(base + msk::q_off_dq(d, bits));
+      uint32_t* Gm = reinterpret_cast<uint32_t*>(base + msk::q_off_gm(d, bits));
+      uint32_t* Um = reinterpret_cast<uint32_t*>(base + msk::q_off_um(d, bits));
+      uint32_t* Dm = reinterpret_cast<uint32_t*>(base + msk::q_off_dm(d, bits));
+      for (int u = 0; u < kUnits; ++u) {
+        const size_t f = static_cast<size_t>(c) * kUnits + u;
+        for (int g = 0; g < ngr; ++g) {
+          const size_t grp = static_cast<size_t>(u) * ngr + g;
+          pack_group_pairs(gq + f * qrow_in, g * 64, bits, Gq + grp * gbytes / 4);
+          pack_group_pairs(uq + f * qrow_in, g * 64, bits, Uq + grp * gbytes / 4);
+          Gm[grp] = gm[(f * ngr + g) * 2] | static_cast<uint32_t>(gm[(f * ngr + g) * 2 + 1]) << 16;
+          Um[grp] = um[(f * ngr + g) * 2] | static_cast<uint32_t>(um[(f * ngr + g) * 2 + 1]) << 16;
+        }
+      }
+      for (int col = 0; col < d; ++col) {
+        pack_group_pairs(dq + static_cast<size_t>(col) * drow_in, c * kUnits, bits, Dq + col * gbytes / 4);
+        const size_t mi = (static_cast<size_t>(col) * ngr_f + c) * 2;
+        Dm[col] = dm[mi] | static_cast<uint32_t>(dm[mi + 1]) << 16;
+      }
+    }
+  };
+  const int n_threads = std::max(1, std::min<int>(16, static_cast<int>(std::thread::hardware_concurrency())));
+  if (n_chunks < 4 || n_threads == 1) {
+    work(0, n_chunks);
+    return;
+  }
+  std::vector<std::thread> th;
+  const int per = (n_chunks + n_threads - 1) / n_threads;
+  for (int i = 0; i < n_threads; ++i) {
+    const int c0 = i * per, c1 = std::min(n_chunks, c0 + per);
+    if (c0 < c1) th.emplace_back(work, c0, c1);
+  }
+  for (auto& t : th) t.join();
 }
 
 struct Group {
@@ -1112,14 +1197,13 @@ ms_status ms_set_router(ms_ctx* ctx, int32_t layer, const void* w_r, const float
   return MS_OK;
 }
 
-ms_status ms_set_expert(ms_ctx* ctx, int32_t layer, int32_t e, const void* w_gate, const void* w_up,
-                        const void* w_down) {
-  MS_CHECK_CTX(ctx);
-  ms_status st = check_layer(ctx, layer);
-  if (st != MS_OK) return st;
+// Write expert (layer, e)'s host blob with `pack` (called with the blob),
+// allocating it unless the expert owns one alone; then drop staged copies of
+// the old contents and copy cached top segments again.
+static ms_status write_expert_blob(ms_ctx* ctx, int32_t layer, int32_t e,
+                                   const std::function<void(unsigned char*)>& pack) {
+  ms_status st = MS_OK;
   const Shape& s = ctx->s;
-  if (e < 0 || e >= s.E) return fail(ctx, MS_E_INVALID, "expert out of range");
-  if (!w_gate || !w_up || !w_down) return fail(ctx, MS_E_INVALID, "weight pointer is NULL");
   LayerState& L = ctx->layers[layer];
   int bi = L.blob_of[e];
   // reuse the blob only if no other (layer, expert) aliases it
@@ -1154,7 +1238,7 @@ ms_status ms_set_expert(ms_ctx* ctx, int32_t layer, int32_t e, const void* w_gat
   // the blob may be read by work in flight: drain it before rewriting
   st = ms_sync(ctx);
   if (st != MS_OK) return st;
-  pack_expert(w_gate, w_up, w_down, s.d, s.F, s.n_chunks, s.elem, ctx->blobs[bi]);
+  pack(ctx->blobs[bi]);
   L.blob_of[e] = bi;
   // copies of the old weights: staging slots are dropped (with any queued
   // prefetch), cached top segments are copied again
@@ -1176,6 +1260,37 @@ ms_status ms_set_expert(ms_ctx* ctx, int32_t layer, int32_t e, const void* w_gat
     }
   }
   return MS_OK;
+}
+
+ms_status ms_set_expert(ms_ctx* ctx, int32_t layer, int32_t e, const void* w_gate, const void* w_up,
+                        const void* w_down) {
+  MS_CHECK_CTX(ctx);
+  ms_status st = check_layer(ctx, layer);
+  if (st != MS_OK) return st;
+  const Shape& s = ctx->s;
+  if (e < 0 || e >= s.E) return fail(ctx, MS_E_INVALID, "expert out of range");
+  if (!w_gate || !w_up || !w_down) return fail(ctx, MS_E_INVALID, "weight pointer is NULL");
+  if (s.bits != 0) return fail(ctx, MS_E_STATE, "this model's experts are b-bit codes (ms_set_expert_q)");
+  return write_expert_blob(ctx, layer, e, [&](unsigned char* blob) {
+    pack_expert(w_gate, w_up, w_down, s.d, s.F, s.n_chunks, s.elem, blob);
+  });
+}
+
+ms_status ms_set_expert_q(ms_ctx* ctx, int32_t layer, int32_t e, const void* gate_q, const void* gate_m,
+                          const void* up_q, const void* up_m, const void* down_q, const void* down_m) {
+  MS_CHECK_CTX(ctx);
+  ms_status st = check_layer(ctx, layer);
+  if (st != MS_OK) return st;
+  const Shape& s = ctx->s;
+  if (e < 0 || e >= s.E) return fail(ctx, MS_E_INVALID, "expert out of range");
+  if (!gate_q || !gate_m || !up_q || !up_m || !down_q || !down_m)
+    return fail(ctx, MS_E_INVALID, "code or metadata pointer is NULL");
+  if (s.bits == 0) return fail(ctx, MS_E_STATE, "this model's experts are not b-bit codes (ms_set_expert)");
+  return write_expert_blob(ctx, layer, e, [&](unsigned char* blob) {
+    pack_expert_q(static_cast<const uint8_t*>(gate_q), static_cast<const uint16_t*>(gate_m),
+                  static_cast<const uint8_t*>(up_q), static_cast<const uint16_t*>(up_m),
+                  static_cast<const uint8_t*>(down_q), static_cast<const uint16_t*>(down_m), s.d, s.F, s.bits, blob);
+  });
 }
 
 ms_status ms_alias_expert(ms_ctx* ctx, int32_t layer, int32_t e, int32_t src_layer, int32_t src_e) {
@@ -1473,7 +1588,7 @@ ms_status ms_forward(ms_ctx* ctx, int32_t layer, const void* h_dev, int32_t T, f
   // or prefill path (matrix cores, launched once the token counts are known)
   bool prefill = s.dtype == MS_BF16 && static_cast<int64_t>(T) * s.K >= 8ll * s.E;
   if (flags & MS_FWD_MATRIX_CORES) prefill = s.dtype == MS_BF16;
-  if (flags & MS_FWD_NO_MATRIX_CORES) prefill = false;
+  if ((flags & MS_FWD_NO_MATRIX_CORES) || s.bits != 0) prefill = false;  // b-bit experts: chunk kernel only
 
   // 2. segments already in VRAM (Eq. (5): processed while missing ones
   //    load): cached tops, staging-buffer groups of this layer whose copies
@@ -1496,6 +1611,7 @@ ms_status ms_forward(ms_ctx* ctx, int32_t layer, const void* h_dev, int32_t T, f
   fa.subs = s.subs;
   fa.n_planes = s.n_chunks * s.subs;
   fa.n_planes_sh = s.n_chunks_sh * s.subs;
+  fa.bits = s.bits;
   std::vector<msk::FfnTask> res_tasks;
   for (int e = 0; e < s.E && !prefill; ++e) {
     const int rc = resident_chunks(L, e);

@@ -31,7 +31,7 @@ INTERVAL_NAMES = ["router", "group", "ffn_resident", "ffn_streamed", "combine",
 class ms_model_desc(ctypes.Structure):
     _fields_ = [(n, ctypes.c_int32) for n in (
         "n_layers", "d_model", "d_ff", "n_experts", "top_k", "n_shared", "d_ff_shared",
-        "dtype", "renormalize", "max_tokens", "n_buffer_slots", "ffn_splits")]
+        "dtype", "renormalize", "max_tokens", "n_buffer_slots", "ffn_splits", "expert_bits")]
 
 
 class ms_sizes(ctypes.Structure):
@@ -80,6 +80,7 @@ def _load():
         "ms_create": [ctypes.POINTER(ms_model_desc), P, U64, I32, ctypes.POINTER(P)],
         "ms_set_router": [P, I32, P, P],
         "ms_set_expert": [P, I32, I32, P, P, P],
+        "ms_set_expert_q": [P, I32, I32, P, P, P, P, P, P],
         "ms_alias_expert": [P, I32, I32, I32, I32],
         "ms_set_shared_expert": [P, I32, I32, P, P, P],
         "ms_configure": [P, P, P, P],
@@ -152,7 +153,7 @@ def model_desc(shape, max_tokens, n_buffer_slots=0, ffn_splits=0):
     return ms_model_desc(shape.n_layers, shape.d_model, shape.d_ff, shape.n_experts, shape.top_k,
                          shape.n_shared, shape.d_ff_shared,
                          MS_BF16 if shape.dtype == "bf16" else MS_F32, shape.renormalize,
-                         max_tokens, n_buffer_slots, ffn_splits)
+                         max_tokens, n_buffer_slots, ffn_splits, getattr(shape, "expert_bits", 0))
 
 
 def _check(st, ctx=None, what=""):
@@ -200,6 +201,15 @@ def ms_set_router(ctx, layer, w_r, bias=None):
 def ms_set_expert(ctx, layer, e, w_gate, w_up, w_down):
     arrs = [np.ascontiguousarray(a) for a in (w_gate, w_up, w_down)]
     _check(lib.ms_set_expert(ctx, layer, e, *[_ptr(a) for a in arrs]), ctx)
+
+
+def ms_set_expert_q(ctx, layer, e, codes, meta):
+    """codes: (gate [F][d*b/8], up [F][d*b/8], down [d][F*b/8]) uint8;
+    meta: (gate [F][d/64][2], up, down [d][F/64][2]) uint16 fp16 patterns."""
+    cs = [np.ascontiguousarray(a, np.uint8) for a in codes]
+    ms_ = [np.ascontiguousarray(a, np.uint16) for a in meta]
+    _check(lib.ms_set_expert_q(ctx, layer, e, _ptr(cs[0]), _ptr(ms_[0]), _ptr(cs[1]), _ptr(ms_[1]),
+                               _ptr(cs[2]), _ptr(ms_[2])), ctx)
 
 
 def ms_alias_expert(ctx, layer, e, src_layer, src_e):

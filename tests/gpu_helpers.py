@@ -19,8 +19,24 @@ def check_close(gpu, ref, dtype, what="y"):
     return err / max(m, 1e-30)
 
 
+def quant_weights(rig, layer):
+    """fp64 dequantized experts of a b-bit rig's layer (cached on the rig)."""
+    from oracle import quant
+    cache = rig.__dict__.setdefault("_deq", {})
+    key = layer % rig.n_sets
+    if key not in cache:
+        s = rig.shape
+        cache[key] = [quant.expert_weights(q.codes, q.meta, q.bits, s.d_model, s.d_ff)
+                      for q in rig.layer_experts(layer)]
+    return cache[key]
+
+
 def oracle_layer(rig, layer, h_f32, tokens=None):
     s = rig.shape
+    if getattr(s, "expert_bits", 0):
+        from oracle import quant
+        return quant.moe_layer(h_f32, rig.routers[layer], quant_weights(rig, layer), s.top_k,
+                               renormalize=s.renormalize, bias=rig.biases[layer], tokens=tokens)
     return oracle.moe_layer(h_f32, rig.routers[layer], rig.layer_experts(layer), s.top_k,
                             renormalize=s.renormalize, bias=rig.biases[layer],
                             shared=rig.shared[layer], tokens=tokens)

@@ -96,3 +96,36 @@ def test_invalid_arguments():
     with pytest.raises(ms.MoeSplitError) as ei:
         ms.ms_split_plan(_desc(synth.TINY), 0, 1.5)
     assert ei.value.status == ms.MS_E_INVALID
+
+
+@pytest.mark.parametrize("bits", [2, 4])
+def test_sizes_of_b_bit_experts(bits):
+    """Per chunk: three 64 x d code blocks of b bits plus one 4-byte (scale,
+    zero) per group of 64 elements of each matrix (12 d bytes); the expert
+    is the whole blob, and a top segment a whole number of chunks."""
+    import dataclasses
+    ms = _ms()
+    shape = dataclasses.replace(synth.MIXTRAL, expert_bits=bits)
+    s = ms.ms_query_sizes(_desc(shape))
+    d = shape.d_model
+    assert s.chunk_bytes == 3 * 64 * d * bits // 8 + 12 * d
+    assert s.expert_bytes == s.n_chunks * s.chunk_bytes == shape.expert_bytes
+    units, tb, c = ms.ms_split_plan(_desc(shape), 12 * (1 << 30) // 32, 0.5)
+    assert units == 7168 and tb == 112 * s.chunk_bytes and c == min(8, (12 * (1 << 30) // 32) // tb)
+
+
+def test_b_bit_experts_reject_unsupported_shapes():
+    import dataclasses
+    ms = _ms()
+    q = dataclasses.replace(synth.MIXTRAL, expert_bits=2)
+    for change, status in ((dict(expert_bits=3), ms.MS_E_INVALID), (dict(dtype="f32"), ms.MS_E_UNSUPPORTED),
+                           (dict(d_ff=14300), ms.MS_E_UNSUPPORTED), (dict(d_model=128), ms.MS_E_UNSUPPORTED),
+                           (dict(n_shared=1, d_ff_shared=128), ms.MS_E_UNSUPPORTED)):
+        with pytest.raises(ms.MoeSplitError) as ei:
+            ms.ms_query_sizes(_desc(dataclasses.replace(q, **change)))
+        assert ei.value.status == status, change
+    desc = _desc(q)
+    desc.ffn_splits = 2
+    with pytest.raises(ms.MoeSplitError) as ei:
+        ms.ms_query_sizes(desc)
+    assert ei.value.status == ms.MS_E_UNSUPPORTED

@@ -60,16 +60,26 @@ class SplitRig:
             self.routers.append(f32)
             self.biases.append(bias)
 
+        bits = getattr(shape, "expert_bits", 0)
+
         def gen(args):
             s, e = args
+            if bits:
+                return s, e, synth.quant_expert(shape, seed, s, e, bits)
             return s, e, synth.expert(shape, seed, s, e)
 
         jobs = [(s, e) for s in range(self.n_sets) for e in range(shape.n_experts)]
         with ThreadPoolExecutor(threads) as pool:
             for s, e, ex in pool.map(gen, jobs):
-                ms.ms_set_expert(self.ctx, s, e, *ex.raw)
-                if keep_f32:
-                    self.experts.setdefault(s, [None] * shape.n_experts)[e] = ex.f32
+                if bits:
+                    # b-bit experts: the oracle gets the same codes and metadata
+                    ms.ms_set_expert_q(self.ctx, s, e, ex.codes, ex.meta)
+                    if keep_f32:
+                        self.experts.setdefault(s, [None] * shape.n_experts)[e] = ex
+                else:
+                    ms.ms_set_expert(self.ctx, s, e, *ex.raw)
+                    if keep_f32:
+                        self.experts.setdefault(s, [None] * shape.n_experts)[e] = ex.f32
                 del ex
         for l in range(self.n_sets, L):
             for e in range(shape.n_experts):
