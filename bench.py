@@ -80,6 +80,9 @@ def _workloads():
         # Mixtral-8x7B-shaped layer, decode batch 1, r = .5, tops of experts 0-3
         "mixtral-decode": dict(shape=synth.MIXTRAL, T=1, r=0.5, budget=lambda tb: 4 * tb,
                                tops=lambda rig: [0, 1, 2, 3]),
+        # the same layer with 2-bit expert codes (the paper's HQQ Mixtral setting)
+        "mixtral-q2-decode": dict(shape=synth.MIXTRAL_Q2, T=1, r=0.5, budget=lambda tb: 4 * tb,
+                                  tops=lambda rig: [0, 1, 2, 3]),
         # DeepSeek-V2-Lite-shaped layer: 4 GiB over 26 layers at r = .5 (19 tops)
         "deepseek-decode": dict(shape=ds1, T=1, r=0.5, budget=lambda tb: (4 * GIB) // 26,
                                 tops=lambda rig: list(range(19))),
@@ -104,6 +107,10 @@ def _stacks():
                               t_moe_us=208.0),
         "mixtral-stack-mixed": dict(shape=synth.MIXTRAL_STACK, budget=12 * GIB, r="mixed", prefill=0, T=1,
                                     n_sets=4, t_moe_us=208.0),
+        # 2-bit expert codes (the paper's HQQ Mixtral): 2 GiB keeps two tops
+        # per layer at r = .5, as 12 GiB does for the bf16 stack
+        "mixtral-q2-stack": dict(shape=synth.MIXTRAL_Q2_STACK, budget=2 * GIB, r=0.5, prefill=0, T=1, n_sets=4,
+                                 t_moe_us=70.0),
         "deepseek-stack": dict(shape=synth.DEEPSEEK, budget=4 * GIB, r=0.5, prefill=512, T=1, n_sets=4,
                                t_moe_us=117.0),
         "qwen-stack": dict(shape=synth.QWEN3, budget=8 * GIB, r=0.5, prefill=2048, T=16, n_sets=4,
@@ -262,6 +269,40 @@ def h2d_link_peak_gbps():
     return n / (ms_ * 1e-3) / 1e9
 
 
+def cpu_baseline_q(rig, hf_list, budget_s):
+    """The b-bit oracle, one thread: routing of each batch, then each row's
+    selected experts over the first eighth of their units (dequantizing only
+    those), scaled by eight; as many batches as fit in about budget_s."""
+    import oracle
+    from oracle import quant
+    s = rig.shape
+    frac = 8
+    hi = (s.d_ff // frac) // 64 * 64
+    T = hf_list[0].shape[0]
+    rows = list(range(min(T, 16)))
+    experts = rig.layer_experts(0)
+    t0 = time.perf_counter()
+    n = 0
+    for hf in hf_list:
+        logits = oracle.router_logits(hf, rig.routers[0], rig.biases[0])
+        idx = oracle.topk(logits, s.top_k)
+        w = oracle.gate_weights(logits, idx, s.renormalize)
+        for t in rows:
+            y = np.zeros(s.d_model)
+            for k in range(s.top_k):
+                q = experts[int(idx[t, k])]
+                y += w[t, k] * quant.expert_range(hf[t], q.codes, q.meta, q.bits, s.d_model, s.d_ff, 0, hi)
+        n += 1
+        if time.perf_counter() - t0 > budget_s:
+            break
+    dt = time.perf_counter() - t0
+    scale = (T / len(rows)) * (s.d_ff / hi)
+    return dict(value=round(dt / n * scale * 1e6, 1), unit="us/layer", cores=1, kind="oracle",
+                sample="%d batches of %d token(s) of the %s layer (router on all rows, %d experts per row "
+                "on %d rows over %d of %d units, dequantized per call, fp64, scaled to the batch and the "
+                "whole expert)" % (n, T, s.name, s.top_k, len(rows), hi, s.d_ff))
+
+
 def cpu_baseline(rig, hf_list, budget_s):
     """The oracle as it stands, one thread, on as many batches of the same
     layer as fit in about budget_s seconds.  For batches of more than 16
@@ -269,6 +310,8 @@ def cpu_baseline(rig, hf_list, budget_s):
     the time is scaled to the whole batch."""
     import oracle
     s = rig.shape
+    if getattr(s, "expert_bits", 0):
+        return cpu_baseline_q(rig, hf_list, budget_s)
     T = hf_list[0].shape[0]
     rows = list(range(min(T, 16)))
     t0 = time.perf_counter()
@@ -505,7 +548,7 @@ def main():
     ap.add_argument("--timeline-out", default=None)
     ap.add_argument("--workload", default="mixtral-decode",
                     help="mixtral-decode (default), deepseek-decode, deepseek-prefill, "
-                         "qwen-decode16, qwen-prefill; stacks: mixtral-stack, mixtral-stack-mixed, "
+                         "qwen-decode16, qwen-prefill, mixtral-q2-decode; stacks: mixtral-stack, mixtral-stack-mixed, mixtral-q2-stack, "
                          "deepseek-stack, qwen-stack")
     ap.add_argument("--pmc-pass", action="store_true",
                     help="only the split pass, with the counter calibration copy before its timed steps "
@@ -617,7 +660,8 @@ def main():
                                % (args.workload, shape.name, "prefill" if T > 16 else "decode", T, r,
                                   int(slots[0])),
                    "d_model": shape.d_model, "d_ff": shape.d_ff, "n_experts": shape.n_experts,
-                   "top_k": shape.top_k, "n_shared": shape.n_shared, "r": r, "tokens_per_step": T},
+                   "top_k": shape.top_k, "n_shared": shape.n_shared, "r": r, "tokens_per_step": T,
+                   "expert_bits": shape.expert_bits or None},
         "roofline": roof,
         "tokens_per_s": round(T * 1e3 / ms_plain, 2),
         "h2d_gbps": None if an["h2d_gbps"] is None else round(an["h2d_gbps"], 2),

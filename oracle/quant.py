@@ -24,15 +24,15 @@ GROUP = 64
 
 
 def unpack_codes(packed, bits, n):
-    """[rows][n * bits / 8] bytes -> [rows][n] integer codes."""
+    """[rows][n * bits / 8] bytes -> [rows][n] integer codes: code i of a row
+    is bits (i % per) * bits of byte i // per, per = 8 / bits."""
     packed = np.asarray(packed, np.uint8)
     per = 8 // bits
     mask = (1 << bits) - 1
-    rows = packed.shape[0]
-    q = np.empty((rows, n), np.int64)
-    for i in range(n):
-        q[:, i] = (packed[:, i // per] >> ((i % per) * bits)) & mask
-    return q
+    shifts = (np.arange(per) * bits).astype(np.uint8)
+    # [rows][n / per][per]: byte i // per, position i % per
+    q = (packed[:, :, None] >> shifts[None, None, :]) & mask
+    return q.reshape(packed.shape[0], n)
 
 
 def fp16_values(bits16):
@@ -45,15 +45,12 @@ def dequantize(packed, meta, bits, n):
 
     packed [rows][n * bits / 8]; meta [rows][n / 64][2] fp16 bit patterns
     (scale, zero)."""
-    q = unpack_codes(packed, bits, n)
+    rows = np.asarray(packed).shape[0]
+    q = unpack_codes(packed, bits, n).reshape(rows, n // GROUP, GROUP)
     meta = np.asarray(meta, np.uint16)
-    s = fp16_values(meta[:, :, 0])
-    z = fp16_values(meta[:, :, 1])
-    w = np.empty(q.shape, np.float64)
-    for i in range(n):
-        g = i // GROUP
-        w[:, i] = (q[:, i] - z[:, g]) * s[:, g]
-    return w
+    s = fp16_values(meta[:, :, 0])[:, :, None]  # group g = i // 64 of element i
+    z = fp16_values(meta[:, :, 1])[:, :, None]
+    return ((q - z) * s).reshape(rows, n)
 
 
 def expert_weights(codes, meta, bits, d, F):
@@ -62,7 +59,7 @@ def expert_weights(codes, meta, bits, d, F):
     wg = dequantize(codes[0], meta[0], bits, d).T
     wu = dequantize(codes[1], meta[1], bits, d).T
     wd = dequantize(codes[2], meta[2], bits, F).T
-    return np.ascontiguousarray(wg), np.ascontiguousarray(wu), np.ascontiguousarray(wd)
+    return wg, wu, wd
 
 
 def expert(h_t, weights):
@@ -73,6 +70,23 @@ def expert(h_t, weights):
     u = h @ wu
     a = g / (1.0 + np.exp(-g)) * u
     return a @ wd
+
+
+def expert_range(h_t, codes, meta, bits, d, F, lo, hi):
+    """E^[lo,hi)(h_t): the expert's sum over intermediate units [lo, hi)
+    (multiples of 64; Sec. 3.1's vertical split), dequantizing only those
+    units' gate and up rows and down columns.  fp64."""
+    assert lo % GROUP == 0 and hi % GROUP == 0 and 0 <= lo <= hi <= F
+    per = 8 // bits
+    wg = dequantize(np.asarray(codes[0])[lo:hi], np.asarray(meta[0])[lo:hi], bits, d)      # [hi-lo][d]
+    wu = dequantize(np.asarray(codes[1])[lo:hi], np.asarray(meta[1])[lo:hi], bits, d)
+    wd = dequantize(np.asarray(codes[2])[:, lo // per:hi // per], np.asarray(meta[2])[:, lo // GROUP:hi // GROUP],
+                    bits, hi - lo)                                                            # [d][hi-lo]
+    h = np.asarray(h_t, np.float64).reshape(-1)
+    g = wg @ h
+    u = wu @ h
+    a = g / (1.0 + np.exp(-g)) * u
+    return wd @ a
 
 
 def moe_layer(h, w_r, experts, K, renormalize=True, bias=None, tokens=None):

@@ -1074,20 +1074,44 @@ __device__ __forceinline__ float dot2bf(uint32_t a, uint32_t b, float c) {
   return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf2_t, a), __builtin_bit_cast(bf2_t, b), c, false);
 }
 
+// Constants in registers the compiler cannot fold: (x & m) | o with m in a
+// vector and o in a scalar register compiles to one v_and_or_b32, whose
+// encoding takes neither a 32-bit literal nor two scalar operands, instead
+// of an AND and an OR with literals.
+template <uint32_t V>
+__device__ __forceinline__ uint32_t sreg_const() {
+  uint32_t r;
+  asm("s_mov_b32 %0, %1" : "=s"(r) : "i"(V));
+  return r;
+}
+template <uint32_t V>
+__device__ __forceinline__ uint32_t vreg_const() {
+  uint32_t r;
+  asm("v_mov_b32 %0, %1" : "=v"(r) : "i"(V));
+  return r;
+}
+
+template <int BITS>
+struct PairMasks {
+  static constexpr uint32_t M = ((1u << BITS) - 1u) << (7 - BITS);
+  uint32_t mask, one;
+  __device__ __forceinline__ PairMasks() : mask(vreg_const<M | (M << 16)>()), one(sreg_const<kBf16OnePair>()) {}
+};
+
 // Pair j of a code word as two bf16 values 1 + q / 2^BITS.
 template <int BITS, int J>
-__device__ __forceinline__ uint32_t code_pair(uint32_t w) {
+__device__ __forceinline__ uint32_t code_pair(uint32_t w, const PairMasks<BITS>& pm) {
   constexpr int SH = (7 - BITS) - J * BITS;
-  constexpr uint32_t M = ((1u << BITS) - 1u) << (7 - BITS);
   const uint32_t x = SH >= 0 ? (w << (SH >= 0 ? SH : 0)) : (w >> (SH < 0 ? -SH : 0));
-  return (x & (M | (M << 16))) | kBf16OnePair;
+  return (x & pm.mask) | pm.one;
 }
 
 // acc[t] = sum over one group's code words (WPG words) of pair . x[t], for
 // the NT rows x[t] (32 bf16 pairs each); each pair is formed once and used
 // by every row.
 template <int BITS, int WPG, int NT>
-__device__ __forceinline__ void group_dot(const uint32_t (&cw)[WPG], const uint32_t (*x)[32], float (&acc)[NT]) {
+__device__ __forceinline__ void group_dot(const uint32_t (&cw)[WPG], const uint32_t (*x)[32], float (&acc)[NT],
+                                          const PairMasks<BITS>& pm) {
   constexpr int PPW = 16 / BITS;  // pairs per word
 #pragma unroll
   for (int t = 0; t < NT; ++t) acc[t] = 0.0f;
@@ -1096,7 +1120,7 @@ __device__ __forceinline__ void group_dot(const uint32_t (&cw)[WPG], const uint3
     const uint32_t w = cw[m];
 #define MSK_QP(J)                                                                 \
   if constexpr (J < PPW) {                                                        \
-    const uint32_t pr = code_pair<BITS, J>(w);                                    \
+    const uint32_t pr = code_pair<BITS, J>(w, pm);                                \
     _Pragma("unroll") for (int t = 0; t < NT; ++t) acc[t] = dot2bf(pr, x[t][m * PPW + J], acc[t]); \
   }
     MSK_QP(0) MSK_QP(1) MSK_QP(2) MSK_QP(3) MSK_QP(4) MSK_QP(5) MSK_QP(6) MSK_QP(7)
@@ -1155,6 +1179,7 @@ struct QCfg {
 };
 
 template <int BITS, int LPU, int GPL, int NT, int B>
+// two waves per SIMD: at most 256 registers per lane
 __global__ __launch_bounds__((QCfg<BITS, LPU, GPL, NT, B>::THREADS)) __attribute__((amdgpu_waves_per_eu(2))) void ffn_q_kernel(FfnArgs a) {
   using Q = QCfg<BITS, LPU, GPL, NT, B>;
   constexpr int WPG = Q::WPG;
@@ -1186,9 +1211,27 @@ __global__ __launch_bounds__((QCfg<BITS, LPU, GPL, NT, B>::THREADS)) __attribute
   const int lane = tid & 63, wave = tid >> 6;
   const int sg = lane / LPU, li = lane % LPU;
   constexpr int V4 = WPG / 4;  // uint4 loads per group
+  const PairMasks<BITS> pm;
+
+  // phase 2 reads its down columns PB at a time, one batch ahead; the first
+  // batch is requested before phase 1 so that it lands meanwhile
+  constexpr int PB = 4;
+  const int ncol = d / Q::THREADS;
+  uint4 dn[PB][V4];
+  uint32_t dmn[PB];
+  auto load_cols = [&](int k0) {
+#pragma unroll
+    for (int b = 0; b < PB; ++b) {
+      const int col = tid + Q::THREADS * min(k0 + b, ncol - 1);  // clamped past the last column
+#pragma unroll
+      for (int v = 0; v < V4; ++v) dn[b][v] = ldw16(Dq + static_cast<size_t>(col) * V4 + v);
+      dmn[b] = Dm[col];
+    }
+  };
 
   for (int tile = 0; tile < n_tok; tile += NT) {
     const int nt = min(NT, n_tok - tile);
+    load_cols(0);
     // ---- phase 1
     {
       uint32_t xh[GPL][NT][32];
@@ -1270,8 +1313,8 @@ __global__ __launch_bounds__((QCfg<BITS, LPU, GPL, NT, B>::THREADS)) __attribute
               uw[4 * v + 3] = ucur[j][i][v].w;
             }
             float ga[NT], ua[NT];
-            group_dot<BITS, WPG, NT>(gw, xh[i], ga);
-            group_dot<BITS, WPG, NT>(uw, xh[i], ua);
+            group_dot<BITS, WPG, NT>(gw, xh[i], ga, pm);
+            group_dot<BITS, WPG, NT>(uw, xh[i], ua, pm);
             const float gs = fp16_lo(gmc[j][i]), gz = C + fp16_hi(gmc[j][i]);
             const float us = fp16_lo(umc[j][i]), uz = C + fp16_hi(umc[j][i]);
 #pragma unroll
@@ -1314,38 +1357,38 @@ __global__ __launch_bounds__((QCfg<BITS, LPU, GPL, NT, B>::THREADS)) __attribute
         for (int p = 0; p < 32; ++p) sum = dot2bf(xa[t][p], kBf16OnePair, sum);
         as[t] = sum;
       }
-      const int ncol = d / Q::THREADS;
-      uint4 dc[V4], dn[V4];
-      uint32_t dmc, dmn;
-      auto load_col = [&](int k, uint4(&dd)[V4], uint32_t& dm) {
-        const int col = tid + Q::THREADS * min(k, ncol - 1);  // clamped past the last column
+      uint4 dc[PB][V4];
+      uint32_t dmc[PB];
+      for (int k0 = 0; k0 < ncol; k0 += PB) {
 #pragma unroll
-        for (int v = 0; v < V4; ++v) dd[v] = ldw16(Dq + static_cast<size_t>(col) * V4 + v);
-        dm = Dm[col];
-      };
-      load_col(0, dn, dmn);
-      for (int k = 0; k < ncol; ++k) {
+        for (int b = 0; b < PB; ++b) {
 #pragma unroll
-        for (int v = 0; v < V4; ++v) dc[v] = dn[v];
-        dmc = dmn;
-        load_col(k + 1, dn, dmn);
-        const int col = tid + Q::THREADS * k;
-        uint32_t dw[WPG];
-#pragma unroll
-        for (int v = 0; v < V4; ++v) {
-          dw[4 * v] = dc[v].x;
-          dw[4 * v + 1] = dc[v].y;
-          dw[4 * v + 2] = dc[v].z;
-          dw[4 * v + 3] = dc[v].w;
+          for (int v = 0; v < V4; ++v) dc[b][v] = dn[b][v];
+          dmc[b] = dmn[b];
         }
-        const float sc = fp16_lo(dmc), zc = C + fp16_hi(dmc);
-        float acc[NT];
-        group_dot<BITS, WPG, NT>(dw, xa, acc);
+        load_cols(k0 + PB);
 #pragma unroll
-        for (int t = 0; t < NT; ++t) {
-          if (t < nt) {
-            const int row = p0 + tile + t;
-            a.part[(static_cast<size_t>(row) * a.n_planes + c) * d + col] = sc * (C * acc[t] - zc * as[t]);
+        for (int b = 0; b < PB; ++b) {
+          if (k0 + b < ncol) {
+            const int col = tid + Q::THREADS * (k0 + b);
+            uint32_t dw[WPG];
+#pragma unroll
+            for (int v = 0; v < V4; ++v) {
+              dw[4 * v] = dc[b][v].x;
+              dw[4 * v + 1] = dc[b][v].y;
+              dw[4 * v + 2] = dc[b][v].z;
+              dw[4 * v + 3] = dc[b][v].w;
+            }
+            const float sc = fp16_lo(dmc[b]), zc = C + fp16_hi(dmc[b]);
+            float acc[NT];
+            group_dot<BITS, WPG, NT>(dw, xa, acc, pm);
+#pragma unroll
+            for (int t = 0; t < NT; ++t) {
+              if (t < nt) {
+                const int row = p0 + tile + t;
+                a.part[(static_cast<size_t>(row) * a.n_planes + c) * d + col] = sc * (C * acc[t] - zc * as[t]);
+              }
+            }
           }
         }
       }

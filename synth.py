@@ -185,19 +185,22 @@ def quantize_rows(w: np.ndarray, bits: int):
     scale[scale == 0] = 1.0
     s16 = scale.astype(np.float16)
     z16 = (-lo / s16.astype(np.float32)).astype(np.float16)
-    q = np.rint(g / s16.astype(np.float32)[:, :, None] + z16.astype(np.float32)[:, :, None])
-    q = np.clip(q, 0, qmax).astype(np.uint8).reshape(rows, n)
+    q = g / s16.astype(np.float32)[:, :, None]
+    q += z16.astype(np.float32)[:, :, None]
+    np.rint(q, out=q)
+    np.clip(q, 0, qmax, out=q)
+    q = q.astype(np.uint8).reshape(rows, n)
     meta = np.stack([s16.view(np.uint16), z16.view(np.uint16)], axis=2)
     return pack_codes(q, bits), np.ascontiguousarray(meta)
 
 
 def quant_expert(shape: ModelShape, seed: int, layer: int, e: int, bits: int) -> QuantExpert:
-    """Expert e of `layer` as b-bit codes (same draws as expert())."""
+    """Expert e of `layer` as b-bit codes: N(0, 0.02) draws in [out][in]
+    order (gate, up [F][d]; down [d][F]), quantized row-group by row-group."""
     d, F = shape.d_model, shape.d_ff
-    wg = _normal(seed, KIND_GATE, layer, e, (d, F), WEIGHT_STD)
-    wu = _normal(seed, KIND_UP, layer, e, (d, F), WEIGHT_STD)
-    wd = _normal(seed, KIND_DOWN, layer, e, (F, d), WEIGHT_STD)
-    parts = [quantize_rows(np.ascontiguousarray(m), bits) for m in (wg.T, wu.T, wd.T)]
+    parts = []
+    for kind, shp in ((KIND_GATE, (F, d)), (KIND_UP, (F, d)), (KIND_DOWN, (d, F))):
+        parts.append(quantize_rows(_normal(seed, kind, layer, e, shp, WEIGHT_STD), bits))
     return QuantExpert(bits, tuple(p[0] for p in parts), tuple(p[1] for p in parts))
 
 

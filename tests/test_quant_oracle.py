@@ -122,3 +122,20 @@ def test_synthetic_quantizer_stays_within_half_a_step(bits):
     # rounding of the zero to fp16 shifts the grid by up to half an fp16 ulp of z
     slack = np.repeat(np.abs(z) * 2.0 ** -11 * s, 64, axis=1)
     assert np.all(np.abs(deq - w) <= 0.5 * step * (1 + 1e-3) + slack + 1e-12)
+
+
+@pytest.mark.parametrize("bits", [2, 4])
+def test_expert_ranges_sum_to_the_expert(bits):
+    """Split identity (Sec. 3.1): the range form over [0, F_top) plus
+    [F_top, F) equals the full expert, within fp64 rounding, for every
+    chunk-aligned split point."""
+    from oracle import quant
+    shape = synth.ModelShape("q-split", 1, 256, 320, 4, 2, expert_bits=bits)
+    qe = synth.quant_expert(shape, 1, 0, 2, bits)
+    ws = quant.expert_weights(qe.codes, qe.meta, bits, 256, 320)
+    h = np.random.default_rng(7).standard_normal(256).astype(np.float32)
+    full = quant.expert(h, ws)
+    for top in range(0, 321, 64):
+        y = (quant.expert_range(h, qe.codes, qe.meta, bits, 256, 320, 0, top)
+             + quant.expert_range(h, qe.codes, qe.meta, bits, 256, 320, top, 320))
+        np.testing.assert_allclose(y, full, rtol=1e-12, atol=1e-14 * np.abs(full).max())
