@@ -143,13 +143,13 @@ inline bool q_supported(int d) { return d % 64 == 0 && d >= 256 && d <= kMaxMode
 //    as data lands (disjoint columns of act);
 //  down (mma_down): out[row][:] = sum_f act[row][f] * D_f over all of the
 //    expert's chunks (chunks < split at base, the rest at base2), 64 rows x
-//    128 columns per work-group, written as the single partial plane.
+//    256 columns per work-group, written as the single partial plane.
 constexpr int kMaxMmaTasks = 80;
 // gate/up work-groups per chunk and row tile: 4 (16 units each) for launches
 // of fewer than kGuSplitBelow row-tile chunks, else 1 (whole chunks)
 constexpr int kGuSplitBelow = 256;
 constexpr int kMmaRows = 64;     // rows (token slots) per work-group
-constexpr int kMmaCols = 128;    // output columns per down work-group
+constexpr int kMmaCols = 256;    // output columns per down work-group
 
 struct MmaTask {
   const unsigned char* base;   // chunk c at base + c * chunk_bytes

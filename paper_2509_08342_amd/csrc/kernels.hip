@@ -1569,6 +1569,123 @@ __global__ __launch_bounds__(256) void mma_gateup_kernel(MmaArgs a) {
   }
 }
 
+// gate/up of whole chunks: a work-group takes 64 rows x 64 units, wave w the
+// units 16 w .. 16 w + 15 for all four 16-row blocks, so every weight
+// fragment is read by one wave only.  The activation rows are staged in LDS
+// in slabs of kGuSlab k (double-buffered, rows padded so that the 16 rows a
+// fragment read touches fall in distinct banks); the next slab's rows and
+// weight fragments load while the current slab computes.
+constexpr int kGuSlab = 128;            // k per staged slab (4 MFMA k-steps)
+constexpr int kGuPitch = kGuSlab + 8;   // bf16 per staged row
+
+__global__ __launch_bounds__(256) void mma_gateup_lds_kernel(MmaArgs a) {
+  __shared__ __align__(16) uint16_t As[2][kMmaRows * kGuPitch];
+  const int wg = blockIdx.x;
+  const MmaTask tk = a.tasks[find_task(a.tasks, a.n_tasks, wg)];
+  const int local = wg - tk.wg_begin;
+  const int mt = local % tk.m_tiles;
+  const int c = tk.chunk_lo + local / tk.m_tiles;
+  const TileRows tr = tile_rows(a, tk, mt);
+  if (tr.n <= 0) return;  // uniform over the work-group
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int d = a.d;
+  const int ksteps = d / 32;
+  const int nslab = (ksteps + 3) / 4;
+  const bool routed = tk.expert >= 0;
+  // staging: piece p = tid + 256 i of a slab is row p / 16, k 8 (p % 16)
+  const uint16_t* hrow[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int row = min((tid >> 4) + 16 * i, tr.n - 1);  // clamped rows: staged, never stored
+    const int tok = routed ? a.perm[tr.p0 + row] / a.K : tr.p0 + row;
+    hrow[i] = static_cast<const uint16_t*>(a.h) + static_cast<size_t>(tok) * d + 8 * (tid & 15);
+  }
+  const uint16_t* G = reinterpret_cast<const uint16_t*>(tk.base + static_cast<size_t>(c) * a.chunk_bytes);
+  const uint16_t* U = G + static_cast<size_t>(kChunkUnits) * d;
+  const int unit = 16 * wave + (lane & 15);  // this lane's B column
+  const int kq = 8 * (lane >> 4);
+  uint4 ast[4], bn[4][2], bc[4][2];
+  auto load_a = [&](int sl) {
+    const int k0 = min(sl, nslab - 1) * kGuSlab;  // clamped: the slab past the last is loaded, not used
+#pragma unroll
+    for (int i = 0; i < 4; ++i) ast[i] = ld16(hrow[i] + min(k0, d - kGuSlab));
+  };
+  // a partial last slab (d % 128 == 64) is staged from k = d - 128; the
+  // compute reads it at the matching offset
+  auto store_a = [&](int buf) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      *reinterpret_cast<uint4*>(&As[buf][((tid >> 4) + 16 * i) * kGuPitch + 8 * (tid & 15)]) = ast[i];
+  };
+  auto load_b = [&](int sl) {
+#pragma unroll
+    for (int s = 0; s < 4; ++s) {
+      const int k = min(4 * sl + s, ksteps - 1) * 32;  // clamped past the last step
+      const size_t off = (static_cast<size_t>(k / kKTile) * kChunkUnits + unit) * kKTile + (k % kKTile) + kq;
+      bn[s][0] = ldw16(G + off);
+      bn[s][1] = ldw16(U + off);
+    }
+  };
+  f32x4_t ag[4], au[4];
+#pragma unroll
+  for (int rb = 0; rb < 4; ++rb) ag[rb] = au[rb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  load_a(0);
+  load_b(0);
+  store_a(0);
+  __syncthreads();
+  for (int sl = 0; sl < nslab; ++sl) {
+    const int buf = sl & 1;
+#pragma unroll
+    for (int s = 0; s < 4; ++s) {
+      bc[s][0] = bn[s][0];
+      bc[s][1] = bn[s][1];
+    }
+    load_a(sl + 1);
+    load_b(sl + 1);
+    // the slab's first k inside the staged rows (a partial last slab sits at
+    // the end of its 128-wide window)
+    const int k0 = sl * kGuSlab, kbase = k0 - min(k0, d - kGuSlab);
+#pragma unroll
+    for (int s = 0; s < 4; ++s) {
+      if (4 * sl + s < ksteps) {
+#pragma unroll
+        for (int rb = 0; rb < 4; ++rb) {
+          if (16 * rb < tr.n) {
+            const uint4 av =
+                *reinterpret_cast<const uint4*>(&As[buf][(16 * rb + (lane & 15)) * kGuPitch + kbase + 32 * s + kq]);
+            const bf16x8_t A = as_bf16x8(av);
+            ag[rb] = mfma16(A, as_bf16x8(bc[s][0]), ag[rb]);
+            au[rb] = mfma16(A, as_bf16x8(bc[s][1]), au[rb]);
+          }
+        }
+      }
+    }
+    if (sl + 1 < nslab) store_a(buf ^ 1);
+    __syncthreads();
+  }
+  uint16_t* act = routed ? a.act : a.act_sh + static_cast<size_t>(-1 - tk.expert) * a.rows_shared * a.f_pad_sh;
+  const int f_pad = routed ? a.f_pad : a.f_pad_sh;
+  const int f = c * kChunkUnits + unit;
+#pragma unroll
+  for (int rb = 0; rb < 4; ++rb) {
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int row = 16 * rb + 4 * (lane >> 4) + r;
+      if (row < tr.n) act[static_cast<size_t>(tr.p0 + row) * f_pad + f] = f2bf(silu(ag[rb][r]) * au[rb][r]);
+    }
+  }
+}
+
+// down: a work-group takes 64 rows x kMmaCols (256) columns over all of the
+// expert's chunks; wave w the rows 16 w .. 16 w + 15.  Per chunk the
+// 64 x 256 down tile is staged transposed in LDS (dt[column][unit]): thread
+// (unit group u = tid % 8, column group g = tid / 8) loads units 8 u .. 8 u
+// + 7 of columns 8 g .. 8 g + 7 (eight 16-byte row pieces), transposes them
+// in registers (v_perm_b32) into eight 16-byte column fragments and writes
+// each with one LDS store.  With a row pitch of 72 units, the 16 lanes of a
+// store pass (8 unit groups x 2 column groups 8 apart) and the 16 lanes of a
+// fragment read (16 consecutive columns) each hit 16 distinct bank quads.
+// Two chunks' tiles are in flight ahead of the one computing.
 __global__ __launch_bounds__(256) void mma_down_kernel(MmaArgs a) {
   constexpr int PITCH = kChunkUnits + 8;  // transposed D tile row: 64 units + pad
   __shared__ __align__(16) uint16_t dt[kMmaCols * PITCH];
@@ -1587,63 +1704,67 @@ __global__ __launch_bounds__(256) void mma_down_kernel(MmaArgs a) {
   const uint16_t* arow = act + static_cast<size_t>(tr.p0 + ar) * f_pad;
   const int kq = 8 * (lane >> 4);
   const int col0 = cb * kMmaCols;
-  f32x4_t acc[8];
+  const int ug = tid & 7, cg = tid >> 3;
+  const int lcol = min(col0 + 8 * cg, d - 8);  // this thread's loaded columns (clamped; never stored past d)
+  constexpr int NF = kMmaCols / 16;
+  f32x4_t acc[NF];
 #pragma unroll
-  for (int nf = 0; nf < 8; ++nf) acc[nf] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  for (int nf = 0; nf < NF; ++nf) acc[nf] = f32x4_t{0.f, 0.f, 0.f, 0.f};
   const bool active = 16 * wave < tr.n;  // waves without rows still stage D tiles
-  // the next chunk's D tile and A fragments load while this chunk computes
-  uint4 dn[4], an[2];
-  auto load_chunk = [&](int c) {
+  uint4 d0[8], a0[2], d1[8], a1[2];
+  auto load_chunk = [&](int c, uint4(&dn)[8], uint4(&an)[2]) {
     const unsigned char* cbase = (c < tk.split ? tk.base : tk.base2) + static_cast<size_t>(c) * a.chunk_bytes;
     const uint16_t* D = reinterpret_cast<const uint16_t*>(cbase) + 2 * static_cast<size_t>(kChunkUnits) * d;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int piece = tid + 256 * i;           // 64 units x 16 pieces of 8 columns
-      const int f = piece >> 4, q = piece & 15;
-      const int col = min(col0 + 8 * q, d - 8);  // clamped; columns past d are never stored
-      dn[i] = ld16(D + static_cast<size_t>(f) * d + col);
-    }
+    for (int r = 0; r < 8; ++r) dn[r] = ld16(D + static_cast<size_t>(8 * ug + r) * d + lcol);
 #pragma unroll
     for (int ks = 0; ks < 2; ++ks) an[ks] = ld16(arow + c * kChunkUnits + 32 * ks + kq);
   };
-  load_chunk(0);
-  for (int c = 0; c < tk.n_chunks; ++c) {
-    uint4 dv[4], av[2];
+  auto step = [&](uint4(&dv)[8], uint4(&av)[2], int next) {
+    // column j of the 8 loaded rows: word j / 2 of each row, low or high half
+    uint4 frag[8];
 #pragma unroll
-    for (int i = 0; i < 4; ++i) dv[i] = dn[i];
-    av[0] = an[0];
-    av[1] = an[1];
-    load_chunk(min(c + 1, tk.n_chunks - 1));  // the last chunk reloads itself (in bounds, unused)
-    // stage D[64 units][128 columns] transposed: dt[column][unit]
+    for (int j = 0; j < 8; ++j) {
+      const uint32_t sel = (j & 1) ? 0x07060302u : 0x05040100u;
+      uint32_t w[8];
+#pragma unroll
+      for (int r = 0; r < 8; ++r) {
+        const uint4 v = dv[r];
+        w[r] = (j >> 1) == 0 ? v.x : (j >> 1) == 1 ? v.y : (j >> 1) == 2 ? v.z : v.w;
+      }
+      frag[j] = make_uint4(__builtin_amdgcn_perm(w[1], w[0], sel), __builtin_amdgcn_perm(w[3], w[2], sel),
+                           __builtin_amdgcn_perm(w[5], w[4], sel), __builtin_amdgcn_perm(w[7], w[6], sel));
+    }
+    const uint4 A0 = av[0], A1 = av[1];
+    load_chunk(next, dv, av);
     __syncthreads();  // previous chunk's readers are done with dt
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int piece = tid + 256 * i;
-      const int f = piece >> 4, q = piece & 15;
-      const uint32_t w4[4] = {dv[i].x, dv[i].y, dv[i].z, dv[i].w};
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        dt[(8 * q + 2 * j) * PITCH + f] = static_cast<uint16_t>(w4[j] & 0xffffu);
-        dt[(8 * q + 2 * j + 1) * PITCH + f] = static_cast<uint16_t>(w4[j] >> 16);
-      }
-    }
+    for (int j = 0; j < 8; ++j) *reinterpret_cast<uint4*>(&dt[(8 * cg + j) * PITCH + 8 * ug]) = frag[j];
     __syncthreads();
     if (active) {
 #pragma unroll
       for (int ks = 0; ks < 2; ++ks) {
-        const bf16x8_t A = as_bf16x8(av[ks]);
+        const bf16x8_t A = as_bf16x8(ks == 0 ? A0 : A1);
 #pragma unroll
-        for (int nf = 0; nf < 8; ++nf) {
+        for (int nf = 0; nf < NF; ++nf) {
           const uint4 bv = *reinterpret_cast<const uint4*>(&dt[(16 * nf + (lane & 15)) * PITCH + 32 * ks + kq]);
           acc[nf] = mfma16(A, as_bf16x8(bv), acc[nf]);
         }
       }
     }
+  };
+  const int nc = tk.n_chunks;
+  load_chunk(0, d0, a0);
+  load_chunk(min(1, nc - 1), d1, a1);
+  for (int c = 0; c < nc; c += 2) {
+    // chunks past the last reload the last one (in bounds, unused)
+    step(d0, a0, min(c + 2, nc - 1));
+    if (c + 1 < nc) step(d1, a1, min(c + 3, nc - 1));
   }
   // epilogue: fp32 rows of the single partial plane
   float* out = routed ? a.part : a.part_sh + static_cast<size_t>(-1 - tk.expert) * a.sh_plane;
 #pragma unroll
-  for (int nf = 0; nf < 8; ++nf) {
+  for (int nf = 0; nf < NF; ++nf) {
     const int col = col0 + 16 * nf + (lane & 15);
     if (col < d) {
 #pragma unroll
@@ -1659,6 +1780,8 @@ hipError_t launch_mma_gateup(const MmaArgs& a, hipStream_t s) {
   if (a.n_wg <= 0 || a.n_tasks <= 0) return hipSuccess;
   if (a.gu_split == 4)
     hipLaunchKernelGGL(mma_gateup_kernel<1>, dim3(a.n_wg), dim3(256), 0, s, a);
+  else if (a.gu_split == 1 && a.d >= kGuSlab)
+    hipLaunchKernelGGL(mma_gateup_lds_kernel, dim3(a.n_wg), dim3(256), 0, s, a);
   else if (a.gu_split == 1)
     hipLaunchKernelGGL(mma_gateup_kernel<4>, dim3(a.n_wg), dim3(256), 0, s, a);
   else
