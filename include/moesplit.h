@@ -407,6 +407,57 @@ ms_status ms_residual_norm(ms_ctx* ctx, const void* h_dev, const float* y_dev, i
 ms_status ms_timeline_begin(ms_ctx* ctx, void* stream, int32_t capacity);
 ms_status ms_timeline_end(ms_ctx* ctx, ms_interval* out, int32_t cap, int32_t* n_out);
 
+/* ---- the decoder loop around the MoE layer ---------------------------------
+ *
+ * Sec. 2.1: each layer is an attention module, h = Norm(x + Att(x))
+ * (Eq. (1)), then the MoE module (Eq. (2), ms_forward); a head follows the
+ * last layer.  The paper defers attention to the designs it cites; these
+ * stateless calls implement causal grouped-query attention with rotary
+ * position embeddings (Mixtral's convention) so that a whole decoder loop
+ * runs on the GPU and the prefetch of Sec. 3.2 overlaps real attention.
+ * Every buffer is a caller-owned device pointer (bf16 as raw 16-bit
+ * patterns, 16-byte aligned where marked), every call is enqueued on
+ * `stream` and returns MS_OK, MS_E_INVALID (bad sizes or pointers; nothing
+ * enqueued), MS_E_UNSUPPORTED (shape beyond the kernels) or MS_E_HIP (the
+ * launch failed).  Norm between modules is ms_residual_norm. */
+
+/* y[t][o] = sum_i x[t][i] w[o][i] (+ add[t][o] if add is not NULL), fp32
+ * accumulation: x [T][n_in] bf16 (16-byte aligned), w [n_out][n_in] bf16
+ * (the nn.Linear layout, 16-byte aligned), y and add [T][n_out] fp32 (add
+ * may alias y).  n_in a multiple of 8, at most 8192. */
+ms_status ms_dense(const void* x, const void* w, int32_t T, int32_t n_in, int32_t n_out, float* y, const float* add,
+                   void* stream);
+
+/* Rotary embedding and key/value append for T tokens at positions
+ * pos0 .. pos0 + T - 1 (pos0 + T <= max_ctx).  qkv [T][(Hq + 2 Hkv) D] fp32:
+ * per token the Hq query heads, then the Hkv key heads, then the Hkv value
+ * heads, D wide each (D even, Hq a multiple of Hkv).  Pair (i, i + D/2) of
+ * a query or key head turns by p * base^(-2 i / D) (angle in double
+ * precision); results are rounded to bf16: q_out [T][Hq][D], keys into
+ * k_cache [Hkv][max_ctx][D] and values (not rotated) into v_cache
+ * [Hkv][max_ctx][D] at row p. */
+ms_status ms_rope_kv(const float* qkv, int32_t T, int32_t Hq, int32_t Hkv, int32_t D, int32_t pos0, double base,
+                     void* q_out, void* k_cache, void* v_cache, int32_t max_ctx, void* stream);
+
+/* Causal grouped-query attention: token t (at position pos0 + t) attends to
+ * cache rows 0 .. pos0 + t; query head h uses key/value head h / (Hq / Hkv);
+ * scores q.k / sqrt(D), softmax with the maximum subtracted, fp32.  q
+ * [T][Hq][D] bf16 (from ms_rope_kv), caches as in ms_rope_kv (16-byte
+ * aligned), out [T][Hq][D] bf16.  MS_E_UNSUPPORTED unless D is a multiple
+ * of 8, Hq / Hkv is 1, 2, 4 or 8 and (Hq / Hkv) (D + pos0 + T) <= 16000
+ * (queries and scores of a work-group in LDS). */
+ms_status ms_attention(const void* q, const void* k_cache, const void* v_cache, int32_t T, int32_t Hq, int32_t Hkv,
+                       int32_t D, int32_t pos0, int32_t max_ctx, void* out, void* stream);
+
+/* Greedy token choice: idx_out[t] = arg max over x[t][0 .. n) (fp32 [T][n]),
+ * the lowest index on ties. */
+ms_status ms_argmax(const float* x, int32_t T, int32_t n, int32_t* idx_out, void* stream);
+
+/* Embedding gather: out[t] = table[ids[t]] (bf16 rows of d, d a multiple of
+ * 8; table and out 16-byte aligned); ids outside [0, n_vocab) are clamped. */
+ms_status ms_embed(const int32_t* ids, const void* table, int32_t n_vocab, int32_t T, int32_t d, void* out,
+                   void* stream);
+
 #ifdef __cplusplus
 }
 #endif

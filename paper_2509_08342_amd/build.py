@@ -10,7 +10,7 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libmoesplit.so")
-SOURCES = ["kernels.hip", "runtime.hip", "planner.cpp"]
+SOURCES = ["kernels.hip", "runtime.hip", "planner.cpp", "decoder.hip"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = [

@@ -102,6 +102,11 @@ def _load():
         "ms_cache_update": [P, P, P],
         "ms_set_cache_policy": [P, I32, ctypes.c_double, ctypes.c_double, U64],
         "ms_set_copy_engine": [P, I32],
+        "ms_dense": [P, P, I32, I32, I32, P, P, P],
+        "ms_rope_kv": [P, I32, I32, I32, I32, I32, ctypes.c_double, P, P, P, I32, P],
+        "ms_attention": [P, P, P, I32, I32, I32, I32, I32, I32, P, P],
+        "ms_argmax": [P, I32, I32, P, P],
+        "ms_embed": [P, P, I32, I32, I32, P, P],
         "ms_timeline_begin": [P, P, I32],
         "ms_timeline_end": [P, ctypes.POINTER(ms_interval), I32, ctypes.POINTER(I32)],
     }
@@ -349,3 +354,29 @@ def ms_timeline_end(ctx, cap=1 << 16):
     _check(lib.ms_timeline_end(ctx, buf, cap, ctypes.byref(n)), ctx)
     return [dict(kind=INTERVAL_NAMES[buf[i].kind], layer=buf[i].layer, t0_ms=buf[i].t0_ms,
                  t1_ms=buf[i].t1_ms, bytes=int(buf[i].bytes)) for i in range(n.value)]
+
+
+# ------------------------------------------------- decoder loop (stateless)
+
+def ms_dense(x, w, T, n_in, n_out, y, add=None, stream=None):
+    _check(lib.ms_dense(_ptr(x), _ptr(w), int(T), int(n_in), int(n_out), _ptr(y),
+                        None if add is None else _ptr(add), _stream(stream)), what="ms_dense")
+
+
+def ms_rope_kv(qkv, T, Hq, Hkv, D, pos0, base, q_out, k_cache, v_cache, max_ctx, stream=None):
+    _check(lib.ms_rope_kv(_ptr(qkv), int(T), int(Hq), int(Hkv), int(D), int(pos0), float(base), _ptr(q_out),
+                          _ptr(k_cache), _ptr(v_cache), int(max_ctx), _stream(stream)), what="ms_rope_kv")
+
+
+def ms_attention(q, k_cache, v_cache, T, Hq, Hkv, D, pos0, max_ctx, out, stream=None):
+    _check(lib.ms_attention(_ptr(q), _ptr(k_cache), _ptr(v_cache), int(T), int(Hq), int(Hkv), int(D), int(pos0),
+                            int(max_ctx), _ptr(out), _stream(stream)), what="ms_attention")
+
+
+def ms_argmax(x, T, n, idx_out, stream=None):
+    _check(lib.ms_argmax(_ptr(x), int(T), int(n), _ptr(idx_out), _stream(stream)), what="ms_argmax")
+
+
+def ms_embed(ids, table, n_vocab, T, d, out, stream=None):
+    _check(lib.ms_embed(_ptr(ids), _ptr(table), int(n_vocab), int(T), int(d), _ptr(out), _stream(stream)),
+           what="ms_embed")

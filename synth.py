@@ -25,6 +25,7 @@ import numpy as np
 
 KIND_GATE, KIND_UP, KIND_DOWN, KIND_ROUTER, KIND_HIDDEN = 0, 1, 2, 3, 4
 KIND_SH_GATE, KIND_SH_UP, KIND_SH_DOWN, KIND_PERM, KIND_WALK = 5, 6, 7, 8, 9
+KIND_QKV, KIND_O, KIND_HEAD, KIND_EMBED, KIND_TOKENS = 10, 11, 12, 13, 14
 
 WEIGHT_STD = 0.02
 
@@ -235,3 +236,44 @@ def walk(shape: ModelShape, seed: int, steps: int, T: int = 1, eps: float = 0.3,
         out.append(storage(x, shape.dtype))
         x = a * x + np.float32(eps) * rng.standard_normal((T, shape.d_model), dtype=np.float32)
     return out
+
+
+# ------------------------------------------------------------ decoder loop --
+
+@dataclasses.dataclass(frozen=True)
+class AttnShape:
+    """Attention and head of a decoder around the MoE layers: Hq query heads
+    and Hkv key/value heads of width D, rotary base, vocabulary size."""
+    n_heads: int
+    n_kv_heads: int
+    head_dim: int
+    rope_base: float
+    vocab: int
+
+
+# Mixtral-8x7B's attention (32 heads, 8 key/value heads of 128, rotary base
+# 1e6) and vocabulary; a tiny one for the tests.
+MIXTRAL_ATTN = AttnShape(32, 8, 128, 1e6, 32000)
+TINY_ATTN = AttnShape(4, 2, 64, 1e4, 512)
+
+
+def attn_weights(shape: ModelShape, attn: AttnShape, seed: int, layer: int):
+    """(w_qkv [(Hq + 2 Hkv) D][d], w_o [d][Hq D]) as (raw, exact_f32) pairs,
+    N(0, 0.02) rounded to the model dtype."""
+    d, D = shape.d_model, attn.head_dim
+    n_qkv = (attn.n_heads + 2 * attn.n_kv_heads) * D
+    qkv = storage(_normal(seed, KIND_QKV, layer, 0, (n_qkv, d), WEIGHT_STD), shape.dtype)
+    o = storage(_normal(seed, KIND_O, layer, 0, (d, attn.n_heads * D), WEIGHT_STD), shape.dtype)
+    return qkv, o
+
+
+def head_weights(shape: ModelShape, attn: AttnShape, seed: int):
+    """(head [V][d] N(0, 0.02), embedding [V][d] N(0, 1)) as (raw, exact_f32)."""
+    head = storage(_normal(seed, KIND_HEAD, 0, 0, (attn.vocab, shape.d_model), WEIGHT_STD), shape.dtype)
+    emb = storage(_normal(seed, KIND_EMBED, 0, 0, (attn.vocab, shape.d_model), 1.0), shape.dtype)
+    return head, emb
+
+
+def prompt_tokens(attn: AttnShape, seed: int, n: int, tag: int = 0) -> np.ndarray:
+    """A seeded prompt of n token ids, uniform over the vocabulary."""
+    return _rng(seed, KIND_TOKENS, tag, 0).integers(0, attn.vocab, size=n).astype(np.int32)
