@@ -118,6 +118,19 @@ def _stacks():
     }
 
 
+# decoder loops: the MoE stack with Mixtral's attention and head, a prompt
+# (time to first token), then greedy decode (time per output token); the
+# cache is warmed by a first generation with LCP replacement
+def _decoders():
+    import synth
+    return {
+        "mixtral-decoder": dict(shape=synth.MIXTRAL_STACK, attn=synth.MIXTRAL_ATTN, budget=12 * GIB, r=0.5,
+                                prompt=512, n_sets=4, t_moe_us=208.0),
+        "mixtral-q2-decoder": dict(shape=synth.MIXTRAL_Q2_STACK, attn=synth.MIXTRAL_ATTN, budget=2 * GIB, r=0.5,
+                                   prompt=512, n_sets=4, t_moe_us=70.0),
+    }
+
+
 METRIC = "MoE-layer decode µs/layer + achieved HBM GB/s; H2D overlap % at fixed VRAM budget"
 KERNEL_KINDS = ("router", "group", "predict", "ffn_resident", "ffn_streamed", "ffn_down", "combine")
 COPY_KINDS = ("copy_miss", "copy_prefetch")
@@ -431,6 +444,106 @@ def trace_summary(d, out, cmd):
     print("wrote %s (%d kernels)" % (out, len(rows)))
 
 
+def run_decoder(args):
+    """A decoder loop: warm-up generation (LCP replacement fills the caches),
+    then a fresh prompt (TTFT) and greedy decode steps (TPOT), then a few
+    decode steps with events around each module (T_att, T_moe, T_head)."""
+    import torch
+    import synth
+    from paper_2509_08342_amd import moesplit as ms
+    from decoder import Decoder
+    cfg = _decoders()[args.workload]
+    shape, attn, P = cfg["shape"], cfg["attn"], cfg["prompt"]
+    L, E = shape.n_layers, shape.n_experts
+    n_warm, n_marks = 16, 4
+    n_new = args.warmup + args.steps + 1
+    max_ctx = P + max(n_warm, n_new + n_marks) + 8
+    t_setup = time.perf_counter()
+    log("generating %s weights (%d distinct sets over %d layers) and attention" % (shape.name, cfg["n_sets"], L))
+    dec = Decoder(shape, attn, seed=0, n_sets=cfg["n_sets"], max_tokens=P, max_ctx=max_ctx,
+                  budget_total=cfg["budget"], keep_f32=False)
+    if args.copy_engine == "dma":
+        ms.ms_set_copy_engine(dec.ctx, ms.MS_COPY_DMA)
+    slots = dec.stack.configure(cfg["r"], cfg["budget"])
+    log("setup %.1f s; warm-up generation (%d + %d tokens, LCP replacement)" % (time.perf_counter() - t_setup,
+                                                                               P, n_warm))
+    ms.ms_set_cache_policy(dec.ctx, ms.MS_CACHE_LCP)
+    ms.ms_reset_plan_stats(dec.ctx)
+    dec.generate(synth.prompt_tokens(attn, 0, P, tag=1), n_warm)
+    ms.ms_sync(dec.ctx)
+    stream = torch.cuda.current_stream()
+
+    def module_times(n):
+        """Per-token T_att, T_moe (summed over layers) and T_head in us."""
+        x1 = torch.empty(1, shape.d_model, dtype=torch.bfloat16, device="cuda")
+        acc = {"att": 0.0, "moe": 0.0, "head": 0.0}
+        for _ in range(n):
+            marks = []
+            dec.embed_ids(dec.ids, 1, x1, stream)
+            dec.step(x1, 1, stream=stream, marks=marks)
+            stream.synchronize()
+            for (name, e0), (_, e1) in zip(marks, marks[1:]):
+                acc[name] += e0.elapsed_time(e1) * 1e3
+        return {k: v / n for k, v in acc.items()}
+
+    plan = None
+    if args.configure:
+        t = module_times(n_marks)
+        hs_, ps_, phs_ = [], [], []
+        for l in range(L):
+            h_, p_, ph_, _ = ms.ms_plan_stats(dec.ctx, l, E)
+            hs_.append(h_)
+            ps_.append(p_)
+            phs_.append(ph_)
+        t_load = shape.expert_bytes / 55e3
+        plan = ms.ms_plan_solve(L, E, shape.top_k, shape.expert_bytes, t["att"] / L, t["moe"] / L, t["head"],
+                                t_load, np.array(hs_), np.array(ps_), np.array(phs_), cfg["budget"], args.zeta)
+        ms.ms_cache_update(dec.ctx, plan["budgets"], plan["theta"].astype(np.float32))
+        log("configurator (T_att %.0f us, T_moe %.0f us, T_head %.0f us): %d moves, theta %.3f..%.3f" % (
+            t["att"] / L, t["moe"] / L, t["head"], plan["iters"], plan["theta"].min(), plan["theta"].max()))
+    if args.policy == "static":
+        ms.ms_set_cache_policy(dec.ctx, ms.MS_CACHE_STATIC)
+    else:
+        ms.ms_set_cache_policy(dec.ctx, {"lcp": ms.MS_CACHE_LCP, "lru": ms.MS_CACHE_LRU, "lfu": ms.MS_CACHE_LFU,
+                                         "rnd": ms.MS_CACHE_RND}[args.policy])
+    dec.reset()
+    ms.ms_reset_stats(dec.ctx)
+    toks, ttft, tpot = dec.generate(synth.prompt_tokens(attn, 0, P, tag=2), n_new)
+    timed = tpot[args.warmup:]
+    st = [ms.ms_stats(dec.ctx, l) for l in range(L)]
+    tm = module_times(n_marks)
+    ms.ms_sync(dec.ctx)
+    tpot_ms = float(np.mean(timed))
+    sel = sum(x["experts_active"] for x in st)
+    hits = sum(x["alpha"] + x["beta"] for x in st)
+    out = {
+        "metric": "decode time per output token (TPOT) of the decoder loop with split experts",
+        "value": round(tpot_ms, 3), "unit": "ms/token", "higher_is_better": False,
+        "data": "synthetic", "dtype": "bf16", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "config": {"workload": "%s: %s, %d layers, attention %d heads / %d kv heads x %d, vocab %d, V_e %.0f GiB, "
+                               "r %s, prompt %d tokens, greedy decode, cache policy %s" % (
+                                   args.workload, shape.name, L, attn.n_heads, attn.n_kv_heads, attn.head_dim,
+                                   attn.vocab, cfg["budget"] / GIB,
+                                   "from the configurator" if plan is not None else cfg["r"], P, args.policy)},
+        "ttft_ms": round(ttft, 2),
+        "tokens_per_s": round(1e3 / tpot_ms, 2),
+        "tpot_ms": {q: round(float(np.percentile(timed, p)), 3) for q, p in (("p10", 10), ("p50", 50), ("p90", 90))},
+        "module_us_per_token": {"attention_per_layer": round(tm["att"] / L, 1), "moe_per_layer": round(tm["moe"] / L, 1),
+                                "head": round(tm["head"], 1)},
+        "hit_rate": round(hits / max(sel, 1), 4),
+        "h2d_bytes_per_token": {"miss": sum(x["bytes_miss"] for x in st) // max(len(tpot) + 1, 1),
+                                "prefetch": sum(x["bytes_prefetch"] for x in st) // max(len(tpot) + 1, 1)},
+        "cache_inserts": sum(x["cache_inserts"] for x in st),
+        "setup_s": round(time.perf_counter() - t_setup, 1),
+    }
+    if plan is not None:
+        out["plan"] = {"moves": plan["iters"], "theta": [round(float(t), 4) for t in plan["theta"]],
+                       "cache": [int(c) for c in plan["cache"]]}
+    log("TTFT %.1f ms, TPOT %.2f ms" % (ttft, tpot_ms))
+    dec.close()
+    print(json.dumps(out), flush=True)
+
+
 def run_stack(args):
     """A whole stack: warm-up statistics pick each layer's cached tops, an
     optional prefill pass, then decode steps through every layer with
@@ -549,6 +662,7 @@ def main():
     ap.add_argument("--workload", default="mixtral-decode",
                     help="mixtral-decode (default), deepseek-decode, deepseek-prefill, "
                          "qwen-decode16, qwen-prefill, mixtral-q2-decode; stacks: mixtral-stack, mixtral-stack-mixed, mixtral-q2-stack, "
+                         "mixtral-decoder, mixtral-q2-decoder, "
                          "deepseek-stack, qwen-stack")
     ap.add_argument("--pmc-pass", action="store_true",
                     help="only the split pass, with the counter calibration copy before its timed steps "
@@ -591,6 +705,9 @@ def main():
     torch.cuda.set_device(0)
     if args.workload in _stacks():
         run_stack(args)
+        return
+    if args.workload in _decoders():
+        run_decoder(args)
         return
     wl = _workloads()[args.workload]
     shape, T = wl["shape"], wl["T"]

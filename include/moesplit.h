@@ -443,9 +443,10 @@ ms_status ms_rope_kv(const float* qkv, int32_t T, int32_t Hq, int32_t Hkv, int32
  * cache rows 0 .. pos0 + t; query head h uses key/value head h / (Hq / Hkv);
  * scores q.k / sqrt(D), softmax with the maximum subtracted, fp32.  q
  * [T][Hq][D] bf16 (from ms_rope_kv), caches as in ms_rope_kv (16-byte
- * aligned), out [T][Hq][D] bf16.  MS_E_UNSUPPORTED unless D is a multiple
- * of 8, Hq / Hkv is 1, 2, 4 or 8 and (Hq / Hkv) (D + pos0 + T) <= 16000
- * (queries and scores of a work-group in LDS). */
+ * aligned), out [T][Hq][D] bf16.  MS_E_UNSUPPORTED unless D is a power
+ * of two in [8, 512], Hq / Hkv is 1, 2, 4 or 8 and
+ * (Hq / Hkv) (5 D + pos0 + T) <= 16000 (queries, scores and partial sums of
+ * a work-group in LDS; Mixtral's 4 x 128 heads: contexts up to 3360). */
 ms_status ms_attention(const void* q, const void* k_cache, const void* v_cache, int32_t T, int32_t Hq, int32_t Hkv,
                        int32_t D, int32_t pos0, int32_t max_ctx, void* out, void* stream);
 

@@ -159,8 +159,7 @@ __global__ void rope_kv_kernel(const float* __restrict__ qkv, int Hq, int Hkv, i
 //
 // Block (t, g): the G = Hq / Hkv query heads of key/value group g for token
 // t, over positions 0 .. pos0 + t.  Scores in LDS ([G][n]); softmax with the
-// row maximum subtracted; each thread then owns (head, column) outputs and
-// sums p * V over the positions.
+// row maximum subtracted; then p . V over the positions.
 template <int BLK>
 __device__ __forceinline__ float block_reduce(float v, bool is_max, float* red) {
 #pragma unroll
@@ -183,7 +182,7 @@ __global__ __launch_bounds__(kAttThreads) void attention_kernel(const uint16_t* 
                                                                 const uint16_t* __restrict__ vc, int Hq, int Hkv,
                                                                 int D, int pos0, int max_ctx,
                                                                 uint16_t* __restrict__ out) {
-  extern __shared__ __align__(16) float att_smem[];  // qf [G][D], then scores [G][n]
+  extern __shared__ __align__(16) float att_smem[];  // qf [G][D], scores [G][n], wave sums [4][G][D]
   __shared__ float red[kAttThreads / 64];
   const int t = blockIdx.x, g = blockIdx.y, tid = threadIdx.x;
   const int n = pos0 + t + 1;
@@ -226,12 +225,49 @@ __global__ __launch_bounds__(kAttThreads) void attention_kernel(const uint16_t* 
     for (int p = tid; p < n; p += kAttThreads) sc[h * n + p] /= sum;
   }
   __syncthreads();
+  // p . V: thread (position lane pl, column group cg) sums 8 columns of every
+  // head over positions pl, pl + PL, ... (one 16-byte V load serves all G
+  // heads); the position lanes of a wave are combined with shuffles, the
+  // waves' sums through LDS (after the scores, which stay in use until then)
+  const int CG = D / 8, PL = kAttThreads / CG;
+  const int cg = tid % CG, pl = tid / CG;
+  float acc[G][8];
+#pragma unroll
+  for (int h = 0; h < G; ++h)
+#pragma unroll
+    for (int e = 0; e < 8; ++e) acc[h][e] = 0.0f;
+  if (pl < PL) {
+    for (int p = pl; p < n; p += PL) {
+      float vf[8];
+      bf16x8_to_f32(*reinterpret_cast<const uint4*>(V + static_cast<size_t>(p) * D + 8 * cg), vf);
+#pragma unroll
+      for (int h = 0; h < G; ++h) {
+        const float pr = sc[h * n + p];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) acc[h][e] = fmaf(pr, vf[e], acc[h][e]);
+      }
+    }
+  }
+  // lanes l and l ^ (CG * 2^j) hold the same columns for other positions
+  for (int m = CG; m < 64; m <<= 1)
+#pragma unroll
+    for (int h = 0; h < G; ++h)
+#pragma unroll
+      for (int e = 0; e < 8; ++e) acc[h][e] += __shfl_xor(acc[h][e], m, 64);
+  float* wsum = sc + G * n;  // [waves][G][D]
+  const int lane = tid & 63, wave = tid >> 6;
+  if (lane < CG && CG <= 64) {
+#pragma unroll
+    for (int h = 0; h < G; ++h)
+#pragma unroll
+      for (int e = 0; e < 8; ++e) wsum[(wave * G + h) * D + 8 * cg + e] = acc[h][e];
+  }
+  __syncthreads();
   for (int o = tid; o < G * D; o += kAttThreads) {
+    float v = 0.0f;
+    for (int w = 0; w < kAttThreads / 64; ++w) v += wsum[w * G * D + o];
     const int h = o / D, col = o - h * D;
-    const float* pr = sc + h * n;
-    float acc = 0.0f;
-    for (int p = 0; p < n; ++p) acc = fmaf(pr[p], bf16_to_f32(V[static_cast<size_t>(p) * D + col]), acc);
-    out[(static_cast<size_t>(t) * Hq + g * G + h) * D + col] = f32_to_bf16(acc);
+    out[(static_cast<size_t>(t) * Hq + g * G + h) * D + col] = f32_to_bf16(v);
   }
 }
 
@@ -330,8 +366,9 @@ ms_status ms_attention(const void* q, const void* k_cache, const void* v_cache, 
   if (!q || !k_cache || !v_cache || !out || !aligned16(k_cache) || !aligned16(v_cache)) return MS_E_INVALID;
   if (Hq % Hkv != 0 || static_cast<int64_t>(pos0) + T > max_ctx) return MS_E_INVALID;
   const int G = Hq / Hkv;
-  if (D % 8 != 0 || G > 8 || static_cast<int64_t>(G) * (D + pos0 + T) > kAttMaxScores) return MS_E_UNSUPPORTED;
-  const size_t lds = sizeof(float) * static_cast<size_t>(G) * (D + pos0 + T);
+  if (D < 8 || D > 512 || (D & (D - 1)) != 0 || G > 8 || static_cast<int64_t>(G) * (5 * D + pos0 + T) > kAttMaxScores)
+    return MS_E_UNSUPPORTED;
+  const size_t lds = sizeof(float) * static_cast<size_t>(G) * (5 * D + pos0 + T);
   const hipStream_t s = static_cast<hipStream_t>(stream);
   const auto* qp = static_cast<const uint16_t*>(q);
   const auto* kp = static_cast<const uint16_t*>(k_cache);
