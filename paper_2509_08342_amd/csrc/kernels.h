@@ -177,7 +177,8 @@ struct MmaArgs {
   int32_t rows_shared;         // shared rows per expert (max T)
   int32_t n_tasks, n_wg;
   int32_t ncb;                 // down: column blocks (ceil(d / kMmaCols))
-  int32_t gu_split;            // gate/up: work-groups per chunk and row tile (1 or 4)
+  int32_t gu_split;            // gate/up: work-groups per chunk and row tile (1 or 4; 1 for b-bit chunks)
+  int32_t bits;                // 0: bf16 chunks; 2 or 4: b-bit chunks (q_chunk_bytes layout)
   MmaTask tasks[kMaxMmaTasks];
 };
 hipError_t launch_mma_gateup(const MmaArgs& a, hipStream_t s);

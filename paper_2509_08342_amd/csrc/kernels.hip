@@ -1776,8 +1776,282 @@ __global__ __launch_bounds__(256) void mma_down_kernel(MmaArgs a) {
   }
 }
 
+// ------------------------------------------- prefill MFMA over b-bit chunks
+//
+// The matrix cores take the code pairs as they are: a B fragment of eight
+// codes becomes eight bf16 values 1 + q / 2^b (the pair form of the b-bit
+// chunk kernel), so an MFMA over one 64-element group yields
+// acc = sum_k a_k (1 + q_k / 2^b) and the group adds s (2^b acc - (2^b + z)
+// asum) with asum = sum_k a_k of the same rows (one group's accumulator is
+// folded in after its two k-steps).  Gate/up: the LDS-staged layout of
+// mma_gateup_lds_kernel with each slab's per-row group sums beside it.
+// Down: a down column's 64 codes are one group and contiguous, so the B
+// fragments load straight from the chunk, without a transpose.
+
+// Code word of elements [kk, kk + 8) of a group (kk a multiple of 8), moved
+// so that they form pairs 0 .. 3.
+template <int BITS>
+__device__ __forceinline__ uint32_t q_word8(const uint32_t* group, int kk) {
+  if constexpr (BITS == 2) return group[kk >> 4] >> (kk & 8);  // 16 codes per word: the upper 8 by 8 bits
+  else return group[kk >> 3];                                 // 8 codes per word
+}
+
+template <int BITS>
+__device__ __forceinline__ uint4 q_frag(uint32_t w, const PairMasks<BITS>& pm) {
+  return make_uint4(code_pair<BITS, 0>(w, pm), code_pair<BITS, 1>(w, pm), code_pair<BITS, 2>(w, pm),
+                    code_pair<BITS, 3>(w, pm));
+}
+
+template <int BITS>
+__global__ __launch_bounds__(256) void mma_gateup_q_kernel(MmaArgs a) {
+  __shared__ __align__(16) uint16_t As[2][kMmaRows * kGuPitch];
+  __shared__ float asum[2][kMmaRows][2];  // per slab buffer: [row][group of the slab]
+  constexpr float C = static_cast<float>(1 << BITS);
+  constexpr int GW = 2 * BITS;  // code words per group
+  const PairMasks<BITS> pm;
+  const int wg = blockIdx.x;
+  const MmaTask tk = a.tasks[find_task(a.tasks, a.n_tasks, wg)];
+  const int local = wg - tk.wg_begin;
+  const int mt = local % tk.m_tiles;
+  const int c = tk.chunk_lo + local / tk.m_tiles;
+  const TileRows tr = tile_rows(a, tk, mt);
+  if (tr.n <= 0) return;  // uniform over the work-group
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int d = a.d, ngr = d / 64;
+  const int ksteps = d / 32;
+  const int nslab = (ksteps + 3) / 4;
+  const uint16_t* hrow[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int row = min((tid >> 4) + 16 * i, tr.n - 1);  // clamped rows: staged, never stored
+    const int tok = a.perm[tr.p0 + row] / a.K;  // b-bit experts are routed only
+    hrow[i] = static_cast<const uint16_t*>(a.h) + static_cast<size_t>(tok) * d + 8 * (tid & 15);
+  }
+  const unsigned char* chunk = tk.base + static_cast<size_t>(c) * a.chunk_bytes;
+  const size_t qrow = static_cast<size_t>(d) * BITS / 8;
+  const uint32_t* Gq = reinterpret_cast<const uint32_t*>(chunk);
+  const uint32_t* Uq = reinterpret_cast<const uint32_t*>(chunk + 64 * qrow);
+  const uint32_t* Gm = reinterpret_cast<const uint32_t*>(chunk + 192 * qrow);
+  const uint32_t* Um = Gm + 64 * ngr;
+  const int unit = 16 * wave + (lane & 15);
+  const int kq = 8 * (lane >> 4);
+  uint4 ast[4];
+  // per slab: two groups x (k-step words of G and U) + the groups' metadata
+  uint32_t gw[2][2], uw[2][2], gmn[2], umn[2];
+  uint32_t gwc[2][2], uwc[2][2], gmc[2], umc[2];
+  auto load_a = [&](int sl) {
+    const int k0 = min(sl, nslab - 1) * kGuSlab;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) ast[i] = ld16(hrow[i] + min(k0, d - kGuSlab));
+  };
+  auto store_a = [&](int buf) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      *reinterpret_cast<uint4*>(&As[buf][((tid >> 4) + 16 * i) * kGuPitch + 8 * (tid & 15)]) = ast[i];
+  };
+  auto load_b = [&](int sl) {
+#pragma unroll
+    for (int gi = 0; gi < 2; ++gi) {
+      const int g = min(2 * sl + gi, ngr - 1);  // clamped past the last group (loaded, not used)
+      const uint32_t* gq = Gq + (static_cast<size_t>(unit) * ngr + g) * GW;
+      const uint32_t* uq = Uq + (static_cast<size_t>(unit) * ngr + g) * GW;
+#pragma unroll
+      for (int s = 0; s < 2; ++s) {
+        gw[gi][s] = q_word8<BITS>(gq, 32 * s + kq);
+        uw[gi][s] = q_word8<BITS>(uq, 32 * s + kq);
+      }
+      gmn[gi] = Gm[static_cast<size_t>(unit) * ngr + g];
+      umn[gi] = Um[static_cast<size_t>(unit) * ngr + g];
+    }
+  };
+  // per-row sums of the staged slab's two 64-wide groups (window-relative)
+  auto row_sums = [&](int buf) {
+    if (tid < 2 * kMmaRows) {
+      const int row = tid >> 1, gi = tid & 1;
+      const uint4* src = reinterpret_cast<const uint4*>(&As[buf][row * kGuPitch + 64 * gi]);
+      float sum = 0.0f;
+#pragma unroll
+      for (int v = 0; v < 8; ++v) {
+        const uint4 x = src[v];
+        sum = dot2bf(x.x, kBf16OnePair, sum);
+        sum = dot2bf(x.y, kBf16OnePair, sum);
+        sum = dot2bf(x.z, kBf16OnePair, sum);
+        sum = dot2bf(x.w, kBf16OnePair, sum);
+      }
+      asum[buf][row][gi] = sum;
+    }
+  };
+  f32x4_t ag[4], au[4];
+#pragma unroll
+  for (int rb = 0; rb < 4; ++rb) ag[rb] = au[rb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  load_a(0);
+  load_b(0);
+  store_a(0);
+  __syncthreads();
+  row_sums(0);
+  __syncthreads();
+  for (int sl = 0; sl < nslab; ++sl) {
+    const int buf = sl & 1;
+#pragma unroll
+    for (int gi = 0; gi < 2; ++gi) {
+#pragma unroll
+      for (int s = 0; s < 2; ++s) {
+        gwc[gi][s] = gw[gi][s];
+        uwc[gi][s] = uw[gi][s];
+      }
+      gmc[gi] = gmn[gi];
+      umc[gi] = umn[gi];
+    }
+    load_a(sl + 1);
+    load_b(sl + 1);
+    const int k0 = sl * kGuSlab, kbase = k0 - min(k0, d - kGuSlab);  // a partial last slab sits at the window's end
+#pragma unroll
+    for (int gi = 0; gi < 2; ++gi) {
+      if (2 * sl + gi < ngr) {
+        const int wgi = (kbase >> 6) + gi;  // the group's half of the staged window
+        const float gs = fp16_lo(gmc[gi]), gz = C + fp16_hi(gmc[gi]);
+        const float us = fp16_lo(umc[gi]), uz = C + fp16_hi(umc[gi]);
+        const uint4 bg0 = q_frag<BITS>(gwc[gi][0], pm), bg1 = q_frag<BITS>(gwc[gi][1], pm);
+        const uint4 bu0 = q_frag<BITS>(uwc[gi][0], pm), bu1 = q_frag<BITS>(uwc[gi][1], pm);
+#pragma unroll
+        for (int rb = 0; rb < 4; ++rb) {
+          if (16 * rb < tr.n) {
+            const uint16_t* ar = &As[buf][(16 * rb + (lane & 15)) * kGuPitch + 64 * wgi + kq];
+            const bf16x8_t A0 = as_bf16x8(*reinterpret_cast<const uint4*>(ar));
+            const bf16x8_t A1 = as_bf16x8(*reinterpret_cast<const uint4*>(ar + 32));
+            f32x4_t cg = mfma16(A0, as_bf16x8(bg0), f32x4_t{0.f, 0.f, 0.f, 0.f});
+            cg = mfma16(A1, as_bf16x8(bg1), cg);
+            f32x4_t cu = mfma16(A0, as_bf16x8(bu0), f32x4_t{0.f, 0.f, 0.f, 0.f});
+            cu = mfma16(A1, as_bf16x8(bu1), cu);
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+              const float xs = asum[buf][16 * rb + 4 * (lane >> 4) + r][wgi];
+              ag[rb][r] += gs * (C * cg[r] - gz * xs);
+              au[rb][r] += us * (C * cu[r] - uz * xs);
+            }
+          }
+        }
+      }
+    }
+    if (sl + 1 < nslab) {
+      store_a(buf ^ 1);
+      __syncthreads();
+      row_sums(buf ^ 1);
+    }
+    __syncthreads();
+  }
+  uint16_t* act = a.act;  // b-bit experts are routed only
+  const int f = c * kChunkUnits + unit;
+#pragma unroll
+  for (int rb = 0; rb < 4; ++rb) {
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int row = 16 * rb + 4 * (lane >> 4) + r;
+      if (row < tr.n) act[static_cast<size_t>(tr.p0 + row) * a.f_pad + f] = f2bf(silu(ag[rb][r]) * au[rb][r]);
+    }
+  }
+}
+
+template <int BITS>
+__global__ __launch_bounds__(256) void mma_down_q_kernel(MmaArgs a) {
+  constexpr float C = static_cast<float>(1 << BITS);
+  constexpr int GW = 2 * BITS;  // code words per column group
+  constexpr int NF = kMmaCols / 16;
+  const PairMasks<BITS> pm;
+  const int wg = blockIdx.x;
+  const MmaTask tk = a.tasks[find_task(a.tasks, a.n_tasks, wg)];
+  const int local = wg - tk.wg_begin;
+  const int mt = local / a.ncb, cb = local % a.ncb;
+  const TileRows tr = tile_rows(a, tk, mt);
+  if (tr.n <= 0) return;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  if (16 * wave >= tr.n) return;  // no rows for this wave (no barrier in this kernel)
+  const int d = a.d;
+  const size_t qrow = static_cast<size_t>(d) * BITS / 8;
+  const int ar = min(16 * wave + (lane & 15), tr.n - 1);
+  const uint16_t* arow = a.act + static_cast<size_t>(tr.p0 + ar) * a.f_pad;
+  const int kq = 8 * (lane >> 4);
+  const int col0 = cb * kMmaCols;
+  f32x4_t acc[NF];
+#pragma unroll
+  for (int nf = 0; nf < NF; ++nf) acc[nf] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  // one chunk: the A fragments of its 64 units, and per column block this
+  // lane's two code words and the column's metadata
+  uint4 an[2], ac[2];
+  uint32_t wn[NF][2], mn[NF], wc[NF][2], mc[NF];
+  auto load_chunk = [&](int cc) {
+    const unsigned char* cbase = (cc < tk.split ? tk.base : tk.base2) + static_cast<size_t>(cc) * a.chunk_bytes;
+    const uint32_t* Dq = reinterpret_cast<const uint32_t*>(cbase + 128 * qrow);
+    const uint32_t* Dm = reinterpret_cast<const uint32_t*>(cbase + 192 * qrow) + 128 * (d / 64);
+#pragma unroll
+    for (int nf = 0; nf < NF; ++nf) {
+      const int col = min(col0 + 16 * nf + (lane & 15), d - 1);  // clamped; columns past d are never stored
+      const uint32_t* grp = Dq + static_cast<size_t>(col) * GW;
+      wn[nf][0] = q_word8<BITS>(grp, kq);
+      wn[nf][1] = q_word8<BITS>(grp, 32 + kq);
+      mn[nf] = Dm[col];
+    }
+#pragma unroll
+    for (int ks = 0; ks < 2; ++ks) an[ks] = ld16(arow + cc * kChunkUnits + 32 * ks + kq);
+  };
+  const int nc = tk.n_chunks;
+  load_chunk(0);
+  for (int cc = 0; cc < nc; ++cc) {
+#pragma unroll
+    for (int nf = 0; nf < NF; ++nf) {
+      wc[nf][0] = wn[nf][0];
+      wc[nf][1] = wn[nf][1];
+      mc[nf] = mn[nf];
+    }
+    ac[0] = an[0];
+    ac[1] = an[1];
+    load_chunk(min(cc + 1, nc - 1));  // the last chunk reloads itself (in bounds, unused)
+    // the chunk's activation sum of each row: this lane's 16 values, then the
+    // four lanes of the row; rows of the result layout come from lane row
+    float xs = 0.0f;
+    const uint32_t av[8] = {ac[0].x, ac[0].y, ac[0].z, ac[0].w, ac[1].x, ac[1].y, ac[1].z, ac[1].w};
+#pragma unroll
+    for (int i = 0; i < 8; ++i) xs = dot2bf(av[i], kBf16OnePair, xs);
+    xs += __shfl_xor(xs, 16, 64);
+    xs += __shfl_xor(xs, 32, 64);
+    float rs[4];
+#pragma unroll
+    for (int r = 0; r < 4; ++r) rs[r] = __shfl(xs, 4 * (lane >> 4) + r, 64);
+    const bf16x8_t A0 = as_bf16x8(ac[0]), A1 = as_bf16x8(ac[1]);
+#pragma unroll
+    for (int nf = 0; nf < NF; ++nf) {
+      f32x4_t cacc = mfma16(A0, as_bf16x8(q_frag<BITS>(wc[nf][0], pm)), f32x4_t{0.f, 0.f, 0.f, 0.f});
+      cacc = mfma16(A1, as_bf16x8(q_frag<BITS>(wc[nf][1], pm)), cacc);
+      const float s = fp16_lo(mc[nf]), z = C + fp16_hi(mc[nf]);
+#pragma unroll
+      for (int r = 0; r < 4; ++r) acc[nf][r] += s * (C * cacc[r] - z * rs[r]);
+    }
+  }
+#pragma unroll
+  for (int nf = 0; nf < NF; ++nf) {
+    const int col = col0 + 16 * nf + (lane & 15);
+    if (col < d) {
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int row = 16 * wave + 4 * (lane >> 4) + r;
+        if (row < tr.n) a.part[static_cast<size_t>(tr.p0 + row) * d + col] = acc[nf][r];
+      }
+    }
+  }
+}
+
 hipError_t launch_mma_gateup(const MmaArgs& a, hipStream_t s) {
   if (a.n_wg <= 0 || a.n_tasks <= 0) return hipSuccess;
+  if (a.bits != 0) {
+    if (a.gu_split != 1 || !q_supported(a.d)) return hipErrorInvalidValue;
+    if (a.bits == 2)
+      hipLaunchKernelGGL(mma_gateup_q_kernel<2>, dim3(a.n_wg), dim3(256), 0, s, a);
+    else if (a.bits == 4)
+      hipLaunchKernelGGL(mma_gateup_q_kernel<4>, dim3(a.n_wg), dim3(256), 0, s, a);
+    else
+      return hipErrorInvalidValue;
+    return hipGetLastError();
+  }
   if (a.gu_split == 4)
     hipLaunchKernelGGL(mma_gateup_kernel<1>, dim3(a.n_wg), dim3(256), 0, s, a);
   else if (a.gu_split == 1 && a.d >= kGuSlab)
@@ -1791,6 +2065,16 @@ hipError_t launch_mma_gateup(const MmaArgs& a, hipStream_t s) {
 
 hipError_t launch_mma_down(const MmaArgs& a, hipStream_t s) {
   if (a.n_wg <= 0 || a.n_tasks <= 0) return hipSuccess;
+  if (a.bits != 0) {
+    if (!q_supported(a.d)) return hipErrorInvalidValue;
+    if (a.bits == 2)
+      hipLaunchKernelGGL(mma_down_q_kernel<2>, dim3(a.n_wg), dim3(256), 0, s, a);
+    else if (a.bits == 4)
+      hipLaunchKernelGGL(mma_down_q_kernel<4>, dim3(a.n_wg), dim3(256), 0, s, a);
+    else
+      return hipErrorInvalidValue;
+    return hipGetLastError();
+  }
   hipLaunchKernelGGL(mma_down_kernel, dim3(a.n_wg), dim3(256), 0, s, a);
   return hipGetLastError();
 }

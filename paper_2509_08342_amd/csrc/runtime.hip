@@ -168,7 +168,7 @@ ms_status derive_shape(const ms_model_desc* d, Shape* s, std::string* err) {
   // slot and per shared expert and token
   s->off_act = off;
   s->off_act_sh = off;
-  if (s->dtype == MS_BF16 && s->bits == 0) {
+  if (s->dtype == MS_BF16) {
     off += align_up(TK * s->n_chunks * kUnits * 2, kAlign);
     s->off_act_sh = off;
     off += align_up(static_cast<uint64_t>(s->n_sh) * s->max_T * s->n_chunks_sh * kUnits * 2, kAlign);
@@ -839,8 +839,9 @@ ms_status prefill_experts(ms_ctx* ctx, int layer, const void* h_dev, int T, cons
                           hipStream_t sm) {
   const Shape& s = ctx->s;
   LayerState& L = ctx->layers[layer];
-  const uint64_t gu_bytes = 2ull * kUnits * s.d * s.elem;  // gate + up bytes of one chunk
-  const uint64_t dn_bytes = 1ull * kUnits * s.d * s.elem;  // down bytes of one chunk
+  // gate + up and down bytes of one chunk (b-bit: codes and their metadata)
+  const uint64_t gu_bytes = s.bits ? 2 * (msk::q_off_uq(s.d, s.bits) + 4ull * s.d) : 2ull * kUnits * s.d * s.elem;
+  const uint64_t dn_bytes = s.bits ? msk::q_off_uq(s.d, s.bits) + 4ull * s.d : 1ull * kUnits * s.d * s.elem;
   msk::MmaArgs ma{};
   ma.h = h_dev;
   ma.offsets = reinterpret_cast<const int32_t*>(ctx->dev(s.off_offsets));
@@ -858,6 +859,7 @@ ms_status prefill_experts(ms_ctx* ctx, int layer, const void* h_dev, int T, cons
   ma.f_pad_sh = s.n_chunks_sh * kUnits;
   ma.rows_shared = s.max_T;
   ma.ncb = (s.d + msk::kMmaCols - 1) / msk::kMmaCols;
+  ma.bits = s.bits;
   auto m_tiles = [&](int e) {
     const int n = e >= 0 ? offs[e + 1] - offs[e] : T;
     return (n + msk::kMmaRows - 1) / msk::kMmaRows;
@@ -871,7 +873,7 @@ ms_status prefill_experts(ms_ctx* ctx, int layer, const void* h_dev, int T, cons
       ma.n_tasks = static_cast<int>(i1 - i0);
       int tiles = 0;
       for (size_t i = i0; i < i1; ++i) tiles += tasks[i].m_tiles * tasks[i].n_chunks;
-      ma.gu_split = tiles < msk::kGuSplitBelow ? 4 : 1;
+      ma.gu_split = (tiles < msk::kGuSplitBelow && s.bits == 0) ? 4 : 1;
       int wg = 0;
       uint64_t bytes = 0;
       for (size_t i = i0; i < i1; ++i) {
@@ -1588,7 +1590,7 @@ ms_status ms_forward(ms_ctx* ctx, int32_t layer, const void* h_dev, int32_t T, f
   // or prefill path (matrix cores, launched once the token counts are known)
   bool prefill = s.dtype == MS_BF16 && static_cast<int64_t>(T) * s.K >= 8ll * s.E;
   if (flags & MS_FWD_MATRIX_CORES) prefill = s.dtype == MS_BF16;
-  if ((flags & MS_FWD_NO_MATRIX_CORES) || s.bits != 0) prefill = false;  // b-bit experts: chunk kernel only
+  if (flags & MS_FWD_NO_MATRIX_CORES) prefill = false;
 
   // 2. segments already in VRAM (Eq. (5): processed while missing ones
   //    load): cached tops, staging-buffer groups of this layer whose copies

@@ -90,3 +90,15 @@ def test_quantized_entry_points_reject_the_other_format():
         with pytest.raises(ms.MoeSplitError) as ei:
             ms.ms_set_expert_q(r2.ctx, 0, 0, qe.codes, qe.meta)
         assert ei.value.status == ms.MS_E_STATE
+
+
+@pytest.mark.parametrize("T", [3, 64, 70])
+def test_quantized_matrix_core_and_chunk_paths_match_oracle(rig, T):
+    """The matrix-core prefill over b-bit chunks (code pairs as bf16 B
+    fragments, scale and zero folded per group) and the chunk kernel both
+    match the oracle at partial and full row tiles."""
+    from paper_2509_08342_amd import moesplit as ms
+    h, hf = rig.hidden(T, tag=600 + T)
+    for flag in (ms.MS_FWD_MATRIX_CORES, ms.MS_FWD_NO_MATRIX_CORES):
+        y, idx, w = _run(rig, h, T, flag)
+        check_layer(rig, 0, hf, y, idx, w)
