@@ -378,8 +378,11 @@ ms_status ms_set_cache_policy(ms_ctx* ctx, int32_t policy, double rho, double om
  * kernels that run beside the copy, except while the copy stream waits for
  * unfinished work of another stream (a staging slot's previous reader, a
  * layer's last forward): those copies still run as the kernel, ordered on
- * the GPU (a DMA transfer queued behind such a wait can hold the host in the
- * runtime's copy call).  Results do not depend on the engine. */
+ * the GPU (a DMA transfer queued behind such a wait can stall for
+ * milliseconds).  Switching to MS_COPY_DMA first makes one 1 MiB DMA
+ * transfer into the library's workspace and waits for it (the first DMA
+ * transfer of a process is slow); MS_E_NOMEM if its pinned source cannot be
+ * allocated.  Results do not depend on the engine. */
 typedef enum {
   MS_COPY_KERNEL = 0,
   MS_COPY_DMA = 1

@@ -405,6 +405,7 @@ struct ms_ctx {
   // engines except while the copy stream waits on unfinished work of
   // another stream (copy_waits)
   int copy_engine = MS_COPY_KERNEL;
+  bool dma_warm = false;  // a DMA transfer has completed in this context
   std::vector<hipEvent_t> copy_waits;
   // pinned host store
   std::vector<unsigned char*> blobs;      // pinned, coherent host memory (never cached by the GPU)
@@ -2112,6 +2113,29 @@ ms_status ms_set_cache_policy(ms_ctx* ctx, int32_t policy, double rho, double om
 ms_status ms_set_copy_engine(ms_ctx* ctx, int32_t engine) {
   MS_CHECK_CTX(ctx);
   if (engine != MS_COPY_KERNEL && engine != MS_COPY_DMA) return fail(ctx, MS_E_INVALID, "unknown copy engine");
+  if (engine == MS_COPY_DMA && !ctx->dma_warm) {
+    // the first DMA transfer of a process takes milliseconds (copies under
+    // 64 KiB do not absorb that): pay it here, into the partials workspace,
+    // which holds nothing between forwards
+    constexpr uint64_t kWarmBytes = 1ull << 20;
+    const uint64_t n = std::min<uint64_t>(kWarmBytes, ctx->s.part_bytes);
+    void* hp = nullptr;
+    if (n > 0 && hipHostMalloc(&hp, n, hipHostMallocDefault) == hipSuccess && hp) {
+      std::memset(hp, 0, n);
+      ms_status st = ms_sync(ctx);
+      if (st == MS_OK) {
+        hipError_t e = hipMemcpyAsync(ctx->dev(ctx->s.off_part), hp, n, hipMemcpyHostToDevice, ctx->copy);
+        if (e == hipSuccess) e = hipStreamSynchronize(ctx->copy);
+        if (e != hipSuccess) st = poison(ctx, "DMA warm-up copy", e);
+      }
+      (void)hipHostFree(hp);
+      if (st != MS_OK) return st;
+      ctx->dma_warm = true;
+    } else {
+      (void)hipGetLastError();
+      return fail(ctx, MS_E_NOMEM, "pinned buffer for the DMA warm-up copy");
+    }
+  }
   ctx->copy_engine = engine;
   return MS_OK;
 }
