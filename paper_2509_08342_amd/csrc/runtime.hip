@@ -28,7 +28,12 @@ namespace {
 
 constexpr int kUnits = msk::kChunkUnits;
 constexpr uint64_t kAlign = 256;
-constexpr uint64_t kGroupTargetBytes = 16ull << 20;  // H2D copy granularity
+// H2D copy granularity: prefetch copies are speculative and dropped when the
+// routing arrives, so they go in small groups; a miss is needed whole, so its
+// copies go in large groups (each copy launch leaves a gap of ~12 us on the
+// link; measured on the Mixtral decode layer and the 32-layer stack)
+constexpr uint64_t kGroupTargetBytes = 16ull << 20;
+constexpr uint64_t kMissGroupTargetBytes = 64ull << 20;
 constexpr int kPrefetchWindow = 2;                   // prefetch groups in flight
 constexpr int kMaxD = msk::kMaxModelDim;
 constexpr int kReserved = 1 << 30;                   // BufSlot::use_order of a reserved slot
@@ -42,7 +47,8 @@ struct Shape {
   uint64_t chunk_bytes;
   int n_chunks, n_chunks_sh;
   uint64_t expert_bytes, shared_bytes;
-  int group_chunks;  // chunks per H2D copy group
+  int group_chunks;       // chunks per H2D copy group of a prefetch
+  int miss_group_chunks;  // ... of a miss
   // fixed pool layout (byte offsets)
   uint64_t off_router, off_bias, off_shared, off_logits, off_logits2, off_offsets, off_perm, off_pos;
   uint64_t off_part, off_part_sh, off_red, off_act, off_act_sh, off_score, off_order, off_buffer, fixed_bytes;
@@ -107,6 +113,7 @@ ms_status derive_shape(const ms_model_desc* d, Shape* s, std::string* err) {
   s->expert_bytes = s->chunk_bytes * s->n_chunks;
   s->shared_bytes = s->chunk_bytes * s->n_chunks_sh;
   s->group_chunks = static_cast<int>(std::max<uint64_t>(1, kGroupTargetBytes / s->chunk_bytes));
+  s->miss_group_chunks = static_cast<int>(std::max<uint64_t>(1, kMissGroupTargetBytes / s->chunk_bytes));
   // work-groups per chunk: one for experts of many chunks (each work-group
   // then streams more bytes, and fewer partial planes reach the combine),
   // two otherwise, doubled until the experts a forward can activate give
@@ -568,7 +575,7 @@ hipError_t group_landed(ms_ctx* ctx, int si, int gi) {
 
 // Point a staging slot at (layer, e) covering chunks [first, n_chunks).  The
 // copy stream first waits for the slot's previous readers.
-ms_status assign_slot(ms_ctx* ctx, int si, int layer, int e, int first) {
+ms_status assign_slot(ms_ctx* ctx, int si, int layer, int e, int first, bool miss) {
   BufSlot& b = ctx->buf[si];
   if (b.has_last_read) {
     const ms_status st = copy_after(ctx, b.last_read);
@@ -578,9 +585,9 @@ ms_status assign_slot(ms_ctx* ctx, int si, int layer, int e, int first) {
   b.expert = e;
   b.first_chunk = first;
   b.groups.clear();
-  // at most group_chunks per copy, in groups of near-equal size (a small
-  // tail copy runs far below the link rate)
-  const int n = ctx->s.n_chunks, G = ctx->s.group_chunks;
+  // at most (miss_)group_chunks per copy, in groups of near-equal size (a
+  // small tail copy runs far below the link rate)
+  const int n = ctx->s.n_chunks, G = miss ? ctx->s.miss_group_chunks : ctx->s.group_chunks;
   const int ng = (n - first + G - 1) / G;
   const int per = ng > 0 ? (n - first + ng - 1) / ng : 1;
   for (int c = first; c < n; c += per) {
@@ -728,7 +735,7 @@ ms_status enqueue_prefetch(ms_ctx* ctx, int layer, const int32_t* experts, int n
     for (const PendingGroup& pg : ctx->pf_queue) queued = queued || pg.slot == si;
     for (const PendingGroup& pg : ctx->pf_inflight) queued = queued || pg.slot == si;
     if (queued) break;
-    ms_status st = assign_slot(ctx, si, layer, e, res);
+    ms_status st = assign_slot(ctx, si, layer, e, res, false);
     if (st != MS_OK) return st;
     ctx->buf[si].tick = ++ctx->tick;
     for (int gi = 0; gi < static_cast<int>(ctx->buf[si].groups.size()); ++gi)
@@ -987,7 +994,7 @@ ms_status prefill_experts(ms_ctx* ctx, int layer, const void* h_dev, int T, cons
       si = find_slot(ctx, layer, e);
       if (si < 0 || ctx->buf[si].first_chunk > res) si = pick_victim(ctx, true);
       if (si < 0) return fail(ctx, MS_E_STATE, "no staging slot can be taken");
-      st = assign_slot(ctx, si, layer, e, res);
+      st = assign_slot(ctx, si, layer, e, res, true);
       if (st != MS_OK) return st;
     }
     BufSlot& b = ctx->buf[si];
@@ -1823,7 +1830,7 @@ ms_status ms_forward(ms_ctx* ctx, int32_t layer, const void* h_dev, int32_t T, f
     } else {
       if (si < 0) si = pick_victim(ctx, true);
       if (si < 0) return fail(ctx, MS_E_STATE, "no staging slot can be taken");
-      st = assign_slot(ctx, si, layer, e, res);
+      st = assign_slot(ctx, si, layer, e, res, true);
       if (st != MS_OK) return st;
     }
     if (hit) L.st.buffer_hits += 1;
