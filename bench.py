@@ -33,7 +33,7 @@ HBM_PEAK_GBPS = 8000.0
 GIB = 1 << 30
 PROFILES = os.path.join(ROOT, "profiles")
 CALIB_BYTES = 256 << 20   # device-to-device copy that calibrates the PMC byte counters
-FFN_KERNELS = ("ffn_chunk_kernel", "mma_gateup_kernel", "mma_down_kernel")
+FFN_KERNELS = ("ffn_chunk_kernel", "ffn_q_kernel", "mma_gateup", "mma_down")
 
 
 def kernel_sources_sha():
@@ -205,6 +205,23 @@ def analyse(tl, steps, ms_per_step):
         miss_bytes=sum(r["bytes"] for r in by.get("copy_miss", [])),
         prefetch_bytes=sum(r["bytes"] for r in by.get("copy_prefetch", [])),
     )
+
+
+PCIE_GEN5_X16_GBPS = 32.0 * 16 * 128 / 130 / 8  # 63.0 GB/s per direction: 32 GT/s x 16 lanes, 128b/130b
+
+
+def copy_roofline(tl):
+    """Host-to-device segment copies (the copy kernel or the DMA engines):
+    bytes per copy / average copy duration against the PCIe 5.0 x16 link."""
+    rs = [r for r in tl if r["kind"] in COPY_KINDS]
+    dur = sum(r["t1_ms"] - r["t0_ms"] for r in rs)
+    if not rs or dur <= 0:
+        return None
+    b = sum(r["bytes"] for r in rs)
+    gbps = b / (dur * 1e-3) / 1e9
+    return dict(bound="pcie", achieved=round(gbps, 2), peak=round(PCIE_GEN5_X16_GBPS, 2), unit="GB/s",
+                frac=round(gbps / PCIE_GEN5_X16_GBPS, 4), launches=len(rs),
+                avg_launch_us=round(dur / len(rs) * 1e3, 2), bytes_per_launch=int(b / len(rs)))
 
 
 def ffn_roofline(an):
@@ -780,6 +797,8 @@ def main():
                    "top_k": shape.top_k, "n_shared": shape.n_shared, "r": r, "tokens_per_step": T,
                    "expert_bits": shape.expert_bits or None},
         "roofline": roof,
+        # the layer as a whole is bound by the link its missing segments cross
+        "copy_roofline": copy_roofline(tl),
         "tokens_per_s": round(T * 1e3 / ms_plain, 2),
         "h2d_gbps": None if an["h2d_gbps"] is None else round(an["h2d_gbps"], 2),
         "overlap": {"h2d_hidden_frac": an["hidden_frac"], "compute_hidden_frac": an["compute_hidden_frac"],
