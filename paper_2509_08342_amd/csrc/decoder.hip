@@ -8,6 +8,7 @@
 
 #include <cstdint>
 
+#include "kernels.h"
 #include "moesplit.h"
 
 namespace {
@@ -353,7 +354,7 @@ ms_status ms_rope_kv(const float* qkv, int32_t T, int32_t Hq, int32_t Hkv, int32
   if (!qkv || !q_out || !k_cache || !v_cache) return MS_E_INVALID;
   if (D % 2 != 0 || Hq % Hkv != 0) return MS_E_INVALID;
   if (static_cast<int64_t>(pos0) + T > max_ctx) return MS_E_INVALID;
-  hipLaunchKernelGGL(rope_kv_kernel, dim3(T, Hq + 2 * Hkv), dim3(64), 0, static_cast<hipStream_t>(stream), qkv, Hq,
+  hipLaunchKernelGGL(rope_kv_kernel, dim3(T, Hq + 2 * Hkv), dim3(64), msk::kGuardLds, static_cast<hipStream_t>(stream), qkv, Hq,
                      Hkv, D, pos0, log2(base), static_cast<uint16_t*>(q_out), static_cast<uint16_t*>(k_cache),
                      static_cast<uint16_t*>(v_cache), max_ctx);
   return launched();
@@ -398,7 +399,7 @@ ms_status ms_embed(const int32_t* ids, const void* table, int32_t n_vocab, int32
   if (T < 0 || n_vocab <= 0 || d <= 0) return MS_E_INVALID;
   if (T == 0) return MS_OK;
   if (!ids || !table || !out || !aligned16(table) || !aligned16(out) || d % 8 != 0) return MS_E_INVALID;
-  hipLaunchKernelGGL(embed_kernel, dim3(T), dim3(256), 0, static_cast<hipStream_t>(stream), ids,
+  hipLaunchKernelGGL(embed_kernel, dim3(T), dim3(256), msk::kGuardLds, static_cast<hipStream_t>(stream), ids,
                      static_cast<const uint16_t*>(table), n_vocab, d, static_cast<uint16_t*>(out));
   return launched();
 }

@@ -187,12 +187,24 @@ hipError_t launch_mma_down(const MmaArgs& a, hipStream_t s);
 // Host-to-device copy of `bytes` (a multiple of 16; both addresses 16-byte
 // aligned) from pinned host memory that the device can address (src is its
 // device-side address) into device memory, by a streaming kernel of
-// kH2dWorkGroups work-groups.  Unlike a DMA-engine copy, it orders after
-// other streams' work through ordinary kernel-to-kernel dependencies.
-constexpr int kH2dWorkGroups = 32;
+// kH2dWorkGroups work-groups of kH2dThreads threads.  Unlike a DMA-engine
+// copy, it orders after other streams' work through ordinary kernel-to-
+// kernel dependencies.
+//
+// Reads of host memory stay in flight for microseconds, and a work-group
+// that shares a CU with them waits behind them: an HBM-bound FFN launch
+// beside a copy ran 2.8x slower than alone while their work-groups could
+// share CUs, 1.2x while they could not.  So each copy work-group holds all
+// of its CU's LDS (kCuLdsBytes), which keeps every work-group that requests
+// LDS off that CU, and kernels that need no LDS request kGuardLds bytes at
+// launch for the same reason.
+constexpr int kH2dWorkGroups = 16;
+constexpr int kH2dThreads = 512;
+constexpr unsigned kCuLdsBytes = 160 * 1024;  // LDS of one gfx950 CU
+constexpr unsigned kGuardLds = 64;
 hipError_t launch_h2d(void* dst, const void* src, uint64_t bytes, hipStream_t s);
-// The same kernel for a device-to-device copy, over enough work-groups to
-// run at HBM rate.
+// A streaming kernel for a device-to-device copy (no LDS held), over enough
+// work-groups to run at HBM rate.
 constexpr int kD2dWorkGroups = 1024;
 hipError_t launch_d2d(void* dst, const void* src, uint64_t bytes, hipStream_t s);
 

@@ -725,9 +725,9 @@ hipError_t launch_logits_route(const LogitsArgs& a, const RouteArgs& ra, hipStre
     const int nb = (a.E + kLmExperts - 1) / kLmExperts;
     const dim3 grid((a.T + kLmTokens - 1) / kLmTokens, nb * mats);
     if (a.dtype == kBF16)
-      hipLaunchKernelGGL(logits_many_kernel<uint16_t>, grid, dim3(256), 0, s, b);
+      hipLaunchKernelGGL(logits_many_kernel<uint16_t>, grid, dim3(256), kGuardLds, s, b);
     else
-      hipLaunchKernelGGL(logits_many_kernel<float>, grid, dim3(256), 0, s, b);
+      hipLaunchKernelGGL(logits_many_kernel<float>, grid, dim3(256), kGuardLds, s, b);
   } else {
     const int n_out = a.T * a.E * mats;
     if (n_out <= kFusedLogits) {  // one launch for logits and route
@@ -739,9 +739,9 @@ hipError_t launch_logits_route(const LogitsArgs& a, const RouteArgs& ra, hipStre
     }
     const dim3 grid((n_out + 3) / 4);
     if (a.dtype == kBF16)
-      hipLaunchKernelGGL(logits_wave_kernel<uint16_t>, grid, dim3(256), 0, s, b);
+      hipLaunchKernelGGL(logits_wave_kernel<uint16_t>, grid, dim3(256), kGuardLds, s, b);
     else
-      hipLaunchKernelGGL(logits_wave_kernel<float>, grid, dim3(256), 0, s, b);
+      hipLaunchKernelGGL(logits_wave_kernel<float>, grid, dim3(256), kGuardLds, s, b);
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
@@ -754,7 +754,7 @@ hipError_t launch_logits_route(const LogitsArgs& a, const RouteArgs& ra, hipStre
   hipLaunchKernelGGL(scan_many_kernel, dim3(1), dim3(64 * kScanWaves), 0, s, ra, nblk);
   if ((e = hipGetLastError()) != hipSuccess) return e;
   if (ra.logits != nullptr) {
-    hipLaunchKernelGGL(scatter_many_kernel, dim3((a.T * ra.K + 255) / 256), dim3(256), 0, s, ra, TB);
+    hipLaunchKernelGGL(scatter_many_kernel, dim3((a.T * ra.K + 255) / 256), dim3(256), kGuardLds, s, ra, TB);
     if ((e = hipGetLastError()) != hipSuccess) return e;
   }
   return hipSuccess;
@@ -2053,11 +2053,11 @@ hipError_t launch_mma_gateup(const MmaArgs& a, hipStream_t s) {
     return hipGetLastError();
   }
   if (a.gu_split == 4)
-    hipLaunchKernelGGL(mma_gateup_kernel<1>, dim3(a.n_wg), dim3(256), 0, s, a);
+    hipLaunchKernelGGL(mma_gateup_kernel<1>, dim3(a.n_wg), dim3(256), kGuardLds, s, a);
   else if (a.gu_split == 1 && a.d >= kGuSlab)
     hipLaunchKernelGGL(mma_gateup_lds_kernel, dim3(a.n_wg), dim3(256), 0, s, a);
   else if (a.gu_split == 1)
-    hipLaunchKernelGGL(mma_gateup_kernel<4>, dim3(a.n_wg), dim3(256), 0, s, a);
+    hipLaunchKernelGGL(mma_gateup_kernel<4>, dim3(a.n_wg), dim3(256), kGuardLds, s, a);
   else
     return hipErrorInvalidValue;
   return hipGetLastError();
@@ -2068,9 +2068,9 @@ hipError_t launch_mma_down(const MmaArgs& a, hipStream_t s) {
   if (a.bits != 0) {
     if (!q_supported(a.d)) return hipErrorInvalidValue;
     if (a.bits == 2)
-      hipLaunchKernelGGL(mma_down_q_kernel<2>, dim3(a.n_wg), dim3(256), 0, s, a);
+      hipLaunchKernelGGL(mma_down_q_kernel<2>, dim3(a.n_wg), dim3(256), kGuardLds, s, a);
     else if (a.bits == 4)
-      hipLaunchKernelGGL(mma_down_q_kernel<4>, dim3(a.n_wg), dim3(256), 0, s, a);
+      hipLaunchKernelGGL(mma_down_q_kernel<4>, dim3(a.n_wg), dim3(256), kGuardLds, s, a);
     else
       return hipErrorInvalidValue;
     return hipGetLastError();
@@ -2155,49 +2155,61 @@ hipError_t launch_residual_norm(const void* h, const float* y, void* out, int T,
 
 // --------------------------------------------------------------- H2D copy
 //
-// Each work-group moves 256 x kH2dUnroll 16-byte pieces per round (all loads
-// of a round issued before its stores), rounds strided over the grid.  32
-// work-groups keep enough PCIe reads in flight to reach the link rate.
+// Each work-group moves NTH x kH2dUnroll 16-byte pieces per round (all loads
+// of a round issued before its stores), rounds strided over the grid.  The
+// host copy's 16 work-groups of 512 threads keep enough PCIe reads in flight
+// to reach the link rate; each holds its CU's LDS (never touched: the
+// allocation alone keeps other work-groups that request LDS off the CU).
 
 constexpr int kH2dUnroll = 4;
 
-__global__ __launch_bounds__(256) void h2d_kernel(uint4* __restrict__ dst, const uint4* __restrict__ src,
-                                                  uint64_t n) {
-  const uint64_t stride = static_cast<uint64_t>(gridDim.x) * 256 * kH2dUnroll;
-  for (uint64_t base = static_cast<uint64_t>(blockIdx.x) * 256 * kH2dUnroll + threadIdx.x; base < n;
+template <int NTH, bool HOLD_CU>
+__global__ __launch_bounds__(NTH) void copy_kernel(uint4* __restrict__ dst, const uint4* __restrict__ src,
+                                                   uint64_t n) {
+  const uint64_t stride = static_cast<uint64_t>(gridDim.x) * NTH * kH2dUnroll;
+  for (uint64_t base = static_cast<uint64_t>(blockIdx.x) * NTH * kH2dUnroll + threadIdx.x; base < n;
        base += stride) {
     uint4 v[kH2dUnroll];
 #pragma unroll
     for (int u = 0; u < kH2dUnroll; ++u) {
-      const uint64_t i = base + static_cast<uint64_t>(u) * 256;
+      const uint64_t i = base + static_cast<uint64_t>(u) * NTH;
       v[u] = src[i < n ? i : n - 1];  // clamped: every load is issued and in bounds
     }
 #pragma unroll
     for (int u = 0; u < kH2dUnroll; ++u) {
-      const uint64_t i = base + static_cast<uint64_t>(u) * 256;
+      const uint64_t i = base + static_cast<uint64_t>(u) * NTH;
       if (i < n) dst[i] = v[u];
+    }
+  }
+  if constexpr (HOLD_CU) {
+    __shared__ uint4 hold[kCuLdsBytes / 16];
+    if (n == 0) {  // the host never launches an empty copy: keeps the allocation, never runs
+      hold[threadIdx.x] = make_uint4(0, 0, 0, 0);
+      __syncthreads();
+      dst[0] = hold[(threadIdx.x + 1) % NTH];
     }
   }
 }
 
+template <int NTH, bool HOLD_CU>
 static hipError_t launch_copy(void* dst, const void* src, uint64_t bytes, int max_wgs, hipStream_t s) {
   if (bytes == 0) return hipSuccess;
   if ((bytes % 16) != 0 || (reinterpret_cast<uintptr_t>(dst) % 16) != 0 || (reinterpret_cast<uintptr_t>(src) % 16) != 0)
     return hipErrorInvalidValue;
   const uint64_t n = bytes / 16;
-  const uint64_t per_wg = 256ull * kH2dUnroll;
+  const uint64_t per_wg = static_cast<uint64_t>(NTH) * kH2dUnroll;
   const int wgs = static_cast<int>(std::min<uint64_t>(max_wgs, (n + per_wg - 1) / per_wg));
-  hipLaunchKernelGGL(h2d_kernel, dim3(wgs), dim3(256), 0, s, static_cast<uint4*>(dst),
+  hipLaunchKernelGGL((copy_kernel<NTH, HOLD_CU>), dim3(wgs), dim3(NTH), 0, s, static_cast<uint4*>(dst),
                      static_cast<const uint4*>(src), n);
   return hipGetLastError();
 }
 
 hipError_t launch_h2d(void* dst, const void* src, uint64_t bytes, hipStream_t s) {
-  return launch_copy(dst, src, bytes, kH2dWorkGroups, s);
+  return launch_copy<kH2dThreads, true>(dst, src, bytes, kH2dWorkGroups, s);
 }
 
 hipError_t launch_d2d(void* dst, const void* src, uint64_t bytes, hipStream_t s) {
-  return launch_copy(dst, src, bytes, kD2dWorkGroups, s);
+  return launch_copy<256, false>(dst, src, bytes, kD2dWorkGroups, s);
 }
 
 // ------------------------------------------------------------------ combine
@@ -2328,14 +2340,14 @@ hipError_t launch_combine(const CombineArgs& a, hipStream_t s) {
   if (a.T <= 0) return hipSuccess;
   const int ncb = (a.d + 255) / 256;
   if (a.n_planes == 1 && (a.n_shared == 0 || a.n_planes_sh == 1)) {
-    hipLaunchKernelGGL(combine_direct_kernel, dim3(a.T, ncb), dim3(64), 0, s, a);
+    hipLaunchKernelGGL(combine_direct_kernel, dim3(a.T, ncb), dim3(64), kGuardLds, s, a);
     return hipGetLastError();
   }
   const int slots = a.T * (a.K + a.n_shared);
   hipLaunchKernelGGL(combine_planes_kernel, dim3(slots, ncb, a.pg), dim3(64 * kCombWaves), 0, s, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(combine_final_kernel, dim3(a.T, ncb), dim3(64), 0, s, a);
+  hipLaunchKernelGGL(combine_final_kernel, dim3(a.T, ncb), dim3(64), kGuardLds, s, a);
   return hipGetLastError();
 }
 
