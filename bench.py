@@ -128,6 +128,11 @@ def _decoders():
                                 prompt=512, n_sets=4, t_moe_us=208.0),
         "mixtral-q2-decoder": dict(shape=synth.MIXTRAL_Q2_STACK, attn=synth.MIXTRAL_ATTN, budget=2 * GIB, r=0.5,
                                    prompt=512, n_sets=4, t_moe_us=70.0),
+        # the budget of the paper's Mixtral TPOT comparison (Sec. 5.2): 160 of
+        # the 256 experts; r = 5/8 caches every expert's top at that budget
+        "mixtral-q2-decoder-160": dict(shape=synth.MIXTRAL_Q2_STACK, attn=synth.MIXTRAL_ATTN,
+                                       budget=160 * synth.MIXTRAL_Q2_STACK.expert_bytes, r=0.625,
+                                       prompt=512, n_sets=4, t_moe_us=70.0),
     }
 
 
@@ -537,7 +542,7 @@ def run_decoder(args):
         "metric": "decode time per output token (TPOT) of the decoder loop with split experts",
         "value": round(tpot_ms, 3), "unit": "ms/token", "higher_is_better": False,
         "data": "synthetic", "dtype": "bf16", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
-        "config": {"workload": "%s: %s, %d layers, attention %d heads / %d kv heads x %d, vocab %d, V_e %.0f GiB, "
+        "config": {"workload": "%s: %s, %d layers, attention %d heads / %d kv heads x %d, vocab %d, V_e %.2f GiB, "
                                "r %s, prompt %d tokens, greedy decode, cache policy %s" % (
                                    args.workload, shape.name, L, attn.n_heads, attn.n_kv_heads, attn.head_dim,
                                    attn.vocab, cfg["budget"] / GIB,

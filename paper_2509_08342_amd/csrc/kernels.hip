@@ -200,14 +200,11 @@ __device__ __forceinline__ void rank_scores(const float* score_s, const RouteArg
     if (a.host_order) a.host_order[r] = e;
     if (a.host_score) a.host_score[e] = v;
   }
-  // the host reads these once the launch completes
-  if (a.host_order && tid < E) __threadfence_system();
 }
 
-// Exclusive scan of cnt[0..E) by wave 0 into offsets (and the host-visible
-// copy, fenced for the host); base (LDS, optional) receives the same values.
-__device__ __forceinline__ void scan_offsets(const int* cnt, int* base, const RouteArgs& a, int lane) {
-  const int E = a.E;
+// Exclusive scan of cnt[0..E) by wave 0 into offs[0..E] (LDS); base (LDS,
+// optional) receives the same values.
+__device__ __forceinline__ void scan_offsets(const int* cnt, int* base, int* offs, int E, int lane) {
   int run = 0;
   for (int e0 = 0; e0 < E; e0 += 64) {
     const int e = e0 + lane;
@@ -220,32 +217,52 @@ __device__ __forceinline__ void scan_offsets(const int* cnt, int* base, const Ro
     }
     if (e < E) {
       if (base) base[e] = run + incl - c;
-      a.offsets[e] = run + incl - c;
-      if (a.host_offsets) a.host_offsets[e] = run + incl - c;
+      offs[e] = run + incl - c;
     }
     run += __shfl(incl, 63, 64);
   }
-  if (lane == 0) {
-    a.offsets[E] = run;
-    if (a.host_offsets) a.host_offsets[E] = run;
-  }
-  // the host reads the offsets once this launch completes
-  if (a.host_offsets) __threadfence_system();
+  if (lane == 0) offs[E] = run;
 }
 
-// Few tokens: everything after the logits in one work-group of NW waves --
-// selection one wave per token; grouping as histogram, exclusive scan, then
-// blocks of 64*NW slots placed in slot order (within a wave by ballot rank,
-// across waves by per-wave counts); prediction sums per wave, then over
-// waves in order.
+// The offsets from LDS to memory and to their host-visible copy.
+__device__ __forceinline__ void store_offsets(const int* offs, const RouteArgs& a, int tid, int NT) {
+  for (int e = tid; e <= a.E; e += NT) {
+    a.offsets[e] = offs[e];
+    if (a.host_offsets) a.host_offsets[e] = offs[e];
+  }
+}
+
+// The host reads the host-visible outputs once the launch completes: the
+// threads that may have written them (tid <= E) fence once, after their
+// last write.
+__device__ __forceinline__ void host_fence(const RouteArgs& a, int tid) {
+  if ((a.host_offsets != nullptr || a.host_order != nullptr || a.host_score != nullptr) && tid <= a.E)
+    __threadfence_system();
+}
+
+// Few tokens (T * K <= kFewSlots): everything after the logits in one
+// work-group of NW waves -- selection one wave per token; grouping as
+// histogram, exclusive scan, then blocks of 64*NW slots placed in slot order
+// (within a wave by ballot rank, across waves by per-wave counts); prediction
+// sums per wave, then over waves in order.  Every result stays in LDS until
+// the last barrier and is then stored once (a barrier after a store to
+// memory would wait for it).
+constexpr int kFewSlots = 1024;
+
 template <int NW>
 __device__ void route_body(const RouteArgs& a) {
+  __shared__ int idx_s[kFewSlots];
+  __shared__ float w_s[kFewSlots];
+  __shared__ int perm_s[kFewSlots];
+  __shared__ int pos_s[kFewSlots];
+  __shared__ int offs_s[kMaxExperts + 1];
   __shared__ int base[kMaxExperts];
   __shared__ float score_s[kMaxExperts];
   __shared__ int wbuf[NW][kMaxExperts];  // per-wave counts / scores
   constexpr int NT = 64 * NW;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int E = a.E, K = a.K;
+  const int TK = a.T * K;
 
   if (a.logits != nullptr) {
     // 1. selection
@@ -254,30 +271,26 @@ __device__ void route_body(const RouteArgs& a) {
       float my_w;
       select_token(a.logits + static_cast<size_t>(t) * E, E, K, a.renormalize, lane, my_idx, my_w);
       if (lane < K) {
-        a.idx[static_cast<size_t>(t) * K + lane] = my_idx;
-        a.w[static_cast<size_t>(t) * K + lane] = my_w;
+        idx_s[t * K + lane] = my_idx;
+        w_s[t * K + lane] = my_w;
       }
     }
-    __threadfence_block();  // idx written above is read back by other waves of this work-group
-    __syncthreads();
-
     // 2. grouping
-    const int TK = a.T * K;
     int* cnt = &wbuf[0][0];
     for (int e = tid; e < E; e += NT) cnt[e] = 0;
     __syncthreads();
     // indices lie in [0, E) (selection above); the clamp only keeps LDS
     // accesses in bounds whatever the input
-    for (int s = tid; s < TK; s += NT) atomicAdd(&cnt[min(max(a.idx[s], 0), E - 1)], 1);
+    for (int s = tid; s < TK; s += NT) atomicAdd(&cnt[min(max(idx_s[s], 0), E - 1)], 1);
     __syncthreads();
-    if (wave == 0) scan_offsets(cnt, base, a, lane);
+    if (wave == 0) scan_offsets(cnt, base, offs_s, E, lane);
     __syncthreads();
     const uint64_t lt = (lane == 0) ? 0ull : ((~0ull) >> (64 - lane));
     for (int b0 = 0; b0 < TK; b0 += NT) {
       for (int i = tid; i < NW * E; i += NT) wbuf[i / E][i % E] = 0;
       __syncthreads();
       const int s = b0 + tid;
-      const int e = (s < TK) ? min(max(a.idx[s], 0), E - 1) : -1;
+      const int e = (s < TK) ? min(max(idx_s[s], 0), E - 1) : -1;
       int rank = 0;
       uint64_t pending = __ballot(e >= 0);
       while (pending) {
@@ -292,8 +305,8 @@ __device__ void route_body(const RouteArgs& a) {
       if (e >= 0) {
         int p = base[e] + rank;
         for (int w2 = 0; w2 < wave; ++w2) p += wbuf[w2][e];
-        a.perm[p] = s;
-        a.pos[s] = p;
+        perm_s[p] = s;
+        pos_s[s] = p;
       }
       __syncthreads();
       for (int e2 = tid; e2 < E; e2 += NT) {
@@ -325,6 +338,18 @@ __device__ void route_body(const RouteArgs& a) {
     __syncthreads();
     rank_scores(score_s, a, tid, NT);
   }
+
+  // 4. the selection and grouping to memory (and the offsets to the host)
+  if (a.logits != nullptr) {
+    for (int i = tid; i < TK; i += NT) {
+      a.idx[i] = idx_s[i];
+      a.w[i] = w_s[i];
+      a.perm[i] = perm_s[i];
+      a.pos[i] = pos_s[i];
+    }
+    store_offsets(offs_s, a, tid, NT);
+  }
+  host_fence(a, tid);
 }
 
 constexpr int kRouteWaves = 16;
@@ -394,6 +419,7 @@ constexpr int kScanWaves = 16;
 
 __global__ __launch_bounds__(64 * kScanWaves) void scan_many_kernel(RouteArgs a, int nblk) {
   __shared__ int tot[kMaxExperts];
+  __shared__ int offs_s[kMaxExperts + 1];
   __shared__ float score_s[kMaxExperts];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int E = a.E;
@@ -431,7 +457,10 @@ __global__ __launch_bounds__(64 * kScanWaves) void scan_many_kernel(RouteArgs a,
       if (lane == 0) tot[e] = run;
     }
     __syncthreads();
-    if (wave == 0) scan_offsets(tot, nullptr, a, lane);
+    if (wave == 0) {
+      scan_offsets(tot, nullptr, offs_s, E, lane);
+      store_offsets(offs_s, a, lane, 64);
+    }
   }
   if (a.logits_pred != nullptr) {
     // per expert (one wave): lanes sum blocks lane, lane + 64, ... in order,
@@ -458,6 +487,7 @@ __global__ __launch_bounds__(64 * kScanWaves) void scan_many_kernel(RouteArgs a,
     __syncthreads();
     rank_scores(score_s, a, tid, 64 * kScanWaves);
   }
+  host_fence(a, tid);
 }
 
 // Many tokens, step 3: slot s of token t (block t / TB) goes to grouped
@@ -529,19 +559,83 @@ __global__ __launch_bounds__(256) void logits_wave_kernel(LogitsArgs a) {
   }
 }
 
-// At most kFusedLogits logits: the route work-group computes them itself
-// (one wave per logit, as above) into LDS and goes on with the route body.
+// At most kFusedLogits logits of at most 16 KiB of token rows: the route
+// work-group computes them itself, in the order above, and goes on with the
+// route body.  The token rows are staged in LDS transposed, row (t, lane l)
+// holding elements l, l + 64, l + 128, ... (pitch fused_pitch bytes), so that
+// a lane reads its fma chain's activations 16 bytes at a time; a wave
+// computes one logit at a time, lane l holding the router elements l + 64 s
+// of a batch of steps in registers (64 bf16 or 32 fp32 ones), all requested
+// at once -- one memory round trip per logit up to d = 4096 in bf16, the
+// first requested before the staging barrier.
 constexpr int kFusedLogits = 32;
+constexpr int kFusedRowBytes = 16 * 64 * kRouteWaves;  // one 16-byte piece per thread
+constexpr int kFusedHBytes = 18 * 1024;
+template <typename W>
+constexpr int fused_batch() { return sizeof(W) == 2 ? 64 : 32; }
+__host__ __device__ constexpr int fused_pitch(int d, int elem) { return ((d / 64) * elem + 15) / 16 * 16 + 16; }
+
+template <typename W, int B>
+__device__ __forceinline__ void fused_load(const W* wrow, int s0, int steps, W (&wv)[B]) {
+#pragma unroll
+  for (int u = 0; u < B; ++u)
+    wv[u] = wrow[static_cast<size_t>(min(s0 + u, steps - 1)) * 64];  // clamped: in bounds, used only in range
+}
 
 template <typename W>
 __global__ __launch_bounds__(64 * kRouteWaves) void route_fused_kernel(LogitsArgs la, RouteArgs ra) {
+  constexpr int VE = 16 / static_cast<int>(sizeof(W));  // elements per 16-byte piece
+  constexpr int B = fused_batch<W>();
   __shared__ float lg[kFusedLogits];
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  __shared__ __align__(16) unsigned char hT[kFusedHBytes];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int d = la.d, steps = d / 64;
+  const int pitch = fused_pitch(d, static_cast<int>(sizeof(W)));
   const int per = la.T * la.E;
   const int n_out = per * (la.wr2 != nullptr ? 2 : 1);
+  const int pieces = la.T * d / VE;  // <= 64 * kRouteWaves (launch condition)
+  auto wrow_of = [&](int o) {
+    const int mat = o / per, e = (o - mat * per) % la.E;
+    return static_cast<const W*>(mat == 0 ? la.wt : la.wt2) + static_cast<size_t>(e) * d + lane;
+  };
+  uint4 hp = make_uint4(0, 0, 0, 0);
+  if (tid < pieces) hp = ld16(static_cast<const W*>(la.h) + static_cast<size_t>(tid) * VE);
+  W wv[B];
+  if (wave < n_out) fused_load(wrow_of(wave), 0, steps, wv);
+  if (tid < pieces) {
+    // elements j .. j + VE - 1 of token t: lanes j % 64 .. + VE - 1, step j / 64
+    const int j0 = tid * VE, t = j0 / d, j = j0 - t * d;
+    W e[VE];
+    *reinterpret_cast<uint4*>(e) = hp;
+#pragma unroll
+    for (int c = 0; c < VE; ++c)
+      *reinterpret_cast<W*>(hT + (static_cast<size_t>(t) * 64 + (j + c) % 64) * pitch + ((j + c) / 64) * sizeof(W)) = e[c];
+  }
+  __syncthreads();
   for (int o = wave; o < n_out; o += kRouteWaves) {
-    const float v = wave_logit<W, kWaveSteps / 2>(la, o, lane);  // 1024 threads: 128 registers a lane
-    if (lane == 0) lg[o] = v;
+    const int mat = o / per, te = o - mat * per;
+    const int t = te / la.E, e = te - t * la.E;
+    const W* wrow = wrow_of(o);
+    const unsigned char* hrow = hT + (static_cast<size_t>(t) * 64 + lane) * pitch;
+    float acc = 0.0f;
+    for (int s0 = 0; s0 < steps; s0 += B) {
+      if (o != wave || s0 != 0) fused_load(wrow, s0, steps, wv);
+      W hv[B];
+#pragma unroll
+      for (int v = 0; v < B / VE; ++v) {
+        uint4 q = make_uint4(0, 0, 0, 0);
+        if (s0 + v * VE < steps) q = *reinterpret_cast<const uint4*>(hrow + static_cast<size_t>(s0 + v * VE) * sizeof(W));
+        *reinterpret_cast<uint4*>(&hv[v * VE]) = q;
+      }
+#pragma unroll
+      for (int u = 0; u < B; ++u)
+        if (s0 + u < steps) acc = fmaf(to_f32(hv[u]), to_f32(wv[u]), acc);
+    }
+#pragma unroll
+    for (int s = 32; s >= 1; s >>= 1) acc = acc + __shfl_down(acc, s, 64);
+    const float* bias = mat == 0 ? la.bias : la.bias2;
+    if (bias != nullptr) acc = acc + bias[e];
+    if (lane == 0) lg[o] = acc;
   }
   __syncthreads();
   RouteArgs a = ra;
@@ -719,8 +813,10 @@ hipError_t launch_logits_route(const LogitsArgs& a, const RouteArgs& ra, hipStre
   }
   const int TB = route_block_tokens(ra.K);
   const int nblk = (a.T + TB - 1) / TB;
-  const bool many = a.T >= kManyTokens && ra.lrank != nullptr && ra.blk != nullptr && ra.psc != nullptr && nblk <= ra.nblk_cap &&
-                    TB * ra.K <= 64 * kSelWaves;
+  const bool many = (a.T >= kManyTokens || (ra.logits != nullptr && a.T * ra.K > kFewSlots)) && ra.lrank != nullptr && ra.blk != nullptr &&
+                    ra.psc != nullptr && nblk <= ra.nblk_cap && TB * ra.K <= 64 * kSelWaves;
+  if (!many && ra.logits != nullptr && a.T * ra.K > kFewSlots)
+    return hipErrorInvalidValue;  // the one-work-group route holds T * K slots
   if (many) {
     const int nb = (a.E + kLmExperts - 1) / kLmExperts;
     const dim3 grid((a.T + kLmTokens - 1) / kLmTokens, nb * mats);
@@ -730,7 +826,10 @@ hipError_t launch_logits_route(const LogitsArgs& a, const RouteArgs& ra, hipStre
       hipLaunchKernelGGL(logits_many_kernel<float>, grid, dim3(256), kGuardLds, s, b);
   } else {
     const int n_out = a.T * a.E * mats;
-    if (n_out <= kFusedLogits) {  // one launch for logits and route
+    const int elem = a.dtype == kBF16 ? 2 : 4;
+    const int64_t row_bytes = static_cast<int64_t>(a.T) * a.d * elem;
+    if (n_out <= kFusedLogits && row_bytes <= kFusedRowBytes &&
+        static_cast<int64_t>(a.T) * 64 * fused_pitch(a.d, elem) <= kFusedHBytes) {  // one launch for logits and route
       if (a.dtype == kBF16)
         hipLaunchKernelGGL(route_fused_kernel<uint16_t>, dim3(1), dim3(64 * kRouteWaves), 0, s, b, ra);
       else
@@ -2214,8 +2313,9 @@ hipError_t launch_d2d(void* dst, const void* src, uint64_t bytes, hipStream_t s)
 
 // ------------------------------------------------------------------ combine
 //
-// Two launches with a fixed summation order (so the output is the same
-// whichever stream or launch produced each partial plane):
+// The partial planes are summed in a fixed order, so the output is the same
+// whichever stream or launch produced each plane.  More than kCombFewTokens
+// tokens: two launches,
 //  1. work-group (term slot, 256 columns, plane group g): wave w sums planes
 //     p = 4 g + w + 4 G j (j ascending, four interleaved accumulators added
 //     in order); the four wave sums are added in wave order -> red[g][slot];
@@ -2304,6 +2404,100 @@ __global__ __launch_bounds__(64) void combine_final_kernel(CombineArgs a) {
   *reinterpret_cast<float4*>(a.y + static_cast<size_t>(t) * a.d + col) = y;
 }
 
+// Few tokens (T <= kCombFewTokens): one launch.  Work-group (32 columns,
+// token t); thread (plane lane pl = tid / 8, column quad tid % 8).  Per term
+// (the token's K routed slots in selection order, then its shared experts):
+// the thread sums planes pl, pl + 32, ... in order; the 8 plane lanes of a
+// wave are added by an xor butterfly over lane bits 3..5; the 4 wave sums
+// are added as (w0 + w1) + (w2 + w3).  Then y[t] = sum_k w[t][k] * S_k in
+// selection order, plus the shared experts' S_s in index order.  A thread
+// keeps 16 plane loads in flight: PER planes of each of 16 / PER terms.
+constexpr int kCombFewTokens = 8;
+constexpr int kCombCols = 32;  // columns per work-group
+constexpr int kCombMaxTerms = kMaxTopK + 8;
+
+__device__ __forceinline__ void comb_term(const CombineArgs& a, int t, int term, const float*& rbase, int& np) {
+  if (term < a.K) {
+    const int row = a.pos[t * a.K + term];
+    rbase = a.part + static_cast<size_t>(row) * a.n_planes * a.d;
+    np = a.n_planes;
+  } else {
+    const int sh = term - a.K;
+    rbase = a.part_sh + static_cast<size_t>(sh) * a.sh_plane + static_cast<size_t>(t) * a.n_planes_sh * a.d;
+    np = a.n_planes_sh;
+  }
+}
+
+template <int PER>
+__global__ __launch_bounds__(256) void combine_few_kernel(CombineArgs a) {
+  constexpr int TPB = 16 / PER;  // terms per batch
+  __shared__ float4 red[kCombMaxTerms][4][kCombCols / 4];
+  const int t = blockIdx.y;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int cq = tid & 7, pl = tid >> 3;  // plane lane 0..31
+  const int col = blockIdx.x * kCombCols + 4 * cq;
+  const bool live = col < a.d;
+  const int n_terms = a.K + a.n_shared;
+  for (int k0 = 0; k0 < n_terms; k0 += TPB) {
+    const float* rb[TPB];
+    int np[TPB];
+    int np_max = 0;
+#pragma unroll
+    for (int j = 0; j < TPB; ++j) {
+      rb[j] = a.part;
+      np[j] = 0;
+      if (k0 + j < n_terms) comb_term(a, t, k0 + j, rb[j], np[j]);
+      np_max = max(np_max, np[j]);
+    }
+    float4 acc[TPB];
+#pragma unroll
+    for (int j = 0; j < TPB; ++j) acc[j] = make_float4(0.f, 0.f, 0.f, 0.f);
+    for (int p0 = pl; p0 < np_max; p0 += 32 * PER) {
+      float4 v[TPB][PER];
+#pragma unroll
+      for (int j = 0; j < TPB; ++j)
+#pragma unroll
+        for (int i = 0; i < PER; ++i) {
+          const int p = min(p0 + 32 * i, np[j] - 1);  // clamped: in bounds, used only in range
+          v[j][i] = (live && np[j] > 0) ? *reinterpret_cast<const float4*>(rb[j] + static_cast<size_t>(p) * a.d + col)
+                                        : make_float4(0.f, 0.f, 0.f, 0.f);
+        }
+#pragma unroll
+      for (int j = 0; j < TPB; ++j)
+#pragma unroll
+        for (int i = 0; i < PER; ++i)
+          if (p0 + 32 * i < np[j]) acc[j] = f4add(acc[j], v[j][i]);
+    }
+#pragma unroll
+    for (int j = 0; j < TPB; ++j) {
+#pragma unroll
+      for (int m = 8; m <= 32; m <<= 1) {
+        float4 o;
+        o.x = __shfl_xor(acc[j].x, m, 64);
+        o.y = __shfl_xor(acc[j].y, m, 64);
+        o.z = __shfl_xor(acc[j].z, m, 64);
+        o.w = __shfl_xor(acc[j].w, m, 64);
+        acc[j] = f4add(acc[j], o);
+      }
+      if (lane < 8 && k0 + j < n_terms) red[k0 + j][wave][cq] = acc[j];
+    }
+  }
+  __syncthreads();
+  if (tid < 8 && live) {
+    float4 y = make_float4(0.f, 0.f, 0.f, 0.f);
+    for (int term = 0; term < n_terms; ++term) {
+      const float4 sum = f4add(f4add(red[term][0][cq], red[term][1][cq]), f4add(red[term][2][cq], red[term][3][cq]));
+      if (term < a.K) {
+        const float wk = a.w[t * a.K + term];
+        y = make_float4(fmaf(wk, sum.x, y.x), fmaf(wk, sum.y, y.y), fmaf(wk, sum.z, y.z), fmaf(wk, sum.w, y.w));
+      } else {
+        y = f4add(y, sum);
+      }
+    }
+    *reinterpret_cast<float4*>(a.y + static_cast<size_t>(t) * a.d + col) = y;
+  }
+}
+
 // One partial plane per slot (prefill path): the same sums in one pass,
 // straight from the partials (a first pass would only copy them).
 __global__ __launch_bounds__(64) void combine_direct_kernel(CombineArgs a) {
@@ -2341,6 +2535,19 @@ hipError_t launch_combine(const CombineArgs& a, hipStream_t s) {
   const int ncb = (a.d + 255) / 256;
   if (a.n_planes == 1 && (a.n_shared == 0 || a.n_planes_sh == 1)) {
     hipLaunchKernelGGL(combine_direct_kernel, dim3(a.T, ncb), dim3(64), kGuardLds, s, a);
+    return hipGetLastError();
+  }
+  if (a.T <= kCombFewTokens && a.K + a.n_shared <= kCombMaxTerms) {
+    const dim3 grid((a.d + kCombCols - 1) / kCombCols, a.T);
+    const int per = (std::max(a.n_planes, a.n_shared > 0 ? a.n_planes_sh : 0) + 31) / 32;
+    if (per <= 1)
+      hipLaunchKernelGGL(combine_few_kernel<1>, grid, dim3(256), 0, s, a);
+    else if (per <= 2)
+      hipLaunchKernelGGL(combine_few_kernel<2>, grid, dim3(256), 0, s, a);
+    else if (per <= 4)
+      hipLaunchKernelGGL(combine_few_kernel<4>, grid, dim3(256), 0, s, a);
+    else
+      hipLaunchKernelGGL(combine_few_kernel<8>, grid, dim3(256), 0, s, a);
     return hipGetLastError();
   }
   const int slots = a.T * (a.K + a.n_shared);
