@@ -530,9 +530,14 @@ def run_decoder(args):
                                          "rnd": ms.MS_CACHE_RND}[args.policy])
     dec.reset()
     ms.ms_reset_stats(dec.ctx)
-    toks, ttft, tpot = dec.generate(synth.prompt_tokens(attn, 0, P, tag=2), n_new)
+    prefill_st = []
+    toks, ttft, tpot = dec.generate(synth.prompt_tokens(attn, 0, P, tag=2), n_new,
+                                    after_prefill=lambda: prefill_st.extend(ms.ms_stats(dec.ctx, l) for l in range(L)))
     timed = tpot[args.warmup:]
     st = [ms.ms_stats(dec.ctx, l) for l in range(L)]
+    # decode steps only: the counters after the prefill subtracted
+    dst = [{k: x[k] - y[k] for k in x} for x, y in zip(st, prefill_st)]
+    n_dec = max(len(tpot), 1)
     tm = module_times(n_marks)
     ms.ms_sync(dec.ctx)
     tpot_ms = float(np.mean(timed))
@@ -553,8 +558,9 @@ def run_decoder(args):
         "module_us_per_token": {"attention_per_layer": round(tm["att"] / L, 1), "moe_per_layer": round(tm["moe"] / L, 1),
                                 "head": round(tm["head"], 1)},
         "hit_rate": round(hits / max(sel, 1), 4),
-        "h2d_bytes_per_token": {"miss": sum(x["bytes_miss"] for x in st) // max(len(tpot) + 1, 1),
-                                "prefetch": sum(x["bytes_prefetch"] for x in st) // max(len(tpot) + 1, 1)},
+        "h2d_bytes_per_decode_token": {k: sum(x["bytes_" + k] for x in dst) // n_dec
+                                       for k in ("miss", "prefetch", "prefetch_used", "prefetch_dropped")},
+        "h2d_bytes_prefill": {k: sum(x["bytes_" + k] for x in prefill_st) for k in ("miss", "prefetch")},
         "cache_inserts": sum(x["cache_inserts"] for x in st),
         "setup_s": round(time.perf_counter() - t_setup, 1),
     }

@@ -131,9 +131,10 @@ class Decoder:
     def embed_ids(self, ids_dev, T, out, stream=None):
         ms.ms_embed(ids_dev, self.embed, self.attn.vocab, T, self.shape.d_model, out, stream)
 
-    def generate(self, prompt, n_new, flags=ms.MS_FWD_PREDICT_NEXT, stream=None, timing=False):
+    def generate(self, prompt, n_new, flags=ms.MS_FWD_PREDICT_NEXT, stream=None, timing=False, after_prefill=None):
         """Prefill the prompt (host int32 ids), then n_new greedy decode steps.
-        Returns (token ids, ttft_ms, [per-token ms])."""
+        after_prefill: called once the first token is out.  Returns (token
+        ids, ttft_ms, [per-token ms])."""
         if stream is None:
             stream = torch.cuda.current_stream()
         P = len(prompt)
@@ -148,6 +149,8 @@ class Decoder:
         stream.synchronize()
         ttft = (time.perf_counter() - t0) * 1e3
         out.append(int(tok.item()))
+        if after_prefill is not None:
+            after_prefill()
         tpot = []
         x1 = torch.empty(1, self.shape.d_model, dtype=torch.bfloat16, device="cuda")
         for _ in range(n_new - 1):
