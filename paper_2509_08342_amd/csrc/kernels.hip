@@ -1555,6 +1555,21 @@ __device__ __forceinline__ uint16_t f2bf(float f) {
   return static_cast<uint16_t>((u + 0x7fffu + ((u >> 16) & 1u)) >> 16);
 }
 
+// Work-groups are dispatched to the 8 XCDs round-robin by index, and each
+// XCD has its own L2.  The matrix-core kernels renumber them so that every
+// XCD runs a contiguous range of logical indices: consecutive indices (the
+// row tiles of one chunk in gate/up, the column blocks of one row tile in
+// down, and in both the work of one expert) then share an L2.  Measured on
+// the Qwen3-shaped prefill: gate/up L2 hits 38% -> 64%, bytes fetched past
+// L2 2.0 -> 1.1 GB per launch (the launch time did not change: these
+// kernels are not bound by those fetches).
+constexpr int kXcds = 8;
+__device__ __forceinline__ int xcd_local(int wg, int n) {
+  const int q = n / kXcds, r = n % kXcds;
+  const int x = wg % kXcds, i = wg / kXcds;
+  return x < r ? x * (q + 1) + i : r * (q + 1) + (x - r) * q + i;
+}
+
 __device__ __forceinline__ int find_task(const MmaTask* tasks, int n, int wg) {
   int ti = 0;
   for (int i = 1; i < n; ++i)
@@ -1591,7 +1606,7 @@ __device__ __forceinline__ TileRows tile_rows(const MmaArgs& a, const MmaTask& t
 template <int NF>
 __global__ __launch_bounds__(256) void mma_gateup_kernel(MmaArgs a) {
   constexpr int KB = NF == 1 ? 4 : 2;  // k steps per batch
-  const int wg = blockIdx.x;
+  const int wg = xcd_local(blockIdx.x, gridDim.x);
   const MmaTask tk = a.tasks[find_task(a.tasks, a.n_tasks, wg)];
   const int local = wg - tk.wg_begin;
   const int mt = local % tk.m_tiles;
@@ -1679,7 +1694,7 @@ constexpr int kGuPitch = kGuSlab + 8;   // bf16 per staged row
 
 __global__ __launch_bounds__(256) void mma_gateup_lds_kernel(MmaArgs a) {
   __shared__ __align__(16) uint16_t As[2][kMmaRows * kGuPitch];
-  const int wg = blockIdx.x;
+  const int wg = xcd_local(blockIdx.x, gridDim.x);
   const MmaTask tk = a.tasks[find_task(a.tasks, a.n_tasks, wg)];
   const int local = wg - tk.wg_begin;
   const int mt = local % tk.m_tiles;
@@ -1788,7 +1803,7 @@ __global__ __launch_bounds__(256) void mma_gateup_lds_kernel(MmaArgs a) {
 __global__ __launch_bounds__(256) void mma_down_kernel(MmaArgs a) {
   constexpr int PITCH = kChunkUnits + 8;  // transposed D tile row: 64 units + pad
   __shared__ __align__(16) uint16_t dt[kMmaCols * PITCH];
-  const int wg = blockIdx.x;
+  const int wg = xcd_local(blockIdx.x, gridDim.x);
   const MmaTask tk = a.tasks[find_task(a.tasks, a.n_tasks, wg)];
   const int local = wg - tk.wg_begin;
   const int mt = local / a.ncb, cb = local % a.ncb;
@@ -1908,7 +1923,7 @@ __global__ __launch_bounds__(256) void mma_gateup_q_kernel(MmaArgs a) {
   constexpr float C = static_cast<float>(1 << BITS);
   constexpr int GW = 2 * BITS;  // code words per group
   const PairMasks<BITS> pm;
-  const int wg = blockIdx.x;
+  const int wg = xcd_local(blockIdx.x, gridDim.x);
   const MmaTask tk = a.tasks[find_task(a.tasks, a.n_tasks, wg)];
   const int local = wg - tk.wg_begin;
   const int mt = local % tk.m_tiles;
@@ -2057,7 +2072,7 @@ __global__ __launch_bounds__(256) void mma_down_q_kernel(MmaArgs a) {
   constexpr int GW = 2 * BITS;  // code words per column group
   constexpr int NF = kMmaCols / 16;
   const PairMasks<BITS> pm;
-  const int wg = blockIdx.x;
+  const int wg = xcd_local(blockIdx.x, gridDim.x);
   const MmaTask tk = a.tasks[find_task(a.tasks, a.n_tasks, wg)];
   const int local = wg - tk.wg_begin;
   const int mt = local / a.ncb, cb = local % a.ncb;
