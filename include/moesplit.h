@@ -71,7 +71,9 @@ typedef enum { MS_F32 = 0, MS_BF16 = 1 } ms_dtype;
  * paper's 2-bit Mixtral setting, Sec. 5.1; see ms_set_expert_q); 0 keeps
  * them in the model dtype.  b-bit experts need dtype MS_BF16, no shared
  * experts, d_ff a multiple of 64, d_model a multiple of 64 in [256, 8192] and
- * ffn_splits 0 or 1 (MS_E_UNSUPPORTED otherwise). */
+ * ffn_splits 0 or 1 (MS_E_UNSUPPORTED otherwise).  Every shape needs
+ * d_ff and d_ff_shared at most 65535 * 64 and n_shared at most 32767
+ * (MS_E_UNSUPPORTED otherwise). */
 typedef struct {
   int32_t n_layers;
   int32_t d_model;

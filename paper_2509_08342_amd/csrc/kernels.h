@@ -9,7 +9,7 @@
 namespace msk {
 
 constexpr int kChunkUnits = 64;    // FFN intermediate units per chunk
-constexpr int kMaxTasks = 120;     // tasks passed by value in one FFN launch
+constexpr int kMaxTasks = 200;     // tasks passed by value in one FFN launch (3.3 KiB of kernel arguments)
 constexpr int kFfnLanesPerUnit = 8;  // lanes sharing one unit row in phase 1
 constexpr int kMaxExperts = 512;   // grouping / ranking kernels' LDS bound
 constexpr int kMaxTopK = 64;
@@ -91,6 +91,19 @@ struct FfnTask {
   int32_t wg_begin;
 };
 
+// The kernels' copy of a task (16 bytes, so that one launch holds many):
+// chunk_lo < 65536 and expert in int16 range, checked at launch.
+struct FfnTaskK {
+  const unsigned char* base;
+  int32_t wg_begin;
+  int16_t expert;
+  uint16_t chunk_lo;
+  FfnTaskK() = default;
+  FfnTaskK(const FfnTask& t)
+      : base(t.base), wg_begin(t.wg_begin), expert(static_cast<int16_t>(t.expert)),
+        chunk_lo(static_cast<uint16_t>(t.chunk_lo)) {}
+};
+
 // Each chunk is computed by `subs` work-groups of 64 / subs units each; the
 // work-group for (chunk c, sub s) writes partial plane c * subs + s.
 struct FfnArgs {
@@ -112,8 +125,10 @@ struct FfnArgs {
   int32_t n_planes_sh;        // shared partial planes: n_chunks_sh * subs
   int32_t bits;               // 0: chunks in the model dtype; 2 or 4: b-bit codes
                               // (bf16 activations, routed experts, subs = 1)
-  FfnTask tasks[kMaxTasks];
+  FfnTaskK tasks[kMaxTasks];  // ascending wg_begin
 };
+static_assert(sizeof(FfnTaskK) == 16, "task records are 16 bytes");
+static_assert(sizeof(FfnArgs) <= 3400, "FFN kernel arguments within the size other launches use");
 // Launches n_wg work-groups; max_tok bounds the tokens of any task.
 hipError_t launch_ffn(const FfnArgs& a, int max_tok, hipStream_t s);
 

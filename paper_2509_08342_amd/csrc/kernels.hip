@@ -862,7 +862,8 @@ hipError_t launch_logits_route(const LogitsArgs& a, const RouteArgs& ra, hipStre
 // --------------------------------------------------------------- SwiGLU FFN
 //
 // A work-group computes UPW units (one sub-range of a 64-unit chunk c) of one
-// expert for all of the expert's tokens, NT tokens at a time:
+// expert for one tile of at most NT of the expert's tokens (the tiles of an
+// expert with more tokens go to neighbouring work-groups):
 //   phase 1: a[t][f] = silu(h_t . G_f) * (h_t . U_f) for its units f
 //            (8 lanes per unit row, 16-byte loads, batches of RB loads per
 //            lane and row stream issued before use);
@@ -880,6 +881,21 @@ hipError_t launch_logits_route(const LogitsArgs& a, const RouteArgs& ra, hipStre
 // CU), launches of fewer than one work-group per CU use RB = 8 (each
 // work-group alone must keep enough bytes in flight to cover the latency).
 
+// Index of the task holding work-group wg: the last task whose first
+// work-group is <= wg (tasks in ascending wg_begin order).
+template <typename TaskT>
+__device__ __forceinline__ int find_task_of(const TaskT* tasks, int n, int wg) {
+  int lo = 0, hi = n - 1;
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if (tasks[mid].wg_begin <= wg)
+      lo = mid;
+    else
+      hi = mid - 1;
+  }
+  return lo;
+}
+
 #ifndef MSK_ROW_BATCH
 #define MSK_ROW_BATCH 4
 #endif
@@ -892,21 +908,181 @@ constexpr int kDeepBelowWgs = MSK_DEEP_BELOW;
 constexpr int kLpu = kFfnLanesPerUnit;
 constexpr int kKTile = 64;                // k elements per gate/up piece
 
-template <typename W, int NT, int Q, int UPW, int RB>
-__global__ __launch_bounds__(UPW * kLpu) void ffn_chunk_kernel(FfnArgs a) {
+// One tile of NTT token rows (nt <= NTT real, the rest zero) of one chunk
+// sub-range.  Each token's sums run in the same order whatever NTT is, so a
+// token's partial does not depend on the tile it was computed in.
+template <typename W, int NTT, int Q, int UPW, int RB>
+__device__ __forceinline__ void ffn_tile(const FfnArgs& a, const W* G, const W* U, const W* D, float* part,
+                                         int a_planes, int plane, bool routed, int p0, int tile, int nt, W* hs,
+                                         float* as, int sub) {
   constexpr int VEC = Vec<W>::N;
   constexpr int THREADS = UPW * kLpu;
   constexpr int STEP = kLpu * VEC;  // k covered by the lanes of a unit per step
   constexpr int PB = (RB < 16 / Q) ? RB : 16 / Q;  // phase-2 rows per batch (<= 2 x 16 loads in flight)
   static_assert(STEP <= kKTile && kKTile % STEP == 0, "a unit's lanes must tile a k piece");
   static_assert(UPW % PB == 0, "phase-2 batches must tile the work-group's units");
-  extern __shared__ __align__(16) unsigned char ffn_smem[];
   const int d = a.d;
-  const int wg = blockIdx.x;
-  int ti = 0;
-  for (int i = 1; i < a.n_tasks; ++i)
-    if (a.tasks[i].wg_begin <= wg) ti = i;
-  const FfnTask tk = a.tasks[ti];
+  const W* hsrc = static_cast<const W*>(a.h);
+  const int tid = threadIdx.x;
+  const int lane_u = tid % kLpu;           // lane within the unit's lane group
+  const int lu = tid / kLpu;               // unit within this work-group
+  const int unit = sub * UPW + lu;         // unit within the chunk
+  const int f_first = sub * UPW;           // first down row of this work-group
+
+  // stage the tile's activations in LDS (zero rows past nt)
+  const int vec_per_row = d / VEC;
+  for (int i = tid; i < NTT * vec_per_row; i += THREADS) {
+    const int t = i / vec_per_row, k = (i - t * vec_per_row) * VEC;
+    uint4 v = make_uint4(0, 0, 0, 0);
+    if (t < nt) {
+      const int tok = routed ? a.perm[p0 + tile + t] / a.K : tile + t;
+      v = ld16(hsrc + static_cast<size_t>(tok) * d + k);
+    }
+    *reinterpret_cast<uint4*>(hs + static_cast<size_t>(t) * d + k) = v;
+  }
+  __syncthreads();
+
+  // phase 1: gate/up dot products of this lane group's unit
+  {
+    float ag[NTT], au[NTT];
+#pragma unroll
+    for (int t = 0; t < NTT; ++t) ag[t] = au[t] = 0.0f;
+    const int n_steps = d / STEP;
+    // software pipeline: batch s0 + RB is loaded while batch s0 is used;
+    // every load is issued (clamped to the last step), used only in range
+    uint4 gr[RB], ur[RB], gn[RB], un[RB];
+    auto load_batch = [&](int s0, uint4(&g)[RB], uint4(&uu)[RB]) {
+#pragma unroll
+      for (int u = 0; u < RB; ++u) {
+        const int sk = min(s0 + u, n_steps - 1) * STEP;  // first k of the step
+        const size_t off =
+            (static_cast<size_t>(sk / kKTile) * kChunkUnits + unit) * kKTile + (sk % kKTile) + lane_u * VEC;
+        g[u] = ldw16(G + off);
+        uu[u] = ldw16(U + off);
+      }
+    };
+    load_batch(0, gn, un);
+    for (int s0 = 0; s0 < n_steps; s0 += RB) {
+#pragma unroll
+      for (int u = 0; u < RB; ++u) {
+        gr[u] = gn[u];
+        ur[u] = un[u];
+      }
+      load_batch(s0 + RB, gn, un);
+#pragma unroll
+      for (int u = 0; u < RB; ++u) {
+        if (s0 + u < n_steps) {
+          const int k = (s0 + u) * STEP + lane_u * VEC;
+          float gv[VEC], uv[VEC];
+          unpack(gr[u], gv);
+          unpack(ur[u], uv);
+#pragma unroll
+          for (int t = 0; t < NTT; ++t) {
+            float hv[VEC];
+            unpack(ld16(hs + static_cast<size_t>(t) * d + k), hv);
+#pragma unroll
+            for (int i = 0; i < VEC; ++i) {
+              ag[t] = fmaf(gv[i], hv[i], ag[t]);
+              au[t] = fmaf(uv[i], hv[i], au[t]);
+            }
+          }
+        }
+      }
+    }
+#pragma unroll
+    for (int t = 0; t < NTT; ++t) {
+#pragma unroll
+      for (int s = 1; s < kLpu; s <<= 1) {
+        ag[t] += __shfl_xor(ag[t], s, 64);
+        au[t] += __shfl_xor(au[t], s, 64);
+      }
+    }
+    if (lane_u == 0) {
+#pragma unroll
+      for (int t = 0; t < NTT; ++t) as[t * UPW + lu] = silu(ag[t]) * au[t];
+    }
+  }
+  __syncthreads();
+
+  // phase 2: partial down-projection over this work-group's units
+  {
+    float y[NTT][Q][VEC];
+#pragma unroll
+    for (int t = 0; t < NTT; ++t)
+#pragma unroll
+      for (int q = 0; q < Q; ++q)
+#pragma unroll
+        for (int i = 0; i < VEC; ++i) y[t][q][i] = 0.0f;
+    // software pipeline as in phase 1 (rows clamped to the work-group's last)
+    uint4 dr[PB][Q], dn[PB][Q];
+    auto load_rows = [&](int f0, uint4(&dd)[PB][Q]) {
+#pragma unroll
+      for (int u = 0; u < PB; ++u)
+#pragma unroll
+        for (int q = 0; q < Q; ++q) {
+          const int col = min((tid + THREADS * q) * VEC, d - VEC);  // clamped; used only if in range
+          dd[u][q] = ldw16(D + static_cast<size_t>(f_first + min(f0 + u, UPW - 1)) * d + col);
+        }
+    };
+    load_rows(0, dn);
+    for (int f0 = 0; f0 < UPW; f0 += PB) {
+#pragma unroll
+      for (int u = 0; u < PB; ++u)
+#pragma unroll
+        for (int q = 0; q < Q; ++q) dr[u][q] = dn[u][q];
+      load_rows(f0 + PB, dn);
+#pragma unroll
+      for (int u = 0; u < PB; ++u) {
+        float av[NTT];
+#pragma unroll
+        for (int t = 0; t < NTT; ++t) av[t] = as[t * UPW + f0 + u];
+#pragma unroll
+        for (int q = 0; q < Q; ++q) {
+          const int col = (tid + THREADS * q) * VEC;
+          if (col < d) {
+            float dv[VEC];
+            unpack(dr[u][q], dv);
+#pragma unroll
+            for (int t = 0; t < NTT; ++t)
+#pragma unroll
+              for (int i = 0; i < VEC; ++i) y[t][q][i] = fmaf(av[t], dv[i], y[t][q][i]);
+          }
+        }
+      }
+    }
+#pragma unroll
+    for (int t = 0; t < NTT; ++t) {
+      if (t < nt) {
+        const int row = routed ? (p0 + tile + t) : (tile + t);
+        float* dst = part + (static_cast<size_t>(row) * a_planes + plane) * d;
+#pragma unroll
+        for (int q = 0; q < Q; ++q) {
+          const int col = (tid + THREADS * q) * VEC;
+          if (col < d) {
+#pragma unroll
+            for (int i = 0; i < VEC; i += 4)
+              *reinterpret_cast<float4*>(dst + col + i) =
+                  make_float4(y[t][q][i], y[t][q][i + 1], y[t][q][i + 2], y[t][q][i + 3]);
+          }
+        }
+      }
+    }
+  }
+  __syncthreads();
+}
+
+// Grid: n_wg x n_tiles work-groups; block b computes token tile b % n_tiles
+// (and every n_tiles-th tile after it) of work-group slot b / n_tiles, so the
+// tiles of an expert with many tokens run side by side.  The tile shape
+// follows the tile's real token count (1, 2, 4 or NT rows), read on the
+// device, so launches enqueued before the routing is known waste no
+// arithmetic on empty rows.
+template <typename W, int NT, int Q, int UPW, int RB>
+__global__ __launch_bounds__(UPW * kLpu) void ffn_chunk_kernel(FfnArgs a, int n_tiles) {
+  extern __shared__ __align__(16) unsigned char ffn_smem[];
+  const int wg = blockIdx.x / n_tiles;
+  const int tile0 = blockIdx.x - wg * n_tiles;
+  const FfnTaskK tk = a.tasks[find_task_of(a.tasks, a.n_tasks, wg)];
   const int local = wg - tk.wg_begin;
   const int c = tk.chunk_lo + local / a.subs;
   const int sub = local % a.subs;
@@ -916,9 +1092,9 @@ __global__ __launch_bounds__(UPW * kLpu) void ffn_chunk_kernel(FfnArgs a) {
     p0 = a.offsets[tk.expert];
     n_tok = a.offsets[tk.expert + 1] - p0;
   }
-  if (n_tok <= 0) return;
+  if (tile0 * NT >= n_tok) return;
 
-  const size_t cd = static_cast<size_t>(kChunkUnits) * d;
+  const size_t cd = static_cast<size_t>(kChunkUnits) * a.d;
   const W* G = reinterpret_cast<const W*>(tk.base + static_cast<size_t>(c) * a.chunk_bytes);
   const W* U = G + cd;
   const W* D = U + cd;
@@ -927,174 +1103,44 @@ __global__ __launch_bounds__(UPW * kLpu) void ffn_chunk_kernel(FfnArgs a) {
   const int a_planes = routed ? a.n_planes : a.n_planes_sh;
   const int plane = c * a.subs + sub;
 
-  W* hs = reinterpret_cast<W*>(ffn_smem);                                  // [NT][d]
-  float* as = reinterpret_cast<float*>(ffn_smem + sizeof(W) * NT * d);     // [NT][UPW]
-  const W* hsrc = static_cast<const W*>(a.h);
+  W* hs = reinterpret_cast<W*>(ffn_smem);                                    // [NT][d]
+  float* as = reinterpret_cast<float*>(ffn_smem + sizeof(W) * NT * a.d);     // [NT][UPW]
 
-  const int tid = threadIdx.x;
-  const int lane_u = tid % kLpu;           // lane within the unit's lane group
-  const int lu = tid / kLpu;               // unit within this work-group
-  const int unit = sub * UPW + lu;         // unit within the chunk
-  const int f_first = sub * UPW;           // first down row of this work-group
-
-  for (int tile = 0; tile < n_tok; tile += NT) {
-    const int nt = min(NT, n_tok - tile);
-    // stage the tile's activations in LDS (zero rows past nt)
-    const int vec_per_row = d / VEC;
-    for (int i = tid; i < NT * vec_per_row; i += THREADS) {
-      const int t = i / vec_per_row, k = (i - t * vec_per_row) * VEC;
-      uint4 v = make_uint4(0, 0, 0, 0);
-      if (t < nt) {
-        const int tok = routed ? a.perm[p0 + tile + t] / a.K : tile + t;
-        v = ld16(hsrc + static_cast<size_t>(tok) * d + k);
-      }
-      *reinterpret_cast<uint4*>(hs + static_cast<size_t>(t) * d + k) = v;
-    }
-    __syncthreads();
-
-    // phase 1: gate/up dot products of this lane group's unit
-    {
-      float ag[NT], au[NT];
-#pragma unroll
-      for (int t = 0; t < NT; ++t) ag[t] = au[t] = 0.0f;
-      const int n_steps = d / STEP;
-      // software pipeline: batch s0 + RB is loaded while batch s0 is used;
-      // every load is issued (clamped to the last step), used only in range
-      uint4 gr[RB], ur[RB], gn[RB], un[RB];
-      auto load_batch = [&](int s0, uint4(&g)[RB], uint4(&uu)[RB]) {
-#pragma unroll
-        for (int u = 0; u < RB; ++u) {
-          const int sk = min(s0 + u, n_steps - 1) * STEP;  // first k of the step
-          const size_t off =
-              (static_cast<size_t>(sk / kKTile) * kChunkUnits + unit) * kKTile + (sk % kKTile) + lane_u * VEC;
-          g[u] = ldw16(G + off);
-          uu[u] = ldw16(U + off);
-        }
-      };
-      load_batch(0, gn, un);
-      for (int s0 = 0; s0 < n_steps; s0 += RB) {
-#pragma unroll
-        for (int u = 0; u < RB; ++u) {
-          gr[u] = gn[u];
-          ur[u] = un[u];
-        }
-        load_batch(s0 + RB, gn, un);
-#pragma unroll
-        for (int u = 0; u < RB; ++u) {
-          if (s0 + u < n_steps) {
-            const int k = (s0 + u) * STEP + lane_u * VEC;
-            float gv[VEC], uv[VEC];
-            unpack(gr[u], gv);
-            unpack(ur[u], uv);
-#pragma unroll
-            for (int t = 0; t < NT; ++t) {
-              float hv[VEC];
-              unpack(ld16(hs + static_cast<size_t>(t) * d + k), hv);
-#pragma unroll
-              for (int i = 0; i < VEC; ++i) {
-                ag[t] = fmaf(gv[i], hv[i], ag[t]);
-                au[t] = fmaf(uv[i], hv[i], au[t]);
-              }
-            }
-          }
-        }
-      }
-#pragma unroll
-      for (int t = 0; t < NT; ++t) {
-#pragma unroll
-        for (int s = 1; s < kLpu; s <<= 1) {
-          ag[t] += __shfl_xor(ag[t], s, 64);
-          au[t] += __shfl_xor(au[t], s, 64);
-        }
-      }
-      if (lane_u == 0) {
-#pragma unroll
-        for (int t = 0; t < NT; ++t) as[t * UPW + lu] = silu(ag[t]) * au[t];
-      }
-    }
-    __syncthreads();
-
-    // phase 2: partial down-projection over this work-group's units
-    {
-      float y[NT][Q][VEC];
-#pragma unroll
-      for (int t = 0; t < NT; ++t)
-#pragma unroll
-        for (int q = 0; q < Q; ++q)
-#pragma unroll
-          for (int i = 0; i < VEC; ++i) y[t][q][i] = 0.0f;
-      // software pipeline as in phase 1 (rows clamped to the work-group's last)
-      uint4 dr[PB][Q], dn[PB][Q];
-      auto load_rows = [&](int f0, uint4(&dd)[PB][Q]) {
-#pragma unroll
-        for (int u = 0; u < PB; ++u)
-#pragma unroll
-          for (int q = 0; q < Q; ++q) {
-            const int col = min((tid + THREADS * q) * VEC, d - VEC);  // clamped; used only if in range
-            dd[u][q] = ldw16(D + static_cast<size_t>(f_first + min(f0 + u, UPW - 1)) * d + col);
-          }
-      };
-      load_rows(0, dn);
-      for (int f0 = 0; f0 < UPW; f0 += PB) {
-#pragma unroll
-        for (int u = 0; u < PB; ++u)
-#pragma unroll
-          for (int q = 0; q < Q; ++q) dr[u][q] = dn[u][q];
-        load_rows(f0 + PB, dn);
-#pragma unroll
-        for (int u = 0; u < PB; ++u) {
-          float av[NT];
-#pragma unroll
-          for (int t = 0; t < NT; ++t) av[t] = as[t * UPW + f0 + u];
-#pragma unroll
-          for (int q = 0; q < Q; ++q) {
-            const int col = (tid + THREADS * q) * VEC;
-            if (col < d) {
-              float dv[VEC];
-              unpack(dr[u][q], dv);
-#pragma unroll
-              for (int t = 0; t < NT; ++t)
-#pragma unroll
-                for (int i = 0; i < VEC; ++i) y[t][q][i] = fmaf(av[t], dv[i], y[t][q][i]);
-            }
-          }
-        }
-      }
-#pragma unroll
-      for (int t = 0; t < NT; ++t) {
-        if (t < nt) {
-          const int row = routed ? (p0 + tile + t) : (tile + t);
-          float* dst = part + (static_cast<size_t>(row) * a_planes + plane) * d;
-#pragma unroll
-          for (int q = 0; q < Q; ++q) {
-            const int col = (tid + THREADS * q) * VEC;
-            if (col < d) {
-#pragma unroll
-              for (int i = 0; i < VEC; i += 4)
-                *reinterpret_cast<float4*>(dst + col + i) =
-                    make_float4(y[t][q][i], y[t][q][i + 1], y[t][q][i + 2], y[t][q][i + 3]);
-            }
-          }
-        }
-      }
-    }
-    __syncthreads();
+  // one tile per work-group (max_tok bounds every task's token count);
+  // later tiles only if it did not
+  const int tile = tile0 * NT;
+  const int nt = min(NT, n_tok - tile);
+#define MSK_FFN_TILE(NTT, T0, N) ffn_tile<W, NTT, Q, UPW, RB>(a, G, U, D, part, a_planes, plane, routed, p0, T0, N, hs, as, sub)
+  if (NT >= 4 && nt == 1) {
+    MSK_FFN_TILE((NT >= 4 ? 1 : NT), tile, nt);
+  } else if (NT >= 8 && nt <= 2) {
+    MSK_FFN_TILE((NT >= 8 ? 2 : NT), tile, nt);
+  } else if (NT >= 8 && nt <= 4) {
+    MSK_FFN_TILE((NT >= 8 ? 4 : NT), tile, nt);
+  } else {
+    MSK_FFN_TILE(NT, tile, nt);
   }
+  for (int t2 = tile + NT * n_tiles; t2 < n_tok; t2 += NT * n_tiles) MSK_FFN_TILE(NT, t2, min(NT, n_tok - t2));
+#undef MSK_FFN_TILE
 }
 
 template <typename W, int NT, int Q, int UPW>
-static hipError_t launch_ffn_one(const FfnArgs& a, hipStream_t s) {
+static hipError_t launch_ffn_one(const FfnArgs& a, int max_tok, hipStream_t s) {
   const size_t lds = sizeof(W) * NT * a.d + sizeof(float) * NT * UPW;
+  const int n_tiles = max(1, (max_tok + NT - 1) / NT);
+  const int64_t grid = static_cast<int64_t>(a.n_wg) * n_tiles;
+  if (grid > 0x7fffffff) return hipErrorInvalidValue;
   // deep batches (bf16 weights) only where few tokens and columns keep the
   // accumulators small enough to leave room for the loads in flight
   if constexpr (NT <= 2 && Q <= 4 && sizeof(W) == 2) {
-    if (a.n_wg < kDeepBelowWgs) {
-      hipLaunchKernelGGL((ffn_chunk_kernel<W, NT, Q, UPW, kRowBatchDeep>), dim3(a.n_wg), dim3(UPW * kLpu), lds, s,
-                         a);
+    if (grid < kDeepBelowWgs) {
+      hipLaunchKernelGGL((ffn_chunk_kernel<W, NT, Q, UPW, kRowBatchDeep>), dim3(grid), dim3(UPW * kLpu), lds, s,
+                         a, n_tiles);
       return hipGetLastError();
     }
   }
-  hipLaunchKernelGGL((ffn_chunk_kernel<W, NT, Q, UPW, kRowBatch>), dim3(a.n_wg), dim3(UPW * kLpu), lds, s, a);
+  hipLaunchKernelGGL((ffn_chunk_kernel<W, NT, Q, UPW, kRowBatch>), dim3(grid), dim3(UPW * kLpu), lds, s, a,
+                     n_tiles);
   return hipGetLastError();
 }
 
@@ -1103,13 +1149,13 @@ constexpr bool ffn_fits(int nt, int q, int vec) { return nt * q * vec <= (q >= 4
 
 // Only the (NT, Q) pairs whose accumulators fit exist.
 template <typename W, int UPW>
-static hipError_t dispatch_ffn(const FfnArgs& a, int nt, int q, hipStream_t s) {
+static hipError_t dispatch_ffn(const FfnArgs& a, int nt, int q, int max_tok, hipStream_t s) {
   constexpr int V = Vec<W>::N;
   // Q_ > 1 exists only where some d <= kMaxModelDim needs it
 #define MSK_FFN_CASE(NT_, Q_)                                                                     \
   if (nt == NT_ && q == Q_) {                                                                     \
     if constexpr (ffn_fits(NT_, Q_, V) && (Q_ == 1 || UPW * kLpu * V * (Q_ / 2) < kMaxModelDim))  \
-      return launch_ffn_one<W, NT_, Q_, UPW>(a, s);                                               \
+      return launch_ffn_one<W, NT_, Q_, UPW>(a, max_tok, s);                                     \
   }
   MSK_FFN_CASE(1, 1) MSK_FFN_CASE(2, 1) MSK_FFN_CASE(4, 1) MSK_FFN_CASE(8, 1)
   MSK_FFN_CASE(1, 2) MSK_FFN_CASE(2, 2) MSK_FFN_CASE(4, 2) MSK_FFN_CASE(8, 2)
@@ -1142,9 +1188,9 @@ static hipError_t launch_ffn_w(const FfnArgs& a, int max_tok, hipStream_t s) {
   if (qq > 8) return hipErrorInvalidValue;
   const int nt = pick_nt(max_tok, a.d, static_cast<int>(sizeof(W)), qq, vec, upw);
   switch (a.subs) {
-    case 1: return dispatch_ffn<W, 64>(a, nt, qq, s);
-    case 2: return dispatch_ffn<W, 32>(a, nt, qq, s);
-    case 4: return dispatch_ffn<W, 16>(a, nt, qq, s);
+    case 1: return dispatch_ffn<W, 64>(a, nt, qq, max_tok, s);
+    case 2: return dispatch_ffn<W, 32>(a, nt, qq, max_tok, s);
+    case 4: return dispatch_ffn<W, 16>(a, nt, qq, max_tok, s);
     default: return hipErrorInvalidValue;
   }
 }
@@ -1287,10 +1333,7 @@ __global__ __launch_bounds__((QCfg<BITS, LPU, GPL, NT, B>::THREADS)) __attribute
   const int d = a.d;
   const int ngr = d / 64;  // groups per gate/up row
   const int wg = blockIdx.x;
-  int ti = 0;
-  for (int i = 1; i < a.n_tasks; ++i)
-    if (a.tasks[i].wg_begin <= wg) ti = i;
-  const FfnTask tk = a.tasks[ti];
+  const FfnTaskK tk = a.tasks[find_task_of(a.tasks, a.n_tasks, wg)];
   const int c = tk.chunk_lo + (wg - tk.wg_begin);
   const int p0 = a.offsets[tk.expert];
   const int n_tok = a.offsets[tk.expert + 1] - p0;
@@ -1571,10 +1614,7 @@ __device__ __forceinline__ int xcd_local(int wg, int n) {
 }
 
 __device__ __forceinline__ int find_task(const MmaTask* tasks, int n, int wg) {
-  int ti = 0;
-  for (int i = 1; i < n; ++i)
-    if (tasks[i].wg_begin <= wg) ti = i;
-  return ti;
+  return find_task_of(tasks, n, wg);
 }
 
 // Rows of a task's row tile: routed experts take grouped positions

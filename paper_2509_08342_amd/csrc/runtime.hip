@@ -88,6 +88,12 @@ ms_status derive_shape(const ms_model_desc* d, Shape* s, std::string* err) {
     *err = "max_tokens * top_k too large";
     return MS_E_UNSUPPORTED;
   }
+  // the FFN kernels' task records hold chunk indices in 16 bits and expert
+  // ids (-1 - s for shared expert s) in int16
+  if (d->d_ff > 65535 * 64 || (d->n_shared > 0 && d->d_ff_shared > 65535 * 64) || d->n_shared > 32767) {
+    *err = "d_ff and d_ff_shared must be at most 4194240, n_shared at most 32767";
+    return MS_E_UNSUPPORTED;
+  }
   s->L = d->n_layers;
   s->d = d->d_model;
   s->F = d->d_ff;
@@ -1857,9 +1863,8 @@ ms_status ms_forward(ms_ctx* ctx, int32_t layer, const void* h_dev, int32_t T, f
       MS_HIP(hipStreamWaitEvent(ctx->side, b.gev[gi], 0));
       fa.n_tasks = 1;
       fa.tasks[0].base = b.base;
-      fa.tasks[0].expert = e;
-      fa.tasks[0].chunk_lo = lo;
-      fa.tasks[0].n_chunks = g.c_hi - lo;
+      fa.tasks[0].expert = static_cast<int16_t>(e);
+      fa.tasks[0].chunk_lo = static_cast<uint16_t>(lo);
       fa.tasks[0].wg_begin = 0;
       fa.n_wg = (g.c_hi - lo) * s.subs;
       ctx->side_work = true;
