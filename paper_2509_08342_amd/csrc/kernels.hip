@@ -928,6 +928,35 @@ __device__ __forceinline__ void ffn_tile(const FfnArgs& a, const W* G, const W* 
   const int lu = tid / kLpu;               // unit within this work-group
   const int unit = sub * UPW + lu;         // unit within the chunk
   const int f_first = sub * UPW;           // first down row of this work-group
+  const int n_steps = d / STEP;
+
+  // gate/up loads of one batch of RB steps (clamped to the last step; used
+  // only in range)
+  auto load_batch = [&](int s0, uint4(&g)[RB], uint4(&uu)[RB]) {
+#pragma unroll
+    for (int u = 0; u < RB; ++u) {
+      const int sk = min(s0 + u, n_steps - 1) * STEP;  // first k of the step
+      const size_t off =
+          (static_cast<size_t>(sk / kKTile) * kChunkUnits + unit) * kKTile + (sk % kKTile) + lane_u * VEC;
+      g[u] = ldw16(G + off);
+      uu[u] = ldw16(U + off);
+    }
+  };
+  // down-row loads of one batch of PB rows (clamped to the work-group's last)
+  auto load_rows = [&](int f0, uint4(&dd)[PB][Q]) {
+#pragma unroll
+    for (int u = 0; u < PB; ++u)
+#pragma unroll
+      for (int q = 0; q < Q; ++q) {
+        const int col = min((tid + THREADS * q) * VEC, d - VEC);  // clamped; used only if in range
+        dd[u][q] = ldw16(D + static_cast<size_t>(f_first + min(f0 + u, UPW - 1)) * d + col);
+      }
+  };
+
+  // the first weight batch is requested before the activations are staged,
+  // so that no work-group waits on the activation load with nothing in flight
+  uint4 gn[RB], un[RB];
+  load_batch(0, gn, un);
 
   // stage the tile's activations in LDS (zero rows past nt)
   const int vec_per_row = d / VEC;
@@ -943,25 +972,13 @@ __device__ __forceinline__ void ffn_tile(const FfnArgs& a, const W* G, const W* 
   __syncthreads();
 
   // phase 1: gate/up dot products of this lane group's unit
+  uint4 dn[PB][Q];
   {
     float ag[NTT], au[NTT];
 #pragma unroll
     for (int t = 0; t < NTT; ++t) ag[t] = au[t] = 0.0f;
-    const int n_steps = d / STEP;
-    // software pipeline: batch s0 + RB is loaded while batch s0 is used;
-    // every load is issued (clamped to the last step), used only in range
-    uint4 gr[RB], ur[RB], gn[RB], un[RB];
-    auto load_batch = [&](int s0, uint4(&g)[RB], uint4(&uu)[RB]) {
-#pragma unroll
-      for (int u = 0; u < RB; ++u) {
-        const int sk = min(s0 + u, n_steps - 1) * STEP;  // first k of the step
-        const size_t off =
-            (static_cast<size_t>(sk / kKTile) * kChunkUnits + unit) * kKTile + (sk % kKTile) + lane_u * VEC;
-        g[u] = ldw16(G + off);
-        uu[u] = ldw16(U + off);
-      }
-    };
-    load_batch(0, gn, un);
+    // software pipeline: batch s0 + RB is loaded while batch s0 is used
+    uint4 gr[RB], ur[RB];
     for (int s0 = 0; s0 < n_steps; s0 += RB) {
 #pragma unroll
       for (int u = 0; u < RB; ++u) {
@@ -989,6 +1006,8 @@ __device__ __forceinline__ void ffn_tile(const FfnArgs& a, const W* G, const W* 
         }
       }
     }
+    // the first down rows are requested before the phase boundary
+    load_rows(0, dn);
 #pragma unroll
     for (int t = 0; t < NTT; ++t) {
 #pragma unroll
@@ -1013,18 +1032,8 @@ __device__ __forceinline__ void ffn_tile(const FfnArgs& a, const W* G, const W* 
       for (int q = 0; q < Q; ++q)
 #pragma unroll
         for (int i = 0; i < VEC; ++i) y[t][q][i] = 0.0f;
-    // software pipeline as in phase 1 (rows clamped to the work-group's last)
-    uint4 dr[PB][Q], dn[PB][Q];
-    auto load_rows = [&](int f0, uint4(&dd)[PB][Q]) {
-#pragma unroll
-      for (int u = 0; u < PB; ++u)
-#pragma unroll
-        for (int q = 0; q < Q; ++q) {
-          const int col = min((tid + THREADS * q) * VEC, d - VEC);  // clamped; used only if in range
-          dd[u][q] = ldw16(D + static_cast<size_t>(f_first + min(f0 + u, UPW - 1)) * d + col);
-        }
-    };
-    load_rows(0, dn);
+    // software pipeline as in phase 1
+    uint4 dr[PB][Q];
     for (int f0 = 0; f0 < UPW; f0 += PB) {
 #pragma unroll
       for (int u = 0; u < PB; ++u)
@@ -1167,9 +1176,12 @@ static hipError_t dispatch_ffn(const FfnArgs& a, int nt, int q, int max_tok, hip
 
 // Tokens per tile: the smallest of {1, 2, 4, 8} covering max_tok, limited so
 // that the LDS tile stays within 64 KiB and the accumulators fit.
+#ifndef MSK_NT_MAX
+#define MSK_NT_MAX 8
+#endif
 static int pick_nt(int max_tok, int d, int elem, int q, int vec, int upw) {
   int nt = 1;
-  while (nt < max_tok && nt < 8) nt <<= 1;
+  while (nt < max_tok && nt < MSK_NT_MAX) nt <<= 1;
   while (nt > 1 &&
          (static_cast<size_t>(nt) * (static_cast<size_t>(d) * elem + sizeof(float) * upw) > 65536 ||
           !ffn_fits(nt, q, vec)))

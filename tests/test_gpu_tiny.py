@@ -59,6 +59,29 @@ def test_tiny_ragged_token_counts(rig, T):
     check_layer(rig, 0, hf, y, idx, w)
 
 
+
+@pytest.mark.parametrize("T", [24, 37, 64])
+def test_tiny_multi_tile_experts_independent_of_residency(rig, T):
+    """Experts with more tokens than one FFN tile spread their tiles over
+    several work-groups, and each tile takes the shape of its real token
+    count (read on the device).  Resident launches size their grid before
+    the routing is known, streamed ones after it; every token's sums run in
+    the same order either way, so outputs are bitwise equal across residency
+    states and match the oracle."""
+    h, hf = rig.hidden(T, tag=700 + T)
+    outs = []
+    for r, tops in ((0.5, [0, 1, 2, 3]), (0.0, []), (1.0, list(range(8))), (0.5, [4, 5, 6, 7])):
+        _setup(rig, r, tops)
+        y, idx, w = _run(rig, h, T)
+        if not outs:
+            check_layer(rig, 0, hf, y, idx, w)
+            counts = np.bincount(idx.cpu().numpy()[:T].reshape(-1), minlength=8)
+            assert counts.max() > 8, counts  # some expert's tokens span two tiles
+            assert (counts % 8 != 0).any(), counts  # and some tile holds fewer than 8
+        outs.append(y.cpu().numpy()[:T])
+    for o in outs[1:]:
+        assert np.array_equal(o, outs[0])
+
 def test_tiny_outputs_independent_of_residency_and_split(rig):
     """Eq. (2) output must not depend on r or on which tops are cached: every
     residency subset at r=0.5, and several subsets at r in {0,.25,.75,1}
