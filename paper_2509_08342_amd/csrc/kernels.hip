@@ -91,6 +91,19 @@ __device__ __forceinline__ void unpack(const uint4 v, float (&o)[8]) {
 
 __device__ __forceinline__ float silu(float x) { return x / (1.0f + expf(-x)); }
 
+// v_mfma_f32_16x16x32_bf16: lane l holds A[row l%16][8 k from 8*(l/16)],
+// B[8 k from 8*(l/16)][column l%16] and the result C[rows 4*(l/16)+r][column
+// l%16].  The k order inside a step is the same for A and B, which is all
+// the contraction needs.
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ bf16x8_t as_bf16x8(uint4 v) { return __builtin_bit_cast(bf16x8_t, v); }
+
+__device__ __forceinline__ f32x4_t mfma16(bf16x8_t a, bf16x8_t b, f32x4_t c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+}
+
 // -------------------------------------------------------------------- route
 //
 // Per token (one wave): K rounds of wave argmax over the untaken experts
@@ -1080,6 +1093,196 @@ __device__ __forceinline__ void ffn_tile(const FfnArgs& a, const W* G, const W* 
   __syncthreads();
 }
 
+// Tiles of 8 bf16 rows: the gate/up dot products run on the matrix cores
+// (v_mfma_f32_16x16x32_bf16; with 8 rows the fma chains of ffn_tile cost
+// more VALU time than the tile's weights take to stream).  A = the tile's
+// rows (rows 8-15 zero), B = 16 units: lane l holds row / unit l % 16 and
+// the 8 k values 8 (l / 16) + [0, 8) of a 32-wide k block, taken for both
+// operands at the same offsets of the chunk's k-tiled rows.  Wave w works on
+// unit block w % NB over every other 64-wide k piece from w / NB; the two k
+// halves are added in LDS (first half + second half), then the SwiGLU
+// product.  The down projection is ffn_tile's.  The activation rows are
+// staged with a pitch of d + kHsPad elements so that the 8 rows' A
+// fragments fall in different LDS banks.  Which path a tile takes depends
+// only on its row count, so a token's partial is the same in every launch.
+constexpr int kMmaTileRows = 8;
+constexpr int kHsPad = 8;
+
+// LDS of an FFN launch: activation tile, SwiGLU tile, and for 8-row bf16
+// tiles the k-half exchange.
+__host__ __device__ constexpr size_t ffn_lds_bytes(int nt, int d, int elem, int upw) {
+  return (nt == kMmaTileRows && elem == 2)
+             ? static_cast<size_t>(nt) * (d + kHsPad) * elem + sizeof(float) * nt * upw + (upw / 16) * 32 * 8 * sizeof(float)
+             : static_cast<size_t>(nt) * d * elem + sizeof(float) * nt * upw;
+}
+
+template <int Q, int UPW, int RB>
+__device__ __forceinline__ void ffn_tile_mma(const FfnArgs& a, const uint16_t* G, const uint16_t* U,
+                                             const uint16_t* D, float* part, int a_planes, int plane, bool routed,
+                                             int p0, int tile, int nt, uint16_t* hs, float* as, float* red, int sub) {
+  using W = uint16_t;
+  constexpr int VEC = 8;
+  constexpr int NTT = kMmaTileRows;
+  constexpr int THREADS = UPW * kLpu;
+  constexpr int NB = UPW / 16;  // unit blocks; 2 NB waves
+  constexpr int KB = 2;         // k pieces per load batch
+  constexpr int PB = (RB < 16 / Q) ? RB : 16 / Q;
+  static_assert(THREADS == 128 * NB, "two waves per unit block");
+  const int d = a.d;
+  const int pitch = d + kHsPad;
+  const W* hsrc = static_cast<const W*>(a.h);
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int ub = wave % NB, kh = wave / NB;
+  const int n = lane & 15, g = lane >> 4;
+  const int unit = sub * UPW + ub * 16 + n;
+  const int f_first = sub * UPW;
+  const int n_kt = d / kKTile;
+  const int npw = (n_kt - kh + 1) / 2;  // k pieces of this wave: kh, kh + 2, ...
+
+  auto load_b = [&](int i0, uint4(&bg)[KB][2], uint4(&bu)[KB][2]) {
+#pragma unroll
+    for (int i = 0; i < KB; ++i) {
+      // clamped (also when this wave has no piece, d = 64); used only in range
+      const int kt = min(kh + 2 * max(0, min(i0 + i, npw - 1)), n_kt - 1);
+      const size_t off = (static_cast<size_t>(kt) * kChunkUnits + unit) * kKTile + g * 8;
+#pragma unroll
+      for (int j = 0; j < 2; ++j) {
+        bg[i][j] = ldw16(G + off + 32 * j);
+        bu[i][j] = ldw16(U + off + 32 * j);
+      }
+    }
+  };
+  auto load_rows = [&](int f0, uint4(&dd)[PB][Q]) {
+#pragma unroll
+    for (int u = 0; u < PB; ++u)
+#pragma unroll
+      for (int q = 0; q < Q; ++q) {
+        const int col = min((tid + THREADS * q) * VEC, d - VEC);  // clamped; used only if in range
+        dd[u][q] = ldw16(D + static_cast<size_t>(f_first + min(f0 + u, UPW - 1)) * d + col);
+      }
+  };
+
+  uint4 bgn[KB][2], bun[KB][2];
+  load_b(0, bgn, bun);
+  // stage the tile's rows (zero past nt), pitch d + kHsPad
+  const int vec_per_row = d / VEC;
+  for (int i = tid; i < NTT * vec_per_row; i += THREADS) {
+    const int t = i / vec_per_row, k = (i - t * vec_per_row) * VEC;
+    uint4 v = make_uint4(0, 0, 0, 0);
+    if (t < nt) {
+      const int tok = routed ? a.perm[p0 + tile + t] / a.K : tile + t;
+      v = ld16(hsrc + static_cast<size_t>(tok) * d + k);
+    }
+    *reinterpret_cast<uint4*>(hs + static_cast<size_t>(t) * pitch + k) = v;
+  }
+  __syncthreads();
+
+  uint4 dn[PB][Q];
+  {
+    f32x4_t cg = {0.0f, 0.0f, 0.0f, 0.0f}, cu = {0.0f, 0.0f, 0.0f, 0.0f};
+    uint4 bgr[KB][2], bur[KB][2];
+    for (int i0 = 0; i0 < npw; i0 += KB) {
+#pragma unroll
+      for (int i = 0; i < KB; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+          bgr[i][j] = bgn[i][j];
+          bur[i][j] = bun[i][j];
+        }
+      load_b(i0 + KB, bgn, bun);
+#pragma unroll
+      for (int i = 0; i < KB; ++i) {
+        if (i0 + i < npw) {
+          const int kt = kh + 2 * (i0 + i);
+#pragma unroll
+          for (int j = 0; j < 2; ++j) {
+            uint4 av = make_uint4(0, 0, 0, 0);
+            if (n < NTT) av = ld16(hs + static_cast<size_t>(n) * pitch + kt * kKTile + 32 * j + g * 8);
+            cg = mfma16(as_bf16x8(av), as_bf16x8(bgr[i][j]), cg);
+            cu = mfma16(as_bf16x8(av), as_bf16x8(bur[i][j]), cu);
+          }
+        }
+      }
+    }
+    // the first down rows are requested before the k halves meet
+    load_rows(0, dn);
+    // lanes g < 2 hold rows 4 g + r < 8
+    if (kh == 1 && g < 2) {
+      float* r = red + (static_cast<size_t>(ub) * 32 + lane) * 8;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        r[i] = cg[i];
+        r[4 + i] = cu[i];
+      }
+    }
+    __syncthreads();
+    if (kh == 0 && g < 2) {
+      const float* r = red + (static_cast<size_t>(ub) * 32 + lane) * 8;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const float sg = cg[i] + r[i], su = cu[i] + r[4 + i];
+        as[(4 * g + i) * UPW + ub * 16 + n] = silu(sg) * su;
+      }
+    }
+  }
+  __syncthreads();
+
+  // phase 2 as in ffn_tile
+  {
+    float y[NTT][Q][VEC];
+#pragma unroll
+    for (int t = 0; t < NTT; ++t)
+#pragma unroll
+      for (int q = 0; q < Q; ++q)
+#pragma unroll
+        for (int i = 0; i < VEC; ++i) y[t][q][i] = 0.0f;
+    uint4 dr[PB][Q];
+    for (int f0 = 0; f0 < UPW; f0 += PB) {
+#pragma unroll
+      for (int u = 0; u < PB; ++u)
+#pragma unroll
+        for (int q = 0; q < Q; ++q) dr[u][q] = dn[u][q];
+      load_rows(f0 + PB, dn);
+#pragma unroll
+      for (int u = 0; u < PB; ++u) {
+        float av[NTT];
+#pragma unroll
+        for (int t = 0; t < NTT; ++t) av[t] = as[t * UPW + f0 + u];
+#pragma unroll
+        for (int q = 0; q < Q; ++q) {
+          const int col = (tid + THREADS * q) * VEC;
+          if (col < d) {
+            float dv[VEC];
+            unpack(dr[u][q], dv);
+#pragma unroll
+            for (int t = 0; t < NTT; ++t)
+#pragma unroll
+              for (int i = 0; i < VEC; ++i) y[t][q][i] = fmaf(av[t], dv[i], y[t][q][i]);
+          }
+        }
+      }
+    }
+#pragma unroll
+    for (int t = 0; t < NTT; ++t) {
+      if (t < nt) {
+        const int row = routed ? (p0 + tile + t) : (tile + t);
+        float* dst = part + (static_cast<size_t>(row) * a_planes + plane) * d;
+#pragma unroll
+        for (int q = 0; q < Q; ++q) {
+          const int col = (tid + THREADS * q) * VEC;
+          if (col < d) {
+#pragma unroll
+            for (int i = 0; i < VEC; i += 4)
+              *reinterpret_cast<float4*>(dst + col + i) =
+                  make_float4(y[t][q][i], y[t][q][i + 1], y[t][q][i + 2], y[t][q][i + 3]);
+          }
+        }
+      }
+    }
+  }
+  __syncthreads();
+}
+
 // Grid: n_wg x n_tiles work-groups; block b computes token tile b % n_tiles
 // (and every n_tiles-th tile after it) of work-group slot b / n_tiles, so the
 // tiles of an expert with many tokens run side by side.  The tile shape
@@ -1112,14 +1315,26 @@ __global__ __launch_bounds__(UPW * kLpu) void ffn_chunk_kernel(FfnArgs a, int n_
   const int a_planes = routed ? a.n_planes : a.n_planes_sh;
   const int plane = c * a.subs + sub;
 
-  W* hs = reinterpret_cast<W*>(ffn_smem);                                    // [NT][d]
-  float* as = reinterpret_cast<float*>(ffn_smem + sizeof(W) * NT * a.d);     // [NT][UPW]
+  constexpr bool kMma = (NT == kMmaTileRows && sizeof(W) == 2);
+  const int hs_pitch = kMma ? a.d + kHsPad : a.d;
+  W* hs = reinterpret_cast<W*>(ffn_smem);                                       // [NT][hs_pitch]
+  float* as = reinterpret_cast<float*>(ffn_smem + sizeof(W) * NT * hs_pitch);  // [NT][UPW]
+  float* red = as + NT * UPW;                                                   // k-half exchange (kMma)
 
   // one tile per work-group (max_tok bounds every task's token count);
   // later tiles only if it did not
   const int tile = tile0 * NT;
   const int nt = min(NT, n_tok - tile);
 #define MSK_FFN_TILE(NTT, T0, N) ffn_tile<W, NTT, Q, UPW, RB>(a, G, U, D, part, a_planes, plane, routed, p0, T0, N, hs, as, sub)
+#define MSK_FFN_FULL(T0, N)                                                                                   \
+  do {                                                                                                        \
+    if constexpr (kMma)                                                                                       \
+      ffn_tile_mma<Q, UPW, RB>(a, reinterpret_cast<const uint16_t*>(G), reinterpret_cast<const uint16_t*>(U), \
+                               reinterpret_cast<const uint16_t*>(D), part, a_planes, plane, routed, p0, T0, N,  \
+                               reinterpret_cast<uint16_t*>(hs), as, red, sub);                                \
+    else                                                                                                      \
+      MSK_FFN_TILE(NT, T0, N);                                                                                \
+  } while (0)
   if (NT >= 4 && nt == 1) {
     MSK_FFN_TILE((NT >= 4 ? 1 : NT), tile, nt);
   } else if (NT >= 8 && nt <= 2) {
@@ -1127,15 +1342,16 @@ __global__ __launch_bounds__(UPW * kLpu) void ffn_chunk_kernel(FfnArgs a, int n_
   } else if (NT >= 8 && nt <= 4) {
     MSK_FFN_TILE((NT >= 8 ? 4 : NT), tile, nt);
   } else {
-    MSK_FFN_TILE(NT, tile, nt);
+    MSK_FFN_FULL(tile, nt);
   }
-  for (int t2 = tile + NT * n_tiles; t2 < n_tok; t2 += NT * n_tiles) MSK_FFN_TILE(NT, t2, min(NT, n_tok - t2));
+  for (int t2 = tile + NT * n_tiles; t2 < n_tok; t2 += NT * n_tiles) MSK_FFN_FULL(t2, min(NT, n_tok - t2));
+#undef MSK_FFN_FULL
 #undef MSK_FFN_TILE
 }
 
 template <typename W, int NT, int Q, int UPW>
 static hipError_t launch_ffn_one(const FfnArgs& a, int max_tok, hipStream_t s) {
-  const size_t lds = sizeof(W) * NT * a.d + sizeof(float) * NT * UPW;
+  const size_t lds = ffn_lds_bytes(NT, a.d, static_cast<int>(sizeof(W)), UPW);
   const int n_tiles = max(1, (max_tok + NT - 1) / NT);
   const int64_t grid = static_cast<int64_t>(a.n_wg) * n_tiles;
   if (grid > 0x7fffffff) return hipErrorInvalidValue;
@@ -1183,7 +1399,7 @@ static int pick_nt(int max_tok, int d, int elem, int q, int vec, int upw) {
   int nt = 1;
   while (nt < max_tok && nt < MSK_NT_MAX) nt <<= 1;
   while (nt > 1 &&
-         (static_cast<size_t>(nt) * (static_cast<size_t>(d) * elem + sizeof(float) * upw) > 65536 ||
+         (ffn_lds_bytes(nt, d, elem, upw) > 65536 ||
           !ffn_fits(nt, q, vec)))
     nt >>= 1;
   return nt;
@@ -1590,19 +1806,7 @@ hipError_t launch_ffn(const FfnArgs& a, int max_tok, hipStream_t s) {
 
 // ------------------------------------------------------------ prefill MFMA
 //
-// v_mfma_f32_16x16x32_bf16: lane l holds A[row l%16][8 k from 8*(l/16)],
-// B[8 k from 8*(l/16)][column l%16] and the result C[rows 4*(l/16)+r][column
-// l%16].  The k order inside a step is the same for A and B, which is all
-// the contraction needs.
-
-typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
-typedef float f32x4_t __attribute__((ext_vector_type(4)));
-
-__device__ __forceinline__ bf16x8_t as_bf16x8(uint4 v) { return __builtin_bit_cast(bf16x8_t, v); }
-
-__device__ __forceinline__ f32x4_t mfma16(bf16x8_t a, bf16x8_t b, f32x4_t c) {
-  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
-}
+// (operand layout of v_mfma_f32_16x16x32_bf16: see mfma16)
 
 // fp32 -> bf16, round to nearest even (finite values)
 __device__ __forceinline__ uint16_t f2bf(float f) {
