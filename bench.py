@@ -246,6 +246,36 @@ def ffn_roofline(an):
                 bytes_per_launch=int(b / n))
 
 
+MFMA_BF16_PEAK_TFLOPS = 2500.0  # dense bf16 matrix-core peak of MI355X
+
+
+def mfma_roofline(an, shape, T, steps):
+    """Matrix-core FFN kernels of the prefill path (gate/up and down launches):
+    algorithmic flops (6 d F per token and selected expert, plus the shared
+    experts' 6 d F_sh per token) over their summed launch durations, against
+    the bf16 dense peak and against the attainable bound min(peak, flops per
+    weight byte x 8 TB/s), where the weight bytes are those the launches
+    read.  None when the forwards took the decode path."""
+    ks = [an["kernels"]["ffn_resident"], an["kernels"]["ffn_streamed"], an["kernels"]["ffn_down"]]
+    if an["kernels"]["ffn_down"]["launches"] == 0:
+        return None
+    ms_tot = sum(k["total_ms"] for k in ks)
+    b = sum(k["bytes"] for k in ks)
+    if ms_tot <= 0 or b <= 0:
+        return None
+    flops_step = 6.0 * shape.d_model * (shape.d_ff * T * shape.top_k + shape.d_ff_shared * T * shape.n_shared)
+    flops = flops_step * steps
+    tflops = flops / (ms_tot * 1e-3) / 1e12
+    intensity = flops / b
+    hbm_tflops = intensity * HBM_PEAK_GBPS * 1e9 / 1e12
+    attainable = min(MFMA_BF16_PEAK_TFLOPS, hbm_tflops)
+    return dict(bound="mfma" if MFMA_BF16_PEAK_TFLOPS < hbm_tflops else "hbm", achieved=round(tflops, 1),
+                peak=MFMA_BF16_PEAK_TFLOPS, unit="TFLOP/s", frac=round(tflops / MFMA_BF16_PEAK_TFLOPS, 4),
+                attainable=round(attainable, 1), attainable_frac=round(tflops / attainable, 4),
+                flop_per_weight_byte=round(intensity, 1), flops_per_step=flops_step,
+                launches=sum(k["launches"] for k in ks))
+
+
 # ------------------------------------------------------------------ timing
 
 def run_steps(rig, hs, steps, warmup, flags, timeline=True, cold=False, T=1, before_timed=None):
@@ -448,6 +478,32 @@ def pmc_summary(fetch_dir, write_dir, workload, out, cmd_fetch, cmd_write):
     with open(out, "w") as f:
         f.write("\n".join(lines))
     print("wrote %s: %d FFN dispatches, %.3f MB per launch" % (out, ffn_n, per / 1e6))
+
+
+def mfma_pmc_summary(d, workload, out, cmd):
+    """SQ_VALU_MFMA_BUSY_CYCLES and GRBM_GUI_ACTIVE per dispatch of a --pmc
+    run of both counters, by kernel, with the busy ratio normalised as
+    busy / (GRBM_GUI_ACTIVE x 256 CUs)."""
+    by = {}
+    for r in _read_rows(d, "counter_collection.csv"):
+        e = by.setdefault(int(r["Dispatch_Id"]), {"name": r["Kernel_Name"]})
+        e[r["Counter_Name"]] = e.get(r["Counter_Name"], 0.0) + float(r["Counter_Value"])
+    kern = {}
+    for e in by.values():
+        short = e["name"].split("(")[0].replace("void ", "")
+        k = kern.setdefault(short, [0, 0.0, 0.0])
+        k[0] += 1
+        k[1] += e.get("SQ_VALU_MFMA_BUSY_CYCLES", 0.0)
+        k[2] += e.get("GRBM_GUI_ACTIVE", 0.0)
+    lines = ["# Matrix-core busy cycles, %s workload, rocprofv3 counters" % workload, "",
+             "Command (from the repository root, on one MI355X):", "", "    " + cmd, "",
+             "| kernel | dispatches | SQ_VALU_MFMA_BUSY_CYCLES / dispatch | GRBM_GUI_ACTIVE / dispatch | "
+             "busy / (GUI_ACTIVE x 256 CUs) |", "|---|---|---|---|---|"]
+    for n, (c, busy, gui) in sorted(kern.items(), key=lambda x: -x[1][1]):
+        lines.append("| `%s` | %d | %.4g | %.4g | %.4f |" % (n, c, busy / c, gui / c, busy / max(gui * 256.0, 1.0)))
+    with open(out, "w") as f:
+        f.write("\n".join(lines) + "\n")
+    print("wrote %s (%d kernels)" % (out, len(kern)))
 
 
 def trace_summary(d, out, cmd):
@@ -698,6 +754,8 @@ def main():
     ap.add_argument("--pmc-summary", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
                     help="summarise two --pmc-pass runs (FETCH_SIZE, WRITE_SIZE) into --out")
     ap.add_argument("--trace-summary", metavar="DIR", help="summarise a --kernel-trace --stats run into --out")
+    ap.add_argument("--mfma-pmc-summary", metavar="DIR",
+                    help="summarise a --pmc SQ_VALU_MFMA_BUSY_CYCLES GRBM_GUI_ACTIVE run into --out")
     ap.add_argument("--r", type=float, default=None,
                     help="split ratio instead of the workload's (the cache keeps the same number of tops)")
     ap.add_argument("--all-tops", action="store_true",
@@ -719,6 +777,9 @@ def main():
         return
     if args.trace_summary:
         trace_summary(args.trace_summary, args.out, " ".join(args.cmd))
+        return
+    if args.mfma_pmc_summary:
+        mfma_pmc_summary(args.mfma_pmc_summary, args.workload, args.out, " ".join(args.cmd))
         return
     if args.gpus != 1:
         print("bench.py measures one GPU: this build of the split-expert layer has no "
@@ -808,6 +869,8 @@ def main():
                    "top_k": shape.top_k, "n_shared": shape.n_shared, "r": r, "tokens_per_step": T,
                    "expert_bits": shape.expert_bits or None},
         "roofline": roof,
+        # prefill: matrix-core utilisation of the FFN kernels (None at decode)
+        "mfma": mfma_roofline(an, shape, T, args.steps),
         # the layer as a whole is bound by the link its missing segments cross
         "copy_roofline": copy_roofline(tl),
         "tokens_per_s": round(T * 1e3 / ms_plain, 2),
@@ -850,6 +913,7 @@ def main():
         an_ar = analyse(tl_ar, args.steps, ms_ar)
         out["all_resident"] = {"us_per_layer": round(ms_ar_plain * 1e3, 1),
                                "us_per_layer_instrumented": round(ms_ar * 1e3, 1), "roofline": ffn_roofline(an_ar),
+                               "mfma": mfma_roofline(an_ar, shape, T, args.steps),
                                "kernels": {k: {"launches": v["launches"],
                                                "avg_us": round(v["total_ms"] / v["launches"] * 1e3, 2)
                                                if v["launches"] else None}

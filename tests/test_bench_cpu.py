@@ -90,3 +90,27 @@ def test_more_than_one_gpu_is_refused(monkeypatch, capsys):
         bench.main()
     assert ei.value.code == 2
     assert "one GPU" in capsys.readouterr().err
+
+
+def test_mfma_roofline_of_prefill_launches():
+    import synth
+    shape = synth.DEEPSEEK  # d 2048, F 1408, K 6, two shared experts of 1408
+    T, steps = 512, 2
+    # two steps: gate/up 0-1 ms and down 1-1.5 ms per step, 1 GB of weights per step
+    tl = [_rec("router", 0, 0.1), _rec("ffn_resident", 0.1, 1.1, 2 * 10 ** 9 // 3),
+          _rec("ffn_down", 1.1, 1.6, 10 ** 9 // 3),
+          _rec("router", 2, 2.1), _rec("ffn_resident", 2.1, 3.1, 2 * 10 ** 9 // 3),
+          _rec("ffn_down", 3.1, 3.6, 10 ** 9 // 3)]
+    an = bench.analyse(tl, steps, 2.0)
+    m = bench.mfma_roofline(an, shape, T, steps)
+    flops_step = 6.0 * 2048 * (1408 * T * 6 + 1408 * T * 2)
+    assert m["flops_per_step"] == pytest.approx(flops_step)
+    assert m["achieved"] == pytest.approx(flops_step * steps / 3e-3 / 1e12, rel=1e-3)
+    assert m["frac"] == pytest.approx(m["achieved"] / 2500.0, abs=1e-4)
+    intensity = flops_step * steps / (2 * (2 * 10 ** 9 // 3 + 10 ** 9 // 3))
+    assert m["flop_per_weight_byte"] == pytest.approx(intensity, rel=1e-3)
+    # 70 GFLOP over 1 GB: 70 flop per byte x 8 TB/s = 560 TFLOP/s < 2500, so HBM bounds it
+    assert m["bound"] == "hbm" and m["attainable"] == pytest.approx(intensity * 8.0, rel=1e-3)
+    assert m["attainable_frac"] == pytest.approx(m["achieved"] / m["attainable"], abs=1e-4)
+    # decode forwards (no down launches) report none
+    assert bench.mfma_roofline(bench.analyse(tl[:2], 1, 1.0), shape, 1, 1) is None
