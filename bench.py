@@ -276,6 +276,57 @@ def mfma_roofline(an, shape, T, steps):
                 launches=sum(k["launches"] for k in ks))
 
 
+def _read(path):
+    try:
+        with open(path) as f:
+            return f.read().strip()
+    except OSError:
+        return None
+
+
+def platform_info():
+    """The machine the figures come from: GPU name, architecture and CU
+    count, its current and peak engine / memory clocks (sysfs DPM tables,
+    else rocm-smi), the PCIe link's current and maximum speed and width, and
+    the host CPU model with the cores this process may use.  Read from sysfs,
+    /proc and a rocm-smi child process; a field that cannot be read is None."""
+    import subprocess
+    import torch
+    info = {}
+    try:
+        pr = torch.cuda.get_device_properties(0)
+        info["gpu"] = {"name": pr.name, "arch": pr.gcnArchName, "compute_units": pr.multi_processor_count,
+                       "memory_gib": round(pr.total_memory / GIB, 1)}
+        bdf = "%04x:%02x:%02x.0" % (pr.pci_domain_id, pr.pci_bus_id, pr.pci_device_id)
+        dev = "/sys/bus/pci/devices/" + bdf
+        info["pcie"] = {"bdf": bdf, "current_link_speed": _read(dev + "/current_link_speed"),
+                        "current_link_width": _read(dev + "/current_link_width"),
+                        "max_link_speed": _read(dev + "/max_link_speed"),
+                        "max_link_width": _read(dev + "/max_link_width")}
+        clocks = {}
+        for key, fname in (("sclk", "pp_dpm_sclk"), ("mclk", "pp_dpm_mclk")):
+            table = _read(dev + "/" + fname)
+            if table:
+                lines = [l for l in table.splitlines() if l.strip()]
+                cur = [l for l in lines if l.rstrip().endswith("*")]
+                clocks[key] = {"current": cur[0].split(":", 1)[1].strip(" *") if cur else None,
+                               "levels": [l.split(":", 1)[1].strip(" *") for l in lines]}
+        if not clocks:
+            try:
+                r = subprocess.run(["rocm-smi", "--showclocks"], capture_output=True, text=True, timeout=30)
+                clocks["rocm_smi"] = [l.strip() for l in r.stdout.splitlines() if "clk" in l.lower()][:8]
+            except (OSError, subprocess.SubprocessError):
+                pass
+        info["clocks"] = clocks or None
+    except Exception as e:  # reporting only: never fail the benchmark
+        info["error"] = repr(e)[:200]
+    cpuinfo = _read("/proc/cpuinfo") or ""
+    models = [l.split(":", 1)[1].strip() for l in cpuinfo.splitlines() if l.startswith("model name")]
+    info["cpu"] = {"model": models[0] if models else None, "logical_cpus": os.cpu_count(),
+                   "usable_cpus": len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity") else None}
+    return info
+
+
 # ------------------------------------------------------------------ timing
 
 def run_steps(rig, hs, steps, warmup, flags, timeline=True, cold=False, T=1, before_timed=None):
@@ -625,6 +676,7 @@ def run_decoder(args):
                        "cache": [int(c) for c in plan["cache"]]}
     log("TTFT %.1f ms, TPOT %.2f ms" % (ttft, tpot_ms))
     dec.close()
+    out["platform"] = platform_info()
     print(json.dumps(out), flush=True)
 
 
@@ -731,6 +783,7 @@ def run_stack(args):
         "h2d_gbps_over_step": round((tot["bytes_miss"] + tot["bytes_prefetch"]) / wall / 1e9, 2),
     })
     st.close()
+    out["platform"] = platform_info()
     print(json.dumps(out), flush=True)
 
 
@@ -923,6 +976,7 @@ def main():
         log("timing the CPU oracle")
         out["cpu_baseline"] = cpu_baseline(rig, [f for _, f in seq], args.cpu_seconds)
     rig.close()
+    out["platform"] = platform_info()
     print(json.dumps(out), flush=True)
 
 
