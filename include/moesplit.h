@@ -65,7 +65,8 @@ typedef enum { MS_F32 = 0, MS_BF16 = 1 } ms_dtype;
  * full-expert slots of the VRAM staging buffer U_b (0 -> 2*top_k: one set for
  * the running layer, one for the next layer's prefetch).  ffn_splits is the
  * number of work-groups that share one 64-unit chunk of the FFN kernel (1, 2
- * or 4; 0 -> chosen from the shape so that a decode step fills the GPU).  It
+ * or 4, and at most 2 when d_model > 4096: MS_E_UNSUPPORTED beyond; 0 ->
+ * chosen from the shape so that a decode step fills the GPU).  It
  * changes the summation grouping, not what is computed.  expert_bits = 2 or
  * 4 stores the routed experts as affine b-bit codes (the HQQ format of the
  * paper's 2-bit Mixtral setting, Sec. 5.1; see ms_set_expert_q); 0 keeps

@@ -15,10 +15,12 @@ constexpr int kMaxExperts = 512;   // grouping / ranking kernels' LDS bound
 constexpr int kMaxTopK = 64;
 constexpr int kMaxModelDim = 8192;  // d_model limit of every kernel
 // Work-groups per chunk the FFN kernel supports at this width and element
-// size (16-byte loads; at most 8 column passes in the down projection).
+// size: 16-byte loads, and a one-row tile's down-projection accumulators
+// (column passes x elements per load) within 32 registers, i.e. at most 4
+// column passes in bf16 and 8 in fp32.
 inline int max_ffn_splits(int d, int elem) {
   int subs = 4;
-  while (subs > 1 && d > (64 / subs) * kFfnLanesPerUnit * (16 / elem) * 8) subs >>= 1;
+  while (subs > 1 && d > (64 / subs) * kFfnLanesPerUnit * (16 / elem) * (2 * elem)) subs >>= 1;
   return subs;
 }
 

@@ -129,3 +129,24 @@ def test_b_bit_experts_reject_unsupported_shapes():
     with pytest.raises(ms.MoeSplitError) as ei:
         ms.ms_query_sizes(desc)
     assert ei.value.status == ms.MS_E_UNSUPPORTED
+
+
+@pytest.mark.parametrize("dtype,d,allowed", [("bf16", 8192, 2), ("f32", 8192, 2), ("bf16", 4096, 4),
+                                              ("f32", 4096, 4), ("bf16", 2048, 4)])
+def test_ffn_splits_bounded_by_the_kernel_table(dtype, d, allowed):
+    """A chunk split over more work-groups needs more column passes per
+    thread in the down projection; splits whose one-row accumulators would
+    exceed the kernel's register budget (bf16 at d = 8192 beyond 2) are
+    refused with MS_E_UNSUPPORTED, and the automatic choice stays within the
+    bound."""
+    ms = _ms()
+    shape = synth.ModelShape("split-limit", 1, d, 256, 8, 2, dtype)
+    for splits in (1, 2, 4):
+        desc = _desc(shape)
+        desc.ffn_splits = splits
+        if splits <= allowed:
+            ms.ms_query_sizes(desc)
+        else:
+            with pytest.raises(ms.MoeSplitError) as ei:
+                ms.ms_query_sizes(desc)
+            assert ei.value.status == ms.MS_E_UNSUPPORTED
