@@ -152,8 +152,8 @@ typedef struct ms_ctx ms_ctx;
 
 /* Derived sizes of a model shape.  MS_E_INVALID if a field is out of range
  * (non-positive sizes, top_k > n_experts, unknown dtype); MS_E_UNSUPPORTED if
- * the kernels do not cover the shape: d_model must be a multiple of 64 and at
- * most 8192, n_experts at most 512, top_k at most 64, and max_tokens * top_k
+ * the kernels do not cover the shape: d_model must be a multiple of 64 in
+ * [256, 8192], n_experts at most 512, top_k at most 64, and max_tokens * top_k
  * at most 2^24. */
 ms_status ms_query_sizes(const ms_model_desc* desc, ms_sizes* out);
 

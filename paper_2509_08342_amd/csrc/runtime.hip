@@ -76,8 +76,10 @@ ms_status derive_shape(const ms_model_desc* d, Shape* s, std::string* err) {
     *err = "invalid model description";
     return MS_E_INVALID;
   }
-  if (d->d_model % 64 != 0 || d->d_model > kMaxD) {
-    *err = "d_model must be a multiple of 64 and at most 8192";
+  // the prefill kernels stage activation slabs of 128 and the decode
+  // kernels' tiles assume a few 64-wide k pieces: d_model in [256, 8192]
+  if (d->d_model % 64 != 0 || d->d_model < 256 || d->d_model > kMaxD) {
+    *err = "d_model must be a multiple of 64 in [256, 8192]";
     return MS_E_UNSUPPORTED;
   }
   if (d->n_experts > msk::kMaxExperts || d->top_k > msk::kMaxTopK) {

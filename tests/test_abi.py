@@ -150,3 +150,14 @@ def test_ffn_splits_bounded_by_the_kernel_table(dtype, d, allowed):
             with pytest.raises(ms.MoeSplitError) as ei:
                 ms.ms_query_sizes(desc)
             assert ei.value.status == ms.MS_E_UNSUPPORTED
+
+
+@pytest.mark.parametrize("d", [64, 128, 192, 8256])
+def test_model_dim_outside_the_kernels_is_refused(d):
+    """d_model outside [256, 8192] (the prefill kernels stage 128-wide
+    activation slabs) is refused with MS_E_UNSUPPORTED in every dtype."""
+    ms = _ms()
+    for dtype in ("bf16", "f32"):
+        with pytest.raises(ms.MoeSplitError) as ei:
+            ms.ms_query_sizes(_desc(synth.ModelShape("narrow", 1, d, 256, 8, 2, dtype)))
+        assert ei.value.status == ms.MS_E_UNSUPPORTED

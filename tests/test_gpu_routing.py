@@ -92,9 +92,9 @@ def test_many_token_router_follows_fixed_logit_order(which):
     tokens (two full 32-token tiles and a ragged one)."""
     import oracle
     from paper_2509_08342_amd import moesplit as ms
-    from test_gpu_tiny import _golden_router_case
+    from test_gpu_tiny import GOLDEN_D, _golden_router_case
     from workload import SplitRig
-    shape = synth.ModelShape("golden-order", 1, 128, 64, 2, 1, "f32")
+    shape = synth.ModelShape("golden-order", 1, GOLDEN_D, 64, 2, 1, "f32")
     h1, w_r, expect = _golden_router_case(which)
     T = 70
     h = np.repeat(h1, T, axis=0)

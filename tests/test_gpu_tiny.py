@@ -237,12 +237,16 @@ def test_tiny_error_codes(rig):
     assert ei.value.status == ms.MS_E_INVALID
 
 
+GOLDEN_D = 256  # the narrowest supported d_model; the cases use elements 0-65, the rest are zero
+
+
 def _golden_router_case(which):
-    """Router of two experts on d = 128 whose top-1 choice depends on the
+    """Router of two experts on d = 256 whose top-1 choice depends on the
     fixed fp32 logit order: expert 0's products follow the golden patterns of
-    tests/golden/two_expert_cases.json, expert 1 has one exact product."""
-    h = np.zeros((1, 128), np.float32)
-    w_r = np.zeros((128, 2), np.float32)
+    tests/golden/two_expert_cases.json (elements beyond them zero, which adds
+    exact zeros to every residue's chain), expert 1 has one exact product."""
+    h = np.zeros((1, GOLDEN_D), np.float32)
+    w_r = np.zeros((GOLDEN_D, 2), np.float32)
     prods = {"a": {0: 2.0 ** 24, 1: 1.0, 65: 1.0}, "b": {0: 2.0 ** 24, 16: 1.0, 32: 1.0},
              "c": {0: 2.0 ** 24, 1: 1.0, 33: 1.0}}[which]
     for j, v in prods.items():
@@ -259,7 +263,7 @@ def _golden_router_case(which):
 def test_router_follows_fixed_logit_order(which):
     import oracle
     from workload import SplitRig
-    shape = synth.ModelShape("golden-order", 1, 128, 64, 2, 1, "f32")
+    shape = synth.ModelShape("golden-order", 1, GOLDEN_D, 64, 2, 1, "f32")
     h, w_r, expect = _golden_router_case(which)
     assert oracle.topk(oracle.router_logits(h, w_r), 1)[0, 0] == expect
     with SplitRig(shape, seed=3, max_tokens=1, budget_bytes=0) as rig:
