@@ -60,3 +60,42 @@ def test_widest_model_dim_independent_of_residency(rig, T):
     for y, idx in outs[1:]:
         assert np.array_equal(idx, outs[0][1])
         assert np.array_equal(y, outs[0][0])
+
+
+# the most experts and the largest top-K the kernels take: 512 experts, top-64
+# (d_ff 128: two chunks, so r = .5 splits every expert); T = 64 and 100 take
+# the many-token routing, and in bf16 the matrix-core path (T K >= 8 E) with
+# more experts than one matrix-core launch holds
+WIDE_E_F32 = synth.ModelShape("wide-e-f32", 1, 256, 128, 512, 64, "f32")
+WIDE_E_BF16 = synth.ModelShape("wide-e-bf16", 1, 256, 128, 512, 64, "bf16")
+MAX_T_E = 100
+
+
+@pytest.fixture(scope="module", params=[WIDE_E_BF16, WIDE_E_F32], ids=lambda s: s.name)
+def rig_e(request):
+    from workload import SplitRig
+    s = request.param
+    r = SplitRig(s, seed=4, max_tokens=MAX_T_E, budget_bytes=s.n_experts * s.expert_bytes)
+    yield r
+    r.close()
+
+
+@pytest.mark.parametrize("T", [1, 5, 16, 64, MAX_T_E])
+def test_most_experts_largest_top_k_parity(rig_e, T):
+    _setup(rig_e, 0.5, list(range(0, 512, 2)))
+    h, hf = rig_e.hidden(T, tag=980 + T)
+    y, idx, w = _run(rig_e, h, T)
+    check_layer(rig_e, 0, hf, y, idx, w)
+
+
+def test_most_experts_independent_of_residency(rig_e):
+    T = 5
+    h, hf = rig_e.hidden(T, tag=990)
+    outs = []
+    for ratio, tops in ((0.5, list(range(0, 512, 2))), (1.0, list(range(512))), (0.0, [])):
+        _setup(rig_e, ratio, tops)
+        y, idx, w = _run(rig_e, h, T)
+        outs.append((y.cpu().numpy()[:T], idx.cpu().numpy()[:T]))
+    for y, idx in outs[1:]:
+        assert np.array_equal(idx, outs[0][1])
+        assert np.array_equal(y, outs[0][0])
