@@ -847,7 +847,7 @@ def main():
         mfma_pmc_summary(args.mfma_pmc_summary, args.workload, args.out, " ".join(args.cmd))
         return
     if args.gpus != 1:
-        print("bench.py measures one GPU: this build of the split-expert layer has no "
+        print("bench.py measures one GPU: the split-expert layer library has no "
               "multi-GPU path; run with --gpus 1", file=sys.stderr)
         sys.exit(2)
 
