@@ -448,6 +448,10 @@ struct ms_ctx {
   hipEvent_t ev_route = nullptr, ev_res = nullptr, ev_side_done = nullptr, ev_last = nullptr;
   hipEvent_t ev_side2_done = nullptr;
   bool has_last = false;
+  // the most recent end-of-work record: ev_last (prediction) or the layer's
+  // last_fwd (a forward records only that one; each marker between kernels
+  // costs the stream a few microseconds)
+  hipEvent_t last_ev = nullptr;
   hipStream_t last_stream = nullptr;
   std::vector<hipEvent_t> free_events;
   // timeline
@@ -844,7 +848,7 @@ void set_route_workspace(ms_ctx* ctx, msk::RouteArgs* r) {
 // Order work on `stream` after the previous forward/prediction of this
 // context (they share the work buffers).
 ms_status order_after_last(ms_ctx* ctx, hipStream_t stream) {
-  if (ctx->has_last && ctx->last_stream != stream) MS_HIP(hipStreamWaitEvent(stream, ctx->ev_last, 0));
+  if (ctx->has_last && ctx->last_stream != stream) MS_HIP(hipStreamWaitEvent(stream, ctx->last_ev, 0));
   return MS_OK;
 }
 
@@ -1168,7 +1172,7 @@ void ms_destroy(ms_ctx* ctx) {
   if (ctx->copy) (void)hipStreamSynchronize(ctx->copy);
   if (ctx->side) (void)hipStreamSynchronize(ctx->side);
   if (ctx->side2) (void)hipStreamSynchronize(ctx->side2);
-  if (ctx->has_last) (void)hipEventSynchronize(ctx->ev_last);
+  if (ctx->has_last) (void)hipEventSynchronize(ctx->last_ev);
   for (LayerState& L : ctx->layers) {
     for (hipEvent_t ev : L.pending_loads) (void)hipEventDestroy(ev);
     if (L.last_fwd) (void)hipEventDestroy(L.last_fwd);
@@ -1341,7 +1345,7 @@ ms_status ms_set_shared_expert(ms_ctx* ctx, int32_t layer, int32_t sidx, const v
   std::vector<unsigned char> tmp(s.shared_bytes);
   pack_expert(w_gate, w_up, w_down, s.d, s.F_sh, s.n_chunks_sh, s.elem, tmp.data());
   const uint64_t off = s.off_shared + align_up(s.shared_bytes, kAlign) * (static_cast<uint64_t>(layer) * s.n_sh + sidx);
-  if (ctx->has_last) MS_HIP(hipEventSynchronize(ctx->ev_last));
+  if (ctx->has_last) MS_HIP(hipEventSynchronize(ctx->last_ev));
   MS_HIP(hipMemcpy(ctx->dev(off), tmp.data(), s.shared_bytes, hipMemcpyHostToDevice));
   ctx->layers[layer].shared_set[sidx] = true;
   return MS_OK;
@@ -1352,7 +1356,7 @@ ms_status ms_sync(ms_ctx* ctx) {
   MS_HIP(hipStreamSynchronize(ctx->copy));
   MS_HIP(hipStreamSynchronize(ctx->side));
   MS_HIP(hipStreamSynchronize(ctx->side2));
-  if (ctx->has_last) MS_HIP(hipEventSynchronize(ctx->ev_last));
+  if (ctx->has_last) MS_HIP(hipEventSynchronize(ctx->last_ev));
   return MS_OK;
 }
 
@@ -1514,6 +1518,7 @@ ms_status ms_predict(ms_ctx* ctx, int32_t layer, const void* h_dev, int32_t T, v
   tl_end(ctx, ti, sm);
   MS_HIP(hipEventRecord(ctx->ev_last, sm));
   ctx->has_last = true;
+  ctx->last_ev = ctx->ev_last;
   ctx->last_stream = sm;
   MS_HIP(hipEventSynchronize(ctx->ev_last));
   std::memcpy(order_out, const_cast<const int32_t*>(ctx->h_order), sizeof(int32_t) * s.E);
@@ -1965,8 +1970,8 @@ ms_status ms_forward(ms_ctx* ctx, int32_t layer, const void* h_dev, int32_t T, f
   }
   MS_HIP(hipEventRecord(L.last_fwd, sm));
   L.has_last_fwd = true;
-  MS_HIP(hipEventRecord(ctx->ev_last, sm));
   ctx->has_last = true;
+  ctx->last_ev = L.last_fwd;
   ctx->last_stream = sm;
 
   // 7. speculative prefetch of the next layer, predicted order (Sec. 3.2)
