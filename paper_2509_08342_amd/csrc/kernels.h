@@ -196,6 +196,8 @@ struct MmaArgs {
   int32_t ncb;                 // down: column blocks (ceil(d / kMmaCols))
   int32_t gu_split;            // gate/up: work-groups per chunk and row tile (1 or 4; 1 for b-bit chunks)
   int32_t bits;                // 0: bf16 chunks; 2 or 4: b-bit chunks (q_chunk_bytes layout)
+  int32_t ksplit;              // down, b-bit: chunk ranges per (row tile, column block), each summed
+                               // into its own partial plane [row][ksplit][d]; 1 for bf16
   MmaTask tasks[kMaxMmaTasks];
 };
 hipError_t launch_mma_gateup(const MmaArgs& a, hipStream_t s);

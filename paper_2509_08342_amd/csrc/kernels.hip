@@ -2331,7 +2331,10 @@ __global__ __launch_bounds__(256) void mma_down_q_kernel(MmaArgs a) {
   const int wg = xcd_local(blockIdx.x, gridDim.x);
   const MmaTask tk = a.tasks[find_task(a.tasks, a.n_tasks, wg)];
   const int local = wg - tk.wg_begin;
-  const int mt = local / a.ncb, cb = local % a.ncb;
+  // work-group = (row tile, column block, chunk range): ranges of
+  // ceil(n_chunks / ksplit) chunks, range ks summed into plane ks
+  const int ks = local % a.ksplit;
+  const int mt = (local / a.ksplit) / a.ncb, cb = (local / a.ksplit) % a.ncb;
   const TileRows tr = tile_rows(a, tk, mt);
   if (tr.n <= 0) return;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -2364,9 +2367,10 @@ __global__ __launch_bounds__(256) void mma_down_q_kernel(MmaArgs a) {
 #pragma unroll
     for (int ks = 0; ks < 2; ++ks) an[ks] = ld16(arow + cc * kChunkUnits + 32 * ks + kq);
   };
-  const int nc = tk.n_chunks;
-  load_chunk(0);
-  for (int cc = 0; cc < nc; ++cc) {
+  const int per = (tk.n_chunks + a.ksplit - 1) / a.ksplit;
+  const int c_lo = min(ks * per, tk.n_chunks), nc = min(tk.n_chunks, c_lo + per);
+  load_chunk(min(c_lo, tk.n_chunks - 1));  // an empty range loads (in bounds) and computes nothing
+  for (int cc = c_lo; cc < nc; ++cc) {
 #pragma unroll
     for (int nf = 0; nf < NF; ++nf) {
       wc[nf][0] = wn[nf][0];
@@ -2404,7 +2408,7 @@ __global__ __launch_bounds__(256) void mma_down_q_kernel(MmaArgs a) {
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         const int row = 16 * wave + 4 * (lane >> 4) + r;
-        if (row < tr.n) a.part[static_cast<size_t>(tr.p0 + row) * d + col] = acc[nf][r];
+        if (row < tr.n) a.part[(static_cast<size_t>(tr.p0 + row) * a.ksplit + ks) * d + col] = acc[nf][r];
       }
     }
   }
@@ -2435,6 +2439,7 @@ hipError_t launch_mma_gateup(const MmaArgs& a, hipStream_t s) {
 
 hipError_t launch_mma_down(const MmaArgs& a, hipStream_t s) {
   if (a.n_wg <= 0 || a.n_tasks <= 0) return hipSuccess;
+  if (a.ksplit < 1 || (a.bits == 0 && a.ksplit != 1)) return hipErrorInvalidValue;
   if (a.bits != 0) {
     if (!q_supported(a.d)) return hipErrorInvalidValue;
     if (a.bits == 2)

@@ -60,6 +60,7 @@ struct Shape {
   uint64_t off_part, off_part_sh, off_red, off_act, off_act_sh, off_score, off_order, off_buffer, fixed_bytes;
   uint64_t off_router_t, off_lrank, off_blk, off_psc;
   int nblk_cap;  // token blocks of the many-token routing
+  int down_splits;  // prefill down projection of b-bit chunks: chunk ranges (partial planes) per slot
   uint64_t router_stride, bias_stride, part_bytes, part_sh_bytes;
   int64_t sh_plane;
 };
@@ -124,6 +125,10 @@ ms_status derive_shape(const ms_model_desc* d, Shape* s, std::string* err) {
   s->chunk_bytes = s->bits ? msk::q_chunk_bytes(s->d, s->bits) : 3ull * kUnits * s->d * s->elem;
   s->n_chunks = (s->F + kUnits - 1) / kUnits;
   s->n_chunks_sh = (s->F_sh + kUnits - 1) / kUnits;
+  // b-bit prefill down projection: a work-group per (64 rows, 256 columns)
+  // loops over the expert's chunks; ranges of >= 16 chunks (at most 8)
+  // spread a launch for one expert over more work-groups
+  s->down_splits = s->bits ? std::max(1, std::min(8, s->n_chunks / 16)) : 1;
   s->expert_bytes = s->chunk_bytes * s->n_chunks;
   s->shared_bytes = s->chunk_bytes * s->n_chunks_sh;
   const uint64_t group_bytes = std::min(kGroupMaxBytes, std::max(kGroupMinBytes, s->expert_bytes / 16));
@@ -887,6 +892,7 @@ ms_status prefill_experts(ms_ctx* ctx, int layer, const void* h_dev, int T, cons
   ma.rows_shared = s.max_T;
   ma.ncb = (s.d + msk::kMmaCols - 1) / msk::kMmaCols;
   ma.bits = s.bits;
+  ma.ksplit = s.down_splits;
   auto m_tiles = [&](int e) {
     const int n = e >= 0 ? offs[e + 1] - offs[e] : T;
     return (n + msk::kMmaRows - 1) / msk::kMmaRows;
@@ -906,7 +912,7 @@ ms_status prefill_experts(ms_ctx* ctx, int layer, const void* h_dev, int T, cons
       for (size_t i = i0; i < i1; ++i) {
         ma.tasks[i - i0] = tasks[i];
         ma.tasks[i - i0].wg_begin = wg;
-        wg += tasks[i].m_tiles * (down ? ma.ncb : tasks[i].n_chunks * ma.gu_split);
+        wg += tasks[i].m_tiles * (down ? ma.ncb * ma.ksplit : tasks[i].n_chunks * ma.gu_split);
         bytes += (down ? dn_bytes : gu_bytes) * tasks[i].n_chunks;
       }
       ma.n_wg = wg;
@@ -1912,7 +1918,7 @@ ms_status ms_forward(ms_ctx* ctx, int32_t layer, const void* h_dev, int32_t T, f
   ca.sh_plane = s.sh_plane;
   ca.rows_routed = rows_routed;
   ca.rows_shared = s.max_T;
-  ca.n_planes = prefill ? 1 : s.n_chunks * s.subs;
+  ca.n_planes = prefill ? s.down_splits : s.n_chunks * s.subs;
   ca.n_planes_sh = prefill ? 1 : s.n_chunks_sh * s.subs;
   ca.red = reinterpret_cast<float*>(ctx->dev(s.off_red));
   ca.pg = msk::combine_groups(T, s.K, s.n_sh, s.d, ca.n_planes);
