@@ -322,6 +322,81 @@ __global__ void embed_kernel(const int32_t* __restrict__ ids, const uint16_t* __
 
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
+// Prompts (T >= kDenseMmaTokens, n_in a multiple of 32): the same product on
+// the matrix cores, v_mfma_f32_16x16x32_bf16 (lane l holds A[row l % 16][8 k
+// from 8 (l / 16)], B[8 k from 8 (l / 16)][column l % 16] and C[rows
+// 4 (l / 16) + r][column l % 16]).  A work-group takes 64 tokens x 64
+// outputs, wave w the outputs 16 w .. 16 w + 15 of all four 16-token blocks.
+// x [T][n_in] and W [n_out][n_in] are both contiguous along k, so each
+// fragment is one 16-byte load; loads run kDenseKb k steps of 32 ahead.
+// Tokens past T and outputs past n_out are clamped on load, never stored.
+constexpr int kDenseMmaTokens = 16;
+constexpr int kDenseKb = 2;
+
+typedef __bf16 dbf16x8_t __attribute__((ext_vector_type(8)));
+typedef float df32x4_t __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ df32x4_t dmfma(uint4 a, uint4 b, df32x4_t c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(dbf16x8_t, a), __builtin_bit_cast(dbf16x8_t, b),
+                                                 c, 0, 0, 0);
+}
+
+__global__ __launch_bounds__(256) void dense_mma_kernel(const uint16_t* __restrict__ x,
+                                                        const uint16_t* __restrict__ w,
+                                                        const float* __restrict__ add, float* __restrict__ y, int T,
+                                                        int n_in, int n_out) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int t0 = blockIdx.x * 64, o0 = blockIdx.y * 64 + 16 * wave;
+  const int n = lane & 15, kq = 8 * (lane >> 4);
+  const uint16_t* wrow = w + static_cast<size_t>(min(o0 + n, n_out - 1)) * n_in + kq;
+  const uint16_t* xrow[4];
+#pragma unroll
+  for (int rb = 0; rb < 4; ++rb) xrow[rb] = x + static_cast<size_t>(min(t0 + 16 * rb + n, T - 1)) * n_in + kq;
+  const int ksteps = n_in / 32;
+  df32x4_t acc[4];
+#pragma unroll
+  for (int rb = 0; rb < 4; ++rb) acc[rb] = df32x4_t{0.f, 0.f, 0.f, 0.f};
+  uint4 bn[kDenseKb], an[kDenseKb][4], bc[kDenseKb], ac[kDenseKb][4];
+  auto load = [&](int s0) {
+#pragma unroll
+    for (int u = 0; u < kDenseKb; ++u) {
+      const int k = min(s0 + u, ksteps - 1) * 32;  // clamped past the last step; used only in range
+      bn[u] = *reinterpret_cast<const uint4*>(wrow + k);
+#pragma unroll
+      for (int rb = 0; rb < 4; ++rb) an[u][rb] = *reinterpret_cast<const uint4*>(xrow[rb] + k);
+    }
+  };
+  load(0);
+  for (int s0 = 0; s0 < ksteps; s0 += kDenseKb) {
+#pragma unroll
+    for (int u = 0; u < kDenseKb; ++u) {
+      bc[u] = bn[u];
+#pragma unroll
+      for (int rb = 0; rb < 4; ++rb) ac[u][rb] = an[u][rb];
+    }
+    load(s0 + kDenseKb);
+#pragma unroll
+    for (int u = 0; u < kDenseKb; ++u)
+      if (s0 + u < ksteps) {
+#pragma unroll
+        for (int rb = 0; rb < 4; ++rb) acc[rb] = dmfma(ac[u][rb], bc[u], acc[rb]);
+      }
+  }
+  const int o = o0 + n;
+  if (o < n_out) {
+#pragma unroll
+    for (int rb = 0; rb < 4; ++rb)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int t = t0 + 16 * rb + 4 * (lane >> 4) + r;
+        if (t < T) {
+          const size_t i = static_cast<size_t>(t) * n_out + o;
+          y[i] = acc[rb][r] + (add ? add[i] : 0.0f);
+        }
+      }
+  }
+}
+
 ms_status launched() { return hipGetLastError() == hipSuccess ? MS_OK : MS_E_HIP; }
 
 }  // namespace
@@ -338,6 +413,11 @@ ms_status ms_dense(const void* x, const void* w, int32_t T, int32_t n_in, int32_
   const dim3 grid((n_out + kDenseRows - 1) / kDenseRows);
   const auto* xp = static_cast<const uint16_t*>(x);
   const auto* wp = static_cast<const uint16_t*>(w);
+  if (T >= kDenseMmaTokens && n_in % 32 == 0) {
+    hipLaunchKernelGGL(dense_mma_kernel, dim3((T + 63) / 64, (n_out + 63) / 64), dim3(256), msk::kGuardLds, s, xp, wp,
+                       add, y, T, n_in, n_out);
+    return launched();
+  }
   if (n_in <= 4096)
     hipLaunchKernelGGL((dense_kernel<4, 8>), grid, dim3(kDenseThreads), 4 * n_in * 2, s, xp, wp, add, y, T, n_in,
                        n_out);

@@ -23,7 +23,11 @@ def _bf16(a):
     return to_device(raw, "bf16"), f.astype(np.float64)
 
 
-@pytest.mark.parametrize("T,n_in,n_out", [(1, 256, 13), (3, 4096, 100), (9, 512, 64), (2, 8192, 24)])
+# T >= 16 with n_in a multiple of 32 takes the matrix-core kernel (ragged
+# 64-token and 64-output tiles); the rest the fma-chain kernel
+@pytest.mark.parametrize("T,n_in,n_out", [(1, 256, 13), (3, 4096, 100), (9, 512, 64), (2, 8192, 24),
+                                          (16, 256, 13), (17, 1024, 70), (64, 4096, 100), (130, 512, 200),
+                                          (40, 8192, 24), (20, 264, 33)])
 def test_dense_matches_numpy(T, n_in, n_out):
     from paper_2509_08342_amd import moesplit as ms
     rng = np.random.default_rng(T + n_in)
