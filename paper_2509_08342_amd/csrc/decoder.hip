@@ -16,6 +16,7 @@ namespace {
 constexpr int kDenseThreads = 256;
 constexpr int kDenseRows = 8;        // output rows per work-group (two per wave)
 constexpr int kAttThreads = 256;
+constexpr int kAttWideThreads = 1024;  // single-token steps
 constexpr int kAttMaxScores = 16000;  // floats of queries and scores a work-group keeps in LDS (< 64 KiB)
 
 __device__ __forceinline__ void bf16x8_to_f32(uint4 v, float (&o)[8]) {
@@ -159,7 +160,9 @@ __global__ void rope_kv_kernel(const float* __restrict__ qkv, int Hq, int Hkv, i
 // ------------------------------------------------------------- attention
 //
 // Block (t, g): the G = Hq / Hkv query heads of key/value group g for token
-// t, over positions 0 .. pos0 + t.  Scores in LDS ([G][n]); softmax with the
+// t, over positions 0 .. pos0 + t, in BLK threads (1024 for a single-token
+// step, whose T x Hkv blocks alone would leave most of the GPU idle; 256
+// otherwise).  Scores in LDS ([G][n]); softmax with the
 // row maximum subtracted; then p . V over the positions.
 template <int BLK>
 __device__ __forceinline__ float block_reduce(float v, bool is_max, float* red) {
@@ -177,25 +180,25 @@ __device__ __forceinline__ float block_reduce(float v, bool is_max, float* red) 
   return r;
 }
 
-template <int G>
-__global__ __launch_bounds__(kAttThreads) void attention_kernel(const uint16_t* __restrict__ q,
+template <int G, int BLK>
+__global__ __launch_bounds__(BLK) void attention_kernel(const uint16_t* __restrict__ q,
                                                                 const uint16_t* __restrict__ kc,
                                                                 const uint16_t* __restrict__ vc, int Hq, int Hkv,
                                                                 int D, int pos0, int max_ctx,
                                                                 uint16_t* __restrict__ out) {
   extern __shared__ __align__(16) float att_smem[];  // qf [G][D], scores [G][n], wave sums [4][G][D]
-  __shared__ float red[kAttThreads / 64];
+  __shared__ float red[BLK / 64];
   const int t = blockIdx.x, g = blockIdx.y, tid = threadIdx.x;
   const int n = pos0 + t + 1;
   float* qf = att_smem;
   float* sc = att_smem + G * D;
-  for (int i = tid; i < G * D; i += kAttThreads)
+  for (int i = tid; i < G * D; i += BLK)
     qf[i] = bf16_to_f32(q[(static_cast<size_t>(t) * Hq + g * G) * D + i]);
   __syncthreads();
   const float scale = 1.0f / sqrtf(static_cast<float>(D));
   const uint16_t* K = kc + static_cast<size_t>(g) * max_ctx * D;
   const uint16_t* V = vc + static_cast<size_t>(g) * max_ctx * D;
-  for (int p = tid; p < n; p += kAttThreads) {
+  for (int p = tid; p < n; p += BLK) {
     float s[G];
 #pragma unroll
     for (int h = 0; h < G; ++h) s[h] = 0.0f;
@@ -213,24 +216,24 @@ __global__ __launch_bounds__(kAttThreads) void attention_kernel(const uint16_t* 
   __syncthreads();
   for (int h = 0; h < G; ++h) {
     float m = -INFINITY;
-    for (int p = tid; p < n; p += kAttThreads) m = fmaxf(m, sc[h * n + p]);
-    m = block_reduce<kAttThreads>(m, true, red);
+    for (int p = tid; p < n; p += BLK) m = fmaxf(m, sc[h * n + p]);
+    m = block_reduce<BLK>(m, true, red);
     float sum = 0.0f;
-    for (int p = tid; p < n; p += kAttThreads) {
+    for (int p = tid; p < n; p += BLK) {
       const float e = expf(sc[h * n + p] - m);
       sc[h * n + p] = e;
       sum += e;
     }
-    sum = block_reduce<kAttThreads>(sum, false, red);
+    sum = block_reduce<BLK>(sum, false, red);
     __syncthreads();
-    for (int p = tid; p < n; p += kAttThreads) sc[h * n + p] /= sum;
+    for (int p = tid; p < n; p += BLK) sc[h * n + p] /= sum;
   }
   __syncthreads();
   // p . V: thread (position lane pl, column group cg) sums 8 columns of every
   // head over positions pl, pl + PL, ... (one 16-byte V load serves all G
   // heads); the position lanes of a wave are combined with shuffles, the
   // waves' sums through LDS (after the scores, which stay in use until then)
-  const int CG = D / 8, PL = kAttThreads / CG;
+  const int CG = D / 8, PL = BLK / CG;
   const int cg = tid % CG, pl = tid / CG;
   float acc[G][8];
 #pragma unroll
@@ -264,9 +267,9 @@ __global__ __launch_bounds__(kAttThreads) void attention_kernel(const uint16_t* 
       for (int e = 0; e < 8; ++e) wsum[(wave * G + h) * D + 8 * cg + e] = acc[h][e];
   }
   __syncthreads();
-  for (int o = tid; o < G * D; o += kAttThreads) {
+  for (int o = tid; o < G * D; o += BLK) {
     float v = 0.0f;
-    for (int w = 0; w < kAttThreads / 64; ++w) v += wsum[w * G * D + o];
+    for (int w = 0; w < BLK / 64; ++w) v += wsum[w * G * D + o];
     const int h = o / D, col = o - h * D;
     out[(static_cast<size_t>(t) * Hq + g * G + h) * D + col] = f32_to_bf16(v);
   }
@@ -449,20 +452,33 @@ ms_status ms_attention(const void* q, const void* k_cache, const void* v_cache, 
   const int G = Hq / Hkv;
   if (D < 8 || D > 512 || (D & (D - 1)) != 0 || G > 8 || static_cast<int64_t>(G) * (5 * D + pos0 + T) > kAttMaxScores)
     return MS_E_UNSUPPORTED;
-  const size_t lds = sizeof(float) * static_cast<size_t>(G) * (5 * D + pos0 + T);
+  // LDS: queries [G][D], scores [G][n], per-wave p.V sums [waves][G][D]
+  const bool wide = T == 1 && static_cast<int64_t>(G) * ((1 + kAttWideThreads / 64) * D + pos0 + T) <= kAttMaxScores;
+  const int waves = (wide ? kAttWideThreads : kAttThreads) / 64;
+  const size_t lds = sizeof(float) * static_cast<size_t>(G) * ((1 + waves) * D + pos0 + T);
   const hipStream_t s = static_cast<hipStream_t>(stream);
   const auto* qp = static_cast<const uint16_t*>(q);
   const auto* kp = static_cast<const uint16_t*>(k_cache);
   const auto* vp = static_cast<const uint16_t*>(v_cache);
   auto* op = static_cast<uint16_t*>(out);
   const dim3 grid(T, Hkv);
+#define MSK_ATT_CASE(G_)                                                                                   \
+  case G_:                                                                                                 \
+    if (wide)                                                                                              \
+      hipLaunchKernelGGL((attention_kernel<G_, kAttWideThreads>), grid, dim3(kAttWideThreads), lds, s, qp, kp, vp, \
+                         Hq, Hkv, D, pos0, max_ctx, op);                                                   \
+    else                                                                                                   \
+      hipLaunchKernelGGL((attention_kernel<G_, kAttThreads>), grid, dim3(kAttThreads), lds, s, qp, kp, vp, Hq, \
+                         Hkv, D, pos0, max_ctx, op);                                                       \
+    break;
   switch (G) {
-    case 1: hipLaunchKernelGGL(attention_kernel<1>, grid, dim3(kAttThreads), lds, s, qp, kp, vp, Hq, Hkv, D, pos0, max_ctx, op); break;
-    case 2: hipLaunchKernelGGL(attention_kernel<2>, grid, dim3(kAttThreads), lds, s, qp, kp, vp, Hq, Hkv, D, pos0, max_ctx, op); break;
-    case 4: hipLaunchKernelGGL(attention_kernel<4>, grid, dim3(kAttThreads), lds, s, qp, kp, vp, Hq, Hkv, D, pos0, max_ctx, op); break;
-    case 8: hipLaunchKernelGGL(attention_kernel<8>, grid, dim3(kAttThreads), lds, s, qp, kp, vp, Hq, Hkv, D, pos0, max_ctx, op); break;
+    MSK_ATT_CASE(1)
+    MSK_ATT_CASE(2)
+    MSK_ATT_CASE(4)
+    MSK_ATT_CASE(8)
     default: return MS_E_UNSUPPORTED;
   }
+#undef MSK_ATT_CASE
   return launched();
 }
 
