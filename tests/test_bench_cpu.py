@@ -114,3 +114,13 @@ def test_mfma_roofline_of_prefill_launches():
     assert m["attainable_frac"] == pytest.approx(m["achieved"] / m["attainable"], abs=1e-4)
     # decode forwards (no down launches) report none
     assert bench.mfma_roofline(bench.analyse(tl[:2], 1, 1.0), shape, 1, 1) is None
+
+
+def test_platform_info_never_fails():
+    """The platform record is reporting only: without a GPU (this test runs
+    on the CPU) it returns the host CPU fields and an error note instead of
+    raising."""
+    info = bench.platform_info()
+    assert info["cpu"]["logical_cpus"] >= 1
+    assert info["cpu"]["usable_cpus"] is None or info["cpu"]["usable_cpus"] >= 1
+    assert "gpu" in info or "error" in info
