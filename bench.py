@@ -452,10 +452,11 @@ def cpu_baseline(rig, hf_list, budget_s):
                 break
     dt = time.perf_counter() - t0
     scale = T / n_rows
+    where = ("every row, one thread" if len(blocks) == 1 and n_rows == T else
+             "%d rows in %d threads of up to %d rows, scaled to the batch" % (n_rows, len(blocks), per))
     return dict(value=round(dt / n * scale * 1e6, 1), unit="us/layer", cores=len(blocks), kind="oracle",
-                sample="%d batches of %d token(s) of the %s layer (router on all rows, %d experts per row on "
-                "%d rows in %d thread(s) of %d rows, fp64, scaled to the batch)"
-                % (n, T, s.name, s.top_k, n_rows, len(blocks), per))
+                sample="%d batches of %d token(s) of the %s layer (router on all rows, %d experts per row on %s; "
+                "experts in fp64)" % (n, T, s.name, s.top_k, where))
 
 
 def log(msg):
