@@ -1,20 +1,26 @@
 """Benchmark of the split-expert MoE layer on one MI355X.
 
-Workload: the Mixtral-8x7B-shaped MoE layer (d=4096, F=14336, E=8, top-2,
-bf16 weights, fp32 accumulation), decode batch 1, split ratio r=0.5 with the
-top segments of experts 0-3 cached in the VRAM pool and every other segment
-in pinned host RAM.  One step = one decode token through the whole hot path:
+Default workload: the Mixtral-8x7B-shaped MoE layer (d=4096, F=14336, E=8,
+top-2, bf16 weights, fp32 accumulation), decode batch 1, split ratio r=0.5
+with the top segments of experts 0-3 cached in the VRAM pool, a staging
+buffer of K=2 whole-expert slots (the paper's buffer), every other segment in
+pinned host RAM.  One step = one decode token through the whole hot path:
 routing + next-layer prediction, grouping, residency resolution and miss
-transfers, resident-segment FFN, streamed-segment FFN, combine, and the
-speculative prefetch for the next token (a one-layer model predicts its own
-next pass).  Inputs are a seeded correlated sequence of N(0,1) tokens, all
-resident in HBM before timing starts.
+transfers, resident-segment FFN, streamed-segment FFN, combine and the
+prefetch pass.  Each token meets the layer as a layer of a deep stack does:
+the staging buffer holds none of the layer's segments when its routing
+arrives (the other layers' misses cycle the buffer between two visits), so
+the step time is the layer's steady state and not a matter of which tokens
+fall into the timed window.  Tokens are independent N(0,1) rows, resident
+in HBM before timing starts.
 
 Prints one JSON line: value = MoE-layer latency in us per layer (lower is
-better); plus the dominant kernel's roofline from HIP events over the timed
-region, H2D bandwidth and overlap figures from the same events, an
-all-resident (r=1) variant that isolates the HBM-bound expert read, and the
-CPU oracle timed on a bounded sample.
+better); plus the expert FFN kernel's roofline from HIP events over the
+timed region, H2D bandwidth and overlap figures from the same events, the
+hit path (every missing segment already staged), an all-resident (r=1)
+variant that isolates the HBM-bound expert read, the Mixtral-shaped
+32-layer stack at a 12 GiB budget (where cross-layer prefetch moves bytes),
+and the CPU oracle timed on a bounded sample.
 """
 from __future__ import annotations
 
@@ -37,10 +43,11 @@ FFN_KERNELS = ("ffn_chunk_kernel", "ffn_q_kernel", "mma_gateup", "mma_down")
 
 
 def kernel_sources_sha():
-    """Hash of the kernel sources: PMC traffic figures hold only for them."""
+    """Hash of the kernel and runtime sources (the runtime picks grids, task
+    lists and splits): PMC traffic figures hold only for them."""
     import hashlib
     h = hashlib.sha256()
-    for f in ("kernels.hip", "kernels.h"):
+    for f in ("kernels.hip", "kernels.h", "runtime.hip"):
         with open(os.path.join(ROOT, "paper_2509_08342_amd", "csrc", f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()
@@ -51,8 +58,9 @@ def pmc_profile_path(workload):
 
 
 def traffic_from_profile(workload):
-    """HBM bytes per FFN launch from the committed PMC summary of this
-    workload, or None when there is none or the kernels changed since."""
+    """(HBM bytes per FFN launch, algorithmic weight bytes per FFN launch of
+    the same profiled run) from the committed PMC summary of this workload,
+    or None when there is none or the sources changed since."""
     path = pmc_profile_path(workload)
     if not os.path.exists(path):
         return None
@@ -65,12 +73,14 @@ def traffic_from_profile(workload):
     if vals.get("kernels_sha256") != kernel_sources_sha():
         return None
     try:
-        return int(vals["ffn_traffic_bytes_per_launch"])
+        return int(vals["ffn_traffic_bytes_per_launch"]), int(vals["ffn_algorithmic_bytes_per_launch"])
     except (KeyError, ValueError):
         return None
 
 # name -> (shape, tokens per step, split ratio, per-layer budget in top
-# segments (None: whole budget of the reference config), which tops to cache)
+# segments (None: whole budget of the reference config), which tops to cache,
+# staging-buffer slots: decode K whole experts, the paper's buffer; prefill
+# the library's default 2K, so one expert's copies overlap another's compute)
 def _workloads():
     import dataclasses
     import synth
@@ -79,21 +89,21 @@ def _workloads():
     return {
         # Mixtral-8x7B-shaped layer, decode batch 1, r = .5, tops of experts 0-3
         "mixtral-decode": dict(shape=synth.MIXTRAL, T=1, r=0.5, budget=lambda tb: 4 * tb,
-                               tops=lambda rig: [0, 1, 2, 3]),
+                               tops=lambda rig: [0, 1, 2, 3], slots=2),
         # the same layer with 2-bit expert codes (the paper's HQQ Mixtral setting)
         "mixtral-q2-decode": dict(shape=synth.MIXTRAL_Q2, T=1, r=0.5, budget=lambda tb: 4 * tb,
-                                  tops=lambda rig: [0, 1, 2, 3]),
+                                  tops=lambda rig: [0, 1, 2, 3], slots=2),
         # DeepSeek-V2-Lite-shaped layer: 4 GiB over 26 layers at r = .5 (19 tops)
         "deepseek-decode": dict(shape=ds1, T=1, r=0.5, budget=lambda tb: (4 * GIB) // 26,
-                                tops=lambda rig: list(range(19))),
+                                tops=lambda rig: list(range(19)), slots=6),
         "deepseek-prefill": dict(shape=ds1, T=512, r=0.5, budget=lambda tb: (4 * GIB) // 26,
-                                 tops=lambda rig: list(range(19))),
+                                 tops=lambda rig: list(range(19)), slots=0),
         # Qwen3-30B-A3B-shaped layer: 8 GiB over 48 layers at r = .5 (37 tops),
         # the Zipf-hot experts cached
         "qwen-decode16": dict(shape=qw1, T=16, r=0.5, budget=lambda tb: (8 * GIB) // 48,
-                              tops=lambda rig: list(np.argsort(-rig.biases[0], kind="stable")[:37])),
+                              tops=lambda rig: list(np.argsort(-rig.biases[0], kind="stable")[:37]), slots=0),
         "qwen-prefill": dict(shape=qw1, T=2048, r=0.5, budget=lambda tb: (8 * GIB) // 48,
-                             tops=lambda rig: list(np.argsort(-rig.biases[0], kind="stable")[:37])),
+                             tops=lambda rig: list(np.argsort(-rig.biases[0], kind="stable")[:37]), slots=0),
     }
 
 # stacked workloads: shape, total budget V_e, uniform r (or "mixed": r by layer
@@ -128,7 +138,7 @@ def _decoders():
                                 prompt=512, n_sets=4, t_moe_us=208.0),
         "mixtral-q2-decoder": dict(shape=synth.MIXTRAL_Q2_STACK, attn=synth.MIXTRAL_ATTN, budget=2 * GIB, r=0.5,
                                    prompt=512, n_sets=4, t_moe_us=70.0),
-        # the budget of the paper's Mixtral TPOT comparison (Sec. 5.2): 160 of
+        # the budget of the paper's Mixtral TPOT comparison (Sec. 4.2): 160 of
         # the 256 experts; r = 5/8 caches every expert's top at that budget
         "mixtral-q2-decoder-160": dict(shape=synth.MIXTRAL_Q2_STACK, attn=synth.MIXTRAL_ATTN,
                                        budget=160 * synth.MIXTRAL_Q2_STACK.expert_bytes, r=0.625,
@@ -172,7 +182,7 @@ def _intersect(u, v):
     return tot
 
 
-def analyse(tl, steps, ms_per_step):
+def analyse(tl, steps, ms_per_step, router_starts=True):
     by = {}
     for r in tl:
         by.setdefault(r["kind"], []).append(r)
@@ -182,7 +192,8 @@ def analyse(tl, steps, ms_per_step):
         dur = sum(r["t1_ms"] - r["t0_ms"] for r in rs)
         kern[k] = dict(launches=len(rs), total_ms=dur, bytes=sum(r["bytes"] for r in rs))
     # per-step latency: from a step's routing launch to its last record
-    starts = sorted(r["t0_ms"] for r in by.get("router", []))
+    # (single-layer workloads: one routing launch per step)
+    starts = sorted(r["t0_ms"] for r in by.get("router", [])) if router_starts else []
     step_ms = []
     for i, t0 in enumerate(starts):
         t1 = starts[i + 1] if i + 1 < len(starts) else float("inf")
@@ -324,14 +335,27 @@ def platform_info():
     models = [l.split(":", 1)[1].strip() for l in cpuinfo.splitlines() if l.startswith("model name")]
     info["cpu"] = {"model": models[0] if models else None, "logical_cpus": os.cpu_count(),
                    "usable_cpus": len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity") else None}
+    try:
+        r = subprocess.run(["lscpu"], capture_output=True, text=True, timeout=30)
+        want = {"Model name": "lscpu_model", "Socket(s)": "sockets", "Core(s) per socket": "cores_per_socket",
+                "Thread(s) per core": "threads_per_core", "CPU(s)": "cpus", "CPU max MHz": "max_mhz"}
+        for line in r.stdout.splitlines():
+            k, _, v = line.partition(":")
+            if k.strip() in want and v.strip():
+                info["cpu"][want[k.strip()]] = v.strip()
+    except (OSError, subprocess.SubprocessError):
+        pass
     return info
 
 
 # ------------------------------------------------------------------ timing
 
-def run_steps(rig, hs, steps, warmup, flags, timeline=True, cold=False, T=1, before_timed=None):
+def run_steps(rig, hs, steps, warmup, flags, timeline=True, cold=False, T=1, before_timed=None, per_step=None):
     """Time `steps` batches of T tokens through layer 0.  cold=True drops the
-    staging buffer before every batch, so each pays all of its misses."""
+    staging buffer before every batch, so each pays all of its misses, as a
+    layer of a deep stack does.  per_step: a list that receives each timed
+    step's span in ms (between HIP events recorded after consecutive
+    forwards on the compute stream)."""
     import torch
     from paper_2509_08342_amd import moesplit as ms
     stream = torch.cuda.current_stream()
@@ -352,18 +376,60 @@ def run_steps(rig, hs, steps, warmup, flags, timeline=True, cold=False, T=1, bef
         # room for every record of the timed steps (events are created up front)
         cap = min(1 << 16, max(1024, steps * (4 * rig.shape.n_experts + 64)))
         ms.ms_timeline_begin(rig.ctx, stream, cap)
+    evs = []
     torch.cuda.synchronize()
     t0 = time.perf_counter()
+    if per_step is not None:
+        evs.append(torch.cuda.Event(enable_timing=True))
+        evs[-1].record(stream)
     for i in range(steps):
         if cold:
             ms.ms_drop_buffer(rig.ctx)
         rig.forward(0, hs[(warmup + i) % len(hs)], T, y, idx, w, flags, stream)
+        if per_step is not None:
+            evs.append(torch.cuda.Event(enable_timing=True))
+            evs[-1].record(stream)
     ms.ms_sync(rig.ctx)
     torch.cuda.synchronize()
     t1 = time.perf_counter()
+    if per_step is not None:
+        per_step.extend(a.elapsed_time(b) for a, b in zip(evs, evs[1:]))
     tl = ms.ms_timeline_end(rig.ctx) if timeline else []
     st = ms.ms_stats(rig.ctx, 0)
     return (t1 - t0) * 1e3 / steps, tl, st
+
+
+def run_hit_path(rig, hs, steps, T=1):
+    """The layer when every selected expert's missing segment is already in
+    the staging buffer (a prediction that was right and a prefetch that had
+    time to land): per step, the buffer is emptied and the token run once
+    untimed to stage its misses, then run again between two HIP events on
+    the compute stream.  Returns the per-step times in ms and the stats of
+    the timed forwards."""
+    import torch
+    from paper_2509_08342_amd import moesplit as ms
+    stream = torch.cuda.current_stream()
+    y, idx, w = rig.outputs(T)
+    per = []
+    hits = 0
+    for i in range(steps):
+        ms.ms_drop_buffer(rig.ctx)
+        rig.forward(0, hs[i % len(hs)], T, y, idx, w, 0, stream)
+        ms.ms_sync(rig.ctx)
+        torch.cuda.synchronize()
+        before = ms.ms_stats(rig.ctx, 0)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        rig.forward(0, hs[i % len(hs)], T, y, idx, w, 0, stream)
+        e1.record(stream)
+        ms.ms_sync(rig.ctx)
+        torch.cuda.synchronize()
+        after = ms.ms_stats(rig.ctx, 0)
+        if after["bytes_miss"] != before["bytes_miss"]:
+            raise RuntimeError("hit path: a staged forward copied missing segments again")
+        hits += after["buffer_hits"] - before["buffer_hits"]
+        per.append(e0.elapsed_time(e1))
+    return per, hits
 
 
 def h2d_link_peak_gbps():
@@ -488,11 +554,21 @@ def _counter_by_dispatch(d):
     return out
 
 
-def pmc_summary(fetch_dir, write_dir, workload, out, cmd_fetch, cmd_write):
+def pmc_summary(fetch_dir, write_dir, workload, out, cmd_fetch, cmd_write, pass_log=None):
     """FETCH_SIZE and WRITE_SIZE (KiB per dispatch) of the FFN kernels in the
     timed steps of a --pmc-pass run, each scaled by the same counter on the
     calibration copy of CALIB_BYTES (the largest __amd_rocclr_copyBuffer
-    dispatch, issued just before the timed steps)."""
+    dispatch, issued just before the timed steps).  pass_log: the JSON line
+    the --pmc-pass run printed, whose algorithmic FFN bytes of the same
+    dispatches are recorded beside the counted traffic."""
+    alg = None
+    if pass_log:
+        with open(pass_log) as f:
+            for line in f:
+                if line.startswith("{") and "pmc_pass" in line:
+                    rec = json.loads(line)
+                    if rec.get("ffn_launches"):
+                        alg = (rec["ffn_launches"], rec["ffn_algorithmic_bytes"])
     res = {}
     for label, d in (("FETCH_SIZE", fetch_dir), ("WRITE_SIZE", write_dir)):
         by = _counter_by_dispatch(d)
@@ -534,11 +610,17 @@ def pmc_summary(fetch_dir, write_dir, workload, out, cmd_fetch, cmd_write):
             ffn_n += cnt
             ffn_bytes += (fb + wb) * cnt
     per = int(ffn_bytes / max(ffn_n, 1))
-    lines += ["", "Figures bench.py reads (valid while the kernel sources hash the same):", "",
+    lines += ["", "Figures bench.py reads (valid while the kernel and runtime sources hash the same):", "",
               "- `workload`: `%s`" % workload,
               "- `ffn_dispatches`: `%d`" % ffn_n,
-              "- `ffn_traffic_bytes_per_launch`: `%d`" % per,
-              "- `kernels_sha256`: `%s`" % kernel_sources_sha(), ""]
+              "- `ffn_traffic_bytes_per_launch`: `%d`" % per]
+    if alg is not None:
+        if alg[0] != ffn_n:
+            raise SystemExit("the pass log counts %d FFN launches, the counters %d" % (alg[0], ffn_n))
+        ap = int(alg[1] / alg[0])
+        lines += ["- `ffn_algorithmic_bytes_per_launch`: `%d`" % ap,
+                  "- `ffn_traffic_ratio`: `%.4f`" % (per / ap)]
+    lines += ["- `kernels_sha256`: `%s`" % kernel_sources_sha(), ""]
     with open(out, "w") as f:
         f.write("\n".join(lines))
     print("wrote %s: %d FFN dispatches, %.3f MB per launch" % (out, ffn_n, per / 1e6))
@@ -693,33 +775,37 @@ def run_decoder(args):
     print(json.dumps(out), flush=True)
 
 
-def run_stack(args):
-    """A whole stack: warm-up statistics pick each layer's cached tops, an
-    optional prefill pass, then decode steps through every layer with
-    cross-layer prediction and prefetch."""
+def measure_stack(name, steps, warmup, copy_engine="kernel", policy="static", configure=False, zeta=0.01,
+                  instrument_steps=0):
+    """A whole stack: warm-up statistics pick each layer's cached tops (or
+    the configurator's plan), an optional prefill pass, then `steps` timed
+    decode steps through every layer with cross-layer prediction and
+    prefetch.  With instrument_steps > 0 the first that many timed tokens run
+    again with the library's timeline on, which gives the copy / kernel
+    overlap figures.  Returns the result dict."""
     import torch
     from paper_2509_08342_amd import moesplit as ms
-    from stack import Stack, decode_inputs, stack_top_bytes
-    cfg = _stacks()[args.workload]
+    from stack import Stack, decode_inputs
+    cfg = _stacks()[name]
     shape, T, P = cfg["shape"], cfg["T"], cfg["prefill"]
     L = shape.n_layers
     t_setup = time.perf_counter()
     log("generating %s weights (%d distinct sets over %d layers)" % (shape.name, cfg["n_sets"], L))
     st = Stack(shape, seed=0, n_sets=cfg["n_sets"], max_tokens=max(T, P), budget_total=cfg["budget"],
                keep_f32=False)
-    if args.copy_engine == "dma":
+    if copy_engine == "dma":
         ms.ms_set_copy_engine(st.ctx, ms.MS_COPY_DMA)
     r = cfg["r"]
     rs = [(0.25, 0.5, 0.75)[l % 3] for l in range(L)] if r == "mixed" else [r] * L
     slots = st.configure(rs, cfg["budget"])
-    n_warm, n_steps = 16, args.steps
-    xs = decode_inputs(shape, 0, n_warm + args.warmup + n_steps, T)
+    n_warm, n_steps = 16, steps
+    xs = decode_inputs(shape, 0, n_warm + warmup + n_steps, T)
     log("setup %.1f s; %d-step warm-up for the cache contents" % (time.perf_counter() - t_setup, n_warm))
     ms.ms_reset_plan_stats(st.ctx)
     counts = st.warmup_counts([x for x, _ in xs[:n_warm]], T)
     st.load_most_selected(counts)
     plan = None
-    if args.configure:
+    if configure:
         # Algorithm 1 on the warm-up statistics, then its cache update
         E = shape.n_experts
         hs_, ps_, phs_ = [], [], []
@@ -730,22 +816,24 @@ def run_stack(args):
             phs_.append(ph_)
         t_load = shape.expert_bytes / 55e3   # us per whole expert at the kernel copy's 55 GB/s
         plan = ms.ms_plan_solve(L, E, shape.top_k, shape.expert_bytes, 0.0, cfg["t_moe_us"], 0.0, t_load,
-                                np.array(hs_), np.array(ps_), np.array(phs_), cfg["budget"], args.zeta)
+                                np.array(hs_), np.array(ps_), np.array(phs_), cfg["budget"], zeta)
         ms.ms_cache_update(st.ctx, plan["budgets"], plan["theta"].astype(np.float32))
         slots = [int(sum(ms.ms_residency(st.ctx, l, E) > 0)) for l in range(L)]
         log("configurator: %d moves, theta %.3f..%.3f, C %d..%d" % (
             plan["iters"], plan["theta"].min(), plan["theta"].max(), min(slots), max(slots)))
-    if args.policy != "static":
+    if policy != "static":
         ms.ms_set_cache_policy(st.ctx, {"lcp": ms.MS_CACHE_LCP, "lru": ms.MS_CACHE_LRU, "lfu": ms.MS_CACHE_LFU,
-                                        "rnd": ms.MS_CACHE_RND}[args.policy])
+                                        "rnd": ms.MS_CACHE_RND}[policy])
     stream = torch.cuda.current_stream()
+    n_slots = int(st.rig.sizes.buffer_bytes // st.rig.sizes.expert_bytes)
     out = {"metric": "MoE-stack decode µs/layer", "unit": "us/layer", "higher_is_better": False,
            "data": "synthetic", "dtype": "bf16", "n_gpus": 1,
            "config": {"workload": "%s: %s, %d layers, V_e %.0f GiB, r %s, C_i %s, %s decode batch %d, "
-                                  "cache policy %s" % (
-               args.workload, shape.name, L, cfg["budget"] / GIB,
+                                  "staging buffer %d whole-expert slots (K for the running layer's misses, "
+                                  "K for the next layer's prefetch), cache policy %s" % (
+               name, shape.name, L, cfg["budget"] / GIB,
                "from the configurator" if plan is not None else r, sorted(set(int(c) for c in slots)),
-               ("prefill %d then" % P) if P else "", T, args.policy)}}
+               ("prefill %d then" % P) if P else "", T, n_slots, policy)}}
     if plan is not None:
         out["plan"] = {"moves": plan["iters"], "theta": [round(float(t), 4) for t in plan["theta"]],
                        "cache": [int(c) for c in plan["cache"]],
@@ -762,14 +850,14 @@ def run_stack(args):
         out["prefill_ms"] = round((time.perf_counter() - t0) * 1e3, 2)
         out["prefill_tokens_per_s"] = round(P / (time.perf_counter() - t0), 1)
         log("prefill %d tokens: %.1f ms" % (P, out["prefill_ms"]))
-    for x, _ in xs[n_warm:n_warm + args.warmup]:
+    for x, _ in xs[n_warm:n_warm + warmup]:
         st.step(x, T)
     ms.ms_sync(st.ctx)
     torch.cuda.synchronize()
     ms.ms_reset_stats(st.ctx)
     step_ms = []
     t0 = time.perf_counter()
-    for x, _ in xs[n_warm + args.warmup:]:
+    for x, _ in xs[n_warm + warmup:]:
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         e0.record(stream)
         st.step(x, T)
@@ -780,11 +868,11 @@ def run_stack(args):
     wall = time.perf_counter() - t0
     per = [a.elapsed_time(b) for a, b in step_ms]
     stats = st.stats()
-    tot = {k: sum(s[k] for s in stats) for k in stats[0]}
+    tot = {k: sum(s_[k] for s_ in stats) for k in stats[0]}
     out.update({
-        "value": round(wall / n_steps / L * 1e6, 1), "steps": n_steps, "warmup": args.warmup,
+        "value": round(wall / n_steps / L * 1e6, 1), "steps": n_steps, "warmup": warmup,
         "ms_per_step": round(wall / n_steps * 1e3, 3),
-        "step_ms": {q: round(float(np.percentile(per, p)), 3) for q, p in (("p10", 10), ("p50", 50), ("p90", 90))},
+        "step_ms": {q: round(float(np.percentile(per, p_)), 3) for q, p_ in (("p10", 10), ("p50", 50), ("p90", 90))},
         "tokens_per_s": round(T * n_steps / wall, 2),
         "selected": tot["selected"], "alpha_beta_gamma": [tot["alpha"], tot["beta"], tot["gamma"]],
         "hit_rate": round((tot["alpha"] + tot["beta"]) / max(tot["experts_active"], 1), 4),
@@ -792,10 +880,37 @@ def run_stack(args):
         "buffer_hits": tot["buffer_hits"], "predicted_hits_per_layer_step": round(
             tot["predicted_hits"] / max(tot["predictions"], 1), 3),
         "h2d_bytes_per_step": {"miss": tot["bytes_miss"] // n_steps, "prefetch": tot["bytes_prefetch"] // n_steps,
-                               "prefetch_used": tot["bytes_prefetch_used"] // n_steps},
+                               "prefetch_used": tot["bytes_prefetch_used"] // n_steps,
+                               "prefetch_dropped_before_issue": tot["bytes_prefetch_dropped"] // n_steps},
         "h2d_gbps_over_step": round((tot["bytes_miss"] + tot["bytes_prefetch"]) / wall / 1e9, 2),
     })
+    if instrument_steps > 0:
+        n_i = min(instrument_steps, n_steps)
+        ms.ms_timeline_begin(st.ctx, stream, min(1 << 16, n_i * L * 64))
+        torch.cuda.synchronize()
+        ti = time.perf_counter()
+        for x, _ in xs[n_warm + warmup:n_warm + warmup + n_i]:
+            st.step(x, T)
+        ms.ms_sync(st.ctx)
+        torch.cuda.synchronize()
+        wi = time.perf_counter() - ti
+        tl = ms.ms_timeline_end(st.ctx)
+        an = analyse(tl, n_i, wi * 1e3 / n_i, router_starts=False)
+        out["overlap"] = {"steps": n_i, "h2d_hidden_frac": an["hidden_frac"],
+                          "compute_hidden_frac": an["compute_hidden_frac"], "eta": an["overlap_eta"],
+                          "copy_ms_per_step": round(an["copy_ms"] / n_i, 3),
+                          "kernel_ms_per_step": round(an["kernel_ms"] / n_i, 3),
+                          "h2d_gbps_during_copies": None if an["h2d_gbps"] is None else round(an["h2d_gbps"], 2)}
+        out["copy_roofline"] = copy_roofline(tl)
+        out["ffn_roofline"] = ffn_roofline(an)
+    out["setup_s"] = round(time.perf_counter() - t_setup, 1)
     st.close()
+    return out
+
+
+def run_stack(args):
+    out = measure_stack(args.workload, args.steps, args.warmup, args.copy_engine, args.policy, args.configure,
+                        args.zeta, instrument_steps=min(args.steps, 32))
     out["platform"] = platform_info()
     print(json.dumps(out), flush=True)
 
@@ -808,6 +923,7 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-all-resident", action="store_true")
+    ap.add_argument("--no-stack", action="store_true", help="skip the 32-layer stack of the default workload")
     ap.add_argument("--timeline-out", default=None)
     ap.add_argument("--workload", default="mixtral-decode",
                     help="mixtral-decode (default), deepseek-decode, deepseek-prefill, "
@@ -819,6 +935,9 @@ def main():
                          "(run under rocprofv3 --pmc)")
     ap.add_argument("--pmc-summary", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
                     help="summarise two --pmc-pass runs (FETCH_SIZE, WRITE_SIZE) into --out")
+    ap.add_argument("--pass-log", default=None, help="--pmc-summary: the JSON line a --pmc-pass run printed")
+    ap.add_argument("--all-resident-pass", action="store_true",
+                    help="--pmc-pass / --pmc-summary: the all-resident variant (r = 1, every expert cached)")
     ap.add_argument("--trace-summary", metavar="DIR", help="summarise a --kernel-trace --stats run into --out")
     ap.add_argument("--mfma-pmc-summary", metavar="DIR",
                     help="summarise a --pmc SQ_VALU_MFMA_BUSY_CYCLES GRBM_GUI_ACTIVE run into --out")
@@ -838,8 +957,9 @@ def main():
     ap.add_argument("--cmd", nargs="*", default=[], help="the profiling command(s), recorded in the summary")
     args = ap.parse_args()
     if args.pmc_summary:
-        pmc_summary(args.pmc_summary[0], args.pmc_summary[1], args.workload,
-                    args.out or pmc_profile_path(args.workload), *(args.cmd + ["", ""])[:2])
+        name = args.workload + ("-resident" if args.all_resident_pass else "")
+        pmc_summary(args.pmc_summary[0], args.pmc_summary[1], name,
+                    args.out or pmc_profile_path(name), *(args.cmd + ["", ""])[:2], pass_log=args.pass_log)
         return
     if args.trace_summary:
         trace_summary(args.trace_summary, args.out, " ".join(args.cmd))
@@ -866,14 +986,17 @@ def main():
         return
     wl = _workloads()[args.workload]
     shape, T = wl["shape"], wl["T"]
+    headline = args.workload == "mixtral-decode"
     t_setup = time.perf_counter()
     log("generating %s weights and filling the pinned store" % shape.name)
     rig = SplitRig(shape, seed=0, max_tokens=T, budget_bytes=shape.n_experts * shape.expert_bytes,
-                   keep_f32=not args.no_cpu_baseline, threads=16, ffn_splits=args.ffn_splits)
+                   keep_f32=not args.no_cpu_baseline, threads=16, ffn_splits=args.ffn_splits,
+                   n_buffer_slots=wl["slots"])
     if args.copy_engine == "dma":
         ms.ms_set_copy_engine(rig.ctx, ms.MS_COPY_DMA)
     n_tok = args.warmup + args.steps
-    seq = synth.walk(shape, 0, n_tok, T=T)
+    # independent N(0, 1) token batches, one per step
+    seq = [synth.hidden(shape, 0, T, tag=1000 + i) for i in range(n_tok)]
     hs = [to_device(raw, shape.dtype) for raw, _ in seq]
     torch.cuda.synchronize()
     setup_s = time.perf_counter() - t_setup
@@ -885,32 +1008,56 @@ def main():
     if args.all_tops:
         tops = list(range(shape.n_experts))
         budget = shape.n_experts * top_bytes(rig, r)
+    if args.all_resident_pass:
+        r, tops, budget = 1.0, list(range(shape.n_experts)), shape.n_experts * shape.expert_bytes
     slots = rig.configure([budget], [r])
     rig.load_tops(0, tops[:int(slots[0])])
     ms.ms_sync(rig.ctx)
+    flags = ms.MS_FWD_PREDICT_NEXT
     if args.pmc_pass:
         def calibrate():
             a = torch.empty(CALIB_BYTES, dtype=torch.uint8, device="cuda")
             b = torch.empty_like(a)
             b.copy_(a)
             torch.cuda.synchronize()
-        ms_p, _, _ = run_steps(rig, hs, args.steps, args.warmup, ms.MS_FWD_PREDICT_NEXT, timeline=False, T=T,
-                               before_timed=calibrate)
+        # the timeline's events do not change the kernels; they give the
+        # algorithmic bytes of the very dispatches the counters see
+        ms_p, tl_p, _ = run_steps(rig, hs, args.steps, args.warmup, flags, timeline=True, cold=True, T=T,
+                                  before_timed=calibrate)
+        an_p = analyse(tl_p, args.steps, ms_p)
+        ks = [an_p["kernels"][k] for k in ("ffn_resident", "ffn_streamed", "ffn_down")]
         rig.close()
         print(json.dumps({"pmc_pass": args.workload, "ms_per_step": round(ms_p, 4), "steps": args.steps,
-                          "calib_bytes": CALIB_BYTES}), flush=True)
+                          "calib_bytes": CALIB_BYTES, "ffn_launches": sum(k["launches"] for k in ks),
+                          "ffn_algorithmic_bytes": sum(k["bytes"] for k in ks)}), flush=True)
         return
-    ms_step, tl, st = run_steps(rig, hs, args.steps, args.warmup, ms.MS_FWD_PREDICT_NEXT, T=T)
-    # the same steps without the timeline's events: the cost of instrumenting
-    ms_plain, _, _ = run_steps(rig, hs, args.steps, args.warmup, ms.MS_FWD_PREDICT_NEXT, timeline=False, T=T)
+    n_slots = int(rig.sizes.buffer_bytes // rig.sizes.expert_bytes)
+    tb = top_bytes(rig, r)
+    # the value: the layer's steady state in a deep stack -- the staging
+    # buffer holds none of its segments when a token's routing arrives
+    per = []
+    ms_plain, _, st = run_steps(rig, hs, args.steps, args.warmup, flags, timeline=False, cold=True, T=T,
+                                per_step=per)
+    # the same steps with the library's timeline on: breakdown, overlap, roofline
+    ms_step, tl, st_i = run_steps(rig, hs, args.steps, args.warmup, flags, timeline=True, cold=True, T=T)
     an = analyse(tl, args.steps, ms_step)
     roof = ffn_roofline(an)
     if roof is not None:
-        roof["traffic"] = traffic_from_profile(args.workload)
+        tr = traffic_from_profile(args.workload)
+        roof["traffic"] = None if tr is None else tr[0]
+        roof["traffic_algorithmic_bytes"] = None if tr is None else tr[1]
+        roof["traffic_ratio"] = None if tr is None else round(tr[0] / tr[1], 4)
+        roof["by_launch"] = {k: ({"launches": v["launches"], "avg_us": round(v["total_ms"] / v["launches"] * 1e3, 2),
+                                  "bytes_per_launch": int(v["bytes"] / v["launches"]),
+                                  "gbps": round(v["bytes"] / (v["total_ms"] * 1e-3) / 1e9, 1)}
+                                 if v["launches"] else None)
+                             for k, v in an["kernels"].items() if k.startswith("ffn")}
     if args.timeline_out:
         with open(args.timeline_out, "w") as f:
             json.dump(dict(split=tl), f)
-
+    sem = float(np.std(per, ddof=1) / np.sqrt(len(per))) if len(per) > 1 else None
+    vram = {"top_segments_cached": int(slots[0]), "top_bytes_each": int(tb),
+            "staging_slots": n_slots, "staging_bytes": int(rig.sizes.buffer_bytes)}
     out = {
         "metric": METRIC,
         # the pass without timeline events; the instrumented pass gives the breakdown
@@ -921,18 +1068,26 @@ def main():
         "warmup": args.warmup,
         "ms_per_step": round(ms_plain, 4),
         "ms_per_step_instrumented": round(ms_step, 4),
-        "step_us": an["step_us"],
+        "value_sem_us": None if sem is None else round(sem * 1e3, 1),
+        "step_us": {q: round(float(np.percentile(per, p_)) * 1e3, 1) for q, p_ in (("p10", 10), ("p50", 50),
+                                                                                   ("p90", 90))},
         "higher_is_better": False,
         "scaling": "weak",
         "vs_baseline": None,
         "dtype": "bf16",
         "data": "synthetic",
-        "config": {"workload": "%s: %s-shaped MoE layer, %s T=%d, r=%.2f, %d top segments cached, other "
-                               "segments in pinned host RAM, prediction + prefetch on"
-                               % (args.workload, shape.name, "prefill" if T > 16 else "decode", T, r,
-                                  int(slots[0])),
+        "config": {"workload": "%s: %s-shaped MoE layer, %s batch of %d independent N(0,1) token(s) per step, "
+                               "r=%.2f; in VRAM: the top segments of %d experts (%.1f MB each) and a staging "
+                               "buffer of %d whole-expert slots that holds none of this layer's segments when a "
+                               "step's routing arrives (a layer of a deep stack: the other layers' misses cycle "
+                               "the buffer between two visits); the bottoms of the cached experts and the other "
+                               "experts whole in pinned host RAM, copied after routing; next-layer prediction "
+                               "and prefetch pass on" % (
+                                   args.workload, shape.name, "prefill" if T > 16 else "decode", T, r,
+                                   int(slots[0]), tb / 1e6, n_slots),
                    "d_model": shape.d_model, "d_ff": shape.d_ff, "n_experts": shape.n_experts,
                    "top_k": shape.top_k, "n_shared": shape.n_shared, "r": r, "tokens_per_step": T,
+                   "n_buffer_slots": n_slots, "buffer_at_routing": "empty", "vram": vram,
                    "expert_bits": shape.expert_bits or None},
         "roofline": roof,
         # prefill: matrix-core utilisation of the FFN kernels (None at decode)
@@ -952,30 +1107,25 @@ def main():
         "setup_s": round(setup_s, 1),
     }
     out["h2d_link_peak_gbps"] = round(h2d_link_peak_gbps(), 2)
+    log("split layer: %.3f ms/step (instrumented %.3f)" % (ms_plain, ms_step))
 
-    # the miss path alone: same tokens and residency, buffer emptied before
-    # every token and no prefetch, so every selected expert's missing
-    # segment is copied after routing
-    ms_cold, tl_cold, st_cold = run_steps(rig, hs, args.steps, args.warmup, 0, cold=True, T=T)
-    an_c = analyse(tl_cold, args.steps, ms_cold)
-    out["cold_miss_path"] = {
-        "us_per_layer": round(ms_cold * 1e3, 1),
-        "h2d_gbps": None if an_c["h2d_gbps"] is None else round(an_c["h2d_gbps"], 2),
-        "h2d_bytes_per_step": an_c["miss_bytes"] // args.steps,
-        "overlap": {"h2d_hidden_frac": an_c["hidden_frac"], "compute_hidden_frac": an_c["compute_hidden_frac"],
-                    "eta": an_c["overlap_eta"]},
-        "roofline": ffn_roofline(an_c),
-        "alpha_beta_gamma": [st_cold["alpha"], st_cold["beta"], st_cold["gamma"]]}
-    log("cold miss path: %.3f ms/step" % ms_cold)
-
-    log("split layer: %.3f ms/step" % ms_step)
+    # the hit path: every missing segment staged before routing
+    hit, hit_experts = run_hit_path(rig, hs[args.warmup:], args.steps, T=T)
+    out["hit_path"] = {"us_per_layer": round(float(np.mean(hit)) * 1e3, 1),
+                       "step_us": {q: round(float(np.percentile(hit, p_)) * 1e3, 1)
+                                   for q, p_ in (("p10", 10), ("p50", 50), ("p90", 90))},
+                       "buffer_hits": int(hit_experts),
+                       "what": "same tokens; each token's missing segments staged by an untimed forward just "
+                               "before, so the timed forward copies nothing (a right prediction whose prefetch "
+                               "landed in time)"}
+    log("hit path: %.3f ms/step" % float(np.mean(hit)))
     if not args.no_all_resident:
-        # all eight experts whole in VRAM (r = 1): the expert read is HBM-bound
+        # all experts whole in VRAM (r = 1): the expert read is HBM-bound
         rig.configure([shape.n_experts * shape.expert_bytes], [1.0])
         rig.load_tops(0, range(shape.n_experts))
         ms.ms_sync(rig.ctx)
-        ms_ar, tl_ar, _ = run_steps(rig, hs, args.steps, args.warmup, ms.MS_FWD_PREDICT_NEXT, T=T)
-        ms_ar_plain, _, _ = run_steps(rig, hs, args.steps, args.warmup, ms.MS_FWD_PREDICT_NEXT, timeline=False, T=T)
+        ms_ar, tl_ar, _ = run_steps(rig, hs, args.steps, args.warmup, flags, T=T)
+        ms_ar_plain, _, _ = run_steps(rig, hs, args.steps, args.warmup, flags, timeline=False, T=T)
         an_ar = analyse(tl_ar, args.steps, ms_ar)
         out["all_resident"] = {"us_per_layer": round(ms_ar_plain * 1e3, 1),
                                "us_per_layer_instrumented": round(ms_ar * 1e3, 1), "roofline": ffn_roofline(an_ar),
@@ -984,14 +1134,27 @@ def main():
                                                "avg_us": round(v["total_ms"] / v["launches"] * 1e3, 2)
                                                if v["launches"] else None}
                                            for k, v in an_ar["kernels"].items()}}
-    log("all-resident variant done")
+        tr = traffic_from_profile(args.workload + "-resident")
+        if tr is not None and out["all_resident"]["roofline"] is not None:
+            out["all_resident"]["roofline"].update(traffic=tr[0], traffic_algorithmic_bytes=tr[1],
+                                                   traffic_ratio=round(tr[0] / tr[1], 4))
+        log("all-resident variant: %.3f ms/step" % ms_ar_plain)
     if not args.no_cpu_baseline:
         log("timing the CPU oracle")
         out["cpu_baseline"] = cpu_baseline(rig, [f for _, f in seq], args.cpu_seconds)
     rig.close()
+    if headline and not args.no_stack:
+        # the Mixtral-shaped 32-layer stack at 12 GiB, r = .5: where
+        # cross-layer prediction and prefetch move bytes
+        log("Mixtral 32-layer stack")
+        stk = measure_stack("mixtral-stack", args.steps, args.warmup, args.copy_engine,
+                            instrument_steps=min(args.steps, 32))
+        out["stack"] = {k: stk.get(k) for k in (
+            "config", "value", "unit", "steps", "warmup", "ms_per_step", "step_ms", "tokens_per_s",
+            "alpha_beta_gamma", "hit_rate", "buffer_hits", "predicted_hits_per_layer_step", "h2d_bytes_per_step",
+            "h2d_gbps_over_step", "overlap", "copy_roofline", "ffn_roofline", "setup_s")}
     out["platform"] = platform_info()
     print(json.dumps(out), flush=True)
-
 
 if __name__ == "__main__":
     main()

@@ -9,7 +9,9 @@ device buffers with torch and sequences the calls.
 Layer i's forward predicts layer i + 1 from h^i and prefetches it
 (Sec. 3.2), so the copies run under layer i's MoE module and layer i + 1's
 attention; layer 0 of the next token is predicted from the last layer's
-output while the head runs (the first layer's window, T_head + T_att)."""
+intermediate activation h^L of the current token (Sec. 3.2, following
+AdapMoE), and its copies run under the head and layer 0's attention (the
+first layer's window, T_head + T_att)."""
 from __future__ import annotations
 
 import time
@@ -105,7 +107,10 @@ class Decoder:
             ms.ms_dense(self.o, wo, T, a.n_heads * a.head_dim, d, self.att, None, stream)
             ms.ms_residual_norm(self.ctx, src, self.att, T, self.h, stream)
             mark("moe")
-            fl = flags if l + 1 < self.L else flags & ~ms.MS_FWD_PREDICT_NEXT
+            # the last layer of a single-token step predicts layer 0 of the
+            # next token from its own intermediate activation h (Sec. 3.2);
+            # a prompt's last layer predicts from its last row below
+            fl = flags if (l + 1 < self.L or T == 1) else flags & ~ms.MS_FWD_PREDICT_NEXT
             ms.ms_forward(self.ctx, l, self.h, T, self.y, self.idx, self.w, fl, stream)
             dst = self.x[l % 2]
             ms.ms_residual_norm(self.ctx, self.h, self.y, T, dst, stream)
@@ -116,10 +121,11 @@ class Decoder:
             src = dst
         mark("head")
         last = src[T - 1:T]
-        if flags & ms.MS_FWD_PREDICT_NEXT:
-            # layer 0 of the next token, predicted from this token's output;
-            # its copies run under the head and layer 0's attention
-            order, _ = ms.ms_predict(self.ctx, 0, last, 1, stream, self.shape.n_experts)
+        if flags & ms.MS_FWD_PREDICT_NEXT and T > 1:
+            # layer 0 of the token after the prompt, predicted from the last
+            # layer's intermediate activation of the prompt's last token; its
+            # copies run under the head and layer 0's attention
+            order, _ = ms.ms_predict(self.ctx, 0, self.h[T - 1:T], 1, stream, self.shape.n_experts)
             ms.ms_prefetch(self.ctx, 0, order[:self.shape.top_k])
         ms.ms_dense(last, self.head, 1, d, V, self.logits, None, stream)
         ms.ms_argmax(self.logits, 1, V, self.ids, stream)

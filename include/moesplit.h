@@ -69,7 +69,7 @@ typedef enum { MS_F32 = 0, MS_BF16 = 1 } ms_dtype;
  * chosen from the shape so that a decode step fills the GPU).  It
  * changes the summation grouping, not what is computed.  expert_bits = 2 or
  * 4 stores the routed experts as affine b-bit codes (the HQQ format of the
- * paper's 2-bit Mixtral setting, Sec. 5.1; see ms_set_expert_q); 0 keeps
+ * paper's 2-bit Mixtral setting, Sec. 4.1; see ms_set_expert_q); 0 keeps
  * them in the model dtype.  b-bit experts need dtype MS_BF16, no shared
  * experts, d_ff a multiple of 64, d_model a multiple of 64 in [256, 8192] and
  * ffn_splits 0 or 1 (MS_E_UNSUPPORTED otherwise).  Every shape needs
@@ -278,7 +278,8 @@ ms_status ms_prefetch(ms_ctx* ctx, int32_t layer, const int32_t* experts, int32_
 /* MoE module of layer i (Eq. (2) without residual and Norm) on T tokens,
  * 0 <= T <= max_tokens:
  *   idx_dev[T][K] (int32): experts with the K largest router logits, in
- *     descending order, lower index first on equal logits;
+ *     descending order, lower index first on equal logits (a NaN logit
+ *     counts as -inf, in the ranking and in the softmax scores);
  *   w_dev[T][K] (fp32): softmax scores of the selected experts, divided by
  *     their sum if renormalize;
  *   y_dev[T][d] (fp32): sum_k w[t][k] * E_{idx[t][k]}(h_t) + shared experts.
@@ -361,10 +362,15 @@ ms_status ms_cache_update(ms_ctx* ctx, const uint64_t* budgets, const float* r);
  * ranks lowest: MS_CACHE_LCP by Eq. (4), MS_CACHE_LRU by last activation,
  * MS_CACHE_LFU by activation count, MS_CACHE_RND uniformly (seeded), each
  * with ties to the lower index.  Missed experts are taken in descending
- * order of the policy's rank, at most one per cache slot and forward, and an
- * expert cached in this forward is not evicted in it.  MS_CACHE_STATIC (the
+ * order of the policy's rank, at most one per cache slot and forward; each
+ * takes the lowest-numbered free slot if there is one, and an expert cached
+ * in this forward is not evicted in it.  MS_CACHE_STATIC (the
  * default) never changes the cache on its own.  rho in (0, 1) and omega > 0
- * parameterise Eq. (4) for the statistics and LCP. */
+ * parameterise Eq. (4) for the statistics and LCP.  MS_CACHE_RND's ranks:
+ * every forward of a layer with a cache draws one key per expert, in index
+ * order, from a SplitMix64 generator (Steele, Lea and Flood, OOPSLA 2014)
+ * whose state this call sets to seed XOR 0x9e3779b97f4a7c15; a key is the
+ * output's top 53 bits.  The generator is shared by the context's layers. */
 typedef enum {
   MS_CACHE_STATIC = 0,
   MS_CACHE_LCP = 1,

@@ -75,6 +75,12 @@ int orc_router_logits(const float *h, const float *w_r, const float *bias,
   return 0;
 }
 
+/* The value a logit is ranked and exponentiated by.  The paper never meets a
+ * non-number; this implementation reads a NaN logit as minus infinity: the
+ * expert ranks with the lowest logits (equal to -inf, so the lower index
+ * first among them) and its softmax score is 0. */
+static float rank_value(float v) { return isnan(v) ? -INFINITY : v; }
+
 /* Top-K selection (Sec. 2.1: the K experts with the highest scores).  Since
  * softmax is monotone, ranking by logit ranks by score; ranking by logit also
  * keeps apart logits that exp() would round to equal scores.  K passes of
@@ -89,7 +95,7 @@ void orc_topk(const float *logits, int T, int E, int K, int32_t *idx) {
       int best = -1;
       for (int e = 0; e < E; ++e) {
         if (taken[e]) continue;
-        if (best < 0 || l[e] > l[best]) best = e;
+        if (best < 0 || rank_value(l[e]) > rank_value(l[best])) best = e;
       }
       taken[best] = 1;
       idx[(size_t)t * K + k] = best;
@@ -99,14 +105,14 @@ void orc_topk(const float *logits, int T, int E, int K, int32_t *idx) {
 }
 
 /* softmax over E logits of one token, in double precision with the maximum
- * subtracted first (Sec. 2.1, s = softmax[R(h)]). */
+ * subtracted first (Sec. 2.1, s = softmax[R(h)]); NaN logits read as -inf. */
 static void softmax_row(const float *l, int E, double *p) {
-  double m = l[0];
+  double m = rank_value(l[0]);
   for (int e = 1; e < E; ++e)
-    if (l[e] > m) m = l[e];
+    if (rank_value(l[e]) > m) m = rank_value(l[e]);
   double z = 0.0;
   for (int e = 0; e < E; ++e) {
-    p[e] = exp((double)l[e] - m);
+    p[e] = exp((double)rank_value(l[e]) - m);
     z += p[e];
   }
   for (int e = 0; e < E; ++e) p[e] /= z;

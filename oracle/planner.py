@@ -206,24 +206,65 @@ def vram_allocation(V_e, zeta, prm, stats, V_start=None, max_iter=100000):
 
 # ------------------------------------------------- online replacement
 
-def replacement_keys(policy, st, last_use):
-    """Ranking key of each expert (larger = keep): LCP Eq. (4), LRU last
-    activation (forward count), LFU activation count."""
+MASK64 = (1 << 64) - 1
+
+
+class SplitMix64:
+    """SplitMix64 (Steele, Lea and Flood, "Fast splittable pseudorandom
+    number generators", OOPSLA 2014, in the 64-bit form Vigna publishes as
+    splitmix64.c): the state advances by the golden-ratio increment
+    0x9e3779b97f4a7c15 and each output is the state passed through the
+    variant-13 mixer (shift-xor 30, multiply 0xbf58476d1ce4e5b9, shift-xor 27,
+    multiply 0x94d049bb133111eb, shift-xor 31).  The random policy draws its
+    keys from it; the generator is counter-based, so both sides can carry
+    their own copy."""
+
+    GAMMA = 0x9E3779B97F4A7C15
+
+    def __init__(self, state):
+        self.state = state & MASK64
+
+    def next(self):
+        self.state = (self.state + self.GAMMA) & MASK64
+        z = self.state
+        z = ((z ^ (z >> 30)) * 0xBF58476D1CE4E5B9) & MASK64
+        z = ((z ^ (z >> 27)) * 0x94D049BB133111EB) & MASK64
+        return z ^ (z >> 31)
+
+
+def rnd_generator(seed):
+    """The random policy's generator for a user seed: the state starts at
+    seed XOR the golden-ratio increment."""
+    return SplitMix64(seed ^ SplitMix64.GAMMA)
+
+
+def replacement_keys(policy, st, last_use, rng=None):
+    """Ranking key of each expert (larger = keep):
+    LCP: the cache priority of Eq. (4) after this forward's statistics;
+    LRU: last_use[e], the count of the layer's forwards up to and including
+         the most recent one that activated e (0 if never);
+    LFU: mu_e, the activations so far;
+    RND: one draw per expert in index order, the top 53 bits of the next
+         SplitMix64 output (rng, from rnd_generator), as a float."""
     if policy == "lcp":
         return lcp_priority(st.mu, st.nu, st.rho, st.omega)
     if policy == "lru":
         return [float(x) for x in last_use]
     if policy == "lfu":
         return list(st.mu)
+    if policy == "rnd":
+        return [float(rng.next() >> 11) for _ in range(st.N)]
     raise ValueError(policy)
 
 
 def replacement_step(cached, counts, key):
-    """Sec. 3.3 on a miss: each activated expert without a cached top, in
-    descending key order (ties to the lower index), at most one per cache
-    slot, takes a free slot or the slot of the lowest-key cached expert
-    (ties to the lower index) not cached in this same step.  cached: list of
-    experts per slot (-1 free), updated in place."""
+    """Sec. 3.3, on a miss: the missed experts are the activated ones
+    (counts[e] > 0) with no cached top.  Taken in descending key order (ties
+    to the lower index), at most as many as there are cache slots, each takes
+    a free slot (the lowest-numbered one) if there is one, else the slot of
+    the cached expert with the lowest key (ties to the lower index) among
+    those not cached in this same step.  cached: list of experts per slot
+    (-1 free), updated in place and returned."""
     N = len(counts)
     missed = sorted((e for e in range(N) if counts[e] > 0 and e not in cached), key=lambda e: (-key[e], e))
     fresh = set()

@@ -1,6 +1,6 @@
 """Oracle of the split-expert MoE layer whose experts are stored as affine
 b-bit codes: the HQQ-quantized MoE weights of the paper's Mixtral setting
-(Sec. 5.1: attention 4-bit, MoE modules 2-bit).
+(Sec. 4.1: attention 4-bit, MoE modules 2-bit).
 
 TEST INFRASTRUCTURE ONLY, like the rest of this package: plain numpy in
 fp64, sharing no code with the GPU library.

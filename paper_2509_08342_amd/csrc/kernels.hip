@@ -58,19 +58,8 @@ __device__ __forceinline__ void load16(const uint16_t* p, float (&o)[8]) {
 
 __device__ __forceinline__ uint4 ld16(const void* p) { return *reinterpret_cast<const uint4*>(p); }
 
-#ifndef MSK_NT_LOADS
-#define MSK_NT_LOADS 0
-#endif
-typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
 // 16-byte load of expert weights, which are streamed once per forward.
-__device__ __forceinline__ uint4 ldw16(const void* p) {
-#if MSK_NT_LOADS
-  const u32x4_t v = __builtin_nontemporal_load(reinterpret_cast<const u32x4_t*>(p));
-  return make_uint4(v.x, v.y, v.z, v.w);
-#else
-  return *reinterpret_cast<const uint4*>(p);
-#endif
-}
+__device__ __forceinline__ uint4 ldw16(const void* p) { return *reinterpret_cast<const uint4*>(p); }
 
 __device__ __forceinline__ void unpack(const uint4 v, float (&o)[4]) {
   o[0] = __uint_as_float(v.x);
@@ -107,7 +96,8 @@ __device__ __forceinline__ f32x4_t mfma16(bf16x8_t a, bf16x8_t b, f32x4_t c) {
 // -------------------------------------------------------------------- route
 //
 // Per token (one wave): K rounds of wave argmax over the untaken experts
-// (larger logit wins, the lower index on equal logits, NaN ranks last), then
+// (larger logit wins, the lower index on equal logits; a NaN logit reads as
+// -inf here and in the softmax scores), then
 // the Eq. (2) weights from exp(logit - max).  Per token for the prediction
 // (Sec. 3.2, Eq. (3)): the softmax of its second logits, added to the
 // lane's running expert sums.  The grouping is a stable counting sort of
@@ -125,7 +115,7 @@ __device__ __forceinline__ void select_token(const float* lg, int E, int K, int 
   for (int q = 0; q < kLanesQ; ++q) {
     const int e = lane + 64 * q;
     float v = e < E ? lg[e] : -INFINITY;
-    if (v != v) v = -INFINITY;  // NaN ranks last, so an index is always found
+    if (v != v) v = -INFINITY;  // NaN reads as -inf, so an index is always found
     lv[q] = v;
   }
   uint32_t taken = 0;
@@ -180,7 +170,9 @@ __device__ __forceinline__ void pred_add(const float* lg, int E, int lane, float
 #pragma unroll
   for (int q = 0; q < kLanesQ; ++q) {
     const int e = lane + 64 * q;
-    lv[q] = e < E ? lg[e] : -INFINITY;
+    float v = e < E ? lg[e] : -INFINITY;
+    if (v != v) v = -INFINITY;  // a NaN logit reads as -inf: score 0
+    lv[q] = v;
     m = fmaxf(m, lv[q]);
   }
 #pragma unroll
@@ -909,15 +901,9 @@ __device__ __forceinline__ int find_task_of(const TaskT* tasks, int n, int wg) {
   return lo;
 }
 
-#ifndef MSK_ROW_BATCH
-#define MSK_ROW_BATCH 4
-#endif
-constexpr int kRowBatch = MSK_ROW_BATCH;  // RB of launches that fill the GPU
+constexpr int kRowBatch = 4;        // RB of launches that fill the GPU
 constexpr int kRowBatchDeep = 8;    // RB of launches with fewer work-groups than CUs
-#ifndef MSK_DEEP_BELOW
-#define MSK_DEEP_BELOW 256
-#endif
-constexpr int kDeepBelowWgs = MSK_DEEP_BELOW;
+constexpr int kDeepBelowWgs = 256;
 constexpr int kLpu = kFfnLanesPerUnit;
 constexpr int kKTile = 64;                // k elements per gate/up piece
 

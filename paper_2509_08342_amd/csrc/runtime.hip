@@ -1016,8 +1016,11 @@ ms_status prefill_experts(ms_ctx* ctx, int layer, const void* h_dev, int T, cons
     const int res = resident_chunks(L, e);
     int si = covering[e];
     if (si < 0) {
+      // a slot of (layer, e) that starts above the resident part (its top
+      // was evicted since) is reassigned, as on the decode path, so that no
+      // two slots ever hold the same expert
       si = find_slot(ctx, layer, e);
-      if (si < 0 || ctx->buf[si].first_chunk > res) si = pick_victim(ctx, true);
+      if (si < 0) si = pick_victim(ctx, true);
       if (si < 0) return fail(ctx, MS_E_STATE, "no staging slot can be taken");
       st = assign_slot(ctx, si, layer, e, res, true);
       if (st != MS_OK) return st;
@@ -1469,7 +1472,10 @@ ms_status ms_residency(ms_ctx* ctx, int32_t layer, uint8_t* state_out) {
 
 ms_status ms_drop_buffer(ms_ctx* ctx) {
   MS_CHECK_CTX(ctx);
+  // groups already issued complete on the copy stream, which orders every
+  // later copy into the same slots after them
   ctx->pf_queue.clear();
+  ctx->pf_inflight.clear();
   for (BufSlot& b : ctx->buf) clear_slot(b);
   return MS_OK;
 }

@@ -5,8 +5,8 @@ shaped 26-layer and Qwen3-30B-A3B-shaped 48-layer prefill + decode).
 Each layer's input is the previous layer's output through the glue
 h_{i+1} = RMSNorm(h_i + y_i) (ms_residual_norm).  Layer i's forward predicts
 layer i+1 from h_i with layer i+1's router and prefetches it (Sec. 3.2); the
-first layer of the next step is predicted from the final hidden state of
-this step.  The cache of each layer holds the top segments of the experts
+first layer of the next step is predicted from the last layer's input h_{L-1}
+of this step (the last layer's intermediate activation, Sec. 3.2).  The cache of each layer holds the top segments of the experts
 selected most often in a warm-up (ties to the lower index) until a cache
 configurator chooses otherwise.  Every step of the layer runs in the
 library's kernels; this module only sequences calls and moves test data.
@@ -65,8 +65,10 @@ class Stack:
         cap = {}
         src = x
         for l in range(self.L):
-            fl = flags if l + 1 < self.L else flags & ~ms.MS_FWD_PREDICT_NEXT
-            ms.ms_forward(self.ctx, l, src, T, self.y, self.idx, self.w, fl, stream)
+            # with MS_FWD_PREDICT_NEXT the last layer predicts layer 0 of the
+            # next step from its own input, the last layer's intermediate
+            # activation (Sec. 3.2)
+            ms.ms_forward(self.ctx, l, src, T, self.y, self.idx, self.w, flags, stream)
             if l in capture or counts is not None:
                 stream.synchronize()
                 idx = self.idx[:T].cpu().numpy()
@@ -78,10 +80,6 @@ class Stack:
             dst = self.h[l % 2]
             ms.ms_residual_norm(self.ctx, src, self.y, T, dst, stream)
             src = dst
-        if flags & ms.MS_FWD_PREDICT_NEXT:
-            # the next step's first layer, predicted from this step's output
-            order, _ = ms.ms_predict(self.ctx, 0, src, T, stream, self.shape.n_experts)
-            ms.ms_prefetch(self.ctx, 0, order[:self.shape.top_k])
         return src, cap
 
     def warmup_counts(self, xs, T):

@@ -3,6 +3,7 @@ overlap figures of a hand-built timeline, the FFN and copy rooflines, and
 the rocprofv3 summaries (PMC scaling by the calibration copy, kernel
 statistics) on small hand-written CSV files."""
 import csv
+import json
 import os
 
 import pytest
@@ -65,13 +66,28 @@ def test_pmc_summary_scales_by_the_calibration_copy(tmp_path):
             [3, "void msk::ffn_chunk_kernel<unsigned short, 1, 1, 64, 4>(msk::FfnArgs)", 4.0],
             [4, "void msk::ffn_chunk_kernel<unsigned short, 1, 1, 64, 4>(msk::FfnArgs)", 4.0]])
     out = str(tmp_path / "pmc.md")
-    bench.pmc_summary(str(tmp_path / "f"), str(tmp_path / "w"), "wl", out, "cmd f", "cmd w")
+    log = tmp_path / "pass.log"
+    log.write_text("[bench] noise\n" + json.dumps({"pmc_pass": "wl", "ffn_launches": 2,
+                                                   "ffn_algorithmic_bytes": 2 * 4000 * 1024}) + "\n")
+    bench.pmc_summary(str(tmp_path / "f"), str(tmp_path / "w"), "wl", out, "cmd f", "cmd w", pass_log=str(log))
     text = open(out).read()
     vals = dict(line.strip("- ").split(": ") for line in text.splitlines() if line.startswith("- `"))
     # dispatches after the calibration copy only; fetch (1000 + 3000) / 2 / 0.5 KiB, write 4 KiB each
     assert vals["`ffn_dispatches`"] == "`2`"
     assert vals["`ffn_traffic_bytes_per_launch`"] == "`%d`" % int((2000 * 2 + 4) * 1024)
+    assert vals["`ffn_algorithmic_bytes_per_launch`"] == "`%d`" % (4000 * 1024)
+    assert vals["`ffn_traffic_ratio`"] == "`%.4f`" % ((4000 + 4) / 4000)
     assert "cmd f" in text and "cmd w" in text
+    # bench reads (traffic, algorithmic bytes) back while the sources hash the same
+    monkey = bench.PROFILES
+    try:
+        bench.PROFILES = str(tmp_path)
+        import shutil
+        shutil.copy(out, bench.pmc_profile_path("wl"))
+        assert bench.traffic_from_profile("wl") == ((4000 + 4) * 1024, 4000 * 1024)
+        assert bench.traffic_from_profile("other") is None
+    finally:
+        bench.PROFILES = monkey
 
 
 def test_trace_summary_orders_kernels_by_time(tmp_path):

@@ -106,3 +106,47 @@ def test_many_token_router_follows_fixed_logit_order(which):
         r.forward(0, torch.from_numpy(h).cuda(), T, y, idx, w)
         torch.cuda.synchronize()
         assert np.all(idx[:, 0].cpu().numpy() == expect)
+
+
+NAN_F32 = synth.ModelShape("nan-f32", 1, 256, 512, 4, 3, "f32")
+NAN_BF16 = synth.ModelShape("nan-bf16", 1, 256, 512, 4, 3, "bf16")
+
+
+@pytest.mark.parametrize("shape,T", [(NAN_F32, 5), (NAN_BF16, 5), (NAN_F32, 100), (NAN_BF16, 100)],
+                         ids=["f32-few", "bf16-few", "f32-many", "bf16-many"])
+def test_nan_router_logits_read_as_minus_infinity(shape, T):
+    """Router columns of experts 1 and 2 hold a NaN, so their logits are NaN
+    for every token.  Read as -inf, they rank below experts 0 and 3 and tie
+    with each other (expert 1 first), with score 0: every token selects the
+    better of 0 and 3, the other, then expert 1 with weight 0.  The
+    prediction ranks 1 and 2 last with score 0.  Both the few- and the
+    many-token routing paths, against the oracle's same reading."""
+    import oracle
+    from paper_2509_08342_amd import moesplit as ms
+    from workload import SplitRig
+    with SplitRig(shape, seed=8, max_tokens=T, budget_bytes=shape.n_experts * shape.expert_bytes) as r:
+        w_raw, _ = synth.router(shape, 8, 0)
+        w_raw = np.array(w_raw, copy=True)
+        f32 = np.array(r.routers[0], copy=True)
+        nan_bits = np.uint16(0x7fc0) if shape.dtype == "bf16" else np.float32(np.nan)
+        for e in (1, 2):
+            w_raw[5, e] = nan_bits
+            f32[5, e] = np.nan
+        ms.ms_set_router(r.ctx, 0, w_raw)
+        r.routers[0] = f32
+        r.configure([2 * shape.expert_bytes], [0.5])
+        r.load_tops(0, [1, 3])
+        h, hf = r.hidden(T, tag=31)
+        y, idx, w = r.outputs(T)
+        r.forward(0, h, T, y, idx, w)
+        torch.cuda.synchronize()
+        check_layer(r, 0, hf, y, idx, w)
+        ig = idx[:T].cpu().numpy()
+        assert np.all(np.sort(ig[:, :2], axis=1) == [0, 3]) and np.all(ig[:, 2] == 1)
+        assert np.all(w[:T, 2].cpu().numpy() == 0.0)
+        assert np.all(np.isfinite(y[:T].cpu().numpy()))
+        order, score = ms.ms_predict(r.ctx, 0, h, T, torch.cuda.current_stream(), shape.n_experts)
+        ref_score, ref_order = oracle.predict(hf, f32)
+        assert ref_order.tolist()[2:] == [1, 2] and order.tolist()[2:] == [1, 2]
+        assert score[1] == 0.0 and score[2] == 0.0
+        check_prediction(order, score, ref_score)

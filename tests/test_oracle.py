@@ -80,6 +80,20 @@ def test_hand_expert_outputs_and_split():
         np.testing.assert_allclose(bot[:2], sp[name + "_bottom"], rtol=1e-15, atol=0)
 
 
+def test_hand_activations():
+    """The SwiGLU intermediate a_f = silu(h.G_f) * (h.U_f) of both hand
+    experts at h = (1, 2), whole and unit by unit (range form)."""
+    g = _golden()
+    ex = _hand_experts(g)
+    h = _pad_d(np.array([[1, 2]], np.float32), 64, 1)[0]
+    ref = g["activations_h12"]
+    for i, name in enumerate(("E0", "E1")):
+        wg, wu, _ = ex[i]
+        np.testing.assert_allclose(oracle.expert_act(h, wg, wu, 0, 2), ref[name], rtol=1e-15, atol=0)
+        np.testing.assert_allclose(oracle.expert_act(h, wg, wu, 1, 2), ref[name][1:], rtol=1e-15, atol=0)
+        np.testing.assert_allclose(oracle.expert_act(h, wg, wu, 0, 1), ref[name][:1], rtol=1e-15, atol=0)
+
+
 # ------------------------------------------------- canonical fp32 logit order
 
 @pytest.mark.parametrize("which", ["a", "b", "c"])
@@ -296,6 +310,32 @@ def test_predict_order_and_scores():
     # one token: the ranking is the ranking of its logits
     s1, o1 = oracle.predict(h[:1], w)
     assert np.array_equal(o1, oracle.topk(oracle.router_logits(h[:1], w), E)[0])
+
+
+def test_nan_logits_read_as_minus_infinity():
+    """Reading: a NaN router logit ranks as -inf (lower index first among
+    equal values) and has softmax score 0.  Row (NaN, 0.5, NaN, -inf, 2):
+    ranking e4, e1, then e0, e2, e3 tied at -inf; scores of e4 and e1 are
+    1 / (1 + e^-1.5) and 1 / (1 + e^1.5), the rest 0, with or without
+    renormalisation; the prediction ranks the same way."""
+    row = np.array([[np.nan, 0.5, np.nan, -np.inf, 2.0]], np.float32)
+    assert oracle.topk(row, 5)[0].tolist() == [4, 1, 0, 2, 3]
+    idx = oracle.topk(row, 2)
+    assert idx[0].tolist() == [4, 1]
+    p4, p1 = 1.0 / (1.0 + math.exp(-1.5)), 1.0 / (1.0 + math.exp(1.5))
+    for renorm in (0, 1):
+        np.testing.assert_allclose(oracle.gate_weights(row, idx, renorm)[0], [p4, p1], rtol=1e-15)
+    w5 = oracle.gate_weights(row, oracle.topk(row, 5), 1)[0]
+    np.testing.assert_allclose(w5, [p4, p1, 0.0, 0.0, 0.0], rtol=1e-15, atol=0)
+    # prediction from logits through the router: a NaN router column
+    d = 64
+    h = np.zeros((2, d), np.float32)
+    h[:, 0] = 1.0
+    w = np.zeros((d, 5), np.float32)
+    w[0] = [np.nan, 0.5, np.nan, -np.inf, 2.0]
+    score, order = oracle.predict(h, w)
+    assert order.tolist() == [4, 1, 0, 2, 3]
+    np.testing.assert_allclose(score, [0.0, 2 * p1, 0.0, 0.0, 2 * p4], rtol=1e-15, atol=0)
 
 
 def test_predict_ties_lower_index_first():
