@@ -150,7 +150,8 @@ def test_qwen_stack_configured_by_algorithm_1_with_lcp():
         plan = ms.ms_plan_solve(L, E, K, shape.expert_bytes, 0.0, 305.0, 0.0, shape.expert_bytes / 55e3,
                                 np.array([s[0] for s in stats]), np.array([s[1] for s in stats]),
                                 np.array([s[2] for s in stats]), budget, 0.01)
-        assert int(plan["budgets"].sum()) == budget
+        # the budget is conserved (less the remainder of the uniform start)
+        assert budget - L < int(plan["budgets"].sum()) <= budget
         ms.ms_cache_update(st.ctx, plan["budgets"], plan["theta"].astype(np.float32))
         for l in range(L):
             units, tb, c = ms.ms_split_plan(st.rig.desc, int(plan["budgets"][l]), float(plan["theta"][l]))
