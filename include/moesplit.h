@@ -291,6 +291,23 @@ ms_status ms_forward(ms_ctx* ctx, int32_t layer, const void* h_dev, int32_t T,
                      float* y_dev, int32_t* idx_dev, float* w_dev, int32_t flags,
                      void* stream);
 
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture elsewhere in their stream, tight serving loops, harnesses that
+ * forbid hipMalloc): ms_forward with its per-forward work buffers (router
+ * logits, grouping, FFN partials, combine sums, activations, routing
+ * workspace) in a fixed array of 64 MiB in device memory that the library
+ * holds on every GPU it runs on until the process ends, instead of in the
+ * context's pool.  Same arguments, semantics and outputs as ms_forward; the
+ * call allocates no device or pinned memory and creates no HIP objects.
+ * MS_E_UNSUPPORTED if the context's work buffers (they grow with
+ * max_tokens) exceed 64 MiB.  Every call on a GPU, from any context, uses
+ * that GPU's one array: calls of one context are ordered like its
+ * ms_forward calls, but calls of two contexts on the same GPU that overlap
+ * in time race on the array and give undefined outputs. */
+ms_status ms_forward_noalloc(ms_ctx* ctx, int32_t layer, const void* h_dev, int32_t T,
+                             float* y_dev, int32_t* idx_dev, float* w_dev, int32_t flags,
+                             void* stream);
+
 /* Wait until every copy and kernel the library issued has finished. */
 ms_status ms_sync(ms_ctx* ctx);
 

@@ -12,6 +12,7 @@
 
 #include <algorithm>
 #include <functional>
+#include <mutex>
 #include <cmath>
 #include <cstdio>
 #include <cstring>
@@ -23,6 +24,19 @@
 #include "kernels.h"
 #include "moesplit.h"
 #include "planner.h"
+
+namespace {
+// Per-forward work buffers of ms_forward_noalloc, for callers that cannot
+// allocate: a fixed array in device memory, one copy per GPU, held until the
+// process ends.
+constexpr uint64_t kStaticScratchBytes = 64ull << 20;
+constexpr int kMaxDevices = 64;
+}  // namespace
+
+// In host code the name is only a stand-in for the symbol: each GPU's copy
+// is reached through the device address hipGetSymbolAddress returns for it
+// (scratch_address below), never through the name.
+static __device__ __align__(256) unsigned char scratch[kStaticScratchBytes];
 
 namespace {
 
@@ -38,6 +52,7 @@ constexpr uint64_t kAlign = 256;
 // token from 4 MiB prefetch groups over 16 MiB, bf16 Mixtral (352 MB) is
 // within 1% from 4 to 16 MiB.
 constexpr uint64_t kGroupMinBytes = 4ull << 20;
+
 constexpr uint64_t kGroupMaxBytes = 16ull << 20;
 constexpr uint64_t kMissGroupTargetBytes = 64ull << 20;
 constexpr int kPrefetchWindow = 2;                   // prefetch groups in flight
@@ -424,6 +439,7 @@ struct ms_ctx {
   double rho = 0.25, omega = 128.0;
   uint64_t rng = 0x9e3779b97f4a7c15ull;
   int device = 0;
+  unsigned char* scratch_addr = nullptr;  // this device's copy of `scratch`
   unsigned char* pool = nullptr;
   uint64_t pool_bytes = 0;
   hipStream_t copy = nullptr, side = nullptr;
@@ -466,7 +482,14 @@ struct ms_ctx {
   std::vector<TlRec> tl;
   std::vector<hipEvent_t> tl_pool;
 
-  unsigned char* dev(uint64_t off) { return pool + off; }
+  // ms_forward_noalloc: while set, the per-forward work buffers (the pool
+  // range [off_logits, off_buffer)) live at work_base instead
+  unsigned char* work_base = nullptr;
+
+  unsigned char* dev(uint64_t off) {
+    if (work_base && off >= s.off_logits && off < s.off_buffer) return work_base + (off - s.off_logits);
+    return pool + off;
+  }
 };
 
 namespace {
@@ -481,6 +504,25 @@ ms_status poison(ms_ctx* ctx, const char* what, hipError_t e) {
   ctx->poisoned = true;
   ctx->err = std::string("HIP error in ") + what + ": " + hipGetErrorString(e);
   return MS_E_HIP;
+}
+
+// Device address of the current GPU's copy of `scratch`, looked up once per
+// device (ms_create calls this with the context's device current).
+std::mutex g_scratch_mu;
+unsigned char* g_scratch_addr[kMaxDevices] = {};
+
+hipError_t scratch_address(int device, unsigned char** out) {
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  *out = nullptr;
+  if (device < 0 || device >= kMaxDevices) return hipSuccess;
+  if (!g_scratch_addr[device]) {
+    void* p = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    g_scratch_addr[device] = static_cast<unsigned char*>(p);
+  }
+  *out = g_scratch_addr[device];
+  return hipSuccess;
 }
 
 ms_status fail(ms_ctx* ctx, ms_status st, const std::string& msg) {
@@ -620,11 +662,7 @@ ms_status assign_slot(ms_ctx* ctx, int si, int layer, int e, int first, bool mis
     g.c_hi = std::min(n, c + per);
     b.groups.push_back(g);
   }
-  while (b.gev.size() < b.groups.size()) {
-    hipEvent_t ev;
-    MS_HIP(hipEventCreateWithFlags(&ev, hipEventDisableTiming));
-    b.gev.push_back(ev);
-  }
+  if (b.gev.size() < b.groups.size()) return fail(ctx, MS_E_STATE, "staging slot has fewer copy events than groups");
   return MS_OK;
 }
 
@@ -1129,6 +1167,8 @@ ms_status ms_create(const ms_model_desc* desc, void* dev_pool, uint64_t pool_byt
   };
   hipError_t e;
   if ((e = hipGetDevice(&ctx->device)) != hipSuccess) return cleanup_fail(e, "hipGetDevice");
+  if ((e = scratch_address(ctx->device, &ctx->scratch_addr)) != hipSuccess)
+    return cleanup_fail(e, "hipGetSymbolAddress(scratch)");
   if ((e = hipStreamCreateWithFlags(&ctx->copy, hipStreamNonBlocking)) != hipSuccess)
     return cleanup_fail(e, "hipStreamCreate(copy)");
   if ((e = hipStreamCreateWithFlags(&ctx->side, hipStreamNonBlocking)) != hipSuccess)
@@ -1167,10 +1207,21 @@ ms_status ms_create(const ms_model_desc* desc, void* dev_pool, uint64_t pool_byt
       return cleanup_fail(e, "hipEventCreate(layer)");
   }
   ctx->buf.resize(s.n_buf);
+  // one completion event per copy group a slot can hold: a slot's content is
+  // cut into at most ceil(n_chunks / group size) groups (assign_slot), so
+  // no forward ever creates one
+  const int g_min = std::max(1, std::min(s.group_chunks, s.miss_group_chunks));
+  const int max_groups = (s.n_chunks + g_min - 1) / g_min;
   for (int i = 0; i < s.n_buf; ++i) {
     ctx->buf[i].base = ctx->dev(s.off_buffer + s.expert_bytes * i);
     if ((e = hipEventCreateWithFlags(&ctx->buf[i].last_read, hipEventDisableTiming)) != hipSuccess)
       return cleanup_fail(e, "hipEventCreate(slot)");
+    for (int g = 0; g < max_groups; ++g) {
+      hipEvent_t ev;
+      if ((e = hipEventCreateWithFlags(&ev, hipEventDisableTiming)) != hipSuccess)
+        return cleanup_fail(e, "hipEventCreate(copy group)");
+      ctx->buf[i].gev.push_back(ev);
+    }
   }
   *out = ctx;
   return MS_OK;
@@ -2000,6 +2051,25 @@ ms_status ms_forward(ms_ctx* ctx, int32_t layer, const void* h_dev, int32_t T, f
   }
   for (BufSlot& b : ctx->buf) b.use_order = -1;
   return MS_OK;
+}
+
+ms_status ms_forward_noalloc(ms_ctx* ctx, int32_t layer, const void* h_dev, int32_t T, float* y_dev,
+                             int32_t* idx_dev, float* w_dev, int32_t flags, void* stream) {
+  MS_CHECK_CTX(ctx);
+  const uint64_t need = ctx->s.off_buffer - ctx->s.off_logits;
+  if (need > kStaticScratchBytes) {
+    char msg[256];
+    std::snprintf(msg, sizeof(msg),
+                  "ms_forward_noalloc: this context's work buffers take %llu bytes, more than the %llu-byte static "
+                  "scratch (lower max_tokens)",
+                  static_cast<unsigned long long>(need), static_cast<unsigned long long>(kStaticScratchBytes));
+    return fail(ctx, MS_E_UNSUPPORTED, msg);
+  }
+  if (!ctx->scratch_addr) return fail(ctx, MS_E_STATE, "ms_forward_noalloc: no static scratch on this device");
+  ctx->work_base = ctx->scratch_addr;
+  const ms_status st = ms_forward(ctx, layer, h_dev, T, y_dev, idx_dev, w_dev, flags, stream);
+  ctx->work_base = nullptr;
+  return st;
 }
 
 ms_status ms_residual_norm(ms_ctx* ctx, const void* h_dev, const float* y_dev, int32_t T, void* out_dev,

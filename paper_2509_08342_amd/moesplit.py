@@ -90,6 +90,7 @@ def _load():
         "ms_predict": [P, I32, P, I32, P, P, P],
         "ms_prefetch": [P, I32, P, I32],
         "ms_forward": [P, I32, P, I32, P, P, P, I32, P],
+        "ms_forward_noalloc": [P, I32, P, I32, P, P, P, I32, P],
         "ms_sync": [P],
         "ms_drop_buffer": [P],
         "ms_stats": [P, I32, ctypes.POINTER(ms_layer_stats)],
@@ -263,6 +264,11 @@ def ms_prefetch(ctx, layer, experts):
 def ms_forward(ctx, layer, h_dev, T, y_dev, idx_dev, w_dev, flags=0, stream=None):
     _check(lib.ms_forward(ctx, layer, _ptr(h_dev), T, _ptr(y_dev), _ptr(idx_dev), _ptr(w_dev), flags,
                           _stream(stream)), ctx)
+
+
+def ms_forward_noalloc(ctx, layer, h_dev, T, y_dev, idx_dev, w_dev, flags=0, stream=None):
+    _check(lib.ms_forward_noalloc(ctx, layer, _ptr(h_dev), T, _ptr(y_dev), _ptr(idx_dev), _ptr(w_dev), flags,
+                                  _stream(stream)), ctx)
 
 
 def ms_sync(ctx):
