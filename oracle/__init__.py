@@ -20,7 +20,8 @@ import numpy as np
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _SRC = os.path.join(_HERE, "moe_oracle.c")
-_LIB_PATH = os.path.join(_HERE, "libmoe_oracle.so")
+_LIB_PATH = os.environ.get("MOE_ORACLE_LIB") or os.path.join(_HERE, "libmoe_oracle.so")
+_SAN_PATH = os.path.join(_HERE, "libmoe_oracle_san.so")
 _lib = None
 _lock = threading.Lock()
 
@@ -31,16 +32,20 @@ _f64p = np.ctypeslib.ndpointer(np.float64, flags="C_CONTIGUOUS")
 _i32p = np.ctypeslib.ndpointer(np.int32, flags="C_CONTIGUOUS")
 
 
-def build_oracle(force: bool = True) -> str:
-    """Compile moe_oracle.c into libmoe_oracle.so with gcc (no GPU toolchain)."""
-    if force or not os.path.exists(_LIB_PATH) or (
-            os.path.getmtime(_LIB_PATH) < os.path.getmtime(_SRC)):
-        tmp = _LIB_PATH + ".tmp%d" % os.getpid()
+def build_oracle(force: bool = True, sanitize: bool = False) -> str:
+    """Compile moe_oracle.c into libmoe_oracle.so with gcc (no GPU toolchain);
+    sanitize=True builds libmoe_oracle_san.so with AddressSanitizer and
+    UndefinedBehaviorSanitizer instead (same floating-point flags)."""
+    path = _SAN_PATH if sanitize else _LIB_PATH
+    if force or not os.path.exists(path) or (os.path.getmtime(path) < os.path.getmtime(_SRC)):
+        tmp = path + ".tmp%d" % os.getpid()
+        san = ["-g", "-fsanitize=address,undefined", "-fno-sanitize-recover=undefined",
+               "-fno-omit-frame-pointer"] if sanitize else []
         cmd = ["gcc", "-O2", "-std=c99", "-fPIC", "-shared", "-ffp-contract=off",
-               "-fno-fast-math", "-Wall", "-Wextra", "-o", tmp, _SRC, "-lm"]
+               "-fno-fast-math", "-Wall", "-Wextra", *san, "-o", tmp, _SRC, "-lm"]
         subprocess.check_call(cmd)
-        os.replace(tmp, _LIB_PATH)
-    return _LIB_PATH
+        os.replace(tmp, path)
+    return path
 
 
 def _load():

@@ -13,7 +13,10 @@ import os
 
 import numpy as np
 
-_LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libmoesplit.so")
+# MOESPLIT_LIB names another build of the same library (the sanitized host
+# build of build.py --sanitize); there is no fallback when it is missing.
+_LIB_PATH = os.environ.get("MOESPLIT_LIB") or os.path.join(os.path.dirname(os.path.abspath(__file__)),
+                                                          "libmoesplit.so")
 
 MS_OK, MS_E_INVALID, MS_E_BUDGET, MS_E_STATE, MS_E_HIP, MS_E_NOMEM, MS_E_UNSUPPORTED = range(7)
 STATUS_NAMES = {0: "MS_OK", 1: "MS_E_INVALID", 2: "MS_E_BUDGET", 3: "MS_E_STATE", 4: "MS_E_HIP",
