@@ -166,6 +166,7 @@ constexpr int kMaxMmaTasks = 80;
 // of fewer than kGuSplitBelow row-tile chunks, else 1 (whole chunks)
 constexpr int kGuSplitBelow = 256;
 constexpr int kMmaRows = 64;     // rows (token slots) per work-group
+constexpr int kTallTileRows = 128;  // experts with this many rows take 128-row gate/up tiles
 constexpr int kMmaCols = 256;    // output columns per down work-group
 
 struct MmaTask {
@@ -198,6 +199,8 @@ struct MmaArgs {
   int32_t bits;                // 0: bf16 chunks; 2 or 4: b-bit chunks (q_chunk_bytes layout)
   int32_t ksplit;              // down, b-bit: chunk ranges per (row tile, column block), each summed
                                // into its own partial plane [row][ksplit][d]; 1 for bf16
+  int32_t tile_rows;           // rows per row tile: kMmaRows, or 2 kMmaRows for bf16 gate/up of whole
+                               // chunks (gu_split 1) of experts with at least kTallTileRows rows
   MmaTask tasks[kMaxMmaTasks];
 };
 hipError_t launch_mma_gateup(const MmaArgs& a, hipStream_t s);

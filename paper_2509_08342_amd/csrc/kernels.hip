@@ -1378,12 +1378,9 @@ static hipError_t dispatch_ffn(const FfnArgs& a, int nt, int q, int max_tok, hip
 
 // Tokens per tile: the smallest of {1, 2, 4, 8} covering max_tok, limited so
 // that the LDS tile stays within 64 KiB and the accumulators fit.
-#ifndef MSK_NT_MAX
-#define MSK_NT_MAX 8
-#endif
 static int pick_nt(int max_tok, int d, int elem, int q, int vec, int upw) {
   int nt = 1;
-  while (nt < max_tok && nt < MSK_NT_MAX) nt <<= 1;
+  while (nt < max_tok && nt < kMmaTileRows) nt <<= 1;
   while (nt > 1 &&
          (ffn_lds_bytes(nt, d, elem, upw) > 65536 ||
           !ffn_fits(nt, q, vec)))
@@ -1826,13 +1823,14 @@ struct TileRows {
 };
 __device__ __forceinline__ TileRows tile_rows(const MmaArgs& a, const MmaTask& tk, int mt) {
   TileRows r;
+  const int rows = a.tile_rows;
   if (tk.expert >= 0) {
     const int b = a.offsets[tk.expert], e = a.offsets[tk.expert + 1];
-    r.p0 = b + mt * kMmaRows;
-    r.n = min(kMmaRows, e - r.p0);
+    r.p0 = b + mt * rows;
+    r.n = min(rows, e - r.p0);
   } else {
-    r.p0 = mt * kMmaRows;
-    r.n = min(kMmaRows, a.T - r.p0);
+    r.p0 = mt * rows;
+    r.n = min(rows, a.T - r.p0);
   }
   return r;
 }
@@ -1925,17 +1923,26 @@ __global__ __launch_bounds__(256) void mma_gateup_kernel(MmaArgs a) {
   }
 }
 
-// gate/up of whole chunks: a work-group takes 64 rows x 64 units, wave w the
-// units 16 w .. 16 w + 15 for all four 16-row blocks, so every weight
-// fragment is read by one wave only.  The activation rows are staged in LDS
-// in slabs of kGuSlab k (double-buffered, rows padded so that the 16 rows a
-// fragment read touches fall in distinct banks); the next slab's rows and
-// weight fragments load while the current slab computes.
+// gate/up of whole chunks for row tiles of 16 RB rows (a.tile_rows): a
+// work-group takes 16 RB rows x 64 units, wave w the units 16 w .. 16 w + 15
+// of every 16-row block, so each weight fragment is read by one wave only.
+// The activation rows are staged in LDS in slabs of kGuSlab k (double
+// buffer, rows padded so that the 16 rows a fragment read touches fall in
+// distinct banks).  No load is waited for in the step that issues it: at
+// slab sl the work-group computes slab sl from LDS with weight fragments
+// issued two slabs earlier (three register sets in turn), stores the rows of
+// slab sl + 1 issued one slab earlier, then issues the loads of slab sl + 2.
+// The k order of every sum is the same as for any other tile height, so a
+// row's activations do not depend on the tile it was computed in.  Needs
+// d % 256 == 0 (whole slabs, an even count of them).
 constexpr int kGuSlab = 128;            // k per staged slab (4 MFMA k-steps)
 constexpr int kGuPitch = kGuSlab + 8;   // bf16 per staged row
 
-__global__ __launch_bounds__(256) void mma_gateup_lds_kernel(MmaArgs a) {
-  __shared__ __align__(16) uint16_t As[2][kMmaRows * kGuPitch];
+template <int RB>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(RB <= 4 ? 3 : 2))) void mma_gateup_rows_kernel(
+    MmaArgs a) {
+  constexpr int ROWS = 16 * RB;
+  __shared__ __align__(16) uint16_t As[2][ROWS * kGuPitch];
   const int wg = xcd_local(blockIdx.x, gridDim.x);
   const MmaTask tk = a.tasks[find_task(a.tasks, a.n_tasks, wg)];
   const int local = wg - tk.wg_begin;
@@ -1948,82 +1955,91 @@ __global__ __launch_bounds__(256) void mma_gateup_lds_kernel(MmaArgs a) {
   const int ksteps = d / 32;
   const int nslab = (ksteps + 3) / 4;
   const bool routed = tk.expert >= 0;
-  // staging: piece p = tid + 256 i of a slab is row p / 16, k 8 (p % 16)
-  const uint16_t* hrow[4];
+  // staging: piece p = tid + 256 i of a slab is row p / 16, k 8 (p % 16);
+  // rows past the tile's real ones repeat its last row (staged, never stored)
+  // (one branch for the whole tile, so that the RB slot loads are in
+  // flight together)
+  int tok[RB];
+  if (routed) {
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int row = min((tid >> 4) + 16 * i, tr.n - 1);  // clamped rows: staged, never stored
-    const int tok = routed ? a.perm[tr.p0 + row] / a.K : tr.p0 + row;
-    hrow[i] = static_cast<const uint16_t*>(a.h) + static_cast<size_t>(tok) * d + 8 * (tid & 15);
+    for (int i = 0; i < RB; ++i) tok[i] = a.perm[tr.p0 + min((tid >> 4) + 16 * i, tr.n - 1)];
+#pragma unroll
+    for (int i = 0; i < RB; ++i) tok[i] /= a.K;
+  } else {
+#pragma unroll
+    for (int i = 0; i < RB; ++i) tok[i] = tr.p0 + min((tid >> 4) + 16 * i, tr.n - 1);
   }
+  size_t hoff[RB];
+#pragma unroll
+  for (int i = 0; i < RB; ++i) hoff[i] = static_cast<size_t>(tok[i]) * d + 8 * (tid & 15);
+  const uint16_t* h = static_cast<const uint16_t*>(a.h);
   const uint16_t* G = reinterpret_cast<const uint16_t*>(tk.base + static_cast<size_t>(c) * a.chunk_bytes);
   const uint16_t* U = G + static_cast<size_t>(kChunkUnits) * d;
   const int unit = 16 * wave + (lane & 15);  // this lane's B column
   const int kq = 8 * (lane >> 4);
-  uint4 ast[4], bn[4][2], bc[4][2];
+  uint4 ast[RB];
   auto load_a = [&](int sl) {
-    const int k0 = min(sl, nslab - 1) * kGuSlab;  // clamped: the slab past the last is loaded, not used
+    const int k0 = min(min(sl, nslab - 1) * kGuSlab, d - kGuSlab);  // past the last slab: reloaded, not used
 #pragma unroll
-    for (int i = 0; i < 4; ++i) ast[i] = ld16(hrow[i] + min(k0, d - kGuSlab));
+    for (int i = 0; i < RB; ++i) ast[i] = ld16(h + hoff[i] + k0);
   };
-  // a partial last slab (d % 128 == 64) is staged from k = d - 128; the
-  // compute reads it at the matching offset
   auto store_a = [&](int buf) {
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
+    for (int i = 0; i < RB; ++i)
       *reinterpret_cast<uint4*>(&As[buf][((tid >> 4) + 16 * i) * kGuPitch + 8 * (tid & 15)]) = ast[i];
   };
-  auto load_b = [&](int sl) {
+  auto load_b = [&](int sl, uint4(&b)[4][2]) {
 #pragma unroll
     for (int s = 0; s < 4; ++s) {
       const int k = min(4 * sl + s, ksteps - 1) * 32;  // clamped past the last step
       const size_t off = (static_cast<size_t>(k / kKTile) * kChunkUnits + unit) * kKTile + (k % kKTile) + kq;
-      bn[s][0] = ldw16(G + off);
-      bn[s][1] = ldw16(U + off);
+      b[s][0] = ldw16(G + off);
+      b[s][1] = ldw16(U + off);
     }
   };
-  f32x4_t ag[4], au[4];
+  f32x4_t ag[RB], au[RB];
 #pragma unroll
-  for (int rb = 0; rb < 4; ++rb) ag[rb] = au[rb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  for (int rb = 0; rb < RB; ++rb) ag[rb] = au[rb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  uint4 b0[4][2], b1[4][2];
   load_a(0);
-  load_b(0);
+  load_b(0, b0);
   store_a(0);
+  load_a(1);
+  load_b(1, b1);
   __syncthreads();
-  for (int sl = 0; sl < nslab; ++sl) {
+  // one slab: compute sl with b (which then takes slab sl + 2), stage
+  // sl + 1.  Every row block is computed, also past the tile's real rows
+  // (their results are not stored): a branch per block would make the
+  // compiler wait for every load in flight at each of them.
+  auto slab = [&](int sl, uint4(&b)[4][2]) {
     const int buf = sl & 1;
 #pragma unroll
     for (int s = 0; s < 4; ++s) {
-      bc[s][0] = bn[s][0];
-      bc[s][1] = bn[s][1];
-    }
-    load_a(sl + 1);
-    load_b(sl + 1);
-    // the slab's first k inside the staged rows (a partial last slab sits at
-    // the end of its 128-wide window)
-    const int k0 = sl * kGuSlab, kbase = k0 - min(k0, d - kGuSlab);
+      bf16x8_t A[RB];
 #pragma unroll
-    for (int s = 0; s < 4; ++s) {
-      if (4 * sl + s < ksteps) {
+      for (int rb = 0; rb < RB; ++rb)
+        A[rb] = as_bf16x8(
+            *reinterpret_cast<const uint4*>(&As[buf][(16 * rb + (lane & 15)) * kGuPitch + 32 * s + kq]));
 #pragma unroll
-        for (int rb = 0; rb < 4; ++rb) {
-          if (16 * rb < tr.n) {
-            const uint4 av =
-                *reinterpret_cast<const uint4*>(&As[buf][(16 * rb + (lane & 15)) * kGuPitch + kbase + 32 * s + kq]);
-            const bf16x8_t A = as_bf16x8(av);
-            ag[rb] = mfma16(A, as_bf16x8(bc[s][0]), ag[rb]);
-            au[rb] = mfma16(A, as_bf16x8(bc[s][1]), au[rb]);
-          }
-        }
+      for (int rb = 0; rb < RB; ++rb) {
+        ag[rb] = mfma16(A[rb], as_bf16x8(b[s][0]), ag[rb]);
+        au[rb] = mfma16(A[rb], as_bf16x8(b[s][1]), au[rb]);
       }
     }
-    if (sl + 1 < nslab) store_a(buf ^ 1);
+    store_a(buf ^ 1);  // after the last slab: the clamped reload, never read
+    load_a(sl + 2);
+    load_b(sl + 2, b);
     __syncthreads();
+  };
+  for (int sl = 0; sl < nslab; sl += 2) {  // nslab is even (d % 256 == 0)
+    slab(sl, b0);
+    slab(sl + 1, b1);
   }
   uint16_t* act = routed ? a.act : a.act_sh + static_cast<size_t>(-1 - tk.expert) * a.rows_shared * a.f_pad_sh;
   const int f_pad = routed ? a.f_pad : a.f_pad_sh;
   const int f = c * kChunkUnits + unit;
 #pragma unroll
-  for (int rb = 0; rb < 4; ++rb) {
+  for (int rb = 0; rb < RB; ++rb) {
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
       const int row = 16 * rb + 4 * (lane >> 4) + r;
@@ -2414,9 +2430,11 @@ hipError_t launch_mma_gateup(const MmaArgs& a, hipStream_t s) {
   }
   if (a.gu_split == 4)
     hipLaunchKernelGGL(mma_gateup_kernel<1>, dim3(a.n_wg), dim3(256), kGuardLds, s, a);
-  else if (a.gu_split == 1 && a.d >= kGuSlab)
-    hipLaunchKernelGGL(mma_gateup_lds_kernel, dim3(a.n_wg), dim3(256), 0, s, a);
-  else if (a.gu_split == 1)
+  else if (a.gu_split == 1 && a.d % (2 * kGuSlab) == 0 && a.tile_rows == 2 * kMmaRows)
+    hipLaunchKernelGGL(mma_gateup_rows_kernel<8>, dim3(a.n_wg), dim3(256), 0, s, a);
+  else if (a.gu_split == 1 && a.d % (2 * kGuSlab) == 0 && a.tile_rows == kMmaRows)
+    hipLaunchKernelGGL(mma_gateup_rows_kernel<4>, dim3(a.n_wg), dim3(256), 0, s, a);
+  else if (a.gu_split == 1 && a.tile_rows == kMmaRows)
     hipLaunchKernelGGL(mma_gateup_kernel<4>, dim3(a.n_wg), dim3(256), kGuardLds, s, a);
   else
     return hipErrorInvalidValue;

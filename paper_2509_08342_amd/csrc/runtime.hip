@@ -938,13 +938,16 @@ ms_status prefill_experts(ms_ctx* ctx, int layer, const void* h_dev, int T, cons
   auto shared_base = [&](int i) {
     return ctx->dev(s.off_shared + align_up(s.shared_bytes, kAlign) * (static_cast<uint64_t>(layer) * s.n_sh + i));
   };
-  auto launch = [&](const std::vector<msk::MmaTask>& tasks, hipStream_t st, bool down) -> ms_status {
+  auto rows_of = [&](int e) { return e >= 0 ? offs[e + 1] - offs[e] : T; };
+  auto launch_group = [&](const std::vector<msk::MmaTask>& tasks, hipStream_t st, bool down,
+                          int tile_rows) -> ms_status {
+    ma.tile_rows = tile_rows;
     for (size_t i0 = 0; i0 < tasks.size(); i0 += msk::kMaxMmaTasks) {
       const size_t i1 = std::min(tasks.size(), i0 + msk::kMaxMmaTasks);
       ma.n_tasks = static_cast<int>(i1 - i0);
       int tiles = 0;
       for (size_t i = i0; i < i1; ++i) tiles += tasks[i].m_tiles * tasks[i].n_chunks;
-      ma.gu_split = (tiles < msk::kGuSplitBelow && s.bits == 0) ? 4 : 1;
+      ma.gu_split = (tile_rows == msk::kMmaRows && tiles < msk::kGuSplitBelow && s.bits == 0) ? 4 : 1;
       int wg = 0;
       uint64_t bytes = 0;
       for (size_t i = i0; i < i1; ++i) {
@@ -960,6 +963,29 @@ ms_status prefill_experts(ms_ctx* ctx, int layer, const void* h_dev, int T, cons
       tl_end(ctx, id, st);
     }
     return MS_OK;
+  };
+  // bf16 gate/up: experts with many rows take 128-row tiles (each weight
+  // fragment then feeds twice the rows) when those tiles still fill the GPU;
+  // the rest keep 64-row tiles.  The tile height changes no result.
+  auto launch = [&](const std::vector<msk::MmaTask>& tasks, hipStream_t st, bool down) -> ms_status {
+    if (down || s.bits != 0 || s.d % 256 != 0) return launch_group(tasks, st, down, msk::kMmaRows);
+    std::vector<msk::MmaTask> tall, rest;
+    int tall_tiles = 0;
+    for (const msk::MmaTask& t : tasks) {
+      const int n = rows_of(t.expert);
+      if (n >= msk::kTallTileRows) {
+        msk::MmaTask t2 = t;
+        t2.m_tiles = (n + msk::kTallTileRows - 1) / msk::kTallTileRows;
+        tall_tiles += t2.m_tiles * t2.n_chunks;
+        tall.push_back(t2);
+      } else {
+        rest.push_back(t);
+      }
+    }
+    if (tall_tiles < msk::kGuSplitBelow) return launch_group(tasks, st, false, msk::kMmaRows);
+    ms_status r = launch_group(tall, st, false, msk::kTallTileRows);
+    if (r != MS_OK || rest.empty()) return r;
+    return launch_group(rest, st, false, msk::kMmaRows);
   };
   auto task = [](const unsigned char* base, const unsigned char* base2, int e, int lo, int n, int split, int mt) {
     msk::MmaTask t{};
