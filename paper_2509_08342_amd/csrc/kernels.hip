@@ -190,20 +190,28 @@ __device__ __forceinline__ void pred_add(const float* lg, int E, int lane, float
 }
 
 // Ranks score_s (LDS, E values) and stores order / score (and their host-
-// visible copies); threads tid < E of a work-group of NT threads.
+// visible copies), by a work-group of NT threads (whole waves): one wave per
+// expert, its lanes comparing against experts lane, lane + 64, ..., the
+// counts summed by a butterfly.  rank(e) = #{o : s_o > s_e or (s_o == s_e
+// and o < e)}, so equal scores keep the lower index first.
 __device__ __forceinline__ void rank_scores(const float* score_s, const RouteArgs& a, int tid, int NT) {
   const int E = a.E;
-  for (int e = tid; e < E; e += NT) {
+  const int lane = tid & 63, wave = tid >> 6, nw = NT >> 6;
+  for (int e = wave; e < E; e += nw) {
     const float v = score_s[e];
     int r = 0;
-    for (int o = 0; o < E; ++o) {
+    for (int o = lane; o < E; o += 64) {
       const float u = score_s[o];
       r += (u > v) || (u == v && o < e);
     }
-    a.order[r] = e;
-    a.score[e] = v;
-    if (a.host_order) a.host_order[r] = e;
-    if (a.host_score) a.host_score[e] = v;
+#pragma unroll
+    for (int s = 32; s >= 1; s >>= 1) r += __shfl_xor(r, s, 64);
+    if (lane == 0) {
+      a.order[r] = e;
+      a.score[e] = v;
+      if (a.host_order) a.host_order[r] = e;
+      if (a.host_score) a.host_score[e] = v;
+    }
   }
 }
 
