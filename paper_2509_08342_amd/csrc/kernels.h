@@ -131,7 +131,8 @@ struct FfnArgs {
 };
 static_assert(sizeof(FfnTaskK) == 16, "task records are 16 bytes");
 static_assert(sizeof(FfnArgs) <= 3400, "FFN kernel arguments within the size other launches use");
-// Launches n_wg work-groups; max_tok bounds the tokens of any task.
+// Launches n_wg work-groups; max_tok must be at least the token count of
+// every task (tokens past the launch's tiles are not computed).
 hipError_t launch_ffn(const FfnArgs& a, int max_tok, hipStream_t s);
 
 // Chunks of b-bit experts (FfnArgs::bits = 2 or 4): affine codes with one

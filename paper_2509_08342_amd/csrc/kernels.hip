@@ -1087,44 +1087,90 @@ __device__ __forceinline__ void ffn_tile(const FfnArgs& a, const W* G, const W* 
   __syncthreads();
 }
 
-// Tiles of 8 bf16 rows: the gate/up dot products run on the matrix cores
-// (v_mfma_f32_16x16x32_bf16; with 8 rows the fma chains of ffn_tile cost
-// more VALU time than the tile's weights take to stream).  A = the tile's
-// rows (rows 8-15 zero), B = 16 units: lane l holds row / unit l % 16 and
-// the 8 k values 8 (l / 16) + [0, 8) of a 32-wide k block, taken for both
-// operands at the same offsets of the chunk's k-tiled rows.  Wave w works on
-// unit block w % NB over every other 64-wide k piece from w / NB; the two k
-// halves are added in LDS (first half + second half), then the SwiGLU
-// product.  The down projection is ffn_tile's.  The activation rows are
-// staged with a pitch of d + kHsPad elements so that the 8 rows' A
-// fragments fall in different LDS banks.  Which path a tile takes depends
-// only on its row count, so a token's partial is the same in every launch.
-constexpr int kMmaTileRows = 8;
-constexpr int kHsPad = 8;
+// Tiles of 5 to 16 bf16 rows run on the matrix cores in both phases
+// (v_mfma_f32_16x16x32_bf16; A = the tile's rows, the last real row repeated
+// past nt, whose results are never stored):
+//   phase 1: B = 16 units of the chunk's k-tiled G and U rows: lane l holds
+//            unit / row l % 16 and the 8 k values 8 (l / 16) + [0, 8) of a
+//            32-wide k block, the A fragments loaded straight from the
+//            activation rows (shared by every work-group of the expert, so
+//            they come from L2).  Wave w works on unit block w % NB over every
+//            other 64-wide k piece from w / NB; the sums over the even and
+//            the odd pieces are added in LDS (even + odd), then the SwiGLU
+//            product a[t][f] (fp32, LDS).
+//   phase 2: y[t][col] = sum_f a[t][f] D[f][col], contracted over f in steps
+//            of 32 units.  Lane (n, g) loads down rows 8 g .. 8 g + 7 of the
+//            step at columns 8 n .. 8 n + 7 of a 128-column block (eight
+//            16-byte pieces, 256 contiguous bytes per row and 16 lanes),
+//            transposes them in registers into eight B fragments (column
+//            8 n + j, j = 0..7) and runs one MFMA per fragment, so that its
+//            results are rows 4 g .. 4 g + 3 of columns 8 n .. 8 n + 7.  a
+//            enters as the bf16 pair hi + lo (hi = a rounded to bf16, lo = the
+//            remainder rounded to bf16; both products are exact in fp32), so
+//            16 bits of a's mantissa reach the sums.  Wave w takes the column
+//            blocks w, w + waves, ...; with 16 units per work-group the step
+//            is half full and its other half is zero.
+// Every row's weights are read once per tile, whatever its height up to 16.
+// Which path a tile takes depends only on its row count, so a token's
+// partial is the same in every launch.
+constexpr int kMmaTileRows = 16;
+constexpr int kDnCols = 128;  // columns of one phase-2 block: 16 lanes x 8
 
-// LDS of an FFN launch: activation tile, SwiGLU tile, and for 8-row bf16
-// tiles the k-half exchange.
-__host__ __device__ constexpr size_t ffn_lds_bytes(int nt, int d, int elem, int upw) {
-  return (nt == kMmaTileRows && elem == 2)
-             ? static_cast<size_t>(nt) * (d + kHsPad) * elem + sizeof(float) * nt * upw + (upw / 16) * 32 * 8 * sizeof(float)
-             : static_cast<size_t>(nt) * d * elem + sizeof(float) * nt * upw;
+__device__ __forceinline__ float bf2f(uint16_t b) { return __uint_as_float(static_cast<uint32_t>(b) << 16); }
+
+// fp32 -> bf16, round to nearest even (finite values)
+__device__ __forceinline__ uint16_t f2bf(float f) {
+  const uint32_t u = __float_as_uint(f);
+  return static_cast<uint16_t>((u + 0x7fffu + ((u >> 16) & 1u)) >> 16);
 }
 
-template <int Q, int UPW, int RB>
+// Eight rows of eight bf16 (one 16-byte piece each) -> eight column
+// fragments: frag[j] = element j of rows 0 .. 7, in row order (v_perm_b32
+// picks the low or high half of word j / 2 of two rows at a time).
+__device__ __forceinline__ void transpose8x8(const uint4 (&rows)[8], uint4 (&frag)[8]) {
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    const uint32_t sel = (j & 1) ? 0x07060302u : 0x05040100u;
+    uint32_t w[8];
+#pragma unroll
+    for (int r = 0; r < 8; ++r) {
+      const uint4 v = rows[r];
+      w[r] = (j >> 1) == 0 ? v.x : (j >> 1) == 1 ? v.y : (j >> 1) == 2 ? v.z : v.w;
+    }
+    frag[j] = make_uint4(__builtin_amdgcn_perm(w[1], w[0], sel), __builtin_amdgcn_perm(w[3], w[2], sel),
+                         __builtin_amdgcn_perm(w[5], w[4], sel), __builtin_amdgcn_perm(w[7], w[6], sel));
+  }
+}
+
+// LDS of an FFN launch of NT-row tiles.  fma-chain tiles: activation rows
+// [nt][d] and SwiGLU values [nt][upw].  Launches of kMmaTileRows bf16 rows
+// run tiles of up to 4 rows on fma chains and larger ones on the matrix
+// cores (SwiGLU values [16][upw] and the even/odd k exchange, 8 floats per
+// lane of each unit block).
+__host__ __device__ constexpr size_t ffn_lds_fma(int nt, int d, int elem, int upw) {
+  return static_cast<size_t>(nt) * d * elem + sizeof(float) * nt * upw;
+}
+__host__ __device__ constexpr size_t ffn_lds_mma(int upw) {
+  return sizeof(float) * (static_cast<size_t>(kMmaTileRows) * upw + (upw / 16) * 64 * 8);
+}
+__host__ __device__ constexpr size_t ffn_lds_bytes(int nt, int d, int elem, int upw) {
+  return (nt == kMmaTileRows && elem == 2)
+             ? (ffn_lds_fma(4, d, elem, upw) > ffn_lds_mma(upw) ? ffn_lds_fma(4, d, elem, upw) : ffn_lds_mma(upw))
+             : ffn_lds_fma(nt, d, elem, upw);
+}
+
+template <int UPW>
 __device__ __forceinline__ void ffn_tile_mma(const FfnArgs& a, const uint16_t* G, const uint16_t* U,
                                              const uint16_t* D, float* part, int a_planes, int plane, bool routed,
-                                             int p0, int tile, int nt, uint16_t* hs, float* as, float* red, int sub) {
+                                             int p0, int tile, int nt, float* as, float* red, int sub) {
   using W = uint16_t;
-  constexpr int VEC = 8;
-  constexpr int NTT = kMmaTileRows;
   constexpr int THREADS = UPW * kLpu;
-  constexpr int NB = UPW / 16;  // unit blocks; 2 NB waves
-  constexpr int KB = 2;         // k pieces per load batch
-  constexpr int PB = (RB < 16 / Q) ? RB : 16 / Q;
-  static_assert(THREADS == 128 * NB, "two waves per unit block");
+  constexpr int NWV = THREADS / 64;  // waves
+  constexpr int NB = UPW / 16;       // unit blocks, two waves each
+  constexpr int KB = 2;              // k pieces per phase-1 load batch
+  constexpr int S = (UPW + 31) / 32;  // 32-unit steps of phase 2
+  static_assert(NWV == 2 * NB, "two waves per unit block");
   const int d = a.d;
-  const int pitch = d + kHsPad;
-  const W* hsrc = static_cast<const W*>(a.h);
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int ub = wave % NB, kh = wave / NB;
   const int n = lane & 15, g = lane >> 4;
@@ -1132,8 +1178,17 @@ __device__ __forceinline__ void ffn_tile_mma(const FfnArgs& a, const uint16_t* G
   const int f_first = sub * UPW;
   const int n_kt = d / kKTile;
   const int npw = (n_kt - kh + 1) / 2;  // k pieces of this wave: kh, kh + 2, ...
+  const int ncb = (d + kDnCols - 1) / kDnCols;
+  const int nblk = wave < ncb ? (ncb - 1 - wave) / NWV + 1 : 0;  // column blocks of this wave
+  // lanes g >= 2 pad a half step (16 units per work-group) with zeros
+  const bool k_live = UPW >= 32 || g < 2;
 
-  auto load_b = [&](int i0, uint4(&bg)[KB][2], uint4(&bu)[KB][2]) {
+  // this lane's A row: tile row n, the last real row past nt
+  const int ar = min(n, nt - 1);
+  const int tok = routed ? a.perm[p0 + tile + ar] / a.K : tile + ar;
+  const W* hrow = static_cast<const W*>(a.h) + static_cast<size_t>(tok) * d + g * 8;
+
+  auto load_b = [&](int i0, uint4(&ba)[KB][2], uint4(&bg)[KB][2], uint4(&bu)[KB][2]) {
 #pragma unroll
     for (int i = 0; i < KB; ++i) {
       // clamped (also when this wave has no piece, d = 64); used only in range
@@ -1141,68 +1196,51 @@ __device__ __forceinline__ void ffn_tile_mma(const FfnArgs& a, const uint16_t* G
       const size_t off = (static_cast<size_t>(kt) * kChunkUnits + unit) * kKTile + g * 8;
 #pragma unroll
       for (int j = 0; j < 2; ++j) {
+        ba[i][j] = ld16(hrow + kt * kKTile + 32 * j);
         bg[i][j] = ldw16(G + off + 32 * j);
         bu[i][j] = ldw16(U + off + 32 * j);
       }
     }
   };
-  auto load_rows = [&](int f0, uint4(&dd)[PB][Q]) {
+  // phase-2 down rows of column block bi (of this wave) and step s
+  auto load_d = [&](int bi, int s, uint4(&dd)[8]) {
+    const int col = min((wave + NWV * bi) * kDnCols + 8 * n, d - 8);  // clamped; stored only if in range
+    const W* src = D + static_cast<size_t>(f_first + 32 * s + 8 * g) * d + col;
 #pragma unroll
-    for (int u = 0; u < PB; ++u)
-#pragma unroll
-      for (int q = 0; q < Q; ++q) {
-        const int col = min((tid + THREADS * q) * VEC, d - VEC);  // clamped; used only if in range
-        dd[u][q] = ldw16(D + static_cast<size_t>(f_first + min(f0 + u, UPW - 1)) * d + col);
-      }
+    for (int r = 0; r < 8; ++r) dd[r] = k_live ? ldw16(src + static_cast<size_t>(r) * d) : make_uint4(0, 0, 0, 0);
   };
 
-  uint4 bgn[KB][2], bun[KB][2];
-  load_b(0, bgn, bun);
-  // stage the tile's rows (zero past nt), pitch d + kHsPad
-  const int vec_per_row = d / VEC;
-  for (int i = tid; i < NTT * vec_per_row; i += THREADS) {
-    const int t = i / vec_per_row, k = (i - t * vec_per_row) * VEC;
-    uint4 v = make_uint4(0, 0, 0, 0);
-    if (t < nt) {
-      const int tok = routed ? a.perm[p0 + tile + t] / a.K : tile + t;
-      v = ld16(hsrc + static_cast<size_t>(tok) * d + k);
-    }
-    *reinterpret_cast<uint4*>(hs + static_cast<size_t>(t) * pitch + k) = v;
-  }
-  __syncthreads();
-
-  uint4 dn[PB][Q];
+  uint4 dn[8];
   {
     f32x4_t cg = {0.0f, 0.0f, 0.0f, 0.0f}, cu = {0.0f, 0.0f, 0.0f, 0.0f};
-    uint4 bgr[KB][2], bur[KB][2];
+    uint4 ban[KB][2], bgn[KB][2], bun[KB][2];
+    load_b(0, ban, bgn, bun);
     for (int i0 = 0; i0 < npw; i0 += KB) {
+      uint4 bar[KB][2], bgr[KB][2], bur[KB][2];
 #pragma unroll
       for (int i = 0; i < KB; ++i)
 #pragma unroll
         for (int j = 0; j < 2; ++j) {
+          bar[i][j] = ban[i][j];
           bgr[i][j] = bgn[i][j];
           bur[i][j] = bun[i][j];
         }
-      load_b(i0 + KB, bgn, bun);
+      load_b(i0 + KB, ban, bgn, bun);
 #pragma unroll
       for (int i = 0; i < KB; ++i) {
         if (i0 + i < npw) {
-          const int kt = kh + 2 * (i0 + i);
 #pragma unroll
           for (int j = 0; j < 2; ++j) {
-            uint4 av = make_uint4(0, 0, 0, 0);
-            if (n < NTT) av = ld16(hs + static_cast<size_t>(n) * pitch + kt * kKTile + 32 * j + g * 8);
-            cg = mfma16(as_bf16x8(av), as_bf16x8(bgr[i][j]), cg);
-            cu = mfma16(as_bf16x8(av), as_bf16x8(bur[i][j]), cu);
+            cg = mfma16(as_bf16x8(bar[i][j]), as_bf16x8(bgr[i][j]), cg);
+            cu = mfma16(as_bf16x8(bar[i][j]), as_bf16x8(bur[i][j]), cu);
           }
         }
       }
     }
     // the first down rows are requested before the k halves meet
-    load_rows(0, dn);
-    // lanes g < 2 hold rows 4 g + r < 8
-    if (kh == 1 && g < 2) {
-      float* r = red + (static_cast<size_t>(ub) * 32 + lane) * 8;
+    if (nblk > 0) load_d(0, 0, dn);
+    if (kh == 1) {
+      float* r = red + (static_cast<size_t>(ub) * 64 + lane) * 8;
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         r[i] = cg[i];
@@ -1210,8 +1248,8 @@ __device__ __forceinline__ void ffn_tile_mma(const FfnArgs& a, const uint16_t* G
       }
     }
     __syncthreads();
-    if (kh == 0 && g < 2) {
-      const float* r = red + (static_cast<size_t>(ub) * 32 + lane) * 8;
+    if (kh == 0) {
+      const float* r = red + (static_cast<size_t>(ub) * 64 + lane) * 8;
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const float sg = cg[i] + r[i], su = cu[i] + r[4 + i];
@@ -1221,55 +1259,59 @@ __device__ __forceinline__ void ffn_tile_mma(const FfnArgs& a, const uint16_t* G
   }
   __syncthreads();
 
-  // phase 2 as in ffn_tile
-  {
-    float y[NTT][Q][VEC];
+  // phase 2: A fragments (row n, units 32 s + 8 g + [0, 8)) as hi / lo bf16
+  bf16x8_t ahi[S], alo[S];
 #pragma unroll
-    for (int t = 0; t < NTT; ++t)
+  for (int s = 0; s < S; ++s) {
+    uint32_t hw[4] = {0u, 0u, 0u, 0u}, lw[4] = {0u, 0u, 0u, 0u};
+    if (k_live) {
+      const float* src = as + n * UPW + 32 * s + 8 * g;
 #pragma unroll
-      for (int q = 0; q < Q; ++q)
-#pragma unroll
-        for (int i = 0; i < VEC; ++i) y[t][q][i] = 0.0f;
-    uint4 dr[PB][Q];
-    for (int f0 = 0; f0 < UPW; f0 += PB) {
-#pragma unroll
-      for (int u = 0; u < PB; ++u)
-#pragma unroll
-        for (int q = 0; q < Q; ++q) dr[u][q] = dn[u][q];
-      load_rows(f0 + PB, dn);
-#pragma unroll
-      for (int u = 0; u < PB; ++u) {
-        float av[NTT];
-#pragma unroll
-        for (int t = 0; t < NTT; ++t) av[t] = as[t * UPW + f0 + u];
-#pragma unroll
-        for (int q = 0; q < Q; ++q) {
-          const int col = (tid + THREADS * q) * VEC;
-          if (col < d) {
-            float dv[VEC];
-            unpack(dr[u][q], dv);
-#pragma unroll
-            for (int t = 0; t < NTT; ++t)
-#pragma unroll
-              for (int i = 0; i < VEC; ++i) y[t][q][i] = fmaf(av[t], dv[i], y[t][q][i]);
-          }
-        }
+      for (int i = 0; i < 8; ++i) {
+        const float v = src[i];
+        const uint16_t hb = f2bf(v);
+        const float hf = bf2f(hb);
+        const uint16_t lb = isfinite(hf) ? f2bf(v - hf) : static_cast<uint16_t>(0);
+        hw[i >> 1] |= static_cast<uint32_t>(hb) << (16 * (i & 1));
+        lw[i >> 1] |= static_cast<uint32_t>(lb) << (16 * (i & 1));
       }
     }
+    ahi[s] = as_bf16x8(make_uint4(hw[0], hw[1], hw[2], hw[3]));
+    alo[s] = as_bf16x8(make_uint4(lw[0], lw[1], lw[2], lw[3]));
+  }
+  for (int bi = 0; bi < nblk; ++bi) {
+    f32x4_t acc[8];
 #pragma unroll
-    for (int t = 0; t < NTT; ++t) {
-      if (t < nt) {
-        const int row = routed ? (p0 + tile + t) : (tile + t);
-        float* dst = part + (static_cast<size_t>(row) * a_planes + plane) * d;
+    for (int j = 0; j < 8; ++j) acc[j] = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
-        for (int q = 0; q < Q; ++q) {
-          const int col = (tid + THREADS * q) * VEC;
-          if (col < d) {
+    for (int s = 0; s < S; ++s) {
+      uint4 dr[8];
 #pragma unroll
-            for (int i = 0; i < VEC; i += 4)
-              *reinterpret_cast<float4*>(dst + col + i) =
-                  make_float4(y[t][q][i], y[t][q][i + 1], y[t][q][i + 2], y[t][q][i + 3]);
-          }
+      for (int r = 0; r < 8; ++r) dr[r] = dn[r];
+      // next: the block's next step, else the next block's first (the last
+      // block reloads its own: in bounds, unused)
+      if (s + 1 < S)
+        load_d(bi, s + 1, dn);
+      else
+        load_d(min(bi + 1, nblk - 1), 0, dn);
+      uint4 frag[8];
+      transpose8x8(dr, frag);
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        acc[j] = mfma16(ahi[s], as_bf16x8(frag[j]), acc[j]);
+        acc[j] = mfma16(alo[s], as_bf16x8(frag[j]), acc[j]);
+      }
+    }
+    const int c0 = (wave + NWV * bi) * kDnCols + 8 * n;
+    if (c0 < d) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int t = 4 * g + i;
+        if (t < nt) {
+          const int row = routed ? (p0 + tile + t) : (tile + t);
+          float* dst = part + (static_cast<size_t>(row) * a_planes + plane) * d + c0;
+          *reinterpret_cast<float4*>(dst) = make_float4(acc[0][i], acc[1][i], acc[2][i], acc[3][i]);
+          *reinterpret_cast<float4*>(dst + 4) = make_float4(acc[4][i], acc[5][i], acc[6][i], acc[7][i]);
         }
       }
     }
@@ -1278,8 +1320,8 @@ __device__ __forceinline__ void ffn_tile_mma(const FfnArgs& a, const uint16_t* G
 }
 
 // Grid: n_wg x n_tiles work-groups; block b computes token tile b % n_tiles
-// (and every n_tiles-th tile after it) of work-group slot b / n_tiles, so the
-// tiles of an expert with many tokens run side by side.  The tile shape
+// of work-group slot b / n_tiles, so the tiles of an expert with many tokens
+// run side by side.  The tile shape
 // follows the tile's real token count (1, 2, 4 or NT rows), read on the
 // device, so launches enqueued before the routing is known waste no
 // arithmetic on empty rows.
@@ -1298,7 +1340,6 @@ __global__ __launch_bounds__(UPW * kLpu) void ffn_chunk_kernel(FfnArgs a, int n_
     p0 = a.offsets[tk.expert];
     n_tok = a.offsets[tk.expert + 1] - p0;
   }
-  if (tile0 * NT >= n_tok) return;
 
   const size_t cd = static_cast<size_t>(kChunkUnits) * a.d;
   const W* G = reinterpret_cast<const W*>(tk.base + static_cast<size_t>(c) * a.chunk_bytes);
@@ -1310,42 +1351,54 @@ __global__ __launch_bounds__(UPW * kLpu) void ffn_chunk_kernel(FfnArgs a, int n_
   const int plane = c * a.subs + sub;
 
   constexpr bool kMma = (NT == kMmaTileRows && sizeof(W) == 2);
-  const int hs_pitch = kMma ? a.d + kHsPad : a.d;
-  W* hs = reinterpret_cast<W*>(ffn_smem);                                       // [NT][hs_pitch]
-  float* as = reinterpret_cast<float*>(ffn_smem + sizeof(W) * NT * hs_pitch);  // [NT][UPW]
-  float* red = as + NT * UPW;                                                   // k-half exchange (kMma)
+  // fma-chain tiles of NTT rows: activation rows [NTT][d], SwiGLU values
+  // after them; matrix-core tiles: SwiGLU values [16][UPW], k exchange after
+  W* hs = reinterpret_cast<W*>(ffn_smem);
+  auto as_of = [&](int ntt) { return reinterpret_cast<float*>(ffn_smem + sizeof(W) * ntt * a.d); };
 
-  // one tile per work-group (max_tok bounds every task's token count);
-  // later tiles only if it did not
+  // one tile per work-group: the launch's n_tiles * NT rows cover every
+  // task's tokens (max_tok bounds them)
   const int tile = tile0 * NT;
-  const int nt = min(NT, n_tok - tile);
-#define MSK_FFN_TILE(NTT, T0, N) ffn_tile<W, NTT, Q, UPW, RB>(a, G, U, D, part, a_planes, plane, routed, p0, T0, N, hs, as, sub)
-#define MSK_FFN_FULL(T0, N)                                                                                   \
-  do {                                                                                                        \
-    if constexpr (kMma)                                                                                       \
-      ffn_tile_mma<Q, UPW, RB>(a, reinterpret_cast<const uint16_t*>(G), reinterpret_cast<const uint16_t*>(U), \
-                               reinterpret_cast<const uint16_t*>(D), part, a_planes, plane, routed, p0, T0, N,  \
-                               reinterpret_cast<uint16_t*>(hs), as, red, sub);                                \
-    else                                                                                                      \
-      MSK_FFN_TILE(NT, T0, N);                                                                                \
-  } while (0)
-  if (NT >= 4 && nt == 1) {
-    MSK_FFN_TILE((NT >= 4 ? 1 : NT), tile, nt);
-  } else if (NT >= 8 && nt <= 2) {
-    MSK_FFN_TILE((NT >= 8 ? 2 : NT), tile, nt);
-  } else if (NT >= 8 && nt <= 4) {
-    MSK_FFN_TILE((NT >= 8 ? 4 : NT), tile, nt);
-  } else {
-    MSK_FFN_FULL(tile, nt);
-  }
-  for (int t2 = tile + NT * n_tiles; t2 < n_tok; t2 += NT * n_tiles) MSK_FFN_FULL(t2, min(NT, n_tok - t2));
-#undef MSK_FFN_FULL
+  if (tile >= n_tok) return;
+  {
+    const int nt = min(NT, n_tok - tile);
+#define MSK_FFN_TILE(NTT) ffn_tile<W, NTT, Q, UPW, RB>(a, G, U, D, part, a_planes, plane, routed, p0, tile, nt, hs, as_of(NTT), sub)
+    if (NT >= 4 && nt == 1) {
+      MSK_FFN_TILE((NT >= 4 ? 1 : NT));
+    } else if (NT >= 8 && nt <= 2) {
+      MSK_FFN_TILE((NT >= 8 ? 2 : NT));
+    } else if (NT >= 8 && nt <= 4) {
+      MSK_FFN_TILE((NT >= 8 ? 4 : NT));
+    } else if constexpr (kMma) {
+      float* as = reinterpret_cast<float*>(ffn_smem);
+      ffn_tile_mma<UPW>(a, reinterpret_cast<const uint16_t*>(G), reinterpret_cast<const uint16_t*>(U),
+                        reinterpret_cast<const uint16_t*>(D), part, a_planes, plane, routed, p0, tile, nt, as,
+                        as + kMmaTileRows * UPW, sub);
+    } else {
+      MSK_FFN_TILE(NT);
+    }
 #undef MSK_FFN_TILE
+  }
 }
+
+// At most kFfnWavesPerCu waves of one FFN launch share a CU: each
+// work-group streams its own weight slice once, and more concurrent streams
+// per CU made the launch slower.  Measured with every expert resident, from
+// the register-limited occupancy down to 8 waves per CU: DeepSeek-V2-Lite-
+// shaped decode 38 -> 30 us (10 -> 4 two-wave work-groups per CU; 6 or more
+// were slow), Qwen3-shaped batch 16 63 -> 62 us (2 four-wave work-groups),
+// Mixtral-shaped 125 -> 123 us (one eight-wave work-group).  A launch asks
+// for LDS (kLdsPerCu per CU) of 1 / (n + 1/2) of the CU for n work-groups,
+// so that n fit and n + 1 do not whatever the allocation granule (up to
+// 2 KiB).
+constexpr int kFfnWavesPerCu = 8;
+constexpr size_t kLdsPerCu = 160 * 1024;
 
 template <typename W, int NT, int Q, int UPW>
 static hipError_t launch_ffn_one(const FfnArgs& a, int max_tok, hipStream_t s) {
-  const size_t lds = ffn_lds_bytes(NT, a.d, static_cast<int>(sizeof(W)), UPW);
+  size_t lds = ffn_lds_bytes(NT, a.d, static_cast<int>(sizeof(W)), UPW);
+  constexpr int kWgPerCu = kFfnWavesPerCu / (UPW * kLpu / 64);
+  if constexpr (kWgPerCu >= 1) lds = std::max(lds, (2 * kLdsPerCu / (2 * kWgPerCu + 1)) & ~size_t{511});
   const int n_tiles = max(1, (max_tok + NT - 1) / NT);
   const int64_t grid = static_cast<int64_t>(a.n_wg) * n_tiles;
   if (grid > 0x7fffffff) return hipErrorInvalidValue;
@@ -1363,8 +1416,12 @@ static hipError_t launch_ffn_one(const FfnArgs& a, int max_tok, hipStream_t s) {
   return hipGetLastError();
 }
 
-// Accumulators the kernel can hold beside its pipelined loads.
-constexpr bool ffn_fits(int nt, int q, int vec) { return nt * q * vec <= (q >= 4 ? 32 : 64); }
+// Accumulators the kernel can hold beside its pipelined loads: those of the
+// largest fma-chain tile (4 rows in a launch of matrix-core tiles, whose own
+// registers do not depend on the tile height or the column passes).
+constexpr bool ffn_fits(int nt, int q, int vec) {
+  return (nt == kMmaTileRows && vec == 8) ? ffn_fits(4, q, vec) : nt * q * vec <= (q >= 4 ? 32 : 64);
+}
 
 // Only the (NT, Q) pairs whose accumulators fit exist.
 template <typename W, int UPW>
@@ -1376,23 +1433,32 @@ static hipError_t dispatch_ffn(const FfnArgs& a, int nt, int q, int max_tok, hip
     if constexpr (ffn_fits(NT_, Q_, V) && (Q_ == 1 || UPW * kLpu * V * (Q_ / 2) < kMaxModelDim))  \
       return launch_ffn_one<W, NT_, Q_, UPW>(a, max_tok, s);                                     \
   }
-  MSK_FFN_CASE(1, 1) MSK_FFN_CASE(2, 1) MSK_FFN_CASE(4, 1) MSK_FFN_CASE(8, 1)
-  MSK_FFN_CASE(1, 2) MSK_FFN_CASE(2, 2) MSK_FFN_CASE(4, 2) MSK_FFN_CASE(8, 2)
-  MSK_FFN_CASE(1, 4) MSK_FFN_CASE(2, 4) MSK_FFN_CASE(4, 4) MSK_FFN_CASE(8, 4)
-  MSK_FFN_CASE(1, 8) MSK_FFN_CASE(2, 8) MSK_FFN_CASE(4, 8) MSK_FFN_CASE(8, 8)
+  MSK_FFN_CASE(1, 1) MSK_FFN_CASE(2, 1) MSK_FFN_CASE(4, 1)
+  MSK_FFN_CASE(1, 2) MSK_FFN_CASE(2, 2) MSK_FFN_CASE(4, 2)
+  MSK_FFN_CASE(1, 4) MSK_FFN_CASE(2, 4) MSK_FFN_CASE(4, 4)
+  MSK_FFN_CASE(1, 8) MSK_FFN_CASE(2, 8) MSK_FFN_CASE(4, 8)
+  if constexpr (sizeof(W) == 2) {
+    MSK_FFN_CASE(kMmaTileRows, 1) MSK_FFN_CASE(kMmaTileRows, 2) MSK_FFN_CASE(kMmaTileRows, 4)
+    MSK_FFN_CASE(kMmaTileRows, 8)
+  } else {
+    MSK_FFN_CASE(8, 1) MSK_FFN_CASE(8, 2) MSK_FFN_CASE(8, 4) MSK_FFN_CASE(8, 8)
+  }
 #undef MSK_FFN_CASE
   return hipErrorInvalidValue;
 }
 
-// Tokens per tile: the smallest of {1, 2, 4, 8} covering max_tok, limited so
-// that the LDS tile stays within 64 KiB and the accumulators fit.
+// Tokens per tile: the smallest of {1, 2, 4, 8} (fp32 weights) or {1, 2, 4,
+// kMmaTileRows} (bf16) covering max_tok, limited so that the LDS stays
+// within 64 KiB and the accumulators fit.  The limit depends only on the
+// shape, so every launch that can hold a tile of more than 4 rows uses the
+// same NT, and such a tile takes the same path in all of them.
 static int pick_nt(int max_tok, int d, int elem, int q, int vec, int upw) {
+  const int cap = elem == 2 ? kMmaTileRows : 8;
+  auto up = [&](int nt) { return (nt == 4 && elem == 2) ? kMmaTileRows : 2 * nt; };
+  auto down = [&](int nt) { return nt == kMmaTileRows ? 4 : nt / 2; };
   int nt = 1;
-  while (nt < max_tok && nt < kMmaTileRows) nt <<= 1;
-  while (nt > 1 &&
-         (ffn_lds_bytes(nt, d, elem, upw) > 65536 ||
-          !ffn_fits(nt, q, vec)))
-    nt >>= 1;
+  while (nt < max_tok && nt < cap) nt = up(nt);
+  while (nt > 1 && (ffn_lds_bytes(nt, d, elem, upw) > 65536 || !ffn_fits(nt, q, vec))) nt = down(nt);
   return nt;
 }
 
@@ -1799,12 +1865,6 @@ hipError_t launch_ffn(const FfnArgs& a, int max_tok, hipStream_t s) {
 //
 // (operand layout of v_mfma_f32_16x16x32_bf16: see mfma16)
 
-// fp32 -> bf16, round to nearest even (finite values)
-__device__ __forceinline__ uint16_t f2bf(float f) {
-  const uint32_t u = __float_as_uint(f);
-  return static_cast<uint16_t>((u + 0x7fffu + ((u >> 16) & 1u)) >> 16);
-}
-
 // Work-groups are dispatched to the 8 XCDs round-robin by index, and each
 // XCD has its own L2.  The matrix-core kernels renumber them so that every
 // XCD runs a contiguous range of logical indices: consecutive indices (the
@@ -2101,20 +2161,9 @@ __global__ __launch_bounds__(256) void mma_down_kernel(MmaArgs a) {
     for (int ks = 0; ks < 2; ++ks) an[ks] = ld16(arow + c * kChunkUnits + 32 * ks + kq);
   };
   auto step = [&](uint4(&dv)[8], uint4(&av)[2], int next) {
-    // column j of the 8 loaded rows: word j / 2 of each row, low or high half
+    // column j of the 8 loaded rows
     uint4 frag[8];
-#pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      const uint32_t sel = (j & 1) ? 0x07060302u : 0x05040100u;
-      uint32_t w[8];
-#pragma unroll
-      for (int r = 0; r < 8; ++r) {
-        const uint4 v = dv[r];
-        w[r] = (j >> 1) == 0 ? v.x : (j >> 1) == 1 ? v.y : (j >> 1) == 2 ? v.z : v.w;
-      }
-      frag[j] = make_uint4(__builtin_amdgcn_perm(w[1], w[0], sel), __builtin_amdgcn_perm(w[3], w[2], sel),
-                           __builtin_amdgcn_perm(w[5], w[4], sel), __builtin_amdgcn_perm(w[7], w[6], sel));
-    }
+    transpose8x8(dv, frag);
     const uint4 A0 = av[0], A1 = av[1];
     load_chunk(next, dv, av);
     __syncthreads();  // previous chunk's readers are done with dt

@@ -154,8 +154,8 @@ def test_qwen_decode_batch16_parity(qwen):
 
 
 def test_qwen_decode_batch16_independent_of_residency(qwen):
-    """Zipf-hot experts take 5-8 of the 16 tokens per tile: their gate/up run
-    on the matrix cores, the others on fma chains.  Which path a tile takes
+    """Zipf-hot experts take 5-16 of the 16 tokens: their tiles run on the
+    matrix cores, the others on fma chains.  Which path a tile takes
     depends only on its row count, so the output is bitwise the same with
     the hot tops cached, with every expert whole in VRAM and with nothing
     cached (every expert streamed after the routing); the configuration of
@@ -165,7 +165,7 @@ def test_qwen_decode_batch16_independent_of_residency(qwen):
     y0, idx0, w0 = _run(qwen, 0, h, 16)
     check_layer(qwen, 0, hf, y0, idx0, w0)
     counts = np.bincount(idx0.cpu().numpy().reshape(-1), minlength=128)
-    assert ((counts > 4) & (counts <= 8)).any() or (counts > 8).any(), counts  # an 8-row tile exists
+    assert (counts > 4).any(), counts  # a matrix-core tile exists
     e_bytes = synth.QWEN3.expert_bytes
     per_layer = (8 << 30) // 48
     for budgets, r, tops in (([128 * e_bytes, 128 * e_bytes], 1.0, list(range(128))), ([0, 0], 0.0, [])):

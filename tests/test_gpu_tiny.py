@@ -82,6 +82,42 @@ def test_tiny_multi_tile_experts_independent_of_residency(rig, T):
     for o in outs[1:]:
         assert np.array_equal(o, outs[0])
 
+# bf16, d = 512 (8 k pieces), F = 512 (8 chunks), 4 experts, top-2: large
+# enough for the matrix-core tiles' k split and column blocks, small enough
+# for the oracle; at these T every expert has 12-36 rows
+MT_BF16 = synth.ModelShape("multi-tile-bf16", 1, 512, 512, 4, 2, "bf16")
+
+
+@pytest.mark.parametrize("T", [37, 50, 64])
+def test_bf16_multi_tile_experts_independent_of_residency(T):
+    """bf16 decode path (forced also where the token count would choose the
+    prefill path): tiles of 5-16 rows run on the matrix cores in both
+    phases, tiles of 1-4 rows on fma chains, and an expert with more rows
+    than one tile spreads over several work-groups.  Outputs match the
+    oracle and are bitwise equal across residency states."""
+    from paper_2509_08342_amd import moesplit as ms
+    from workload import SplitRig, top_bytes
+    s = MT_BF16
+    with SplitRig(s, seed=5, max_tokens=64, budget_bytes=s.n_experts * s.expert_bytes) as r:
+        h, hf = r.hidden(T, tag=900 + T)
+        outs = []
+        for ratio, tops in ((0.5, [0, 1]), (0.0, []), (1.0, list(range(4))), (0.5, [2, 3]), (0.25, [1, 3])):
+            r.configure([s.n_experts * top_bytes(r, ratio)], [ratio])
+            r.load_tops(0, tops)
+            y, idx, w = r.outputs(T)
+            r.forward(0, h, T, y, idx, w, ms.MS_FWD_NO_MATRIX_CORES)
+            torch.cuda.synchronize()
+            if not outs:
+                check_layer(r, 0, hf, y, idx, w)
+                counts = np.bincount(idx.cpu().numpy()[:T].reshape(-1), minlength=4)
+                assert counts.max() > 16, counts  # some expert spans two tiles
+                tails = counts[counts > 0] % 16
+                assert ((tails > 4) | (tails == 0)).any() and ((tails >= 1) & (tails <= 4)).any(), counts
+            outs.append(y.cpu().numpy()[:T])
+        for o in outs[1:]:
+            assert np.array_equal(o, outs[0])
+
+
 def test_tiny_outputs_independent_of_residency_and_split(rig):
     """Eq. (2) output must not depend on r or on which tops are cached: every
     residency subset at r=0.5, and several subsets at r in {0,.25,.75,1}
