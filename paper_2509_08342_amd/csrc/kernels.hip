@@ -104,17 +104,32 @@ __device__ __forceinline__ f32x4_t mfma16(bf16x8_t a, bf16x8_t b, f32x4_t c) {
 // the T*K slots by expert.  The prediction ranking orders experts by
 // descending summed score, the lower index first on equal scores.
 
-constexpr int kLanesQ = kMaxExperts / 64;  // expert values held per lane
+// Expert values per lane of a launch (QN = ceil(E / 64), a power of two):
+// the routing kernels exist for QN = 1, 2, 4 and 8, so that a lane loops over
+// its real experts only.  Lanes past E hold -inf and add nothing, so QN
+// changes no result.
+__host__ __device__ constexpr int lanes_q(int E) { return E <= 64 ? 1 : E <= 128 ? 2 : E <= 256 ? 4 : 8; }
+static_assert(kMaxExperts <= 64 * 8, "at most 8 expert values per lane");
 
-// Selection of one token by one wave; lanes k < K return the k-th pick and
-// its weight.
-__device__ __forceinline__ void select_token(const float* lg, int E, int K, int renormalize, int lane,
-                                             int& my_idx, float& my_w) {
-  float lv[kLanesQ];
+// The logits of one token: lane l holds experts l + 64 q (-inf past E).
+template <int QN>
+__device__ __forceinline__ void load_lanes(const float* lg, int E, int lane, float (&lv)[QN]) {
 #pragma unroll
-  for (int q = 0; q < kLanesQ; ++q) {
+  for (int q = 0; q < QN; ++q) {
     const int e = lane + 64 * q;
-    float v = e < E ? lg[e] : -INFINITY;
+    lv[q] = e < E ? lg[e] : -INFINITY;
+  }
+}
+
+// Selection of one token by one wave from its logits (load_lanes); lanes
+// k < K return the k-th pick and its weight.
+template <int QN>
+__device__ __forceinline__ void select_token(const float (&lg)[QN], int E, int K, int renormalize, int lane,
+                                             int& my_idx, float& my_w) {
+  float lv[QN];
+#pragma unroll
+  for (int q = 0; q < QN; ++q) {
+    float v = lg[q];
     if (v != v) v = -INFINITY;  // NaN reads as -inf, so an index is always found
     lv[q] = v;
   }
@@ -125,7 +140,7 @@ __device__ __forceinline__ void select_token(const float* lg, int E, int K, int 
     float bv = -INFINITY;
     int bi = 0x7fffffff;
 #pragma unroll
-    for (int q = 0; q < kLanesQ; ++q) {
+    for (int q = 0; q < QN; ++q) {
       const int e = lane + 64 * q;
       if (e < E && !((taken >> q) & 1u) && (lv[q] > bv || (lv[q] == bv && e < bi))) {
         bv = lv[q];
@@ -154,7 +169,7 @@ __device__ __forceinline__ void select_token(const float* lg, int E, int K, int 
   if (!renormalize) {
     float part = 0.0f;
 #pragma unroll
-    for (int q = 0; q < kLanesQ; ++q)
+    for (int q = 0; q < QN; ++q)
       if (lane + 64 * q < E) part += expf(lv[q] - m);
 #pragma unroll
     for (int s = 32; s >= 1; s >>= 1) part += __shfl_xor(part, s, 64);
@@ -163,14 +178,16 @@ __device__ __forceinline__ void select_token(const float* lg, int E, int K, int 
   my_w = my_ex / z;
 }
 
-// acc[q] (expert lane + 64 q) += softmax(lg)[expert], one token, one wave.
-__device__ __forceinline__ void pred_add(const float* lg, int E, int lane, float (&acc)[kLanesQ]) {
-  float lv[kLanesQ];
+// acc[q] (expert lane + 64 q) += softmax(lg)[expert], one token's second
+// logits (load_lanes), one wave.
+template <int QN>
+__device__ __forceinline__ void pred_add(const float (&lg)[QN], int E, int lane, float (&acc)[QN]) {
+  float lv[QN];
   float m = -INFINITY;
 #pragma unroll
-  for (int q = 0; q < kLanesQ; ++q) {
+  for (int q = 0; q < QN; ++q) {
     const int e = lane + 64 * q;
-    float v = e < E ? lg[e] : -INFINITY;
+    float v = e < E ? lg[q] : -INFINITY;
     if (v != v) v = -INFINITY;  // a NaN logit reads as -inf: score 0
     lv[q] = v;
     m = fmaxf(m, lv[q]);
@@ -179,14 +196,14 @@ __device__ __forceinline__ void pred_add(const float* lg, int E, int lane, float
   for (int s = 32; s >= 1; s >>= 1) m = fmaxf(m, __shfl_xor(m, s, 64));
   float z = 0.0f;
 #pragma unroll
-  for (int q = 0; q < kLanesQ; ++q) {
+  for (int q = 0; q < QN; ++q) {
     lv[q] = (lane + 64 * q < E) ? expf(lv[q] - m) : 0.0f;
     z += lv[q];
   }
 #pragma unroll
   for (int s = 32; s >= 1; s >>= 1) z += __shfl_xor(z, s, 64);
 #pragma unroll
-  for (int q = 0; q < kLanesQ; ++q) acc[q] += lv[q] / z;
+  for (int q = 0; q < QN; ++q) acc[q] += lv[q] / z;
 }
 
 // Ranks score_s (LDS, E values) and stores order / score (and their host-
@@ -262,7 +279,7 @@ __device__ __forceinline__ void host_fence(const RouteArgs& a, int tid) {
 // memory would wait for it).
 constexpr int kFewSlots = 1024;
 
-template <int NW>
+template <int NW, int QN>
 __device__ void route_body(const RouteArgs& a) {
   __shared__ int idx_s[kFewSlots];
   __shared__ float w_s[kFewSlots];
@@ -277,12 +294,19 @@ __device__ void route_body(const RouteArgs& a) {
   const int E = a.E, K = a.K;
   const int TK = a.T * K;
 
+  // the prediction logits of this wave's first token are requested with its
+  // selection logits (one memory round trip for both)
+  float lp[QN];
+  if (a.logits_pred != nullptr && wave < a.T) load_lanes(a.logits_pred + static_cast<size_t>(wave) * E, E, lane, lp);
+
   if (a.logits != nullptr) {
     // 1. selection
     for (int t = wave; t < a.T; t += NW) {
       int my_idx;
       float my_w;
-      select_token(a.logits + static_cast<size_t>(t) * E, E, K, a.renormalize, lane, my_idx, my_w);
+      float lg[QN];
+      load_lanes(a.logits + static_cast<size_t>(t) * E, E, lane, lg);
+      select_token(lg, E, K, a.renormalize, lane, my_idx, my_w);
       if (lane < K) {
         idx_s[t * K + lane] = my_idx;
         w_s[t * K + lane] = my_w;
@@ -333,14 +357,17 @@ __device__ void route_body(const RouteArgs& a) {
 
   if (a.logits_pred != nullptr) {
     // 3. prediction ranking
-    float acc[kLanesQ];
+    float acc[QN];
 #pragma unroll
-    for (int q = 0; q < kLanesQ; ++q) acc[q] = 0.0f;
-    for (int t = wave; t < a.T; t += NW) pred_add(a.logits_pred + static_cast<size_t>(t) * E, E, lane, acc);
+    for (int q = 0; q < QN; ++q) acc[q] = 0.0f;
+    for (int t = wave; t < a.T; t += NW) {
+      if (t != wave) load_lanes(a.logits_pred + static_cast<size_t>(t) * E, E, lane, lp);
+      pred_add(lp, E, lane, acc);
+    }
     float* ws = reinterpret_cast<float*>(&wbuf[0][0]);
     __syncthreads();
 #pragma unroll
-    for (int q = 0; q < kLanesQ; ++q)
+    for (int q = 0; q < QN; ++q)
       if (lane + 64 * q < E) ws[wave * kMaxExperts + lane + 64 * q] = acc[q];
     __syncthreads();
     for (int e = tid; e < E; e += NT) {
@@ -367,7 +394,8 @@ __device__ void route_body(const RouteArgs& a) {
 
 constexpr int kRouteWaves = 16;
 
-__global__ __launch_bounds__(64 * kRouteWaves) void route_kernel(RouteArgs a) { route_body<kRouteWaves>(a); }
+template <int QN>
+__global__ __launch_bounds__(64 * kRouteWaves) void route_kernel(RouteArgs a) { route_body<kRouteWaves, QN>(a); }
 
 // Many tokens, step 1 (work-group b: tokens [b TB, (b+1) TB), one wave per
 // token): selection, then each slot's rank among the block's earlier slots
@@ -375,6 +403,7 @@ __global__ __launch_bounds__(64 * kRouteWaves) void route_kernel(RouteArgs a) { 
 // prediction score sums (waves in order) into psc[b][e].
 constexpr int kSelWaves = 4;
 
+template <int QN>
 __global__ __launch_bounds__(64 * kSelWaves) void select_many_kernel(RouteArgs a, int TB) {
   __shared__ int sidx[64 * kSelWaves];
   __shared__ int cnt[kMaxExperts];
@@ -387,7 +416,9 @@ __global__ __launch_bounds__(64 * kSelWaves) void select_many_kernel(RouteArgs a
     for (int t = t0 + wave; t < t1; t += kSelWaves) {
       int my_idx;
       float my_w;
-      select_token(a.logits + static_cast<size_t>(t) * E, E, K, a.renormalize, lane, my_idx, my_w);
+      float lg[QN];
+      load_lanes(a.logits + static_cast<size_t>(t) * E, E, lane, lg);
+      select_token(lg, E, K, a.renormalize, lane, my_idx, my_w);
       if (lane < K) {
         a.idx[static_cast<size_t>(t) * K + lane] = my_idx;
         a.w[static_cast<size_t>(t) * K + lane] = my_w;
@@ -407,12 +438,16 @@ __global__ __launch_bounds__(64 * kSelWaves) void select_many_kernel(RouteArgs a
     for (int e = tid; e < E; e += 64 * kSelWaves) a.blk[static_cast<size_t>(e) * a.nblk_cap + b] = cnt[e];
   }
   if (a.logits_pred != nullptr) {
-    float acc[kLanesQ];
+    float acc[QN];
 #pragma unroll
-    for (int q = 0; q < kLanesQ; ++q) acc[q] = 0.0f;
-    for (int t = t0 + wave; t < t1; t += kSelWaves) pred_add(a.logits_pred + static_cast<size_t>(t) * E, E, lane, acc);
+    for (int q = 0; q < QN; ++q) acc[q] = 0.0f;
+    for (int t = t0 + wave; t < t1; t += kSelWaves) {
+      float lp[QN];
+      load_lanes(a.logits_pred + static_cast<size_t>(t) * E, E, lane, lp);
+      pred_add(lp, E, lane, acc);
+    }
 #pragma unroll
-    for (int q = 0; q < kLanesQ; ++q)
+    for (int q = 0; q < QN; ++q)
       if (lane + 64 * q < E) wsc[wave][lane + 64 * q] = acc[q];
     __syncthreads();
     for (int e = tid; e < E; e += 64 * kSelWaves) {
@@ -595,7 +630,7 @@ __device__ __forceinline__ void fused_load(const W* wrow, int s0, int steps, W (
     wv[u] = wrow[static_cast<size_t>(min(s0 + u, steps - 1)) * 64];  // clamped: in bounds, used only in range
 }
 
-template <typename W>
+template <typename W, int QN>
 __global__ __launch_bounds__(64 * kRouteWaves) void route_fused_kernel(LogitsArgs la, RouteArgs ra) {
   constexpr int VE = 16 / static_cast<int>(sizeof(W));  // elements per 16-byte piece
   constexpr int B = fused_batch<W>();
@@ -654,7 +689,7 @@ __global__ __launch_bounds__(64 * kRouteWaves) void route_fused_kernel(LogitsArg
   RouteArgs a = ra;
   a.logits = ra.logits != nullptr ? lg : nullptr;
   a.logits_pred = ra.logits_pred != nullptr ? (ra.logits != nullptr ? lg + per : lg) : nullptr;
-  route_body<kRouteWaves>(a);
+  route_body<kRouteWaves, QN>(a);
 }
 
 // Many tokens: the same order, with each lane running the fma chains of 8
@@ -843,10 +878,18 @@ hipError_t launch_logits_route(const LogitsArgs& a, const RouteArgs& ra, hipStre
     const int64_t row_bytes = static_cast<int64_t>(a.T) * a.d * elem;
     if (n_out <= kFusedLogits && row_bytes <= kFusedRowBytes &&
         static_cast<int64_t>(a.T) * 64 * fused_pitch(a.d, elem) <= kFusedHBytes) {  // one launch for logits and route
-      if (a.dtype == kBF16)
-        hipLaunchKernelGGL(route_fused_kernel<uint16_t>, dim3(1), dim3(64 * kRouteWaves), 0, s, b, ra);
-      else
-        hipLaunchKernelGGL(route_fused_kernel<float>, dim3(1), dim3(64 * kRouteWaves), 0, s, b, ra);
+#define MSK_FUSED(QN_)                                                                              \
+  if (a.dtype == kBF16)                                                                             \
+    hipLaunchKernelGGL((route_fused_kernel<uint16_t, QN_>), dim3(1), dim3(64 * kRouteWaves), 0, s, b, ra); \
+  else                                                                                              \
+    hipLaunchKernelGGL((route_fused_kernel<float, QN_>), dim3(1), dim3(64 * kRouteWaves), 0, s, b, ra)
+      switch (lanes_q(ra.E)) {
+        case 1: MSK_FUSED(1); break;
+        case 2: MSK_FUSED(2); break;
+        case 4: MSK_FUSED(4); break;
+        default: MSK_FUSED(8); break;
+      }
+#undef MSK_FUSED
       return hipGetLastError();
     }
     const dim3 grid((n_out + 3) / 4);
@@ -857,11 +900,17 @@ hipError_t launch_logits_route(const LogitsArgs& a, const RouteArgs& ra, hipStre
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
+  const int qn = lanes_q(ra.E);
   if (!many) {
-    hipLaunchKernelGGL(route_kernel, dim3(1), dim3(64 * kRouteWaves), 0, s, ra);
+    auto* k = qn == 1 ? route_kernel<1> : qn == 2 ? route_kernel<2> : qn == 4 ? route_kernel<4> : route_kernel<8>;
+    hipLaunchKernelGGL(k, dim3(1), dim3(64 * kRouteWaves), 0, s, ra);
     return hipGetLastError();
   }
-  hipLaunchKernelGGL(select_many_kernel, dim3(nblk), dim3(64 * kSelWaves), 0, s, ra, TB);
+  auto* sel = qn == 1   ? select_many_kernel<1>
+              : qn == 2 ? select_many_kernel<2>
+              : qn == 4 ? select_many_kernel<4>
+                        : select_many_kernel<8>;
+  hipLaunchKernelGGL(sel, dim3(nblk), dim3(64 * kSelWaves), 0, s, ra, TB);
   if ((e = hipGetLastError()) != hipSuccess) return e;
   hipLaunchKernelGGL(scan_many_kernel, dim3(1), dim3(64 * kScanWaves), 0, s, ra, nblk);
   if ((e = hipGetLastError()) != hipSuccess) return e;
@@ -890,9 +939,10 @@ hipError_t launch_logits_route(const LogitsArgs& a, const RouteArgs& ra, hipStre
 // and a given chunk is always split the same way, so its partials do not
 // depend on which launch computed it.  Loads run one batch ahead of use;
 // the batch depth RB only changes how many are in flight, not the order of
-// any sum: launches of many work-groups use RB = 4 (more work-groups per
-// CU), launches of fewer than one work-group per CU use RB = 8 (each
-// work-group alone must keep enough bytes in flight to cover the latency).
+// any sum: launches with several work-groups per CU use RB = 4, launches
+// of fewer work-groups than CUs or of one (whole-chunk) work-group per CU
+// use RB = 8 (each work-group alone must keep enough bytes in flight to
+// cover the latency).
 
 // Index of the task holding work-group wg: the last task whose first
 // work-group is <= wg (tasks in ascending wg_begin order).
@@ -910,7 +960,7 @@ __device__ __forceinline__ int find_task_of(const TaskT* tasks, int n, int wg) {
 }
 
 constexpr int kRowBatch = 4;        // RB of launches that fill the GPU
-constexpr int kRowBatchDeep = 8;    // RB of launches with fewer work-groups than CUs
+constexpr int kRowBatchDeep = 8;    // RB where one work-group per CU carries the loads
 constexpr int kDeepBelowWgs = 256;
 constexpr int kLpu = kFfnLanesPerUnit;
 constexpr int kKTile = 64;                // k elements per gate/up piece
@@ -1403,9 +1453,13 @@ static hipError_t launch_ffn_one(const FfnArgs& a, int max_tok, hipStream_t s) {
   const int64_t grid = static_cast<int64_t>(a.n_wg) * n_tiles;
   if (grid > 0x7fffffff) return hipErrorInvalidValue;
   // deep batches (bf16 weights) only where few tokens and columns keep the
-  // accumulators small enough to leave room for the loads in flight
+  // accumulators small enough to leave room for the loads in flight, and
+  // where one work-group alone keeps its CU's loads in flight: launches of
+  // fewer work-groups than CUs, and whole-chunk work-groups (one per CU;
+  // measured on the Mixtral-shaped decode FFN: 123.5 -> 121.5 us; with two
+  // or more work-groups per CU deeper batches were slower)
   if constexpr (NT <= 2 && Q <= 4 && sizeof(W) == 2) {
-    if (grid < kDeepBelowWgs) {
+    if (grid < kDeepBelowWgs || kWgPerCu == 1) {
       hipLaunchKernelGGL((ffn_chunk_kernel<W, NT, Q, UPW, kRowBatchDeep>), dim3(grid), dim3(UPW * kLpu), lds, s,
                          a, n_tiles);
       return hipGetLastError();
@@ -2714,28 +2768,42 @@ __global__ __launch_bounds__(64 * kCombWaves) void combine_planes_kernel(Combine
   }
 }
 
+// The loads of up to 16 (term, group) partial sums are in flight at once:
+// PG groups of 16 / PG terms.
+template <int PG>
 __global__ __launch_bounds__(64) void combine_final_kernel(CombineArgs a) {
+  constexpr int TB = PG >= 16 ? 1 : 16 / PG;  // terms per batch
   const int t = blockIdx.x;
   const int col = blockIdx.y * 256 + threadIdx.x * 4;
   if (col >= a.d) return;
   const int TK = a.T * a.K;
   const int n_slots = TK + a.T * a.n_shared;
+  const int n_terms = a.K + a.n_shared;
   float4 y = make_float4(0.f, 0.f, 0.f, 0.f);
-  for (int term = 0; term < a.K + a.n_shared; ++term) {
-    const int slot = term < a.K ? t * a.K + term : TK + t * a.n_shared + (term - a.K);
-    float4 v[kCombMaxGroups];
+  for (int k0 = 0; k0 < n_terms; k0 += TB) {
+    float4 v[TB][PG];
 #pragma unroll
-    for (int g = 0; g < kCombMaxGroups; ++g)  // clamped loads, unused ones dropped below
-      v[g] = *reinterpret_cast<const float4*>(a.red + (static_cast<size_t>(min(g, a.pg - 1)) * n_slots + slot) * a.d + col);
-    float4 sum = v[0];
+    for (int j = 0; j < TB; ++j) {
+      const int term = min(k0 + j, n_terms - 1);  // clamped: in bounds, used only in range
+      const int slot = term < a.K ? t * a.K + term : TK + t * a.n_shared + (term - a.K);
 #pragma unroll
-    for (int g = 1; g < kCombMaxGroups; ++g)
-      if (g < a.pg) sum = f4add(sum, v[g]);
-    if (term < a.K) {
-      const float wk = a.w[t * a.K + term];
-      y = make_float4(fmaf(wk, sum.x, y.x), fmaf(wk, sum.y, y.y), fmaf(wk, sum.z, y.z), fmaf(wk, sum.w, y.w));
-    } else {
-      y = f4add(y, sum);
+      for (int g = 0; g < PG; ++g)
+        v[j][g] = *reinterpret_cast<const float4*>(a.red + (static_cast<size_t>(g) * n_slots + slot) * a.d + col);
+    }
+#pragma unroll
+    for (int j = 0; j < TB; ++j) {
+      const int term = k0 + j;
+      if (term < n_terms) {
+        float4 sum = v[j][0];
+#pragma unroll
+        for (int g = 1; g < PG; ++g) sum = f4add(sum, v[j][g]);
+        if (term < a.K) {
+          const float wk = a.w[t * a.K + term];
+          y = make_float4(fmaf(wk, sum.x, y.x), fmaf(wk, sum.y, y.y), fmaf(wk, sum.z, y.z), fmaf(wk, sum.w, y.w));
+        } else {
+          y = f4add(y, sum);
+        }
+      }
     }
   }
   *reinterpret_cast<float4*>(a.y + static_cast<size_t>(t) * a.d + col) = y;
@@ -2891,7 +2959,12 @@ hipError_t launch_combine(const CombineArgs& a, hipStream_t s) {
   hipLaunchKernelGGL(combine_planes_kernel, dim3(slots, ncb, a.pg), dim3(64 * kCombWaves), 0, s, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(combine_final_kernel, dim3(a.T, ncb), dim3(64), kGuardLds, s, a);
+  auto* fin = a.pg == 1   ? combine_final_kernel<1>
+              : a.pg == 2 ? combine_final_kernel<2>
+              : a.pg == 4 ? combine_final_kernel<4>
+              : a.pg == 8 ? combine_final_kernel<8>
+                          : combine_final_kernel<16>;
+  hipLaunchKernelGGL(fin, dim3(a.T, ncb), dim3(64), kGuardLds, s, a);
   return hipGetLastError();
 }
 
