@@ -111,6 +111,69 @@ __device__ __forceinline__ f32x4_t mfma16(bf16x8_t a, bf16x8_t b, f32x4_t c) {
 __host__ __device__ constexpr int lanes_q(int E) { return E <= 64 ? 1 : E <= 128 ? 2 : E <= 256 ? 4 : 8; }
 static_assert(kMaxExperts <= 64 * 8, "at most 8 expert values per lane");
 
+// Wave-wide reductions whose result does not depend on the order of the
+// combination (argmax with the lower index on equal values, max of floats,
+// integer sums) move data with DPP inside rows of 16 lanes -- lane i with
+// i ^ 1, i ^ 2 (quad permutes), i ^ 7 (half-row mirror), i ^ 15 (row
+// mirror) -- and read the four row results with v_readlane, instead of six
+// LDS-crossbar permutes.  Floating-point sums keep their fixed butterflies.
+constexpr int kDppXor1 = 0xB1;        // quad_perm [1, 0, 3, 2]
+constexpr int kDppXor2 = 0x4E;        // quad_perm [2, 3, 0, 1]
+constexpr int kDppHalfMirror = 0x141;  // row_half_mirror
+constexpr int kDppMirror = 0x140;      // row_mirror
+
+template <int CTRL>
+__device__ __forceinline__ int dpp_move(int x) {
+  return __builtin_amdgcn_update_dpp(0, x, CTRL, 0xf, 0xf, false);
+}
+template <int CTRL>
+__device__ __forceinline__ float dpp_move(float x) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), CTRL, 0xf, 0xf, false));
+}
+__device__ __forceinline__ int lane_read(int x, int l) { return __builtin_amdgcn_readlane(x, l); }
+__device__ __forceinline__ float lane_read(float x, int l) {
+  return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(x), l));
+}
+
+// (v, i) takes (ov, oi) if that is larger, or equal with a lower index.
+__device__ __forceinline__ void argmax_take(float& v, int& i, float ov, int oi) {
+  const bool take = ov > v || (ov == v && oi < i);
+  v = take ? ov : v;
+  i = take ? oi : i;
+}
+template <int CTRL>
+__device__ __forceinline__ void argmax_row_step(float& v, int& i) {
+  argmax_take(v, i, dpp_move<CTRL>(v), dpp_move<CTRL>(i));
+}
+// Every lane gets the wave's largest v and the lowest i among equal ones
+// (v never NaN).
+__device__ __forceinline__ void wave_argmax(float& v, int& i) {
+  argmax_row_step<kDppXor1>(v, i);
+  argmax_row_step<kDppXor2>(v, i);
+  argmax_row_step<kDppHalfMirror>(v, i);
+  argmax_row_step<kDppMirror>(v, i);
+  float bv = lane_read(v, 0);
+  int bi = lane_read(i, 0);
+#pragma unroll
+  for (int r = 1; r < 4; ++r) argmax_take(bv, bi, lane_read(v, 16 * r), lane_read(i, 16 * r));
+  v = bv;
+  i = bi;
+}
+__device__ __forceinline__ float wave_max(float v) {
+  v = fmaxf(v, dpp_move<kDppXor1>(v));
+  v = fmaxf(v, dpp_move<kDppXor2>(v));
+  v = fmaxf(v, dpp_move<kDppHalfMirror>(v));
+  v = fmaxf(v, dpp_move<kDppMirror>(v));
+  return fmaxf(fmaxf(lane_read(v, 0), lane_read(v, 16)), fmaxf(lane_read(v, 32), lane_read(v, 48)));
+}
+__device__ __forceinline__ int wave_sum(int v) {
+  v += dpp_move<kDppXor1>(v);
+  v += dpp_move<kDppXor2>(v);
+  v += dpp_move<kDppHalfMirror>(v);
+  v += dpp_move<kDppMirror>(v);
+  return (lane_read(v, 0) + lane_read(v, 16)) + (lane_read(v, 32) + lane_read(v, 48));
+}
+
 // The logits of one token: lane l holds experts l + 64 q (-inf past E).
 template <int QN>
 __device__ __forceinline__ void load_lanes(const float* lg, int E, int lane, float (&lv)[QN]) {
@@ -147,15 +210,7 @@ __device__ __forceinline__ void select_token(const float (&lg)[QN], int E, int K
         bi = e;
       }
     }
-#pragma unroll
-    for (int s = 32; s >= 1; s >>= 1) {
-      const float ov = __shfl_xor(bv, s, 64);
-      const int oi = __shfl_xor(bi, s, 64);
-      if (ov > bv || (ov == bv && oi < bi)) {
-        bv = ov;
-        bi = oi;
-      }
-    }
+    wave_argmax(bv, bi);
     if ((bi & 63) == lane) taken |= 1u << (bi >> 6);
     if (k == 0) m = bv;  // the first pick is the largest logit
     const float ex = expf(bv - m);
@@ -192,8 +247,7 @@ __device__ __forceinline__ void pred_add(const float (&lg)[QN], int E, int lane,
     lv[q] = v;
     m = fmaxf(m, lv[q]);
   }
-#pragma unroll
-  for (int s = 32; s >= 1; s >>= 1) m = fmaxf(m, __shfl_xor(m, s, 64));
+  m = wave_max(m);
   float z = 0.0f;
 #pragma unroll
   for (int q = 0; q < QN; ++q) {
@@ -209,9 +263,13 @@ __device__ __forceinline__ void pred_add(const float (&lg)[QN], int E, int lane,
 // Ranks score_s (LDS, E values) and stores order / score (and their host-
 // visible copies), by a work-group of NT threads (whole waves): one wave per
 // expert, its lanes comparing against experts lane, lane + 64, ..., the
-// counts summed by a butterfly.  rank(e) = #{o : s_o > s_e or (s_o == s_e
-// and o < e)}, so equal scores keep the lower index first.
-__device__ __forceinline__ void rank_scores(const float* score_s, const RouteArgs& a, int tid, int NT) {
+// counts summed over the wave.  rank(e) = #{o : s_o > s_e or (s_o == s_e
+// and o < e)}, so equal scores keep the lower index first.  The order is
+// collected in LDS (order_s) and stored by consecutive threads, so that the
+// host-visible copies cross the bus as whole rows rather than one 4-byte
+// write per expert.
+__device__ __forceinline__ void rank_scores(const float* score_s, int* order_s, const RouteArgs& a, int tid,
+                                            int NT) {
   const int E = a.E;
   const int lane = tid & 63, wave = tid >> 6, nw = NT >> 6;
   for (int e = wave; e < E; e += nw) {
@@ -221,14 +279,17 @@ __device__ __forceinline__ void rank_scores(const float* score_s, const RouteArg
       const float u = score_s[o];
       r += (u > v) || (u == v && o < e);
     }
-#pragma unroll
-    for (int s = 32; s >= 1; s >>= 1) r += __shfl_xor(r, s, 64);
-    if (lane == 0) {
-      a.order[r] = e;
-      a.score[e] = v;
-      if (a.host_order) a.host_order[r] = e;
-      if (a.host_score) a.host_score[e] = v;
-    }
+    r = wave_sum(r);
+    if (lane == 0) order_s[r] = e;
+  }
+  __syncthreads();
+  for (int i = tid; i < E; i += NT) {
+    const int e = order_s[i];
+    const float v = score_s[i];
+    a.order[i] = e;
+    a.score[i] = v;
+    if (a.host_order) a.host_order[i] = e;
+    if (a.host_score) a.host_score[i] = v;
   }
 }
 
@@ -249,7 +310,7 @@ __device__ __forceinline__ void scan_offsets(const int* cnt, int* base, int* off
       if (base) base[e] = run + incl - c;
       offs[e] = run + incl - c;
     }
-    run += __shfl(incl, 63, 64);
+    run += lane_read(incl, 63);
   }
   if (lane == 0) offs[E] = run;
 }
@@ -332,7 +393,7 @@ __device__ void route_body(const RouteArgs& a) {
       uint64_t pending = __ballot(e >= 0);
       while (pending) {
         const int leader = __ffsll(static_cast<unsigned long long>(pending)) - 1;
-        const int le = __shfl(e, leader, 64);
+        const int le = lane_read(e, leader);
         const uint64_t same = __ballot(e == le);
         if (e == le) rank = __popcll(same & lt);
         if (lane == leader) wbuf[wave][le] = __popcll(same);
@@ -376,7 +437,7 @@ __device__ void route_body(const RouteArgs& a) {
       score_s[e] = sc;
     }
     __syncthreads();
-    rank_scores(score_s, a, tid, NT);
+    rank_scores(score_s, &wbuf[1][0], a, tid, NT);
   }
 
   // 4. the selection and grouping to memory (and the offsets to the host)
@@ -464,45 +525,48 @@ __global__ __launch_bounds__(64 * kSelWaves) void select_many_kernel(RouteArgs a
 // experts into offsets; the prediction scores summed over blocks in order,
 // and their ranking.
 constexpr int kScanWaves = 16;
+constexpr int kScanGroup = 8;  // experts per wave whose loads are in flight together
 
 __global__ __launch_bounds__(64 * kScanWaves) void scan_many_kernel(RouteArgs a, int nblk) {
   __shared__ int tot[kMaxExperts];
   __shared__ int offs_s[kMaxExperts + 1];
   __shared__ float score_s[kMaxExperts];
+  __shared__ int order_s[kMaxExperts];
+  // a wave takes kScanGroup experts at a time (e0, e0 + kScanWaves, ...) and
+  // requests their values of 64 blocks together, so that the experts of a
+  // wave cost one memory round trip per 64 blocks, not one each
+  constexpr int EG = kScanGroup;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int E = a.E;
   if (a.logits != nullptr) {
-    // per expert (one wave): the counts of up to kScanPer x 64 blocks are
-    // loaded together, then scanned 64 at a time
-    constexpr int kScanPer = 8;
-    for (int e = wave; e < E; e += kScanWaves) {
-      int* row = a.blk + static_cast<size_t>(e) * a.nblk_cap;
-      int run = 0;
-      for (int B0 = 0; B0 < nblk; B0 += 64 * kScanPer) {
-        int cv[kScanPer];
+    // per expert: exclusive scan of its block counts, 64 blocks at a time
+    for (int e0 = wave; e0 < E; e0 += EG * kScanWaves) {
+      int run[EG];
 #pragma unroll
-        for (int j = 0; j < kScanPer; ++j) {
-          const int b = B0 + 64 * j + lane;
-          cv[j] = row[min(b, nblk - 1)];  // every load issued, in bounds
-        }
+      for (int j = 0; j < EG; ++j) run[j] = 0;
+      for (int B0 = 0; B0 < nblk; B0 += 64) {
+        const int b = B0 + lane;
+        int cv[EG];
 #pragma unroll
-        for (int j = 0; j < kScanPer; ++j)
-          if (B0 + 64 * j + lane >= nblk) cv[j] = 0;
+        for (int j = 0; j < EG; ++j)  // clamped: every load in bounds, used only in range
+          cv[j] = a.blk[static_cast<size_t>(min(e0 + kScanWaves * j, E - 1)) * a.nblk_cap + min(b, nblk - 1)];
 #pragma unroll
-        for (int j = 0; j < kScanPer; ++j) {
-          const int b = B0 + 64 * j + lane;
-          const int c = cv[j];
+        for (int j = 0; j < EG; ++j) {
+          const int e = e0 + kScanWaves * j;
+          const int c = b < nblk ? cv[j] : 0;
           int incl = c;
 #pragma unroll
           for (int s = 1; s < 64; s <<= 1) {
             const int o = __shfl_up(incl, s, 64);
             if (lane >= s) incl += o;
           }
-          if (b < nblk) row[b] = run + incl - c;
-          run += __shfl(incl, 63, 64);
+          if (e < E && b < nblk) a.blk[static_cast<size_t>(e) * a.nblk_cap + b] = run[j] + incl - c;
+          run[j] += lane_read(incl, 63);
         }
       }
-      if (lane == 0) tot[e] = run;
+#pragma unroll
+      for (int j = 0; j < EG; ++j)
+        if (lane == 0 && e0 + kScanWaves * j < E) tot[e0 + kScanWaves * j] = run[j];
     }
     __syncthreads();
     if (wave == 0) {
@@ -511,29 +575,32 @@ __global__ __launch_bounds__(64 * kScanWaves) void scan_many_kernel(RouteArgs a,
     }
   }
   if (a.logits_pred != nullptr) {
-    // per expert (one wave): lanes sum blocks lane, lane + 64, ... in order,
-    // then a fixed halving tree over the lanes
-    for (int e = wave; e < E; e += kScanWaves) {
-      float sc = 0.0f;
-      for (int B0 = 0; B0 < nblk; B0 += 64 * 8) {
-        float pv[8];
+    // per expert: lanes sum blocks lane, lane + 64, ... in order, then a
+    // fixed halving tree over the lanes
+    for (int e0 = wave; e0 < E; e0 += EG * kScanWaves) {
+      float sc[EG];
 #pragma unroll
-        for (int j = 0; j < 8; ++j) {
-          const int b = B0 + 64 * j + lane;
-          pv[j] = a.psc[static_cast<size_t>(min(b, nblk - 1)) * E + e];  // every load issued, in bounds
-        }
+      for (int j = 0; j < EG; ++j) sc[j] = 0.0f;
+      for (int B0 = 0; B0 < nblk; B0 += 64) {
+        const int b = B0 + lane;
+        float pv[EG];
 #pragma unroll
-        for (int j = 0; j < 8; ++j)
-          if (B0 + 64 * j + lane >= nblk) pv[j] = 0.0f;
+        for (int j = 0; j < EG; ++j)  // clamped: every load in bounds, used only in range
+          pv[j] = a.psc[static_cast<size_t>(min(b, nblk - 1)) * E + min(e0 + kScanWaves * j, E - 1)];
 #pragma unroll
-        for (int j = 0; j < 8; ++j) sc += pv[j];  // blocks lane, lane + 64, ... in order
+        for (int j = 0; j < EG; ++j)
+          if (b < nblk) sc[j] += pv[j];
       }
 #pragma unroll
-      for (int s = 32; s >= 1; s >>= 1) sc = sc + __shfl_down(sc, s, 64);
-      if (lane == 0) score_s[e] = sc;
+      for (int j = 0; j < EG; ++j) {
+        float v = sc[j];
+#pragma unroll
+        for (int s = 32; s >= 1; s >>= 1) v = v + __shfl_down(v, s, 64);
+        if (lane == 0 && e0 + kScanWaves * j < E) score_s[e0 + kScanWaves * j] = v;
+      }
     }
     __syncthreads();
-    rank_scores(score_s, a, tid, 64 * kScanWaves);
+    rank_scores(score_s, order_s, a, tid, 64 * kScanWaves);
   }
   host_fence(a, tid);
 }
