@@ -162,7 +162,7 @@ inline bool q_supported(int d) { return d % 64 == 0 && d >= 256 && d <= kMaxMode
 //  down (mma_down): out[row][:] = sum_f act[row][f] * D_f over all of the
 //    expert's chunks (chunks < split at base, the rest at base2), 64 rows x
 //    256 columns per work-group, written as the single partial plane.
-constexpr int kMaxMmaTasks = 80;
+constexpr int kMaxMmaTasks = 192;  // tasks by value in one matrix-core launch (7.7 KiB of kernel arguments)
 // gate/up work-groups per chunk and row tile: 4 (16 units each) for launches
 // of fewer than kGuSplitBelow row-tile chunks, else 1 (whole chunks)
 constexpr int kGuSplitBelow = 256;
@@ -204,6 +204,8 @@ struct MmaArgs {
                                // chunks (gu_split 1) of experts with at least kTallTileRows rows
   MmaTask tasks[kMaxMmaTasks];
 };
+// kernel arguments of this size were measured to reach the kernels intact
+static_assert(sizeof(MmaArgs) <= 8000, "matrix-core kernel arguments within 8000 bytes");
 hipError_t launch_mma_gateup(const MmaArgs& a, hipStream_t s);
 hipError_t launch_mma_down(const MmaArgs& a, hipStream_t s);
 
