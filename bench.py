@@ -628,8 +628,12 @@ def pmc_summary(fetch_dir, write_dir, workload, out, cmd_fetch, cmd_write, pass_
 
 def mfma_pmc_summary(d, workload, out, cmd):
     """SQ_VALU_MFMA_BUSY_CYCLES and GRBM_GUI_ACTIVE per dispatch of a --pmc
-    run of both counters, by kernel, with the busy ratio normalised as
-    busy / (GRBM_GUI_ACTIVE x 256 CUs)."""
+    run of both counters, by kernel.  As rocprofv3 reports them on this GPU,
+    GRBM_GUI_ACTIVE is summed over the 8 XCDs (per dispatch it is 8 x the
+    kernel's cycles) and SQ_VALU_MFMA_BUSY_CYCLES over the 1024 SIMDs (16
+    busy cycles per v_mfma_f32_16x16x32_bf16, the rate of the 2.5 PFLOP/s
+    bf16 peak), so the matrix cores' busy fraction is
+    busy / (GRBM_GUI_ACTIVE / 8 x 1024)."""
     by = {}
     for r in _read_rows(d, "counter_collection.csv"):
         e = by.setdefault(int(r["Dispatch_Id"]), {"name": r["Kernel_Name"]})
@@ -643,10 +647,14 @@ def mfma_pmc_summary(d, workload, out, cmd):
         k[2] += e.get("GRBM_GUI_ACTIVE", 0.0)
     lines = ["# Matrix-core busy cycles, %s workload, rocprofv3 counters" % workload, "",
              "Command (from the repository root, on one MI355X):", "", "    " + cmd, "",
+             "GRBM_GUI_ACTIVE is summed over the 8 XCDs (8 x the kernel's cycles per dispatch) and "
+             "SQ_VALU_MFMA_BUSY_CYCLES over the 1024 SIMDs (16 cycles per 16x16x32 bf16 MFMA), so the "
+             "matrix cores are busy for busy / (GUI_ACTIVE / 8 x 1024) of the kernel's time.", "",
              "| kernel | dispatches | SQ_VALU_MFMA_BUSY_CYCLES / dispatch | GRBM_GUI_ACTIVE / dispatch | "
-             "busy / (GUI_ACTIVE x 256 CUs) |", "|---|---|---|---|---|"]
+             "kernel cycles (GUI_ACTIVE / 8) | MFMA busy fraction |", "|---|---|---|---|---|---|"]
     for n, (c, busy, gui) in sorted(kern.items(), key=lambda x: -x[1][1]):
-        lines.append("| `%s` | %d | %.4g | %.4g | %.4f |" % (n, c, busy / c, gui / c, busy / max(gui * 256.0, 1.0)))
+        lines.append("| `%s` | %d | %.4g | %.4g | %.4g | %.4f |" % (
+            n, c, busy / c, gui / c, gui / c / 8.0, busy / max(gui / 8.0 * 1024.0, 1.0)))
     with open(out, "w") as f:
         f.write("\n".join(lines) + "\n")
     print("wrote %s (%d kernels)" % (out, len(kern)))
