@@ -10,6 +10,7 @@ namespace msk {
 
 constexpr int kChunkUnits = 64;    // FFN intermediate units per chunk
 constexpr int kMaxTasks = 200;     // tasks passed by value in one FFN launch (3.3 KiB of kernel arguments)
+static_assert(kMaxTasks <= 256, "find_task_of reads at most 256 task starts");
 constexpr int kFfnLanesPerUnit = 8;  // lanes sharing one unit row in phase 1
 constexpr int kMaxExperts = 512;   // grouping / ranking kernels' LDS bound
 constexpr int kMaxTopK = 64;
@@ -163,6 +164,7 @@ inline bool q_supported(int d) { return d % 64 == 0 && d >= 256 && d <= kMaxMode
 //    expert's chunks (chunks < split at base, the rest at base2), 64 rows x
 //    256 columns per work-group, written as the single partial plane.
 constexpr int kMaxMmaTasks = 192;  // tasks by value in one matrix-core launch (7.7 KiB of kernel arguments)
+static_assert(kMaxMmaTasks <= 256, "find_task_of reads at most 256 task starts");
 // gate/up work-groups per chunk and row tile: 4 (16 units each) for launches
 // of fewer than kGuSplitBelow row-tile chunks, else 1 (whole chunks)
 constexpr int kGuSplitBelow = 256;

@@ -1015,15 +1015,17 @@ hipError_t launch_logits_route(const LogitsArgs& a, const RouteArgs& ra, hipStre
 // work-group is <= wg (tasks in ascending wg_begin order).
 template <typename TaskT>
 __device__ __forceinline__ int find_task_of(const TaskT* tasks, int n, int wg) {
-  int lo = 0, hi = n - 1;
-  while (lo < hi) {
-    const int mid = (lo + hi + 1) >> 1;
-    if (tasks[mid].wg_begin <= wg)
-      lo = mid;
-    else
-      hi = mid - 1;
-  }
-  return lo;
+  // the starts are ascending from 0: the task is the count of starts <= wg,
+  // less one; every lane reads up to four starts at once (no chain of
+  // dependent reads)
+  const int lane = threadIdx.x & 63;
+  int b[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) b[j] = tasks[min(64 * j + lane, n - 1)].wg_begin;  // clamped: in bounds
+  int cnt = 0;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) cnt += __popcll(__ballot(64 * j + lane < n && b[j] <= wg));
+  return __builtin_amdgcn_readfirstlane(cnt - 1);
 }
 
 constexpr int kRowBatch = 4;        // RB of launches that fill the GPU
