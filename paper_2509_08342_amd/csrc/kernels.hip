@@ -926,7 +926,7 @@ hipError_t launch_logits_route(const LogitsArgs& a, const RouteArgs& ra, hipStre
     b.wr2 = nullptr;
     b.wt2 = nullptr;
   }
-  const int TB = route_block_tokens(ra.K);
+  const int TB = route_block_tokens(a.T, ra.K);
   const int nblk = (a.T + TB - 1) / TB;
   const bool many = (a.T >= kManyTokens || (ra.logits != nullptr && a.T * ra.K > kFewSlots)) && ra.lrank != nullptr && ra.blk != nullptr &&
                     ra.psc != nullptr && nblk <= ra.nblk_cap && TB * ra.K <= 64 * kSelWaves;

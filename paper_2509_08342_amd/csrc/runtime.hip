@@ -217,8 +217,7 @@ ms_status derive_shape(const ms_model_desc* d, Shape* s, std::string* err) {
   }
 
   // many-token routing workspace
-  const int tb = msk::route_block_tokens(s->K);
-  s->nblk_cap = (s->max_T + tb - 1) / tb;
+  s->nblk_cap = msk::route_block_cap(s->max_T, s->K);
   s->off_lrank = off;
   off += align_up(TK * 4, kAlign);
   s->off_blk = off;
