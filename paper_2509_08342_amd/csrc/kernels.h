@@ -182,7 +182,7 @@ static_assert(kMaxMmaTasks <= 256, "find_task_of reads at most 256 task starts")
 // of fewer than kGuSplitBelow row-tile chunks, else 1 (whole chunks)
 constexpr int kGuSplitBelow = 256;
 constexpr int kMmaRows = 64;     // rows (token slots) per work-group
-constexpr int kTallTileRows = 128;  // experts with this many rows take 128-row gate/up tiles
+constexpr int kGdMaxRows = 192;  // rows per tile of the LDS-staged gate/up kernel (bf16, d % 128 == 0)
 constexpr int kMmaCols = 256;    // output columns per down work-group
 
 struct MmaTask {
@@ -215,8 +215,8 @@ struct MmaArgs {
   int32_t bits;                // 0: bf16 chunks; 2 or 4: b-bit chunks (q_chunk_bytes layout)
   int32_t ksplit;              // down, b-bit: chunk ranges per (row tile, column block), each summed
                                // into its own partial plane [row][ksplit][d]; 1 for bf16
-  int32_t tile_rows;           // rows per row tile: kMmaRows, or 2 kMmaRows for bf16 gate/up of whole
-                               // chunks (gu_split 1) of experts with at least kTallTileRows rows
+  int32_t tile_rows;           // rows per row tile: kMmaRows, or kGdMaxRows for the bf16 gate/up of
+                               // whole chunks (gu_split 1, d % 128 == 0)
   MmaTask tasks[kMaxMmaTasks];
 };
 // kernel arguments of this size were measured to reach the kernels intact

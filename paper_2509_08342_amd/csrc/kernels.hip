@@ -2114,26 +2114,190 @@ __global__ __launch_bounds__(256) void mma_gateup_kernel(MmaArgs a) {
   }
 }
 
-// gate/up of whole chunks for row tiles of 16 RB rows (a.tile_rows): a
-// work-group takes 16 RB rows x 64 units, wave w the units 16 w .. 16 w + 15
-// of every 16-row block, so each weight fragment is read by one wave only.
-// The activation rows are staged in LDS in slabs of kGuSlab k (double
-// buffer, rows padded so that the 16 rows a fragment read touches fall in
-// distinct banks).  No load is waited for in the step that issues it: at
-// slab sl the work-group computes slab sl from LDS with weight fragments
-// issued two slabs earlier (three register sets in turn), stores the rows of
-// slab sl + 1 issued one slab earlier, then issues the loads of slab sl + 2.
-// The k order of every sum is the same as for any other tile height, so a
-// row's activations do not depend on the tile it was computed in.  Needs
-// d % 256 == 0 (whole slabs, an even count of them).
+// activation rows of the b-bit gate/up kernel are staged in LDS in slabs of
+// kGuSlab k, rows padded so that the 16 rows a fragment read touches fall in
+// distinct banks
 constexpr int kGuSlab = 128;            // k per staged slab (4 MFMA k-steps)
 constexpr int kGuPitch = kGuSlab + 8;   // bf16 per staged row
 
+// gate/up with both operands staged by direct global -> LDS loads
+// (global_load_lds_dwordx4: a lane's 16 bytes land at the LDS address in M0
+// + 16 lane, with no register in between, so the registers hold only the
+// accumulators and the fragments of one k step).  A work-group takes one
+// chunk (64 units of G and of U) for a row tile of up to kGdMaxRows rows and
+// takes the height of its tile: 64, 128 or 192 rows, so that an expert's
+// rows usually fit one tile and its weights are read once.  The k loop runs
+// over stages of 64 k in a ring of as many LDS buffers as kGdLds holds for
+// that height (6, 5 or 4): the loads of all but one are in flight while a
+// stage is computed, which is what keeps HBM busy (with one stage ahead, the
+// loads in flight per CU cover too little of the memory latency).  A wave
+// waits for its own loads of a stage, then a barrier makes every wave's
+// loads visible and frees the buffer read before for the next loads.  The
+// loads are issued from inline assembly, so the compiler, which would
+// otherwise wait for every load in flight into an LDS array before reading
+// any part of it, leaves the waits to the kernel.  A load moves 8 rows of
+// 128 bytes (whole cache lines).  Staged rows hold 8 pieces of 8 k; piece p
+// of row r sits in slot p ^ (r % 8), so the 8 lanes an LDS read serves
+// together (8 rows at one piece) hit distinct banks.  The waves split the
+// tile kGdWaves / 2 x 2: wave (wr, wc) takes the row blocks wr, wr +
+// kGdWaves / 2, ... and units 32 wc .. 32 wc + 31 of G and of U.  The k
+// order of every sum is that of the other gate/up kernels.
+constexpr int kGdWaves = 8;                                  // waves per work-group
+constexpr int kGdLds = 160 * 1024;                           // LDS of a work-group (one per CU)
+constexpr int kGdSlab = 64;                                  // k per stage
+constexpr int kGdMaxRB = 12;                                 // row blocks of 16 per tile at most
+constexpr int kGdRowBytes = 2 * kGdSlab;                     // one staged row: a cache line
+constexpr int kGdLoadBytes = 64 * 16;                        // one load: 8 rows
+constexpr int kGdBlockBytes = 16 * kGdRowBytes;              // one 16-row block
+constexpr int kGdBBytes = kChunkUnits * kGdRowBytes;         // G (or U) units of a stage
+static_assert(kGdMaxRB * 16 == kGdMaxRows, "tile height of the staged gate/up kernel");
+static_assert(kGdSlab == kKTile, "a stage is one k piece of the gate/up layout");
+
+// 16 bytes per lane from global memory to LDS byte address lds + 16 lane
+// (lds uniform over the wave); M0 is restored for the compiler
+__device__ __forceinline__ void lds_load16(const void* g, uint32_t lds) {
+  uint32_t keep;
+  asm volatile(
+      "s_mov_b32 %0, m0\n\t"
+      "s_mov_b32 m0, %2\n\t"
+      "global_load_lds_dwordx4 %1, off\n\t"
+      "s_mov_b32 m0, %0"
+      : "=&s"(keep)
+      : "v"(g), "s"(lds)
+      : "memory");
+}
+
+__device__ __forceinline__ uint32_t lds_address(const void* p) {
+  return static_cast<uint32_t>(reinterpret_cast<uintptr_t>((const __attribute__((address_space(3))) void*)(p)));
+}
+
+// wait until at most N of this wave's vector memory loads are in flight
+template <int N>
+__device__ __forceinline__ void wait_vm() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+
+// barrier without a memory fence (a fence would wait for every load in
+// flight into LDS): this wave's LDS reads are complete first, and the
+// clobber keeps the compiler from moving LDS accesses across it
+__device__ __forceinline__ void bare_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
+
+__device__ __forceinline__ bf16x8_t lds_frag(const unsigned char* p) {
+  return as_bf16x8(*reinterpret_cast<const uint4*>(p));
+}
+
 template <int RB>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(RB <= 4 ? 3 : 2))) void mma_gateup_rows_kernel(
-    MmaArgs a) {
-  constexpr int ROWS = 16 * RB;
-  __shared__ __align__(16) uint16_t As[2][ROWS * kGuPitch];
+__device__ __forceinline__ void gd_tile(const MmaArgs& a, const MmaTask& tk, int c, const TileRows& tr,
+                                        unsigned char* lds) {
+  constexpr int WR = kGdWaves / 2;            // row groups of waves
+  constexpr int NA = 2 * RB / kGdWaves;       // activation loads per wave and stage
+  constexpr int NB = 8 / kGdWaves;            // G (and U) loads per wave and stage
+  constexpr int NL = NA + 2 * NB;             // loads per wave and stage
+  constexpr int HB = RB / WR;                 // row blocks per wave
+  constexpr int ABYTES = RB * kGdBlockBytes;  // activation rows of a stage
+  constexpr int SBYTES = ABYTES + 2 * kGdBBytes;
+  constexpr int NST = kGdLds / SBYTES;        // stages in the ring
+  static_assert(RB % WR == 0 && (2 * RB) % kGdWaves == 0 && RB <= kGdMaxRB, "row blocks");
+  static_assert(NST >= 2 && (NST - 2) * NL < 64, "ring depth");
+  const int lane = threadIdx.x & 63;
+  const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int wr = w >> 1, wc = w & 1;
+  const int d = a.d, nsl = d / kGdSlab;
+  const bool routed = tk.expert >= 0;
+  // loads: lane -> row (unit) lane / 8 of the 8 a load covers; its slot
+  // lane % 8 holds piece (lane % 8) ^ (lane / 8)
+  const int lrow = lane >> 3;
+  const int lpiece = (lane & 7) ^ lrow;
+  const uint16_t* hsrc[NA];
+#pragma unroll
+  for (int j = 0; j < NA; ++j) {
+    const int r = min(8 * (w + kGdWaves * j) + lrow, tr.n - 1);  // rows past the tile repeat its last (never stored)
+    const int tok = routed ? a.perm[tr.p0 + r] / a.K : tr.p0 + r;
+    hsrc[j] = static_cast<const uint16_t*>(a.h) + static_cast<size_t>(tok) * d + 8 * lpiece;
+  }
+  const uint16_t* G = reinterpret_cast<const uint16_t*>(tk.base + static_cast<size_t>(c) * a.chunk_bytes) +
+                      (8 * w + lrow) * kKTile + 8 * lpiece;
+  const uint16_t* U = G + static_cast<size_t>(kChunkUnits) * d;
+  const uint32_t lbase = lds_address(lds) + w * kGdLoadBytes;
+  auto issue = [&](int sl, int buf) {  // stages past the last reload it (in bounds, never read)
+    const int k0 = min(sl, nsl - 1) * kGdSlab;
+    const uint32_t st = lbase + buf * SBYTES;
+#pragma unroll
+    for (int j = 0; j < NA; ++j) lds_load16(hsrc[j] + k0, st + kGdWaves * j * kGdLoadBytes);
+    const size_t bo = static_cast<size_t>(k0) * kChunkUnits;
+#pragma unroll
+    for (int j = 0; j < NB; ++j) {
+      const int go = 8 * kGdWaves * j * kKTile;  // units 8 (w + kGdWaves j) ..
+      lds_load16(G + bo + go, st + ABYTES + kGdWaves * j * kGdLoadBytes);
+      lds_load16(U + bo + go, st + ABYTES + kGdBBytes + kGdWaves * j * kGdLoadBytes);
+    }
+  };
+  // fragment reads: lane -> row (unit) lane % 16 of a block, piece 4 s +
+  // lane / 16 of k step s
+  int fo[2];
+#pragma unroll
+  for (int s = 0; s < 2; ++s) fo[s] = (lane & 15) * kGdRowBytes + 16 * ((4 * s + (lane >> 4)) ^ (lane & 7));
+  f32x4_t ag[HB][2], au[HB][2];
+#pragma unroll
+  for (int i = 0; i < HB; ++i)
+#pragma unroll
+    for (int n = 0; n < 2; ++n) ag[i][n] = au[i][n] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  auto compute = [&](int buf) {
+    const unsigned char* st = lds + buf * SBYTES;
+#pragma unroll
+    for (int s = 0; s < 2; ++s) {
+      const unsigned char* sg = st + ABYTES + 2 * wc * kGdBlockBytes + fo[s];
+      const unsigned char* su = sg + kGdBBytes;
+      const unsigned char* sa = st + wr * kGdBlockBytes + fo[s];
+      const bf16x8_t g0 = lds_frag(sg), g1 = lds_frag(sg + kGdBlockBytes);
+      const bf16x8_t u0 = lds_frag(su), u1 = lds_frag(su + kGdBlockBytes);
+      bf16x8_t A[HB];
+#pragma unroll
+      for (int i = 0; i < HB; ++i) A[i] = lds_frag(sa + WR * i * kGdBlockBytes);
+#pragma unroll
+      for (int i = 0; i < HB; ++i) {
+        ag[i][0] = mfma16(A[i], g0, ag[i][0]);
+        ag[i][1] = mfma16(A[i], g1, ag[i][1]);
+        au[i][0] = mfma16(A[i], u0, au[i][0]);
+        au[i][1] = mfma16(A[i], u1, au[i][1]);
+      }
+    }
+  };
+#pragma unroll
+  for (int p = 0; p < NST - 1; ++p) issue(p, p);
+  // stage sl sits in buffer sl % NST; at sl this wave's loads of it are in
+  // (those of the NST - 2 later stages may not be), every wave's after the
+  // barrier, which also frees the buffer read at sl - 1 for stage sl + NST - 1
+  int cur = 0, nxt = NST - 1;
+  for (int sl = 0; sl < nsl; ++sl) {
+    wait_vm<(NST - 2) * NL>();
+    bare_barrier();
+    issue(sl + NST - 1, nxt);
+    compute(cur);
+    cur = cur + 1 == NST ? 0 : cur + 1;
+    nxt = nxt + 1 == NST ? 0 : nxt + 1;
+  }
+  wait_vm<0>();  // the reloads past the last stage land before the work-group ends
+  uint16_t* act = routed ? a.act : a.act_sh + static_cast<size_t>(-1 - tk.expert) * a.rows_shared * a.f_pad_sh;
+  const int f_pad = routed ? a.f_pad : a.f_pad_sh;
+#pragma unroll
+  for (int i = 0; i < HB; ++i) {
+    const int rb = WR * i + wr;
+#pragma unroll
+    for (int n = 0; n < 2; ++n) {
+      const int f = c * kChunkUnits + 32 * wc + 16 * n + (lane & 15);
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int row = 16 * rb + 4 * (lane >> 4) + r;
+        if (row < tr.n) act[static_cast<size_t>(tr.p0 + row) * f_pad + f] = f2bf(silu(ag[i][n][r]) * au[i][n][r]);
+      }
+    }
+  }
+}
+
+__global__ __launch_bounds__(64 * kGdWaves) void mma_gateup_dma_kernel(MmaArgs a) {
+  __shared__ __align__(16) unsigned char lds[kGdLds];
   const int wg = xcd_local(blockIdx.x, gridDim.x);
   const MmaTask tk = a.tasks[find_task(a.tasks, a.n_tasks, wg)];
   const int local = wg - tk.wg_begin;
@@ -2141,102 +2305,12 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(RB <= 4 ? 3
   const int c = tk.chunk_lo + local / tk.m_tiles;
   const TileRows tr = tile_rows(a, tk, mt);
   if (tr.n <= 0) return;  // uniform over the work-group
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int d = a.d;
-  const int ksteps = d / 32;
-  const int nslab = (ksteps + 3) / 4;
-  const bool routed = tk.expert >= 0;
-  // staging: piece p = tid + 256 i of a slab is row p / 16, k 8 (p % 16);
-  // rows past the tile's real ones repeat its last row (staged, never stored)
-  // (one branch for the whole tile, so that the RB slot loads are in
-  // flight together)
-  int tok[RB];
-  if (routed) {
-#pragma unroll
-    for (int i = 0; i < RB; ++i) tok[i] = a.perm[tr.p0 + min((tid >> 4) + 16 * i, tr.n - 1)];
-#pragma unroll
-    for (int i = 0; i < RB; ++i) tok[i] /= a.K;
-  } else {
-#pragma unroll
-    for (int i = 0; i < RB; ++i) tok[i] = tr.p0 + min((tid >> 4) + 16 * i, tr.n - 1);
-  }
-  size_t hoff[RB];
-#pragma unroll
-  for (int i = 0; i < RB; ++i) hoff[i] = static_cast<size_t>(tok[i]) * d + 8 * (tid & 15);
-  const uint16_t* h = static_cast<const uint16_t*>(a.h);
-  const uint16_t* G = reinterpret_cast<const uint16_t*>(tk.base + static_cast<size_t>(c) * a.chunk_bytes);
-  const uint16_t* U = G + static_cast<size_t>(kChunkUnits) * d;
-  const int unit = 16 * wave + (lane & 15);  // this lane's B column
-  const int kq = 8 * (lane >> 4);
-  uint4 ast[RB];
-  auto load_a = [&](int sl) {
-    const int k0 = min(min(sl, nslab - 1) * kGuSlab, d - kGuSlab);  // past the last slab: reloaded, not used
-#pragma unroll
-    for (int i = 0; i < RB; ++i) ast[i] = ld16(h + hoff[i] + k0);
-  };
-  auto store_a = [&](int buf) {
-#pragma unroll
-    for (int i = 0; i < RB; ++i)
-      *reinterpret_cast<uint4*>(&As[buf][((tid >> 4) + 16 * i) * kGuPitch + 8 * (tid & 15)]) = ast[i];
-  };
-  auto load_b = [&](int sl, uint4(&b)[4][2]) {
-#pragma unroll
-    for (int s = 0; s < 4; ++s) {
-      const int k = min(4 * sl + s, ksteps - 1) * 32;  // clamped past the last step
-      const size_t off = (static_cast<size_t>(k / kKTile) * kChunkUnits + unit) * kKTile + (k % kKTile) + kq;
-      b[s][0] = ldw16(G + off);
-      b[s][1] = ldw16(U + off);
-    }
-  };
-  f32x4_t ag[RB], au[RB];
-#pragma unroll
-  for (int rb = 0; rb < RB; ++rb) ag[rb] = au[rb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-  uint4 b0[4][2], b1[4][2];
-  load_a(0);
-  load_b(0, b0);
-  store_a(0);
-  load_a(1);
-  load_b(1, b1);
-  __syncthreads();
-  // one slab: compute sl with b (which then takes slab sl + 2), stage
-  // sl + 1.  Every row block is computed, also past the tile's real rows
-  // (their results are not stored): a branch per block would make the
-  // compiler wait for every load in flight at each of them.
-  auto slab = [&](int sl, uint4(&b)[4][2]) {
-    const int buf = sl & 1;
-#pragma unroll
-    for (int s = 0; s < 4; ++s) {
-      bf16x8_t A[RB];
-#pragma unroll
-      for (int rb = 0; rb < RB; ++rb)
-        A[rb] = as_bf16x8(
-            *reinterpret_cast<const uint4*>(&As[buf][(16 * rb + (lane & 15)) * kGuPitch + 32 * s + kq]));
-#pragma unroll
-      for (int rb = 0; rb < RB; ++rb) {
-        ag[rb] = mfma16(A[rb], as_bf16x8(b[s][0]), ag[rb]);
-        au[rb] = mfma16(A[rb], as_bf16x8(b[s][1]), au[rb]);
-      }
-    }
-    store_a(buf ^ 1);  // after the last slab: the clamped reload, never read
-    load_a(sl + 2);
-    load_b(sl + 2, b);
-    __syncthreads();
-  };
-  for (int sl = 0; sl < nslab; sl += 2) {  // nslab is even (d % 256 == 0)
-    slab(sl, b0);
-    slab(sl + 1, b1);
-  }
-  uint16_t* act = routed ? a.act : a.act_sh + static_cast<size_t>(-1 - tk.expert) * a.rows_shared * a.f_pad_sh;
-  const int f_pad = routed ? a.f_pad : a.f_pad_sh;
-  const int f = c * kChunkUnits + unit;
-#pragma unroll
-  for (int rb = 0; rb < RB; ++rb) {
-#pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int row = 16 * rb + 4 * (lane >> 4) + r;
-      if (row < tr.n) act[static_cast<size_t>(tr.p0 + row) * f_pad + f] = f2bf(silu(ag[rb][r]) * au[rb][r]);
-    }
-  }
+  if (tr.n <= 64)
+    gd_tile<4>(a, tk, c, tr, lds);
+  else if (tr.n <= 128)
+    gd_tile<8>(a, tk, c, tr, lds);
+  else
+    gd_tile<12>(a, tk, c, tr, lds);
 }
 
 // Work-group barrier that orders LDS only: a __syncthreads() also orders
@@ -2631,10 +2705,8 @@ hipError_t launch_mma_gateup(const MmaArgs& a, hipStream_t s) {
   }
   if (a.gu_split == 4)
     hipLaunchKernelGGL(mma_gateup_kernel<1>, dim3(a.n_wg), dim3(256), kGuardLds, s, a);
-  else if (a.gu_split == 1 && a.d % (2 * kGuSlab) == 0 && a.tile_rows == 2 * kMmaRows)
-    hipLaunchKernelGGL(mma_gateup_rows_kernel<8>, dim3(a.n_wg), dim3(256), 0, s, a);
-  else if (a.gu_split == 1 && a.d % (2 * kGuSlab) == 0 && a.tile_rows == kMmaRows)
-    hipLaunchKernelGGL(mma_gateup_rows_kernel<4>, dim3(a.n_wg), dim3(256), 0, s, a);
+  else if (a.gu_split == 1 && a.d % (2 * kGdSlab) == 0 && a.tile_rows <= kGdMaxRows)
+    hipLaunchKernelGGL(mma_gateup_dma_kernel, dim3(a.n_wg), dim3(64 * kGdWaves), 0, s, a);
   else if (a.gu_split == 1 && a.tile_rows == kMmaRows)
     hipLaunchKernelGGL(mma_gateup_kernel<4>, dim3(a.n_wg), dim3(256), kGuardLds, s, a);
   else

@@ -963,28 +963,21 @@ ms_status prefill_experts(ms_ctx* ctx, int layer, const void* h_dev, int T, cons
     }
     return MS_OK;
   };
-  // bf16 gate/up: experts with many rows take 128-row tiles (each weight
-  // fragment then feeds twice the rows) when those tiles still fill the GPU;
-  // the rest keep 64-row tiles.  The tile height changes no result.
+  // bf16 gate/up with d % 128 == 0: row tiles of up to kGdMaxRows rows, so
+  // that an expert's rows usually fit one tile and its weights are read once
+  // (the kernel sizes each work-group to its tile), when those tiles fill the
+  // GPU; otherwise 64-row tiles, split four ways per chunk when even those
+  // are few.  The tile height changes no result.
   auto launch = [&](const std::vector<msk::MmaTask>& tasks, hipStream_t st, bool down) -> ms_status {
-    if (down || s.bits != 0 || s.d % 256 != 0) return launch_group(tasks, st, down, msk::kMmaRows);
-    std::vector<msk::MmaTask> tall, rest;
-    int tall_tiles = 0;
-    for (const msk::MmaTask& t : tasks) {
-      const int n = rows_of(t.expert);
-      if (n >= msk::kTallTileRows) {
-        msk::MmaTask t2 = t;
-        t2.m_tiles = (n + msk::kTallTileRows - 1) / msk::kTallTileRows;
-        tall_tiles += t2.m_tiles * t2.n_chunks;
-        tall.push_back(t2);
-      } else {
-        rest.push_back(t);
-      }
+    if (down || s.bits != 0 || s.d % 128 != 0) return launch_group(tasks, st, down, msk::kMmaRows);
+    std::vector<msk::MmaTask> tall = tasks;
+    int tiles = 0;
+    for (msk::MmaTask& t : tall) {
+      t.m_tiles = (rows_of(t.expert) + msk::kGdMaxRows - 1) / msk::kGdMaxRows;
+      tiles += t.m_tiles * t.n_chunks;
     }
-    if (tall_tiles < msk::kGuSplitBelow) return launch_group(tasks, st, false, msk::kMmaRows);
-    ms_status r = launch_group(tall, st, false, msk::kTallTileRows);
-    if (r != MS_OK || rest.empty()) return r;
-    return launch_group(rest, st, false, msk::kMmaRows);
+    if (tiles < msk::kGuSplitBelow) return launch_group(tasks, st, false, msk::kMmaRows);
+    return launch_group(tall, st, false, msk::kGdMaxRows);
   };
   auto task = [](const unsigned char* base, const unsigned char* base2, int e, int lo, int n, int split, int mt) {
     msk::MmaTask t{};

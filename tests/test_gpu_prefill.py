@@ -13,6 +13,11 @@ torch = pytest.importorskip("torch")
 
 TINY_BF16 = synth.ModelShape("tiny-bf16", 1, 256, 512, 8, 2, "bf16")
 TINY_SHARED = synth.ModelShape("tiny-bf16-shared", 2, 256, 384, 16, 4, "bf16", n_shared=2, d_ff_shared=320)
+# 32 chunks per expert and a skewed router: at T = 300 and 400 the experts
+# hold 0 .. 389 rows, so the LDS-staged gate/up launch (at least 256 tiles of
+# up to 192 rows) runs 64-, 128- and 192-row tiles and hot experts span two
+# and three tiles
+SKEWED = synth.ModelShape("skewed-bf16", 1, 256, 2048, 8, 2, "bf16", zipf=0.8)
 
 
 def _ms():
@@ -108,3 +113,27 @@ def test_prefill_shared_experts_decode_and_prefill(rig):
         for flags in (ms.MS_FWD_MATRIX_CORES, ms.MS_FWD_NO_MATRIX_CORES):
             y, idx, w = _run(r, h, 64, flags, layer=1)
             check_layer(r, 1, hf, y, idx, w)
+
+
+@pytest.mark.parametrize("T", [300, 400])
+def test_prefill_tall_tiles_parity_and_residency(T):
+    """All experts resident: the staged gate/up kernel's tiles of every
+    height match the oracle; with experts split or streamed, their chunks
+    go through the other gate/up kernel, and no output bit changes."""
+    ms = _ms()
+    from workload import SplitRig
+    shape = SKEWED
+    with SplitRig(shape, seed=7, max_tokens=400, budget_bytes=8 * shape.expert_bytes) as r:
+        h, hf = r.hidden(T, tag=T)
+        _configure(r, 1.0, list(range(8)))
+        y0, idx0, w0 = _run(r, h, T, ms.MS_FWD_MATRIX_CORES)
+        counts = np.bincount(idx0.cpu().numpy().reshape(-1), minlength=8)
+        tiles = [min(192, n - t) for n in counts for t in range(0, n, 192)]
+        assert counts.max() > 192 and len(tiles) * 32 >= 256
+        assert {(n + 63) // 64 for n in tiles} == {1, 2, 3}  # 64-, 128- and 192-row tiles
+        check_layer(r, 0, hf, y0, idx0, w0)
+        for ratio, tops in ((0.5, [0, 2, 4, 6]), (0.0, []), (0.25, [1, 3, 5, 7]), (1.0, list(range(8)))):
+            _configure(r, ratio, tops)
+            y, idx, w = _run(r, h, T, ms.MS_FWD_MATRIX_CORES)
+            assert torch.equal(idx, idx0)
+            assert torch.equal(y, y0), "r=%s tops=%s" % (ratio, tops)
