@@ -2423,6 +2423,163 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void m
   }
 }
 
+// down with both operands staged by direct global -> LDS loads, in the ring
+// of the staged gate/up kernel: one stage per chunk (64 units), a work-group
+// takes a row tile of up to kGdMaxRows rows (64, 128 or 192 by its rows) x
+// kMmaCols columns over all of the expert's chunks.  The down rows of a chunk
+// are staged as they sit in memory (unit-major); the B fragments (8 units of
+// one column) come out of LDS with transposing reads (ds_read_b64_tr_b16: in
+// each 16-lane group, lanes 4 r .. 4 r + 3 give row r of a 4 x 16 tile of
+// 16-bit values and lane i receives its column i), two per fragment.  The 16
+// byte slots of staged down row u are permuted by 2 (u % 4), so the four
+// rows a 16-lane transposing read touches fall in distinct banks.  The waves
+// split the tile kGdWaves / 2 x 2: wave (wr, wc) takes the row blocks wr, wr
+// + kGdWaves / 2, ... and columns 128 wc .. 128 wc + 127.  The k order of
+// every sum (chunks in order, 32 units per MFMA, the same units in the same
+// lanes) is that of mma_down_kernel, so the two give the same bits.
+constexpr int kDdRowBytes = 2 * kMmaCols;                    // one staged down row
+constexpr int kDdBBytes = kChunkUnits * kDdRowBytes;         // the down rows of a stage
+static_assert(kGdWaves == 8 && kMmaCols == 256, "wave split of the staged down kernel");
+
+typedef short v4i16_t __attribute__((ext_vector_type(4)));
+
+// 4 x 16 transposing read (see above) at LDS byte address p
+__device__ __forceinline__ v4i16_t lds_read_tr16(const unsigned char* p) {
+  return __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+      (__attribute__((address_space(3))) v4i16_t*)((const __attribute__((address_space(3))) unsigned char*)(p)));
+}
+
+template <int RB>
+__device__ __forceinline__ void dd_tile(const MmaArgs& a, const MmaTask& tk, int col0, const TileRows& tr,
+                                        unsigned char* lds) {
+  constexpr int WR = kGdWaves / 2;                   // row groups of waves
+  constexpr int NA = 2 * RB / kGdWaves;              // activation loads per wave and stage
+  constexpr int ND = kDdBBytes / kGdLoadBytes / kGdWaves;  // down loads per wave and stage
+  constexpr int NL = NA + ND;
+  constexpr int HB = RB / WR;                        // row blocks per wave
+  constexpr int NF = kMmaCols / 32;                  // column blocks of 16 per wave
+  constexpr int ABYTES = RB * kGdBlockBytes;
+  constexpr int SBYTES = ABYTES + kDdBBytes;
+  constexpr int NST = kGdLds / SBYTES;
+  static_assert(RB % WR == 0 && (2 * RB) % kGdWaves == 0 && RB <= kGdMaxRB, "row blocks");
+  static_assert(NST >= 2 && (NST - 2) * NL < 64, "ring depth");
+  const int lane = threadIdx.x & 63;
+  const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int wr = w >> 1, wc = w & 1;
+  const int d = a.d, nc = tk.n_chunks;
+  const bool routed = tk.expert >= 0;
+  const uint16_t* act = routed ? a.act : a.act_sh + static_cast<size_t>(-1 - tk.expert) * a.rows_shared * a.f_pad_sh;
+  const int f_pad = routed ? a.f_pad : a.f_pad_sh;
+  // activation loads: as in the gate/up kernel (8 rows of one chunk's 64 units)
+  const int lrow = lane >> 3;
+  const uint16_t* asrc[NA];
+#pragma unroll
+  for (int j = 0; j < NA; ++j) {
+    const int r = min(8 * (w + kGdWaves * j) + lrow, tr.n - 1);  // rows past the tile repeat its last (never stored)
+    asrc[j] = act + static_cast<size_t>(tr.p0 + r) * f_pad + 8 * ((lane & 7) ^ lrow);
+  }
+  // down loads: 2 rows of 512 bytes each; lane -> row lane / 32, slot lane
+  // % 32, which holds piece (lane % 32) ^ (2 (row % 4))
+  int doff[ND];
+#pragma unroll
+  for (int j = 0; j < ND; ++j) {
+    const int u = 2 * (w + kGdWaves * j) + (lane >> 5);
+    doff[j] = u * d + col0 + 8 * ((lane & 31) ^ (2 * (u & 3)));
+  }
+  const uint32_t lbase = lds_address(lds) + w * kGdLoadBytes;
+  auto issue = [&](int c, int buf) {  // chunks past the last reload it (in bounds, never read)
+    c = min(c, nc - 1);
+    const uint32_t st = lbase + buf * SBYTES;
+#pragma unroll
+    for (int j = 0; j < NA; ++j) lds_load16(asrc[j] + c * kChunkUnits, st + kGdWaves * j * kGdLoadBytes);
+    const uint16_t* D = reinterpret_cast<const uint16_t*>((c < tk.split ? tk.base : tk.base2) +
+                                                          static_cast<size_t>(c) * a.chunk_bytes) +
+                        2 * static_cast<size_t>(kChunkUnits) * d;
+#pragma unroll
+    for (int j = 0; j < ND; ++j) lds_load16(D + doff[j], st + ABYTES + kGdWaves * j * kGdLoadBytes);
+  };
+  // fragment reads: activations as in the gate/up kernel; down fragments of
+  // k step s and column block nf: lane (q = lane / 16, r = lane / 4 % 4, j =
+  // lane % 4) reads units 32 s + 8 q + r (+ 4) at columns 16 nf + 4 j .. + 3,
+  // whose slot is 16 wc + 2 (nf ^ r) + j / 2 (nf ^ r = 4 (nf / 4) + (nf % 4
+  // ^ r))
+  int fo[2];
+#pragma unroll
+  for (int s = 0; s < 2; ++s) fo[s] = (lane & 15) * kGdRowBytes + 16 * ((4 * s + (lane >> 4)) ^ (lane & 7));
+  const int tq = lane >> 4, tr4 = (lane >> 2) & 3, tj = lane & 3;
+  const int tbase = ABYTES + (8 * tq + tr4) * kDdRowBytes + 16 * (16 * wc + (tj >> 1)) + 8 * (tj & 1);
+  int tx[4];
+#pragma unroll
+  for (int b = 0; b < 4; ++b) tx[b] = tbase + 32 * (b ^ tr4);
+  f32x4_t acc[HB][NF];
+#pragma unroll
+  for (int i = 0; i < HB; ++i)
+#pragma unroll
+    for (int n = 0; n < NF; ++n) acc[i][n] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  auto compute = [&](int buf) {
+    const unsigned char* st = lds + buf * SBYTES;
+#pragma unroll
+    for (int s = 0; s < 2; ++s) {
+      bf16x8_t B[NF];
+#pragma unroll
+      for (int n = 0; n < NF; ++n) {
+        const unsigned char* p = st + tx[n & 3] + 128 * (n >> 2) + 32 * s * kDdRowBytes;
+        const v4i16_t lo = lds_read_tr16(p), hi = lds_read_tr16(p + 4 * kDdRowBytes);
+        B[n] = __builtin_bit_cast(bf16x8_t, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+      }
+      const unsigned char* sa = st + wr * kGdBlockBytes + fo[s];
+#pragma unroll
+      for (int i = 0; i < HB; ++i) {
+        const bf16x8_t A = lds_frag(sa + WR * i * kGdBlockBytes);
+#pragma unroll
+        for (int n = 0; n < NF; ++n) acc[i][n] = mfma16(A, B[n], acc[i][n]);
+      }
+    }
+  };
+#pragma unroll
+  for (int p = 0; p < NST - 1; ++p) issue(p, p);
+  int cur = 0, nxt = NST - 1;
+  for (int c = 0; c < nc; ++c) {
+    wait_vm<(NST - 2) * NL>();
+    bare_barrier();
+    issue(c + NST - 1, nxt);
+    compute(cur);
+    cur = cur + 1 == NST ? 0 : cur + 1;
+    nxt = nxt + 1 == NST ? 0 : nxt + 1;
+  }
+  wait_vm<0>();  // the reloads past the last chunk land before the work-group ends
+  float* out = routed ? a.part : a.part_sh + static_cast<size_t>(-1 - tk.expert) * a.sh_plane;
+#pragma unroll
+  for (int i = 0; i < HB; ++i) {
+    const int rb = WR * i + wr;
+#pragma unroll
+    for (int n = 0; n < NF; ++n) {
+      const int col = col0 + 128 * wc + 16 * n + (lane & 15);
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int row = 16 * rb + 4 * (lane >> 4) + r;
+        if (row < tr.n) out[static_cast<size_t>(tr.p0 + row) * d + col] = acc[i][n][r];
+      }
+    }
+  }
+}
+
+__global__ __launch_bounds__(64 * kGdWaves) void mma_down_dma_kernel(MmaArgs a) {
+  __shared__ __align__(16) unsigned char lds[kGdLds];
+  const int wg = xcd_local(blockIdx.x, gridDim.x);
+  const MmaTask tk = a.tasks[find_task(a.tasks, a.n_tasks, wg)];
+  const int local = wg - tk.wg_begin;
+  const int mt = local / a.ncb, cb = local % a.ncb;
+  const TileRows tr = tile_rows(a, tk, mt);
+  if (tr.n <= 0) return;  // uniform over the work-group
+  if (tr.n <= 64)
+    dd_tile<4>(a, tk, cb * kMmaCols, tr, lds);
+  else if (tr.n <= 128)
+    dd_tile<8>(a, tk, cb * kMmaCols, tr, lds);
+  else
+    dd_tile<12>(a, tk, cb * kMmaCols, tr, lds);
+}
+
 // ------------------------------------------- prefill MFMA over b-bit chunks
 //
 // The matrix cores take the code pairs as they are: a B fragment of eight
@@ -2727,7 +2884,12 @@ hipError_t launch_mma_down(const MmaArgs& a, hipStream_t s) {
       return hipErrorInvalidValue;
     return hipGetLastError();
   }
-  hipLaunchKernelGGL(mma_down_kernel, dim3(a.n_wg), dim3(256), 0, s, a);
+  if (a.tile_rows == kGdMaxRows && a.d % kMmaCols == 0)
+    hipLaunchKernelGGL(mma_down_dma_kernel, dim3(a.n_wg), dim3(64 * kGdWaves), 0, s, a);
+  else if (a.tile_rows == kMmaRows)
+    hipLaunchKernelGGL(mma_down_kernel, dim3(a.n_wg), dim3(256), 0, s, a);
+  else
+    return hipErrorInvalidValue;
   return hipGetLastError();
 }
 

@@ -968,16 +968,17 @@ ms_status prefill_experts(ms_ctx* ctx, int layer, const void* h_dev, int T, cons
   // (the kernel sizes each work-group to its tile), when those tiles fill the
   // GPU; otherwise 64-row tiles, split four ways per chunk when even those
   // are few.  The tile height changes no result.
+  // The bf16 down projection with d % kMmaCols == 0 always takes such tiles.
   auto launch = [&](const std::vector<msk::MmaTask>& tasks, hipStream_t st, bool down) -> ms_status {
-    if (down || s.bits != 0 || s.d % 128 != 0) return launch_group(tasks, st, down, msk::kMmaRows);
+    if (s.bits != 0 || s.d % (down ? msk::kMmaCols : 128) != 0) return launch_group(tasks, st, down, msk::kMmaRows);
     std::vector<msk::MmaTask> tall = tasks;
     int tiles = 0;
     for (msk::MmaTask& t : tall) {
       t.m_tiles = (rows_of(t.expert) + msk::kGdMaxRows - 1) / msk::kGdMaxRows;
       tiles += t.m_tiles * t.n_chunks;
     }
-    if (tiles < msk::kGuSplitBelow) return launch_group(tasks, st, false, msk::kMmaRows);
-    return launch_group(tall, st, false, msk::kGdMaxRows);
+    if (!down && tiles < msk::kGuSplitBelow) return launch_group(tasks, st, false, msk::kMmaRows);
+    return launch_group(tall, st, down, msk::kGdMaxRows);
   };
   auto task = [](const unsigned char* base, const unsigned char* base2, int e, int lo, int n, int split, int mt) {
     msk::MmaTask t{};

@@ -137,3 +137,24 @@ def test_prefill_tall_tiles_parity_and_residency(T):
             y, idx, w = _run(r, h, T, ms.MS_FWD_MATRIX_CORES)
             assert torch.equal(idx, idx0)
             assert torch.equal(y, y0), "r=%s tops=%s" % (ratio, tops)
+
+
+@pytest.mark.parametrize("d", [320, 384])
+def test_prefill_widths_off_the_staged_kernels(d):
+    """d % 256 != 0 keeps the down projection on the 64-row kernel, and d =
+    320 (d % 128 != 0) the gate/up too; oracle parity and outputs bitwise
+    independent of residency there as well."""
+    ms = _ms()
+    from workload import SplitRig
+    shape = synth.ModelShape("odd-d-bf16", 1, d, 2048, 8, 2, "bf16", zipf=0.8)
+    T = 256
+    with SplitRig(shape, seed=8, max_tokens=T, budget_bytes=8 * shape.expert_bytes) as r:
+        h, hf = r.hidden(T, tag=d)
+        _configure(r, 1.0, list(range(8)))
+        y0, idx0, w0 = _run(r, h, T, ms.MS_FWD_MATRIX_CORES)
+        check_layer(r, 0, hf, y0, idx0, w0)
+        for ratio, tops in ((0.5, [1, 2, 5, 6]), (0.0, [])):
+            _configure(r, ratio, tops)
+            y, idx, w = _run(r, h, T, ms.MS_FWD_MATRIX_CORES)
+            assert torch.equal(idx, idx0)
+            assert torch.equal(y, y0), "r=%s tops=%s" % (ratio, tops)
