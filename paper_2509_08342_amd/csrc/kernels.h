@@ -217,12 +217,39 @@ struct MmaArgs {
                                // into its own partial plane [row][ksplit][d]; 1 for bf16
   int32_t tile_rows;           // rows per row tile: kMmaRows, or kGdMaxRows for the bf16 gate/up of
                                // whole chunks (gu_split 1, d % 128 == 0)
+  // tasks planned on the device (launch_prefill_plan), or null for `tasks`:
+  // dtasks[dcount[0]] over dcount[1] work-groups; the grid is an upper bound
+  // and work-groups past dcount[1] exit (LDS-staged kernels only)
+  const MmaTask* dtasks;
+  const int32_t* dcount;
   MmaTask tasks[kMaxMmaTasks];
 };
 // kernel arguments of this size were measured to reach the kernels intact
 static_assert(sizeof(MmaArgs) <= 8000, "matrix-core kernel arguments within 8000 bytes");
 hipError_t launch_mma_gateup(const MmaArgs& a, hipStream_t s);
 hipError_t launch_mma_down(const MmaArgs& a, hipStream_t s);
+
+// Prefill work planned on the device right after the routing, so that the
+// resident experts' matrix-core launches need no host round trip: for every
+// routed expert with tokens and resident chunks, a gate/up task over those
+// chunks, and a down task when all of its chunks are resident; for every
+// shared expert, both.  Row tiles of tile_rows rows; tasks in expert order,
+// then the shared experts.  One work-group of kMaxPlanTasks threads.
+constexpr int kMaxPlanTasks = 256;   // routed + shared experts of a planned forward
+constexpr int kMaxPlanShared = 4;
+struct PlanArgs {
+  const int32_t* offsets;            // [E+1] grouping offsets of this forward
+  MmaTask* gu;                       // [kMaxPlanTasks] out
+  MmaTask* dn;                       // [kMaxPlanTasks] out
+  int32_t* counts;                   // [4] out: gate/up tasks and work-groups, down tasks and work-groups
+  const unsigned char* cache_base;   // top of routed expert e at cache_base + top_bytes * slot[e]
+  uint64_t top_bytes;
+  const unsigned char* shared[kMaxPlanShared];
+  int32_t E, T, n_chunks, n_chunks_sh, n_sh, ncb, tile_rows;
+  int16_t res[kMaxPlanTasks];        // resident chunks of routed expert e (a snapshot at launch)
+  int16_t slot[kMaxPlanTasks];       // its cache slot (when res[e] > 0)
+};
+hipError_t launch_prefill_plan(const PlanArgs& a, hipStream_t s);
 
 // Host-to-device copy of `bytes` (a multiple of 16; both addresses 16-byte
 // aligned) from pinned host memory that the device can address (src is its

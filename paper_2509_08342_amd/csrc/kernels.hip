@@ -2296,11 +2296,28 @@ __device__ __forceinline__ void gd_tile(const MmaArgs& a, const MmaTask& tk, int
   }
 }
 
+// this work-group's task and its index within the task, from the kernel
+// arguments or from tasks planned on the device; false past the planned ones
+__device__ __forceinline__ bool staged_task(const MmaArgs& a, MmaTask& tk, int& local) {
+  int wg;
+  if (a.dtasks) {
+    const int n_wg = a.dcount[1];
+    if (static_cast<int>(blockIdx.x) >= n_wg) return false;
+    wg = xcd_local(blockIdx.x, n_wg);
+    tk = a.dtasks[find_task(a.dtasks, a.dcount[0], wg)];
+  } else {
+    wg = xcd_local(blockIdx.x, gridDim.x);
+    tk = a.tasks[find_task(a.tasks, a.n_tasks, wg)];
+  }
+  local = wg - tk.wg_begin;
+  return true;
+}
+
 __global__ __launch_bounds__(64 * kGdWaves) void mma_gateup_dma_kernel(MmaArgs a) {
   __shared__ __align__(16) unsigned char lds[kGdLds];
-  const int wg = xcd_local(blockIdx.x, gridDim.x);
-  const MmaTask tk = a.tasks[find_task(a.tasks, a.n_tasks, wg)];
-  const int local = wg - tk.wg_begin;
+  MmaTask tk;
+  int local;
+  if (!staged_task(a, tk, local)) return;
   const int mt = local % tk.m_tiles;
   const int c = tk.chunk_lo + local / tk.m_tiles;
   const TileRows tr = tile_rows(a, tk, mt);
@@ -2566,9 +2583,9 @@ __device__ __forceinline__ void dd_tile(const MmaArgs& a, const MmaTask& tk, int
 
 __global__ __launch_bounds__(64 * kGdWaves) void mma_down_dma_kernel(MmaArgs a) {
   __shared__ __align__(16) unsigned char lds[kGdLds];
-  const int wg = xcd_local(blockIdx.x, gridDim.x);
-  const MmaTask tk = a.tasks[find_task(a.tasks, a.n_tasks, wg)];
-  const int local = wg - tk.wg_begin;
+  MmaTask tk;
+  int local;
+  if (!staged_task(a, tk, local)) return;
   const int mt = local / a.ncb, cb = local % a.ncb;
   const TileRows tr = tile_rows(a, tk, mt);
   if (tr.n <= 0) return;  // uniform over the work-group
@@ -2848,7 +2865,88 @@ __global__ __launch_bounds__(256) void mma_down_q_kernel(MmaArgs a) {
   }
 }
 
+// Prefill plan (see launch_prefill_plan): thread i takes routed expert i,
+// or shared expert i - E; exclusive scans over the threads give each task
+// its index and first work-group.
+__global__ __launch_bounds__(kMaxPlanTasks) void prefill_plan_kernel(PlanArgs p) {
+  __shared__ int4 sc[2][kMaxPlanTasks];
+  const int i = threadIdx.x;
+  MmaTask t{};
+  int gu_w = 0, dn_w = 0, gu_c = 0, dn_c = 0;
+  if (i < p.E) {
+    const int n = p.offsets[i + 1] - p.offsets[i];
+    const int res = p.res[i];
+    if (n > 0 && res > 0) {
+      t.base = p.cache_base + p.top_bytes * static_cast<uint64_t>(p.slot[i]);
+      t.expert = i;
+      t.m_tiles = (n + p.tile_rows - 1) / p.tile_rows;
+      gu_c = res;
+      gu_w = t.m_tiles * res;
+      if (res >= p.n_chunks) {
+        dn_c = p.n_chunks;
+        dn_w = t.m_tiles * p.ncb;
+      }
+    }
+  } else if (i < p.E + p.n_sh && p.T > 0) {
+    const int sh = i - p.E;
+    t.base = p.shared[sh];
+    t.expert = -1 - sh;
+    t.m_tiles = (p.T + p.tile_rows - 1) / p.tile_rows;
+    gu_c = dn_c = p.n_chunks_sh;
+    gu_w = t.m_tiles * p.n_chunks_sh;
+    dn_w = t.m_tiles * p.ncb;
+  }
+  // inclusive scan of (gate/up task, gate/up work-groups, down task, down work-groups)
+  int4 v = make_int4(gu_w > 0, gu_w, dn_w > 0, dn_w);
+  int cur = 0;
+  sc[0][i] = v;
+  __syncthreads();
+  for (int off = 1; off < kMaxPlanTasks; off <<= 1) {
+    if (i >= off) {
+      const int4 o = sc[cur][i - off];
+      v = make_int4(v.x + o.x, v.y + o.y, v.z + o.z, v.w + o.w);
+    }
+    sc[cur ^ 1][i] = v;
+    cur ^= 1;
+    __syncthreads();
+  }
+  t.base2 = t.base;
+  if (gu_w > 0) {
+    MmaTask g = t;
+    g.n_chunks = gu_c;
+    g.wg_begin = v.y - gu_w;
+    p.gu[v.x - 1] = g;
+  }
+  if (dn_w > 0) {
+    MmaTask g = t;
+    g.n_chunks = dn_c;
+    g.split = dn_c;  // every chunk from base
+    g.wg_begin = v.w - dn_w;
+    p.dn[v.z - 1] = g;
+  }
+  if (i == kMaxPlanTasks - 1) {
+    p.counts[0] = v.x;
+    p.counts[1] = v.y;
+    p.counts[2] = v.z;
+    p.counts[3] = v.w;
+  }
+}
+
+hipError_t launch_prefill_plan(const PlanArgs& a, hipStream_t s) {
+  if (a.E < 0 || a.n_sh < 0 || a.n_sh > kMaxPlanShared || a.E + a.n_sh > kMaxPlanTasks || a.tile_rows <= 0)
+    return hipErrorInvalidValue;
+  hipLaunchKernelGGL(prefill_plan_kernel, dim3(1), dim3(kMaxPlanTasks), 0, s, a);
+  return hipGetLastError();
+}
+
 hipError_t launch_mma_gateup(const MmaArgs& a, hipStream_t s) {
+  if (a.dtasks) {
+    if (a.n_wg <= 0) return hipSuccess;
+    if (a.bits != 0 || a.gu_split != 1 || a.d % (2 * kGdSlab) != 0 || a.tile_rows > kGdMaxRows || !a.dcount)
+      return hipErrorInvalidValue;
+    hipLaunchKernelGGL(mma_gateup_dma_kernel, dim3(a.n_wg), dim3(64 * kGdWaves), 0, s, a);
+    return hipGetLastError();
+  }
   if (a.n_wg <= 0 || a.n_tasks <= 0) return hipSuccess;
   if (a.bits != 0) {
     if (a.gu_split != 1 || !q_supported(a.d)) return hipErrorInvalidValue;
@@ -2872,6 +2970,13 @@ hipError_t launch_mma_gateup(const MmaArgs& a, hipStream_t s) {
 }
 
 hipError_t launch_mma_down(const MmaArgs& a, hipStream_t s) {
+  if (a.dtasks) {
+    if (a.n_wg <= 0) return hipSuccess;
+    if (a.bits != 0 || a.ksplit != 1 || a.d % kMmaCols != 0 || a.tile_rows != kGdMaxRows || !a.dcount)
+      return hipErrorInvalidValue;
+    hipLaunchKernelGGL(mma_down_dma_kernel, dim3(a.n_wg), dim3(64 * kGdWaves), 0, s, a);
+    return hipGetLastError();
+  }
   if (a.n_wg <= 0 || a.n_tasks <= 0) return hipSuccess;
   if (a.ksplit < 1 || (a.bits == 0 && a.ksplit != 1)) return hipErrorInvalidValue;
   if (a.bits != 0) {

@@ -74,6 +74,7 @@ struct Shape {
   uint64_t off_router, off_bias, off_shared, off_logits, off_logits2, off_offsets, off_perm, off_pos;
   uint64_t off_part, off_part_sh, off_red, off_act, off_act_sh, off_score, off_order, off_buffer, fixed_bytes;
   uint64_t off_router_t, off_lrank, off_blk, off_psc;
+  uint64_t off_plan;  // prefill tasks planned on the device: gate/up, down, counts
   int nblk_cap;  // token blocks of the many-token routing
   int down_splits;  // prefill down projection of b-bit chunks: chunk ranges (partial planes) per slot
   uint64_t router_stride, bias_stride, part_bytes, part_sh_bytes;
@@ -224,6 +225,9 @@ ms_status derive_shape(const ms_model_desc* d, Shape* s, std::string* err) {
   off += align_up(static_cast<uint64_t>(s->E) * s->nblk_cap * 4, kAlign);
   s->off_psc = off;
   off += align_up(static_cast<uint64_t>(s->E) * s->nblk_cap * 4, kAlign);
+
+  s->off_plan = off;
+  off += align_up(2 * msk::kMaxPlanTasks * sizeof(msk::MmaTask) + 4 * sizeof(int32_t), kAlign);
 
   s->off_score = off;
   off += align_up(static_cast<uint64_t>(s->E) * 4, kAlign);
@@ -904,14 +908,18 @@ ms_status order_after_last(ms_ctx* ctx, hipStream_t stream) {
 //   side stream (after that gate/up): per expert with missing chunks, issue
 //     the copies, gate/up per group as it lands, then its down projection,
 //     then release its staging slot.
-ms_status prefill_experts(ms_ctx* ctx, int layer, const void* h_dev, int T, const std::vector<int32_t>& offs,
-                          hipStream_t sm) {
+// gate + up and down bytes of one chunk (b-bit: codes and their metadata)
+uint64_t mma_gu_bytes(const Shape& s) {
+  return s.bits ? 2 * (msk::q_off_uq(s.d, s.bits) + 4ull * s.d) : 2ull * kUnits * s.d * s.elem;
+}
+uint64_t mma_dn_bytes(const Shape& s) {
+  return s.bits ? msk::q_off_uq(s.d, s.bits) + 4ull * s.d : 1ull * kUnits * s.d * s.elem;
+}
+
+// The fields of the matrix-core kernels' arguments that every launch of a
+// forward shares.
+void mma_common(ms_ctx* ctx, const void* h_dev, int T, msk::MmaArgs& ma) {
   const Shape& s = ctx->s;
-  LayerState& L = ctx->layers[layer];
-  // gate + up and down bytes of one chunk (b-bit: codes and their metadata)
-  const uint64_t gu_bytes = s.bits ? 2 * (msk::q_off_uq(s.d, s.bits) + 4ull * s.d) : 2ull * kUnits * s.d * s.elem;
-  const uint64_t dn_bytes = s.bits ? msk::q_off_uq(s.d, s.bits) + 4ull * s.d : 1ull * kUnits * s.d * s.elem;
-  msk::MmaArgs ma{};
   ma.h = h_dev;
   ma.offsets = reinterpret_cast<const int32_t*>(ctx->dev(s.off_offsets));
   ma.perm = reinterpret_cast<const int32_t*>(ctx->dev(s.off_perm));
@@ -930,6 +938,86 @@ ms_status prefill_experts(ms_ctx* ctx, int layer, const void* h_dev, int T, cons
   ma.ncb = (s.d + msk::kMmaCols - 1) / msk::kMmaCols;
   ma.bits = s.bits;
   ma.ksplit = s.down_splits;
+}
+
+// Whether the resident part of a prefill forward is planned on the device
+// (LDS-staged kernels for both projections, a task per expert within the
+// plan kernel's reach).
+bool plan_on_device(const Shape& s) {
+  return s.bits == 0 && s.dtype == MS_BF16 && s.d % msk::kMmaCols == 0 && s.n_sh <= msk::kMaxPlanShared &&
+         s.E + s.n_sh <= msk::kMaxPlanTasks;
+}
+
+// Launch the plan, then the resident experts' gate/up and down over it, on
+// sm right after the routing (work-groups past the planned ones exit).
+// Returns the timeline records of the two launches (bytes set once the
+// routing is known).
+ms_status launch_planned(ms_ctx* ctx, int layer, const void* h_dev, int T, hipStream_t sm, int* tl_gu, int* tl_dn) {
+  const Shape& s = ctx->s;
+  LayerState& L = ctx->layers[layer];
+  msk::PlanArgs pa{};
+  auto* plan = reinterpret_cast<msk::MmaTask*>(ctx->dev(s.off_plan));
+  auto* counts = reinterpret_cast<int32_t*>(plan + 2 * msk::kMaxPlanTasks);
+  pa.offsets = reinterpret_cast<const int32_t*>(ctx->dev(s.off_offsets));
+  pa.gu = plan;
+  pa.dn = plan + msk::kMaxPlanTasks;
+  pa.counts = counts;
+  pa.cache_base = L.cache_base;
+  pa.top_bytes = L.top_bytes;
+  for (int i = 0; i < s.n_sh; ++i)
+    pa.shared[i] = ctx->dev(s.off_shared + align_up(s.shared_bytes, kAlign) * (static_cast<uint64_t>(layer) * s.n_sh + i));
+  pa.E = s.E;
+  pa.T = T;
+  pa.n_chunks = s.n_chunks;
+  pa.n_chunks_sh = s.n_chunks_sh;
+  pa.n_sh = s.n_sh;
+  pa.ncb = (s.d + msk::kMmaCols - 1) / msk::kMmaCols;
+  pa.tile_rows = msk::kGdMaxRows;
+  // upper bounds of the work-groups: sum over experts of resident chunks x
+  // ceil(rows / tile) <= resident chunks + chunks x ceil(T K / tile)
+  const int extra_tiles = static_cast<int>((static_cast<int64_t>(T) * s.K + msk::kGdMaxRows - 1) / msk::kGdMaxRows);
+  const int sh_tiles = (T + msk::kGdMaxRows - 1) / msk::kGdMaxRows;
+  int64_t gu_wg = static_cast<int64_t>(s.n_chunks) * extra_tiles + static_cast<int64_t>(s.n_sh) * sh_tiles * s.n_chunks_sh;
+  int64_t n_full = 0;
+  for (int e = 0; e < s.E; ++e) {
+    const int rc = resident_chunks(L, e);
+    pa.res[e] = static_cast<int16_t>(rc);
+    pa.slot[e] = static_cast<int16_t>(rc > 0 ? L.slot_of[e] : 0);
+    gu_wg += rc;
+    n_full += rc >= s.n_chunks;
+  }
+  const int64_t dn_wg = (n_full + extra_tiles + static_cast<int64_t>(s.n_sh) * sh_tiles) * pa.ncb;
+  MS_HIP(msk::launch_prefill_plan(pa, sm));
+  msk::MmaArgs ma{};
+  mma_common(ctx, h_dev, T, ma);
+  ma.tile_rows = msk::kGdMaxRows;
+  ma.gu_split = 1;
+  ma.dtasks = pa.gu;
+  ma.dcount = counts;
+  ma.n_wg = static_cast<int>(std::min<int64_t>(gu_wg, INT32_MAX));
+  *tl_gu = tl_begin(ctx, sm, MS_IV_FFN_RESIDENT, layer, 0);
+  MS_HIP(msk::launch_mma_gateup(ma, sm));
+  tl_end(ctx, *tl_gu, sm);
+  ma.dtasks = pa.dn;
+  ma.dcount = counts + 2;
+  ma.n_wg = static_cast<int>(std::min<int64_t>(dn_wg, INT32_MAX));
+  *tl_dn = tl_begin(ctx, sm, MS_IV_FFN_DOWN, layer, 0);
+  MS_HIP(msk::launch_mma_down(ma, sm));
+  tl_end(ctx, *tl_dn, sm);
+  return MS_OK;
+}
+
+// Prefill experts once the routing is known.  With `planned`, the resident
+// chunks' gate/up, the down of fully resident experts and the shared experts
+// were launched before (launch_planned); the rest goes here.
+ms_status prefill_experts(ms_ctx* ctx, int layer, const void* h_dev, int T, const std::vector<int32_t>& offs,
+                          hipStream_t sm, bool planned) {
+  const Shape& s = ctx->s;
+  LayerState& L = ctx->layers[layer];
+  const uint64_t gu_bytes = mma_gu_bytes(s);
+  const uint64_t dn_bytes = mma_dn_bytes(s);
+  msk::MmaArgs ma{};
+  mma_common(ctx, h_dev, T, ma);
   auto m_tiles = [&](int e) {
     const int n = e >= 0 ? offs[e + 1] - offs[e] : T;
     return (n + msk::kMmaRows - 1) / msk::kMmaRows;
@@ -1002,11 +1090,11 @@ ms_status prefill_experts(ms_ctx* ctx, int layer, const void* h_dev, int T, cons
     L.st.experts_active += 1;
     const int res = resident_chunks(L, e);
     const unsigned char* top = res > 0 ? L.cache_base + L.top_bytes * L.slot_of[e] : nullptr;
-    if (res > 0) gu.push_back(task(top, nullptr, e, 0, res, 0, m_tiles(e)));
+    if (res > 0 && !planned) gu.push_back(task(top, nullptr, e, 0, res, 0, m_tiles(e)));
     if (res >= s.n_chunks) {
       L.st.alpha += 1;
       complete[e] = 1;
-      dn.push_back(task(top, top, e, 0, s.n_chunks, s.n_chunks, m_tiles(e)));
+      if (!planned) dn.push_back(task(top, top, e, 0, s.n_chunks, s.n_chunks, m_tiles(e)));
       continue;
     }
     if (res > 0)
@@ -1041,13 +1129,18 @@ ms_status prefill_experts(ms_ctx* ctx, int layer, const void* h_dev, int T, cons
       b.use_order = use_counter++;  // read first, by the compute stream
     }
   }
-  for (int i = 0; i < s.n_sh; ++i) {
+  for (int i = 0; i < s.n_sh && !planned; ++i) {
     gu.push_back(task(shared_base(i), nullptr, -1 - i, 0, s.n_chunks_sh, 0, m_tiles(-1)));
     dn.push_back(task(shared_base(i), shared_base(i), -1 - i, 0, s.n_chunks_sh, s.n_chunks_sh, m_tiles(-1)));
   }
+  // the side streams below need the resident gate/up only if an expert is
+  // still missing chunks (a marker between kernels costs the stream a few
+  // microseconds)
+  bool any_missing = false;
+  for (int e = 0; e < s.E && !any_missing; ++e) any_missing = offs[e + 1] > offs[e] && !complete[e];
   ms_status st = launch(gu, sm, false);
   if (st != MS_OK) return st;
-  MS_HIP(hipEventRecord(ctx->ev_res, sm));
+  if (any_missing) MS_HIP(hipEventRecord(ctx->ev_res, sm));
   st = launch(dn, sm, true);
   if (st != MS_OK) return st;
   for (int e = 0; e < s.E; ++e) {
@@ -1063,6 +1156,7 @@ ms_status prefill_experts(ms_ctx* ctx, int layer, const void* h_dev, int T, cons
   // miss evicts them.
   // Missing experts alternate between two side streams: each expert's
   // launches are small (a few row tiles), so two run side by side.
+  if (!any_missing) return MS_OK;
   MS_HIP(hipStreamWaitEvent(ctx->side, ctx->ev_res, 0));
   MS_HIP(hipStreamWaitEvent(ctx->side2, ctx->ev_res, 0));
   for (int e = 0; e < s.E; ++e)
@@ -1701,6 +1795,14 @@ ms_status ms_forward(ms_ctx* ctx, int32_t layer, const void* h_dev, int32_t T, f
   bool prefill = s.dtype == MS_BF16 && static_cast<int64_t>(T) * s.K >= 8ll * s.E;
   if (flags & MS_FWD_MATRIX_CORES) prefill = s.dtype == MS_BF16;
   if (flags & MS_FWD_NO_MATRIX_CORES) prefill = false;
+  // prefill: the resident experts' launches are planned on the device and
+  // follow the routing at once (no host round trip)
+  const bool planned = prefill && plan_on_device(s);
+  int tl_pgu = -1, tl_pdn = -1;
+  if (planned) {
+    const ms_status pst = launch_planned(ctx, layer, h_dev, T, sm, &tl_pgu, &tl_pdn);
+    if (pst != MS_OK) return pst;
+  }
 
   // 2. segments already in VRAM (Eq. (5): processed while missing ones
   //    load): cached tops, staging-buffer groups of this layer whose copies
@@ -1818,6 +1920,17 @@ ms_status ms_forward(ms_ctx* ctx, int32_t layer, const void* h_dev, int32_t T, f
   ctx->pf_inflight.clear();  // in-flight groups complete on their own
 
   // bytes of the resident launches now that the active experts are known
+  if (tl_pgu >= 0 || tl_pdn >= 0) {
+    uint64_t gu = static_cast<uint64_t>(s.n_sh) * s.n_chunks_sh, dn = static_cast<uint64_t>(s.n_sh) * s.n_chunks_sh;
+    for (int e = 0; e < s.E; ++e) {
+      if (offs[e + 1] == offs[e]) continue;
+      const int rc = resident_chunks(L, e);
+      gu += rc;
+      if (rc >= s.n_chunks) dn += s.n_chunks;
+    }
+    if (tl_pgu >= 0) ctx->tl[tl_pgu].bytes = gu * mma_gu_bytes(s);
+    if (tl_pdn >= 0) ctx->tl[tl_pdn].bytes = dn * mma_dn_bytes(s);
+  }
   for (size_t bi = 0; bi < res_tl.size(); ++bi) {
     if (res_tl[bi] < 0) continue;
     uint64_t bytes = 0;
@@ -1968,7 +2081,7 @@ ms_status ms_forward(ms_ctx* ctx, int32_t layer, const void* h_dev, int32_t T, f
     }
   }
   } else {
-    st = prefill_experts(ctx, layer, h_dev, T, offs, sm);
+    st = prefill_experts(ctx, layer, h_dev, T, offs, sm, planned);
     if (st != MS_OK) return st;
   }
   for (BufSlot& b : ctx->buf)
