@@ -462,7 +462,7 @@ __global__ __launch_bounds__(64 * kRouteWaves) void route_kernel(RouteArgs a) { 
 // token): selection, then each slot's rank among the block's earlier slots
 // of the same expert and the block's expert counts blk[e][b]; the block's
 // prediction score sums (waves in order) into psc[b][e].
-constexpr int kSelWaves = 4;
+constexpr int kSelWaves = 16;  // one wave per token of a block of at most 16
 
 template <int QN>
 __global__ __launch_bounds__(64 * kSelWaves) void select_many_kernel(RouteArgs a, int TB) {
@@ -767,124 +767,135 @@ __global__ __launch_bounds__(64 * kRouteWaves) void route_fused_kernel(LogitsArg
 // The halving tree pairs residues l and l + 32, l + 16, l + 8 across lanes
 // m ^ 4, m ^ 2, m ^ 1 -- each level a butterfly in which the two lanes keep
 // opposite halves of the outputs -- and l + 4, + 2, + 1 inside the lane.
-constexpr int kLmTokens = 32;   // tokens per work-group (8 per wave)
-constexpr int kLmExperts = 16;  // experts per work-group
+// TT x TE is a lane's output tile: 4 x 4 (a wave 8 tokens x 16 experts),
+// or 2 x 2 (4 tokens x 8 experts) for launches that the larger tile would
+// leave with too few waves; the last level of the halving tree of the 2 x 2
+// tile adds across lanes m, m ^ 1 in both of them.
+template <int TT, int TE>
+struct LmTile {
+  static constexpr int NO = TT * TE;           // outputs per lane
+  static constexpr int TOKENS = 4 * 2 * TT;    // per work-group (4 waves)
+  static constexpr int EXPERTS = 4 * TE;       // per work-group
+  static_assert((TT == 4 && TE == 4) || (TT == 2 && TE == 2), "lane tiles");
+};
+constexpr int kLmBigBelowWgs = 512;  // 4 x 4 tiles when they give at least this many work-groups
 
-template <typename W>
+template <typename W, int TT, int TE>
 __global__ __launch_bounds__(256) void logits_many_kernel(LogitsArgs a) {
+  using Tile = LmTile<TT, TE>;
+  constexpr int NO = Tile::NO;
   constexpr int VPR = static_cast<int>(8 * sizeof(W)) / 16;  // 16-byte loads per row and step
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int m = lane & 7, o = lane >> 3;
-  const int nb = (a.E + kLmExperts - 1) / kLmExperts;
+  const int nb = (a.E + Tile::EXPERTS - 1) / Tile::EXPERTS;
   const int mat = blockIdx.y / nb, eb = blockIdx.y - mat * nb;
   const W* wt = static_cast<const W*>(mat == 0 ? a.wt : a.wt2);
   const float* bias = mat == 0 ? a.bias : a.bias2;
   float* out = mat == 0 ? a.logits : a.logits2;
-  const int tq0 = blockIdx.x * kLmTokens + 8 * wave + 4 * (o >> 2);  // this lane's first token
-  const int eq0 = eb * kLmExperts + 4 * (o & 3);                      // this lane's first expert
-  const W* hp[4];
-  const W* wp[4];
+  const int tq0 = blockIdx.x * Tile::TOKENS + 2 * TT * wave + TT * (o >> 2);  // this lane's first token
+  const int eq0 = eb * Tile::EXPERTS + TE * (o & 3);                          // this lane's first expert
+  const W* hp[TT];
+  const W* wp[TE];
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    hp[i] = static_cast<const W*>(a.h) + static_cast<size_t>(min(tq0 + i, a.T - 1)) * a.d + 8 * m;
-    wp[i] = wt + static_cast<size_t>(min(eq0 + i, a.E - 1)) * a.d + 8 * m;
-  }
-  float acc[16][8];
+  for (int i = 0; i < TT; ++i) hp[i] = static_cast<const W*>(a.h) + static_cast<size_t>(min(tq0 + i, a.T - 1)) * a.d + 8 * m;
 #pragma unroll
-  for (int q = 0; q < 16; ++q)
+  for (int i = 0; i < TE; ++i) wp[i] = wt + static_cast<size_t>(min(eq0 + i, a.E - 1)) * a.d + 8 * m;
+  float acc[NO][8];
+#pragma unroll
+  for (int q = 0; q < NO; ++q)
 #pragma unroll
     for (int k = 0; k < 8; ++k) acc[q][k] = 0.0f;
   const int steps = a.d / 64;
-  uint4 hn[4][VPR], wn[4][VPR];
-#pragma unroll
-  for (int i = 0; i < 4; ++i)
+  // the loads of P steps are in flight in P register sets, each reloaded
+  // right after its step (the last steps reload the last one: in bounds,
+  // never used); P = 2 for 4 x 4 tiles, whose accumulators take most of the
+  // registers (measured on Qwen3-shaped prefill routing: 58 -> 54 us)
+  constexpr int P = NO == 16 ? 2 : 4;
+  uint4 hs[P][TT][VPR], ws[P][TE][VPR];
+  auto load_step = [&](int st, uint4 (&hx)[TT][VPR], uint4 (&wx)[TE][VPR]) {
+    const size_t off = static_cast<size_t>(64) * min(st, steps - 1);
 #pragma unroll
     for (int v = 0; v < VPR; ++v) {
-      hn[i][v] = ld16(hp[i] + 8 / VPR * v);
-      wn[i][v] = ld16(wp[i] + 8 / VPR * v);
+#pragma unroll
+      for (int i = 0; i < TT; ++i) hx[i][v] = ld16(hp[i] + off + 8 / VPR * v);
+#pragma unroll
+      for (int i = 0; i < TE; ++i) wx[i][v] = ld16(wp[i] + off + 8 / VPR * v);
     }
-  for (int st = 0; st < steps; ++st) {
-    uint4 hc[4][VPR], wc[4][VPR];
+  };
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
-#pragma unroll
-      for (int v = 0; v < VPR; ++v) {
-        hc[i][v] = hn[i][v];
-        wc[i][v] = wn[i][v];
-      }
-    // next step's loads (the last step reloads itself: always in bounds)
-    const size_t nx = static_cast<size_t>(64) * min(st + 1, steps - 1);
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-#pragma unroll
-      for (int v = 0; v < VPR; ++v) {
-        hn[i][v] = ld16(hp[i] + nx + 8 / VPR * v);
-        wn[i][v] = ld16(wp[i] + nx + 8 / VPR * v);
-      }
-    float wf[4][8];
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
+  for (int p = 0; p < P; ++p) load_step(p, hs[p], ws[p]);
+  auto fma_step = [&](const uint4 (&hc)[TT][VPR], const uint4 (&wc)[TE][VPR]) {
+    auto to8 = [&](const uint4 (&x)[VPR], float (&f)[8]) {
       if constexpr (VPR == 1) {
-        unpack(wc[i][0], wf[i]);
+        unpack(x[0], f);
       } else {
         float lo[4], hi[4];
-        unpack(wc[i][0], lo);
-        unpack(wc[i][1], hi);
+        unpack(x[0], lo);
+        unpack(x[1], hi);
 #pragma unroll
         for (int k = 0; k < 4; ++k) {
-          wf[i][k] = lo[k];
-          wf[i][4 + k] = hi[k];
+          f[k] = lo[k];
+          f[4 + k] = hi[k];
         }
       }
-    }
+    };
+    float wf[TE][8];
 #pragma unroll
-    for (int ti = 0; ti < 4; ++ti) {
+    for (int i = 0; i < TE; ++i) to8(wc[i], wf[i]);
+#pragma unroll
+    for (int ti = 0; ti < TT; ++ti) {
       float hf[8];
-      if constexpr (VPR == 1) {
-        unpack(hc[ti][0], hf);
-      } else {
-        float lo[4], hi[4];
-        unpack(hc[ti][0], lo);
-        unpack(hc[ti][1], hi);
+      to8(hc[ti], hf);
 #pragma unroll
-        for (int k = 0; k < 4; ++k) {
-          hf[k] = lo[k];
-          hf[4 + k] = hi[k];
-        }
-      }
+      for (int ei = 0; ei < TE; ++ei)
 #pragma unroll
-      for (int ei = 0; ei < 4; ++ei)
+        for (int k = 0; k < 8; ++k) acc[TE * ti + ei][k] = fmaf(hf[k], wf[ei][k], acc[TE * ti + ei][k]);
+    }
+  };
+  int st = 0;
+  for (; st + P <= steps; st += P) {
 #pragma unroll
-        for (int k = 0; k < 8; ++k) acc[4 * ti + ei][k] = fmaf(hf[k], wf[ei][k], acc[4 * ti + ei][k]);
+    for (int p = 0; p < P; ++p) {
+      fma_step(hs[p], ws[p]);
+      load_step(st + p + P, hs[p], ws[p]);
     }
   }
-  // residues l, l + 32 (lanes m, m ^ 4): keep outputs [8 b2, 8 b2 + 8)
-  float r1[8][8];
+  // steps % P last steps, their loads already in sets 0 .. steps % P - 1
+#pragma unroll
+  for (int p = 0; p < P - 1; ++p)
+    if (st + p < steps) fma_step(hs[p], ws[p]);
+  // residues l, l + 32 (lanes m, m ^ 4), then l + 16 (m ^ 2): each level a
+  // butterfly in which the two lanes keep opposite halves of the outputs
+  float r1[NO / 2][8];
   {
     const bool up = (m & 4) != 0;
 #pragma unroll
-    for (int j = 0; j < 8; ++j)
+    for (int j = 0; j < NO / 2; ++j)
 #pragma unroll
       for (int k = 0; k < 8; ++k) {
-        const float send = up ? acc[j][k] : acc[j + 8][k];
-        const float keep = up ? acc[j + 8][k] : acc[j][k];
+        const float send = up ? acc[j][k] : acc[j + NO / 2][k];
+        const float keep = up ? acc[j + NO / 2][k] : acc[j][k];
         r1[j][k] = keep + __shfl_xor(send, 4, 64);
       }
   }
-  float r2[4][8];
+  float r2[NO / 4][8];
   {
     const bool up = (m & 2) != 0;
 #pragma unroll
-    for (int j = 0; j < 4; ++j)
+    for (int j = 0; j < NO / 4; ++j)
 #pragma unroll
       for (int k = 0; k < 8; ++k) {
-        const float send = up ? r1[j][k] : r1[j + 4][k];
-        const float keep = up ? r1[j + 4][k] : r1[j][k];
+        const float send = up ? r1[j][k] : r1[j + NO / 4][k];
+        const float keep = up ? r1[j + NO / 4][k] : r1[j][k];
         r2[j][k] = keep + __shfl_xor(send, 2, 64);
       }
   }
-  float r3[2][8];
-  {
+  // l + 8 (m ^ 1): a butterfly again for 4 x 4 tiles (this lane then holds
+  // outputs q = 2 m + j), both lanes the same sum for 2 x 2 ones (output q =
+  // m / 2, written by the even lane)
+  constexpr int NJ = NO == 16 ? 2 : 1;
+  float r3[NJ][8];
+  if constexpr (NO == 16) {
     const bool up = (m & 1) != 0;
 #pragma unroll
     for (int j = 0; j < 2; ++j)
@@ -894,15 +905,17 @@ __global__ __launch_bounds__(256) void logits_many_kernel(LogitsArgs a) {
         const float keep = up ? r2[j + 2][k] : r2[j][k];
         r3[j][k] = keep + __shfl_xor(send, 1, 64);
       }
-  }
-  // this lane now holds outputs q = 2 m + j (token q / 4, expert q % 4)
+  } else {
 #pragma unroll
-  for (int j = 0; j < 2; ++j) {
+    for (int k = 0; k < 8; ++k) r3[0][k] = r2[0][k] + __shfl_xor(r2[0][k], 1, 64);
+  }
+#pragma unroll
+  for (int j = 0; j < NJ; ++j) {
     const float* r = r3[j];
     float v = ((r[0] + r[4]) + (r[2] + r[6])) + ((r[1] + r[5]) + (r[3] + r[7]));
-    const int q = 2 * m + j;
-    const int t = tq0 + (q >> 2), e = eq0 + (q & 3);
-    if (t < a.T && e < a.E) {
+    const int q = NO == 16 ? 2 * m + j : m >> 1;
+    const int t = tq0 + q / TE, e = eq0 + q % TE;
+    if ((NO == 16 || (m & 1) == 0) && t < a.T && e < a.E) {
       if (bias != nullptr) v = v + bias[e];
       out[static_cast<size_t>(t) * a.E + e] = v;
     }
@@ -933,12 +946,23 @@ hipError_t launch_logits_route(const LogitsArgs& a, const RouteArgs& ra, hipStre
   if (!many && ra.logits != nullptr && a.T * ra.K > kFewSlots)
     return hipErrorInvalidValue;  // the one-work-group route holds T * K slots
   if (many) {
-    const int nb = (a.E + kLmExperts - 1) / kLmExperts;
-    const dim3 grid((a.T + kLmTokens - 1) / kLmTokens, nb * mats);
-    if (a.dtype == kBF16)
-      hipLaunchKernelGGL(logits_many_kernel<uint16_t>, grid, dim3(256), kGuardLds, s, b);
-    else
-      hipLaunchKernelGGL(logits_many_kernel<float>, grid, dim3(256), kGuardLds, s, b);
+    using Big = LmTile<4, 4>;
+    using Small = LmTile<2, 2>;
+    const int nb = (a.E + Big::EXPERTS - 1) / Big::EXPERTS;
+    const dim3 grid((a.T + Big::TOKENS - 1) / Big::TOKENS, nb * mats);
+    if (static_cast<int64_t>(grid.x) * grid.y >= kLmBigBelowWgs) {
+      if (a.dtype == kBF16)
+        hipLaunchKernelGGL((logits_many_kernel<uint16_t, 4, 4>), grid, dim3(256), kGuardLds, s, b);
+      else
+        hipLaunchKernelGGL((logits_many_kernel<float, 4, 4>), grid, dim3(256), kGuardLds, s, b);
+    } else {
+      const int nbs = (a.E + Small::EXPERTS - 1) / Small::EXPERTS;
+      const dim3 gs((a.T + Small::TOKENS - 1) / Small::TOKENS, nbs * mats);
+      if (a.dtype == kBF16)
+        hipLaunchKernelGGL((logits_many_kernel<uint16_t, 2, 2>), gs, dim3(256), kGuardLds, s, b);
+      else
+        hipLaunchKernelGGL((logits_many_kernel<float, 2, 2>), gs, dim3(256), kGuardLds, s, b);
+    }
   } else {
     const int n_out = a.T * a.E * mats;
     const int elem = a.dtype == kBF16 ? 2 : 4;
@@ -977,6 +1001,7 @@ hipError_t launch_logits_route(const LogitsArgs& a, const RouteArgs& ra, hipStre
               : qn == 2 ? select_many_kernel<2>
               : qn == 4 ? select_many_kernel<4>
                         : select_many_kernel<8>;
+  if (TB > kSelWaves) return hipErrorInvalidValue;
   hipLaunchKernelGGL(sel, dim3(nblk), dim3(64 * kSelWaves), 0, s, ra, TB);
   if ((e = hipGetLastError()) != hipSuccess) return e;
   hipLaunchKernelGGL(scan_many_kernel, dim3(1), dim3(64 * kScanWaves), 0, s, ra, nblk);
