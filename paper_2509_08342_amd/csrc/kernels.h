@@ -86,6 +86,11 @@ struct RouteArgs {
   int32_t* order;           // [E]
   float* host_score;        // host-visible or NULL
   int32_t* host_order;      // host-visible or NULL
+  // host-visible completion word or NULL: set to seq once every host-visible
+  // output above is visible to the host (the host polls it instead of
+  // waiting for the launch to complete)
+  int32_t* host_seq;
+  int32_t seq;
   // many-token workspace (ignored below kManyTokens tokens)
   int32_t* lrank;           // [T*K] rank of a slot among its block's slots of the same expert
   int32_t* blk;             // [E][nblk_cap] per-block expert counts, then their prefix sums

@@ -329,6 +329,14 @@ __device__ __forceinline__ void store_offsets(const int* offs, const RouteArgs& 
 __device__ __forceinline__ void host_fence(const RouteArgs& a, int tid) {
   if ((a.host_offsets != nullptr || a.host_order != nullptr || a.host_score != nullptr) && tid <= a.E)
     __threadfence_system();
+  // then the completion word: after a barrier every writer has fenced
+  if (a.host_seq != nullptr) {
+    __syncthreads();
+    if (tid == 0) {
+      __threadfence_system();
+      *reinterpret_cast<volatile int32_t*>(a.host_seq) = a.seq;
+    }
+  }
 }
 
 // Few tokens (T * K <= kFewSlots): everything after the logits in one

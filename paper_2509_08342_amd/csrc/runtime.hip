@@ -405,6 +405,11 @@ struct LayerState {
   std::vector<hipEvent_t> pending_loads;
   hipEvent_t last_fwd = nullptr;
   bool has_last_fwd = false;
+  // the end of this layer's last forward is recorded into last_fwd only when
+  // something waits for it (a marker between two kernels costs the stream a
+  // few microseconds); until then it is the end of fwd_stream's work so far
+  bool fwd_unrecorded = false;
+  hipStream_t fwd_stream = nullptr;
   // prediction made for this layer (Eq. (3)), checked at its next routing
   std::vector<int> pred_order;
   bool has_pred = false;
@@ -464,6 +469,11 @@ struct ms_ctx {
   int32_t* d_offsets_map = nullptr;  // device views of the three buffers above
   int32_t* d_order_map = nullptr;
   float* d_score_map = nullptr;
+  // routing completion word (host-visible): the routing launch of a forward
+  // sets it to that forward's number once the offsets are visible
+  int32_t* h_seq = nullptr;
+  int32_t* d_seq_map = nullptr;
+  uint32_t route_seq = 0;
   std::vector<LayerState> layers;
   std::vector<BufSlot> buf;
   uint64_t tick = 0;
@@ -893,8 +903,31 @@ void set_route_workspace(ms_ctx* ctx, msk::RouteArgs* r) {
 
 // Order work on `stream` after the previous forward/prediction of this
 // context (they share the work buffers).
+ms_status flush_fwd(ms_ctx* ctx, LayerState& L);
+ms_status flush_all_fwd(ms_ctx* ctx);
 ms_status order_after_last(ms_ctx* ctx, hipStream_t stream) {
-  if (ctx->has_last && ctx->last_stream != stream) MS_HIP(hipStreamWaitEvent(stream, ctx->last_ev, 0));
+  if (ctx->has_last && ctx->last_stream != stream) {
+    const ms_status st = flush_all_fwd(ctx);
+    if (st != MS_OK) return st;
+    MS_HIP(hipStreamWaitEvent(stream, ctx->last_ev, 0));
+  }
+  return MS_OK;
+}
+
+// Record a layer's end-of-forward event left unrecorded (recorded now, it
+// marks at least the end of that forward), and every layer's.
+ms_status flush_fwd(ms_ctx* ctx, LayerState& L) {
+  if (L.fwd_unrecorded) {
+    MS_HIP(hipEventRecord(L.last_fwd, L.fwd_stream));
+    L.fwd_unrecorded = false;
+  }
+  return MS_OK;
+}
+ms_status flush_all_fwd(ms_ctx* ctx) {
+  for (LayerState& L : ctx->layers) {
+    const ms_status st = flush_fwd(ctx, L);
+    if (st != MS_OK) return st;
+  }
   return MS_OK;
 }
 
@@ -1305,6 +1338,11 @@ ms_status ms_create(const ms_model_desc* desc, void* dev_pool, uint64_t pool_byt
     return cleanup_fail(e, "hipHostGetDevicePointer(order)");
   if ((e = hipHostGetDevicePointer(reinterpret_cast<void**>(&ctx->d_score_map), ctx->h_score, 0)) != hipSuccess)
     return cleanup_fail(e, "hipHostGetDevicePointer(score)");
+  if ((e = hipHostMalloc(reinterpret_cast<void**>(&ctx->h_seq), sizeof(int32_t), mflags)) != hipSuccess)
+    return cleanup_fail(e, "hipHostMalloc(seq)");
+  *reinterpret_cast<volatile int32_t*>(ctx->h_seq) = 0;
+  if ((e = hipHostGetDevicePointer(reinterpret_cast<void**>(&ctx->d_seq_map), ctx->h_seq, 0)) != hipSuccess)
+    return cleanup_fail(e, "hipHostGetDevicePointer(seq)");
   ctx->layers.resize(s.L);
   for (LayerState& L : ctx->layers) {
     L.blob_of.assign(s.E, -1);
@@ -1345,6 +1383,7 @@ void ms_destroy(ms_ctx* ctx) {
   if (ctx->copy) (void)hipStreamSynchronize(ctx->copy);
   if (ctx->side) (void)hipStreamSynchronize(ctx->side);
   if (ctx->side2) (void)hipStreamSynchronize(ctx->side2);
+  (void)flush_all_fwd(ctx);
   if (ctx->has_last) (void)hipEventSynchronize(ctx->last_ev);
   for (LayerState& L : ctx->layers) {
     for (hipEvent_t ev : L.pending_loads) (void)hipEventDestroy(ev);
@@ -1367,6 +1406,7 @@ void ms_destroy(ms_ctx* ctx) {
   if (ctx->h_offsets) (void)hipHostFree(ctx->h_offsets);
   if (ctx->h_order) (void)hipHostFree(ctx->h_order);
   if (ctx->h_score) (void)hipHostFree(ctx->h_score);
+  if (ctx->h_seq) (void)hipHostFree(ctx->h_seq);
   if (ctx->copy) (void)hipStreamDestroy(ctx->copy);
   if (ctx->side) (void)hipStreamDestroy(ctx->side);
   if (ctx->side2) (void)hipStreamDestroy(ctx->side2);
@@ -1518,6 +1558,8 @@ ms_status ms_set_shared_expert(ms_ctx* ctx, int32_t layer, int32_t sidx, const v
   std::vector<unsigned char> tmp(s.shared_bytes);
   pack_expert(w_gate, w_up, w_down, s.d, s.F_sh, s.n_chunks_sh, s.elem, tmp.data());
   const uint64_t off = s.off_shared + align_up(s.shared_bytes, kAlign) * (static_cast<uint64_t>(layer) * s.n_sh + sidx);
+  st = flush_all_fwd(ctx);
+  if (st != MS_OK) return st;
   if (ctx->has_last) MS_HIP(hipEventSynchronize(ctx->last_ev));
   MS_HIP(hipMemcpy(ctx->dev(off), tmp.data(), s.shared_bytes, hipMemcpyHostToDevice));
   ctx->layers[layer].shared_set[sidx] = true;
@@ -1529,6 +1571,8 @@ ms_status ms_sync(ms_ctx* ctx) {
   MS_HIP(hipStreamSynchronize(ctx->copy));
   MS_HIP(hipStreamSynchronize(ctx->side));
   MS_HIP(hipStreamSynchronize(ctx->side2));
+  const ms_status st = flush_all_fwd(ctx);
+  if (st != MS_OK) return st;
   if (ctx->has_last) MS_HIP(hipEventSynchronize(ctx->last_ev));
   return MS_OK;
 }
@@ -1593,6 +1637,8 @@ ms_status ms_load_top(ms_ctx* ctx, int32_t layer, int32_t e) {
     }
   if (slot < 0) return fail(ctx, MS_E_BUDGET, "no free top-segment slot in this layer");
   if (L.has_last_fwd) {
+    st = flush_fwd(ctx, L);
+    if (st != MS_OK) return st;
     st = copy_after(ctx, L.last_fwd);
     if (st != MS_OK) return st;
   }
@@ -1777,6 +1823,8 @@ ms_status ms_forward(ms_ctx* ctx, int32_t layer, const void* h_dev, int32_t T, f
   ga.perm = d_perm;
   ga.pos = d_pos;
   ga.host_offsets = ctx->d_offsets_map;
+  ga.host_seq = ctx->d_seq_map;
+  ga.seq = static_cast<int32_t>(++ctx->route_seq);
   set_route_workspace(ctx, &ga);
   if (predict_next) {
     ga.logits_pred = la.logits2;
@@ -1788,7 +1836,12 @@ ms_status ms_forward(ms_ctx* ctx, int32_t layer, const void* h_dev, int32_t T, f
   int ti = tl_begin(ctx, sm, MS_IV_ROUTER, layer, router_bytes);
   MS_HIP(msk::launch_logits_route(la, ga, sm));
   tl_end(ctx, ti, sm);
-  MS_HIP(hipEventRecord(ctx->ev_route, sm));
+  // The host learns the routing from the completion word; side streams order
+  // after it through ev_route, needed only when an expert misses chunks (a
+  // marker between two kernels costs the stream a few microseconds).
+  bool all_res = true;
+  for (int e = 0; e < s.E && all_res; ++e) all_res = resident_chunks(L, e) >= s.n_chunks;
+  if (!all_res) MS_HIP(hipEventRecord(ctx->ev_route, sm));
 
   // decode path (chunk kernel, launched before the host sees the routing)
   // or prefill path (matrix cores, launched once the token counts are known)
@@ -1902,10 +1955,16 @@ ms_status ms_forward(ms_ctx* ctx, int32_t layer, const void* h_dev, int32_t T, f
   if (any_pre) MS_HIP(hipEventRecord(ctx->ev_res, sm));
 
   // 3. wait for the routing result on the host, keeping prefetch copies fed
-  for (;;) {
-    const hipError_t q = hipEventQuery(ctx->ev_route);
-    if (q == hipSuccess) break;
-    if (q != hipErrorNotReady) return poison(ctx, "hipEventQuery(route)", q);
+  // (a launch that failed never sets the completion word: the stream is
+  // checked now and then)
+  for (int spin = 0;; ++spin) {
+    if (*reinterpret_cast<volatile int32_t*>(ctx->h_seq) == ga.seq) break;
+    if ((spin & 255) == 255) {
+      const hipError_t q = hipStreamQuery(sm);
+      if (q != hipSuccess && q != hipErrorNotReady) return poison(ctx, "hipStreamQuery(route)", q);
+      if (q == hipSuccess && *reinterpret_cast<volatile int32_t*>(ctx->h_seq) != ga.seq)
+        return poison(ctx, "routing completion word", hipErrorLaunchFailure);
+    }
     st = pump_prefetch(ctx);
     if (st != MS_OK) return st;
   }
@@ -1961,7 +2020,7 @@ ms_status ms_forward(ms_ctx* ctx, int32_t layer, const void* h_dev, int32_t T, f
   //    groups that landed by now, then one launch per group still to land,
   //    each after its copy event.  Slots read by the resident launch are
   //    released only after it (the side stream waits for it).
-  MS_HIP(hipStreamWaitEvent(ctx->side, any_pre ? ctx->ev_res : ctx->ev_route, 0));
+  if (any_pre || !all_res) MS_HIP(hipStreamWaitEvent(ctx->side, any_pre ? ctx->ev_res : ctx->ev_route, 0));
   // slots already holding an active expert's missing part are reserved so
   // that no other miss of this forward evicts them first
   for (int e = 0; e < s.E; ++e) {
@@ -2163,7 +2222,9 @@ ms_status ms_forward(ms_ctx* ctx, int32_t layer, const void* h_dev, int32_t T, f
       L.st.cache_inserts += 1;
     }
   }
-  MS_HIP(hipEventRecord(L.last_fwd, sm));
+  // the end of this forward, recorded when something waits for it
+  L.fwd_unrecorded = true;
+  L.fwd_stream = sm;
   L.has_last_fwd = true;
   ctx->has_last = true;
   ctx->last_ev = L.last_fwd;
