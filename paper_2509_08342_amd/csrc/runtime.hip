@@ -11,6 +11,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <chrono>
 #include <functional>
 #include <mutex>
 #include <cmath>
@@ -58,6 +59,7 @@ constexpr uint64_t kMissGroupTargetBytes = 64ull << 20;
 constexpr int kPrefetchWindow = 2;                   // prefetch groups in flight
 constexpr int kMaxD = msk::kMaxModelDim;
 constexpr int kReserved = 1 << 30;                   // BufSlot::use_order of a reserved slot
+constexpr int kRouteCheckMs = 20;  // the host's wait for a routing checks the stream this often
 
 uint64_t align_up(uint64_t x, uint64_t a) { return (x + a - 1) / a * a; }
 
@@ -1955,18 +1957,22 @@ ms_status ms_forward(ms_ctx* ctx, int32_t layer, const void* h_dev, int32_t T, f
   if (any_pre) MS_HIP(hipEventRecord(ctx->ev_res, sm));
 
   // 3. wait for the routing result on the host, keeping prefetch copies fed
-  // (a launch that failed never sets the completion word: the stream is
-  // checked now and then)
-  for (int spin = 0;; ++spin) {
-    if (*reinterpret_cast<volatile int32_t*>(ctx->h_seq) == ga.seq) break;
-    if ((spin & 255) == 255) {
-      const hipError_t q = hipStreamQuery(sm);
-      if (q != hipSuccess && q != hipErrorNotReady) return poison(ctx, "hipStreamQuery(route)", q);
-      if (q == hipSuccess && *reinterpret_cast<volatile int32_t*>(ctx->h_seq) != ga.seq)
-        return poison(ctx, "routing completion word", hipErrorLaunchFailure);
+  // (a launch that failed never sets the completion word: after a wait far
+  // longer than a routing, the stream is checked every kRouteCheckMs; a
+  // query puts a marker into the stream, which costs it microseconds)
+  {
+    auto next_check = std::chrono::steady_clock::now() + std::chrono::milliseconds(kRouteCheckMs);
+    while (*reinterpret_cast<volatile int32_t*>(ctx->h_seq) != ga.seq) {
+      if (std::chrono::steady_clock::now() >= next_check) {
+        const hipError_t q = hipStreamQuery(sm);
+        if (q != hipSuccess && q != hipErrorNotReady) return poison(ctx, "hipStreamQuery(route)", q);
+        if (q == hipSuccess && *reinterpret_cast<volatile int32_t*>(ctx->h_seq) != ga.seq)
+          return poison(ctx, "routing completion word", hipErrorLaunchFailure);
+        next_check = std::chrono::steady_clock::now() + std::chrono::milliseconds(kRouteCheckMs);
+      }
+      st = pump_prefetch(ctx);
+      if (st != MS_OK) return st;
     }
-    st = pump_prefetch(ctx);
-    if (st != MS_OK) return st;
   }
   std::vector<int32_t> offs(s.E + 1);
   for (int e = 0; e <= s.E; ++e) offs[e] = reinterpret_cast<volatile int32_t*>(ctx->h_offsets)[e];
