@@ -188,6 +188,7 @@ static_assert(kMaxMmaTasks <= 256, "find_task_of reads at most 256 task starts")
 constexpr int kGuSplitBelow = 256;
 constexpr int kMmaRows = 64;     // rows (token slots) per work-group
 constexpr int kGdMaxRows = 192;  // rows per tile of the LDS-staged gate/up kernel (bf16, d % 128 == 0)
+constexpr int kGdChunks = 2;     // chunks per work-group of the LDS-staged gate/up kernel
 constexpr int kMmaCols = 256;    // output columns per down work-group
 
 struct MmaTask {

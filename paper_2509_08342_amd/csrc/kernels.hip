@@ -2156,8 +2156,9 @@ constexpr int kGuPitch = kGuSlab + 8;   // bf16 per staged row
 // gate/up with both operands staged by direct global -> LDS loads
 // (global_load_lds_dwordx4: a lane's 16 bytes land at the LDS address in M0
 // + 16 lane, with no register in between, so the registers hold only the
-// accumulators and the fragments of one k step).  A work-group takes one
-// chunk (64 units of G and of U) for a row tile of up to kGdMaxRows rows and
+// accumulators and the fragments of one k step).  A work-group takes a pair
+// of chunks (kGdChunks; 64 units of G and of U each, so that every staged
+// activation row feeds both) for a row tile of up to kGdMaxRows rows and
 // takes the height of its tile: 64, 128 or 192 rows, so that an expert's
 // rows usually fit one tile and its weights are read once.  The k loop runs
 // over stages of 64 k in a ring of as many LDS buffers as kGdLds holds for
@@ -2173,8 +2174,10 @@ constexpr int kGuPitch = kGuSlab + 8;   // bf16 per staged row
 // of row r sits in slot p ^ (r % 8), so the 8 lanes an LDS read serves
 // together (8 rows at one piece) hit distinct banks.  The waves split the
 // tile kGdWaves / 2 x 2: wave (wr, wc) takes the row blocks wr, wr +
-// kGdWaves / 2, ... and units 32 wc .. 32 wc + 31 of G and of U.  The k
-// order of every sum is that of the other gate/up kernels.
+// kGdWaves / 2, ... and all 64 units of G and of U of chunk wc of the pair
+// (a task's odd last chunk: the pair's second half loads the first again and
+// stores nothing).  The k order of every sum is that of the other gate/up
+// kernels.
 constexpr int kGdWaves = 8;                                  // waves per work-group
 constexpr int kGdLds = 160 * 1024;                           // LDS of a work-group (one per CU)
 constexpr int kGdSlab = 64;                                  // k per stage
@@ -2221,25 +2224,23 @@ __device__ __forceinline__ bf16x8_t lds_frag(const unsigned char* p) {
 }
 
 template <int RB>
-__device__ __forceinline__ void gd_tile(const MmaArgs& a, const MmaTask& tk, int c, const TileRows& tr,
+__device__ __forceinline__ void gd_tile(const MmaArgs& a, const MmaTask& tk, int c, bool has2, const TileRows& tr,
                                         unsigned char* lds) {
   constexpr int WR = kGdWaves / 2;            // row groups of waves
   constexpr int NA = 2 * RB / kGdWaves;       // activation loads per wave and stage
-  constexpr int NB = 8 / kGdWaves;            // G (and U) loads per wave and stage
-  constexpr int NL = NA + 2 * NB;             // loads per wave and stage
+  constexpr int NL = NA + 4;                  // loads per wave and stage (one of each of G, U of both chunks)
   constexpr int HB = RB / WR;                 // row blocks per wave
   constexpr int ABYTES = RB * kGdBlockBytes;  // activation rows of a stage
-  constexpr int SBYTES = ABYTES + 2 * kGdBBytes;
+  constexpr int SBYTES = ABYTES + 4 * kGdBBytes;
   constexpr int NST = kGdLds / SBYTES;        // stages in the ring
+  static_assert(kGdWaves == 8, "one G and one U load of each chunk per wave and stage");
   static_assert(RB % WR == 0 && (2 * RB) % kGdWaves == 0 && RB <= kGdMaxRB, "row blocks");
   static_assert(NST >= 2 && (NST - 2) * NL < 64, "ring depth");
   const int lane = threadIdx.x & 63;
   const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const int wr = w >> 1, wc = w & 1;
+  const int wr = w >> 1, wc = w & 1;  // wc: the chunk of the pair
   const int d = a.d, nsl = d / kGdSlab;
   const bool routed = tk.expert >= 0;
-  // loads: lane -> row (unit) lane / 8 of the 8 a load covers; its slot
-  // lane % 8 holds piece (lane % 8) ^ (lane / 8)
   const int lrow = lane >> 3;
   const int lpiece = (lane & 7) ^ lrow;
   const uint16_t* hsrc[NA];
@@ -2249,9 +2250,13 @@ __device__ __forceinline__ void gd_tile(const MmaArgs& a, const MmaTask& tk, int
     const int tok = routed ? a.perm[tr.p0 + r] / a.K : tr.p0 + r;
     hsrc[j] = static_cast<const uint16_t*>(a.h) + static_cast<size_t>(tok) * d + 8 * lpiece;
   }
-  const uint16_t* G = reinterpret_cast<const uint16_t*>(tk.base + static_cast<size_t>(c) * a.chunk_bytes) +
-                      (8 * w + lrow) * kKTile + 8 * lpiece;
-  const uint16_t* U = G + static_cast<size_t>(kChunkUnits) * d;
+  // a pair's second chunk is the first again when the task has no second
+  // (loaded, never stored)
+  const uint16_t* G0 = reinterpret_cast<const uint16_t*>(tk.base + static_cast<size_t>(c) * a.chunk_bytes) +
+                       (8 * w + lrow) * kKTile + 8 * lpiece;
+  const uint16_t* G1 = reinterpret_cast<const uint16_t*>(tk.base + static_cast<size_t>(has2 ? c + 1 : c) * a.chunk_bytes) +
+                       (8 * w + lrow) * kKTile + 8 * lpiece;
+  const size_t uo = static_cast<size_t>(kChunkUnits) * d;  // U after G
   const uint32_t lbase = lds_address(lds) + w * kGdLoadBytes;
   auto issue = [&](int sl, int buf) {  // stages past the last reload it (in bounds, never read)
     const int k0 = min(sl, nsl - 1) * kGdSlab;
@@ -2259,49 +2264,45 @@ __device__ __forceinline__ void gd_tile(const MmaArgs& a, const MmaTask& tk, int
 #pragma unroll
     for (int j = 0; j < NA; ++j) lds_load16(hsrc[j] + k0, st + kGdWaves * j * kGdLoadBytes);
     const size_t bo = static_cast<size_t>(k0) * kChunkUnits;
-#pragma unroll
-    for (int j = 0; j < NB; ++j) {
-      const int go = 8 * kGdWaves * j * kKTile;  // units 8 (w + kGdWaves j) ..
-      lds_load16(G + bo + go, st + ABYTES + kGdWaves * j * kGdLoadBytes);
-      lds_load16(U + bo + go, st + ABYTES + kGdBBytes + kGdWaves * j * kGdLoadBytes);
-    }
+    lds_load16(G0 + bo, st + ABYTES);
+    lds_load16(G0 + uo + bo, st + ABYTES + kGdBBytes);
+    lds_load16(G1 + bo, st + ABYTES + 2 * kGdBBytes);
+    lds_load16(G1 + uo + bo, st + ABYTES + 3 * kGdBBytes);
   };
-  // fragment reads: lane -> row (unit) lane % 16 of a block, piece 4 s +
-  // lane / 16 of k step s
   int fo[2];
 #pragma unroll
   for (int s = 0; s < 2; ++s) fo[s] = (lane & 15) * kGdRowBytes + 16 * ((4 * s + (lane >> 4)) ^ (lane & 7));
-  f32x4_t ag[HB][2], au[HB][2];
+  f32x4_t ag[HB][4], au[HB][4];
 #pragma unroll
   for (int i = 0; i < HB; ++i)
 #pragma unroll
-    for (int n = 0; n < 2; ++n) ag[i][n] = au[i][n] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    for (int n = 0; n < 4; ++n) ag[i][n] = au[i][n] = f32x4_t{0.f, 0.f, 0.f, 0.f};
   auto compute = [&](int buf) {
     const unsigned char* st = lds + buf * SBYTES;
 #pragma unroll
     for (int s = 0; s < 2; ++s) {
-      const unsigned char* sg = st + ABYTES + 2 * wc * kGdBlockBytes + fo[s];
+      const unsigned char* sg = st + ABYTES + 2 * wc * kGdBBytes + fo[s];
       const unsigned char* su = sg + kGdBBytes;
       const unsigned char* sa = st + wr * kGdBlockBytes + fo[s];
-      const bf16x8_t g0 = lds_frag(sg), g1 = lds_frag(sg + kGdBlockBytes);
-      const bf16x8_t u0 = lds_frag(su), u1 = lds_frag(su + kGdBlockBytes);
-      bf16x8_t A[HB];
+      bf16x8_t g[4], u[4];
 #pragma unroll
-      for (int i = 0; i < HB; ++i) A[i] = lds_frag(sa + WR * i * kGdBlockBytes);
+      for (int n = 0; n < 4; ++n) {
+        g[n] = lds_frag(sg + n * kGdBlockBytes);
+        u[n] = lds_frag(su + n * kGdBlockBytes);
+      }
 #pragma unroll
       for (int i = 0; i < HB; ++i) {
-        ag[i][0] = mfma16(A[i], g0, ag[i][0]);
-        ag[i][1] = mfma16(A[i], g1, ag[i][1]);
-        au[i][0] = mfma16(A[i], u0, au[i][0]);
-        au[i][1] = mfma16(A[i], u1, au[i][1]);
+        const bf16x8_t A = lds_frag(sa + WR * i * kGdBlockBytes);
+#pragma unroll
+        for (int n = 0; n < 4; ++n) {
+          ag[i][n] = mfma16(A, g[n], ag[i][n]);
+          au[i][n] = mfma16(A, u[n], au[i][n]);
+        }
       }
     }
   };
 #pragma unroll
   for (int p = 0; p < NST - 1; ++p) issue(p, p);
-  // stage sl sits in buffer sl % NST; at sl this wave's loads of it are in
-  // (those of the NST - 2 later stages may not be), every wave's after the
-  // barrier, which also frees the buffer read at sl - 1 for stage sl + NST - 1
   int cur = 0, nxt = NST - 1;
   for (int sl = 0; sl < nsl; ++sl) {
     wait_vm<(NST - 2) * NL>();
@@ -2312,14 +2313,15 @@ __device__ __forceinline__ void gd_tile(const MmaArgs& a, const MmaTask& tk, int
     nxt = nxt + 1 == NST ? 0 : nxt + 1;
   }
   wait_vm<0>();  // the reloads past the last stage land before the work-group ends
+  if (wc == 1 && !has2) return;
   uint16_t* act = routed ? a.act : a.act_sh + static_cast<size_t>(-1 - tk.expert) * a.rows_shared * a.f_pad_sh;
   const int f_pad = routed ? a.f_pad : a.f_pad_sh;
 #pragma unroll
   for (int i = 0; i < HB; ++i) {
     const int rb = WR * i + wr;
 #pragma unroll
-    for (int n = 0; n < 2; ++n) {
-      const int f = c * kChunkUnits + 32 * wc + 16 * n + (lane & 15);
+    for (int n = 0; n < 4; ++n) {
+      const int f = (c + wc) * kChunkUnits + 16 * n + (lane & 15);
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         const int row = 16 * rb + 4 * (lane >> 4) + r;
@@ -2352,15 +2354,16 @@ __global__ __launch_bounds__(64 * kGdWaves) void mma_gateup_dma_kernel(MmaArgs a
   int local;
   if (!staged_task(a, tk, local)) return;
   const int mt = local % tk.m_tiles;
-  const int c = tk.chunk_lo + local / tk.m_tiles;
+  const int c = tk.chunk_lo + kGdChunks * (local / tk.m_tiles);  // the first chunk of the pair
+  const bool has2 = c + 1 < tk.chunk_lo + tk.n_chunks;
   const TileRows tr = tile_rows(a, tk, mt);
   if (tr.n <= 0) return;  // uniform over the work-group
   if (tr.n <= 64)
-    gd_tile<4>(a, tk, c, tr, lds);
+    gd_tile<4>(a, tk, c, has2, tr, lds);
   else if (tr.n <= 128)
-    gd_tile<8>(a, tk, c, tr, lds);
+    gd_tile<8>(a, tk, c, has2, tr, lds);
   else
-    gd_tile<12>(a, tk, c, tr, lds);
+    gd_tile<12>(a, tk, c, has2, tr, lds);
 }
 
 // Work-group barrier that orders LDS only: a __syncthreads() also orders
@@ -2914,7 +2917,7 @@ __global__ __launch_bounds__(kMaxPlanTasks) void prefill_plan_kernel(PlanArgs p)
       t.expert = i;
       t.m_tiles = (n + p.tile_rows - 1) / p.tile_rows;
       gu_c = res;
-      gu_w = t.m_tiles * res;
+      gu_w = t.m_tiles * ((res + kGdChunks - 1) / kGdChunks);
       if (res >= p.n_chunks) {
         dn_c = p.n_chunks;
         dn_w = t.m_tiles * p.ncb;
@@ -2926,7 +2929,7 @@ __global__ __launch_bounds__(kMaxPlanTasks) void prefill_plan_kernel(PlanArgs p)
     t.expert = -1 - sh;
     t.m_tiles = (p.T + p.tile_rows - 1) / p.tile_rows;
     gu_c = dn_c = p.n_chunks_sh;
-    gu_w = t.m_tiles * p.n_chunks_sh;
+    gu_w = t.m_tiles * ((p.n_chunks_sh + kGdChunks - 1) / kGdChunks);
     dn_w = t.m_tiles * p.ncb;
   }
   // inclusive scan of (gate/up task, gate/up work-groups, down task, down work-groups)

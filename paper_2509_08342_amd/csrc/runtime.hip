@@ -1075,7 +1075,11 @@ ms_status prefill_experts(ms_ctx* ctx, int layer, const void* h_dev, int T, cons
       for (size_t i = i0; i < i1; ++i) {
         ma.tasks[i - i0] = tasks[i];
         ma.tasks[i - i0].wg_begin = wg;
-        wg += tasks[i].m_tiles * (down ? ma.ncb * ma.ksplit : tasks[i].n_chunks * ma.gu_split);
+        // (the LDS-staged gate/up kernel takes kGdChunks chunks per work-group)
+        const bool staged = !down && s.bits == 0 && ma.gu_split == 1 && s.d % 128 == 0;
+        const int per = staged ? (tasks[i].n_chunks + msk::kGdChunks - 1) / msk::kGdChunks
+                               : tasks[i].n_chunks * ma.gu_split;
+        wg += tasks[i].m_tiles * (down ? ma.ncb * ma.ksplit : per);
         bytes += (down ? dn_bytes : gu_bytes) * tasks[i].n_chunks;
       }
       ma.n_wg = wg;
