@@ -94,7 +94,8 @@ struct RouteArgs {
   // many-token workspace (ignored below kManyTokens tokens)
   int32_t* lrank;           // [T*K] rank of a slot among its block's slots of the same expert
   int32_t* blk;             // [E][nblk_cap] per-block expert counts, then their prefix sums
-  float* psc;               // [nblk_cap][E] per-block prediction score sums
+  float* psc;               // [E][nblk_cap] per-block prediction score sums (a block's expert-major, so
+                            // that the sums over blocks read contiguous memory)
   int32_t nblk_cap;
 };
 // Logits launch, then the route launch on them.

@@ -469,7 +469,7 @@ __global__ __launch_bounds__(64 * kRouteWaves) void route_kernel(RouteArgs a) { 
 // Many tokens, step 1 (work-group b: tokens [b TB, (b+1) TB), one wave per
 // token): selection, then each slot's rank among the block's earlier slots
 // of the same expert and the block's expert counts blk[e][b]; the block's
-// prediction score sums (waves in order) into psc[b][e].
+// prediction score sums (waves in order) into psc[e][b].
 constexpr int kSelWaves = 16;  // one wave per token of a block of at most 16
 
 template <int QN>
@@ -523,7 +523,7 @@ __global__ __launch_bounds__(64 * kSelWaves) void select_many_kernel(RouteArgs a
       float sc = wsc[0][e];
 #pragma unroll
       for (int w2 = 1; w2 < kSelWaves; ++w2) sc += wsc[w2][e];
-      a.psc[static_cast<size_t>(b) * E + e] = sc;
+      a.psc[static_cast<size_t>(e) * a.nblk_cap + b] = sc;
     }
   }
 }
@@ -594,7 +594,7 @@ __global__ __launch_bounds__(64 * kScanWaves) void scan_many_kernel(RouteArgs a,
         float pv[EG];
 #pragma unroll
         for (int j = 0; j < EG; ++j)  // clamped: every load in bounds, used only in range
-          pv[j] = a.psc[static_cast<size_t>(min(b, nblk - 1)) * E + min(e0 + kScanWaves * j, E - 1)];
+          pv[j] = a.psc[static_cast<size_t>(min(e0 + kScanWaves * j, E - 1)) * a.nblk_cap + min(b, nblk - 1)];
 #pragma unroll
         for (int j = 0; j < EG; ++j)
           if (b < nblk) sc[j] += pv[j];
