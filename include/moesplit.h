@@ -286,7 +286,10 @@ ms_status ms_prefetch(ms_ctx* ctx, int32_t layer, const int32_t* experts, int32_
  * Enqueued on `stream`; returns after the missing segments have been
  * issued (the host waits for the routing result).  Outputs are valid once
  * `stream` has completed.  h_dev, y_dev, idx_dev, w_dev must not be reused
- * by the caller before that. */
+ * by the caller before that.  The library marks the end of the forward on
+ * `stream` only when something waits for it (ms_sync, ms_load_top, a
+ * forward on another stream, ms_destroy), so `stream` must stay valid until
+ * then. */
 ms_status ms_forward(ms_ctx* ctx, int32_t layer, const void* h_dev, int32_t T,
                      float* y_dev, int32_t* idx_dev, float* w_dev, int32_t flags,
                      void* stream);
