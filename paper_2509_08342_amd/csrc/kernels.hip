@@ -3375,19 +3375,32 @@ __global__ __launch_bounds__(64) void combine_direct_kernel(CombineArgs a) {
   const int col = blockIdx.y * 256 + threadIdx.x * 4;
   if (col >= a.d) return;
   float4 y = make_float4(0.f, 0.f, 0.f, 0.f);
-  for (int term = 0; term < a.K + a.n_shared; ++term) {
-    float4 v;
-    if (term < a.K) {
-      const int row = a.pos[t * a.K + term];
-      v = *reinterpret_cast<const float4*>(a.part + static_cast<size_t>(row) * a.d + col);
-      const float wk = a.w[t * a.K + term];
-      y = make_float4(fmaf(wk, v.x, y.x), fmaf(wk, v.y, y.y), fmaf(wk, v.z, y.z), fmaf(wk, v.w, y.w));
-    } else {
-      v = *reinterpret_cast<const float4*>(a.part_sh + static_cast<size_t>(term - a.K) * a.sh_plane +
-                                           static_cast<size_t>(t) * a.d + col);
-      y = f4add(y, v);
+  // routed terms in batches of kDirectBatch: their rows, then their partial
+  // loads, all in flight before the first is added (the order of the sum is
+  // the terms' order)
+  constexpr int kDirectBatch = 8;
+  for (int k0 = 0; k0 < a.K; k0 += kDirectBatch) {
+    int row[kDirectBatch];
+    float wk[kDirectBatch];
+#pragma unroll
+    for (int j = 0; j < kDirectBatch; ++j) {
+      const int k = min(k0 + j, a.K - 1);  // clamped: in bounds, used only below K
+      row[j] = a.pos[t * a.K + k];
+      wk[j] = a.w[t * a.K + k];
     }
+    float4 v[kDirectBatch];
+#pragma unroll
+    for (int j = 0; j < kDirectBatch; ++j)
+      v[j] = *reinterpret_cast<const float4*>(a.part + static_cast<size_t>(row[j]) * a.d + col);
+#pragma unroll
+    for (int j = 0; j < kDirectBatch; ++j)
+      if (k0 + j < a.K)
+        y = make_float4(fmaf(wk[j], v[j].x, y.x), fmaf(wk[j], v[j].y, y.y), fmaf(wk[j], v[j].z, y.z),
+                        fmaf(wk[j], v[j].w, y.w));
   }
+  for (int sh = 0; sh < a.n_shared; ++sh)
+    y = f4add(y, *reinterpret_cast<const float4*>(a.part_sh + static_cast<size_t>(sh) * a.sh_plane +
+                                                  static_cast<size_t>(t) * a.d + col));
   *reinterpret_cast<float4*>(a.y + static_cast<size_t>(t) * a.d + col) = y;
 }
 
