@@ -2162,9 +2162,8 @@ constexpr int kGuPitch = kGuSlab + 8;   // bf16 per staged row
 // takes the height of its tile: 64, 128 or 192 rows, so that an expert's
 // rows usually fit one tile and its weights are read once.  The k loop runs
 // over stages of 64 k in a ring of as many LDS buffers as kGdLds holds for
-// that height (6, 5 or 4): the loads of all but one are in flight while a
-// stage is computed, which is what keeps HBM busy (with one stage ahead, the
-// loads in flight per CU cover too little of the memory latency).  A wave
+// that height (4, 3 or 2): the loads of all but one are in flight while a
+// stage is computed.  A wave
 // waits for its own loads of a stage, then a barrier makes every wave's
 // loads visible and frees the buffer read before for the next loads.  The
 // loads are issued from inline assembly, so the compiler, which would
