@@ -189,7 +189,14 @@ static_assert(kMaxMmaTasks <= 256, "find_task_of reads at most 256 task starts")
 constexpr int kGuSplitBelow = 256;
 constexpr int kMmaRows = 64;     // rows (token slots) per work-group
 constexpr int kGdMaxRows = 192;  // rows per tile of the LDS-staged gate/up kernel (bf16, d % 128 == 0)
-constexpr int kGdChunks = 2;     // chunks per work-group of the LDS-staged gate/up kernel
+// chunks per work-group of the LDS-staged gate/up kernel: four for a task of
+// at most 64 rows and at least 16 chunks (its activation rows then feed four
+// chunks' weights, and it still spreads over enough work-groups), else two
+// (measured: DeepSeek-V2-Lite prefill 512, 22 chunks per expert, gate/up 184
+// -> 175 us; Qwen3 prefill 2048, 12 chunks, 215 -> 223 us with four)
+__host__ __device__ inline int gd_group_chunks(int task_rows, int task_chunks) {
+  return task_rows <= 64 && task_chunks >= 16 ? 4 : 2;
+}
 constexpr int kMmaCols = 256;    // output columns per down work-group
 
 struct MmaTask {

@@ -2157,8 +2157,8 @@ constexpr int kGuPitch = kGuSlab + 8;   // bf16 per staged row
 // (global_load_lds_dwordx4: a lane's 16 bytes land at the LDS address in M0
 // + 16 lane, with no register in between, so the registers hold only the
 // accumulators and the fragments of one k step).  A work-group takes a pair
-// of chunks (kGdChunks; 64 units of G and of U each, so that every staged
-// activation row feeds both) for a row tile of up to kGdMaxRows rows and
+// or four chunks (gd_group_chunks; 64 units of G and of U each, so that every
+// staged activation row feeds all of them) for a row tile of up to kGdMaxRows rows and
 // takes the height of its tile: 64, 128 or 192 rows, so that an expert's
 // rows usually fit one tile and its weights are read once.  The k loop runs
 // over stages of 64 k in a ring of as many LDS buffers as kGdLds holds for
@@ -2173,10 +2173,10 @@ constexpr int kGuPitch = kGuSlab + 8;   // bf16 per staged row
 // of row r sits in slot p ^ (r % 8), so the 8 lanes an LDS read serves
 // together (8 rows at one piece) hit distinct banks.  The waves split the
 // tile kGdWaves / 2 x 2: wave (wr, wc) takes the row blocks wr, wr +
-// kGdWaves / 2, ... and all 64 units of G and of U of chunk wc of the pair
-// (a task's odd last chunk: the pair's second half loads the first again and
-// stores nothing).  The k order of every sum is that of the other gate/up
-// kernels.
+// kGdWaves / 2, ... and all 64 units of G and of U of the chunks of half wc
+// of the group (a group that runs past the task's last chunk loads that one
+// again and stores nothing for it).  The k order of every sum is that of the
+// other gate/up kernels.
 constexpr int kGdWaves = 8;                                  // waves per work-group
 constexpr int kGdLds = 160 * 1024;                           // LDS of a work-group (one per CU)
 constexpr int kGdSlab = 64;                                  // k per stage
@@ -2222,22 +2222,23 @@ __device__ __forceinline__ bf16x8_t lds_frag(const unsigned char* p) {
   return as_bf16x8(*reinterpret_cast<const uint4*>(p));
 }
 
-template <int RB>
-__device__ __forceinline__ void gd_tile(const MmaArgs& a, const MmaTask& tk, int c, bool has2, const TileRows& tr,
+template <int RB, int NC>
+__device__ __forceinline__ void gd_tile(const MmaArgs& a, const MmaTask& tk, int c, int nv, const TileRows& tr,
                                         unsigned char* lds) {
   constexpr int WR = kGdWaves / 2;            // row groups of waves
+  constexpr int CPW = NC / 2;                 // chunks per wave (its column group's)
   constexpr int NA = 2 * RB / kGdWaves;       // activation loads per wave and stage
-  constexpr int NL = NA + 4;                  // loads per wave and stage (one of each of G, U of both chunks)
+  constexpr int NL = NA + 2 * NC;             // loads per wave and stage (one of each of G, U of every chunk)
   constexpr int HB = RB / WR;                 // row blocks per wave
   constexpr int ABYTES = RB * kGdBlockBytes;  // activation rows of a stage
-  constexpr int SBYTES = ABYTES + 4 * kGdBBytes;
+  constexpr int SBYTES = ABYTES + 2 * NC * kGdBBytes;
   constexpr int NST = kGdLds / SBYTES;        // stages in the ring
-  static_assert(kGdWaves == 8, "one G and one U load of each chunk per wave and stage");
+  static_assert(kGdWaves == 8 && (NC == 2 || NC == 4), "one G and one U load of each chunk per wave and stage");
   static_assert(RB % WR == 0 && (2 * RB) % kGdWaves == 0 && RB <= kGdMaxRB, "row blocks");
   static_assert(NST >= 2 && (NST - 2) * NL < 64, "ring depth");
   const int lane = threadIdx.x & 63;
   const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const int wr = w >> 1, wc = w & 1;  // wc: the chunk of the pair
+  const int wr = w >> 1, wc = w & 1;  // wc: the column group (chunks wc CPW ..)
   const int d = a.d, nsl = d / kGdSlab;
   const bool routed = tk.expert >= 0;
   const int lrow = lane >> 3;
@@ -2249,12 +2250,12 @@ __device__ __forceinline__ void gd_tile(const MmaArgs& a, const MmaTask& tk, int
     const int tok = routed ? a.perm[tr.p0 + r] / a.K : tr.p0 + r;
     hsrc[j] = static_cast<const uint16_t*>(a.h) + static_cast<size_t>(tok) * d + 8 * lpiece;
   }
-  // a pair's second chunk is the first again when the task has no second
-  // (loaded, never stored)
-  const uint16_t* G0 = reinterpret_cast<const uint16_t*>(tk.base + static_cast<size_t>(c) * a.chunk_bytes) +
-                       (8 * w + lrow) * kKTile + 8 * lpiece;
-  const uint16_t* G1 = reinterpret_cast<const uint16_t*>(tk.base + static_cast<size_t>(has2 ? c + 1 : c) * a.chunk_bytes) +
-                       (8 * w + lrow) * kKTile + 8 * lpiece;
+  // chunks of the group past the task's last load that one again (never stored)
+  const uint16_t* Gc[NC];
+#pragma unroll
+  for (int j = 0; j < NC; ++j)
+    Gc[j] = reinterpret_cast<const uint16_t*>(tk.base + static_cast<size_t>(c + min(j, nv - 1)) * a.chunk_bytes) +
+            (8 * w + lrow) * kKTile + 8 * lpiece;
   const size_t uo = static_cast<size_t>(kChunkUnits) * d;  // U after G
   const uint32_t lbase = lds_address(lds) + w * kGdLoadBytes;
   auto issue = [&](int sl, int buf) {  // stages past the last reload it (in bounds, never read)
@@ -2263,40 +2264,48 @@ __device__ __forceinline__ void gd_tile(const MmaArgs& a, const MmaTask& tk, int
 #pragma unroll
     for (int j = 0; j < NA; ++j) lds_load16(hsrc[j] + k0, st + kGdWaves * j * kGdLoadBytes);
     const size_t bo = static_cast<size_t>(k0) * kChunkUnits;
-    lds_load16(G0 + bo, st + ABYTES);
-    lds_load16(G0 + uo + bo, st + ABYTES + kGdBBytes);
-    lds_load16(G1 + bo, st + ABYTES + 2 * kGdBBytes);
-    lds_load16(G1 + uo + bo, st + ABYTES + 3 * kGdBBytes);
+#pragma unroll
+    for (int j = 0; j < NC; ++j) {
+      lds_load16(Gc[j] + bo, st + ABYTES + 2 * j * kGdBBytes);
+      lds_load16(Gc[j] + uo + bo, st + ABYTES + (2 * j + 1) * kGdBBytes);
+    }
   };
   int fo[2];
 #pragma unroll
   for (int s = 0; s < 2; ++s) fo[s] = (lane & 15) * kGdRowBytes + 16 * ((4 * s + (lane >> 4)) ^ (lane & 7));
-  f32x4_t ag[HB][4], au[HB][4];
+  f32x4_t ag[HB][CPW][4], au[HB][CPW][4];
 #pragma unroll
   for (int i = 0; i < HB; ++i)
 #pragma unroll
-    for (int n = 0; n < 4; ++n) ag[i][n] = au[i][n] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    for (int q = 0; q < CPW; ++q)
+#pragma unroll
+      for (int n = 0; n < 4; ++n) ag[i][q][n] = au[i][q][n] = f32x4_t{0.f, 0.f, 0.f, 0.f};
   auto compute = [&](int buf) {
     const unsigned char* st = lds + buf * SBYTES;
 #pragma unroll
     for (int s = 0; s < 2; ++s) {
-      const unsigned char* sg = st + ABYTES + 2 * wc * kGdBBytes + fo[s];
-      const unsigned char* su = sg + kGdBBytes;
       const unsigned char* sa = st + wr * kGdBlockBytes + fo[s];
-      bf16x8_t g[4], u[4];
+      bf16x8_t g[CPW][4], u[CPW][4];
 #pragma unroll
-      for (int n = 0; n < 4; ++n) {
-        g[n] = lds_frag(sg + n * kGdBlockBytes);
-        u[n] = lds_frag(su + n * kGdBlockBytes);
+      for (int q = 0; q < CPW; ++q) {
+        const unsigned char* sg = st + ABYTES + 2 * (wc * CPW + q) * kGdBBytes + fo[s];
+        const unsigned char* su = sg + kGdBBytes;
+#pragma unroll
+        for (int n = 0; n < 4; ++n) {
+          g[q][n] = lds_frag(sg + n * kGdBlockBytes);
+          u[q][n] = lds_frag(su + n * kGdBlockBytes);
+        }
       }
 #pragma unroll
       for (int i = 0; i < HB; ++i) {
         const bf16x8_t A = lds_frag(sa + WR * i * kGdBlockBytes);
 #pragma unroll
-        for (int n = 0; n < 4; ++n) {
-          ag[i][n] = mfma16(A, g[n], ag[i][n]);
-          au[i][n] = mfma16(A, u[n], au[i][n]);
-        }
+        for (int q = 0; q < CPW; ++q)
+#pragma unroll
+          for (int n = 0; n < 4; ++n) {
+            ag[i][q][n] = mfma16(A, g[q][n], ag[i][q][n]);
+            au[i][q][n] = mfma16(A, u[q][n], au[i][q][n]);
+          }
       }
     }
   };
@@ -2312,19 +2321,23 @@ __device__ __forceinline__ void gd_tile(const MmaArgs& a, const MmaTask& tk, int
     nxt = nxt + 1 == NST ? 0 : nxt + 1;
   }
   wait_vm<0>();  // the reloads past the last stage land before the work-group ends
-  if (wc == 1 && !has2) return;
   uint16_t* act = routed ? a.act : a.act_sh + static_cast<size_t>(-1 - tk.expert) * a.rows_shared * a.f_pad_sh;
   const int f_pad = routed ? a.f_pad : a.f_pad_sh;
 #pragma unroll
-  for (int i = 0; i < HB; ++i) {
-    const int rb = WR * i + wr;
+  for (int q = 0; q < CPW; ++q) {
+    const int j = wc * CPW + q;
+    if (j >= nv) continue;
 #pragma unroll
-    for (int n = 0; n < 4; ++n) {
-      const int f = (c + wc) * kChunkUnits + 16 * n + (lane & 15);
+    for (int i = 0; i < HB; ++i) {
+      const int rb = WR * i + wr;
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int row = 16 * rb + 4 * (lane >> 4) + r;
-        if (row < tr.n) act[static_cast<size_t>(tr.p0 + row) * f_pad + f] = f2bf(silu(ag[i][n][r]) * au[i][n][r]);
+      for (int n = 0; n < 4; ++n) {
+        const int f = (c + j) * kChunkUnits + 16 * n + (lane & 15);
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int row = 16 * rb + 4 * (lane >> 4) + r;
+          if (row < tr.n) act[static_cast<size_t>(tr.p0 + row) * f_pad + f] = f2bf(silu(ag[i][q][n][r]) * au[i][q][n][r]);
+        }
       }
     }
   }
@@ -2353,16 +2366,20 @@ __global__ __launch_bounds__(64 * kGdWaves) void mma_gateup_dma_kernel(MmaArgs a
   int local;
   if (!staged_task(a, tk, local)) return;
   const int mt = local % tk.m_tiles;
-  const int c = tk.chunk_lo + kGdChunks * (local / tk.m_tiles);  // the first chunk of the pair
-  const bool has2 = c + 1 < tk.chunk_lo + tk.n_chunks;
+  const int per =
+      gd_group_chunks(tk.expert >= 0 ? a.offsets[tk.expert + 1] - a.offsets[tk.expert] : a.T, tk.n_chunks);
+  const int c = tk.chunk_lo + per * (local / tk.m_tiles);  // the group's first chunk
+  const int nv = min(per, tk.chunk_lo + tk.n_chunks - c);   // its chunks in the task
   const TileRows tr = tile_rows(a, tk, mt);
   if (tr.n <= 0) return;  // uniform over the work-group
-  if (tr.n <= 64)
-    gd_tile<4>(a, tk, c, has2, tr, lds);
+  if (per == 4)
+    gd_tile<4, 4>(a, tk, c, nv, tr, lds);  // (a task of at most 64 rows: one tile of at most 64)
+  else if (tr.n <= 64)
+    gd_tile<4, 2>(a, tk, c, nv, tr, lds);
   else if (tr.n <= 128)
-    gd_tile<8>(a, tk, c, has2, tr, lds);
+    gd_tile<8, 2>(a, tk, c, nv, tr, lds);
   else
-    gd_tile<12>(a, tk, c, has2, tr, lds);
+    gd_tile<12, 2>(a, tk, c, nv, tr, lds);
 }
 
 // Work-group barrier that orders LDS only: a __syncthreads() also orders
@@ -2916,7 +2933,7 @@ __global__ __launch_bounds__(kMaxPlanTasks) void prefill_plan_kernel(PlanArgs p)
       t.expert = i;
       t.m_tiles = (n + p.tile_rows - 1) / p.tile_rows;
       gu_c = res;
-      gu_w = t.m_tiles * ((res + kGdChunks - 1) / kGdChunks);
+      gu_w = t.m_tiles * ((res + gd_group_chunks(n, res) - 1) / gd_group_chunks(n, res));
       if (res >= p.n_chunks) {
         dn_c = p.n_chunks;
         dn_w = t.m_tiles * p.ncb;
@@ -2928,7 +2945,7 @@ __global__ __launch_bounds__(kMaxPlanTasks) void prefill_plan_kernel(PlanArgs p)
     t.expert = -1 - sh;
     t.m_tiles = (p.T + p.tile_rows - 1) / p.tile_rows;
     gu_c = dn_c = p.n_chunks_sh;
-    gu_w = t.m_tiles * ((p.n_chunks_sh + kGdChunks - 1) / kGdChunks);
+    gu_w = t.m_tiles * ((p.n_chunks_sh + gd_group_chunks(p.T, p.n_chunks_sh) - 1) / gd_group_chunks(p.T, p.n_chunks_sh));
     dn_w = t.m_tiles * p.ncb;
   }
   // inclusive scan of (gate/up task, gate/up work-groups, down task, down work-groups)

@@ -1075,10 +1075,10 @@ ms_status prefill_experts(ms_ctx* ctx, int layer, const void* h_dev, int T, cons
       for (size_t i = i0; i < i1; ++i) {
         ma.tasks[i - i0] = tasks[i];
         ma.tasks[i - i0].wg_begin = wg;
-        // (the LDS-staged gate/up kernel takes kGdChunks chunks per work-group)
+        // (the LDS-staged gate/up kernel takes gd_group_chunks chunks per work-group)
         const bool staged = !down && s.bits == 0 && ma.gu_split == 1 && s.d % 128 == 0;
-        const int per = staged ? (tasks[i].n_chunks + msk::kGdChunks - 1) / msk::kGdChunks
-                               : tasks[i].n_chunks * ma.gu_split;
+        const int gc = msk::gd_group_chunks(rows_of(tasks[i].expert), tasks[i].n_chunks);
+        const int per = staged ? (tasks[i].n_chunks + gc - 1) / gc : tasks[i].n_chunks * ma.gu_split;
         wg += tasks[i].m_tiles * (down ? ma.ncb * ma.ksplit : per);
         bytes += (down ? dn_bytes : gu_bytes) * tasks[i].n_chunks;
       }
