@@ -137,7 +137,9 @@ __device__ __forceinline__ float lane_read(float x, int l) {
 
 // (v, i) takes (ov, oi) if that is larger, or equal with a lower index.
 __device__ __forceinline__ void argmax_take(float& v, int& i, float ov, int oi) {
-  const bool take = ov > v || (ov == v && oi < i);
+  // bitwise, not short-circuit, so that it compiles to compares and selects
+  // rather than branches (a branch per comparison costs the wave far more)
+  const bool take = (ov > v) | ((ov == v) & (oi < i));
   v = take ? ov : v;
   i = take ? oi : i;
 }
@@ -185,7 +187,11 @@ __device__ __forceinline__ void load_lanes(const float* lg, int E, int lane, flo
 }
 
 // Selection of one token by one wave from its logits (load_lanes); lanes
-// k < K return the k-th pick and its weight.
+// k < K return the k-th pick and its weight.  A round takes the wave's
+// largest untaken logit (a float max over the lanes) and then the lowest
+// expert index holding it (ballots), which is the argmax with the lower
+// index first on equal logits; the exponentials of the picks and their sum
+// (in pick order) follow the rounds.
 template <int QN>
 __device__ __forceinline__ void select_token(const float (&lg)[QN], int E, int K, int renormalize, int lane,
                                              int& my_idx, float& my_w) {
@@ -196,30 +202,36 @@ __device__ __forceinline__ void select_token(const float (&lg)[QN], int E, int K
     if (v != v) v = -INFINITY;  // NaN reads as -inf, so an index is always found
     lv[q] = v;
   }
-  uint32_t taken = 0;
-  float m = 0.0f, zsel = 0.0f, my_ex = 0.0f;
+  uint32_t open = 0;  // bit q: expert lane + 64 q exists and is not taken
+#pragma unroll
+  for (int q = 0; q < QN; ++q) open |= (lane + 64 * q < E ? 1u : 0u) << q;
+  float m = 0.0f, my_v = -INFINITY;
   my_idx = 0;
   for (int k = 0; k < K; ++k) {
-    float bv = -INFINITY;
-    int bi = 0x7fffffff;
+    float c = -INFINITY;
+#pragma unroll
+    for (int q = 0; q < QN; ++q) c = fmaxf(c, ((open >> q) & 1u) ? lv[q] : -INFINITY);
+    const float bv = wave_max(c);
+    int bi = 0;
+    bool found = false;
 #pragma unroll
     for (int q = 0; q < QN; ++q) {
-      const int e = lane + 64 * q;
-      if (e < E && !((taken >> q) & 1u) && (lv[q] > bv || (lv[q] == bv && e < bi))) {
-        bv = lv[q];
-        bi = e;
+      const uint64_t hit = __ballot(((open >> q) & 1u) && lv[q] == bv);
+      if (!found && hit != 0) {
+        bi = 64 * q + __ffsll(static_cast<unsigned long long>(hit)) - 1;
+        found = true;
       }
     }
-    wave_argmax(bv, bi);
-    if ((bi & 63) == lane) taken |= 1u << (bi >> 6);
+    if ((bi & 63) == lane) open &= ~(1u << (bi >> 6));
     if (k == 0) m = bv;  // the first pick is the largest logit
-    const float ex = expf(bv - m);
-    zsel += ex;
     if (lane == k) {
-      my_ex = ex;
+      my_v = bv;
       my_idx = bi;
     }
   }
+  const float my_ex = lane < K ? expf(my_v - m) : 0.0f;
+  float zsel = 0.0f;
+  for (int k = 0; k < K; ++k) zsel += lane_read(my_ex, k);
   float z = zsel;
   if (!renormalize) {
     float part = 0.0f;
@@ -260,37 +272,29 @@ __device__ __forceinline__ void pred_add(const float (&lg)[QN], int E, int lane,
   for (int q = 0; q < QN; ++q) acc[q] += lv[q] / z;
 }
 
-// Ranks score_s (LDS, E values) and stores order / score (and their host-
-// visible copies), by a work-group of NT threads (whole waves): one wave per
-// expert, its lanes comparing against experts lane, lane + 64, ..., the
-// counts summed over the wave.  rank(e) = #{o : s_o > s_e or (s_o == s_e
-// and o < e)}, so equal scores keep the lower index first.  The order is
-// collected in LDS (order_s) and stored by consecutive threads, so that the
-// host-visible copies cross the bus as whole rows rather than one 4-byte
-// write per expert.
-__device__ __forceinline__ void rank_scores(const float* score_s, int* order_s, const RouteArgs& a, int tid,
-                                            int NT) {
-  const int E = a.E;
-  const int lane = tid & 63, wave = tid >> 6, nw = NT >> 6;
-  for (int e = wave; e < E; e += nw) {
-    const float v = score_s[e];
-    int r = 0;
-    for (int o = lane; o < E; o += 64) {
-      const float u = score_s[o];
-      r += (u > v) || (u == v && o < e);
-    }
-    r = wave_sum(r);
-    if (lane == 0) order_s[r] = e;
-  }
-  __syncthreads();
-  for (int i = tid; i < E; i += NT) {
-    const int e = order_s[i];
-    const float v = score_s[i];
-    a.order[i] = e;
-    a.score[i] = v;
-    if (a.host_order) a.host_order[i] = e;
-    if (a.host_score) a.host_score[i] = v;
-  }
+// Ranks of E scores: rank(e) = #{o : s_o > s_e, or s_o == s_e and o < e},
+// so equal scores keep the lower index first.  rank_key(s_e, e) packs the
+// order-preserving integer image of the float (the float order for every
+// non-NaN score, and a strict total order whatever the values, so the ranks
+// always form a permutation) above ~e, and rank(e) = #{o : key_o > key_e}.
+// The E x E comparisons are shared by the NT threads of the work-group:
+// thread (e, part) counts one part of the o range and adds its count to
+// rank_s[e] (LDS, zero before the call).
+__device__ __forceinline__ uint64_t rank_key(float v, int e) {
+  const uint32_t b = __float_as_uint(v);
+  const uint32_t k = (b & 0x80000000u) ? ~b : (b | 0x80000000u);
+  return (static_cast<uint64_t>(k) << 32) | static_cast<uint32_t>(~e);
+}
+__device__ __forceinline__ void rank_count(const uint64_t* key_s, int* rank_s, int E, int tid, int NT) {
+  const int parts = max(1, NT / E);
+  const int per = (E + parts - 1) / parts;
+  if (tid >= E * parts) return;
+  const int e = tid % E, part = tid / E;
+  const uint64_t v = key_s[e];
+  const int o0 = part * per, o1 = min(E, o0 + per);
+  int r = 0;
+  for (int o = o0; o < o1; ++o) r += key_s[o] > v;
+  if (r != 0) atomicAdd(&rank_s[e], r);
 }
 
 // Exclusive scan of cnt[0..E) by wave 0 into offs[0..E] (LDS); base (LDS,
@@ -315,150 +319,165 @@ __device__ __forceinline__ void scan_offsets(const int* cnt, int* base, int* off
   if (lane == 0) offs[E] = run;
 }
 
-// The offsets from LDS to memory and to their host-visible copy.
-__device__ __forceinline__ void store_offsets(const int* offs, const RouteArgs& a, int tid, int NT) {
-  for (int e = tid; e <= a.E; e += NT) {
-    a.offsets[e] = offs[e];
-    if (a.host_offsets) a.host_offsets[e] = offs[e];
-  }
-}
-
-// The host reads the host-visible outputs once the launch completes: the
-// threads that may have written them (tid <= E) fence once, after their
-// last write.
-__device__ __forceinline__ void host_fence(const RouteArgs& a, int tid) {
-  if ((a.host_offsets != nullptr || a.host_order != nullptr || a.host_score != nullptr) && tid <= a.E)
-    __threadfence_system();
-  // then the completion word: after a barrier every writer has fenced
-  if (a.host_seq != nullptr) {
-    __syncthreads();
-    if (tid == 0) {
-      __threadfence_system();
-      *reinterpret_cast<volatile int32_t*>(a.host_seq) = a.seq;
+// The host-visible copies of the routing (offsets, prediction order and
+// scores, from LDS), then the completion word: all written by wave 0 alone,
+// so that one system-scope fence of that wave orders every copy before the
+// word.  Whole rows of consecutive values, so they cross the bus as few
+// large writes.
+__device__ __forceinline__ void host_publish(const RouteArgs& a, const int* offs_s, const int* order_s,
+                                             const float* score_s, int wave, int lane) {
+  if (wave != 0) return;
+  const bool any = a.host_offsets != nullptr || a.host_order != nullptr || a.host_score != nullptr;
+  if (!any && a.host_seq == nullptr) return;
+  if (a.host_offsets != nullptr && offs_s != nullptr)
+    for (int e = lane; e <= a.E; e += 64) a.host_offsets[e] = offs_s[e];
+  if (order_s != nullptr) {
+    for (int i = lane; i < a.E; i += 64) {
+      if (a.host_order != nullptr) a.host_order[i] = order_s[i];
+      if (a.host_score != nullptr) a.host_score[i] = score_s[i];
     }
   }
+  __threadfence_system();
+  if (a.host_seq != nullptr && lane == 0) *reinterpret_cast<volatile int32_t*>(a.host_seq) = a.seq;
 }
 
-// Few tokens (T * K <= kFewSlots): everything after the logits in one
-// work-group of NW waves -- selection one wave per token; grouping as
-// histogram, exclusive scan, then blocks of 64*NW slots placed in slot order
-// (within a wave by ballot rank, across waves by per-wave counts); prediction
-// sums per wave, then over waves in order.  Every result stays in LDS until
-// the last barrier and is then stored once (a barrier after a store to
-// memory would wait for it).
+// Few tokens (T * K <= kFewSlots <= 64 NW, so one slot per thread):
+// everything after the logits in one work-group of NW waves, in four
+// barrier-separated steps --
+//   1. per token, one wave: its selection, and its softmax of the second
+//      logits added to the wave's running expert sums (prediction);
+//   2. per wave: each of its 64 slots' rank among the wave's earlier slots of
+//      the same expert, and the wave's count of each expert (ballots); the
+//      prediction scores, summed over the waves in order;
+//   3. wave 0: expert totals and their exclusive scan (offsets); all threads:
+//      the ranks of the prediction scores;
+//   4. slot s goes to offsets[e] + (earlier waves' slots of e) + (its rank
+//      in its wave), a stable counting sort; expert e goes to position
+//      rank(e) of the prediction order.
+// Every result stays in LDS until the last barrier and is then stored once
+// (a barrier after a store to memory would wait for it).
 constexpr int kFewSlots = 1024;
 
 template <int NW, int QN>
 __device__ void route_body(const RouteArgs& a) {
+  static_assert(kFewSlots <= 64 * NW, "one slot per thread");
   __shared__ int idx_s[kFewSlots];
   __shared__ float w_s[kFewSlots];
   __shared__ int perm_s[kFewSlots];
   __shared__ int pos_s[kFewSlots];
   __shared__ int offs_s[kMaxExperts + 1];
-  __shared__ int base[kMaxExperts];
+  __shared__ int cnt_s[kMaxExperts];
   __shared__ float score_s[kMaxExperts];
-  __shared__ int wbuf[NW][kMaxExperts];  // per-wave counts / scores
+  __shared__ uint64_t key_s[kMaxExperts];
+  __shared__ int rank_s[kMaxExperts];
+  __shared__ int order_s[kMaxExperts];
+  __shared__ int wcnt[NW][kMaxExperts];    // per-wave slot counts
+  __shared__ float wsum[NW][kMaxExperts];  // per-wave prediction sums
   constexpr int NT = 64 * NW;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int E = a.E, K = a.K;
   const int TK = a.T * K;
+  const bool sel = a.logits != nullptr, pred = a.logits_pred != nullptr;
 
-  // the prediction logits of this wave's first token are requested with its
-  // selection logits (one memory round trip for both)
-  float lp[QN];
-  if (a.logits_pred != nullptr && wave < a.T) load_lanes(a.logits_pred + static_cast<size_t>(wave) * E, E, lane, lp);
+  // counts and ranks start at zero (each wave clears its own row of counts;
+  // all are first read after the next barrier)
+  for (int e = lane; e < E; e += 64) wcnt[wave][e] = 0;
+  for (int e = tid; e < E; e += NT) rank_s[e] = 0;
 
-  if (a.logits != nullptr) {
-    // 1. selection
-    for (int t = wave; t < a.T; t += NW) {
+  // 1. selection and prediction sums, one wave per token; both rows of a
+  //    token are requested together (one memory round trip)
+  float acc[QN];
+#pragma unroll
+  for (int q = 0; q < QN; ++q) acc[q] = 0.0f;
+  for (int t = wave; t < a.T; t += NW) {
+    float lg[QN], lp[QN];
+    if (sel) load_lanes(a.logits + static_cast<size_t>(t) * E, E, lane, lg);
+    if (pred) load_lanes(a.logits_pred + static_cast<size_t>(t) * E, E, lane, lp);
+    if (sel) {
       int my_idx;
       float my_w;
-      float lg[QN];
-      load_lanes(a.logits + static_cast<size_t>(t) * E, E, lane, lg);
       select_token(lg, E, K, a.renormalize, lane, my_idx, my_w);
       if (lane < K) {
         idx_s[t * K + lane] = my_idx;
         w_s[t * K + lane] = my_w;
       }
     }
-    // 2. grouping
-    int* cnt = &wbuf[0][0];
-    for (int e = tid; e < E; e += NT) cnt[e] = 0;
-    __syncthreads();
-    // indices lie in [0, E) (selection above); the clamp only keeps LDS
-    // accesses in bounds whatever the input
-    for (int s = tid; s < TK; s += NT) atomicAdd(&cnt[min(max(idx_s[s], 0), E - 1)], 1);
-    __syncthreads();
-    if (wave == 0) scan_offsets(cnt, base, offs_s, E, lane);
-    __syncthreads();
-    const uint64_t lt = (lane == 0) ? 0ull : ((~0ull) >> (64 - lane));
-    for (int b0 = 0; b0 < TK; b0 += NT) {
-      for (int i = tid; i < NW * E; i += NT) wbuf[i / E][i % E] = 0;
-      __syncthreads();
-      const int s = b0 + tid;
-      const int e = (s < TK) ? min(max(idx_s[s], 0), E - 1) : -1;
-      int rank = 0;
-      uint64_t pending = __ballot(e >= 0);
-      while (pending) {
-        const int leader = __ffsll(static_cast<unsigned long long>(pending)) - 1;
-        const int le = lane_read(e, leader);
-        const uint64_t same = __ballot(e == le);
-        if (e == le) rank = __popcll(same & lt);
-        if (lane == leader) wbuf[wave][le] = __popcll(same);
-        pending &= ~same;
-      }
-      __syncthreads();
-      if (e >= 0) {
-        int p = base[e] + rank;
-        for (int w2 = 0; w2 < wave; ++w2) p += wbuf[w2][e];
-        perm_s[p] = s;
-        pos_s[s] = p;
-      }
-      __syncthreads();
-      for (int e2 = tid; e2 < E; e2 += NT) {
-        int add = 0;
-        for (int w2 = 0; w2 < NW; ++w2) add += wbuf[w2][e2];
-        base[e2] += add;
-      }
-      __syncthreads();
-    }
+    if (pred) pred_add(lp, E, lane, acc);
   }
-
-  if (a.logits_pred != nullptr) {
-    // 3. prediction ranking
-    float acc[QN];
-#pragma unroll
-    for (int q = 0; q < QN; ++q) acc[q] = 0.0f;
-    for (int t = wave; t < a.T; t += NW) {
-      if (t != wave) load_lanes(a.logits_pred + static_cast<size_t>(t) * E, E, lane, lp);
-      pred_add(lp, E, lane, acc);
-    }
-    float* ws = reinterpret_cast<float*>(&wbuf[0][0]);
-    __syncthreads();
+  if (pred) {
 #pragma unroll
     for (int q = 0; q < QN; ++q)
-      if (lane + 64 * q < E) ws[wave * kMaxExperts + lane + 64 * q] = acc[q];
-    __syncthreads();
+      if (lane + 64 * q < E) wsum[wave][lane + 64 * q] = acc[q];
+  }
+  __syncthreads();
+
+  // 2. per-wave slot ranks and counts; prediction scores
+  int ge = -1, grank = 0;
+  if (sel) {
+    // indices lie in [0, E) (selection above); the clamp only keeps LDS
+    // accesses in bounds whatever the input
+    ge = tid < TK ? min(max(idx_s[tid], 0), E - 1) : -1;
+    const uint64_t lt = (lane == 0) ? 0ull : ((~0ull) >> (64 - lane));
+    uint64_t pending = __ballot(ge >= 0);
+    while (pending) {
+      const int leader = __ffsll(static_cast<unsigned long long>(pending)) - 1;
+      const int le = lane_read(ge, leader);
+      const uint64_t same = __ballot(ge == le);
+      if (ge == le) grank = __popcll(same & lt);
+      if (lane == leader) wcnt[wave][le] = __popcll(same);
+      pending &= ~same;
+    }
+  }
+  if (pred) {
     for (int e = tid; e < E; e += NT) {
       float sc = 0.0f;
-      for (int w2 = 0; w2 < NW; ++w2) sc += ws[w2 * kMaxExperts + e];
+      for (int w2 = 0; w2 < NW; ++w2) sc += wsum[w2][e];
       score_s[e] = sc;
+      key_s[e] = rank_key(sc, e);
     }
-    __syncthreads();
-    rank_scores(score_s, &wbuf[1][0], a, tid, NT);
   }
+  __syncthreads();
 
-  // 4. the selection and grouping to memory (and the offsets to the host)
-  if (a.logits != nullptr) {
+  // 3. offsets (wave 0); prediction ranks (all threads)
+  if (sel && wave == 0) {
+    for (int e = lane; e < E; e += 64) {
+      int c = 0;
+      for (int w2 = 0; w2 < NW; ++w2) c += wcnt[w2][e];
+      cnt_s[e] = c;
+    }
+    scan_offsets(cnt_s, nullptr, offs_s, E, lane);
+  }
+  if (pred) rank_count(key_s, rank_s, E, tid, NT);
+  __syncthreads();
+
+  // 4. grouped positions; prediction order
+  if (ge >= 0) {
+    int p = offs_s[ge] + grank;
+    for (int w2 = 0; w2 < wave; ++w2) p += wcnt[w2][ge];
+    perm_s[p] = tid;
+    pos_s[tid] = p;
+  }
+  if (pred)
+    for (int e = tid; e < E; e += NT) order_s[rank_s[e]] = e;
+  __syncthreads();
+
+  // the results to memory, then their host-visible copies
+  if (sel) {
     for (int i = tid; i < TK; i += NT) {
       a.idx[i] = idx_s[i];
       a.w[i] = w_s[i];
       a.perm[i] = perm_s[i];
       a.pos[i] = pos_s[i];
     }
-    store_offsets(offs_s, a, tid, NT);
+    for (int e = tid; e <= E; e += NT) a.offsets[e] = offs_s[e];
   }
-  host_fence(a, tid);
+  if (pred) {
+    for (int i = tid; i < E; i += NT) {
+      a.order[i] = order_s[i];
+      a.score[i] = score_s[i];
+    }
+  }
+  host_publish(a, sel ? offs_s : nullptr, pred ? order_s : nullptr, score_s, wave, lane);
 }
 
 constexpr int kRouteWaves = 16;
@@ -539,13 +558,17 @@ __global__ __launch_bounds__(64 * kScanWaves) void scan_many_kernel(RouteArgs a,
   __shared__ int tot[kMaxExperts];
   __shared__ int offs_s[kMaxExperts + 1];
   __shared__ float score_s[kMaxExperts];
+  __shared__ uint64_t key_s[kMaxExperts];
+  __shared__ int rank_s[kMaxExperts];
   __shared__ int order_s[kMaxExperts];
   // a wave takes kScanGroup experts at a time (e0, e0 + kScanWaves, ...) and
   // requests their values of 64 blocks together, so that the experts of a
   // wave cost one memory round trip per 64 blocks, not one each
   constexpr int EG = kScanGroup;
+  constexpr int NT = 64 * kScanWaves;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int E = a.E;
+  for (int e = tid; e < E; e += NT) rank_s[e] = 0;  // first read after the next barrier
   if (a.logits != nullptr) {
     // per expert: exclusive scan of its block counts, 64 blocks at a time
     for (int e0 = wave; e0 < E; e0 += EG * kScanWaves) {
@@ -576,11 +599,6 @@ __global__ __launch_bounds__(64 * kScanWaves) void scan_many_kernel(RouteArgs a,
       for (int j = 0; j < EG; ++j)
         if (lane == 0 && e0 + kScanWaves * j < E) tot[e0 + kScanWaves * j] = run[j];
     }
-    __syncthreads();
-    if (wave == 0) {
-      scan_offsets(tot, nullptr, offs_s, E, lane);
-      store_offsets(offs_s, a, lane, 64);
-    }
   }
   if (a.logits_pred != nullptr) {
     // per expert: lanes sum blocks lane, lane + 64, ... in order, then a
@@ -604,13 +622,31 @@ __global__ __launch_bounds__(64 * kScanWaves) void scan_many_kernel(RouteArgs a,
         float v = sc[j];
 #pragma unroll
         for (int s = 32; s >= 1; s >>= 1) v = v + __shfl_down(v, s, 64);
-        if (lane == 0 && e0 + kScanWaves * j < E) score_s[e0 + kScanWaves * j] = v;
+        if (lane == 0 && e0 + kScanWaves * j < E) {
+          score_s[e0 + kScanWaves * j] = v;
+          key_s[e0 + kScanWaves * j] = rank_key(v, e0 + kScanWaves * j);
+        }
       }
     }
-    __syncthreads();
-    rank_scores(score_s, order_s, a, tid, 64 * kScanWaves);
   }
-  host_fence(a, tid);
+  __syncthreads();
+  // offsets (wave 0); prediction ranks (all threads)
+  if (a.logits != nullptr && wave == 0) scan_offsets(tot, nullptr, offs_s, E, lane);
+  if (a.logits_pred != nullptr) rank_count(key_s, rank_s, E, tid, NT);
+  __syncthreads();
+  if (a.logits_pred != nullptr)
+    for (int e = tid; e < E; e += NT) order_s[rank_s[e]] = e;
+  __syncthreads();
+  if (a.logits != nullptr)
+    for (int e = tid; e <= E; e += NT) a.offsets[e] = offs_s[e];
+  if (a.logits_pred != nullptr) {
+    for (int i = tid; i < E; i += NT) {
+      a.order[i] = order_s[i];
+      a.score[i] = score_s[i];
+    }
+  }
+  host_publish(a, a.logits != nullptr ? offs_s : nullptr, a.logits_pred != nullptr ? order_s : nullptr, score_s,
+               wave, lane);
 }
 
 // Many tokens, step 3: slot s of token t (block t / TB) goes to grouped
