@@ -175,6 +175,27 @@ __device__ __forceinline__ int wave_sum(int v) {
   v += dpp_move<kDppMirror>(v);
   return (lane_read(v, 0) + lane_read(v, 16)) + (lane_read(v, 32) + lane_read(v, 48));
 }
+__device__ __forceinline__ uint32_t wave_umax(uint32_t v) {
+  v = max(v, static_cast<uint32_t>(dpp_move<kDppXor1>(static_cast<int>(v))));
+  v = max(v, static_cast<uint32_t>(dpp_move<kDppXor2>(static_cast<int>(v))));
+  v = max(v, static_cast<uint32_t>(dpp_move<kDppHalfMirror>(static_cast<int>(v))));
+  v = max(v, static_cast<uint32_t>(dpp_move<kDppMirror>(static_cast<int>(v))));
+  const uint32_t a = static_cast<uint32_t>(lane_read(static_cast<int>(v), 0));
+  const uint32_t b = static_cast<uint32_t>(lane_read(static_cast<int>(v), 16));
+  const uint32_t c = static_cast<uint32_t>(lane_read(static_cast<int>(v), 32));
+  const uint32_t d = static_cast<uint32_t>(lane_read(static_cast<int>(v), 48));
+  return max(max(a, b), max(c, d));
+}
+
+// Order-preserving integer image of a non-NaN float (-0 reads as +0, so
+// equal floats have equal keys), and back.
+__device__ __forceinline__ uint32_t float_key(float v) {
+  const uint32_t b = __float_as_uint(v == 0.0f ? 0.0f : v);
+  return (b & 0x80000000u) ? ~b : (b | 0x80000000u);
+}
+__device__ __forceinline__ float key_float(uint32_t k) {
+  return __uint_as_float((k & 0x80000000u) ? (k & 0x7fffffffu) : ~k);
+}
 
 // The logits of one token: lane l holds experts l + 64 q (-inf past E).
 template <int QN>
@@ -188,48 +209,53 @@ __device__ __forceinline__ void load_lanes(const float* lg, int E, int lane, flo
 
 // Selection of one token by one wave from its logits (load_lanes); lanes
 // k < K return the k-th pick and its weight.  A round takes the wave's
-// largest untaken logit (a float max over the lanes) and then the lowest
-// expert index holding it (ballots), which is the argmax with the lower
-// index first on equal logits; the exponentials of the picks and their sum
-// (in pick order) follow the rounds.
+// largest untaken logit (an unsigned max over the lanes of the logits'
+// order-preserving keys; untaken experts only, the others read as key 0,
+// below every logit's) and then the lowest expert index holding it
+// (ballots), which is the argmax with the lower index first on equal
+// logits; the exponentials of the picks and their sum (in pick order)
+// follow the rounds.
 template <int QN>
 __device__ __forceinline__ void select_token(const float (&lg)[QN], int E, int K, int renormalize, int lane,
                                              int& my_idx, float& my_w) {
   float lv[QN];
+  uint32_t kv[QN];
 #pragma unroll
   for (int q = 0; q < QN; ++q) {
     float v = lg[q];
     if (v != v) v = -INFINITY;  // NaN reads as -inf, so an index is always found
     lv[q] = v;
+    kv[q] = float_key(v);  // >= key(-inf) > 0
   }
   uint32_t open = 0;  // bit q: expert lane + 64 q exists and is not taken
 #pragma unroll
   for (int q = 0; q < QN; ++q) open |= (lane + 64 * q < E ? 1u : 0u) << q;
-  float m = 0.0f, my_v = -INFINITY;
+  uint32_t mk = 0, my_k = 0;
   my_idx = 0;
   for (int k = 0; k < K; ++k) {
-    float c = -INFINITY;
+    uint32_t c = 0;
 #pragma unroll
-    for (int q = 0; q < QN; ++q) c = fmaxf(c, ((open >> q) & 1u) ? lv[q] : -INFINITY);
-    const float bv = wave_max(c);
+    for (int q = 0; q < QN; ++q) c = max(c, ((open >> q) & 1u) ? kv[q] : 0u);
+    const uint32_t bk = wave_umax(c);
     int bi = 0;
     bool found = false;
 #pragma unroll
     for (int q = 0; q < QN; ++q) {
-      const uint64_t hit = __ballot(((open >> q) & 1u) && lv[q] == bv);
+      const uint64_t hit = __ballot(((open >> q) & 1u) && kv[q] == bk);
       if (!found && hit != 0) {
         bi = 64 * q + __ffsll(static_cast<unsigned long long>(hit)) - 1;
         found = true;
       }
     }
     if ((bi & 63) == lane) open &= ~(1u << (bi >> 6));
-    if (k == 0) m = bv;  // the first pick is the largest logit
+    if (k == 0) mk = bk;  // the first pick is the largest logit
     if (lane == k) {
-      my_v = bv;
+      my_k = bk;
       my_idx = bi;
     }
   }
-  const float my_ex = lane < K ? expf(my_v - m) : 0.0f;
+  const float m = key_float(mk);
+  const float my_ex = lane < K ? expf(key_float(my_k) - m) : 0.0f;
   float zsel = 0.0f;
   for (int k = 0; k < K; ++k) zsel += lane_read(my_ex, k);
   float z = zsel;
@@ -288,11 +314,12 @@ __device__ __forceinline__ uint64_t rank_key(float v, int e) {
 __device__ __forceinline__ void rank_count(const uint64_t* key_s, int* rank_s, int E, int tid, int NT) {
   const int parts = max(1, NT / E);
   const int per = (E + parts - 1) / parts;
-  if (tid >= E * parts) return;
+  if (tid < 0 || tid >= E * parts) return;
   const int e = tid % E, part = tid / E;
   const uint64_t v = key_s[e];
   const int o0 = part * per, o1 = min(E, o0 + per);
   int r = 0;
+#pragma unroll 4
   for (int o = o0; o < o1; ++o) r += key_s[o] > v;
   if (r != 0) atomicAdd(&rank_s[e], r);
 }
@@ -319,25 +346,24 @@ __device__ __forceinline__ void scan_offsets(const int* cnt, int* base, int* off
   if (lane == 0) offs[E] = run;
 }
 
-// The host-visible copies of the routing (offsets, prediction order and
-// scores, from LDS), then the completion word: all written by wave 0 alone,
+// The host-visible copies of the routing, all written by one wave (wave 0)
 // so that one system-scope fence of that wave orders every copy before the
-// word.  Whole rows of consecutive values, so they cross the bus as few
+// completion word: host_rows as soon as the offsets and the prediction
+// scores are known (their writes cross the bus while the work-group goes
+// on), host_publish with the prediction order at the end, then the fence and
+// the word.  Whole rows of consecutive values, so they cross the bus as few
 // large writes.
-__device__ __forceinline__ void host_publish(const RouteArgs& a, const int* offs_s, const int* order_s,
-                                             const float* score_s, int wave, int lane) {
-  if (wave != 0) return;
-  const bool any = a.host_offsets != nullptr || a.host_order != nullptr || a.host_score != nullptr;
-  if (!any && a.host_seq == nullptr) return;
+__device__ __forceinline__ void host_rows(const RouteArgs& a, const int* offs_s, const float* score_s, int lane) {
   if (a.host_offsets != nullptr && offs_s != nullptr)
     for (int e = lane; e <= a.E; e += 64) a.host_offsets[e] = offs_s[e];
-  if (order_s != nullptr) {
-    for (int i = lane; i < a.E; i += 64) {
-      if (a.host_order != nullptr) a.host_order[i] = order_s[i];
-      if (a.host_score != nullptr) a.host_score[i] = score_s[i];
-    }
-  }
-  __threadfence_system();
+  if (a.host_score != nullptr && score_s != nullptr)
+    for (int i = lane; i < a.E; i += 64) a.host_score[i] = score_s[i];
+}
+__device__ __forceinline__ void host_publish(const RouteArgs& a, const int* order_s, int lane) {
+  if (a.host_order != nullptr && order_s != nullptr)
+    for (int i = lane; i < a.E; i += 64) a.host_order[i] = order_s[i];
+  if (a.host_offsets != nullptr || a.host_order != nullptr || a.host_score != nullptr || a.host_seq != nullptr)
+    __threadfence_system();
   if (a.host_seq != nullptr && lane == 0) *reinterpret_cast<volatile int32_t*>(a.host_seq) = a.seq;
 }
 
@@ -347,10 +373,10 @@ __device__ __forceinline__ void host_publish(const RouteArgs& a, const int* offs
 //   1. per token, one wave: its selection, and its softmax of the second
 //      logits added to the wave's running expert sums (prediction);
 //   2. per wave: each of its 64 slots' rank among the wave's earlier slots of
-//      the same expert, and the wave's count of each expert (ballots); the
-//      prediction scores, summed over the waves in order;
-//   3. wave 0: expert totals and their exclusive scan (offsets); all threads:
-//      the ranks of the prediction scores;
+//      the same expert, and the wave's count of each expert; the prediction
+//      scores, summed over the waves in order;
+//   3. wave 0: expert totals and their exclusive scan (offsets); the other
+//      waves: the ranks of the prediction scores;
 //   4. slot s goes to offsets[e] + (earlier waves' slots of e) + (its rank
 //      in its wave), a stable counting sort; expert e goes to position
 //      rank(e) of the prediction order.
@@ -358,21 +384,39 @@ __device__ __forceinline__ void host_publish(const RouteArgs& a, const int* offs
 // (a barrier after a store to memory would wait for it).
 constexpr int kFewSlots = 1024;
 
+// The route body's LDS (a kernel may overlay it with what it needs before
+// the body starts).
+template <int NW>
+struct RouteLds {
+  uint64_t key_s[kMaxExperts];
+  int idx_s[kFewSlots];
+  float w_s[kFewSlots];
+  int perm_s[kFewSlots];
+  int pos_s[kFewSlots];
+  int offs_s[kMaxExperts + 1];
+  int cnt_s[kMaxExperts];
+  float score_s[kMaxExperts];
+  int rank_s[kMaxExperts];
+  int order_s[kMaxExperts];
+  int wcnt[NW][kMaxExperts];    // per-wave slot counts
+  float wsum[NW][kMaxExperts];  // per-wave prediction sums
+};
+
 template <int NW, int QN>
-__device__ void route_body(const RouteArgs& a) {
+__device__ void route_body(const RouteArgs& a, RouteLds<NW>& L) {
   static_assert(kFewSlots <= 64 * NW, "one slot per thread");
-  __shared__ int idx_s[kFewSlots];
-  __shared__ float w_s[kFewSlots];
-  __shared__ int perm_s[kFewSlots];
-  __shared__ int pos_s[kFewSlots];
-  __shared__ int offs_s[kMaxExperts + 1];
-  __shared__ int cnt_s[kMaxExperts];
-  __shared__ float score_s[kMaxExperts];
-  __shared__ uint64_t key_s[kMaxExperts];
-  __shared__ int rank_s[kMaxExperts];
-  __shared__ int order_s[kMaxExperts];
-  __shared__ int wcnt[NW][kMaxExperts];    // per-wave slot counts
-  __shared__ float wsum[NW][kMaxExperts];  // per-wave prediction sums
+  int* idx_s = L.idx_s;
+  float* w_s = L.w_s;
+  int* perm_s = L.perm_s;
+  int* pos_s = L.pos_s;
+  int* offs_s = L.offs_s;
+  int* cnt_s = L.cnt_s;
+  float* score_s = L.score_s;
+  uint64_t* key_s = L.key_s;
+  int* rank_s = L.rank_s;
+  int* order_s = L.order_s;
+  auto& wcnt = L.wcnt;
+  auto& wsum = L.wsum;
   constexpr int NT = 64 * NW;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int E = a.E, K = a.K;
@@ -417,15 +461,14 @@ __device__ void route_body(const RouteArgs& a) {
     // indices lie in [0, E) (selection above); the clamp only keeps LDS
     // accesses in bounds whatever the input
     ge = tid < TK ? min(max(idx_s[tid], 0), E - 1) : -1;
-    const uint64_t lt = (lane == 0) ? 0ull : ((~0ull) >> (64 - lane));
-    uint64_t pending = __ballot(ge >= 0);
-    while (pending) {
-      const int leader = __ffsll(static_cast<unsigned long long>(pending)) - 1;
-      const int le = lane_read(ge, leader);
-      const uint64_t same = __ballot(ge == le);
-      if (ge == le) grank = __popcll(same & lt);
-      if (lane == leader) wcnt[wave][le] = __popcll(same);
-      pending &= ~same;
+    // the wave's tokens in order: the slots of one token (distinct experts)
+    // take the running count of their expert as their rank and add one, so
+    // the counts end as the wave's counts
+    const int s0 = wave * 64, s1 = min(TK, s0 + 64);
+    if (s0 < s1) {
+      const int t_first = s0 / K, t_last = (s1 - 1) / K, my_t = tid / K;
+      for (int t = t_first; t <= t_last; ++t)
+        if (my_t == t && ge >= 0) grank = atomicAdd(&wcnt[wave][ge], 1);
     }
   }
   if (pred) {
@@ -438,16 +481,20 @@ __device__ void route_body(const RouteArgs& a) {
   }
   __syncthreads();
 
-  // 3. offsets (wave 0); prediction ranks (all threads)
-  if (sel && wave == 0) {
-    for (int e = lane; e < E; e += 64) {
-      int c = 0;
-      for (int w2 = 0; w2 < NW; ++w2) c += wcnt[w2][e];
-      cnt_s[e] = c;
+  // 3. offsets and the first host-visible copies (wave 0); prediction ranks
+  //    (the other waves when wave 0 has the offsets to do)
+  if (wave == 0) {
+    if (sel) {
+      for (int e = lane; e < E; e += 64) {
+        int c = 0;
+        for (int w2 = 0; w2 < NW; ++w2) c += wcnt[w2][e];
+        cnt_s[e] = c;
+      }
+      scan_offsets(cnt_s, nullptr, offs_s, E, lane);
     }
-    scan_offsets(cnt_s, nullptr, offs_s, E, lane);
+    host_rows(a, sel ? offs_s : nullptr, pred ? score_s : nullptr, lane);
   }
-  if (pred) rank_count(key_s, rank_s, E, tid, NT);
+  if (pred) rank_count(key_s, rank_s, E, sel ? tid - 64 : tid, sel ? NT - 64 : NT);
   __syncthreads();
 
   // 4. grouped positions; prediction order
@@ -477,13 +524,16 @@ __device__ void route_body(const RouteArgs& a) {
       a.score[i] = score_s[i];
     }
   }
-  host_publish(a, sel ? offs_s : nullptr, pred ? order_s : nullptr, score_s, wave, lane);
+  if (wave == 0) host_publish(a, pred ? order_s : nullptr, lane);
 }
 
 constexpr int kRouteWaves = 16;
 
 template <int QN>
-__global__ __launch_bounds__(64 * kRouteWaves) void route_kernel(RouteArgs a) { route_body<kRouteWaves, QN>(a); }
+__global__ __launch_bounds__(64 * kRouteWaves) void route_kernel(RouteArgs a) {
+  __shared__ RouteLds<kRouteWaves> lds;
+  route_body<kRouteWaves, QN>(a, lds);
+}
 
 // Many tokens, step 1 (work-group b: tokens [b TB, (b+1) TB), one wave per
 // token): selection, then each slot's rank among the block's earlier slots
@@ -630,9 +680,14 @@ __global__ __launch_bounds__(64 * kScanWaves) void scan_many_kernel(RouteArgs a,
     }
   }
   __syncthreads();
-  // offsets (wave 0); prediction ranks (all threads)
-  if (a.logits != nullptr && wave == 0) scan_offsets(tot, nullptr, offs_s, E, lane);
-  if (a.logits_pred != nullptr) rank_count(key_s, rank_s, E, tid, NT);
+  // offsets and the first host-visible copies (wave 0); prediction ranks
+  // (the other waves when wave 0 has the offsets to do)
+  const bool sel = a.logits != nullptr, pred = a.logits_pred != nullptr;
+  if (wave == 0) {
+    if (sel) scan_offsets(tot, nullptr, offs_s, E, lane);
+    host_rows(a, sel ? offs_s : nullptr, pred ? score_s : nullptr, lane);
+  }
+  if (pred) rank_count(key_s, rank_s, E, sel ? tid - 64 : tid, sel ? NT - 64 : NT);
   __syncthreads();
   if (a.logits_pred != nullptr)
     for (int e = tid; e < E; e += NT) order_s[rank_s[e]] = e;
@@ -645,8 +700,7 @@ __global__ __launch_bounds__(64 * kScanWaves) void scan_many_kernel(RouteArgs a,
       a.score[i] = score_s[i];
     }
   }
-  host_publish(a, a.logits != nullptr ? offs_s : nullptr, a.logits_pred != nullptr ? order_s : nullptr, score_s,
-               wave, lane);
+  if (wave == 0) host_publish(a, pred ? order_s : nullptr, lane);
 }
 
 // Many tokens, step 3: slot s of token t (block t / TB) goes to grouped
@@ -747,6 +801,7 @@ __global__ __launch_bounds__(64 * kRouteWaves) void route_fused_kernel(LogitsArg
   constexpr int B = fused_batch<W>();
   __shared__ float lg[kFusedLogits];
   __shared__ __align__(16) unsigned char hT[kFusedHBytes];
+  __shared__ RouteLds<kRouteWaves> lds;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int d = la.d, steps = d / 64;
   const int pitch = fused_pitch(d, static_cast<int>(sizeof(W)));
@@ -800,7 +855,7 @@ __global__ __launch_bounds__(64 * kRouteWaves) void route_fused_kernel(LogitsArg
   RouteArgs a = ra;
   a.logits = ra.logits != nullptr ? lg : nullptr;
   a.logits_pred = ra.logits_pred != nullptr ? (ra.logits != nullptr ? lg + per : lg) : nullptr;
-  route_body<kRouteWaves, QN>(a);
+  route_body<kRouteWaves, QN>(a, lds);
 }
 
 // Many tokens: the same order, with each lane running the fma chains of 8
