@@ -3409,12 +3409,16 @@ template <int PER>
 __global__ __launch_bounds__(256) void combine_few_kernel(CombineArgs a) {
   constexpr int TPB = 16 / PER;  // terms per batch
   __shared__ float4 red[kCombMaxTerms][4][kCombCols / 4];
+  __shared__ float w_s[kMaxTopK];
   const int t = blockIdx.y;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int cq = tid & 7, pl = tid >> 3;  // plane lane 0..31
   const int col = blockIdx.x * kCombCols + 4 * cq;
   const bool live = col < a.d;
   const int n_terms = a.K + a.n_shared;
+  // the token's weights, requested with the first partial loads (read after
+  // the barrier)
+  if (tid < a.K) w_s[tid] = a.w[t * a.K + tid];
   for (int k0 = 0; k0 < n_terms; k0 += TPB) {
     const float* rb[TPB];
     int np[TPB];
@@ -3447,6 +3451,7 @@ __global__ __launch_bounds__(256) void combine_few_kernel(CombineArgs a) {
     }
 #pragma unroll
     for (int j = 0; j < TPB; ++j) {
+      if (k0 + j >= n_terms) continue;  // the same for the whole work-group
 #pragma unroll
       for (int m = 8; m <= 32; m <<= 1) {
         float4 o;
@@ -3456,7 +3461,7 @@ __global__ __launch_bounds__(256) void combine_few_kernel(CombineArgs a) {
         o.w = __shfl_xor(acc[j].w, m, 64);
         acc[j] = f4add(acc[j], o);
       }
-      if (lane < 8 && k0 + j < n_terms) red[k0 + j][wave][cq] = acc[j];
+      if (lane < 8) red[k0 + j][wave][cq] = acc[j];
     }
   }
   __syncthreads();
@@ -3465,7 +3470,7 @@ __global__ __launch_bounds__(256) void combine_few_kernel(CombineArgs a) {
     for (int term = 0; term < n_terms; ++term) {
       const float4 sum = f4add(f4add(red[term][0][cq], red[term][1][cq]), f4add(red[term][2][cq], red[term][3][cq]));
       if (term < a.K) {
-        const float wk = a.w[t * a.K + term];
+        const float wk = w_s[term];
         y = make_float4(fmaf(wk, sum.x, y.x), fmaf(wk, sum.y, y.y), fmaf(wk, sum.z, y.z), fmaf(wk, sum.w, y.w));
       } else {
         y = f4add(y, sum);
