@@ -772,6 +772,93 @@ __global__ __launch_bounds__(256) void logits_wave_kernel(LogitsArgs a) {
   }
 }
 
+// Few tokens: a work-group takes a block of TB tokens, staged once in LDS as
+// fp32, transposed (row (t, lane l) holds elements l, l + 64, ... of token
+// t, kFewPitch(d) bytes apart), and one (router, expert) per wave: lane l
+// requests its router elements l + 64 s a batch at a time and runs the TB
+// fma chains of residue l side by side, each in the order above; then the
+// same halving tree per token.  So every logit has the bits of
+// logits_wave_kernel, from one router load per TB tokens instead of one
+// load of the router and of the token row per logit.
+constexpr int kFewWaves = 4;
+constexpr int kFewBatch = 32;              // router steps requested together
+constexpr int kFewLdsBytes = 80 * 1024;    // staged token rows of a work-group
+__host__ __device__ constexpr int few_pitch(int d) { return ((d / 64) * 4 + 15) / 16 * 16 + 16; }
+
+template <typename W, int TB>
+__global__ __launch_bounds__(64 * kFewWaves) void logits_few_kernel(LogitsArgs a) {
+  constexpr int VE = 16 / static_cast<int>(sizeof(W));
+  extern __shared__ __align__(16) unsigned char few_lds[];
+  float* hT = reinterpret_cast<float*>(few_lds);
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int d = a.d, steps = d / 64, pf = few_pitch(d) / 4;
+  const int t0 = blockIdx.x * TB, nt = min(TB, a.T - t0);
+  // stage the block's token rows (16 bytes per thread and pass)
+  const int pieces = nt * d / VE;
+  for (int i = tid; i < pieces; i += 64 * kFewWaves) {
+    const int j0 = i * VE, t = j0 / d, j = j0 - t * d;
+    const uint4 hp = ld16(static_cast<const W*>(a.h) + static_cast<size_t>(t0) * d + j0);
+    const uint32_t hw[4] = {hp.x, hp.y, hp.z, hp.w};
+#pragma unroll
+    for (int c = 0; c < VE; ++c) {
+      const float v = sizeof(W) == 2 ? __uint_as_float((c & 1) ? (hw[c / 2] & 0xffff0000u) : (hw[c / 2] << 16))
+                                     : __uint_as_float(hw[c]);
+      hT[(t * 64 + (j + c) % 64) * pf + (j + c) / 64] = v;
+    }
+  }
+  const int mats = a.wr2 != nullptr ? 2 : 1;
+  const int o = blockIdx.y * kFewWaves + wave;  // (router, expert) of this wave
+  const bool live = o < a.E * mats;
+  const int mat = live ? o / a.E : 0, e = live ? o - mat * a.E : 0;
+  const W* wrow = static_cast<const W*>(mat == 0 ? a.wt : a.wt2) + static_cast<size_t>(e) * d + lane;
+  W wv[kFewBatch];
+#pragma unroll
+  for (int u = 0; u < kFewBatch; ++u) wv[u] = wrow[static_cast<size_t>(min(u, steps - 1)) * 64];  // clamped: in bounds
+  __syncthreads();
+  if (!live) return;  // whole waves, after the only barrier
+  float acc[TB];
+#pragma unroll
+  for (int t = 0; t < TB; ++t) acc[t] = 0.0f;
+  for (int s0 = 0; s0 < steps; s0 += kFewBatch) {
+    if (s0 != 0) {
+#pragma unroll
+      for (int u = 0; u < kFewBatch; ++u)
+        wv[u] = wrow[static_cast<size_t>(min(s0 + u, steps - 1)) * 64];  // clamped: in bounds, used only in range
+    }
+#pragma unroll
+    for (int u0 = 0; u0 < kFewBatch; u0 += 4) {
+      if (s0 + u0 >= steps) break;
+      float hx[TB][4];
+#pragma unroll
+      for (int t = 0; t < TB; ++t) {
+        const float4 q = *reinterpret_cast<const float4*>(hT + (t * 64 + lane) * pf + s0 + u0);
+        hx[t][0] = q.x;
+        hx[t][1] = q.y;
+        hx[t][2] = q.z;
+        hx[t][3] = q.w;
+      }
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        if (s0 + u0 + u < steps) {
+          const float w = to_f32(wv[u0 + u]);
+#pragma unroll
+          for (int t = 0; t < TB; ++t) acc[t] = fmaf(hx[t][u], w, acc[t]);
+        }
+      }
+    }
+  }
+  const float* bias = mat == 0 ? a.bias : a.bias2;
+  float* out = mat == 0 ? a.logits : a.logits2;
+#pragma unroll
+  for (int t = 0; t < TB; ++t) {
+    float v = acc[t];
+#pragma unroll
+    for (int s = 32; s >= 1; s >>= 1) v = v + __shfl_down(v, s, 64);
+    if (bias != nullptr) v = v + bias[e];
+    if (lane == 0 && t < nt) out[static_cast<size_t>(t0 + t) * a.E + e] = v;
+  }
+}
+
 // At most kFusedLogits logits of at most 16 KiB of token rows: the route
 // work-group computes them itself, in the order above, and goes on with the
 // route body.  The token rows are staged in LDS transposed, row (t, lane l)
@@ -1082,11 +1169,30 @@ hipError_t launch_logits_route(const LogitsArgs& a, const RouteArgs& ra, hipStre
 #undef MSK_FUSED
       return hipGetLastError();
     }
-    const dim3 grid((n_out + 3) / 4);
-    if (a.dtype == kBF16)
-      hipLaunchKernelGGL(logits_wave_kernel<uint16_t>, grid, dim3(256), kGuardLds, s, b);
-    else
-      hipLaunchKernelGGL(logits_wave_kernel<float>, grid, dim3(256), kGuardLds, s, b);
+    const int tb = a.T >= 3 ? 4 : a.T;  // tokens per work-group
+    const size_t few_bytes = static_cast<size_t>(tb) * 64 * few_pitch(a.d);
+    if (few_bytes <= kFewLdsBytes) {
+      const dim3 grid((a.T + tb - 1) / tb, (a.E * mats + kFewWaves - 1) / kFewWaves);
+#define MSK_FEW(TB_)                                                                                      \
+  if (a.dtype == kBF16)                                                                                   \
+    hipLaunchKernelGGL((logits_few_kernel<uint16_t, TB_>), grid, dim3(64 * kFewWaves), few_bytes, s, b); \
+  else                                                                                                    \
+    hipLaunchKernelGGL((logits_few_kernel<float, TB_>), grid, dim3(64 * kFewWaves), few_bytes, s, b)
+      if (tb == 1) {
+        MSK_FEW(1);
+      } else if (tb == 2) {
+        MSK_FEW(2);
+      } else {
+        MSK_FEW(4);
+      }
+#undef MSK_FEW
+    } else {
+      const dim3 grid((n_out + 3) / 4);
+      if (a.dtype == kBF16)
+        hipLaunchKernelGGL(logits_wave_kernel<uint16_t>, grid, dim3(256), kGuardLds, s, b);
+      else
+        hipLaunchKernelGGL(logits_wave_kernel<float>, grid, dim3(256), kGuardLds, s, b);
+    }
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
