@@ -50,9 +50,10 @@ struct LogitsArgs {
 // tiles of 8 tokens x 16 experts per wave, selection and per-block expert
 // counts for blocks of route_block_tokens(T, K) tokens, one work-group for the
 // scans over blocks (and the prediction ranking), then the scatter of the
-// grouping.  Fewer tokens: one wave per logit, then one work-group for
-// everything after the logits -- a single launch when there are at most 32
-// logits.
+// grouping.  Fewer tokens: one wave per router row against a block of up to
+// four staged token rows (or one wave per logit when such a block does not
+// fit LDS), then one work-group for everything after the logits -- a single
+// launch, one wave per logit, when there are at most 32 logits.
 constexpr int kManyTokens = 64;
 // Tokens per block: 4 (one per wave of the selection), or 16 from
 // kBigBlockTokens tokens on (with at most 16 selected experts per token), so
