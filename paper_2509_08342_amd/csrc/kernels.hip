@@ -461,14 +461,30 @@ __device__ void route_body(const RouteArgs& a, RouteLds<NW>& L) {
     // indices lie in [0, E) (selection above); the clamp only keeps LDS
     // accesses in bounds whatever the input
     ge = tid < TK ? min(max(idx_s[tid], 0), E - 1) : -1;
-    // the wave's tokens in order: the slots of one token (distinct experts)
-    // take the running count of their expert as their rank and add one, so
-    // the counts end as the wave's counts
     const int s0 = wave * 64, s1 = min(TK, s0 + 64);
     if (s0 < s1) {
-      const int t_first = s0 / K, t_last = (s1 - 1) / K, my_t = tid / K;
-      for (int t = t_first; t <= t_last; ++t)
-        if (my_t == t && ge >= 0) grank = atomicAdd(&wcnt[wave][ge], 1);
+      const int t_first = s0 / K, t_last = (s1 - 1) / K;
+      if (t_last - t_first < E) {
+        // the wave's tokens in order: the slots of one token (distinct
+        // experts) take the running count of their expert as their rank and
+        // add one, so the counts end as the wave's counts
+        const int my_t = tid / K;
+        for (int t = t_first; t <= t_last; ++t)
+          if (my_t == t && ge >= 0) grank = atomicAdd(&wcnt[wave][ge], 1);
+      } else {
+        // more tokens than experts in the wave: one ballot per distinct
+        // expert instead (the same ranks and counts)
+        const uint64_t lt = (lane == 0) ? 0ull : ((~0ull) >> (64 - lane));
+        uint64_t pending = __ballot(ge >= 0);
+        while (pending) {
+          const int leader = __ffsll(static_cast<unsigned long long>(pending)) - 1;
+          const int le = lane_read(ge, leader);
+          const uint64_t same = __ballot(ge == le);
+          if (ge == le) grank = __popcll(same & lt);
+          if (lane == leader) wcnt[wave][le] = __popcll(same);
+          pending &= ~same;
+        }
+      }
     }
   }
   if (pred) {
@@ -781,8 +797,9 @@ __global__ __launch_bounds__(256) void logits_wave_kernel(LogitsArgs a) {
 // logits_wave_kernel, from one router load per TB tokens instead of one
 // load of the router and of the token row per logit.
 constexpr int kFewWaves = 4;
-constexpr int kFewBatch = 32;              // router steps requested together
+constexpr int kFewBatch = 64;              // router steps requested together
 constexpr int kFewLdsBytes = 80 * 1024;    // staged token rows of a work-group
+constexpr int kFewMinWgs = 64;
 __host__ __device__ constexpr int few_pitch(int d) { return ((d / 64) * 4 + 15) / 16 * 16 + 16; }
 
 template <typename W, int TB>
@@ -1169,7 +1186,12 @@ hipError_t launch_logits_route(const LogitsArgs& a, const RouteArgs& ra, hipStre
 #undef MSK_FUSED
       return hipGetLastError();
     }
-    const int tb = a.T >= 3 ? 4 : a.T;  // tokens per work-group
+    // tokens per work-group: up to four, fewer while the grid would have
+    // under kFewMinWgs work-groups (few experts: the waves would not cover
+    // enough CUs)
+    int tb = a.T >= 3 ? 4 : a.T;
+    const int ey = (a.E * mats + kFewWaves - 1) / kFewWaves;
+    while (tb > 1 && ((a.T + tb - 1) / tb) * ey < kFewMinWgs) tb /= 2;
     const size_t few_bytes = static_cast<size_t>(tb) * 64 * few_pitch(a.d);
     if (few_bytes <= kFewLdsBytes) {
       const dim3 grid((a.T + tb - 1) / tb, (a.E * mats + kFewWaves - 1) / kFewWaves);
