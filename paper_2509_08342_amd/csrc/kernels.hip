@@ -112,11 +112,11 @@ __host__ __device__ constexpr int lanes_q(int E) { return E <= 64 ? 1 : E <= 128
 static_assert(kMaxExperts <= 64 * 8, "at most 8 expert values per lane");
 
 // Wave-wide reductions whose result does not depend on the order of the
-// combination (argmax with the lower index on equal values, max of floats,
-// integer sums) move data with DPP inside rows of 16 lanes -- lane i with
-// i ^ 1, i ^ 2 (quad permutes), i ^ 7 (half-row mirror), i ^ 15 (row
-// mirror) -- and read the four row results with v_readlane, instead of six
-// LDS-crossbar permutes.  Floating-point sums keep their fixed butterflies.
+// combination (max of floats, unsigned max) move data with DPP inside rows
+// of 16 lanes -- lane i with i ^ 1, i ^ 2 (quad permutes), i ^ 7 (half-row
+// mirror), i ^ 15 (row mirror) -- and read the four row results with
+// v_readlane, instead of six LDS-crossbar permutes.  Floating-point sums
+// keep their fixed butterflies.
 constexpr int kDppXor1 = 0xB1;        // quad_perm [1, 0, 3, 2]
 constexpr int kDppXor2 = 0x4E;        // quad_perm [2, 3, 0, 1]
 constexpr int kDppHalfMirror = 0x141;  // row_half_mirror
@@ -135,45 +135,12 @@ __device__ __forceinline__ float lane_read(float x, int l) {
   return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(x), l));
 }
 
-// (v, i) takes (ov, oi) if that is larger, or equal with a lower index.
-__device__ __forceinline__ void argmax_take(float& v, int& i, float ov, int oi) {
-  // bitwise, not short-circuit, so that it compiles to compares and selects
-  // rather than branches (a branch per comparison costs the wave far more)
-  const bool take = (ov > v) | ((ov == v) & (oi < i));
-  v = take ? ov : v;
-  i = take ? oi : i;
-}
-template <int CTRL>
-__device__ __forceinline__ void argmax_row_step(float& v, int& i) {
-  argmax_take(v, i, dpp_move<CTRL>(v), dpp_move<CTRL>(i));
-}
-// Every lane gets the wave's largest v and the lowest i among equal ones
-// (v never NaN).
-__device__ __forceinline__ void wave_argmax(float& v, int& i) {
-  argmax_row_step<kDppXor1>(v, i);
-  argmax_row_step<kDppXor2>(v, i);
-  argmax_row_step<kDppHalfMirror>(v, i);
-  argmax_row_step<kDppMirror>(v, i);
-  float bv = lane_read(v, 0);
-  int bi = lane_read(i, 0);
-#pragma unroll
-  for (int r = 1; r < 4; ++r) argmax_take(bv, bi, lane_read(v, 16 * r), lane_read(i, 16 * r));
-  v = bv;
-  i = bi;
-}
 __device__ __forceinline__ float wave_max(float v) {
   v = fmaxf(v, dpp_move<kDppXor1>(v));
   v = fmaxf(v, dpp_move<kDppXor2>(v));
   v = fmaxf(v, dpp_move<kDppHalfMirror>(v));
   v = fmaxf(v, dpp_move<kDppMirror>(v));
   return fmaxf(fmaxf(lane_read(v, 0), lane_read(v, 16)), fmaxf(lane_read(v, 32), lane_read(v, 48)));
-}
-__device__ __forceinline__ int wave_sum(int v) {
-  v += dpp_move<kDppXor1>(v);
-  v += dpp_move<kDppXor2>(v);
-  v += dpp_move<kDppHalfMirror>(v);
-  v += dpp_move<kDppMirror>(v);
-  return (lane_read(v, 0) + lane_read(v, 16)) + (lane_read(v, 32) + lane_read(v, 48));
 }
 __device__ __forceinline__ uint32_t wave_umax(uint32_t v) {
   v = max(v, static_cast<uint32_t>(dpp_move<kDppXor1>(static_cast<int>(v))));
