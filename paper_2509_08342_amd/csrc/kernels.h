@@ -52,8 +52,7 @@ struct LogitsArgs {
 // scans over blocks (and the prediction ranking), then the scatter of the
 // grouping.  Fewer tokens: one wave per router row against a block of up to
 // four staged token rows (or one wave per logit when such a block does not
-// fit LDS), then one work-group for everything after the logits -- a single
-// launch, one wave per logit, when there are at most 32 logits.
+// fit LDS), then one work-group for everything after the logits.
 constexpr int kManyTokens = 64;
 // Tokens per block: 4 (one per wave of the selection), or 16 from
 // kBigBlockTokens tokens on (with at most 16 selected experts per token), so

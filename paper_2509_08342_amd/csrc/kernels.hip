@@ -351,8 +351,7 @@ __device__ __forceinline__ void host_publish(const RouteArgs& a, const int* orde
 // (a barrier after a store to memory would wait for it).
 constexpr int kFewSlots = 1024;
 
-// The route body's LDS (a kernel may overlay it with what it needs before
-// the body starts).
+// The route body's LDS.
 template <int NW>
 struct RouteLds {
   uint64_t key_s[kMaxExperts];
@@ -843,92 +842,6 @@ __global__ __launch_bounds__(64 * kFewWaves) void logits_few_kernel(LogitsArgs a
   }
 }
 
-// At most kFusedLogits logits of at most 16 KiB of token rows: the route
-// work-group computes them itself, in the order above, and goes on with the
-// route body.  The token rows are staged in LDS transposed, row (t, lane l)
-// holding elements l, l + 64, l + 128, ... (pitch fused_pitch bytes), so that
-// a lane reads its fma chain's activations 16 bytes at a time; a wave
-// computes one logit at a time, lane l holding the router elements l + 64 s
-// of a batch of steps in registers (64 bf16 or 32 fp32 ones), all requested
-// at once -- one memory round trip per logit up to d = 4096 in bf16, the
-// first requested before the staging barrier.
-constexpr int kFusedLogits = 32;
-constexpr int kFusedRowBytes = 16 * 64 * kRouteWaves;  // one 16-byte piece per thread
-constexpr int kFusedHBytes = 18 * 1024;
-template <typename W>
-constexpr int fused_batch() { return sizeof(W) == 2 ? 64 : 32; }
-__host__ __device__ constexpr int fused_pitch(int d, int elem) { return ((d / 64) * elem + 15) / 16 * 16 + 16; }
-
-template <typename W, int B>
-__device__ __forceinline__ void fused_load(const W* wrow, int s0, int steps, W (&wv)[B]) {
-#pragma unroll
-  for (int u = 0; u < B; ++u)
-    wv[u] = wrow[static_cast<size_t>(min(s0 + u, steps - 1)) * 64];  // clamped: in bounds, used only in range
-}
-
-template <typename W, int QN>
-__global__ __launch_bounds__(64 * kRouteWaves) void route_fused_kernel(LogitsArgs la, RouteArgs ra) {
-  constexpr int VE = 16 / static_cast<int>(sizeof(W));  // elements per 16-byte piece
-  constexpr int B = fused_batch<W>();
-  __shared__ float lg[kFusedLogits];
-  __shared__ __align__(16) unsigned char hT[kFusedHBytes];
-  __shared__ RouteLds<kRouteWaves> lds;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int d = la.d, steps = d / 64;
-  const int pitch = fused_pitch(d, static_cast<int>(sizeof(W)));
-  const int per = la.T * la.E;
-  const int n_out = per * (la.wr2 != nullptr ? 2 : 1);
-  const int pieces = la.T * d / VE;  // <= 64 * kRouteWaves (launch condition)
-  auto wrow_of = [&](int o) {
-    const int mat = o / per, e = (o - mat * per) % la.E;
-    return static_cast<const W*>(mat == 0 ? la.wt : la.wt2) + static_cast<size_t>(e) * d + lane;
-  };
-  uint4 hp = make_uint4(0, 0, 0, 0);
-  if (tid < pieces) hp = ld16(static_cast<const W*>(la.h) + static_cast<size_t>(tid) * VE);
-  W wv[B];
-  if (wave < n_out) fused_load(wrow_of(wave), 0, steps, wv);
-  if (tid < pieces) {
-    // elements j .. j + VE - 1 of token t: lanes j % 64 .. + VE - 1, step j / 64
-    const int j0 = tid * VE, t = j0 / d, j = j0 - t * d;
-    W e[VE];
-    *reinterpret_cast<uint4*>(e) = hp;
-#pragma unroll
-    for (int c = 0; c < VE; ++c)
-      *reinterpret_cast<W*>(hT + (static_cast<size_t>(t) * 64 + (j + c) % 64) * pitch + ((j + c) / 64) * sizeof(W)) = e[c];
-  }
-  __syncthreads();
-  for (int o = wave; o < n_out; o += kRouteWaves) {
-    const int mat = o / per, te = o - mat * per;
-    const int t = te / la.E, e = te - t * la.E;
-    const W* wrow = wrow_of(o);
-    const unsigned char* hrow = hT + (static_cast<size_t>(t) * 64 + lane) * pitch;
-    float acc = 0.0f;
-    for (int s0 = 0; s0 < steps; s0 += B) {
-      if (o != wave || s0 != 0) fused_load(wrow, s0, steps, wv);
-      W hv[B];
-#pragma unroll
-      for (int v = 0; v < B / VE; ++v) {
-        uint4 q = make_uint4(0, 0, 0, 0);
-        if (s0 + v * VE < steps) q = *reinterpret_cast<const uint4*>(hrow + static_cast<size_t>(s0 + v * VE) * sizeof(W));
-        *reinterpret_cast<uint4*>(&hv[v * VE]) = q;
-      }
-#pragma unroll
-      for (int u = 0; u < B; ++u)
-        if (s0 + u < steps) acc = fmaf(to_f32(hv[u]), to_f32(wv[u]), acc);
-    }
-#pragma unroll
-    for (int s = 32; s >= 1; s >>= 1) acc = acc + __shfl_down(acc, s, 64);
-    const float* bias = mat == 0 ? la.bias : la.bias2;
-    if (bias != nullptr) acc = acc + bias[e];
-    if (lane == 0) lg[o] = acc;
-  }
-  __syncthreads();
-  RouteArgs a = ra;
-  a.logits = ra.logits != nullptr ? lg : nullptr;
-  a.logits_pred = ra.logits_pred != nullptr ? (ra.logits != nullptr ? lg + per : lg) : nullptr;
-  route_body<kRouteWaves, QN>(a, lds);
-}
-
 // Many tokens: the same order, with each lane running the fma chains of 8
 // consecutive residues (l = 8 m + k, k < 8, m = lane % 8) for a 4-token x
 // 4-expert output tile (o = lane / 8 picks the tile), reading 16 bytes per
@@ -1135,24 +1048,6 @@ hipError_t launch_logits_route(const LogitsArgs& a, const RouteArgs& ra, hipStre
     }
   } else {
     const int n_out = a.T * a.E * mats;
-    const int elem = a.dtype == kBF16 ? 2 : 4;
-    const int64_t row_bytes = static_cast<int64_t>(a.T) * a.d * elem;
-    if (n_out <= kFusedLogits && row_bytes <= kFusedRowBytes &&
-        static_cast<int64_t>(a.T) * 64 * fused_pitch(a.d, elem) <= kFusedHBytes) {  // one launch for logits and route
-#define MSK_FUSED(QN_)                                                                              \
-  if (a.dtype == kBF16)                                                                             \
-    hipLaunchKernelGGL((route_fused_kernel<uint16_t, QN_>), dim3(1), dim3(64 * kRouteWaves), 0, s, b, ra); \
-  else                                                                                              \
-    hipLaunchKernelGGL((route_fused_kernel<float, QN_>), dim3(1), dim3(64 * kRouteWaves), 0, s, b, ra)
-      switch (lanes_q(ra.E)) {
-        case 1: MSK_FUSED(1); break;
-        case 2: MSK_FUSED(2); break;
-        case 4: MSK_FUSED(4); break;
-        default: MSK_FUSED(8); break;
-      }
-#undef MSK_FUSED
-      return hipGetLastError();
-    }
     // tokens per work-group: up to four, fewer while the grid would have
     // under kFewMinWgs work-groups (few experts: the waves would not cover
     // enough CUs)

@@ -1,8 +1,8 @@
 """GPU parity at the widest supported model dimension, d_model = 8192, in
 bf16 and fp32: two column groups per thread in the FFN's down projection,
-tiles limited by the activation rows' LDS size, the fused routing launch at
-its row-size limit (bf16, one token) and the separate logits launch beyond
-it, the matrix-core prefill path (bf16, T K >= 8 E) and the many-token
+tiles limited by the activation rows' LDS size, the few-token logits one
+wave per logit where a block of token rows does not fit LDS, the
+matrix-core prefill path (bf16, T K >= 8 E) and the many-token
 routing at the context's max_tokens.  Selected experts exact, outputs within
 the dtype tolerance, and bitwise equal across residency states."""
 import numpy as np
