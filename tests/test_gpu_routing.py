@@ -2,7 +2,8 @@
 the transposed router, block-wise selection and counts, scan, scatter):
 oracle parity at ragged token counts for both dtypes, the fixed logit order
 on the golden cases, and bitwise agreement of the selection with the
-few-token path on the same tokens."""
+few-token path on the same tokens; and of the few-token path, whose logits
+kernel stages blocks of up to four token rows, with single-token forwards."""
 import numpy as np
 import pytest
 
@@ -58,6 +59,34 @@ def test_many_token_prediction_matches_oracle(rig, T):
     order, score = ms.ms_predict(rig.ctx, 0, h, T, torch.cuda.current_stream(), E)
     ref_score, _ = oracle.predict(hf, rig.routers[0], rig.biases[0])
     check_prediction(order, score, ref_score)
+
+
+# 64 experts, top-4: the few-token logits kernel takes blocks of 4 token rows
+# (T = 16, or 8 with the prediction router), 2 (T = 10) or 1 (T = 3), the
+# block shrinking while its grid would have under 64 work-groups
+BLOCK_BF16 = synth.ModelShape("block-bf16", 1, 256, 256, 64, 4, "bf16")
+
+
+@pytest.mark.parametrize("T,predict", [(16, False), (8, True), (10, False), (3, False)])
+def test_few_token_blocks_select_like_single_tokens(T, predict):
+    """Each token's logits keep the fixed order whatever block of staged
+    token rows they are computed in, so a batch selects the same experts with
+    bitwise equal weights as each of its tokens alone, and matches the
+    oracle."""
+    from paper_2509_08342_amd import moesplit as ms
+    flags = ms.MS_FWD_PREDICT_NEXT if predict else 0
+    r = _rig(BLOCK_BF16, 16)
+    try:
+        h, hf = r.hidden(T, tag=900 + T)
+        y, idx, w = _run(r, h, T, flags)
+        check_layer(r, 0, hf, y, idx, w)
+        idx_b, w_b = idx.cpu().numpy(), w.cpu().numpy()
+        for t in range(T):
+            _, i1, w1 = _run(r, h[t:t + 1].contiguous(), 1, flags)
+            assert np.array_equal(i1.cpu().numpy()[0], idx_b[t]), t
+            assert np.array_equal(w1.cpu().numpy()[0].view(np.uint32), w_b[t].view(np.uint32)), t
+    finally:
+        r.close()
 
 
 def test_many_token_selection_equals_few_token_path(rig):
