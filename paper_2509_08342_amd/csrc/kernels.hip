@@ -756,7 +756,7 @@ __global__ __launch_bounds__(256) void logits_wave_kernel(LogitsArgs a) {
 
 // Few tokens: a work-group takes a block of TB tokens, staged once in LDS as
 // fp32, transposed (row (t, lane l) holds elements l, l + 64, ... of token
-// t, kFewPitch(d) bytes apart), and one (router, expert) per wave: lane l
+// t, few_pitch(d) bytes apart), and one (router, expert) per wave: lane l
 // requests its router elements l + 64 s a batch at a time and runs the TB
 // fma chains of residue l side by side, each in the order above; then the
 // same halving tree per token.  So every logit has the bits of
@@ -765,7 +765,7 @@ __global__ __launch_bounds__(256) void logits_wave_kernel(LogitsArgs a) {
 constexpr int kFewWaves = 4;
 constexpr int kFewBatch = 64;              // router steps requested together
 constexpr int kFewLdsBytes = 80 * 1024;    // staged token rows of a work-group
-constexpr int kFewMinWgs = 64;
+constexpr int kFewMinWgs = 64;             // the token block shrinks below this grid size
 __host__ __device__ constexpr int few_pitch(int d) { return ((d / 64) * 4 + 15) / 16 * 16 + 16; }
 
 template <typename W, int TB>
